@@ -1,0 +1,288 @@
+"""fp64 CPU oracle for the memory-module stage (test infrastructure).
+
+TEST INFRASTRUCTURE ONLY: the yardstick the GPU library is checked against.
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the GPU path;
+the arithmetic lives in ``tgm_oracle.c`` (plain C, fp64) and this module only
+marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tgm_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_i32p = C.POINTER(C.c_int32)
+_i64p = C.POINTER(C.c_int64)
+_f64p = C.POINTER(C.c_double)
+_f32p = C.POINTER(C.c_float)
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (fp64, OpenMP over independent units)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+class _Desc(C.Structure):
+    _fields_ = [("N", C.c_int), ("E", C.c_int64),
+                ("src", _i32p), ("dst", _i32p), ("neg", _i32p), ("t", _f64p),
+                ("efeat", _f32p),
+                ("D_e", C.c_int), ("M", C.c_int), ("D_t", C.c_int), ("H", C.c_int),
+                ("nb", C.c_int), ("B", C.c_int), ("s", C.c_int),
+                ("W_ih", _f32p), ("W_hh", _f32p), ("b_ih", _f32p), ("b_hh", _f32p),
+                ("omega", _f64p), ("beta", _f64p),
+                ("W_q", _f32p), ("b_q", _f32p), ("W_k", _f32p), ("b_k", _f32p),
+                ("W_v", _f32p), ("b_v", _f32p), ("W_o", _f32p), ("b_o", _f32p)]
+
+
+class _StepOut(C.Structure):
+    _fields_ = [("iter", C.c_int64), ("b", C.c_int32), ("R", C.c_int32), ("n_U", C.c_int32),
+                ("pad_", C.c_int32),
+                ("root", _i32p), ("root_ts", _f64p), ("nbr", _i32p), ("eid", _i32p),
+                ("nts", _f64p), ("cnt", _i32p), ("U", _i32p), ("root_pos", _i32p),
+                ("nbr_pos", _i32p), ("f_mem", _f64p), ("f_mem_ts", _f64p), ("f_mail", _f64p),
+                ("f_mail_ts", _f64p), ("f_ver", _i32p), ("s_new", _f64p),
+                ("new_mem_ts", _f64p), ("h", _f64p), ("winner", _i64p)]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = C.CDLL(_LIB)
+        L.orc_time_encode.argtypes = [C.c_int, _f64p, _f64p, C.c_double, _f64p]
+        L.orc_gru_cell.argtypes = [C.c_int, C.c_int, _f64p, _f64p, _f64p, _f64p, _f64p, _f64p,
+                                   _f64p]
+        L.orc_embed_one.argtypes = [C.c_int] * 4 + [_f64p] * 10 + [_f64p, C.c_double, C.c_int,
+                                                                    _f64p, _f64p, _f64p, _f64p]
+        L.orc_sample.argtypes = [C.c_int, C.c_int64, _i32p, _i32p, _f64p, C.c_int, _i32p, _f64p,
+                                 C.c_int, _i32p, _i32p, _f64p, _i32p]
+        L.orc_sample.restype = C.c_int
+        L.orc_create.argtypes = [C.POINTER(_Desc)]
+        L.orc_create.restype = C.c_void_p
+        L.orc_destroy.argtypes = [C.c_void_p]
+        L.orc_flush.argtypes = [C.c_void_p]
+        L.orc_set_state.argtypes = [C.c_void_p, C.c_int64, _f64p, _f64p, _f64p, _f64p, _i32p]
+        L.orc_get_state.argtypes = [C.c_void_p, _f64p, _f64p, _f64p, _f64p, _i32p]
+        L.orc_next_iter.argtypes = [C.c_void_p]
+        L.orc_next_iter.restype = C.c_int64
+        L.orc_step.argtypes = [C.c_void_p, C.POINTER(_StepOut)]
+        L.orc_step.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a, typ):
+    if a is None:
+        return C.cast(None, typ)
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(typ)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Building blocks (used by the pins)
+# ---------------------------------------------------------------------------
+
+def time_encode(omega, beta, dt) -> np.ndarray:
+    omega, beta = _f64(omega), _f64(beta)
+    out = np.empty(len(omega))
+    lib().orc_time_encode(len(omega), _p(omega, _f64p), _p(beta, _f64p), float(dt),
+                          _p(out, _f64p))
+    return out
+
+
+def gru_cell(W_ih, W_hh, b_ih, b_hh, x, h) -> np.ndarray:
+    W_ih, W_hh, b_ih, b_hh, x, h = map(_f64, (W_ih, W_hh, b_ih, b_hh, x, h))
+    M = h.shape[0]
+    D_x = x.shape[0]
+    assert W_ih.shape == (3 * M, D_x) and W_hh.shape == (3 * M, M)
+    out = np.empty(M)
+    lib().orc_gru_cell(M, D_x, *(_p(a, _f64p) for a in (W_ih, W_hh, b_ih, b_hh, x, h)),
+                       _p(out, _f64p))
+    return out
+
+
+def embed_one(w, H, s_v, tq, s_u, f, nts) -> np.ndarray:
+    """Embedding of one root from explicit neighbour rows (``w`` a Weights)."""
+    s_v = _f64(s_v)
+    M = s_v.shape[0]
+    s_u = _f64(s_u).reshape(-1, M)
+    cnt = s_u.shape[0]
+    D_t = len(w.omega)
+    D_e = w.W_k.shape[1] - M - D_t
+    f = _f64(f).reshape(cnt, D_e) if D_e > 0 else np.zeros((cnt, 0))
+    nts = _f64(nts).reshape(cnt)
+    ws = [_f64(x) for x in (w.omega, w.beta, w.W_q, w.b_q, w.W_k, w.b_k, w.W_v, w.b_v,
+                             w.W_o, w.b_o)]
+    out = np.empty(M)
+    lib().orc_embed_one(M, D_e, D_t, H, *(_p(x, _f64p) for x in ws), _p(s_v, _f64p), float(tq),
+                        cnt, _p(np.ascontiguousarray(s_u), _f64p),
+                        _p(np.ascontiguousarray(f), _f64p), _p(nts, _f64p), _p(out, _f64p))
+    return out
+
+
+def sample(N, src, dst, t, root, root_ts, nb):
+    src = np.ascontiguousarray(src, dtype=np.int32)
+    dst = np.ascontiguousarray(dst, dtype=np.int32)
+    t = _f64(t)
+    root = np.ascontiguousarray(root, dtype=np.int32)
+    root_ts = _f64(root_ts)
+    R = len(root)
+    nbr = np.empty((R, nb), np.int32)
+    eid = np.empty((R, nb), np.int32)
+    nts = np.empty((R, nb), np.float64)
+    cnt = np.empty(R, np.int32)
+    rc = lib().orc_sample(N, len(src), _p(src, _i32p), _p(dst, _i32p), _p(t, _f64p), R,
+                          _p(root, _i32p), _p(root_ts, _f64p), nb, _p(nbr, _i32p),
+                          _p(eid, _i32p), _p(nts, _f64p), _p(cnt, _i32p))
+    assert rc == 0
+    return nbr, eid, nts, cnt
+
+
+# ---------------------------------------------------------------------------
+# Stateful driver
+# ---------------------------------------------------------------------------
+
+@dataclass
+class StepResult:
+    iter: int
+    b: int
+    R: int
+    n_U: int
+    root: np.ndarray
+    root_ts: np.ndarray
+    nbr: np.ndarray
+    eid: np.ndarray
+    nts: np.ndarray
+    cnt: np.ndarray
+    U: np.ndarray
+    root_pos: np.ndarray
+    nbr_pos: np.ndarray
+    f_mem: np.ndarray
+    f_mem_ts: np.ndarray
+    f_mail: np.ndarray
+    f_mail_ts: np.ndarray
+    f_ver: np.ndarray
+    s_new: np.ndarray
+    new_mem_ts: np.ndarray
+    h: np.ndarray
+    winner: np.ndarray
+
+
+class Oracle:
+    """Runs the stage iteration by iteration on a workload (``workloads.Workload``)."""
+
+    def __init__(self, wl, w, s: int | None = None):
+        self.wl = wl
+        self.s = wl.s if s is None else s
+        self.M, self.D_m, self.N, self.nb, self.B = wl.M, wl.D_m, wl.N, wl.nb, wl.B
+        self._keep = []
+
+        def keep(a, dt):
+            a = np.ascontiguousarray(a, dtype=dt)
+            self._keep.append(a)
+            return a
+
+        d = _Desc()
+        d.N, d.E = wl.N, wl.E
+        d.src = _p(keep(wl.src, np.int32), _i32p)
+        d.dst = _p(keep(wl.dst, np.int32), _i32p)
+        d.neg = _p(keep(wl.neg, np.int32), _i32p)
+        d.t = _p(keep(wl.t, np.float64), _f64p)
+        d.efeat = _p(keep(wl.efeat, np.float32), _f32p) if wl.D_e > 0 else C.cast(None, _f32p)
+        d.D_e, d.M, d.D_t, d.H, d.nb, d.B, d.s = (wl.D_e, wl.M, wl.D_t, wl.H, wl.nb, wl.B,
+                                                  self.s)
+        for name in ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v",
+                     "W_o", "b_o"):
+            setattr(d, name, _p(keep(getattr(w, name), np.float32), _f32p))
+        d.omega = _p(keep(w.omega, np.float64), _f64p)
+        d.beta = _p(keep(w.beta, np.float64), _f64p)
+        self._desc = d
+        h = lib().orc_create(C.byref(d))
+        if not h:
+            raise ValueError("oracle: invalid description")
+        self._h = h
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            lib().orc_destroy(h)
+            self._h = None
+
+    @property
+    def next_iter(self) -> int:
+        return int(lib().orc_next_iter(self._h))
+
+    def step(self, want: str = "all") -> StepResult | None:
+        """Run the next iteration; ``want='light'`` skips the big float outputs."""
+        B, nb, N, M, D_m = self.B, self.nb, self.N, self.M, self.D_m
+        R = 3 * B
+        o = _StepOut()
+        arrs = dict(root=np.empty(R, np.int32), root_ts=np.empty(R), nbr=np.empty(R * nb, np.int32),
+                    eid=np.empty(R * nb, np.int32), nts=np.empty(R * nb), cnt=np.empty(R, np.int32),
+                    U=np.empty(N, np.int32), root_pos=np.empty(R, np.int32),
+                    nbr_pos=np.empty(R * nb, np.int32), f_mem_ts=np.empty(N),
+                    f_mail_ts=np.empty(N), f_ver=np.empty(N, np.int32), new_mem_ts=np.empty(N),
+                    winner=np.empty(N, np.int64))
+        if want == "all":
+            arrs.update(f_mem=np.empty(N * M), f_mail=np.empty(N * D_m + 1),
+                        s_new=np.empty(N * M), h=np.empty(R * M))
+        for k, fld in _StepOut._fields_:
+            if k in arrs:
+                setattr(o, k, _p(arrs[k], fld))
+        rc = lib().orc_step(self._h, C.byref(o))
+        if rc == -2:
+            return None
+        assert rc == 0
+        R, nU = o.R, o.n_U
+        g = lambda k, n, shape=None: (arrs[k][:n].reshape(shape) if shape else arrs[k][:n]) \
+            if k in arrs else None
+        return StepResult(
+            iter=o.iter, b=o.b, R=R, n_U=nU, root=g("root", R), root_ts=g("root_ts", R),
+            nbr=g("nbr", R * nb, (R, nb)), eid=g("eid", R * nb, (R, nb)),
+            nts=g("nts", R * nb, (R, nb)), cnt=g("cnt", R), U=g("U", nU),
+            root_pos=g("root_pos", R), nbr_pos=g("nbr_pos", R * nb, (R, nb)),
+            f_mem=g("f_mem", nU * M, (nU, M)), f_mem_ts=g("f_mem_ts", nU),
+            f_mail=g("f_mail", nU * D_m, (nU, D_m)), f_mail_ts=g("f_mail_ts", nU),
+            f_ver=g("f_ver", nU), s_new=g("s_new", nU * M, (nU, M)),
+            new_mem_ts=g("new_mem_ts", nU), h=g("h", R * M, (R, M)), winner=g("winner", nU))
+
+    def flush(self):
+        lib().orc_flush(self._h)
+
+    def state(self):
+        N, M, D_m = self.N, self.M, self.D_m
+        mem, mem_ts = np.empty((N, M)), np.empty(N)
+        mail, mail_ts = np.empty((N, D_m)), np.empty(N)
+        ver = np.empty(N, np.int32)
+        lib().orc_get_state(self._h, _p(mem, _f64p), _p(mem_ts, _f64p),
+                            _p(mail, _f64p) if D_m else C.cast(None, _f64p),
+                            _p(mail_ts, _f64p), _p(ver, _i32p))
+        return dict(mem=mem, mem_ts=mem_ts, mail=mail, mail_ts=mail_ts, ver=ver)
+
+    def set_state(self, it, mem, mem_ts, mail, mail_ts, ver):
+        mem, mem_ts, mail, mail_ts = map(_f64, (mem, mem_ts, mail, mail_ts))
+        ver = np.ascontiguousarray(ver, dtype=np.int32)
+        lib().orc_set_state(self._h, int(it), _p(mem, _f64p), _p(mem_ts, _f64p),
+                            _p(mail, _f64p), _p(mail_ts, _f64p), _p(ver, _i32p))

@@ -1,0 +1,720 @@
+/*
+ * tgm_oracle.c -- plain fp64 CPU oracle for the per-batch memory-module stage
+ * of memory-based temporal GNN training, as pipelined by MSPipe (Sheng, Su,
+ * Huang, Wu; KDD'24, arXiv 2402.15113).
+ *
+ * TEST INFRASTRUCTURE.  This file is the yardstick the GPU library is checked
+ * against; it is not part of the product.  Only the test-suite, the smoke check
+ * and the CPU-baseline leg of the benchmark load it.  It shares no code, header,
+ * table or helper with the HIP path.
+ *
+ * What it computes, step by step, for iteration i (batch of events
+ * [iB, min(E,(i+1)B)) ):
+ *   0. snapshot: the node state with the write sets of iterations <= i-1-s
+ *      applied in order (Eq. 2 of Sec. 3.1 with the paper's k = s + 1;
+ *      iterations before the first write set see the initial state, the
+ *      warm-up rule of Appendix D, Algorithm 1);
+ *   1. roots: source, destination and negative of every event, at its time;
+ *   2. most-recent-nb temporal neighbours of each root, strictly earlier events
+ *      only (Sec. 5 training settings; Appendix D.1);
+ *   3. node set U = sorted unique(roots + sampled neighbours) and its state;
+ *   4. memory update s' = GRU(mail || phi(mail_ts - mem_ts), mem) for nodes
+ *      with mail (mem() of Eq. 1; Delta-t as defined under Eq. 1);
+ *   5. embedding h = emb(s'_v, s'_u | u in N(v)): one layer of multi-head
+ *      scaled dot-product attention with a cosine time encoding (emb() of
+ *      Eq. 1, "a single layer GAT");
+ *   6. messages m = msg(s'_v, s'_u, y_uv(t)) as identity concatenation (msg()
+ *      of Eq. 1);
+ *   7. latest-message reduce: one message per node, the one with the largest
+ *      (t, e, role), role src = 0 < dst = 1;
+ *   8. write set W_i of the positive endpoints, queued until iteration i+1+s.
+ *
+ * Everything floating is fp64; fp32 inputs (edge features, weights) are widened
+ * exactly.  Parallel loops (OpenMP) run over independent nodes or roots only;
+ * every dot product is summed in a fixed order, so results do not depend on the
+ * thread count.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)
+#define ORC_EEND (-2)
+
+/* ------------------------------------------------------------------------- */
+/* Time encoding: phi(dt)_d = cos(omega_d * dt + beta_d), the cosine functional
+ * time encoding the paper's models inherit (TGAT, Xu et al. 2020), applied to
+ * the time gaps Delta-t of Eq. 1.  omega and beta are inputs.                */
+void orc_time_encode(int D_t, const double *omega, const double *beta,
+                     double dt, double *out)
+{
+    for (int d = 0; d < D_t; ++d)
+        out[d] = cos(omega[d] * dt + beta[d]);
+}
+
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/* ------------------------------------------------------------------------- */
+/* Memory updater mem() of Eq. 1: the GRU cell (Cho et al. 2014).
+ *   r = sig(W_ir x + b_ir + W_hr h + b_hr)
+ *   z = sig(W_iz x + b_iz + W_hz h + b_hz)
+ *   n = tanh(W_in x + b_in + r * (W_hn h + b_hn))
+ *   h' = (1 - z) * n + z * h
+ * W_ih is [3M x D_x] and W_hh is [3M x M], row blocks in gate order r, z, n. */
+void orc_gru_cell(int M, int D_x, const double *W_ih, const double *W_hh,
+                  const double *b_ih, const double *b_hh,
+                  const double *x, const double *h, double *out)
+{
+    for (int j = 0; j < M; ++j) {
+        double ir = b_ih[j], iz = b_ih[M + j], in_ = b_ih[2 * M + j];
+        double hr = b_hh[j], hz = b_hh[M + j], hn = b_hh[2 * M + j];
+        const double *wr = W_ih + (size_t)j * D_x;
+        const double *wz = W_ih + (size_t)(M + j) * D_x;
+        const double *wn = W_ih + (size_t)(2 * M + j) * D_x;
+        for (int k = 0; k < D_x; ++k) {
+            ir += wr[k] * x[k];
+            iz += wz[k] * x[k];
+            in_ += wn[k] * x[k];
+        }
+        const double *ur = W_hh + (size_t)j * M;
+        const double *uz = W_hh + (size_t)(M + j) * M;
+        const double *un = W_hh + (size_t)(2 * M + j) * M;
+        for (int k = 0; k < M; ++k) {
+            hr += ur[k] * h[k];
+            hz += uz[k] * h[k];
+            hn += un[k] * h[k];
+        }
+        double r = sigmoid(ir + hr);
+        double z = sigmoid(iz + hz);
+        double n = tanh(in_ + r * hn);
+        out[j] = (1.0 - z) * n + z * h[j];
+    }
+}
+
+/* y[rows] = W[rows x cols] * x[cols] + b[rows] */
+static void matvec(int rows, int cols, const double *W, const double *b,
+                   const double *x, double *y)
+{
+    for (int r = 0; r < rows; ++r) {
+        double acc = b ? b[r] : 0.0;
+        const double *w = W + (size_t)r * cols;
+        for (int k = 0; k < cols; ++k)
+            acc += w[k] * x[k];
+        y[r] = acc;
+    }
+}
+
+/* ------------------------------------------------------------------------- */
+/* Embedding module emb() of Eq. 1 for one root v queried at time tq, from its
+ * updated memory s_v and its cnt sampled neighbours u_j (memories s_u[j],
+ * edge features f[j], event times nts[j]):
+ *   q   = W_q [s_v || phi(0)] + b_q
+ *   K_j = W_k [s_u_j || f_j || phi(tq - nts_j)] + b_k,  V_j likewise with W_v
+ *   per head eta (width d_h = M / H):
+ *     alpha_j = softmax_j( q_eta . K_eta,j / sqrt(d_h) ),  a_eta = sum_j alpha_j V_eta,j
+ *   a = concat_eta a_eta  (a = 0 when cnt = 0)
+ *   h = ReLU(W_o [a || s_v] + b_o)
+ * Attention width d_a = M.                                                    */
+typedef struct {
+    int M, D_e, D_t, H;
+    const double *omega, *beta;
+    const double *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+} orc_attn_w;
+
+static void embed_root(const orc_attn_w *w, const double *s_v, double tq,
+                       int cnt, const double *const *s_u, const double *const *f,
+                       const double *nts, double *h_out)
+{
+    const int M = w->M, D_e = w->D_e, D_t = w->D_t, H = w->H;
+    const int d_a = M, d_h = M / H;
+    const int D_q = M + D_t, D_kv = M + D_e + D_t;
+    double *buf = (double *)malloc(sizeof(double) *
+        (size_t)(D_q + d_a + D_kv + 2 * (size_t)(cnt > 0 ? cnt : 1) * d_a + cnt + d_a + d_a + M));
+    double *xq = buf;                      /* [D_q] */
+    double *q = xq + D_q;                  /* [d_a] */
+    double *kap = q + d_a;                 /* [D_kv] */
+    double *K = kap + D_kv;                /* [cnt x d_a] */
+    double *V = K + (size_t)(cnt > 0 ? cnt : 1) * d_a;
+    double *sc = V + (size_t)(cnt > 0 ? cnt : 1) * d_a;   /* [cnt] */
+    double *a = sc + cnt;                  /* [d_a] */
+    double *xo = a + d_a;                  /* [d_a + M] */
+
+    memcpy(xq, s_v, sizeof(double) * M);
+    orc_time_encode(D_t, w->omega, w->beta, 0.0, xq + M);
+    matvec(d_a, D_q, w->W_q, w->b_q, xq, q);
+
+    for (int j = 0; j < cnt; ++j) {
+        memcpy(kap, s_u[j], sizeof(double) * M);
+        for (int d = 0; d < D_e; ++d)
+            kap[M + d] = f[j][d];
+        orc_time_encode(D_t, w->omega, w->beta, tq - nts[j], kap + M + D_e);
+        matvec(d_a, D_kv, w->W_k, w->b_k, kap, K + (size_t)j * d_a);
+        matvec(d_a, D_kv, w->W_v, w->b_v, kap, V + (size_t)j * d_a);
+    }
+
+    const double scale = 1.0 / sqrt((double)d_h);
+    for (int k = 0; k < d_a; ++k)
+        a[k] = 0.0;
+    for (int eta = 0; eta < H; ++eta) {
+        const int o = eta * d_h;
+        if (cnt == 0)
+            break;
+        double mx = -INFINITY;
+        for (int j = 0; j < cnt; ++j) {
+            double dot = 0.0;
+            for (int k = 0; k < d_h; ++k)
+                dot += q[o + k] * K[(size_t)j * d_a + o + k];
+            sc[j] = dot * scale;
+            if (sc[j] > mx)
+                mx = sc[j];
+        }
+        /* softmax; the shift by the maximum leaves the value unchanged */
+        double den = 0.0;
+        for (int j = 0; j < cnt; ++j) {
+            sc[j] = exp(sc[j] - mx);
+            den += sc[j];
+        }
+        for (int j = 0; j < cnt; ++j) {
+            const double al = sc[j] / den;
+            for (int k = 0; k < d_h; ++k)
+                a[o + k] += al * V[(size_t)j * d_a + o + k];
+        }
+    }
+
+    memcpy(xo, a, sizeof(double) * d_a);
+    memcpy(xo + d_a, s_v, sizeof(double) * M);
+    matvec(M, d_a + M, w->W_o, w->b_o, xo, h_out);
+    for (int k = 0; k < M; ++k)
+        if (h_out[k] < 0.0)
+            h_out[k] = 0.0;
+    free(buf);
+}
+
+/* Exported form of embed_root for tests: s_u is [cnt x M], f is [cnt x D_e]. */
+void orc_embed_one(int M, int D_e, int D_t, int H,
+                   const double *omega, const double *beta,
+                   const double *W_q, const double *b_q,
+                   const double *W_k, const double *b_k,
+                   const double *W_v, const double *b_v,
+                   const double *W_o, const double *b_o,
+                   const double *s_v, double tq, int cnt,
+                   const double *s_u, const double *f, const double *nts,
+                   double *h_out)
+{
+    orc_attn_w w = {M, D_e, D_t, H, omega, beta, W_q, b_q, W_k, b_k, W_v, b_v, W_o, b_o};
+    const double **pu = (const double **)malloc(sizeof(void *) * (cnt > 0 ? cnt : 1));
+    const double **pf = (const double **)malloc(sizeof(void *) * (cnt > 0 ? cnt : 1));
+    for (int j = 0; j < cnt; ++j) {
+        pu[j] = s_u + (size_t)j * M;
+        pf[j] = f + (size_t)j * D_e;
+    }
+    embed_root(&w, s_v, tq, cnt, pu, pf, nts, h_out);
+    free(pu);
+    free(pf);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Temporal adjacency: for every node, the events that touch it, in event order.
+ * Events are sorted by (t, e), so each list is sorted by (t, e) too.  A
+ * self-loop is listed once.                                                   */
+typedef struct {
+    int N;
+    int64_t E;
+    int64_t *off;   /* [N+1] */
+    int32_t *ev;    /* event ids */
+} orc_adj;
+
+static int build_adj(orc_adj *g, int N, int64_t E, const int32_t *src, const int32_t *dst)
+{
+    g->N = N;
+    g->E = E;
+    g->off = (int64_t *)calloc((size_t)N + 1, sizeof(int64_t));
+    if (!g->off)
+        return ORC_EINVAL;
+    for (int64_t e = 0; e < E; ++e) {
+        g->off[src[e] + 1]++;
+        if (dst[e] != src[e])
+            g->off[dst[e] + 1]++;
+    }
+    for (int v = 0; v < N; ++v)
+        g->off[v + 1] += g->off[v];
+    g->ev = (int32_t *)malloc(sizeof(int32_t) * (size_t)(g->off[N] > 0 ? g->off[N] : 1));
+    int64_t *fill = (int64_t *)malloc(sizeof(int64_t) * (size_t)N);
+    if (!g->ev || !fill)
+        return ORC_EINVAL;
+    memcpy(fill, g->off, sizeof(int64_t) * (size_t)N);
+    for (int64_t e = 0; e < E; ++e) {
+        g->ev[fill[src[e]]++] = (int32_t)e;
+        if (dst[e] != src[e])
+            g->ev[fill[dst[e]]++] = (int32_t)e;
+    }
+    free(fill);
+    return ORC_OK;
+}
+
+static void free_adj(orc_adj *g)
+{
+    free(g->off);
+    free(g->ev);
+    g->off = NULL;
+    g->ev = NULL;
+}
+
+/* Most-recent-nb temporal neighbours of root v at query time tq: among the
+ * events e' touching v with t[e'] < tq (strictly earlier), the nb largest by
+ * (t[e'], e'), newest first.  The neighbour is the other endpoint (v itself for
+ * a self-loop).  Unused slots hold nbr = eid = -1 and nts = 0.               */
+static void sample_root(const orc_adj *g, const int32_t *src, const int32_t *dst,
+                        const double *t, int v, double tq, int nb,
+                        int32_t *nbr, int32_t *eid, double *nts, int32_t *cnt)
+{
+    int64_t lo = g->off[v], hi = g->off[v + 1];
+    /* first list position whose event time is >= tq (binary search) */
+    while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (t[g->ev[mid]] < tq)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    int c = 0;
+    for (int64_t k = lo - 1; k >= g->off[v] && c < nb; --k, ++c) {
+        int32_t e = g->ev[k];
+        nbr[c] = (src[e] == v) ? dst[e] : src[e];
+        eid[c] = e;
+        nts[c] = t[e];
+    }
+    *cnt = c;
+    for (; c < nb; ++c) {
+        nbr[c] = -1;
+        eid[c] = -1;
+        nts[c] = 0.0;
+    }
+}
+
+/* Exported sampler over a stream (builds the adjacency on every call). */
+int orc_sample(int N, int64_t E, const int32_t *src, const int32_t *dst, const double *t,
+               int R, const int32_t *root, const double *root_ts, int nb,
+               int32_t *nbr, int32_t *eid, double *nts, int32_t *cnt)
+{
+    orc_adj g;
+    if (build_adj(&g, N, E, src, dst) != ORC_OK)
+        return ORC_EINVAL;
+    for (int r = 0; r < R; ++r)
+        sample_root(&g, src, dst, t, root[r], root_ts[r], nb, nbr + (size_t)r * nb,
+                    eid + (size_t)r * nb, nts + (size_t)r * nb, cnt + r);
+    free_adj(&g);
+    return ORC_OK;
+}
+
+static int cmp_i32(const void *a, const void *b)
+{
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+/* ------------------------------------------------------------------------- */
+/* The stateful driver.                                                        */
+typedef struct {
+    int64_t iter;
+    int n;
+    int32_t *node;
+    double *mem, *mem_ts, *mail, *mail_ts;
+} orc_wset;
+
+typedef struct {
+    int N;
+    int64_t E;
+    const int32_t *src, *dst, *neg;
+    const double *t;
+    const float *efeat;
+    int D_e, M, D_t, H, nb, B, s;
+    int D_m, D_x;
+    /* fp64 weights */
+    double *W_ih, *W_hh, *b_ih, *b_hh, *omega, *beta;
+    double *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+    orc_adj adj;
+    /* committed state */
+    double *mem, *mem_ts, *mail, *mail_ts;
+    int32_t *ver;
+    /* queued write sets, oldest first */
+    orc_wset *q;
+    int nq, capq;
+    int64_t next_iter;
+} orc_ctx;
+
+typedef struct {
+    int N;
+    int64_t E;
+    const int32_t *src, *dst, *neg;
+    const double *t;
+    const float *efeat;
+    int D_e, M, D_t, H, nb, B, s;
+    const float *W_ih, *W_hh, *b_ih, *b_hh;
+    const double *omega, *beta;
+    const float *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+} orc_desc;
+
+/* Per-iteration outputs; every pointer may be NULL.  Capacities: R = 3B roots,
+ * U <= N nodes. */
+typedef struct {
+    int64_t iter;
+    int32_t b, R, n_U, pad_;
+    int32_t *root;
+    double *root_ts;
+    int32_t *nbr, *eid;
+    double *nts;
+    int32_t *cnt;
+    int32_t *U, *root_pos, *nbr_pos;
+    double *f_mem, *f_mem_ts, *f_mail, *f_mail_ts;
+    int32_t *f_ver;
+    double *s_new, *new_mem_ts;
+    double *h;
+    int64_t *winner;
+} orc_step_out;
+
+static double *widen(const float *x, size_t n)
+{
+    double *y = (double *)malloc(sizeof(double) * (n ? n : 1));
+    for (size_t i = 0; i < n; ++i)
+        y[i] = (double)x[i];
+    return y;
+}
+
+static double *copyd(const double *x, size_t n)
+{
+    double *y = (double *)malloc(sizeof(double) * (n ? n : 1));
+    if (n)
+        memcpy(y, x, sizeof(double) * n);
+    return y;
+}
+
+void *orc_create(const orc_desc *d)
+{
+    if (!d || d->N <= 0 || d->E < 0 || d->M <= 0 || d->H <= 0 || d->M % d->H != 0 ||
+        d->nb < 0 || d->B <= 0 || d->s < 0 || d->D_t < 0 || d->D_e < 0)
+        return NULL;
+    orc_ctx *c = (orc_ctx *)calloc(1, sizeof(orc_ctx));
+    c->N = d->N; c->E = d->E;
+    c->src = d->src; c->dst = d->dst; c->neg = d->neg; c->t = d->t; c->efeat = d->efeat;
+    c->D_e = d->D_e; c->M = d->M; c->D_t = d->D_t; c->H = d->H; c->nb = d->nb;
+    c->B = d->B; c->s = d->s;
+    c->D_m = 2 * d->M + d->D_e;
+    c->D_x = c->D_m + d->D_t;
+    const int M = c->M, D_x = c->D_x, D_t = c->D_t, D_e = c->D_e;
+    c->W_ih = widen(d->W_ih, (size_t)3 * M * D_x);
+    c->W_hh = widen(d->W_hh, (size_t)3 * M * M);
+    c->b_ih = widen(d->b_ih, (size_t)3 * M);
+    c->b_hh = widen(d->b_hh, (size_t)3 * M);
+    c->omega = copyd(d->omega, (size_t)D_t);
+    c->beta = copyd(d->beta, (size_t)D_t);
+    c->W_q = widen(d->W_q, (size_t)M * (M + D_t));
+    c->b_q = widen(d->b_q, (size_t)M);
+    c->W_k = widen(d->W_k, (size_t)M * (M + D_e + D_t));
+    c->b_k = widen(d->b_k, (size_t)M);
+    c->W_v = widen(d->W_v, (size_t)M * (M + D_e + D_t));
+    c->b_v = widen(d->b_v, (size_t)M);
+    c->W_o = widen(d->W_o, (size_t)M * (2 * M));
+    c->b_o = widen(d->b_o, (size_t)M);
+    if (build_adj(&c->adj, c->N, c->E, c->src, c->dst) != ORC_OK)
+        return NULL;
+    c->mem = (double *)calloc((size_t)c->N * M, sizeof(double));
+    c->mem_ts = (double *)calloc((size_t)c->N, sizeof(double));
+    c->mail = (double *)calloc((size_t)c->N * c->D_m + 1, sizeof(double));
+    c->mail_ts = (double *)calloc((size_t)c->N, sizeof(double));
+    c->ver = (int32_t *)malloc(sizeof(int32_t) * (size_t)c->N);
+    for (int v = 0; v < c->N; ++v)
+        c->ver[v] = -1;
+    c->capq = c->s + 2;
+    c->q = (orc_wset *)calloc((size_t)c->capq, sizeof(orc_wset));
+    return c;
+}
+
+static void free_wset(orc_wset *w)
+{
+    free(w->node); free(w->mem); free(w->mem_ts); free(w->mail); free(w->mail_ts);
+    memset(w, 0, sizeof(*w));
+}
+
+void orc_destroy(void *p)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (!c)
+        return;
+    free(c->W_ih); free(c->W_hh); free(c->b_ih); free(c->b_hh); free(c->omega); free(c->beta);
+    free(c->W_q); free(c->b_q); free(c->W_k); free(c->b_k); free(c->W_v); free(c->b_v);
+    free(c->W_o); free(c->b_o);
+    free_adj(&c->adj);
+    free(c->mem); free(c->mem_ts); free(c->mail); free(c->mail_ts); free(c->ver);
+    for (int k = 0; k < c->nq; ++k)
+        free_wset(&c->q[k]);
+    free(c->q);
+    free(c);
+}
+
+/* Apply the oldest queued write set to the committed state (last writer wins). */
+static void apply_oldest(orc_ctx *c)
+{
+    orc_wset *w = &c->q[0];
+    const int M = c->M, D_m = c->D_m;
+    for (int k = 0; k < w->n; ++k) {
+        const int v = w->node[k];
+        memcpy(c->mem + (size_t)v * M, w->mem + (size_t)k * M, sizeof(double) * M);
+        memcpy(c->mail + (size_t)v * D_m, w->mail + (size_t)k * D_m, sizeof(double) * D_m);
+        c->mem_ts[v] = w->mem_ts[k];
+        c->mail_ts[v] = w->mail_ts[k];
+        c->ver[v] = (int32_t)w->iter;
+    }
+    free_wset(w);
+    memmove(c->q, c->q + 1, sizeof(orc_wset) * (size_t)(c->nq - 1));
+    c->nq--;
+    memset(&c->q[c->nq], 0, sizeof(orc_wset));
+}
+
+/* Commit every queued write set (end of the run). */
+void orc_flush(void *p)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    while (c->nq > 0)
+        apply_oldest(c);
+}
+
+/* Replace the committed state and the iteration counter; drops the queue.
+ * Reads at iterations i >= it then see this state plus the write sets of
+ * iterations it .. i-1-s. */
+void orc_set_state(void *p, int64_t it, const double *mem, const double *mem_ts,
+                   const double *mail, const double *mail_ts, const int32_t *ver)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    while (c->nq > 0) {
+        free_wset(&c->q[0]);
+        memmove(c->q, c->q + 1, sizeof(orc_wset) * (size_t)(c->nq - 1));
+        c->nq--;
+    }
+    memcpy(c->mem, mem, sizeof(double) * (size_t)c->N * c->M);
+    memcpy(c->mem_ts, mem_ts, sizeof(double) * (size_t)c->N);
+    memcpy(c->mail, mail, sizeof(double) * (size_t)c->N * c->D_m);
+    memcpy(c->mail_ts, mail_ts, sizeof(double) * (size_t)c->N);
+    memcpy(c->ver, ver, sizeof(int32_t) * (size_t)c->N);
+    c->next_iter = it;
+}
+
+void orc_get_state(void *p, double *mem, double *mem_ts, double *mail, double *mail_ts,
+                   int32_t *ver)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (mem) memcpy(mem, c->mem, sizeof(double) * (size_t)c->N * c->M);
+    if (mem_ts) memcpy(mem_ts, c->mem_ts, sizeof(double) * (size_t)c->N);
+    if (mail) memcpy(mail, c->mail, sizeof(double) * (size_t)c->N * c->D_m);
+    if (mail_ts) memcpy(mail_ts, c->mail_ts, sizeof(double) * (size_t)c->N);
+    if (ver) memcpy(ver, c->ver, sizeof(int32_t) * (size_t)c->N);
+}
+
+int64_t orc_next_iter(void *p) { return ((orc_ctx *)p)->next_iter; }
+
+/* One iteration of the stage.  Returns ORC_EEND when the stream is exhausted. */
+int orc_step(void *p, orc_step_out *o)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    const int64_t i = c->next_iter;
+    const int64_t lo = i * c->B;
+    if (lo >= c->E)
+        return ORC_EEND;
+    const int64_t hi = (lo + c->B < c->E) ? lo + c->B : c->E;
+    const int b = (int)(hi - lo);
+    const int R = 3 * b, nb = c->nb, M = c->M, D_m = c->D_m, D_x = c->D_x;
+    const int D_t = c->D_t, D_e = c->D_e, N = c->N;
+
+    /* 0. snapshot: apply every queued write set of iteration <= i-1-s */
+    while (c->nq > 0 && c->q[0].iter <= i - 1 - c->s)
+        apply_oldest(c);
+
+    /* 1. roots: sources, then destinations, then negatives, at the event time */
+    int32_t *root = (int32_t *)malloc(sizeof(int32_t) * R);
+    double *rts = (double *)malloc(sizeof(double) * R);
+    for (int k = 0; k < b; ++k) {
+        root[k] = c->src[lo + k];
+        root[b + k] = c->dst[lo + k];
+        root[2 * b + k] = c->neg[lo + k];
+        rts[k] = rts[b + k] = rts[2 * b + k] = c->t[lo + k];
+    }
+
+    /* 2. temporal sampling */
+    const size_t RS = (size_t)R * (nb > 0 ? nb : 1);
+    int32_t *nbr = (int32_t *)malloc(sizeof(int32_t) * RS);
+    int32_t *eid = (int32_t *)malloc(sizeof(int32_t) * RS);
+    double *nts = (double *)malloc(sizeof(double) * RS);
+    int32_t *cnt = (int32_t *)malloc(sizeof(int32_t) * R);
+    for (int r = 0; r < R; ++r)
+        sample_root(&c->adj, c->src, c->dst, c->t, root[r], rts[r], nb,
+                    nbr + (size_t)r * nb, eid + (size_t)r * nb, nts + (size_t)r * nb, cnt + r);
+
+    /* 3. node set: sorted unique ids of roots and valid neighbours */
+    int32_t *ids = (int32_t *)malloc(sizeof(int32_t) * (R + RS));
+    size_t nid = 0;
+    for (int r = 0; r < R; ++r)
+        ids[nid++] = root[r];
+    for (size_t k = 0; k < (size_t)R * nb; ++k)
+        if (nbr[k] >= 0)
+            ids[nid++] = nbr[k];
+    qsort(ids, nid, sizeof(int32_t), cmp_i32);
+    int nU = 0;
+    for (size_t k = 0; k < nid; ++k)
+        if (nU == 0 || ids[k] != ids[nU - 1])
+            ids[nU++] = ids[k];
+    int32_t *pos = (int32_t *)malloc(sizeof(int32_t) * N);
+    for (int v = 0; v < N; ++v)
+        pos[v] = -1;
+    for (int k = 0; k < nU; ++k)
+        pos[ids[k]] = k;
+
+    /* fetched rows from the snapshot */
+    double *fm = (double *)malloc(sizeof(double) * (size_t)nU * M);
+    double *fmts = (double *)malloc(sizeof(double) * nU);
+    double *fl = (double *)malloc(sizeof(double) * ((size_t)nU * D_m + 1));
+    double *flts = (double *)malloc(sizeof(double) * nU);
+    int32_t *fver = (int32_t *)malloc(sizeof(int32_t) * nU);
+    for (int k = 0; k < nU; ++k) {
+        const int v = ids[k];
+        memcpy(fm + (size_t)k * M, c->mem + (size_t)v * M, sizeof(double) * M);
+        memcpy(fl + (size_t)k * D_m, c->mail + (size_t)v * D_m, sizeof(double) * D_m);
+        fmts[k] = c->mem_ts[v];
+        flts[k] = c->mail_ts[v];
+        fver[k] = c->ver[v];
+    }
+
+    /* 4. memory update of every node in U that holds mail */
+    double *sn = (double *)malloc(sizeof(double) * (size_t)nU * M);
+    double *nmts = (double *)malloc(sizeof(double) * nU);
+    #pragma omp parallel for schedule(dynamic, 8)
+    for (int k = 0; k < nU; ++k) {
+        if (fver[k] >= 0) {
+            double *x = (double *)malloc(sizeof(double) * D_x);
+            memcpy(x, fl + (size_t)k * D_m, sizeof(double) * D_m);
+            orc_time_encode(D_t, c->omega, c->beta, flts[k] - fmts[k], x + D_m);
+            orc_gru_cell(M, D_x, c->W_ih, c->W_hh, c->b_ih, c->b_hh, x, fm + (size_t)k * M,
+                         sn + (size_t)k * M);
+            nmts[k] = flts[k];
+            free(x);
+        } else {
+            memcpy(sn + (size_t)k * M, fm + (size_t)k * M, sizeof(double) * M);
+            nmts[k] = fmts[k];
+        }
+    }
+
+    /* 5. embeddings of every root */
+    double *h = (double *)malloc(sizeof(double) * (size_t)R * M);
+    orc_attn_w aw = {M, D_e, D_t, c->H, c->omega, c->beta, c->W_q, c->b_q, c->W_k, c->b_k,
+                     c->W_v, c->b_v, c->W_o, c->b_o};
+    #pragma omp parallel for schedule(dynamic, 8)
+    for (int r = 0; r < R; ++r) {
+        const int cr = cnt[r];
+        const double **pu = (const double **)malloc(sizeof(void *) * (nb > 0 ? nb : 1));
+        const double **pf = (const double **)malloc(sizeof(void *) * (nb > 0 ? nb : 1));
+        double *frow = (double *)malloc(sizeof(double) * ((size_t)(nb > 0 ? nb : 1) * D_e + 1));
+        for (int j = 0; j < cr; ++j) {
+            const size_t sl = (size_t)r * nb + j;
+            pu[j] = sn + (size_t)pos[nbr[sl]] * M;
+            for (int d = 0; d < D_e; ++d)
+                frow[(size_t)j * D_e + d] = (double)c->efeat[(size_t)eid[sl] * D_e + d];
+            pf[j] = frow + (size_t)j * D_e;
+        }
+        embed_root(&aw, sn + (size_t)pos[root[r]] * M, rts[r], cr, pu, pf,
+                   nts + (size_t)r * nb, h + (size_t)r * M);
+        free(pu); free(pf); free(frow);
+    }
+
+    /* 6-7. messages of the positive events and the latest-message reduce:
+     * per endpoint node, the candidate (t, e, role) that is largest wins */
+    int64_t *win = (int64_t *)malloc(sizeof(int64_t) * (nU > 0 ? nU : 1));
+    for (int k = 0; k < nU; ++k)
+        win[k] = -1;
+    for (int64_t e = lo; e < hi; ++e) {
+        for (int role = 0; role < 2; ++role) {
+            const int w = role == 0 ? c->src[e] : c->dst[e];
+            const int k = pos[w];
+            const int64_t cand = 2 * e + role;
+            if (win[k] < 0) {
+                win[k] = cand;
+            } else {
+                const int64_t e0 = win[k] / 2;
+                const int r0 = (int)(win[k] % 2);
+                const int later = (c->t[e] > c->t[e0]) ||
+                                  (c->t[e] == c->t[e0] && (e > e0 || (e == e0 && role > r0)));
+                if (later)
+                    win[k] = cand;
+            }
+        }
+    }
+
+    /* 8. write set of iteration i: updated memory and the winning message */
+    orc_wset W;
+    memset(&W, 0, sizeof(W));
+    W.iter = i;
+    int nw = 0;
+    for (int k = 0; k < nU; ++k)
+        nw += win[k] >= 0;
+    W.n = nw;
+    W.node = (int32_t *)malloc(sizeof(int32_t) * (nw ? nw : 1));
+    W.mem = (double *)malloc(sizeof(double) * ((size_t)nw * M + 1));
+    W.mem_ts = (double *)malloc(sizeof(double) * (nw ? nw : 1));
+    W.mail = (double *)malloc(sizeof(double) * ((size_t)nw * D_m + 1));
+    W.mail_ts = (double *)malloc(sizeof(double) * (nw ? nw : 1));
+    int w_ = 0;
+    for (int k = 0; k < nU; ++k) {
+        if (win[k] < 0)
+            continue;
+        const int64_t e = win[k] / 2;
+        const int role = (int)(win[k] % 2);
+        const int other = role == 0 ? c->dst[e] : c->src[e];
+        W.node[w_] = ids[k];
+        memcpy(W.mem + (size_t)w_ * M, sn + (size_t)k * M, sizeof(double) * M);
+        W.mem_ts[w_] = nmts[k];
+        double *ml = W.mail + (size_t)w_ * D_m;
+        memcpy(ml, sn + (size_t)k * M, sizeof(double) * M);
+        memcpy(ml + M, sn + (size_t)pos[other] * M, sizeof(double) * M);
+        for (int d = 0; d < D_e; ++d)
+            ml[2 * M + d] = (double)c->efeat[(size_t)e * D_e + d];
+        W.mail_ts[w_] = c->t[e];
+        ++w_;
+    }
+    if (c->nq == c->capq) {
+        c->capq *= 2;
+        c->q = (orc_wset *)realloc(c->q, sizeof(orc_wset) * (size_t)c->capq);
+    }
+    c->q[c->nq++] = W;
+
+    /* outputs */
+    if (o) {
+        o->iter = i; o->b = b; o->R = R; o->n_U = nU;
+        if (o->root) memcpy(o->root, root, sizeof(int32_t) * R);
+        if (o->root_ts) memcpy(o->root_ts, rts, sizeof(double) * R);
+        if (o->nbr) memcpy(o->nbr, nbr, sizeof(int32_t) * (size_t)R * nb);
+        if (o->eid) memcpy(o->eid, eid, sizeof(int32_t) * (size_t)R * nb);
+        if (o->nts) memcpy(o->nts, nts, sizeof(double) * (size_t)R * nb);
+        if (o->cnt) memcpy(o->cnt, cnt, sizeof(int32_t) * R);
+        if (o->U) memcpy(o->U, ids, sizeof(int32_t) * nU);
+        if (o->root_pos)
+            for (int r = 0; r < R; ++r) o->root_pos[r] = pos[root[r]];
+        if (o->nbr_pos)
+            for (size_t k = 0; k < (size_t)R * nb; ++k)
+                o->nbr_pos[k] = nbr[k] >= 0 ? pos[nbr[k]] : -1;
+        if (o->f_mem) memcpy(o->f_mem, fm, sizeof(double) * (size_t)nU * M);
+        if (o->f_mem_ts) memcpy(o->f_mem_ts, fmts, sizeof(double) * nU);
+        if (o->f_mail) memcpy(o->f_mail, fl, sizeof(double) * (size_t)nU * D_m);
+        if (o->f_mail_ts) memcpy(o->f_mail_ts, flts, sizeof(double) * nU);
+        if (o->f_ver) memcpy(o->f_ver, fver, sizeof(int32_t) * nU);
+        if (o->s_new) memcpy(o->s_new, sn, sizeof(double) * (size_t)nU * M);
+        if (o->new_mem_ts) memcpy(o->new_mem_ts, nmts, sizeof(double) * nU);
+        if (o->h) memcpy(o->h, h, sizeof(double) * (size_t)R * M);
+        if (o->winner) memcpy(o->winner, win, sizeof(int64_t) * nU);
+    }
+
+    free(root); free(rts); free(nbr); free(eid); free(nts); free(cnt); free(ids); free(pos);
+    free(fm); free(fmts); free(fl); free(flts); free(fver); free(sn); free(nmts); free(h);
+    free(win);
+    c->next_iter = i + 1;
+    return ORC_OK;
+}
