@@ -1,0 +1,245 @@
+/*
+ * tgm.h -- C ABI of libtgm, the MI355X (gfx950) implementation of the per-batch
+ * memory-module stage of memory-based temporal GNN training.
+ *
+ * Method: MSPipe, "Efficient Temporal GNN Training via Staleness-Aware
+ * Pipeline" (Sheng, Su, Huang, Wu; KDD'24, arXiv 2402.15113).  One training
+ * iteration i processes a batch of B consecutive events of a time-sorted event
+ * stream (Sec. 2, event-based dynamic graphs).  Its memory-module stage is:
+ *
+ *   tgm_batch_roots    roots of the batch: sources, destinations, negatives
+ *   tgm_sample         most-recent-nb temporal neighbours of every root
+ *   tgm_node_set       sorted unique node set U of roots and neighbours
+ *   tgm_fetch_memory   node memory and mailbox of U as of iteration i-1-s
+ *   tgm_update_memory  GRU memory update of U, latest-message reduce,
+ *                      staged write-back of the batch's endpoints
+ *   tgm_embed          time-encoded multi-head attention embedding of roots
+ *
+ * Conventions shared by every call:
+ *  - All array arguments are DEVICE pointers unless marked "host".  Arrays are
+ *    dense and row-major; "[a x b]" means a rows of b elements.
+ *  - Ids are int32 in [0, N); timestamps are fp64; features, memory and
+ *    weights are fp32.  Event e (0-based) has src[e], dst[e], t[e], neg[e] and
+ *    edge-feature row efeat[e].  Events are sorted by (t, e).
+ *  - Every compute call takes a HIP stream (hipStream_t passed as void*; NULL
+ *    is the legacy default stream), enqueues its kernels there and returns
+ *    without synchronising.  Argument checks are done on the host before
+ *    anything is enqueued; on failure nothing is enqueued.  Faults raised by
+ *    the device surface after the caller synchronises, through
+ *    tgm_last_device_error().
+ *  - Handles own the device memory they allocate at creation and free it in
+ *    their destroy call.  Per-batch calls allocate nothing.  Arrays passed to
+ *    tgm_graph_create are BORROWED: they must stay alive and unchanged until
+ *    the graph is destroyed.
+ *  - A handle must not be used from two streams or threads at once.
+ */
+#ifndef TGM_H
+#define TGM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tgm_status_t;
+#define TGM_OK 0
+#define TGM_EINVAL (-1)   /* null pointer, bad size or dimension             */
+#define TGM_ERANGE (-2)   /* input content out of range (ids, unsorted time) */
+#define TGM_EORDER (-3)   /* iteration protocol violated (see fetch/update)  */
+#define TGM_ESIZE (-4)    /* a capacity given at creation is exceeded        */
+#define TGM_EDEVICE (-5)  /* a HIP runtime call failed                       */
+#define TGM_ENOMEM (-6)   /* device allocation failed at creation            */
+
+typedef struct tgm_graph *tgm_graph_t;
+typedef struct tgm_state *tgm_state_t;
+typedef struct tgm_model *tgm_model_t;
+
+/* Static string for a status code. */
+const char *tgm_status_str(tgm_status_t status);
+/* First HIP error recorded by a library call since the last query (then
+ * cleared), as TGM_EDEVICE, or TGM_OK.  Also polls hipGetLastError(). */
+tgm_status_t tgm_last_device_error(void);
+/* ABI version: major * 100 + minor. */
+int32_t tgm_version(void);
+
+/* ------------------------------------------------------------------------
+ * Event graph (Sec. 2: the event set y_uv(t) of a dynamic graph).
+ *
+ * tgm_graph_create builds, on the device, the temporal adjacency used by the
+ * sampler: for every node, the events that touch it (as source or
+ * destination; a self-loop once), sorted by (t, e).  src, dst, t and neg are
+ * [E] device arrays; efeat is [E x D_e] fp32 on the device, NULL iff D_e == 0.
+ * All are borrowed.  The call checks ids in [0, N), t non-decreasing, and
+ * synchronises `stream` once (creation is not a per-batch call).
+ * Errors: TGM_EINVAL (sizes, null), TGM_ERANGE (content), TGM_ENOMEM.
+ */
+tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *src, const int32_t *dst,
+                              const double *t, const int32_t *neg, const float *efeat,
+                              int32_t D_e, void *stream, tgm_graph_t *out);
+tgm_status_t tgm_graph_destroy(tgm_graph_t g);
+/* Host outputs; any pointer may be NULL.  n_adj = total adjacency entries. */
+tgm_status_t tgm_graph_info(tgm_graph_t g, int32_t *N, int64_t *E, int32_t *D_e,
+                            int64_t *n_adj);
+
+/* Roots of the batch of events [first_event, first_event + b): the training
+ * samples of an iteration are its events, each with a source, a destination
+ * and one negative destination (Sec. 5, training settings: equal numbers of
+ * positive and negative pairs; Appendix E: three nodes per sample).
+ * Output root[3b] = src[batch] ++ dst[batch] ++ neg[batch], root_ts[3b] = the
+ * event time, repeated three times. */
+tgm_status_t tgm_batch_roots(tgm_graph_t g, int64_t first_event, int32_t b, int32_t *root,
+                             double *root_ts, void *stream);
+
+/* Most-recent-nb temporal neighbour sampling (Sec. 5: the 10 most recent
+ * 1-hop neighbours; Appendix D.1: fixed-size most-recent sampler).  For root
+ * r = (v, root_ts[r]) the neighbours are the events e' touching v with
+ * t[e'] < root_ts[r] (strictly earlier), the nb largest by (t[e'], e'),
+ * newest first; the neighbour is the other endpoint (v for a self-loop).
+ * Outputs: nbr, eid [R x nb] int32, nts [R x nb] fp64 (event time), cnt [R].
+ * Slots j >= cnt[r] hold nbr = eid = -1, nts = 0.  1 <= nb <= 64.  R may be 0. */
+tgm_status_t tgm_sample(tgm_graph_t g, const int32_t *root, const double *root_ts, int32_t R,
+                        int32_t nb, int32_t *nbr, int32_t *eid, double *nts, int32_t *cnt,
+                        void *stream);
+
+/* Node set of the subgraph: U = sorted unique(root[0..R) and every valid
+ * nbr).  nodes [cap] receives U, *n_nodes (device int32) its size, root_pos
+ * [R] and nbr_pos [R x nb] the position in U of every root and neighbour (-1
+ * for empty slots).  cap must be >= min(N, R * (nb + 1)).  Uses the graph's
+ * scratch: calls on one graph must be stream-ordered. */
+tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t R, const int32_t *nbr,
+                          int32_t nb, int32_t *nodes, int32_t *n_nodes, int32_t cap,
+                          int32_t *root_pos, int32_t *nbr_pos, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Node memory and mailbox (Sec. 2: node memory s_v; Sec. 3.1, Eq. 2: reads
+ * of stale memory).  Per node: mem [M] fp32, mem_ts fp64 (time of the last
+ * memory update), mail [D_m] fp32 with D_m = 2M + D_e (the pending message),
+ * mail_ts fp64 (its event time) and ver int32 (iteration of the last write,
+ * -1 = never written; a node has mail iff ver >= 0).  Initially all zero and
+ * ver = -1.
+ *
+ * Staleness s >= 0: a fetch at iteration i sees exactly the writes of
+ * iterations <= i-1-s (the paper's staleness k equals s + 1; s = 0 is strictly
+ * sequential).  Writes of later iterations are staged in a ring of s + 1
+ * write sets and committed, in iteration order, by the fetch that first needs
+ * them.  max_batch bounds b of every update.
+ */
+tgm_status_t tgm_state_create(int32_t N, int32_t M, int32_t D_m, int32_t s, int32_t max_batch,
+                              void *stream, tgm_state_t *out);
+tgm_status_t tgm_state_destroy(tgm_state_t st);
+/* Back to the initial state at iteration 0 (tables zero, ver = -1). */
+tgm_status_t tgm_state_reset(tgm_state_t st, void *stream);
+/* Commit every staged write set. */
+tgm_status_t tgm_state_flush(tgm_state_t st, void *stream);
+/* Copy the committed tables out: mem [N x M], mem_ts [N], mail [N x D_m],
+ * mail_ts [N], ver [N] (device; any may be NULL). */
+tgm_status_t tgm_state_read(tgm_state_t st, float *mem, double *mem_ts, float *mail,
+                            double *mail_ts, int32_t *ver, void *stream);
+/* Replace the committed tables (same layouts) and restart the protocol at
+ * iteration `iter`: staged write sets are dropped, and a fetch at i >= iter
+ * sees the loaded tables plus the writes of iterations iter .. i-1-s. */
+tgm_status_t tgm_state_load(tgm_state_t st, int64_t iter, const float *mem, const double *mem_ts,
+                            const float *mail, const double *mail_ts, const int32_t *ver,
+                            void *stream);
+
+/* Memory fetch of iteration `iter` (Alg. 1's fetch_memory, after its wait
+ * until the update of iteration iter-k is done, with k = s + 1).  First commits
+ * every staged write set of iteration <= iter-1-s, then gathers, for the
+ * *n_nodes (device) nodes in nodes[]: mem [cap x M], mem_ts [cap],
+ * mail [cap x D_m], mail_ts [cap], ver [cap].  Rows past *n_nodes are not
+ * written.  TGM_EORDER if the update of some iteration <= iter-1-s has not
+ * been issued, or if iter is below a previously fetched iteration. */
+tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int32_t *nodes,
+                              const int32_t *n_nodes, int32_t cap, float *mem, double *mem_ts,
+                              float *mail, double *mail_ts, int32_t *ver, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Model (Eq. 1: msg, mem, emb).  Weights are HOST arrays, copied and packed
+ * at creation:
+ *   GRU memory updater: W_ih [3M x D_x], W_hh [3M x M], b_ih, b_hh [3M], gate
+ *     row blocks in order r, z, n; D_x = D_m + D_t.
+ *   Time encoding phi(dt)_d = cos(omega_d dt + beta_d): omega, beta [D_t] fp64.
+ *   Attention (d_a = M, H heads of width M / H):
+ *     W_q [M x (M + D_t)], b_q [M]; W_k, W_v [M x (M + D_e + D_t)], b_k, b_v [M];
+ *     W_o [M x 2M], b_o [M].
+ * max_nodes and max_roots bound the node-set size and R of every call.
+ */
+typedef struct {
+    int32_t M, D_e, D_t, H, nb;
+    int32_t max_nodes, max_roots;
+} tgm_model_desc;
+
+typedef struct {
+    const float *W_ih, *W_hh, *b_ih, *b_hh;
+    const double *omega, *beta;
+    const float *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+} tgm_weights;
+
+tgm_status_t tgm_model_create(const tgm_model_desc *desc, const tgm_weights *w, void *stream,
+                              tgm_model_t *out);
+tgm_status_t tgm_model_destroy(tgm_model_t m);
+
+/* Memory update of iteration `iter` (Eq. 1 with the stale reads of Eq. 2;
+ * Alg. 1's update_mem):
+ *  - for every node p < *n_nodes of the fetched set with ver[p] >= 0:
+ *      mem_new[p] = GRU([mail[p] || phi(mail_ts[p] - mem_ts[p])], mem[p]),
+ *      new_mem_ts[p] = mail_ts[p]  (Delta-t as defined under Eq. 1);
+ *    otherwise mem_new[p] = mem[p], new_mem_ts[p] = mem_ts[p];
+ *  - messages of the b positive events [first_event, first_event + b)
+ *    (identity msg: [s'_self || s'_other || efeat[e]], time t[e]) and the
+ *    latest-message reduce: per endpoint node the message with the largest
+ *    (t, e, role), role src = 0 < dst = 1;
+ *  - stages the write set of iteration `iter`: for each endpoint node w,
+ *    mem <- mem_new[w], mem_ts <- new_mem_ts[w], mail <- winning message,
+ *    mail_ts <- its time, ver <- iter.
+ * src_pos / dst_pos [b] are the positions in the node set of each event's
+ * source and destination (the first and second thirds of root_pos).
+ * Outputs: mem_new [cap x M], new_mem_ts [cap] (may be NULL), winner [cap]
+ * int64 (may be NULL): 2e + role of the winning message per node, -1 if none.
+ * TGM_EORDER unless iter is the next iteration after the last update (0 after
+ * create/reset, `iter` after load) and the fetch of iter has been issued. */
+tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
+                               const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
+                               const float *mem, const double *mem_ts, const float *mail,
+                               const double *mail_ts, const int32_t *ver, int64_t first_event,
+                               int32_t b, const int32_t *src_pos, const int32_t *dst_pos,
+                               float *mem_new, double *new_mem_ts, int64_t *winner,
+                               void *stream);
+
+/* Embedding (Eq. 1's emb, "a single layer GAT" in the paper; here one layer of
+ * H-head scaled dot-product attention over the sampled neighbours):
+ *   q   = W_q [s'_v || phi(0)] + b_q
+ *   K_j = W_k [s'_u_j || efeat[eid_j] || phi(root_ts - nts_j)] + b_k, V_j with W_v
+ *   a   = concat over heads of softmax_j(q.K_j / sqrt(M/H)) V_j  (0 if cnt = 0)
+ *   h   = ReLU(W_o [a || s'_v] + b_o)
+ * root_pos [R], root_ts [R], nbr_pos/eid/nts [R x nb], cnt [R] as produced by
+ * the calls above; mem_new [cap x M] the updated memory of the node set.
+ * Output h [R x M]. */
+tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
+                       const int32_t *root_pos, const double *root_ts, const int32_t *nbr_pos,
+                       const int32_t *eid, const double *nts, const int32_t *cnt,
+                       const float *mem_new, const int32_t *n_nodes, int32_t cap, float *h,
+                       void *stream);
+
+/* ------------------------------------------------------------------------
+ * Per-kernel timing.  When enabled, every kernel the library launches is
+ * bracketed by two HIP events recorded on its own stream; tgm_profile_get
+ * synchronises those events and reports, per kernel name, the number of
+ * launches and their summed duration.  Off by default; enabling it adds two
+ * event records per launch.  Not thread-safe.
+ */
+tgm_status_t tgm_profile_enable(int32_t on);
+/* Drops everything recorded so far. */
+tgm_status_t tgm_profile_reset(void);
+/* Folds pending records into the totals; returns the number of kernel names. */
+int32_t tgm_profile_count(void);
+/* Totals of the k-th kernel name (0 <= k < tgm_profile_count()).  *name is a
+ * static string. */
+tgm_status_t tgm_profile_get(int32_t k, const char **name, int64_t *launches, double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TGM_H */

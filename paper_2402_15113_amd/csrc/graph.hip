@@ -1,0 +1,411 @@
+// Event graph, batch roots, temporal sampler and node set.
+#include <hipcub/hipcub.hpp>
+
+#include <climits>
+
+#include "common.h"
+
+using namespace tgm;
+
+namespace {
+
+// ------------------------------------------------------------ graph build
+// Checks ids in [0, N) and t non-decreasing.  bad[0]: id out of range,
+// bad[1]: time out of order.
+__global__ void k_validate(int64_t E, int32_t N, const int32_t *__restrict__ src,
+                           const int32_t *__restrict__ dst, const int32_t *__restrict__ neg,
+                           const double *__restrict__ t, int32_t *bad)
+{
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t a = src[e], b = dst[e], c = neg[e];
+        if (a < 0 || a >= N || b < 0 || b >= N || c < 0 || c >= N)
+            atomicOr(&bad[0], 1);
+        if (e + 1 < E && !(t[e] <= t[e + 1]))
+            atomicOr(&bad[1], 1);
+    }
+}
+
+// Incidence 2e is (src[e], e); incidence 2e + 1 is (dst[e], e), or the
+// sentinel key N for a self-loop so that it sorts past every list.
+__global__ void k_incidences(int64_t E, int32_t N, const int32_t *__restrict__ src,
+                             const int32_t *__restrict__ dst, int32_t *__restrict__ key,
+                             int32_t *__restrict__ val)
+{
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < E;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t a = src[e], b = dst[e];
+        key[2 * e] = a;
+        key[2 * e + 1] = (a == b) ? N : b;
+        val[2 * e] = (int32_t)e;
+        val[2 * e + 1] = (int32_t)e;
+    }
+}
+
+// off[v] = first position whose (sorted) key is >= v, for v in [0, N].
+__global__ void k_offsets(int64_t n, int32_t N, const int32_t *__restrict__ key,
+                          int64_t *__restrict__ off)
+{
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k <= n;
+         k += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t prev = (k == 0) ? -1 : key[k - 1];
+        const int32_t cur = (k == n) ? N + 1 : key[k];
+        for (int32_t v = prev + 1; v <= cur && v <= N; ++v)
+            off[v] = k;
+    }
+}
+
+__global__ void k_adj_records(int64_t n, const int32_t *__restrict__ key,
+                              const int32_t *__restrict__ val, const int32_t *__restrict__ src,
+                              const int32_t *__restrict__ dst, const double *__restrict__ t,
+                              AdjRec *__restrict__ adj)
+{
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n;
+         k += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t v = key[k], e = val[k];
+        AdjRec r;
+        r.ts = t[e];
+        r.eid = e;
+        r.nbr = (src[e] == v) ? dst[e] : src[e];
+        adj[k] = r;
+    }
+}
+
+int grid_for(int64_t n, int block)
+{
+    int64_t g = cdiv(n, block);
+    if (g > 65536)
+        g = 65536;
+    return (int)(g < 1 ? 1 : g);
+}
+
+// ------------------------------------------------------------ batch roots
+__global__ void k_batch_roots(int64_t first, int32_t b, const int32_t *__restrict__ src,
+                              const int32_t *__restrict__ dst, const int32_t *__restrict__ neg,
+                              const double *__restrict__ t, int32_t *__restrict__ root,
+                              double *__restrict__ root_ts)
+{
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= b)
+        return;
+    const int64_t e = first + k;
+    const double te = t[e];
+    root[k] = src[e];
+    root[b + k] = dst[e];
+    root[2 * b + k] = neg[e];
+    root_ts[k] = te;
+    root_ts[b + k] = te;
+    root_ts[2 * b + k] = te;
+}
+
+// ------------------------------------------------------------ sampler
+// One wavefront per root.  The root's adjacency list is sorted by (t, e);
+// the wavefront finds p = the first entry with ts >= tq by a 64-ary search
+// (each round, lane l probes the last entry of the l-th of 64 equal segments,
+// and the ballot's popcount names the segment holding p), then lanes
+// j < nb read entries p-1-j: the nb most recent strictly earlier events,
+// newest first.
+__global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
+                                                const AdjRec *__restrict__ adj,
+                                                const int32_t *__restrict__ root,
+                                                const double *__restrict__ root_ts, int32_t R,
+                                                int32_t N, int32_t nb, int32_t *__restrict__ nbr,
+                                                int32_t *__restrict__ eid,
+                                                double *__restrict__ nts,
+                                                int32_t *__restrict__ cnt)
+{
+    const int r = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    if (r >= R)
+        return;
+    const int32_t v = root[r];
+    const double tq = root_ts[r];
+    const bool ok = v >= 0 && v < N;   // an id out of range samples nothing
+    const int64_t base = ok ? off[v] : 0;
+    int64_t lo = base, hi = ok ? off[v + 1] : 0;
+    while (hi - lo > kWave) {
+        const int64_t step = (hi - lo + kWave - 1) / kWave;
+        const int64_t probe = lo + (int64_t)(lane + 1) * step - 1;
+        const bool below = probe < hi && adj[probe].ts < tq;
+        const int c = __popcll(__ballot(below));
+        const int64_t nlo = lo + (int64_t)c * step;
+        const int64_t nhi = nlo + step < hi ? nlo + step : hi;
+        lo = nlo;
+        hi = nhi;
+    }
+    const int64_t idx = lo + lane;
+    const bool below = idx < hi && adj[idx].ts < tq;
+    const int64_t p = lo + __popcll(__ballot(below));
+    const int64_t avail = p - base;
+    const int c = avail < nb ? (int)avail : nb;
+    if (lane < nb) {
+        const int64_t o = (int64_t)r * nb + lane;
+        if (lane < c) {
+            const AdjRec a = adj[p - 1 - lane];
+            nbr[o] = a.nbr;
+            eid[o] = a.eid;
+            nts[o] = a.ts;
+        } else {
+            nbr[o] = -1;
+            eid[o] = -1;
+            nts[o] = 0.0;
+        }
+    }
+    if (lane == 0)
+        cnt[r] = c;
+}
+
+// ------------------------------------------------------------ node set
+// One workgroup: marks roots and neighbours in an LDS bitmap over node ids,
+// scans the word popcounts to number the set bits in id order (which sorts
+// and deduplicates in one pass), then maps every root and neighbour to its
+// position.
+constexpr int kNsThreads = 1024;
+constexpr int kNsMaxWords = 1 << 14;   // 2^19 node ids
+
+__global__ __launch_bounds__(kNsThreads) void k_node_set(
+    int32_t N, const int32_t *__restrict__ root, int32_t R, const int32_t *__restrict__ nbr,
+    int32_t Rnb, int32_t *__restrict__ nodes, int32_t *__restrict__ n_nodes,
+    int32_t *__restrict__ root_pos, int32_t *__restrict__ nbr_pos)
+{
+    extern __shared__ uint32_t ns_lds[];
+    const int W = (N + 31) >> 5;
+    uint32_t *bits = ns_lds;          // [W]
+    uint32_t *pre = ns_lds + W;       // [W] exclusive prefix of popcounts
+    __shared__ uint32_t part[kNsThreads];
+    const int tid = threadIdx.x;
+
+    for (int k = tid; k < W; k += kNsThreads)
+        bits[k] = 0u;
+    __syncthreads();
+    // ids outside [0, N) are not members; they map to position -1
+    for (int k = tid; k < R; k += kNsThreads) {
+        const int32_t v = root[k];
+        if (v >= 0 && v < N)
+            atomicOr(&bits[v >> 5], 1u << (v & 31));
+    }
+    for (int k = tid; k < Rnb; k += kNsThreads) {
+        const int32_t v = nbr[k];
+        if (v >= 0 && v < N)
+            atomicOr(&bits[v >> 5], 1u << (v & 31));
+    }
+    __syncthreads();
+
+    // contiguous word ranges per thread, then a block scan of the range sums
+    const int per = (W + kNsThreads - 1) / kNsThreads;
+    const int w0 = tid * per, w1 = min(W, w0 + per);
+    uint32_t sum = 0;
+    for (int k = w0; k < w1; ++k)
+        sum += __popc(bits[k]);
+    part[tid] = sum;
+    __syncthreads();
+    for (int o = 1; o < kNsThreads; o <<= 1) {
+        const uint32_t x = tid >= o ? part[tid - o] : 0u;
+        __syncthreads();
+        part[tid] += x;
+        __syncthreads();
+    }
+    uint32_t run = part[tid] - sum;   // exclusive
+    for (int k = w0; k < w1; ++k) {
+        pre[k] = run;
+        uint32_t m = bits[k];
+        uint32_t p = run;
+        while (m) {
+            const int b = __ffs(m) - 1;
+            nodes[p++] = (k << 5) + b;
+            m &= m - 1;
+        }
+        run = p;
+    }
+    if (tid == kNsThreads - 1)
+        *n_nodes = (int32_t)part[kNsThreads - 1];
+    __syncthreads();
+
+    for (int k = tid; k < R; k += kNsThreads) {
+        const int32_t v = root[k];
+        root_pos[k] = (v < 0 || v >= N)
+                          ? -1
+                          : (int32_t)(pre[v >> 5] +
+                                      __popc(bits[v >> 5] & ((1u << (v & 31)) - 1u)));
+    }
+    for (int k = tid; k < Rnb; k += kNsThreads) {
+        const int32_t v = nbr[k];
+        nbr_pos[k] = (v < 0 || v >= N)
+                         ? -1
+                         : (int32_t)(pre[v >> 5] +
+                                     __popc(bits[v >> 5] & ((1u << (v & 31)) - 1u)));
+    }
+}
+
+}  // namespace
+
+// ======================================================================== API
+
+extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *src,
+                                         const int32_t *dst, const double *t,
+                                         const int32_t *neg, const float *efeat, int32_t D_e,
+                                         void *stream, tgm_graph_t *out)
+{
+    if (!out || N <= 0 || E < 0 || D_e < 0 || 2 * E >= (int64_t)INT_MAX)
+        return TGM_EINVAL;
+    if (E > 0 && (!src || !dst || !t || !neg))
+        return TGM_EINVAL;
+    if ((D_e > 0) != (efeat != nullptr) && E > 0)
+        return TGM_EINVAL;
+    *out = nullptr;
+    hipStream_t s = as_stream(stream);
+    tgm_graph *g = new tgm_graph();
+    g->N = N;
+    g->E = E;
+    g->D_e = D_e;
+    g->src = src;
+    g->dst = dst;
+    g->t = t;
+    g->neg = neg;
+    g->efeat = efeat;
+
+    const int64_t n2 = 2 * E;
+    int32_t *bad = nullptr, *key = nullptr, *val = nullptr, *key2 = nullptr, *val2 = nullptr;
+    void *tmp = nullptr;
+    size_t tmp_bytes = 0;
+    tgm_status_t st = TGM_OK;
+    auto fail = [&](tgm_status_t code) {
+        st = code;
+    };
+    do {
+        if (hipMalloc(&g->off, sizeof(int64_t) * (N + 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (hipMalloc(&bad, sizeof(int32_t) * 2) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (hipMemsetAsync(bad, 0, sizeof(int32_t) * 2, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+        if (E == 0) {
+            if (hipMemsetAsync(g->off, 0, sizeof(int64_t) * (N + 1), s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+            if (hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+            break;
+        }
+        hipLaunchKernelGGL(k_validate, dim3(grid_for(E, 256)), dim3(256), 0, s, E, N, src, dst,
+                           neg, t, bad);
+        int32_t hbad[2] = {0, 0};
+        if (hipMemcpyAsync(hbad, bad, sizeof(hbad), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+        if (hbad[0] || hbad[1]) { fail(TGM_ERANGE); break; }
+
+        if (hipMalloc(&key, sizeof(int32_t) * n2) != hipSuccess ||
+            hipMalloc(&val, sizeof(int32_t) * n2) != hipSuccess ||
+            hipMalloc(&key2, sizeof(int32_t) * n2) != hipSuccess ||
+            hipMalloc(&val2, sizeof(int32_t) * n2) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        hipLaunchKernelGGL(k_incidences, dim3(grid_for(E, 256)), dim3(256), 0, s, E, N, src, dst,
+                           key, val);
+        int bits = 1;
+        while ((1ll << bits) <= (int64_t)N)
+            ++bits;
+        // LSD radix sort is stable: within a node, incidences keep event order
+        if (hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_bytes, key, key2, val, val2, (int)n2,
+                                               0, bits, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+        if (hipMalloc(&tmp, tmp_bytes) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (hipcub::DeviceRadixSort::SortPairs(tmp, tmp_bytes, key, key2, val, val2, (int)n2, 0,
+                                               bits, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+        hipLaunchKernelGGL(k_offsets, dim3(grid_for(n2 + 1, 256)), dim3(256), 0, s, n2, N, key2,
+                           g->off);
+        int64_t n_adj = 0;
+        if (hipMemcpyAsync(&n_adj, g->off + N, sizeof(int64_t), hipMemcpyDeviceToHost, s) !=
+                hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+        g->n_adj = n_adj;
+        if (hipMalloc(&g->adj, sizeof(AdjRec) * (n_adj > 0 ? n_adj : 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (n_adj > 0)
+            hipLaunchKernelGGL(k_adj_records, dim3(grid_for(n_adj, 256)), dim3(256), 0, s, n_adj,
+                               key2, val2, src, dst, t, g->adj);
+        if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
+    } while (0);
+    hipFree(bad);
+    hipFree(key);
+    hipFree(val);
+    hipFree(key2);
+    hipFree(val2);
+    hipFree(tmp);
+    if (st != TGM_OK) {
+        tgm_graph_destroy(g);
+        return st;
+    }
+    *out = g;
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_graph_destroy(tgm_graph_t g)
+{
+    if (!g)
+        return TGM_EINVAL;
+    hipFree(g->off);
+    hipFree(g->adj);
+    delete g;
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_graph_info(tgm_graph_t g, int32_t *N, int64_t *E, int32_t *D_e,
+                                       int64_t *n_adj)
+{
+    if (!g)
+        return TGM_EINVAL;
+    if (N) *N = g->N;
+    if (E) *E = g->E;
+    if (D_e) *D_e = g->D_e;
+    if (n_adj) *n_adj = g->n_adj;
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_batch_roots(tgm_graph_t g, int64_t first_event, int32_t b,
+                                        int32_t *root, double *root_ts, void *stream)
+{
+    if (!g || b < 0 || first_event < 0 || first_event + b > g->E)
+        return TGM_EINVAL;
+    if (b == 0)
+        return TGM_OK;
+    if (!root || !root_ts)
+        return TGM_EINVAL;
+    TGM_LAUNCH(k_batch_roots, dim3(cdiv(b, 256)), dim3(256), 0, as_stream(stream),
+                       first_event, b, g->src, g->dst, g->neg, g->t, root, root_ts);
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_sample(tgm_graph_t g, const int32_t *root, const double *root_ts,
+                                   int32_t R, int32_t nb, int32_t *nbr, int32_t *eid,
+                                   double *nts, int32_t *cnt, void *stream)
+{
+    if (!g || R < 0 || nb < 1 || nb > kWave)
+        return TGM_EINVAL;
+    if (R == 0)
+        return TGM_OK;
+    if (!root || !root_ts || !nbr || !eid || !nts || !cnt)
+        return TGM_EINVAL;
+    const int per_block = 256 / kWave;
+    TGM_LAUNCH(k_sample, dim3(cdiv(R, per_block)), dim3(256), 0, as_stream(stream),
+                       g->off, g->adj, root, root_ts, R, g->N, nb, nbr, eid, nts, cnt);
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t R,
+                                     const int32_t *nbr, int32_t nb, int32_t *nodes,
+                                     int32_t *n_nodes, int32_t cap, int32_t *root_pos,
+                                     int32_t *nbr_pos, void *stream)
+{
+    if (!g || R < 0 || nb < 0 || !n_nodes)
+        return TGM_EINVAL;
+    const int64_t need = std::min<int64_t>(g->N, (int64_t)R * (nb + 1));
+    if (cap < need)
+        return TGM_ESIZE;
+    if ((R > 0 && (!root || !nodes || !root_pos)) || ((int64_t)R * nb > 0 && (!nbr || !nbr_pos)))
+        return TGM_EINVAL;
+    const int W = (g->N + 31) >> 5;
+    if (W > kNsMaxWords)
+        return TGM_EINVAL;
+    const size_t lds = sizeof(uint32_t) * 2 * W;
+    static bool lds_opt_in = false;
+    if (!lds_opt_in) {
+        TGM_HIP(hipFuncSetAttribute((const void *)k_node_set,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize,
+                                    (int)(sizeof(uint32_t) * 2 * kNsMaxWords)));
+        lds_opt_in = true;
+    }
+    TGM_LAUNCH(k_node_set, dim3(1), dim3(kNsThreads), lds, as_stream(stream), g->N, root,
+                       R, nbr, R * nb, nodes, n_nodes, root_pos, nbr_pos);
+    return TGM_OK;
+}

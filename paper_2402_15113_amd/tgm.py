@@ -1,0 +1,263 @@
+"""ctypes binding of libtgm (include/tgm.h), function for function.
+
+Argument marshalling only: device arrays are torch tensors on the GPU (passed
+by data pointer), streams are torch streams.  Every computation happens in
+the library's HIP kernels.  A missing library is an error, never a fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libtgm.so")
+
+TGM_OK, TGM_EINVAL, TGM_ERANGE, TGM_EORDER, TGM_ESIZE, TGM_EDEVICE, TGM_ENOMEM = \
+    0, -1, -2, -3, -4, -5, -6
+
+# Every exported symbol of include/tgm.h
+SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_create",
+           "tgm_graph_destroy", "tgm_graph_info", "tgm_batch_roots", "tgm_sample",
+           "tgm_node_set", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
+           "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
+           "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
+           "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
+
+
+class TgmError(RuntimeError):
+    def __init__(self, fn, code):
+        self.code = code
+        super().__init__(f"{fn}: {status_str(code)} ({code})")
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [("M", C.c_int32), ("D_e", C.c_int32), ("D_t", C.c_int32), ("H", C.c_int32),
+                ("nb", C.c_int32), ("max_nodes", C.c_int32), ("max_roots", C.c_int32)]
+
+
+_fp = C.POINTER(C.c_float)
+_dp = C.POINTER(C.c_double)
+
+
+class Weights(C.Structure):
+    _fields_ = [("W_ih", _fp), ("W_hh", _fp), ("b_ih", _fp), ("b_hh", _fp),
+                ("omega", _dp), ("beta", _dp),
+                ("W_q", _fp), ("b_q", _fp), ("W_k", _fp), ("b_k", _fp), ("W_v", _fp),
+                ("b_v", _fp), ("W_o", _fp), ("b_o", _fp)]
+
+
+_lib = None
+V, I32, I64, P = C.c_void_p, C.c_int32, C.c_int64, C.c_void_p
+
+
+def lib():
+    """Load libtgm.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -c 'import __graft_entry__ as g; g.build()'`")
+        L = C.CDLL(LIB_PATH)
+        L.tgm_status_str.argtypes = [I32]
+        L.tgm_status_str.restype = C.c_char_p
+        L.tgm_last_device_error.restype = I32
+        L.tgm_version.restype = I32
+        sig = {
+            "tgm_graph_create": [I32, I64, P, P, P, P, P, I32, V, C.POINTER(V)],
+            "tgm_graph_destroy": [V],
+            "tgm_graph_info": [V, P, P, P, P],
+            "tgm_batch_roots": [V, I64, I32, P, P, V],
+            "tgm_sample": [V, P, P, I32, I32, P, P, P, P, V],
+            "tgm_node_set": [V, P, I32, P, I32, P, P, I32, P, P, V],
+            "tgm_state_create": [I32, I32, I32, I32, I32, V, C.POINTER(V)],
+            "tgm_state_destroy": [V],
+            "tgm_state_reset": [V, V],
+            "tgm_state_flush": [V, V],
+            "tgm_state_read": [V, P, P, P, P, P, V],
+            "tgm_state_load": [V, I64, P, P, P, P, P, V],
+            "tgm_fetch_memory": [V, I64, P, P, I32, P, P, P, P, P, V],
+            "tgm_model_create": [C.POINTER(ModelDesc), C.POINTER(Weights), V, C.POINTER(V)],
+            "tgm_model_destroy": [V],
+            "tgm_update_memory": [V, V, V, I64, P, P, I32, P, P, P, P, P, I64, I32, P, P, P, P, P,
+                                  V],
+            "tgm_embed": [V, V, I32, I32, P, P, P, P, P, P, P, P, I32, P, V],
+        }
+        sig["tgm_profile_enable"] = [I32]
+        sig["tgm_profile_reset"] = []
+        sig["tgm_profile_count"] = []
+        sig["tgm_profile_get"] = [I32, C.POINTER(C.c_char_p), C.POINTER(I64),
+                                  C.POINTER(C.c_double)]
+        for name, args in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = I32
+        _lib = L
+    return _lib
+
+
+def status_str(code: int) -> str:
+    return lib().tgm_status_str(int(code)).decode()
+
+
+def _check(fn, rc):
+    if rc != TGM_OK:
+        raise TgmError(fn, rc)
+
+
+def _p(t):
+    """Device pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    return C.c_void_p(t.data_ptr())
+
+
+def _s(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+def last_device_error() -> int:
+    return lib().tgm_last_device_error()
+
+
+def version() -> int:
+    return lib().tgm_version()
+
+
+def tgm_profile_enable(on: bool):
+    _check("tgm_profile_enable", lib().tgm_profile_enable(1 if on else 0))
+
+
+def tgm_profile_reset():
+    _check("tgm_profile_reset", lib().tgm_profile_reset())
+
+
+def tgm_profile_read() -> dict:
+    """{kernel name: (launches, total ms)}; synchronises the recorded events."""
+    L = lib()
+    out = {}
+    for k in range(L.tgm_profile_count()):
+        name, n, ms = C.c_char_p(), C.c_int64(), C.c_double()
+        _check("tgm_profile_get", L.tgm_profile_get(k, C.byref(name), C.byref(n), C.byref(ms)))
+        out[name.value.decode()] = (n.value, ms.value)
+    return out
+
+
+# ------------------------------------------------------------------ graph
+def tgm_graph_create(N, src, dst, t, neg, efeat, stream=None):
+    E = int(src.numel())
+    D_e = 0 if efeat is None else int(efeat.shape[1])
+    h = V()
+    _check("tgm_graph_create", lib().tgm_graph_create(N, E, _p(src), _p(dst), _p(t), _p(neg),
+                                                      _p(efeat), D_e, _s(stream), C.byref(h)))
+    return h
+
+
+def tgm_graph_destroy(g):
+    _check("tgm_graph_destroy", lib().tgm_graph_destroy(g))
+
+
+def tgm_graph_info(g):
+    N, E, D_e, n_adj = C.c_int32(), C.c_int64(), C.c_int32(), C.c_int64()
+    _check("tgm_graph_info", lib().tgm_graph_info(g, C.byref(N), C.byref(E), C.byref(D_e),
+                                                  C.byref(n_adj)))
+    return N.value, E.value, D_e.value, n_adj.value
+
+
+def tgm_batch_roots(g, first_event, b, root, root_ts, stream=None):
+    _check("tgm_batch_roots", lib().tgm_batch_roots(g, first_event, b, _p(root), _p(root_ts),
+                                                    _s(stream)))
+
+
+def tgm_sample(g, root, root_ts, R, nb, nbr, eid, nts, cnt, stream=None):
+    _check("tgm_sample", lib().tgm_sample(g, _p(root), _p(root_ts), R, nb, _p(nbr), _p(eid),
+                                          _p(nts), _p(cnt), _s(stream)))
+
+
+def tgm_node_set(g, root, R, nbr, nb, nodes, n_nodes, cap, root_pos, nbr_pos, stream=None):
+    _check("tgm_node_set", lib().tgm_node_set(g, _p(root), R, _p(nbr), nb, _p(nodes),
+                                              _p(n_nodes), cap, _p(root_pos), _p(nbr_pos),
+                                              _s(stream)))
+
+
+# ------------------------------------------------------------------ state
+def tgm_state_create(N, M, D_m, s, max_batch, stream=None):
+    h = V()
+    _check("tgm_state_create", lib().tgm_state_create(N, M, D_m, s, max_batch, _s(stream),
+                                                      C.byref(h)))
+    return h
+
+
+def tgm_state_destroy(st):
+    _check("tgm_state_destroy", lib().tgm_state_destroy(st))
+
+
+def tgm_state_reset(st, stream=None):
+    _check("tgm_state_reset", lib().tgm_state_reset(st, _s(stream)))
+
+
+def tgm_state_flush(st, stream=None):
+    _check("tgm_state_flush", lib().tgm_state_flush(st, _s(stream)))
+
+
+def tgm_state_read(st, mem, mem_ts, mail, mail_ts, ver, stream=None):
+    _check("tgm_state_read", lib().tgm_state_read(st, _p(mem), _p(mem_ts), _p(mail),
+                                                  _p(mail_ts), _p(ver), _s(stream)))
+
+
+def tgm_state_load(st, it, mem, mem_ts, mail, mail_ts, ver, stream=None):
+    _check("tgm_state_load", lib().tgm_state_load(st, it, _p(mem), _p(mem_ts), _p(mail),
+                                                  _p(mail_ts), _p(ver), _s(stream)))
+
+
+def tgm_fetch_memory(st, it, nodes, n_nodes, cap, mem, mem_ts, mail, mail_ts, ver, stream=None):
+    _check("tgm_fetch_memory", lib().tgm_fetch_memory(st, it, _p(nodes), _p(n_nodes), cap,
+                                                      _p(mem), _p(mem_ts), _p(mail), _p(mail_ts),
+                                                      _p(ver), _s(stream)))
+
+
+# ------------------------------------------------------------------ model
+def tgm_model_create(M, D_e, D_t, H, nb, max_nodes, max_roots, w, stream=None):
+    """``w`` holds numpy weights (fp32; omega and beta fp64), see workloads.Weights."""
+    d = ModelDesc(M, D_e, D_t, H, nb, max_nodes, max_roots)
+    keep = {}
+
+    def arr(name, dt):
+        a = np.ascontiguousarray(getattr(w, name), dtype=dt)
+        keep[name] = a
+        return a.ctypes.data_as(_fp if dt == np.float32 else _dp)
+
+    ws = Weights()
+    for name in ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v",
+                 "W_o", "b_o"):
+        setattr(ws, name, arr(name, np.float32))
+    ws.omega = arr("omega", np.float64)
+    ws.beta = arr("beta", np.float64)
+    h = V()
+    _check("tgm_model_create", lib().tgm_model_create(C.byref(d), C.byref(ws), _s(stream),
+                                                      C.byref(h)))
+    return h
+
+
+def tgm_model_destroy(m):
+    _check("tgm_model_destroy", lib().tgm_model_destroy(m))
+
+
+def tgm_update_memory(st, m, g, it, nodes, n_nodes, cap, mem, mem_ts, mail, mail_ts, ver,
+                      first_event, b, src_pos, dst_pos, mem_new, new_mem_ts=None, winner=None,
+                      stream=None):
+    _check("tgm_update_memory", lib().tgm_update_memory(
+        st, m, g, it, _p(nodes), _p(n_nodes), cap, _p(mem), _p(mem_ts), _p(mail), _p(mail_ts),
+        _p(ver), first_event, b, _p(src_pos), _p(dst_pos), _p(mem_new), _p(new_mem_ts),
+        _p(winner), _s(stream)))
+
+
+def tgm_embed(m, g, R, nb, root_pos, root_ts, nbr_pos, eid, nts, cnt, mem_new, n_nodes, cap, h,
+              stream=None):
+    _check("tgm_embed", lib().tgm_embed(m, g, R, nb, _p(root_pos), _p(root_ts), _p(nbr_pos),
+                                        _p(eid), _p(nts), _p(cnt), _p(mem_new), _p(n_nodes), cap,
+                                        _p(h), _s(stream)))

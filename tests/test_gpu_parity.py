@@ -1,0 +1,285 @@
+"""GPU path (libtgm through its C ABI) against the fp64 oracle.
+
+Bit-exact: roots, sampled neighbours / event ids / times / counts, the node
+set and every position map, fetched versions and timestamps, new memory
+timestamps, latest-message winners, committed versions and timestamps.
+Floating point (fetched memory and mail, updated memory s', embeddings h,
+committed tables): |gpu - oracle| <= 1e-5 + 1e-4 |oracle| element-wise
+(fp32 vs fp64).
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from workloads import custom_workload, make_weights, make_workload  # noqa: E402
+
+ATOL, RTOL = 1e-5, 1e-4
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2402_15113_amd import tgm
+    tgm.lib()   # fails loudly when the library is missing
+
+
+def close(name, g, o):
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    assert g.shape == o.shape, (name, g.shape, o.shape)
+    err = np.abs(g - o)
+    bad = err > ATOL + RTOL * np.abs(o)
+    if bad.any():
+        k = np.unravel_index(np.argmax(err - (ATOL + RTOL * np.abs(o))), err.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())}/{bad.size} outside tolerance; worst at "
+                             f"{k}: gpu {g[k]!r} oracle {o[k]!r}")
+    return float(err.max()) if err.size else 0.0
+
+
+def exact(name, g, o):
+    g, o = np.asarray(g), np.asarray(o)
+    assert g.shape == o.shape, (name, g.shape, o.shape)
+    if not np.array_equal(g, o):
+        k = np.argwhere(g != o)[0]
+        raise AssertionError(f"{name}: {int((g != o).sum())} mismatches; first at {tuple(k)}: "
+                             f"gpu {g[tuple(k)]!r} oracle {o[tuple(k)]!r}")
+
+
+def compare_step(go, r):
+    """go: Stage.outputs(); r: oracle StepResult of the same iteration."""
+    assert go["iter"] == r.iter and go["b"] == r.b
+    exact("root", go["root"], r.root)
+    exact("root_ts", go["root_ts"], r.root_ts)
+    exact("cnt", go["cnt"], r.cnt)
+    exact("nbr", go["nbr"], r.nbr)
+    exact("eid", go["eid"], r.eid)
+    exact("nts", go["nts"], r.nts)
+    assert go["n_U"] == r.n_U
+    exact("U", go["U"], r.U)
+    exact("root_pos", go["root_pos"], r.root_pos)
+    exact("nbr_pos", go["nbr_pos"], r.nbr_pos)
+    exact("f_ver", go["f_ver"], r.f_ver)
+    exact("f_mem_ts", go["f_mem_ts"], r.f_mem_ts)
+    exact("f_mail_ts", go["f_mail_ts"], r.f_mail_ts)
+    exact("new_mem_ts", go["new_mem_ts"], r.new_mem_ts)
+    exact("winner", go["winner"], r.winner)
+    e = {}
+    e["f_mem"] = close("f_mem", go["f_mem"], r.f_mem)
+    e["f_mail"] = close("f_mail", go["f_mail"], r.f_mail)
+    e["s_new"] = close("s_new", go["s_new"], r.s_new)
+    e["h"] = close("h", go["h"], r.h)
+    return e
+
+
+def compare_state(gs, os_):
+    exact("ver", gs["ver"], os_["ver"])
+    exact("mem_ts", gs["mem_ts"], os_["mem_ts"])
+    exact("mail_ts", gs["mail_ts"], os_["mail_ts"])
+    close("mem", gs["mem"], os_["mem"])
+    close("mail", gs["mail"], os_["mail"])
+
+
+def run_pair(orc, wl, w, n_iters=None, s=None, first=0, init=None, check_every=1):
+    from paper_2402_15113_amd.stage import from_workload
+    st = from_workload(wl, w, s=s)
+    o = orc.Oracle(wl, w, s=s)
+    if init is not None:
+        st.load_state(first, **init)
+        o.set_state(first, **init)
+    n = (wl.n_iters - first) if n_iters is None else n_iters
+    worst = {}
+    for k in range(n):
+        i = first + k
+        print(f"[parity] {wl.name} s={st.s} iter {i}", flush=True)
+        st.step(i)
+        want = (k % check_every == 0) or k == n - 1
+        r = o.step(want="all" if want else "light")
+        if want:
+            for key, v in compare_step(st.outputs(), r).items():
+                worst[key] = max(worst.get(key, 0.0), v)
+    st.flush()
+    o.flush()
+    compare_state(st.state(), o.state())
+    st.close()
+    return worst
+
+
+@pytest.mark.parametrize("s", [0, 2])
+def test_tiny_full_run(orc, s):
+    wl = make_workload("tiny", s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random")
+    worst = run_pair(orc, wl, w)
+    print("worst abs errors", worst)
+
+
+def test_tiny_ragged_tail(orc):
+    wl = make_workload("tiny", E=19_937, s=1)   # last batch holds 137 events
+    assert wl.E % wl.B != 0
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    run_pair(orc, wl, w)
+
+
+def tie_heavy(seed, N=13, E=300, span=40, D_e=3, B=7, M=8, D_t=5, H=2, nb=3, s=1):
+    r = np.random.default_rng(seed)
+    src = r.integers(0, N, E)
+    dst = r.integers(0, N, E)
+    dst[::9] = src[::9]   # self-loops
+    t = np.sort(r.integers(0, span, E)).astype(np.float64)
+    neg = r.integers(0, N, E)
+    f = r.standard_normal((E, D_e)).astype(np.float32) if D_e else None
+    return custom_workload(f"ties{seed}", N, src, dst, t, neg, f, M=M, D_t=D_t, H=H, nb=nb, B=B,
+                           s=s, seed=seed)
+
+
+@pytest.mark.parametrize("seed,kw", [(0, {}), (1, dict(nb=1, s=0)), (2, dict(D_e=0, s=3)),
+                                     (3, dict(nb=64, B=5, M=20, H=4, D_t=1)),
+                                     (4, dict(M=36, H=3, D_e=17, D_t=23, B=11, nb=10))])
+def test_tie_heavy_edge_cases(orc, seed, kw):
+    """Integer timestamps with many ties, self-loops, roots without history,
+    dims that are not multiples of the 16-wide MFMA tiles, nb = 1 and 64."""
+    wl = tie_heavy(seed, **kw)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, seed=seed, beta="random")
+    run_pair(orc, wl, w)
+
+
+def test_wiki_full_run(orc):
+    """The bench workload (WIKI-shaped, B = 600, s = 1), every batch."""
+    wl = make_workload("wiki")
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    worst = run_pair(orc, wl, w, check_every=8)
+    print("worst abs errors", worst)
+
+
+def test_lastfm_no_edge_features_window(orc):
+    """LastFM-shaped: D_e = 0, heavy repetition (latest-message reduce and
+    write-set conflicts), B = 2000, s = 2: first 24 batches."""
+    wl = make_workload("lastfm")
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    run_pair(orc, wl, w, n_iters=24)
+
+
+@pytest.mark.parametrize("s", [1, 2, 4])
+def test_reddit_window(orc, s):
+    wl = make_workload("reddit", s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    run_pair(orc, wl, w, n_iters=16)
+
+
+def test_mid_run_window_from_synthetic_state(orc):
+    """A window in the middle of the REDDIT-shaped stream (batches 560..575),
+    both sides started from the same seeded synthetic state."""
+    wl = make_workload("reddit", s=2)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    j = 560
+    r = np.random.default_rng(7)
+    N, M, D_m = wl.N, wl.M, wl.D_m
+    lo, _ = wl.batch(j)
+    mem_ts = np.floor(r.uniform(0, wl.t[lo - 1], N))
+    init = dict(mem=r.uniform(-1, 1, (N, M)).astype(np.float32).astype(np.float64),
+                mem_ts=mem_ts,
+                mail=r.standard_normal((N, D_m)).astype(np.float32).astype(np.float64),
+                mail_ts=np.minimum(mem_ts + np.floor(r.exponential(3600, N)), wl.t[lo - 1]),
+                ver=np.where(r.random(N) < 0.9, r.integers(0, j - 2, N), -1).astype(np.int32))
+    run_pair(orc, wl, w, n_iters=16, first=j, init=init)
+
+
+def test_sampler_full_size_sampled_roots(orc):
+    """REDDIT-shaped full graph (672k events, max degree ~184k): the sampler
+    at a random sample of (node, time) roots against the oracle's sampler."""
+    from paper_2402_15113_amd import tgm
+    wl = make_workload("reddit", with_features=False)
+    dev = torch.device("cuda:0")
+    T = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+    src, dst, t, neg = (T(wl.src, torch.int32), T(wl.dst, torch.int32), T(wl.t, torch.float64),
+                        T(wl.neg, torch.int32))
+    g = tgm.tgm_graph_create(wl.N, src, dst, t, neg, None)
+    r = np.random.default_rng(3)
+    R, nb = 4096, 10
+    # half hot nodes (high degree), half uniform; times on and between event times
+    deg = np.bincount(np.concatenate([wl.src, wl.dst]), minlength=wl.N)
+    hot = np.argsort(deg)[-50:]
+    root = np.where(r.random(R) < 0.5, r.choice(hot, R), r.integers(0, wl.N, R)).astype(np.int32)
+    rts = np.where(r.random(R) < 0.5, wl.t[r.integers(0, wl.E, R)],
+                   r.uniform(-5, wl.t[-1] + 5, R))
+    nbr, eid, nts, cnt = (torch.empty((R, nb), dtype=torch.int32, device=dev),
+                          torch.empty((R, nb), dtype=torch.int32, device=dev),
+                          torch.empty((R, nb), dtype=torch.float64, device=dev),
+                          torch.empty(R, dtype=torch.int32, device=dev))
+    tgm.tgm_sample(g, T(root, torch.int32), T(rts, torch.float64), R, nb, nbr, eid, nts, cnt)
+    torch.cuda.synchronize()
+    onbr, oeid, onts, ocnt = orc.sample(wl.N, wl.src, wl.dst, wl.t, root, rts, nb)
+    exact("cnt", cnt.cpu().numpy(), ocnt)
+    exact("nbr", nbr.cpu().numpy(), onbr)
+    exact("eid", eid.cpu().numpy(), oeid)
+    exact("nts", nts.cpu().numpy(), onts)
+    _, _, _, n_adj = tgm.tgm_graph_info(g)
+    assert n_adj == 2 * wl.E - int((wl.src == wl.dst).sum())
+    tgm.tgm_graph_destroy(g)
+
+
+def test_deterministic_rerun():
+    """Two runs of the same stream are bit-identical (no fp atomics)."""
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=6000, s=2)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    outs = []
+    for _ in range(2):
+        st = from_workload(wl, w)
+        for i in range(wl.n_iters):
+            st.step(i)
+        o = st.outputs()
+        st.flush()
+        outs.append((o, st.state()))
+        st.close()
+    (a, sa), (b, sb) = outs
+    for k in ("h", "s_new", "f_mail"):
+        assert np.array_equal(a[k], b[k]), k
+    for k in sa:
+        assert np.array_equal(sa[k], sb[k]), k
+
+
+def test_protocol_errors():
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=2000, s=1)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w)
+    st.step(0)
+    st.step(1)
+    with pytest.raises(tgm.TgmError) as ei:   # iteration 1 again: not the next update
+        st.step(1)
+    assert ei.value.code == tgm.TGM_EORDER
+    with pytest.raises(tgm.TgmError) as ei:   # fetch at 4 needs the update of 2
+        tgm.tgm_fetch_memory(st.st, 4, st.nodes, st.n_nodes, st.cap, st.f_mem, st.f_mem_ts,
+                             st.f_mail, st.f_mail_ts, st.f_ver)
+    assert ei.value.code == tgm.TGM_EORDER
+    with pytest.raises(tgm.TgmError) as ei:
+        tgm.tgm_sample(st.g, st.root, st.root_ts, 3, 0, st.nbr, st.eid, st.nts, st.cnt)
+    assert ei.value.code == tgm.TGM_EINVAL
+    with pytest.raises(tgm.TgmError) as ei:
+        tgm.tgm_node_set(st.g, st.root, 3 * wl.B, st.nbr, wl.nb, st.nodes, st.n_nodes, 5,
+                         st.root_pos, st.nbr_pos)
+    assert ei.value.code == tgm.TGM_ESIZE
+    torch.cuda.synchronize()
+    assert tgm.last_device_error() == tgm.TGM_OK
+    st.close()
+
+
+def test_graph_create_rejects_bad_content():
+    from paper_2402_15113_amd import tgm
+    dev = torch.device("cuda:0")
+    src = torch.tensor([0, 1, 2], dtype=torch.int32, device=dev)
+    dst = torch.tensor([1, 2, 5], dtype=torch.int32, device=dev)   # 5 >= N
+    t = torch.tensor([0.0, 1.0, 2.0], dtype=torch.float64, device=dev)
+    with pytest.raises(tgm.TgmError) as ei:
+        tgm.tgm_graph_create(4, src, dst, t, src, None)
+    assert ei.value.code == tgm.TGM_ERANGE
+    dst = torch.tensor([1, 2, 3], dtype=torch.int32, device=dev)
+    t = torch.tensor([0.0, 2.0, 1.0], dtype=torch.float64, device=dev)   # unsorted
+    with pytest.raises(tgm.TgmError) as ei:
+        tgm.tgm_graph_create(4, src, dst, t, src, None)
+    assert ei.value.code == tgm.TGM_ERANGE
