@@ -1,0 +1,250 @@
+#!/usr/bin/env python3
+"""Throughput of the per-batch memory-module stage on one MI355X.
+
+One step = one batch through the whole stage (roots, most-recent-k sampling,
+node set, versioned fetch, GRU memory update + latest-message reduce + staged
+write-back, time-encoded attention embedding), with every input resident in
+HBM before the timed region starts.  Workload: the WIKI-shaped synthetic
+stream (9,227 nodes, 157,474 events, edge features 172, memory 100, time
+encoding 100, 2 heads, batch 600, 10 neighbours, staleness 1).  When the
+requested steps run past the stream's last batch, the next epoch starts from
+the initial memory state (a reset inside the timed region).
+
+Passes:
+  1. warm-up, then K timed steps bracketed by device synchronisation -> value;
+  2. the same steps again with the library's per-kernel HIP-event timing on
+     -> average launch duration per kernel (the roofline's denominator);
+  3. an untimed replay that reads back each step's sizes (valid slots, node
+     set, nodes with mail) -> algorithmic flops and bytes per launch;
+  4. the fp64 oracle on the host cores for a bounded sample of the same
+     batches -> cpu_baseline.
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "temporal events/sec per batch stage (sample+fetch+GRU+embed); HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+FP32_MFMA_PEAK_TFS = 157.3     # MI355X dense fp32 matrix
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2402_15113_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def run_steps(stage, first_step, K, n_iters):
+    """Enqueue K steps starting at global step `first_step` (epochs wrap)."""
+    from paper_2402_15113_amd import tgm
+    for k in range(first_step, first_step + K):
+        i = k % n_iters
+        if i == 0 and k > 0:
+            tgm.tgm_state_reset(stage.st, stream=stage.stream)
+        stage.step(i)
+
+
+def account(stage, W, K, n_iters):
+    """Per-step sizes of the timed steps, read back from an untimed replay."""
+    import torch
+    from paper_2402_15113_amd import tgm
+    tgm.tgm_state_reset(stage.st, stream=stage.stream)
+    stage.want_winner = True
+    rows = []
+    for k in range(W + K):
+        i = k % n_iters
+        if i == 0 and k > 0:
+            tgm.tgm_state_reset(stage.st, stream=stage.stream)
+        stage.step(i)
+        if k >= W:
+            torch.cuda.synchronize()
+            b = stage.last[1]
+            R = 3 * b
+            n = int(stage.n_nodes.item())
+            rows.append(dict(b=b, R=R, slots=int(stage.cnt[:R].sum().item()), n_U=n,
+                             n_mail=int((stage.f_ver[:n] >= 0).sum().item()),
+                             n_win=int((stage.winner[:n] >= 0).sum().item())))
+    stage.want_winner = False
+    return rows
+
+
+def work_model(wl, rows):
+    """Algorithmic flops / bytes per launch of each kernel (averaged over the
+    timed steps).  Counts only useful work: valid slots, nodes with mail,
+    winning messages; no tile padding."""
+    M, D_e, D_t, D_m, nb = wl.M, wl.D_e, wl.D_t, wl.D_m, wl.nb
+    D_x = D_m + D_t
+    n = len(rows)
+    avg = lambda key: sum(r[key] for r in rows) / n
+    slots, R, n_U, n_mail, n_win, b = (avg("slots"), avg("R"), avg("n_U"), avg("n_mail"),
+                                       avg("n_win"), avg("b"))
+    f, d = 4, 8
+    return {
+        # per node with mail: the three gates over [x | h]
+        "k_gru": dict(flops=n_mail * 2 * 3 * M * (D_x + M),
+                      bytes=n_U * (M * f + d + d + 4) + n_mail * D_m * f + n_U * M * f),
+        # per valid slot: [efeat || phi] -> [K | V] and the two head dot products;
+        # per root: the output projection
+        "k_attn": dict(flops=slots * (2 * (D_e + D_t) * 2 * M + 4 * M) + R * 2 * (2 * M) * M,
+                       bytes=slots * (D_e * f + 4 + 4 + d) + R * (M * f + 4 + d + 4) + R * M * f),
+        "k_node_proj": dict(flops=n_U * 2 * M * 3 * M, bytes=n_U * (M * f + 3 * M * f)),
+        # roots in, offsets, the sampled records, outputs
+        "k_sample": dict(flops=0, bytes=R * (4 + d + 16) + slots * 16 + R * nb * (4 + 4 + d) + R * 4),
+        "k_node_set": dict(flops=0, bytes=R * 4 * 2 + R * nb * 4 * 2 + n_U * 4),
+        "k_gather_state": dict(flops=0, bytes=2 * n_U * ((M + D_m) * f + d + d + 4) + n_U * 4),
+        "k_commit": dict(flops=0, bytes=2 * n_win * ((M + D_m) * f + d + d) + 2 * b * 4),
+        "k_stage": dict(flops=0, bytes=n_win * (2 * M * f + D_e * f + (M + D_m) * f + 3 * d)
+                        + 2 * b * 12),
+        "k_latest": dict(flops=0, bytes=2 * b * 8),
+        "k_batch_roots": dict(flops=0, bytes=b * (3 * 4 + d) + 3 * b * (4 + d)),
+    }
+
+
+def cpu_baseline(wl, w, W, seconds):
+    import oracle
+    oracle.build(force=False)
+    o = oracle.Oracle(wl, w)
+    for _ in range(W):                       # state before the timed batches
+        if o.step(want="light") is None:
+            break
+    events, t0, nb_done, epochs = 0, time.perf_counter(), 0, 0
+    first = o.next_iter
+    while time.perf_counter() - t0 < seconds:
+        r = o.step(want="all")
+        if r is None:                        # next epoch from the initial state
+            o = oracle.Oracle(wl, w)
+            epochs += 1
+            continue
+        events += r.b
+        nb_done += 1
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": events / dt, "unit": "events/s", "cores": threads, "kind": "oracle",
+            "sample": f"fp64 oracle on the same stream: {nb_done} batches from batch {first} "
+                      f"({epochs} epoch restarts), {events} events in {dt:.1f} s, "
+                      f"OpenMP over nodes/roots"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="wiki", help="wiki (default), tiny, reddit, lastfm")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    from workloads import make_weights, make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    tgm.lib()
+    K, W = args.steps, args.warmup
+    wl = make_workload(args.workload)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    log(f"workload {wl.name}: N={wl.N} E={wl.E} B={wl.B} s={wl.s} iters/epoch={wl.n_iters}")
+    stage = from_workload(wl, w)
+    stage.want_winner = False
+    n_it = wl.n_iters
+    torch.cuda.synchronize()
+
+    # pass 1: timed
+    run_steps(stage, 0, W, n_it)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run_steps(stage, W, K, n_it)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    events = sum(min(wl.E, (k % n_it + 1) * wl.B) - (k % n_it) * wl.B for k in range(W, W + K))
+    value = events / dt
+    log(f"timed: {K} steps, {events} events, {dt * 1e3:.2f} ms -> {value:,.0f} events/s")
+
+    out = {"metric": METRIC, "value": value, "unit": "events/s", "n_gpus": 1, "steps": K,
+           "warmup": W, "ms_per_step": dt * 1e3 / K, "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": f"{wl.name}-shaped synthetic stream", "nodes": wl.N,
+                      "events": wl.E, "edge_feat": wl.D_e, "memory": wl.M, "time_enc": wl.D_t,
+                      "heads": wl.H, "global_batch": wl.B, "neighbours": wl.nb,
+                      "staleness": wl.s, "graph": wl.meta.get("graph", "")}}
+
+    if not args.no_profile:
+        # pass 2: per-kernel durations (HIP events on the launch stream)
+        tgm.tgm_state_reset(stage.st, stream=stage.stream)
+        run_steps(stage, 0, W, n_it)
+        torch.cuda.synchronize()
+        tgm.tgm_profile_reset()
+        tgm.tgm_profile_enable(True)
+        tp = time.perf_counter()
+        run_steps(stage, W, K, n_it)
+        torch.cuda.synchronize()
+        tp = time.perf_counter() - tp
+        tgm.tgm_profile_enable(False)
+        prof = tgm.tgm_profile_read()
+        # pass 3: algorithmic work per launch
+        rows = account(stage, W, K, n_it)
+        work = work_model(wl, rows)
+        kernels = {}
+        for name, (launches, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
+            avg_s = ms / launches * 1e-3
+            wk = work.get(name, {"flops": 0, "bytes": 0})
+            kernels[name] = {"launches": launches, "avg_us": avg_s * 1e6,
+                             "share": ms / sum(v[1] for v in prof.values()),
+                             "GB/s": wk["bytes"] / avg_s / 1e9,
+                             "TFLOP/s": wk["flops"] / avg_s / 1e12}
+        dom = max(prof, key=lambda k: prof[k][1])
+        dk = kernels[dom]
+        mfma = work.get(dom, {}).get("flops", 0) > 0
+        achieved = dk["TFLOP/s"] if mfma else dk["GB/s"]
+        peak = FP32_MFMA_PEAK_TFS if mfma else HBM_PEAK_GBS
+        traffic = None
+        pmc_path = os.path.join(ROOT, "profiles", f"{dom}_{wl.name}_pmc.json")
+        if os.path.exists(pmc_path):
+            pmc = json.load(open(pmc_path))
+            if pmc.get("source_hash") == source_hash(*pmc.get("sources", [])):
+                traffic = pmc.get("hbm_bytes_per_launch")
+        out["roofline"] = {"kernel": dom, "bound": "mfma" if mfma else "hbm",
+                           "achieved": achieved, "peak": peak,
+                           "unit": "TFLOP/s" if mfma else "GB/s", "frac": achieved / peak,
+                           "traffic": traffic,
+                           "algorithmic_per_launch": work.get(dom),
+                           "avg_launch_us": dk["avg_us"]}
+        out["kernels"] = kernels
+        out["profiled_ms_per_step"] = tp * 1e3 / K
+        out["per_step"] = {k: sum(r[k] for r in rows) / len(rows)
+                           for k in ("R", "slots", "n_U", "n_mail", "n_win")}
+        log(f"dominant kernel {dom}: {dk['avg_us']:.1f} us, {achieved:.2f} "
+            f"{out['roofline']['unit']} ({100 * achieved / peak:.1f}% of peak)")
+    stage.close()
+
+    if not args.no_cpu_baseline:
+        log(f"oracle baseline ({args.cpu_seconds:.0f} s budget)")
+        out["cpu_baseline"] = cpu_baseline(wl, w, W, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
