@@ -203,7 +203,11 @@ def main():
         torch.cuda.synchronize()
         tp = time.perf_counter() - tp
         tgm.tgm_profile_enable(False)
-        prof = tgm.tgm_profile_read()
+        prof = {}
+        for name, (launches, ms) in tgm.tgm_profile_read().items():
+            base = name.split("<")[0]   # template instances count as their kernel
+            n0, m0 = prof.get(base, (0, 0.0))
+            prof[base] = (n0 + launches, m0 + ms)
         # pass 3: algorithmic work per launch
         rows = account(stage, W, K, n_it)
         work = work_model(wl, rows)

@@ -103,6 +103,12 @@ tgm_status_t tgm_sample(tgm_graph_t g, const int32_t *root, const double *root_t
                         int32_t nb, int32_t *nbr, int32_t *eid, double *nts, int32_t *cnt,
                         void *stream);
 
+/* tgm_batch_roots followed by tgm_sample over the 3b roots, in one pass:
+ * same outputs (root, root_ts [3b]; nbr, eid, nts [3b x nb]; cnt [3b]). */
+tgm_status_t tgm_sample_batch(tgm_graph_t g, int64_t first_event, int32_t b, int32_t nb,
+                              int32_t *root, double *root_ts, int32_t *nbr, int32_t *eid,
+                              double *nts, int32_t *cnt, void *stream);
+
 /* Node set of the subgraph: U = sorted unique(root[0..R) and every valid
  * nbr).  nodes [cap] receives U, *n_nodes (device int32) its size, root_pos
  * [R] and nbr_pos [R x nb] the position in U of every root and neighbour (-1
@@ -165,6 +171,9 @@ tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int32_t *nodes
  *     W_q [M x (M + D_t)], b_q [M]; W_k, W_v [M x (M + D_e + D_t)], b_k, b_v [M];
  *     W_o [M x 2M], b_o [M].
  * max_nodes and max_roots bound the node-set size and R of every call.
+ * Limits of this implementation: M <= 128 and divisible by H, 1 <= nb <= 64,
+ * D_e <= 256, and the attention tile of 80 slots x (D_e + D_t) fp32 must fit
+ * the 160 KB of LDS of a workgroup (D_e + D_t <= 384); else TGM_EINVAL.
  */
 typedef struct {
     int32_t M, D_e, D_t, H, nb;

@@ -147,12 +147,48 @@ __device__ __forceinline__ f4 mfma_k16(f4 a, f4 b, f4 c)
     return c;
 }
 
-// Cosine time encoding with the phase formed in fp64: time gaps reach 1e8 s,
-// where an fp32 phase would be off by whole radians.
+// Cosine time encoding cos(omega * dt + beta).  Time gaps reach 1e8 s, where
+// an fp32 phase is off by whole radians, so the phase is formed and reduced to
+// a fraction of a turn in fp64 (to within ~2e-8 rad for |phase| <= 1e8).  The
+// cosine of the reduced angle uses the symmetries of cos to fold the angle into
+// [0, pi/2] (x = 2 pi h, h in [0, 1/4]; beyond a quarter turn
+// cos(2 pi h) = -cos(2 pi (1/2 - h))) and then the Taylor series of cos through
+// the x^12 term, whose truncation error on [0, pi/2] is below
+// (pi/2)^14 / 14! < 1e-8; fp32 rounding keeps the total within ~2e-7.
+__device__ __forceinline__ float cos_turns(float f)   // cos(2 pi f), |f| <= 1/2
+{
+    float h = fabsf(f);
+    const bool flip = h > 0.25f;
+    h = flip ? 0.5f - h : h;
+    const float x = h * 6.28318530717958648f;
+    const float x2 = x * x;
+    // 1 - x^2/2! + x^4/4! - ... + x^12/12!, Horner in x^2
+    float p = 2.08767569878680989792e-9f;         //  1/12!
+    p = fmaf(p, x2, -2.75573192239858906526e-7f);  // -1/10!
+    p = fmaf(p, x2, 2.48015873015873015873e-5f);   //  1/8!
+    p = fmaf(p, x2, -1.38888888888888888889e-3f);  // -1/6!
+    p = fmaf(p, x2, 4.16666666666666666667e-2f);   //  1/4!
+    p = fmaf(p, x2, -0.5f);                        // -1/2!
+    p = fmaf(p, x2, 1.0f);
+    return flip ? -p : p;
+}
+
 __device__ __forceinline__ float time_enc(double omega, double beta, double dt)
 {
-    return (float)cos(fma(omega, dt, beta));
+    const double ph = fma(omega, dt, beta);
+    const double rev = ph * 0.15915494309189535;   // phase in turns: ph / (2 pi)
+    return cos_turns((float)(rev - rint(rev)));    // [-1/2, 1/2] turn, exact in fp64
 }
+
+// Software pipelining: a loop loads the next k-chunk's operand while it
+// multiplies the current one.  Left alone, the compiler sinks such a load to
+// its use in the next iteration (and waits for it there); consuming the
+// registers here, after the iteration's MFMAs have been issued, keeps the load
+// one iteration ahead.
+__device__ __forceinline__ void keep_loaded(const f4 &a) { asm volatile("" ::"v"(a)); }
+// Keeps the scheduler from moving instructions across this point (used right
+// after the prefetch loads so they are issued before the iteration's MFMAs).
+__device__ __forceinline__ void issue_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 __device__ __forceinline__ float wave_sum(float v)
 {
@@ -183,6 +219,108 @@ __device__ __forceinline__ void wave_copy_row(float *__restrict__ dst,
         for (int k = lane; k < n; k += kWave)
             dst[k] = src[k];
     }
+}
+
+// Block-wide gather of `rows` rows of `n` floats into LDS: row r of the
+// destination (stride `lds_stride` floats, starting at column `col0`) is
+// src[off[r] .. off[r] + n), or zeros when off[r] < 0.  `off` lives in LDS.
+// Every thread issues up to kStageUnroll loads before its stores, so a block's
+// row gathers are in flight together instead of one dependent row at a time.
+constexpr int kStageUnroll = 8;
+
+template <int W>
+struct VecOf;
+template <>
+struct VecOf<4> { typedef f4 T; };
+template <>
+struct VecOf<2> { typedef f2 T; };
+template <>
+struct VecOf<1> { typedef float T; };
+
+template <int W>
+__device__ __forceinline__ void stage_rows_w(float *__restrict__ lds, int lds_stride, int col0,
+                                             const float *__restrict__ src,
+                                             const int64_t *__restrict__ off, int rows, int n)
+{
+    typedef typename VecOf<W>::T V;
+    const int per_row = n / W;
+    const int total = rows * per_row;
+    const int nt = blockDim.x;
+    for (int base = threadIdx.x; base < total; base += nt * kStageUnroll) {
+        V v[kStageUnroll];
+#pragma unroll
+        for (int u = 0; u < kStageUnroll; ++u) {
+            const int idx = base + u * nt;
+            if (idx < total) {
+                const int r = idx / per_row, c = idx - r * per_row;
+                const int64_t o = off[r];
+                v[u] = o >= 0 ? *reinterpret_cast<const V *>(src + o + (int64_t)c * W) : V(0);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kStageUnroll; ++u) {
+            const int idx = base + u * nt;
+            if (idx < total) {
+                const int r = idx / per_row, c = idx - r * per_row;
+                *reinterpret_cast<V *>(lds + r * lds_stride + col0 + c * W) = v[u];
+            }
+        }
+    }
+}
+
+// Rows staged by one wavefront: up to RMAX rows of n floats, lanes across the
+// columns in W-float vectors (n <= 64 * W * CMAX).  load() issues every load
+// of the wave's rows at once (no per-element index division); store() writes
+// them to LDS.  Rows with off < 0, and columns past n, are zero.
+template <int W, int RMAX, int CMAX>
+struct WaveRows {
+    typedef typename VecOf<W>::T V;
+    V v[RMAX][CMAX];
+
+    __device__ __forceinline__ void load(const float *__restrict__ src, const int64_t (&off)[RMAX],
+                                         int n, int lane)
+    {
+        const int nv = n / W;
+#pragma unroll
+        for (int i = 0; i < RMAX; ++i)
+#pragma unroll
+            for (int c = 0; c < CMAX; ++c) {
+                const int cc = lane + kWave * c;
+                v[i][c] = (off[i] >= 0 && cc < nv)
+                              ? *reinterpret_cast<const V *>(src + off[i] + (int64_t)cc * W)
+                              : V(0);
+            }
+    }
+
+    // row i goes to LDS row lrow[i] (skipped when lrow[i] < 0)
+    __device__ __forceinline__ void store(float *__restrict__ lds, int stride, int col0,
+                                          const int (&lrow)[RMAX], int n, int lane) const
+    {
+        const int nv = n / W;
+#pragma unroll
+        for (int i = 0; i < RMAX; ++i)
+#pragma unroll
+            for (int c = 0; c < CMAX; ++c) {
+                const int cc = lane + kWave * c;
+                if (lrow[i] >= 0 && cc < nv)
+                    *reinterpret_cast<V *>(lds + lrow[i] * stride + col0 + cc * W) = v[i][c];
+            }
+    }
+};
+
+// `ld` is the source row stride in floats (every off[r] is a multiple of it).
+__device__ __forceinline__ void stage_rows(float *__restrict__ lds, int lds_stride, int col0,
+                                           const float *__restrict__ src, int64_t ld,
+                                           const int64_t *__restrict__ off, int rows, int n)
+{
+    const bool a16 = (reinterpret_cast<uintptr_t>(src) & 15) == 0;
+    const bool a8 = (reinterpret_cast<uintptr_t>(src) & 7) == 0;
+    if (a16 && (n & 3) == 0 && (ld & 3) == 0 && (col0 & 3) == 0 && (lds_stride & 3) == 0)
+        stage_rows_w<4>(lds, lds_stride, col0, src, off, rows, n);
+    else if (a8 && (n & 1) == 0 && (ld & 1) == 0 && (col0 & 1) == 0 && (lds_stride & 1) == 0)
+        stage_rows_w<2>(lds, lds_stride, col0, src, off, rows, n);
+    else
+        stage_rows_w<1>(lds, lds_stride, col0, src, off, rows, n);
 }
 
 // ---------------------------------------------------------------- host

@@ -105,21 +105,13 @@ __global__ void k_batch_roots(int64_t first, int32_t b, const int32_t *__restric
 // and the ballot's popcount names the segment holding p), then lanes
 // j < nb read entries p-1-j: the nb most recent strictly earlier events,
 // newest first.
-__global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
-                                                const AdjRec *__restrict__ adj,
-                                                const int32_t *__restrict__ root,
-                                                const double *__restrict__ root_ts, int32_t R,
-                                                int32_t N, int32_t nb, int32_t *__restrict__ nbr,
-                                                int32_t *__restrict__ eid,
-                                                double *__restrict__ nts,
-                                                int32_t *__restrict__ cnt)
+__device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
+                                           const AdjRec *__restrict__ adj, int r, int32_t v,
+                                           double tq, int32_t N, int32_t nb,
+                                           int32_t *__restrict__ nbr, int32_t *__restrict__ eid,
+                                           double *__restrict__ nts, int32_t *__restrict__ cnt)
 {
-    const int r = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
     const int lane = threadIdx.x & 63;
-    if (r >= R)
-        return;
-    const int32_t v = root[r];
-    const double tq = root_ts[r];
     const bool ok = v >= 0 && v < N;   // an id out of range samples nothing
     const int64_t base = ok ? off[v] : 0;
     int64_t lo = base, hi = ok ? off[v + 1] : 0;
@@ -155,6 +147,44 @@ __global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
         cnt[r] = c;
 }
 
+__global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
+                                                const AdjRec *__restrict__ adj,
+                                                const int32_t *__restrict__ root,
+                                                const double *__restrict__ root_ts, int32_t R,
+                                                int32_t N, int32_t nb, int32_t *__restrict__ nbr,
+                                                int32_t *__restrict__ eid,
+                                                double *__restrict__ nts,
+                                                int32_t *__restrict__ cnt)
+{
+    const int r = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
+    if (r >= R)
+        return;
+    sample_one(off, adj, r, root[r], root_ts[r], N, nb, nbr, eid, nts, cnt);
+}
+
+// Roots of a batch and their sampling in one pass: wavefront r takes root r
+// of src[batch] ++ dst[batch] ++ neg[batch] straight from the event arrays.
+__global__ __launch_bounds__(256) void k_sample_batch(
+    const int64_t *__restrict__ off, const AdjRec *__restrict__ adj, int64_t first, int32_t b,
+    const int32_t *__restrict__ src, const int32_t *__restrict__ dst,
+    const int32_t *__restrict__ neg, const double *__restrict__ t, int32_t N, int32_t nb,
+    int32_t *__restrict__ root, double *__restrict__ root_ts, int32_t *__restrict__ nbr,
+    int32_t *__restrict__ eid, double *__restrict__ nts, int32_t *__restrict__ cnt)
+{
+    const int r = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
+    if (r >= 3 * b)
+        return;
+    const int third = r / b, k = r - third * b;
+    const int64_t e = first + k;
+    const int32_t v = third == 0 ? src[e] : (third == 1 ? dst[e] : neg[e]);
+    const double tq = t[e];
+    if ((threadIdx.x & 63) == 0) {
+        root[r] = v;
+        root_ts[r] = tq;
+    }
+    sample_one(off, adj, r, v, tq, N, nb, nbr, eid, nts, cnt);
+}
+
 // ------------------------------------------------------------ node set
 // One workgroup: marks roots and neighbours in an LDS bitmap over node ids,
 // scans the word popcounts to number the set bits in id order (which sorts
@@ -162,6 +192,7 @@ __global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
 // position.
 constexpr int kNsThreads = 1024;
 constexpr int kNsMaxWords = 1 << 14;   // 2^19 node ids
+constexpr int kNsBatch = 24;   // ids each thread has in flight
 
 __global__ __launch_bounds__(kNsThreads) void k_node_set(
     int32_t N, const int32_t *__restrict__ root, int32_t R, const int32_t *__restrict__ nbr,
@@ -178,16 +209,20 @@ __global__ __launch_bounds__(kNsThreads) void k_node_set(
     for (int k = tid; k < W; k += kNsThreads)
         bits[k] = 0u;
     __syncthreads();
-    // ids outside [0, N) are not members; they map to position -1
-    for (int k = tid; k < R; k += kNsThreads) {
-        const int32_t v = root[k];
-        if (v >= 0 && v < N)
-            atomicOr(&bits[v >> 5], 1u << (v & 31));
-    }
-    for (int k = tid; k < Rnb; k += kNsThreads) {
-        const int32_t v = nbr[k];
-        if (v >= 0 && v < N)
-            atomicOr(&bits[v >> 5], 1u << (v & 31));
+    // ids outside [0, N) are not members; they map to position -1.  Each
+    // thread loads kNsBatch ids before marking them, so the loads overlap.
+    const int total = R + Rnb;
+    for (int base = tid; base < total; base += kNsThreads * kNsBatch) {
+        int32_t v[kNsBatch];
+#pragma unroll
+        for (int u = 0; u < kNsBatch; ++u) {
+            const int k = base + u * kNsThreads;
+            v[u] = k < R ? root[k] : (k < total ? nbr[k - R] : -1);
+        }
+#pragma unroll
+        for (int u = 0; u < kNsBatch; ++u)
+            if (v[u] >= 0 && v[u] < N)
+                atomicOr(&bits[v[u] >> 5], 1u << (v[u] & 31));
     }
     __syncthreads();
 
@@ -221,19 +256,28 @@ __global__ __launch_bounds__(kNsThreads) void k_node_set(
         *n_nodes = (int32_t)part[kNsThreads - 1];
     __syncthreads();
 
-    for (int k = tid; k < R; k += kNsThreads) {
-        const int32_t v = root[k];
-        root_pos[k] = (v < 0 || v >= N)
-                          ? -1
-                          : (int32_t)(pre[v >> 5] +
-                                      __popc(bits[v >> 5] & ((1u << (v & 31)) - 1u)));
-    }
-    for (int k = tid; k < Rnb; k += kNsThreads) {
-        const int32_t v = nbr[k];
-        nbr_pos[k] = (v < 0 || v >= N)
-                         ? -1
-                         : (int32_t)(pre[v >> 5] +
-                                     __popc(bits[v >> 5] & ((1u << (v & 31)) - 1u)));
+    for (int base = tid; base < total; base += kNsThreads * kNsBatch) {
+        int32_t v[kNsBatch];
+#pragma unroll
+        for (int u = 0; u < kNsBatch; ++u) {
+            const int k = base + u * kNsThreads;
+            v[u] = k < R ? root[k] : (k < total ? nbr[k - R] : -1);
+        }
+#pragma unroll
+        for (int u = 0; u < kNsBatch; ++u) {
+            const int k = base + u * kNsThreads;
+            if (k < total) {
+                const int32_t x = v[u];
+                const int32_t q = (x < 0 || x >= N)
+                                      ? -1
+                                      : (int32_t)(pre[x >> 5] +
+                                                  __popc(bits[x >> 5] & ((1u << (x & 31)) - 1u)));
+                if (k < R)
+                    root_pos[k] = q;
+                else
+                    nbr_pos[k - R] = q;
+            }
+        }
     }
 }
 
@@ -379,6 +423,24 @@ extern "C" tgm_status_t tgm_sample(tgm_graph_t g, const int32_t *root, const dou
     const int per_block = 256 / kWave;
     TGM_LAUNCH(k_sample, dim3(cdiv(R, per_block)), dim3(256), 0, as_stream(stream),
                        g->off, g->adj, root, root_ts, R, g->N, nb, nbr, eid, nts, cnt);
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_sample_batch(tgm_graph_t g, int64_t first_event, int32_t b,
+                                         int32_t nb, int32_t *root, double *root_ts,
+                                         int32_t *nbr, int32_t *eid, double *nts, int32_t *cnt,
+                                         void *stream)
+{
+    if (!g || b < 0 || first_event < 0 || first_event + b > g->E || nb < 1 || nb > kWave)
+        return TGM_EINVAL;
+    if (b == 0)
+        return TGM_OK;
+    if (!root || !root_ts || !nbr || !eid || !nts || !cnt)
+        return TGM_EINVAL;
+    const int per_block = 256 / kWave;
+    TGM_LAUNCH(k_sample_batch, dim3(cdiv(3 * (int64_t)b, per_block)), dim3(256), 0,
+               as_stream(stream), g->off, g->adj, first_event, b, g->src, g->dst, g->neg, g->t,
+               g->N, nb, root, root_ts, nbr, eid, nts, cnt);
     return TGM_OK;
 }
 

@@ -1,7 +1,9 @@
 // Memory update (GRU + latest-message reduce + staged write-back) and the
 // attention embedding.  The dense contractions run on fp32 MFMA
 // (v_mfma_f32_16x16x4_f32); everything else is vector code.
+#include <algorithm>
 #include <cmath>
+#include <utility>
 
 #include "common.h"
 
@@ -16,14 +18,64 @@ constexpr int kAttMaxRB = 5;   // 16-row slot blocks per workgroup
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 // ------------------------------------------------------------------ GRU
-// One workgroup per 16 node-set rows, one wavefront per 16-wide block of
-// hidden units (round-robin when there are more blocks than waves).  The
-// rows' GRU inputs [mail || phi(mail_ts - mem_ts) | mem] are staged once in
-// LDS; each wave accumulates the four gate pre-activations of its hidden
-// block (r and z over [x | h]; n split into its x part and its h part, which
-// the reset gate scales) and applies the gates in registers.
-// Also resets the latest-message slots of its rows (consumed next by k_latest).
-__global__ __launch_bounds__(512) void k_gru(
+// Workgroup (blockIdx.x, blockIdx.y) owns 16 node-set rows and one 16-wide
+// block of hidden units; its kGruKS wavefronts split the reduction (k) range.
+// The rows' GRU inputs [mail || phi(mail_ts - mem_ts) | mem] are staged in LDS
+// with the row loads of the block in flight together; each wave accumulates
+// partial gate pre-activations for its k-chunks (r and z over [x | h]; n split
+// into its x part and its h part, which the reset gate scales) with the next
+// chunk's weights prefetched; the partials are summed in a fixed wave order
+// (deterministic) and the gates applied.  The hb = 0 workgroups also reset the
+// latest-message slots of their rows (consumed next by k_latest) and write the
+// new memory timestamps.
+constexpr int kGruKS = 4;
+
+// k-chunks [cb, ce) of one part (x or h) of the GRU: three gate accumulators,
+// weights double-buffered in registers (sets A and B alternate, no copies).
+// `cofs` is the part's first chunk in the LDS row.
+__device__ __forceinline__ void gru_part(const f4 *__restrict__ w, int64_t gs, int64_t kstep,
+                                         int hb, int lane, const float *arow, int cb, int ce,
+                                         int cofs, f4 &ar, f4 &az, f4 &an)
+{
+    if (cb >= ce)
+        return;
+    const f4 *pw = w + (int64_t)(cb - cofs) * kstep + (int64_t)hb * kWave + lane;
+    f4 a0 = pw[0], a1 = pw[gs], a2 = pw[2 * gs];
+    keep_loaded(a0);
+    keep_loaded(a1);
+    keep_loaded(a2);
+    int c = cb;
+    for (; c + 1 < ce; c += 2) {
+        const f4 *q = pw + kstep;
+        const f4 b0 = q[0], b1 = q[gs], b2 = q[2 * gs];
+        issue_fence();
+        {
+            const f4 a = *reinterpret_cast<const f4 *>(arow + c * 16);
+            ar = mfma_k16(a, a0, ar);
+            az = mfma_k16(a, a1, az);
+            an = mfma_k16(a, a2, an);
+        }
+        pw += 2 * kstep;
+        a0 = pw[0];
+        a1 = pw[gs];
+        a2 = pw[2 * gs];
+        issue_fence();
+        {
+            const f4 a = *reinterpret_cast<const f4 *>(arow + (c + 1) * 16);
+            ar = mfma_k16(a, b0, ar);
+            az = mfma_k16(a, b1, az);
+            an = mfma_k16(a, b2, an);
+        }
+    }
+    if (c < ce) {
+        const f4 a = *reinterpret_cast<const f4 *>(arow + c * 16);
+        ar = mfma_k16(a, a0, ar);
+        az = mfma_k16(a, a1, az);
+        an = mfma_k16(a, a2, an);
+    }
+}
+
+__global__ __launch_bounds__(64 * kGruKS) void k_gru(
     const int32_t *__restrict__ n_nodes, const float *__restrict__ mem,
     const double *__restrict__ mem_ts, const float *__restrict__ mail,
     const double *__restrict__ mail_ts, const int32_t *__restrict__ ver,
@@ -32,99 +84,151 @@ __global__ __launch_bounds__(512) void k_gru(
     int KXC, int KHC, int MB, float *__restrict__ mem_new, double *__restrict__ new_mem_ts,
     int32_t *__restrict__ win)
 {
+    // LDS: A [16][SA] | partial sums [KS][4][64] f4 | omega, beta [D_t] fp64
     extern __shared__ float lds[];
     __shared__ int s_has[16];
     const int n = *n_nodes;
-    const int row0 = blockIdx.x * 16;
-    if (row0 >= n)
-        return;
     const int KX = KXC * 16, KH = KHC * 16;
     const int SA = KX + KH + 4;
-    const int nw = blockDim.x >> 6;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-
-    for (int rr = wave; rr < 16; rr += nw) {
-        const int p = row0 + rr;
-        float *a = lds + rr * SA;
-        if (p < n) {
-            const bool has = ver[p] >= 0;
-            if (lane == 0) {
-                s_has[rr] = has;
-                win[p] = -1;
-            }
-            for (int k = lane; k < KH; k += kWave)
-                a[KX + k] = k < M ? mem[(int64_t)p * M + k] : 0.f;
-            if (has) {
-                for (int k = lane; k < D_m; k += kWave)
-                    a[k] = mail[(int64_t)p * D_m + k];
-                const double dt = mail_ts[p] - mem_ts[p];
-                for (int d = lane; d < D_t; d += kWave)
-                    a[D_m + d] = time_enc(omega[d], beta[d], dt);
-                for (int k = D_m + D_t + lane; k < KX; k += kWave)
-                    a[k] = 0.f;
-            } else {
-                for (int k = lane; k < KX; k += kWave)
-                    a[k] = 0.f;
-            }
-        } else {
-            if (lane == 0)
-                s_has[rr] = 0;
-            for (int k = lane; k < KX + KH; k += kWave)
-                a[k] = 0.f;
-        }
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+    f4 *red = reinterpret_cast<f4 *>(lds + 16 * SA);
+    double *s_om = reinterpret_cast<double *>(lds + 16 * SA + kGruKS * 4 * kWave * 4);
+    double *s_be = s_om + D_t;
+    if (n <= 0)
+        return;
+    for (int d = tid; d < D_t; d += blockDim.x) {
+        s_om[d] = omega[d];
+        s_be[d] = beta[d];
     }
-    __syncthreads();
-
+    const int KC = KXC + KHC;
+    const int c0 = (wave * KC) / kGruKS, c1 = ((wave + 1) * KC) / kGruKS;
     const float *arow = lds + (lane & 15) * SA + 4 * (lane >> 4);
     const int64_t gx = (int64_t)KXC * MB * kWave;   // stride between gates in bx
     const int64_t gh = (int64_t)KHC * MB * kWave;
-    for (int hb = wave; hb < MB; hb += nw) {
-        f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-        const f4 *px = bx + (int64_t)hb * kWave + lane;
-        for (int kc = 0; kc < KXC; ++kc) {
-            const f4 a = *reinterpret_cast<const f4 *>(arow + kc * 16);
-            const f4 b0 = px[0], b1 = px[gx], b2 = px[2 * gx];
-            px += (int64_t)MB * kWave;
-            ar = mfma_k16(a, b0, ar);
-            az = mfma_k16(a, b1, az);
-            anx = mfma_k16(a, b2, anx);
-        }
-        const f4 *ph = bh + (int64_t)hb * kWave + lane;
-        for (int kc = 0; kc < KHC; ++kc) {
-            const f4 a = *reinterpret_cast<const f4 *>(arow + KX + kc * 16);
-            const f4 b0 = ph[0], b1 = ph[gh], b2 = ph[2 * gh];
-            ph += (int64_t)MB * kWave;
-            ar = mfma_k16(a, b0, ar);
-            az = mfma_k16(a, b1, az);
-            anh = mfma_k16(a, b2, anh);
-        }
-        const int col = hb * 16 + (lane & 15);
-        if (col < M) {
-            const int MP = MB * 16;
-            const float br = bias[col], bz = bias[MP + col], bin = bias[2 * MP + col],
-                        bhn = bias[3 * MP + col];
+    const int64_t kstep = (int64_t)MB * kWave;
+    const bool al =
+        ((reinterpret_cast<uintptr_t>(mail) | reinterpret_cast<uintptr_t>(mem)) & 15) == 0 &&
+        (D_m & 3) == 0 && (M & 3) == 0;   // 16-byte rows: vector loads
+    const int padx = KX - D_m - D_t, padh = KH - M;
+
+    // Tiles (row block r, hidden block hb).  Workgroup w runs on XCD w % 8, and
+    // the XCD x workgroups share the row blocks r = x (mod 8), so the MB tiles
+    // that stage the same 16 rows meet in one L2.  Within an XCD the tiles go
+    // in row-block-major order; the first one past the node set ends the loop.
+    const int nx = gridDim.x >= 8 ? 8 : 1;
+    const int xcd = blockIdx.x % nx, slot = blockIdx.x / nx;
+    const int per_xcd = (gridDim.x - xcd + nx - 1) / nx;   // workgroups on this XCD
+    for (int k = slot;; k += per_xcd) {
+        const int rl = k / MB;                  // the XCD's rl-th row block
+        const int hb = k - rl * MB;
+        const int row0 = (rl * nx + xcd) * 16;
+        if (row0 >= n)
+            break;
+        const int nvalid = min(16, n - row0);
+        __syncthreads();   // the previous tile is done with LDS
+        {
+            // wave w stages rows w, w + 4, w + 8, w + 12 of the tile: one round of
+            // loads for their versions, times, mail and memory
+            int64_t offm[4], offh[4];
+            int lr[4], vr[4];
+            double mts[4], lts[4];
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int rr = 4 * (lane >> 4) + v;
-                const int p = row0 + rr;
-                if (p < n) {
-                    const float h = lds[rr * SA + KX + col];
-                    float o = h;
-                    if (s_has[rr]) {
-                        const float r = sigmoidf_(ar[v] + br);
-                        const float z = sigmoidf_(az[v] + bz);
-                        const float nn = tanhf(anx[v] + bin + r * (anh[v] + bhn));
-                        o = (1.0f - z) * nn + z * h;
+            for (int i = 0; i < 4; ++i) {
+                const int r = wave + 4 * i;
+                const int p = row0 + r;
+                const bool live = r < nvalid;
+                lr[i] = r;
+                vr[i] = live ? ver[p] : -1;
+                mts[i] = live ? mem_ts[p] : 0.0;
+                lts[i] = live ? mail_ts[p] : 0.0;
+                offm[i] = live ? (int64_t)p * D_m : -1;
+                offh[i] = live ? (int64_t)p * M : -1;
+            }
+            if (al) {
+                WaveRows<4, 4, 2> xm;
+                WaveRows<4, 4, 1> xh;
+                xm.load(mail, offm, D_m, lane);
+                xh.load(mem, offh, M, lane);
+                xm.store(lds, SA, 0, lr, D_m, lane);
+                xh.store(lds, SA, KX, lr, M, lane);
+            } else {
+                WaveRows<1, 4, 8> xm;
+                WaveRows<1, 4, 2> xh;
+                xm.load(mail, offm, D_m, lane);
+                xh.load(mem, offh, M, lane);
+                xm.store(lds, SA, 0, lr, D_m, lane);
+                xh.store(lds, SA, KX, lr, M, lane);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = lr[i];
+                const bool has = vr[i] >= 0;
+                const double dt = lts[i] - mts[i];
+                float *row = lds + r * SA;
+                for (int d = lane; d < D_t; d += kWave)
+                    row[D_m + d] = has ? time_enc(s_om[d], s_be[d], dt) : 0.f;
+                for (int k = lane; k < padx; k += kWave)
+                    row[D_m + D_t + k] = 0.f;
+                for (int k = lane; k < padh; k += kWave)
+                    row[KX + M + k] = 0.f;
+                if (lane == 0) {
+                    s_has[r] = has;
+                    if (hb == 0 && r < nvalid) {
+                        win[row0 + r] = -1;
+                        if (new_mem_ts)
+                            new_mem_ts[row0 + r] = has ? lts[i] : mts[i];
                     }
-                    mem_new[(int64_t)p * M + col] = o;
                 }
             }
         }
-    }
-    if (new_mem_ts && threadIdx.x < 16) {
-        const int p = row0 + threadIdx.x;
-        if (p < n)
-            new_mem_ts[p] = s_has[threadIdx.x] ? mail_ts[p] : mem_ts[p];
+        __syncthreads();
+
+        f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
+        // x part chunks [c0, min(c1, KXC)), then h part chunks.  Each part is a
+        // two-set register ping-pong: the weights of chunk c + 1 are loaded while
+        // chunk c is multiplied, then the set of chunk c is refilled with chunk
+        // c + 2 (the packed weights carry padding chunks past the end).
+        {
+            const int xe = c1 < KXC ? c1 : KXC;
+            const int hs = c0 > KXC ? c0 : KXC;
+            gru_part(bx, gx, kstep, hb, lane, arow, c0, xe, 0, ar, az, anx);
+            gru_part(bh, gh, kstep, hb, lane, arow, hs, c1, KXC, ar, az, anh);
+        }
+        red[(wave * 4 + 0) * kWave + lane] = ar;
+        red[(wave * 4 + 1) * kWave + lane] = az;
+        red[(wave * 4 + 2) * kWave + lane] = anx;
+        red[(wave * 4 + 3) * kWave + lane] = anh;
+        __syncthreads();
+
+        // epilogue: thread (v, lane) finishes output element v of lane's 4
+        {
+            const int v = wave;   // kGruKS == 4 waves cover the 4 values of a lane
+            const int col = hb * 16 + (lane & 15);
+            const int rr = 4 * (lane >> 4) + v;
+            const int p = row0 + rr;
+            if (col < M && rr < nvalid) {
+                float gsum[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float acc = 0.f;
+                    for (int w = 0; w < kGruKS; ++w)
+                        acc += red[(w * 4 + q) * kWave + lane][v];
+                    gsum[q] = acc;
+                }
+                const int MP = MB * 16;
+                const float h = lds[rr * SA + KX + col];
+                float o = h;
+                if (s_has[rr]) {
+                    const float r = sigmoidf_(gsum[0] + bias[col]);
+                    const float z = sigmoidf_(gsum[1] + bias[MP + col]);
+                    const float nn =
+                        tanhf(gsum[2] + bias[2 * MP + col] + r * (gsum[3] + bias[3 * MP + col]));
+                    o = (1.0f - z) * nn + z * h;
+                }
+                mem_new[(int64_t)p * M + col] = o;
+            }
+        }
     }
 }
 
@@ -158,46 +262,87 @@ __global__ __launch_bounds__(256) void k_latest(int32_t n_cand, const int32_t *_
         atomicMax(&win[p], c);
 }
 
-// Stage the write set of one iteration: one wavefront per candidate; the
-// winning candidate of its node writes the node's new memory, its message
-// [s'_self || s'_other || efeat[e]] and the timestamps.
-__global__ __launch_bounds__(256) void k_stage(
-    int32_t n_cand, const int32_t *__restrict__ n_nodes, int64_t first, int M, int D_m, int D_e,
-    const int32_t *__restrict__ src,
-    const int32_t *__restrict__ dst, const double *__restrict__ t,
-    const float *__restrict__ efeat, const int32_t *__restrict__ src_pos,
-    const int32_t *__restrict__ dst_pos, const int32_t *__restrict__ win,
-    const float *__restrict__ mem_new, const int32_t *__restrict__ ver,
-    const double *__restrict__ mem_ts, const double *__restrict__ mail_ts,
-    int32_t *__restrict__ r_flag, int32_t *__restrict__ r_node, float *__restrict__ r_mem,
-    double *__restrict__ r_mem_ts, float *__restrict__ r_mail, double *__restrict__ r_mail_ts)
+// Stage the write set of iteration i, and commit an older one, in one launch.
+// Wavefronts c < n_cand each take one candidate of iteration i: the winning
+// candidate of its node writes the node's new memory, its message
+// [s'_self || s'_other || efeat[e]] and the timestamps -- into the ring slot of
+// iteration i, or straight into the tables when the staleness is 0.
+// Wavefronts n_cand <= c < n_cand + n_commit copy the flagged rows of the ring
+// slot of iteration c_iter (= i - s) into the tables: every fetch up to
+// iteration i has already been issued, and the next one needs exactly the
+// writes through i - s.
+struct StageArgs {
+    int32_t n_cand, n_commit;
+    int64_t first, iter, c_iter;
+    int M, D_m, D_e;
+    bool direct;
+    const int32_t *n_nodes, *src, *dst, *src_pos, *dst_pos, *win, *ver;
+    const double *t, *mem_ts, *mail_ts;
+    const float *efeat, *mem_new;
+    // destination ring slot of iteration i
+    int32_t *r_flag, *r_node;
+    float *r_mem, *r_mail;
+    double *r_mem_ts, *r_mail_ts;
+    // ring slot committed in this launch
+    const int32_t *c_flag, *c_node;
+    const float *c_mem, *c_mail;
+    const double *c_mem_ts, *c_mail_ts;
+    // committed tables
+    float *mem, *mail;
+    double *t_mem_ts, *t_mail_ts;
+    int32_t *t_ver;
+};
+
+__global__ __launch_bounds__(256) void k_stage(StageArgs g)
 {
     const int c = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
     const int lane = threadIdx.x & 63;
-    if (c >= n_cand)
-        return;
-    const int k = c >> 1, role = c & 1;
-    const int n = *n_nodes;
-    const int p = role ? dst_pos[k] : src_pos[k];
-    const int q = role ? src_pos[k] : dst_pos[k];
-    if (p < 0 || p >= n || q < 0 || q >= n || win[p] != c) {
-        if (lane == 0)
-            r_flag[c] = 0;
+    const int M = g.M, D_m = g.D_m, D_e = g.D_e;
+    if (c >= g.n_cand) {
+        const int k = c - g.n_cand;
+        if (k >= g.n_commit || !g.c_flag[k])
+            return;
+        const int32_t v = g.c_node[k];
+        wave_copy_row(g.mem + (int64_t)v * M, g.c_mem + (int64_t)k * M, M, lane);
+        wave_copy_row(g.mail + (int64_t)v * D_m, g.c_mail + (int64_t)k * D_m, D_m, lane);
+        if (lane == 0) {
+            g.t_mem_ts[v] = g.c_mem_ts[k];
+            g.t_mail_ts[v] = g.c_mail_ts[k];
+            g.t_ver[v] = (int32_t)g.c_iter;
+        }
         return;
     }
-    const int64_t e = first + k;
-    const float *sp = mem_new + (int64_t)p * M;
-    float *ml = r_mail + (int64_t)c * D_m;
-    wave_copy_row(r_mem + (int64_t)c * M, sp, M, lane);
+    const int k = c >> 1, role = c & 1;
+    const int n = *g.n_nodes;
+    const int p = role ? g.dst_pos[k] : g.src_pos[k];
+    const int q = role ? g.src_pos[k] : g.dst_pos[k];
+    if (p < 0 || p >= n || q < 0 || q >= n || g.win[p] != c) {
+        if (lane == 0 && !g.direct)
+            g.r_flag[c] = 0;
+        return;
+    }
+    const int64_t e = g.first + k;
+    const int32_t w = role ? g.dst[e] : g.src[e];
+    const float *sp = g.mem_new + (int64_t)p * M;
+    float *dm = g.direct ? g.mem + (int64_t)w * M : g.r_mem + (int64_t)c * M;
+    float *ml = g.direct ? g.mail + (int64_t)w * D_m : g.r_mail + (int64_t)c * D_m;
+    wave_copy_row(dm, sp, M, lane);
     wave_copy_row(ml, sp, M, lane);
-    wave_copy_row(ml + M, mem_new + (int64_t)q * M, M, lane);
+    wave_copy_row(ml + M, g.mem_new + (int64_t)q * M, M, lane);
     if (D_e > 0)
-        wave_copy_row(ml + 2 * M, efeat + e * D_e, D_e, lane);
+        wave_copy_row(ml + 2 * M, g.efeat + e * D_e, D_e, lane);
     if (lane == 0) {
-        r_flag[c] = 1;
-        r_node[c] = role ? dst[e] : src[e];
-        r_mem_ts[c] = ver[p] >= 0 ? mail_ts[p] : mem_ts[p];
-        r_mail_ts[c] = t[e];
+        const double mts = g.ver[p] >= 0 ? g.mail_ts[p] : g.mem_ts[p];
+        if (g.direct) {
+            g.t_mem_ts[w] = mts;
+            g.t_mail_ts[w] = g.t[e];
+            g.t_ver[w] = (int32_t)g.iter;
+        } else {
+            g.r_flag[c] = 1;
+            g.r_node[c] = w;
+            g.r_mem_ts[c] = mts;
+            g.r_mail_ts[c] = g.t[e];
+        }
     }
 }
 
@@ -220,33 +365,90 @@ __global__ __launch_bounds__(512) void k_node_proj(const int32_t *__restrict__ n
                                                    int PC, const f4 *__restrict__ pb, int PNB,
                                                    float *__restrict__ P)
 {
+    // persistent over 16-row tiles (launched with 4..8 waves); wave w owns
+    // column blocks w, w + nw, w + 2nw
+    // (a block past the last is a copy of w: it stores the same values), three
+    // independent accumulators fed from double-buffered weight registers
     extern __shared__ float lds[];
     const int n = *n_nodes;
-    const int row0 = blockIdx.x * 16;
-    if (row0 >= n)
-        return;
     const int K = PC * 16, SA = K + 4, ldP = PNB * 16;
     const int nw = blockDim.x >> 6;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    for (int rr = wave; rr < 16; rr += nw) {
-        const int p = row0 + rr;
-        for (int k = lane; k < K; k += kWave)
-            lds[rr * SA + k] = (p < n && k < M) ? mem_new[(int64_t)p * M + k] : 0.f;
-    }
-    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
+    const int cb0 = wave;
+    const int cb1 = wave + nw < PNB ? wave + nw : wave;
+    const int cb2 = wave + 2 * nw < PNB ? wave + 2 * nw : wave;
+    const int64_t o1 = (int64_t)(cb1 - cb0) * kWave, o2 = (int64_t)(cb2 - cb0) * kWave;
+    const int64_t kstep = (int64_t)PNB * kWave;
     const float *arow = lds + (lane & 15) * SA + 4 * (lane >> 4);
-    for (int cb = wave; cb < PNB; cb += nw) {
-        f4 acc = {0, 0, 0, 0};
-        const f4 *pp = pb + (int64_t)cb * kWave + lane;
-        for (int kc = 0; kc < PC; ++kc) {
-            acc = mfma_k16(*reinterpret_cast<const f4 *>(arow + kc * 16), *pp, acc);
-            pp += (int64_t)PNB * kWave;
+    for (int row0 = blockIdx.x * 16; row0 < n; row0 += gridDim.x * 16) {
+        __syncthreads();   // the previous tile is done with LDS
+        {
+            int64_t off[4];
+            int lr[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {   // wave w stages rows w + nw i (nw >= 4)
+                const int r = wave + nw * i;
+                lr[i] = r < 16 ? r : -1;
+                off[i] = (r < 16 && row0 + r < n) ? (int64_t)(row0 + r) * M : -1;
+            }
+            if ((M & 3) == 0 && (reinterpret_cast<uintptr_t>(mem_new) & 15) == 0) {
+                WaveRows<4, 4, 1> x;
+                x.load(mem_new, off, M, lane);
+                x.store(lds, SA, 0, lr, M, lane);
+            } else {
+                WaveRows<1, 4, 2> x;
+                x.load(mem_new, off, M, lane);
+                x.store(lds, SA, 0, lr, M, lane);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (lr[i] >= 0)
+                    for (int k = M + lane; k < K; k += kWave)
+                        lds[lr[i] * SA + k] = 0.f;
         }
+        __syncthreads();
+        if (cb0 >= PNB)
+            continue;
+        f4 c0 = {0, 0, 0, 0}, c1 = c0, c2 = c0;
+        const f4 *p = pb + (int64_t)cb0 * kWave + lane;
+        f4 x0 = p[0], x1 = p[o1], x2 = p[o2];
+        keep_loaded(x0);
+        keep_loaded(x1);
+        keep_loaded(x2);
+        auto mma = [&](int kc, const f4 w0, const f4 w1, const f4 w2) {
+            const f4 a = *reinterpret_cast<const f4 *>(arow + kc * 16);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                c0 = mfma_16x16x4(a[j], w0[j], c0);
+                c1 = mfma_16x16x4(a[j], w1[j], c1);
+                c2 = mfma_16x16x4(a[j], w2[j], c2);
+            }
+        };
+        int kc = 0;
+        for (; kc + 1 < PC; kc += 2) {   // weights carry padding chunks past the end
+            const f4 *q = p + kstep;
+            const f4 y0 = q[0], y1 = q[o1], y2 = q[o2];
+            issue_fence();
+            mma(kc, x0, x1, x2);
+            p += 2 * kstep;
+            x0 = p[0];
+            x1 = p[o1];
+            x2 = p[o2];
+            issue_fence();
+            mma(kc + 1, y0, y1, y2);
+        }
+        if (kc < PC)
+            mma(kc, x0, x1, x2);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int p = row0 + 4 * (lane >> 4) + v;
-            if (p < n)
-                P[(int64_t)p * ldP + cb * 16 + (lane & 15)] = acc[v];
+            const int r = row0 + 4 * (lane >> 4) + v;
+            if (r < n) {
+                float *out = P + (int64_t)r * ldP + (lane & 15);
+                out[cb0 * 16] = c0[v];
+                out[cb1 * 16] = c1[v];
+                out[cb2 * 16] = c2[v];
+            }
         }
     }
 }
@@ -273,22 +475,35 @@ struct AttnArgs {
 
 // Attention embedding of RT roots per workgroup (their RT*nb slots fill RBa
 // 16-row MFMA blocks):
-//  1. stage each slot's [efeat[eid] || phi(t_root - t_slot)] row in LDS;
-//  2. one MFMA GEMM gives the per-slot part of K and V for all heads;
-//  3. add the node projections of the neighbour and the biases (K, V back to
-//     LDS); q = P_q[root] + (W_q^t phi(0) + b_q);
-//  4. one wavefront per (root, head): scores, softmax, weighted sum of V;
-//  5. the output projection ReLU(W_o [a || s'_v] + b_o) as a second MFMA GEMM.
+//  1. metadata of the slots and roots, and the time-encoding constants, to LDS
+//     (one round of loads);
+//  2. each slot's [efeat[eid] || phi(t_root - t_slot)] row, the roots' query
+//     and s'_v rows to LDS (one round of loads, all in flight together);
+//  3. one MFMA GEMM gives the per-slot part of K and V for all heads; its
+//     accumulators start from the neighbour's node projection plus the bias,
+//     and the (row block, column block) tiles are dealt out evenly over the
+//     waves; K and V go back to LDS;
+//  4. scores (one thread per (root, head, slot)), softmax (one thread per
+//     (root, head)) and the weighted sum of V (one thread per output);
+//  5. the output projection ReLU(W_o [a || s'_v] + b_o) as a second MFMA GEMM
+//     whose weights were fetched before step 4.
+constexpr int kAttMaxSlots = kAttMaxRB * 16;
+constexpr int kAttMaxOC = 16;   // 16-wide k-chunks of the output projection (2M <= 256)
+
+template <int RB>   // 16-row slot blocks per workgroup (3..5)
 __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
 {
     extern __shared__ float lds[];
+    __shared__ int s_np[kAttMaxSlots];         // neighbour's node-set position, -1 if none
+    __shared__ int64_t s_qoff[kAttMaxSlots], s_voff[kAttMaxSlots];
+    __shared__ int s_cnt[kAttMaxSlots];
     const int r0 = blockIdx.x * g.RT;
     const int nroots = min(g.RT, g.R - r0);
     if (nroots <= 0)
         return;
-    const int M = g.M, nb = g.nb, D_e = g.D_e, D_t = g.D_t;
+    const int M = g.M, nb = g.nb, D_e = g.D_e, D_t = g.D_t, H = g.H;
     const int n = *g.n_nodes;   // positions and event ids are bounds-checked
-    const int RA = g.RBa * 16;
+    const int RA = RB * 16;
     const int KF = g.KFC * 16, SA = KF + 4;
     const int SKV = g.KVNB * 16 + 4;
     const int ORB = (g.RT + 15) / 16;
@@ -296,164 +511,296 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
     float *A = lds;                                   // [RA][SA], then K|V [RA][SKV]
     float *Q = lds + RA * (SA > SKV ? SA : SKV);      // [RT][M]
     float *AO = Q + g.RT * M;                         // [ORB*16][SAO]: [a || s'_v]
+    float *S = AO + ORB * 16 * SAO;                   // [RT*H*nb] scores, then weights
+    // [D_t] fp64 frequencies and phases, at an 8-byte aligned float offset
+    double *s_om = reinterpret_cast<double *>(lds + (((S - lds) + RA * H + 1) & ~(int64_t)1));
+    double *s_be = s_om + D_t;
     const int nw = blockDim.x >> 6;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
 
-    // 1. slot rows
-    for (int sr = wave; sr < RA; sr += nw) {
-        float *row = A + sr * SA;
-        const int r = sr / nb, j = sr - r * nb;
-        const bool valid = r < nroots && j < g.cnt[r0 + r];
-        if (valid) {
-            const int64_t sl = (int64_t)(r0 + r) * nb + j;
-            const int64_t e = g.eid[sl];
-            if (D_e > 0 && e >= 0 && e < g.E)
-                wave_copy_row(row, g.efeat + e * D_e, D_e, lane);
-            else
-                for (int k = lane; k < D_e; k += kWave)
-                    row[k] = 0.f;
-            const double dt = g.root_ts[r0 + r] - g.nts[sl];
-            for (int d = lane; d < D_t; d += kWave)
-                row[D_e + d] = time_enc(g.omega[d], g.beta[d], dt);
-            for (int k = D_e + D_t + lane; k < KF; k += kWave)
-                row[k] = 0.f;
-        } else {
-            for (int k = lane; k < KF; k += kWave)
-                row[k] = 0.f;
-        }
-    }
-    // query rows and the s'_v half of the output-projection input
-    for (int r = wave; r < ORB * 16; r += nw) {
-        float *ao = AO + r * SAO;
+    // 1. metadata of the roots and the time-encoding constants
+    for (int r = tid; r < ORB * 16; r += blockDim.x) {
         const int pv = r < nroots ? g.root_pos[r0 + r] : -1;
         const bool ok = pv >= 0 && pv < n;
-        const float *pq = g.P + (int64_t)(ok ? pv : 0) * g.ldP;
-        const float *sv = g.mem_new + (int64_t)(ok ? pv : 0) * M;
-        for (int k = lane; k < M; k += kWave) {
-            if (r < g.RT)
-                Q[r * M + k] = (ok ? pq[k] : 0.f) + g.c_q[k];
-            ao[M + k] = ok ? sv[k] : 0.f;
-            if (r >= nroots)
-                ao[k] = 0.f;
-        }
-        for (int k = 2 * M + lane; k < g.OC * 16; k += kWave)
-            ao[k] = 0.f;
+        s_qoff[r] = ok ? (int64_t)pv * g.ldP : -1;
+        s_voff[r] = ok ? (int64_t)pv * M : -1;
+        s_cnt[r] = r < nroots ? g.cnt[r0 + r] : 0;
+    }
+    for (int d = tid; d < D_t; d += blockDim.x) {
+        s_om[d] = g.omega[d];
+        s_be[d] = g.beta[d];
     }
     __syncthreads();
 
-    // 2. per-slot K|V GEMM; wave w owns column blocks w and w + nw (at most
-    //    kMaxCB blocks per wave; all indices below are compile-time so the
-    //    accumulators stay in registers)
-    f4 acc[kAttMaxCB][kAttMaxRB];
-    const float *arow = A + (lane & 15) * SA + 4 * (lane >> 4);
+    // GEMM tiles of this wave: column blocks cb0 = wave and cb1 = wave + nw
+    // (cb1 = cb0 when past the last block: the copy computes and stores the same
+    // values) over all RB row blocks, so each A fragment read from LDS feeds
+    // both column blocks.
+    const int cb0 = wave, cb1 = wave + nw < g.KVNB ? wave + nw : wave;
+    const bool has_tiles = cb0 < g.KVNB;
+
+    // 2. rows: query and s'_v (small, loaded first), slot features, time codes
+    const bool qv4 = (M & 3) == 0;
+    f4 qreg[2], vreg[2];
+    const int nq4 = qv4 ? nroots * (M >> 2) : 0, nv4 = qv4 ? ORB * 16 * (M >> 2) : 0;
 #pragma unroll
-    for (int i = 0; i < kAttMaxCB; ++i) {
-        const int cb = wave + i * nw;
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        qreg[u] = f4{0, 0, 0, 0};
+        vreg[u] = f4{0, 0, 0, 0};
+        if (i < nq4) {
+            const int r = i / (M >> 2), c = i - r * (M >> 2);
+            if (s_qoff[r] >= 0)
+                qreg[u] = *reinterpret_cast<const f4 *>(g.P + s_qoff[r] + 4 * c);
+        }
+        if (i < nv4) {
+            const int r = i / (M >> 2), c = i - r * (M >> 2);
+            if (s_voff[r] >= 0)
+                vreg[u] = *reinterpret_cast<const f4 *>(g.mem_new + s_voff[r] + 4 * c);
+        }
+    }
+    {
+        // wave w stages slot rows sr = w + nw i: their metadata (uniform loads),
+        // edge-feature rows and time codes, in one round of loads
+        constexpr int RPW = 2 * RB;   // rows per wave: RB * 16 / kMaxWaves
+        int64_t eoff[RPW];
+        int lr[RPW], npos[RPW], valid[RPW];
+        double dts[RPW];
 #pragma unroll
-        for (int rb = 0; rb < kAttMaxRB; ++rb)
-            acc[i][rb] = f4{0, 0, 0, 0};
-        if (cb < g.KVNB) {
-            const f4 *pb = g.kv_b + (int64_t)cb * kWave + lane;
-            for (int kc = 0; kc < g.KFC; ++kc) {
-                const f4 b = *pb;
-                pb += (int64_t)g.KVNB * kWave;
-#pragma unroll
-                for (int rb = 0; rb < kAttMaxRB; ++rb)
-                    if (rb < g.RBa)
-                        acc[i][rb] = mfma_k16(
-                            *reinterpret_cast<const f4 *>(arow + rb * 16 * SA + kc * 16), b,
-                            acc[i][rb]);
+        for (int i = 0; i < RPW; ++i) {
+            const int sr = wave + nw * i;
+            const int r = sr / nb, j = sr - r * nb;
+            lr[i] = sr;
+            valid[i] = 0;
+            eoff[i] = -1;
+            npos[i] = -1;
+            dts[i] = 0.0;
+            if (r < nroots) {
+                const int64_t sl = (int64_t)(r0 + r) * nb + j;
+                const int c = g.cnt[r0 + r];
+                const int64_t e = g.eid[sl];
+                const int q = g.nbr_pos[sl];
+                dts[i] = g.root_ts[r0 + r] - g.nts[sl];
+                valid[i] = j < c;
+                eoff[i] = (valid[i] && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
+                npos[i] = (valid[i] && q >= 0 && q < n) ? q : -1;
             }
         }
+        const uintptr_t ea = reinterpret_cast<uintptr_t>(g.efeat);
+        if (D_e > 0) {
+            if ((ea & 15) == 0 && (D_e & 3) == 0) {
+                WaveRows<4, RPW, 1> xf;
+                xf.load(g.efeat, eoff, D_e, lane);
+                xf.store(A, SA, 0, lr, D_e, lane);
+            } else if ((ea & 7) == 0 && (D_e & 1) == 0) {
+                WaveRows<2, RPW, 2> xf;
+                xf.load(g.efeat, eoff, D_e, lane);
+                xf.store(A, SA, 0, lr, D_e, lane);
+            } else {
+                WaveRows<1, RPW, 4> xf;
+                xf.load(g.efeat, eoff, D_e, lane);
+                xf.store(A, SA, 0, lr, D_e, lane);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            float *row = A + lr[i] * SA;
+            for (int d = lane; d < D_t; d += kWave)
+                row[D_e + d] = valid[i] ? time_enc(s_om[d], s_be[d], dts[i]) : 0.f;
+            for (int k = D_e + D_t + lane; k < KF; k += kWave)
+                row[k] = 0.f;
+            if (lane == 0)
+                s_np[lr[i]] = npos[i];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        if (i < nq4) {
+            const int r = i / (M >> 2), c = i - r * (M >> 2);
+            *reinterpret_cast<f4 *>(Q + r * M + 4 * c) = qreg[u];
+        }
+        if (i < nv4) {
+            const int r = i / (M >> 2), c = i - r * (M >> 2);
+            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) = vreg[u];
+        }
+    }
+    if (qv4) {   // rows past the first 2 * blockDim vectors
+        for (int i = tid + 2 * blockDim.x; i < max(nq4, nv4); i += blockDim.x) {
+            const int r = i / (M >> 2), c = i - r * (M >> 2);
+            if (i < nq4)
+                *reinterpret_cast<f4 *>(Q + r * M + 4 * c) =
+                    s_qoff[r] >= 0 ? *reinterpret_cast<const f4 *>(g.P + s_qoff[r] + 4 * c)
+                                   : f4{0, 0, 0, 0};
+            if (i < nv4)
+                *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
+                    s_voff[r] >= 0 ? *reinterpret_cast<const f4 *>(g.mem_new + s_voff[r] + 4 * c)
+                                   : f4{0, 0, 0, 0};
+        }
+    } else {     // scalar path for M % 4 != 0
+        for (int i = tid; i < ORB * 16 * M; i += blockDim.x) {
+            const int r = i / M, k = i - r * M;
+            if (r < nroots)
+                Q[r * M + k] = s_qoff[r] >= 0 ? g.P[s_qoff[r] + k] : 0.f;
+            AO[r * SAO + M + k] = s_voff[r] >= 0 ? g.mem_new[s_voff[r] + k] : 0.f;
+        }
+    }
+    {
+        // AO: columns [0, M) of rows without a root and the padding [2M, ..)
+        const int w2 = g.OC * 16 - M;
+        for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
+            const int r = idx / w2, c = idx - r * w2;
+            if (c >= M || r >= nroots)
+                AO[r * SAO + (c < M ? c : M + c)] = 0.f;
+        }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < nroots * M; idx += blockDim.x)
+        Q[idx] += g.c_q[idx % M];
+
+    // 3. per-slot K|V GEMM; the accumulators start as P[nbr][M + col] + bias
+    f4 acc[2][RB];
+    const float *arow = A + (lane & 15) * SA + 4 * (lane >> 4);
+    const int64_t kstep = (int64_t)g.KVNB * kWave;
+    if (has_tiles) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int col = (i ? cb1 : cb0) * 16 + (lane & 15);
+            const bool ok = col < 2 * M;
+            const float bias = ok ? (col < M ? g.b_k[col] : g.b_v[col - M]) : 0.f;
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int np = s_np[rb * 16 + 4 * (lane >> 4) + v];
+                    acc[i][rb][v] =
+                        bias + ((ok && np >= 0) ? g.P[(int64_t)np * g.ldP + M + col] : 0.f);
+                }
+        }
+        const f4 *p0 = g.kv_b + (int64_t)cb0 * kWave + lane;
+        const int64_t o1 = (int64_t)(cb1 - cb0) * kWave;
+// one k-chunk: the RB A fragments, then the MFMAs k-slice-major over the
+// 2 x RB independent accumulators
+#define TGM_ATT_MMA(KC, B0, B1)                                                              \
+    {                                                                                       \
+        f4 a_[RB];                                                                          \
+        _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                                   \
+            a_[rb] = *reinterpret_cast<const f4 *>(arow + rb * 16 * SA + (KC) * 16);        \
+        _Pragma("unroll") for (int j = 0; j < 4; ++j)                                       \
+        {                                                                                   \
+            _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                               \
+            {                                                                               \
+                acc[0][rb] = mfma_16x16x4(a_[rb][j], (B0)[j], acc[0][rb]);                  \
+                acc[1][rb] = mfma_16x16x4(a_[rb][j], (B1)[j], acc[1][rb]);                  \
+            }                                                                               \
+        }                                                                                   \
+    }
+        // two register sets of weights alternate (chunk kc + 1 loads while kc
+        // multiplies); the packed weights carry padding chunks past the end
+        f4 x0 = p0[0], x1 = p0[o1];
+        keep_loaded(x0);
+        keep_loaded(x1);
+        int kc = 0;
+        for (; kc + 1 < g.KFC; kc += 2) {
+            const f4 *q = p0 + kstep;
+            const f4 y0 = q[0], y1 = q[o1];
+            issue_fence();
+            TGM_ATT_MMA(kc, x0, x1)
+            p0 += 2 * kstep;
+            x0 = p0[0];
+            x1 = p0[o1];
+            issue_fence();
+            TGM_ATT_MMA(kc + 1, y0, y1)
+        }
+        if (kc < g.KFC) {
+            TGM_ATT_MMA(kc, x0, x1)
+        }
+#undef TGM_ATT_MMA
     }
     __syncthreads();   // every read of the slot rows is done
 
-    // 3. K | V rows: per-slot part + node projection of the neighbour + bias.
-    //    Column col < M is K, col in [M, 2M) is V; both sit at P[M + col].
     float *KV = A;
+    if (has_tiles) {
 #pragma unroll
-    for (int i = 0; i < kAttMaxCB; ++i) {
-        const int cb = wave + i * nw;
-        const int col = cb * 16 + (lane & 15);
-        if (cb < g.KVNB && col < 2 * M) {
-            const float bias = col < M ? g.b_k[col] : g.b_v[col - M];
+        for (int i = 0; i < 2; ++i) {
+            const int col = (i ? cb1 : cb0) * 16 + (lane & 15);
 #pragma unroll
-            for (int rb = 0; rb < kAttMaxRB; ++rb) {
-                if (rb < g.RBa) {
+            for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int row = rb * 16 + 4 * (lane >> 4) + v;
-                        const int r = row / nb, j = row - r * nb;
-                        if (r < nroots && j < g.cnt[r0 + r]) {
-                            const int np = g.nbr_pos[(int64_t)(r0 + r) * nb + j];
-                            const float pk =
-                                (np >= 0 && np < n) ? g.P[(int64_t)np * g.ldP + M + col] : 0.f;
-                            KV[row * SKV + col] = acc[i][rb][v] + bias + pk;
-                        }
-                    }
-                }
-            }
+                for (int v = 0; v < 4; ++v)
+                    KV[(rb * 16 + 4 * (lane >> 4) + v) * SKV + col] = acc[i][rb][v];
         }
     }
+    // the output projection's weights: fetched now, used in step 5
+    f4 ob[kAttMaxOC];
+    const int ocb = wave;   // waves beyond ONB have no output column block
+#pragma unroll
+    for (int kc = 0; kc < kAttMaxOC; ++kc)
+        ob[kc] = (ocb < g.ONB && kc < g.OC)
+                     ? g.out_b[((int64_t)kc * g.ONB + ocb) * kWave + lane]
+                     : f4{0, 0, 0, 0};
     __syncthreads();
 
-    // 4. per (root, head) attention; head width d_h <= 128
-    const int d_h = M / g.H;
+    // 4. attention: scores, softmax, weighted sum of V
+    const int d_h = M / H;
     const float scale = 1.0f / sqrtf((float)d_h);
-    for (int task = wave; task < nroots * g.H; task += nw) {
-        const int r = task / g.H, eta = task - r * g.H;
-        const int c = g.cnt[r0 + r];
-        const int o = eta * d_h;
-        const float *qr = Q + r * M + o;
-        float *ao = AO + r * SAO + o;
-        // lane j keeps score j
-        float my_s = -INFINITY;
-        for (int j = 0; j < c; ++j) {
-            const float *kr = KV + (r * nb + j) * SKV + o;
-            float part = 0.f;
-            if (lane < d_h)
-                part = qr[lane] * kr[lane];
-            if (lane + kWave < d_h)
-                part += qr[lane + kWave] * kr[lane + kWave];
-            const float sj = wave_sum(part) * scale;
-            if (lane == j)
-                my_s = sj;
+    const int nsc = nroots * H * nb;
+    for (int idx = tid; idx < nsc; idx += blockDim.x) {
+        const int r = idx / (H * nb), rem = idx - r * (H * nb);
+        const int eta = rem / nb, j = rem - eta * nb;
+        float sc = -INFINITY;
+        if (j < s_cnt[r]) {
+            const float *qr = Q + r * M + eta * d_h;
+            const float *kr = KV + (r * nb + j) * SKV + eta * d_h;
+            float dot = 0.f;
+            for (int d = 0; d < d_h; ++d)
+                dot += qr[d] * kr[d];
+            sc = dot * scale;
         }
-        float mx = my_s;
-#pragma unroll
-        for (int sh = 32; sh > 0; sh >>= 1)
-            mx = fmaxf(mx, __shfl_xor(mx, sh, kWave));
-        const float ex = lane < c ? expf(my_s - mx) : 0.f;
-        const float den = wave_sum(ex);
-        const float alpha = c > 0 ? ex / den : 0.f;
-        float a0 = 0.f, a1 = 0.f;
+        S[idx] = sc;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < nroots * H; idx += blockDim.x) {
+        const int r = idx / H;
+        float *sr = S + idx * nb;
+        const int c = s_cnt[r];
+        float mx = -INFINITY;
+        for (int j = 0; j < c; ++j)
+            mx = fmaxf(mx, sr[j]);
+        float den = 0.f;
         for (int j = 0; j < c; ++j) {
-            const float al = __shfl(alpha, j, kWave);
-            const float *vr = KV + (r * nb + j) * SKV + M + o;
-            if (lane < d_h)
-                a0 += al * vr[lane];
-            if (lane + kWave < d_h)
-                a1 += al * vr[lane + kWave];
+            const float e = expf(sr[j] - mx);
+            sr[j] = e;
+            den += e;
         }
-        if (lane < d_h)
-            ao[lane] = a0;
-        if (lane + kWave < d_h)
-            ao[lane + kWave] = a1;
+        for (int j = 0; j < c; ++j)
+            sr[j] = sr[j] / den;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < nroots * M; idx += blockDim.x) {
+        const int r = idx / M, k = idx - r * M;
+        const int eta = k / d_h;
+        const float *al = S + (r * H + eta) * nb;
+        const int c = s_cnt[r];
+        float a = 0.f;
+        for (int j = 0; j < c; ++j)
+            a += al[j] * KV[(r * nb + j) * SKV + M + k];
+        AO[r * SAO + k] = a;   // 0 when the root has no neighbours
     }
     __syncthreads();
 
     // 5. h = ReLU(W_o [a || s'_v] + b_o)
-    const float *orow = AO + (lane & 15) * SAO + 4 * (lane >> 4);
-    for (int cb = wave; cb < g.ONB; cb += nw) {
+    if (ocb < g.ONB) {
+        const float *orow = AO + (lane & 15) * SAO + 4 * (lane >> 4);
+        const int col = ocb * 16 + (lane & 15);
         for (int orb = 0; orb < ORB; ++orb) {
             f4 ac = {0, 0, 0, 0};
-            const f4 *pb = g.out_b + (int64_t)cb * kWave + lane;
-            for (int kc = 0; kc < g.OC; ++kc) {
-                ac = mfma_k16(*reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + kc * 16), *pb,
-                              ac);
-                pb += (int64_t)g.ONB * kWave;
-            }
-            const int col = cb * 16 + (lane & 15);
+#pragma unroll
+            for (int kc = 0; kc < kAttMaxOC; ++kc)
+                if (kc < g.OC)
+                    ac = mfma_k16(*reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + kc * 16),
+                                  ob[kc], ac);
             if (col < M) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -480,14 +827,39 @@ __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q,
     c_q[k] = (float)acc;
 }
 
+bool attn_lds_opt_in(int bytes)
+{
+    return hipFuncSetAttribute((const void *)k_attn<3>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               bytes) == hipSuccess &&
+           hipFuncSetAttribute((const void *)k_attn<4>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               bytes) == hipSuccess &&
+           hipFuncSetAttribute((const void *)k_attn<5>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               bytes) == hipSuccess;
+}
+
 int waves_for(int blocks) { return blocks < kMaxWaves ? (blocks < 1 ? 1 : blocks) : kMaxWaves; }
 
-size_t gru_lds(const tgm_model *m) { return sizeof(float) * 16 * ((m->KXC + m->KHC) * 16 + 4); }
+size_t gru_lds(const tgm_model *m)
+{
+    return sizeof(float) * (16 * ((m->KXC + m->KHC) * 16 + 4) + kGruKS * 4 * kWave * 4) +
+           2 * sizeof(double) * m->D_t;
+}
+
+// Persistent grid of k_gru: the tiles of the largest node set, capped at the
+// workgroups that fit on the device at once.
+int gru_grid(const tgm_model *m, int cap)
+{
+    const int64_t tiles = cdiv(cap, 16) * m->MB;
+    const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / gru_lds(m));
+    const int64_t resident = 256LL * std::min(per_cu, 8);
+    return (int)std::max<int64_t>(1, std::min(tiles, resident));
+}
 size_t proj_lds(const tgm_model *m) { return sizeof(float) * 16 * (m->PC * 16 + 4); }
 
 int attn_roots(const tgm_model *m, int *RBa)
 {
-    // slots of RT roots fill at most 5 MFMA row blocks
+    // slots of RT roots fill at most 5 MFMA row blocks; for 1 <= nb <= 64 this
+    // gives 3 <= RBa <= 5 (the instantiations of k_attn)
     int rb = 5;
     int RT = (16 * rb) / m->nb;
     if (RT < 1)
@@ -503,8 +875,10 @@ size_t attn_lds(const tgm_model *m)
     const int RA = RBa * 16;
     const int SA = m->KFC * 16 + 4, SKV = m->KVNB * 16 + 4;
     const int ORB = (RT + 15) / 16;
-    return sizeof(float) * ((size_t)RA * (SA > SKV ? SA : SKV) + (size_t)RT * m->M +
-                            (size_t)ORB * 16 * (m->OC * 16 + 4));
+    const size_t before_s = (size_t)RA * (SA > SKV ? SA : SKV) + (size_t)RT * m->M +
+                            (size_t)ORB * 16 * (m->OC * 16 + 4);
+    const size_t om = (before_s + (size_t)RA * m->H + 1) & ~(size_t)1;   // as in k_attn
+    return sizeof(float) * om + 2 * sizeof(double) * m->D_t;
 }
 
 }  // namespace
@@ -540,10 +914,11 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     *out = nullptr;
     const int M = d->M, D_e = d->D_e, D_t = d->D_t, H = d->H, nb = d->nb;
     // limits of the kernels' tiling: K|V column blocks fit kMaxWaves * kAttMaxCB
-    // wavefront slots (M <= 128) and a head is at most two lanes wide per lane
+    // wavefront slots (M <= 128), a wavefront stages rows of at most 256 edge
+    // features (so D_m <= 512); LDS bounds D_e + D_t (checked below)
     if (M <= 0 || D_e < 0 || D_t < 0 || H <= 0 || M % H != 0 || nb < 1 || nb > 64 ||
         d->max_nodes <= 0 || d->max_roots < 0 || 2 * M > 16 * kMaxWaves * kAttMaxCB ||
-        M / H > 2 * kWave)
+        D_e > 256)
         return TGM_EINVAL;
     if (!w->W_ih || !w->W_hh || !w->b_ih || !w->b_hh || (D_t > 0 && (!w->omega || !w->beta)) ||
         !w->W_q || !w->b_q || !w->W_k || !w->b_k || !w->W_v || !w->b_v || !w->W_o || !w->b_o)
@@ -600,6 +975,13 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
         }
     auto kvb = pack_b(wkv.data(), 2 * M, KF, 0, KF, m->KFC, m->KVNB);
     auto ob = pack_b(w->W_o, M, 2 * M, 0, 2 * M, m->OC, m->ONB);
+    // two zero k-chunks past the end of every packed operand: the kernels
+    // load chunks kc + 1 and kc + 2 while multiplying chunk kc
+    bx.resize(bx.size() + 2 * (size_t)m->MB * kWave * 4, 0.f);
+    bh.resize(bh.size() + 2 * (size_t)m->MB * kWave * 4, 0.f);
+    pb.resize(pb.size() + 2 * (size_t)m->PNB * kWave * 4, 0.f);
+    kvb.resize(kvb.size() + 2 * (size_t)m->KVNB * kWave * 4, 0.f);
+    ob.resize(ob.size() + 2 * (size_t)m->ONB * kWave * 4, 0.f);
 
     float *wq_dev = nullptr;
     tgm_status_t st = TGM_OK;
@@ -648,8 +1030,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             hipFuncSetAttribute((const void *)k_node_proj,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)proj_lds(m)) != hipSuccess ||
-            hipFuncSetAttribute((const void *)k_attn, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                (int)attn_lds(m)) != hipSuccess) {
+            !attn_lds_opt_in((int)attn_lds(m))) {
             st = TGM_EINVAL;   // dimensions beyond the LDS of one workgroup
             break;
         }
@@ -693,32 +1074,61 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
         return TGM_EORDER;   // the slot still holds an uncommitted write set
     hipStream_t s = as_stream(stream);
     if (cap > 0) {
-        const int nw = waves_for(m->MB);
-        TGM_LAUNCH(k_gru, dim3(cdiv(cap, 16)), dim3(64 * nw), gru_lds(m), s, n_nodes, mem,
+        TGM_LAUNCH(k_gru, dim3(gru_grid(m, cap)), dim3(64 * kGruKS), gru_lds(m), s, n_nodes, mem,
                            mem_ts, mail, mail_ts, ver, m->gru_bx, m->gru_bh, m->gru_bias,
                            m->omega, m->beta, m->M, m->D_m, m->D_t, m->KXC, m->KHC, m->MB,
                            mem_new, new_mem_ts, st->win);
     }
     const int n_cand = 2 * b;
     const size_t base = (size_t)(iter % slots) * st->ring_rows();
+    // the write set of iteration iter - s is committed by this launch when it
+    // is the next one due (s = 0: the current write set goes to the tables)
+    const bool direct = st->s == 0;
+    const int64_t cj = iter - st->s;
+    const tgm_state::Slot &cs = st->ring[((cj % slots) + slots) % slots];
+    const bool fuse = !direct && cj >= 0 && cj == st->committed_through + 1 && cs.staged &&
+                      cs.iter == cj;
+    const int n_commit = fuse ? 2 * cs.b : 0;
     if (n_cand > 0) {
         TGM_LAUNCH(k_latest, dim3(cdiv(n_cand, 256)), dim3(256), 0, s, n_cand, n_nodes,
-                           src_pos, dst_pos, st->win);
-        TGM_LAUNCH(k_stage, dim3(cdiv(n_cand, 4)), dim3(256), 0, s, n_cand, n_nodes,
-                           first_event,
-                           m->M, m->D_m, m->D_e, g->src, g->dst, g->t, g->efeat, src_pos, dst_pos,
-                           st->win, mem_new, ver, mem_ts, mail_ts, st->r_flag + base,
-                           st->r_node + base, st->r_mem + base * st->M, st->r_mem_ts + base,
-                           st->r_mail + base * st->D_m, st->r_mail_ts + base);
+                   src_pos, dst_pos, st->win);
+    }
+    if (n_cand + n_commit > 0) {
+        const size_t cbase = (size_t)(((cj % slots) + slots) % slots) * st->ring_rows();
+        StageArgs a;
+        a.n_cand = n_cand; a.n_commit = n_commit;
+        a.first = first_event; a.iter = iter; a.c_iter = cj;
+        a.M = m->M; a.D_m = m->D_m; a.D_e = m->D_e; a.direct = direct;
+        a.n_nodes = n_nodes; a.src = g->src; a.dst = g->dst; a.src_pos = src_pos;
+        a.dst_pos = dst_pos; a.win = st->win; a.ver = ver;
+        a.t = g->t; a.mem_ts = mem_ts; a.mail_ts = mail_ts; a.efeat = g->efeat;
+        a.mem_new = mem_new;
+        a.r_flag = st->r_flag + base; a.r_node = st->r_node + base;
+        a.r_mem = st->r_mem + base * st->M; a.r_mail = st->r_mail + base * st->D_m;
+        a.r_mem_ts = st->r_mem_ts + base; a.r_mail_ts = st->r_mail_ts + base;
+        a.c_flag = st->r_flag + cbase; a.c_node = st->r_node + cbase;
+        a.c_mem = st->r_mem + cbase * st->M; a.c_mail = st->r_mail + cbase * st->D_m;
+        a.c_mem_ts = st->r_mem_ts + cbase; a.c_mail_ts = st->r_mail_ts + cbase;
+        a.mem = st->mem; a.mail = st->mail; a.t_mem_ts = st->mem_ts; a.t_mail_ts = st->mail_ts;
+        a.t_ver = st->ver;
+        TGM_LAUNCH(k_stage, dim3(cdiv(n_cand + n_commit, 4)), dim3(256), 0, s, a);
     }
     if (winner && cap > 0) {
         TGM_LAUNCH(k_winner_out, dim3(cdiv(cap, 256)), dim3(256), 0, s, n_nodes, cap,
                            first_event, st->win, winner);
     }
-    tgm_state::Slot &sl = st->ring[iter % slots];
-    sl.iter = iter;
-    sl.b = b;
-    sl.staged = true;
+    if (fuse) {
+        st->ring[cj % slots].staged = false;
+        st->committed_through = cj;
+    }
+    if (direct) {
+        st->committed_through = iter;
+    } else {
+        tgm_state::Slot &sl = st->ring[iter % slots];
+        sl.iter = iter;
+        sl.b = b;
+        sl.staged = true;
+    }
     st->staged_through = iter;
     return TGM_OK;
 }
@@ -738,8 +1148,12 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
     if (!root_pos || !root_ts || !nbr_pos || !eid || !nts || !cnt || !mem_new || !h || cap == 0)
         return TGM_EINVAL;
     hipStream_t s = as_stream(stream);
-    TGM_LAUNCH(k_node_proj, dim3(cdiv(cap, 16)), dim3(64 * waves_for(m->PNB)),
-                       proj_lds(m), s, n_nodes, mem_new, m->M, m->PC, m->proj_b, m->PNB, m->P);
+    // persistent grid: at most the tiles of the largest node set, at most two
+    // workgroups per CU; every wave owns up to three column blocks
+    const int proj_waves = std::max<int>(4, std::min<int>(kMaxWaves, (int)cdiv(m->PNB, 3)));
+    const int proj_grid = (int)std::min<int64_t>(cdiv(cap, 16), 512);
+    TGM_LAUNCH(k_node_proj, dim3(proj_grid), dim3(64 * proj_waves), proj_lds(m), s, n_nodes,
+               mem_new, m->M, m->PC, m->proj_b, m->PNB, m->P);
     AttnArgs a;
     a.R = R; a.nb = nb; a.RT = attn_roots(m, &a.RBa); a.M = m->M; a.H = m->H;
     a.E = g->E; a.n_nodes = n_nodes;
@@ -752,6 +1166,13 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
     a.b_k = m->b_k; a.b_v = m->b_v; a.c_q = m->c_q;
     a.out_b = m->out_b; a.OC = m->OC; a.ONB = m->ONB; a.b_o = m->b_o;
     a.mem_new = mem_new; a.h = h;
-    TGM_LAUNCH(k_attn, dim3(cdiv(R, a.RT)), dim3(64 * kMaxWaves), attn_lds(m), s, a);
+    const dim3 grid(cdiv(R, a.RT)), block(64 * kMaxWaves);
+    const size_t lds = attn_lds(m);
+    switch (a.RBa) {
+    case 3: TGM_LAUNCH(k_attn<3>, grid, block, lds, s, a); break;
+    case 4: TGM_LAUNCH(k_attn<4>, grid, block, lds, s, a); break;
+    case 5: TGM_LAUNCH(k_attn<5>, grid, block, lds, s, a); break;
+    default: return TGM_EINVAL;
+    }
     return TGM_OK;
 }

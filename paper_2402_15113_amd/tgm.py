@@ -19,7 +19,7 @@ TGM_OK, TGM_EINVAL, TGM_ERANGE, TGM_EORDER, TGM_ESIZE, TGM_EDEVICE, TGM_ENOMEM =
 
 # Every exported symbol of include/tgm.h
 SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_create",
-           "tgm_graph_destroy", "tgm_graph_info", "tgm_batch_roots", "tgm_sample",
+           "tgm_graph_destroy", "tgm_graph_info", "tgm_batch_roots", "tgm_sample", "tgm_sample_batch",
            "tgm_node_set", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
            "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
@@ -70,6 +70,7 @@ def lib():
             "tgm_graph_info": [V, P, P, P, P],
             "tgm_batch_roots": [V, I64, I32, P, P, V],
             "tgm_sample": [V, P, P, I32, I32, P, P, P, P, V],
+            "tgm_sample_batch": [V, I64, I32, I32, P, P, P, P, P, P, V],
             "tgm_node_set": [V, P, I32, P, I32, P, P, I32, P, P, V],
             "tgm_state_create": [I32, I32, I32, I32, I32, V, C.POINTER(V)],
             "tgm_state_destroy": [V],
@@ -176,6 +177,12 @@ def tgm_batch_roots(g, first_event, b, root, root_ts, stream=None):
 def tgm_sample(g, root, root_ts, R, nb, nbr, eid, nts, cnt, stream=None):
     _check("tgm_sample", lib().tgm_sample(g, _p(root), _p(root_ts), R, nb, _p(nbr), _p(eid),
                                           _p(nts), _p(cnt), _s(stream)))
+
+
+def tgm_sample_batch(g, first_event, b, nb, root, root_ts, nbr, eid, nts, cnt, stream=None):
+    _check("tgm_sample_batch", lib().tgm_sample_batch(g, first_event, b, nb, _p(root),
+                                                      _p(root_ts), _p(nbr), _p(eid), _p(nts),
+                                                      _p(cnt), _s(stream)))
 
 
 def tgm_node_set(g, root, R, nbr, nb, nodes, n_nodes, cap, root_pos, nbr_pos, stream=None):

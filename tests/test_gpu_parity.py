@@ -283,3 +283,90 @@ def test_graph_create_rejects_bad_content():
     with pytest.raises(tgm.TgmError) as ei:
         tgm.tgm_graph_create(4, src, dst, t, src, None)
     assert ei.value.code == tgm.TGM_ERANGE
+
+
+def test_sample_batch_equals_roots_then_sample():
+    """tgm_sample_batch == tgm_batch_roots followed by tgm_sample, bit for bit."""
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("lastfm", E=60_000)   # no edge features
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w)
+    dev = st.dev
+    for i in (0, 7, wl.n_iters - 1):
+        lo, hi = wl.batch(i)
+        b = hi - lo
+        R, nb = 3 * b, wl.nb
+        tgm.tgm_sample_batch(st.g, lo, b, nb, st.root, st.root_ts, st.nbr, st.eid, st.nts, st.cnt)
+        root2 = torch.empty(R, dtype=torch.int32, device=dev)
+        rts2 = torch.empty(R, dtype=torch.float64, device=dev)
+        nbr2 = torch.empty((R, nb), dtype=torch.int32, device=dev)
+        eid2 = torch.empty((R, nb), dtype=torch.int32, device=dev)
+        nts2 = torch.empty((R, nb), dtype=torch.float64, device=dev)
+        cnt2 = torch.empty(R, dtype=torch.int32, device=dev)
+        tgm.tgm_batch_roots(st.g, lo, b, root2, rts2)
+        tgm.tgm_sample(st.g, root2, rts2, R, nb, nbr2, eid2, nts2, cnt2)
+        torch.cuda.synchronize()
+        for a, c in ((st.root[:R], root2), (st.root_ts[:R], rts2), (st.nbr[:R], nbr2),
+                     (st.eid[:R], eid2), (st.nts[:R], nts2), (st.cnt[:R], cnt2)):
+            assert torch.equal(a, c)
+    st.close()
+
+
+@pytest.mark.parametrize("s", [1, 3])
+def test_fetch_ahead_order(orc, s):
+    """With s >= 1 the fetch of iteration i+1 may be issued before the update of
+    iteration i (the prefetch that staleness allows); results are unchanged."""
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=4000, s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w)
+    o = orc.Oracle(wl, w)
+    bufs = []
+    dev = st.dev
+    for i in range(wl.n_iters):
+        # iteration i: sample + node set + fetch into its own buffers
+        lo, hi = wl.batch(i)
+        b = hi - lo
+        R, nb, cap = 3 * b, wl.nb, st.cap
+        z = lambda shape, dt: torch.zeros(shape, dtype=dt, device=dev)
+        B = dict(root=z(R, torch.int32), rts=z(R, torch.float64), nbr=z((R, nb), torch.int32),
+                 eid=z((R, nb), torch.int32), nts=z((R, nb), torch.float64),
+                 cnt=z(R, torch.int32), nodes=z(cap, torch.int32), n=z(1, torch.int32),
+                 rpos=z(R, torch.int32), npos=z((R, nb), torch.int32),
+                 mem=z((cap, wl.M), torch.float32), mts=z(cap, torch.float64),
+                 mail=z((cap, wl.D_m), torch.float32), lts=z(cap, torch.float64),
+                 ver=z(cap, torch.int32), new=z((cap, wl.M), torch.float32),
+                 h=z((R, wl.M), torch.float32), lo=lo, b=b)
+        tgm.tgm_sample_batch(st.g, lo, b, nb, B["root"], B["rts"], B["nbr"], B["eid"], B["nts"],
+                             B["cnt"])
+        tgm.tgm_node_set(st.g, B["root"], R, B["nbr"], nb, B["nodes"], B["n"], cap, B["rpos"],
+                         B["npos"])
+        tgm.tgm_fetch_memory(st.st, i, B["nodes"], B["n"], cap, B["mem"], B["mts"], B["mail"],
+                             B["lts"], B["ver"])
+        bufs.append(B)
+        if i >= 1:   # the update of the previous iteration, after this fetch
+            j = i - 1
+            P = bufs[j]
+            tgm.tgm_update_memory(st.st, st.m, st.g, j, P["nodes"], P["n"], cap, P["mem"],
+                                  P["mts"], P["mail"], P["lts"], P["ver"], P["lo"], P["b"],
+                                  P["rpos"][:P["b"]], P["rpos"][P["b"]:2 * P["b"]], P["new"])
+            tgm.tgm_embed(st.m, st.g, 3 * P["b"], nb, P["rpos"], P["rts"], P["npos"], P["eid"],
+                          P["nts"], P["cnt"], P["new"], P["n"], cap, P["h"])
+            r = o.step()
+            torch.cuda.synchronize()
+            n = int(P["n"].item())
+            exact("f_ver", P["ver"][:n].cpu().numpy(), r.f_ver)
+            close("h", P["h"][:3 * P["b"]].cpu().numpy(), r.h)
+            bufs[j] = None
+    j = wl.n_iters - 1
+    P = bufs[j]
+    tgm.tgm_update_memory(st.st, st.m, st.g, j, P["nodes"], P["n"], st.cap, P["mem"], P["mts"],
+                          P["mail"], P["lts"], P["ver"], P["lo"], P["b"], P["rpos"][:P["b"]],
+                          P["rpos"][P["b"]:2 * P["b"]], P["new"])
+    o.step()
+    st.flush()
+    o.flush()
+    compare_state(st.state(), o.state())
+    st.close()
