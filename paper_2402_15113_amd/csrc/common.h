@@ -76,6 +76,8 @@ struct tgm_graph {
     int64_t *off = nullptr;           // [N + 1]
     tgm::AdjRec *adj = nullptr;       // [n_adj]
     int64_t n_adj = 0;
+    int32_t *ns_stamp = nullptr;      // [N] node-set epoch stamps (scratch of tgm_node_set)
+    int32_t ns_epoch = 0;             // epoch of the last tgm_node_set call
 };
 
 struct tgm_state {
@@ -118,7 +120,7 @@ struct tgm_model {
     // attention: per-slot part [efeat || phi] -> [K | V]
     int32_t KFC = 0, KVNB = 0;           // chunks of D_e + D_t, 16-col blocks of 2M
     tgm::f4 *kv_b = nullptr;
-    float *b_k = nullptr, *b_v = nullptr, *c_q = nullptr;   // [M] each
+    float *pbias = nullptr;   // [PNB*16] bias of the node projection: c_q | b_k | b_v | 0
     // output projection
     int32_t OC = 0, ONB = 0;             // chunks of 2M, 16-col blocks of M
     tgm::f4 *out_b = nullptr;
@@ -271,12 +273,15 @@ __device__ __forceinline__ void stage_rows_w(float *__restrict__ lds, int lds_st
 // Rows staged by one wavefront: up to RMAX rows of n floats, lanes across the
 // columns in W-float vectors (n <= 64 * W * CMAX).  load() issues every load
 // of the wave's rows at once (no per-element index division); store() writes
-// them to LDS.  Rows with off < 0, and columns past n, are zero.
+// them to LDS.  Rows with off < 0, and columns past n, are zero.  src must
+// hold at least W elements (the dead lanes read its first vector).
 template <int W, int RMAX, int CMAX>
 struct WaveRows {
     typedef typename VecOf<W>::T V;
     V v[RMAX][CMAX];
 
+    // Branch-free: a dead lane reads src[0], and the value is only masked in
+    // store(), so no load is waited for before the first store.
     __device__ __forceinline__ void load(const float *__restrict__ src, const int64_t (&off)[RMAX],
                                          int n, int lane)
     {
@@ -286,15 +291,16 @@ struct WaveRows {
 #pragma unroll
             for (int c = 0; c < CMAX; ++c) {
                 const int cc = lane + kWave * c;
-                v[i][c] = (off[i] >= 0 && cc < nv)
-                              ? *reinterpret_cast<const V *>(src + off[i] + (int64_t)cc * W)
-                              : V(0);
+                const bool ok = off[i] >= 0 && cc < nv;
+                v[i][c] = *reinterpret_cast<const V *>(src + (ok ? off[i] + (int64_t)cc * W : 0));
             }
     }
 
-    // row i goes to LDS row lrow[i] (skipped when lrow[i] < 0)
+    // row i goes to LDS row lrow[i] (skipped when lrow[i] < 0); off must be the
+    // offsets given to load()
     __device__ __forceinline__ void store(float *__restrict__ lds, int stride, int col0,
-                                          const int (&lrow)[RMAX], int n, int lane) const
+                                          const int (&lrow)[RMAX], const int64_t (&off)[RMAX],
+                                          int n, int lane) const
     {
         const int nv = n / W;
 #pragma unroll
@@ -303,7 +309,8 @@ struct WaveRows {
             for (int c = 0; c < CMAX; ++c) {
                 const int cc = lane + kWave * c;
                 if (lrow[i] >= 0 && cc < nv)
-                    *reinterpret_cast<V *>(lds + lrow[i] * stride + col0 + cc * W) = v[i][c];
+                    *reinterpret_cast<V *>(lds + lrow[i] * stride + col0 + cc * W) =
+                        off[i] >= 0 ? v[i][c] : V(0);
             }
     }
 };

@@ -186,97 +186,138 @@ __global__ __launch_bounds__(256) void k_sample_batch(
 }
 
 // ------------------------------------------------------------ node set
-// One workgroup: marks roots and neighbours in an LDS bitmap over node ids,
-// scans the word popcounts to number the set bits in id order (which sorts
-// and deduplicates in one pass), then maps every root and neighbour to its
-// position.
-constexpr int kNsThreads = 1024;
-constexpr int kNsMaxWords = 1 << 14;   // 2^19 node ids
-constexpr int kNsBatch = 24;   // ids each thread has in flight
+// Two launches.  k_ns_mark stamps every valid root and neighbour id into the
+// graph's per-node stamp array with this call's epoch (plain stores: all
+// writers of one id write the same value, so no atomics and no clearing).
+// In k_ns_pos every workgroup turns the stamps into a membership bitmap
+// (one ballot per 64 ids), scans its word popcounts (which numbers the
+// members in id order: sorted and deduplicated in one pass), writes its share
+// of U and maps its slice of roots and neighbours to their positions.  The
+// bitmap is rebuilt per workgroup because it is small (N/8 bytes) and L2-hot;
+// that replaces a grid-wide barrier.
+constexpr int kNsThreads = 256;
+constexpr int kNsWaves = kNsThreads / kWave;
+constexpr int kNsIds = 8;                          // ids per thread in k_ns_pos
+constexpr int kNsIdsPerBlock = kNsThreads * kNsIds;
+constexpr int kNsMaxWords = 1 << 13;               // 2^19 node ids
 
-__global__ __launch_bounds__(kNsThreads) void k_node_set(
-    int32_t N, const int32_t *__restrict__ root, int32_t R, const int32_t *__restrict__ nbr,
-    int32_t Rnb, int32_t *__restrict__ nodes, int32_t *__restrict__ n_nodes,
-    int32_t *__restrict__ root_pos, int32_t *__restrict__ nbr_pos)
+__global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ p, int32_t n, int32_t v)
 {
-    extern __shared__ uint32_t ns_lds[];
-    const int W = (N + 31) >> 5;
-    uint32_t *bits = ns_lds;          // [W]
-    uint32_t *pre = ns_lds + W;       // [W] exclusive prefix of popcounts
-    __shared__ uint32_t part[kNsThreads];
-    const int tid = threadIdx.x;
+    const int k = blockIdx.x * 256 + threadIdx.x;
+    if (k < n)
+        p[k] = v;
+}
 
-    for (int k = tid; k < W; k += kNsThreads)
-        bits[k] = 0u;
-    __syncthreads();
-    // ids outside [0, N) are not members; they map to position -1.  Each
-    // thread loads kNsBatch ids before marking them, so the loads overlap.
-    const int total = R + Rnb;
-    for (int base = tid; base < total; base += kNsThreads * kNsBatch) {
-        int32_t v[kNsBatch];
+__global__ __launch_bounds__(256) void k_ns_mark(int32_t N, const int32_t *__restrict__ root,
+                                                 int32_t R, const int32_t *__restrict__ nbr,
+                                                 int32_t total, int32_t *__restrict__ stamp,
+                                                 int32_t epoch)
+{
+    const int k = blockIdx.x * 256 + threadIdx.x;
+    if (k >= total)
+        return;
+    const int32_t x = k < R ? root[k] : nbr[k - R];
+    if (x >= 0 && x < N)
+        stamp[x] = epoch;
+}
+
+__global__ __launch_bounds__(kNsThreads) void k_ns_pos(
+    int32_t N, const int32_t *__restrict__ stamp, int32_t epoch,
+    const int32_t *__restrict__ root, int32_t R, const int32_t *__restrict__ nbr, int32_t total,
+    int32_t *__restrict__ nodes, int32_t *__restrict__ n_nodes, int32_t *__restrict__ root_pos,
+    int32_t *__restrict__ nbr_pos)
+{
+    extern __shared__ uint64_t ns_mask[];                 // [NW] membership words
+    const int NW = (N + 63) >> 6;
+    uint32_t *pre = reinterpret_cast<uint32_t *>(ns_mask + NW);   // [NW] exclusive prefix
+    __shared__ uint32_t wave_tot[kNsWaves];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // this workgroup's ids, loaded first so their latency hides behind the scan
+    const int k0 = blockIdx.x * kNsIdsPerBlock + tid;
+    int32_t x[kNsIds];
 #pragma unroll
-        for (int u = 0; u < kNsBatch; ++u) {
-            const int k = base + u * kNsThreads;
-            v[u] = k < R ? root[k] : (k < total ? nbr[k - R] : -1);
+    for (int u = 0; u < kNsIds; ++u) {
+        const int k = k0 + u * kNsThreads;
+        x[u] = k < R ? root[k] : (k < total ? nbr[k - R] : -1);
+    }
+
+    // 1. membership words, four 64-id loads in flight per wave
+    for (int w0 = wave; w0 < NW; w0 += 4 * kNsWaves) {
+        int32_t f[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int id = (w0 + u * kNsWaves) * kWave + lane;
+            f[u] = id < N ? stamp[id] : 0;
         }
 #pragma unroll
-        for (int u = 0; u < kNsBatch; ++u)
-            if (v[u] >= 0 && v[u] < N)
-                atomicOr(&bits[v[u] >> 5], 1u << (v[u] & 31));
+        for (int u = 0; u < 4; ++u) {
+            const int w = w0 + u * kNsWaves;
+            const uint64_t m = __ballot(f[u] == epoch);
+            if (w < NW && lane == 0)
+                ns_mask[w] = m;
+        }
     }
     __syncthreads();
 
-    // contiguous word ranges per thread, then a block scan of the range sums
-    const int per = (W + kNsThreads - 1) / kNsThreads;
-    const int w0 = tid * per, w1 = min(W, w0 + per);
+    // 2. exclusive prefix of the word popcounts: contiguous word ranges per
+    // thread, a shuffle scan per wave, then the wave totals
+    const int per = (NW + kNsThreads - 1) / kNsThreads;
+    const int wa = min(NW, tid * per), wz = min(NW, wa + per);
     uint32_t sum = 0;
-    for (int k = w0; k < w1; ++k)
-        sum += __popc(bits[k]);
-    part[tid] = sum;
+    for (int w = wa; w < wz; ++w)
+        sum += (uint32_t)__popcll(ns_mask[w]);
+    uint32_t inc = sum;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o, kWave);
+        if (lane >= o)
+            inc += y;
+    }
+    if (lane == kWave - 1)
+        wave_tot[wave] = inc;
     __syncthreads();
-    for (int o = 1; o < kNsThreads; o <<= 1) {
-        const uint32_t x = tid >= o ? part[tid - o] : 0u;
-        __syncthreads();
-        part[tid] += x;
-        __syncthreads();
+    uint32_t before = 0, all = 0;
+#pragma unroll
+    for (int v = 0; v < kNsWaves; ++v) {
+        const uint32_t t = wave_tot[v];
+        before += v < wave ? t : 0u;
+        all += t;
     }
-    uint32_t run = part[tid] - sum;   // exclusive
-    for (int k = w0; k < w1; ++k) {
-        pre[k] = run;
-        uint32_t m = bits[k];
-        uint32_t p = run;
-        while (m) {
-            const int b = __ffs(m) - 1;
-            nodes[p++] = (k << 5) + b;
-            m &= m - 1;
-        }
-        run = p;
+    uint32_t run = before + inc - sum;
+    for (int w = wa; w < wz; ++w) {
+        pre[w] = run;
+        run += (uint32_t)__popcll(ns_mask[w]);
     }
-    if (tid == kNsThreads - 1)
-        *n_nodes = (int32_t)part[kNsThreads - 1];
     __syncthreads();
 
-    for (int base = tid; base < total; base += kNsThreads * kNsBatch) {
-        int32_t v[kNsBatch];
+    // 3. this workgroup's share of U: one wave per membership word
+    for (int w = blockIdx.x * kNsWaves + wave; w < NW; w += gridDim.x * kNsWaves) {
+        const uint64_t m = ns_mask[w];
+        if ((m >> lane) & 1ull)
+            nodes[pre[w] + (uint32_t)__popcll(m & ((1ull << lane) - 1ull))] = w * kWave + lane;
+    }
+    if (blockIdx.x == 0 && tid == 0)
+        *n_nodes = (int32_t)all;
+
+    // 4. positions of this workgroup's roots and neighbours (-1 for ids
+    // outside [0, N), which are not members)
 #pragma unroll
-        for (int u = 0; u < kNsBatch; ++u) {
-            const int k = base + u * kNsThreads;
-            v[u] = k < R ? root[k] : (k < total ? nbr[k - R] : -1);
-        }
-#pragma unroll
-        for (int u = 0; u < kNsBatch; ++u) {
-            const int k = base + u * kNsThreads;
-            if (k < total) {
-                const int32_t x = v[u];
-                const int32_t q = (x < 0 || x >= N)
-                                      ? -1
-                                      : (int32_t)(pre[x >> 5] +
-                                                  __popc(bits[x >> 5] & ((1u << (x & 31)) - 1u)));
-                if (k < R)
-                    root_pos[k] = q;
-                else
-                    nbr_pos[k - R] = q;
+    for (int u = 0; u < kNsIds; ++u) {
+        const int k = k0 + u * kNsThreads;
+        if (k < total) {
+            const int32_t v = x[u];
+            int32_t q = -1;
+            if (v >= 0 && v < N) {
+                const int w = v >> 6;
+                q = (int32_t)(pre[w] +
+                              (uint32_t)__popcll(ns_mask[w] & ((1ull << (v & 63)) - 1ull)));
             }
+            if (k < R)
+                root_pos[k] = q;
+            else
+                nbr_pos[k - R] = q;
         }
     }
 }
@@ -319,6 +360,8 @@ extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *sr
     do {
         if (hipMalloc(&g->off, sizeof(int64_t) * (N + 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
         if (hipMalloc(&bad, sizeof(int32_t) * 2) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (hipMalloc(&g->ns_stamp, sizeof(int32_t) * N) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (hipMemsetAsync(g->ns_stamp, 0, sizeof(int32_t) * N, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         if (hipMemsetAsync(bad, 0, sizeof(int32_t) * 2, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         if (E == 0) {
             if (hipMemsetAsync(g->off, 0, sizeof(int64_t) * (N + 1), s) != hipSuccess) { fail(TGM_EDEVICE); break; }
@@ -380,6 +423,7 @@ extern "C" tgm_status_t tgm_graph_destroy(tgm_graph_t g)
         return TGM_EINVAL;
     hipFree(g->off);
     hipFree(g->adj);
+    hipFree(g->ns_stamp);
     delete g;
     return TGM_OK;
 }
@@ -449,25 +493,35 @@ extern "C" tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t
                                      int32_t *n_nodes, int32_t cap, int32_t *root_pos,
                                      int32_t *nbr_pos, void *stream)
 {
-    if (!g || R < 0 || nb < 0 || !n_nodes)
+    if (!g || R < 0 || nb < 0 || !n_nodes || (int64_t)R * (nb + 1) > INT32_MAX)
         return TGM_EINVAL;
     const int64_t need = std::min<int64_t>(g->N, (int64_t)R * (nb + 1));
     if (cap < need)
         return TGM_ESIZE;
     if ((R > 0 && (!root || !nodes || !root_pos)) || ((int64_t)R * nb > 0 && (!nbr || !nbr_pos)))
         return TGM_EINVAL;
-    const int W = (g->N + 31) >> 5;
-    if (W > kNsMaxWords)
+    const int NW = (g->N + 63) >> 6;
+    if (NW > kNsMaxWords)
         return TGM_EINVAL;
-    const size_t lds = sizeof(uint32_t) * 2 * W;
+    const size_t lds = (sizeof(uint64_t) + sizeof(uint32_t)) * NW;
     static bool lds_opt_in = false;
     if (!lds_opt_in) {
-        TGM_HIP(hipFuncSetAttribute((const void *)k_node_set,
+        TGM_HIP(hipFuncSetAttribute((const void *)k_ns_pos,
                                     hipFuncAttributeMaxDynamicSharedMemorySize,
-                                    (int)(sizeof(uint32_t) * 2 * kNsMaxWords)));
+                                    (int)((sizeof(uint64_t) + sizeof(uint32_t)) * kNsMaxWords)));
         lds_opt_in = true;
     }
-    TGM_LAUNCH(k_node_set, dim3(1), dim3(kNsThreads), lds, as_stream(stream), g->N, root,
-                       R, nbr, R * nb, nodes, n_nodes, root_pos, nbr_pos);
+    hipStream_t s = as_stream(stream);
+    if (g->ns_epoch == INT32_MAX) {   // stamps restart from zero
+        TGM_LAUNCH(k_fill_i32, dim3(cdiv(g->N, 256)), dim3(256), 0, s, g->ns_stamp, g->N, 0);
+        g->ns_epoch = 0;
+    }
+    const int32_t epoch = ++g->ns_epoch;
+    const int32_t total = (int32_t)((int64_t)R * (nb + 1));
+    if (total > 0)
+        TGM_LAUNCH(k_ns_mark, dim3(cdiv(total, 256)), dim3(256), 0, s, g->N, root, R, nbr, total,
+                   g->ns_stamp, epoch);
+    TGM_LAUNCH(k_ns_pos, dim3((unsigned)std::max<int64_t>(1, cdiv(total, kNsIdsPerBlock))), dim3(kNsThreads), lds, s,
+               g->N, g->ns_stamp, epoch, root, R, nbr, total, nodes, n_nodes, root_pos, nbr_pos);
     return TGM_OK;
 }

@@ -129,57 +129,67 @@ __global__ __launch_bounds__(64 * kGruKS) void k_gru(
         __syncthreads();   // the previous tile is done with LDS
         {
             // wave w stages rows w, w + 4, w + 8, w + 12 of the tile: one round of
-            // loads for their versions, times, mail and memory
+            // loads for their versions, times, mail and memory (branch-free: rows
+            // past the node set read the tile's first row and drop it); the time
+            // codes are computed while the rows are in flight
             int64_t offm[4], offh[4];
-            int lr[4], vr[4];
-            double mts[4], lts[4];
+            int lr[4];
+            bool has[4];
+            double dts[4], nts_[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int r = wave + 4 * i;
-                const int p = row0 + r;
                 const bool live = r < nvalid;
+                const int p = row0 + (live ? r : 0);
+                const int v = ver[p];
+                const double mt = mem_ts[p], lt = mail_ts[p];
                 lr[i] = r;
-                vr[i] = live ? ver[p] : -1;
-                mts[i] = live ? mem_ts[p] : 0.0;
-                lts[i] = live ? mail_ts[p] : 0.0;
+                has[i] = live && v >= 0;
+                dts[i] = lt - mt;
+                nts_[i] = has[i] ? lt : mt;
                 offm[i] = live ? (int64_t)p * D_m : -1;
                 offh[i] = live ? (int64_t)p * M : -1;
             }
+            auto finish_rows = [&]() {
+                for (int d = lane; d < D_t; d += kWave) {
+                    const double om = s_om[d], be = s_be[d];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        lds[lr[i] * SA + D_m + d] = has[i] ? time_enc(om, be, dts[i]) : 0.f;
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float *row = lds + lr[i] * SA;
+                    for (int k = lane; k < padx; k += kWave)
+                        row[D_m + D_t + k] = 0.f;
+                    for (int k = lane; k < padh; k += kWave)
+                        row[KX + M + k] = 0.f;
+                    if (lane == 0) {
+                        s_has[lr[i]] = has[i];
+                        if (hb == 0 && lr[i] < nvalid) {
+                            win[row0 + lr[i]] = -1;
+                            if (new_mem_ts)
+                                new_mem_ts[row0 + lr[i]] = nts_[i];
+                        }
+                    }
+                }
+            };
             if (al) {
                 WaveRows<4, 4, 2> xm;
                 WaveRows<4, 4, 1> xh;
                 xm.load(mail, offm, D_m, lane);
                 xh.load(mem, offh, M, lane);
-                xm.store(lds, SA, 0, lr, D_m, lane);
-                xh.store(lds, SA, KX, lr, M, lane);
+                finish_rows();
+                xm.store(lds, SA, 0, lr, offm, D_m, lane);
+                xh.store(lds, SA, KX, lr, offh, M, lane);
             } else {
                 WaveRows<1, 4, 8> xm;
                 WaveRows<1, 4, 2> xh;
                 xm.load(mail, offm, D_m, lane);
                 xh.load(mem, offh, M, lane);
-                xm.store(lds, SA, 0, lr, D_m, lane);
-                xh.store(lds, SA, KX, lr, M, lane);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = lr[i];
-                const bool has = vr[i] >= 0;
-                const double dt = lts[i] - mts[i];
-                float *row = lds + r * SA;
-                for (int d = lane; d < D_t; d += kWave)
-                    row[D_m + d] = has ? time_enc(s_om[d], s_be[d], dt) : 0.f;
-                for (int k = lane; k < padx; k += kWave)
-                    row[D_m + D_t + k] = 0.f;
-                for (int k = lane; k < padh; k += kWave)
-                    row[KX + M + k] = 0.f;
-                if (lane == 0) {
-                    s_has[r] = has;
-                    if (hb == 0 && r < nvalid) {
-                        win[row0 + r] = -1;
-                        if (new_mem_ts)
-                            new_mem_ts[row0 + r] = has ? lts[i] : mts[i];
-                    }
-                }
+                finish_rows();
+                xm.store(lds, SA, 0, lr, offm, D_m, lane);
+                xh.store(lds, SA, KX, lr, offh, M, lane);
             }
         }
         __syncthreads();
@@ -363,6 +373,7 @@ __global__ void k_winner_out(const int32_t *__restrict__ n_nodes, int32_t cap, i
 __global__ __launch_bounds__(512) void k_node_proj(const int32_t *__restrict__ n_nodes,
                                                    const float *__restrict__ mem_new, int M,
                                                    int PC, const f4 *__restrict__ pb, int PNB,
+                                                   const float *__restrict__ pbias,
                                                    float *__restrict__ P)
 {
     // persistent over 16-row tiles (launched with 4..8 waves); wave w owns
@@ -395,11 +406,11 @@ __global__ __launch_bounds__(512) void k_node_proj(const int32_t *__restrict__ n
             if ((M & 3) == 0 && (reinterpret_cast<uintptr_t>(mem_new) & 15) == 0) {
                 WaveRows<4, 4, 1> x;
                 x.load(mem_new, off, M, lane);
-                x.store(lds, SA, 0, lr, M, lane);
+                x.store(lds, SA, 0, lr, off, M, lane);
             } else {
                 WaveRows<1, 4, 2> x;
                 x.load(mem_new, off, M, lane);
-                x.store(lds, SA, 0, lr, M, lane);
+                x.store(lds, SA, 0, lr, off, M, lane);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -440,14 +451,16 @@ __global__ __launch_bounds__(512) void k_node_proj(const int32_t *__restrict__ n
         }
         if (kc < PC)
             mma(kc, x0, x1, x2);
+        const float e0 = pbias[cb0 * 16 + (lane & 15)], e1 = pbias[cb1 * 16 + (lane & 15)],
+                    e2 = pbias[cb2 * 16 + (lane & 15)];
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int r = row0 + 4 * (lane >> 4) + v;
             if (r < n) {
                 float *out = P + (int64_t)r * ldP + (lane & 15);
-                out[cb0 * 16] = c0[v];
-                out[cb1 * 16] = c1[v];
-                out[cb2 * 16] = c2[v];
+                out[cb0 * 16] = c0[v] + e0;
+                out[cb1 * 16] = c1[v] + e1;
+                out[cb2 * 16] = c2[v] + e2;
             }
         }
     }
@@ -465,7 +478,7 @@ struct AttnArgs {
     const double *omega, *beta;
     const f4 *kv_b;
     int KFC, KVNB;
-    const float *b_k, *b_v, *c_q;
+    const float *pbias;   // c_q | b_k | b_v: the rows of P carry it already
     const f4 *out_b;
     int OC, ONB;
     const float *b_o;
@@ -489,6 +502,7 @@ struct AttnArgs {
 //     whose weights were fetched before step 4.
 constexpr int kAttMaxSlots = kAttMaxRB * 16;
 constexpr int kAttMaxOC = 16;   // 16-wide k-chunks of the output projection (2M <= 256)
+constexpr int kAttPre = 6;      // time-code k-chunks whose weights are preloaded
 
 template <int RB>   // 16-row slot blocks per workgroup (3..5)
 __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
@@ -497,6 +511,9 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
     __shared__ int s_np[kAttMaxSlots];         // neighbour's node-set position, -1 if none
     __shared__ int64_t s_qoff[kAttMaxSlots], s_voff[kAttMaxSlots];
     __shared__ int s_cnt[kAttMaxSlots];
+    __shared__ int64_t s_eoff[kAttMaxSlots];   // edge-feature row offset, -1 if none
+    __shared__ double s_dt[kAttMaxSlots];      // t_root - t_slot
+    __shared__ int s_ok[kAttMaxSlots];         // slot holds a sampled neighbour
     const int r0 = blockIdx.x * g.RT;
     const int nroots = min(g.RT, g.R - r0);
     if (nroots <= 0)
@@ -519,13 +536,33 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
 
-    // 1. metadata of the roots and the time-encoding constants
+    // 1. metadata of the roots and of the slots (one round of loads, issued
+    // together), and the time-encoding constants
     for (int r = tid; r < ORB * 16; r += blockDim.x) {
         const int pv = r < nroots ? g.root_pos[r0 + r] : -1;
         const bool ok = pv >= 0 && pv < n;
         s_qoff[r] = ok ? (int64_t)pv * g.ldP : -1;
         s_voff[r] = ok ? (int64_t)pv * M : -1;
         s_cnt[r] = r < nroots ? g.cnt[r0 + r] : 0;
+    }
+    for (int sr = tid; sr < RA; sr += blockDim.x) {
+        const int r = sr / nb, j = sr - r * nb;
+        int c = 0, q = -1;
+        int64_t e = -1;
+        double t_root = 0.0, t_slot = 0.0;
+        if (r < nroots) {
+            const int64_t sl = (int64_t)(r0 + r) * nb + j;
+            c = g.cnt[r0 + r];
+            e = g.eid[sl];
+            q = g.nbr_pos[sl];
+            t_root = g.root_ts[r0 + r];
+            t_slot = g.nts[sl];
+        }
+        const bool ok = j < c;
+        s_ok[sr] = ok;
+        s_dt[sr] = t_root - t_slot;
+        s_eoff[sr] = (ok && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
+        s_np[sr] = (ok && q >= 0 && q < n) ? q : -1;
     }
     for (int d = tid; d < D_t; d += blockDim.x) {
         s_om[d] = g.omega[d];
@@ -540,146 +577,101 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
     const int cb0 = wave, cb1 = wave + nw < g.KVNB ? wave + nw : wave;
     const bool has_tiles = cb0 < g.KVNB;
 
-    // 2. rows: query and s'_v (small, loaded first), slot features, time codes
-    const bool qv4 = (M & 3) == 0;
-    f4 qreg[2], vreg[2];
-    const int nq4 = qv4 ? nroots * (M >> 2) : 0, nv4 = qv4 ? ORB * 16 * (M >> 2) : 0;
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int i = tid + u * blockDim.x;
-        qreg[u] = f4{0, 0, 0, 0};
-        vreg[u] = f4{0, 0, 0, 0};
-        if (i < nq4) {
-            const int r = i / (M >> 2), c = i - r * (M >> 2);
-            if (s_qoff[r] >= 0)
-                qreg[u] = *reinterpret_cast<const f4 *>(g.P + s_qoff[r] + 4 * c);
-        }
-        if (i < nv4) {
-            const int r = i / (M >> 2), c = i - r * (M >> 2);
-            if (s_voff[r] >= 0)
-                vreg[u] = *reinterpret_cast<const f4 *>(g.mem_new + s_voff[r] + 4 * c);
-        }
-    }
-    {
-        // wave w stages slot rows sr = w + nw i: their metadata (uniform loads),
-        // edge-feature rows and time codes, in one round of loads
-        constexpr int RPW = 2 * RB;   // rows per wave: RB * 16 / kMaxWaves
-        int64_t eoff[RPW];
-        int lr[RPW], npos[RPW], valid[RPW];
-        double dts[RPW];
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            const int sr = wave + nw * i;
-            const int r = sr / nb, j = sr - r * nb;
-            lr[i] = sr;
-            valid[i] = 0;
-            eoff[i] = -1;
-            npos[i] = -1;
-            dts[i] = 0.0;
-            if (r < nroots) {
-                const int64_t sl = (int64_t)(r0 + r) * nb + j;
-                const int c = g.cnt[r0 + r];
-                const int64_t e = g.eid[sl];
-                const int q = g.nbr_pos[sl];
-                dts[i] = g.root_ts[r0 + r] - g.nts[sl];
-                valid[i] = j < c;
-                eoff[i] = (valid[i] && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
-                npos[i] = (valid[i] && q >= 0 && q < n) ? q : -1;
-            }
-        }
-        const uintptr_t ea = reinterpret_cast<uintptr_t>(g.efeat);
-        if (D_e > 0) {
-            if ((ea & 15) == 0 && (D_e & 3) == 0) {
-                WaveRows<4, RPW, 1> xf;
-                xf.load(g.efeat, eoff, D_e, lane);
-                xf.store(A, SA, 0, lr, D_e, lane);
-            } else if ((ea & 7) == 0 && (D_e & 1) == 0) {
-                WaveRows<2, RPW, 2> xf;
-                xf.load(g.efeat, eoff, D_e, lane);
-                xf.store(A, SA, 0, lr, D_e, lane);
-            } else {
-                WaveRows<1, RPW, 4> xf;
-                xf.load(g.efeat, eoff, D_e, lane);
-                xf.store(A, SA, 0, lr, D_e, lane);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            float *row = A + lr[i] * SA;
-            for (int d = lane; d < D_t; d += kWave)
-                row[D_e + d] = valid[i] ? time_enc(s_om[d], s_be[d], dts[i]) : 0.f;
-            for (int k = D_e + D_t + lane; k < KF; k += kWave)
-                row[k] = 0.f;
-            if (lane == 0)
-                s_np[lr[i]] = npos[i];
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int i = tid + u * blockDim.x;
-        if (i < nq4) {
-            const int r = i / (M >> 2), c = i - r * (M >> 2);
-            *reinterpret_cast<f4 *>(Q + r * M + 4 * c) = qreg[u];
-        }
-        if (i < nv4) {
-            const int r = i / (M >> 2), c = i - r * (M >> 2);
-            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) = vreg[u];
-        }
-    }
-    if (qv4) {   // rows past the first 2 * blockDim vectors
-        for (int i = tid + 2 * blockDim.x; i < max(nq4, nv4); i += blockDim.x) {
-            const int r = i / (M >> 2), c = i - r * (M >> 2);
-            if (i < nq4)
-                *reinterpret_cast<f4 *>(Q + r * M + 4 * c) =
-                    s_qoff[r] >= 0 ? *reinterpret_cast<const f4 *>(g.P + s_qoff[r] + 4 * c)
-                                   : f4{0, 0, 0, 0};
-            if (i < nv4)
-                *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
-                    s_voff[r] >= 0 ? *reinterpret_cast<const f4 *>(g.mem_new + s_voff[r] + 4 * c)
-                                   : f4{0, 0, 0, 0};
-        }
-    } else {     // scalar path for M % 4 != 0
-        for (int i = tid; i < ORB * 16 * M; i += blockDim.x) {
-            const int r = i / M, k = i - r * M;
-            if (r < nroots)
-                Q[r * M + k] = s_qoff[r] >= 0 ? g.P[s_qoff[r] + k] : 0.f;
-            AO[r * SAO + M + k] = s_voff[r] >= 0 ? g.mem_new[s_voff[r] + k] : 0.f;
-        }
-    }
-    {
-        // AO: columns [0, M) of rows without a root and the padding [2M, ..)
-        const int w2 = g.OC * 16 - M;
-        for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
-            const int r = idx / w2, c = idx - r * w2;
-            if (c >= M || r >= nroots)
-                AO[r * SAO + (c < M ? c : M + c)] = 0.f;
-        }
-    }
-    __syncthreads();
-    for (int idx = tid; idx < nroots * M; idx += blockDim.x)
-        Q[idx] += g.c_q[idx % M];
-
-    // 3. per-slot K|V GEMM; the accumulators start as P[nbr][M + col] + bias
-    f4 acc[2][RB];
-    const float *arow = A + (lane & 15) * SA + 4 * (lane >> 4);
+    // 2. every load of the slot rows, in the order it is consumed (a wave's
+    // loads complete in issue order): the weights of the chunks made of time
+    // codes only, the edge-feature rows, the accumulator seeds P[nbr][M + col];
+    // the time codes are computed while they are in flight
+    const int P1 = min(D_t / 16, kAttPre);   // k-chunks of time codes only
     const int64_t kstep = (int64_t)g.KVNB * kWave;
-    if (has_tiles) {
+    const f4 *p0 = g.kv_b + (int64_t)(has_tiles ? cb0 : 0) * kWave + lane;
+    const int64_t o1 = (int64_t)(cb1 - cb0) * kWave;
+    f4 bpre[kAttPre][2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int col = (i ? cb1 : cb0) * 16 + (lane & 15);
-            const bool ok = col < 2 * M;
-            const float bias = ok ? (col < M ? g.b_k[col] : g.b_v[col - M]) : 0.f;
+    for (int kc = 0; kc < kAttPre; ++kc) {   // chunks past P1 are loaded and unused
+        bpre[kc][0] = p0[kc * kstep];
+        bpre[kc][1] = p0[kc * kstep + o1];
+    }
+    issue_fence();   // every weight load goes out before the row loads
+    // query rows (the node projection carries the folded bias c_q; a root
+    // without a position gets c_q alone) and s'_v rows: two vectors per thread
+    // now (branch-free), stored after the GEMM; the rest after the GEMM
+    const bool qv4 = (M & 3) == 0 && (reinterpret_cast<uintptr_t>(g.mem_new) & 15) == 0;
+    const int M4 = qv4 ? M >> 2 : 0, M4c = qv4 ? M >> 2 : 1;
+    const int nq4 = nroots * M4, nv4 = ORB * 16 * M4;
+    f4 qreg[2], vreg[2];
 #pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        const int rq = i < nq4 ? i / M4c : 0, cq = i < nq4 ? i - rq * M4c : 0;
+        const int rv = i < nv4 ? i / M4c : 0, cv = i < nv4 ? i - rv * M4c : 0;
+        const int64_t oq = s_qoff[rq], ov = s_voff[rv];
+        qreg[u] = *reinterpret_cast<const f4 *>(oq >= 0 && qv4 ? g.P + oq + 4 * cq
+                                                               : g.pbias + 4 * cq);
+        vreg[u] = *reinterpret_cast<const f4 *>(ov >= 0 && qv4 ? g.mem_new + ov + 4 * cv
+                                                               : g.mem_new);
+    }
+    // wave w stages slot rows w + kMaxWaves i (the launch has kMaxWaves waves)
+    constexpr int RPW = 2 * RB;   // RB * 16 / kMaxWaves
+    int64_t eoff[RPW];
+    int lr[RPW];
+    double dts[RPW];
+    bool oks[RPW];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int np = s_np[rb * 16 + 4 * (lane >> 4) + v];
-                    acc[i][rb][v] =
-                        bias + ((ok && np >= 0) ? g.P[(int64_t)np * g.ldP + M + col] : 0.f);
-                }
-        }
-        const f4 *p0 = g.kv_b + (int64_t)cb0 * kWave + lane;
-        const int64_t o1 = (int64_t)(cb1 - cb0) * kWave;
+    for (int i = 0; i < RPW; ++i) {
+        lr[i] = wave + kMaxWaves * i;
+        eoff[i] = s_eoff[lr[i]];
+        dts[i] = s_dt[lr[i]];
+        oks[i] = s_ok[lr[i]] != 0;
+    }
+    const bool vec_e = D_e > 0 && g.E > 0 && (reinterpret_cast<uintptr_t>(g.efeat) & 15) == 0 &&
+                       (D_e & 3) == 0 && (D_t & 3) == 0;
+    // issued on every path (the other paths read P[0] and drop it), so the
+    // waits below count the same loads on every path
+    int64_t eoffv[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i)
+        eoffv[i] = vec_e ? eoff[i] : -1;
+    WaveRows<4, RPW, 1> xf;
+    xf.load(vec_e ? g.efeat : g.P, eoffv, D_e, lane);
+    // seeds: the neighbour's row of P (node projection plus bias), or the bias
+    // alone for a slot without a neighbour; columns past 2M read column 0
+    f4 seed[2][RB];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int c = (i ? cb1 : cb0) * 16 + (lane & 15);
+        const int col = M + (c < 2 * M ? c : 0);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int np = s_np[rb * 16 + 4 * (lane >> 4) + v];
+                seed[i][rb][v] = *(np >= 0 ? g.P + (int64_t)np * g.ldP + col : g.pbias + col);
+            }
+    }
+    // time codes phi(t_root - t_slot) in columns [0, D_t) (the RPW rows of a
+    // column are independent chains) and the zero padding past D_t + D_e
+    for (int d = lane; d < D_t; d += kWave) {
+        const double om = s_om[d], be = s_be[d];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+            A[lr[i] * SA + d] = oks[i] ? time_enc(om, be, dts[i]) : 0.f;
+    }
+    for (int k = D_t + D_e + lane; k < KF; k += kWave)
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+            A[lr[i] * SA + k] = 0.f;
+    __syncthreads();
+
+    // 3. per-slot K|V GEMM over [phi || efeat]: first the time-code chunks
+    // (weights in registers, so no wait on the loads still in flight), then the
+    // edge-feature rows go to LDS and the remaining chunks stream their weights
+    f4 acc[2][RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        acc[0][rb] = f4{0, 0, 0, 0};
+        acc[1][rb] = f4{0, 0, 0, 0};
+    }
+    const float *arow = A + (lane & 15) * SA + 4 * (lane >> 4);
 // one k-chunk: the RB A fragments, then the MFMAs k-slice-major over the
 // 2 x RB independent accumulators
 #define TGM_ATT_MMA(KC, B0, B1)                                                              \
@@ -696,20 +688,37 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
             }                                                                               \
         }                                                                                   \
     }
+    if (has_tiles) {
+#pragma unroll
+        for (int kc = 0; kc < kAttPre; ++kc)
+            if (kc < P1)
+                TGM_ATT_MMA(kc, bpre[kc][0], bpre[kc][1])
+    }
+    // the weights of chunks P1 and P1 + 1 (the packed weights carry two zero
+    // chunks past the end), then the edge-feature rows to columns [D_t, D_t + D_e)
+    // (no chunk read so far touches them)
+    const f4 *pk = p0 + P1 * kstep;
+    f4 x0 = pk[0], x1 = pk[o1];
+    if (vec_e) {
+        xf.store(A, SA, D_t, lr, eoffv, D_e, lane);
+    } else if (D_e > 0) {   // unaligned or empty edge features: plain copies
+        for (int i = 0; i < RPW; ++i)
+            for (int k = lane; k < D_e; k += kWave)
+                A[lr[i] * SA + D_t + k] = eoff[i] >= 0 ? g.efeat[eoff[i] + k] : 0.f;
+    }
+    __syncthreads();
+    if (has_tiles) {
         // two register sets of weights alternate (chunk kc + 1 loads while kc
-        // multiplies); the packed weights carry padding chunks past the end
-        f4 x0 = p0[0], x1 = p0[o1];
-        keep_loaded(x0);
-        keep_loaded(x1);
-        int kc = 0;
+        // multiplies)
+        int kc = P1;
         for (; kc + 1 < g.KFC; kc += 2) {
-            const f4 *q = p0 + kstep;
+            const f4 *q = pk + kstep;
             const f4 y0 = q[0], y1 = q[o1];
             issue_fence();
             TGM_ATT_MMA(kc, x0, x1)
-            p0 += 2 * kstep;
-            x0 = p0[0];
-            x1 = p0[o1];
+            pk += 2 * kstep;
+            x0 = pk[0];
+            x1 = pk[o1];
             issue_fence();
             TGM_ATT_MMA(kc + 1, y0, y1)
         }
@@ -717,6 +726,12 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
             TGM_ATT_MMA(kc, x0, x1)
         }
 #undef TGM_ATT_MMA
+        // K|V = GEMM + seed
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+                acc[i][rb] += seed[i][rb];
     }
     __syncthreads();   // every read of the slot rows is done
 
@@ -732,6 +747,49 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
                     KV[(rb * 16 + 4 * (lane >> 4) + v) * SKV + col] = acc[i][rb][v];
         }
     }
+    // the query rows and the [. || s'_v] rows of the output projection's input
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        if (i < nq4) {
+            const int r = i / M4c, c = i - r * M4c;
+            *reinterpret_cast<f4 *>(Q + r * M + 4 * c) = qreg[u];
+        }
+        if (i < nv4) {
+            const int r = i / M4c, c = i - r * M4c;
+            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
+                s_voff[r] >= 0 ? vreg[u] : f4{0, 0, 0, 0};
+        }
+    }
+    if (qv4) {   // vectors past the first two per thread
+        for (int i = tid + 2 * blockDim.x; i < max(nq4, nv4); i += blockDim.x) {
+            const int r = i / M4c, c = i - r * M4c;
+            if (i < nq4)
+                *reinterpret_cast<f4 *>(Q + r * M + 4 * c) =
+                    *reinterpret_cast<const f4 *>(s_qoff[r] >= 0 ? g.P + s_qoff[r] + 4 * c
+                                                                 : g.pbias + 4 * c);
+            if (i < nv4)
+                *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
+                    s_voff[r] >= 0 ? *reinterpret_cast<const f4 *>(g.mem_new + s_voff[r] + 4 * c)
+                                   : f4{0, 0, 0, 0};
+        }
+    } else {     // scalar path
+        for (int i = tid; i < ORB * 16 * M; i += blockDim.x) {
+            const int r = i / M, k = i - r * M;
+            if (r < nroots)
+                Q[r * M + k] = s_qoff[r] >= 0 ? g.P[s_qoff[r] + k] : g.pbias[k];
+            AO[r * SAO + M + k] = s_voff[r] >= 0 ? g.mem_new[s_voff[r] + k] : 0.f;
+        }
+    }
+    {
+        // AO: columns [0, M) of rows without a root and the padding [2M, ..)
+        const int w2 = g.OC * 16 - M;
+        for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
+            const int r = idx / w2, c = idx - r * w2;
+            if (c >= M || r >= nroots)
+                AO[r * SAO + (c < M ? c : M + c)] = 0.f;
+        }
+    }
     // the output projection's weights: fetched now, used in step 5
     f4 ob[kAttMaxOC];
     const int ocb = wave;   // waves beyond ONB have no output column block
@@ -742,7 +800,9 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
                      : f4{0, 0, 0, 0};
     __syncthreads();
 
-    // 4. attention: scores, softmax, weighted sum of V
+    // 4. attention: scores (one thread per (root, head, slot)), softmax (one
+    // wave per (root, head): lane j holds slot j, reductions over lanes) and
+    // the weighted sum of V (one thread per output)
     const int d_h = M / H;
     const float scale = 1.0f / sqrtf((float)d_h);
     const int nsc = nroots * H * nb;
@@ -761,21 +821,21 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
         S[idx] = sc;
     }
     __syncthreads();
-    for (int idx = tid; idx < nroots * H; idx += blockDim.x) {
-        const int r = idx / H;
-        float *sr = S + idx * nb;
-        const int c = s_cnt[r];
-        float mx = -INFINITY;
-        for (int j = 0; j < c; ++j)
-            mx = fmaxf(mx, sr[j]);
-        float den = 0.f;
-        for (int j = 0; j < c; ++j) {
-            const float e = expf(sr[j] - mx);
-            sr[j] = e;
-            den += e;
-        }
-        for (int j = 0; j < c; ++j)
-            sr[j] = sr[j] / den;
+    for (int pr = wave; pr < nroots * H; pr += nw) {
+        const int c = s_cnt[pr / H];
+        float *sr = S + pr * nb;
+        const float sc = lane < c ? sr[lane] : -INFINITY;
+        float mx = sc;
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o >>= 1)
+            mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+        const float e = lane < c ? expf(sc - mx) : 0.f;
+        float den = e;
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o >>= 1)
+            den += __shfl_xor(den, o, kWave);
+        if (lane < c)
+            sr[lane] = e / den;
     }
     __syncthreads();
     for (int idx = tid; idx < nroots * M; idx += blockDim.x) {
@@ -790,23 +850,29 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
     }
     __syncthreads();
 
-    // 5. h = ReLU(W_o [a || s'_v] + b_o)
+    // 5. h = ReLU(W_o [a || s'_v] + b_o), two accumulators over alternate chunks
     if (ocb < g.ONB) {
         const float *orow = AO + (lane & 15) * SAO + 4 * (lane >> 4);
         const int col = ocb * 16 + (lane & 15);
         for (int orb = 0; orb < ORB; ++orb) {
-            f4 ac = {0, 0, 0, 0};
+            f4 ac0 = {0, 0, 0, 0}, ac1 = ac0;
 #pragma unroll
-            for (int kc = 0; kc < kAttMaxOC; ++kc)
+            for (int kc = 0; kc < kAttMaxOC; kc += 2) {
                 if (kc < g.OC)
-                    ac = mfma_k16(*reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + kc * 16),
-                                  ob[kc], ac);
+                    ac0 = mfma_k16(*reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + kc * 16),
+                                   ob[kc], ac0);
+                if (kc + 1 < g.OC)
+                    ac1 = mfma_k16(
+                        *reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + (kc + 1) * 16),
+                        ob[kc + 1], ac1);
+            }
             if (col < M) {
+                const float bo = g.b_o[col];
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int r = orb * 16 + 4 * (lane >> 4) + v;
                     if (r < nroots)
-                        g.h[(int64_t)(r0 + r) * M + col] = fmaxf(ac[v] + g.b_o[col], 0.f);
+                        g.h[(int64_t)(r0 + r) * M + col] = fmaxf(ac0[v] + ac1[v] + bo, 0.f);
                 }
             }
         }
@@ -814,9 +880,8 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
 }
 
 // q bias folded at creation: c_q = W_q^t phi(0) + b_q with phi(0)_d = cos(beta_d).
-__global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q,
-                              const float *__restrict__ b_q, const double *__restrict__ beta,
-                              float *__restrict__ c_q)
+__global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, const float *b_q,
+                              const double *__restrict__ beta, float *c_q)   // may alias b_q
 {
     const int k = blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= M)
@@ -897,9 +962,7 @@ extern "C" tgm_status_t tgm_model_destroy(tgm_model_t m)
     hipFree(m->proj_b);
     hipFree(m->P);
     hipFree(m->kv_b);
-    hipFree(m->b_k);
-    hipFree(m->b_v);
-    hipFree(m->c_q);
+    hipFree(m->pbias);
     hipFree(m->out_b);
     hipFree(m->b_o);
     delete m;
@@ -970,8 +1033,11 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     std::vector<float> wkv((size_t)2 * M * (KF > 0 ? KF : 1), 0.f);
     for (int n = 0; n < M; ++n)
         for (int k = 0; k < KF; ++k) {
-            wkv[(size_t)n * KF + k] = w->W_k[(size_t)n * Dkv + M + k];
-            wkv[(size_t)(M + n) * KF + k] = w->W_v[(size_t)n * Dkv + M + k];
+            // slot row order [phi || efeat]: column k < D_t is time code k, the
+            // rest edge feature k - D_t (W's own order is [s || efeat || phi])
+            const int src = k < D_t ? M + D_e + k : M + k - D_t;
+            wkv[(size_t)n * KF + k] = w->W_k[(size_t)n * Dkv + src];
+            wkv[(size_t)(M + n) * KF + k] = w->W_v[(size_t)n * Dkv + src];
         }
     auto kvb = pack_b(wkv.data(), 2 * M, KF, 0, KF, m->KFC, m->KVNB);
     auto ob = pack_b(w->W_o, M, 2 * M, 0, 2 * M, m->OC, m->ONB);
@@ -980,7 +1046,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     bx.resize(bx.size() + 2 * (size_t)m->MB * kWave * 4, 0.f);
     bh.resize(bh.size() + 2 * (size_t)m->MB * kWave * 4, 0.f);
     pb.resize(pb.size() + 2 * (size_t)m->PNB * kWave * 4, 0.f);
-    kvb.resize(kvb.size() + 2 * (size_t)m->KVNB * kWave * 4, 0.f);
+    // (and at least kAttPre chunks: k_attn preloads that many)
+    kvb.resize((size_t)std::max(m->KFC + 2, kAttPre) * m->KVNB * kWave * 4, 0.f);
     ob.resize(ob.size() + 2 * (size_t)m->ONB * kWave * 4, 0.f);
 
     float *wq_dev = nullptr;
@@ -995,8 +1062,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             !alloc((void **)&m->beta, sizeof(double) * D_t) ||
             !alloc((void **)&m->proj_b, pb.size() * 4) ||
             !alloc((void **)&m->P, sizeof(float) * (size_t)d->max_nodes * m->PNB * 16) ||
-            !alloc((void **)&m->kv_b, kvb.size() * 4) || !alloc((void **)&m->b_k, 4 * M) ||
-            !alloc((void **)&m->b_v, 4 * M) || !alloc((void **)&m->c_q, 4 * M) ||
+            !alloc((void **)&m->kv_b, kvb.size() * 4) ||
+            !alloc((void **)&m->pbias, sizeof(float) * m->PNB * 16) ||
             !alloc((void **)&m->out_b, ob.size() * 4) || !alloc((void **)&m->b_o, 4 * M) ||
             !alloc((void **)&wq_dev, sizeof(float) * (size_t)M * Dq)) {
             st = TGM_ENOMEM;
@@ -1011,15 +1078,18 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
         }
         if ((st = upload(m->proj_b, pb.data(), pb.size() * 4)) != TGM_OK) break;
         if ((st = upload(m->kv_b, kvb.data(), kvb.size() * 4)) != TGM_OK) break;
-        if ((st = upload(m->b_k, w->b_k, 4 * M)) != TGM_OK) break;
-        if ((st = upload(m->b_v, w->b_v, 4 * M)) != TGM_OK) break;
+        {   // b_q (folded into c_q in place below), b_k, b_v, zero padding
+            std::vector<float> pbias((size_t)m->PNB * 16, 0.f);
+            std::copy(w->b_q, w->b_q + M, pbias.begin());
+            std::copy(w->b_k, w->b_k + M, pbias.begin() + M);
+            std::copy(w->b_v, w->b_v + M, pbias.begin() + 2 * M);
+            if ((st = upload(m->pbias, pbias.data(), pbias.size() * 4)) != TGM_OK) break;
+        }
         if ((st = upload(m->out_b, ob.data(), ob.size() * 4)) != TGM_OK) break;
         if ((st = upload(m->b_o, w->b_o, 4 * M)) != TGM_OK) break;
         if ((st = upload(wq_dev, w->W_q, sizeof(float) * (size_t)M * Dq)) != TGM_OK) break;
-        float *bq_dev = m->c_q;   // b_q staged in c_q, folded in place
-        if ((st = upload(bq_dev, w->b_q, 4 * M)) != TGM_OK) break;
         hipLaunchKernelGGL(k_fold_q_bias, dim3(cdiv(M, 64)), dim3(64), 0, s, M, D_t, wq_dev,
-                           bq_dev, m->beta, m->c_q);
+                           m->pbias, m->beta, m->pbias);
         if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) {
             st = TGM_EDEVICE;
             break;
@@ -1153,7 +1223,7 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
     const int proj_waves = std::max<int>(4, std::min<int>(kMaxWaves, (int)cdiv(m->PNB, 3)));
     const int proj_grid = (int)std::min<int64_t>(cdiv(cap, 16), 512);
     TGM_LAUNCH(k_node_proj, dim3(proj_grid), dim3(64 * proj_waves), proj_lds(m), s, n_nodes,
-               mem_new, m->M, m->PC, m->proj_b, m->PNB, m->P);
+               mem_new, m->M, m->PC, m->proj_b, m->PNB, m->pbias, m->P);
     AttnArgs a;
     a.R = R; a.nb = nb; a.RT = attn_roots(m, &a.RBa); a.M = m->M; a.H = m->H;
     a.E = g->E; a.n_nodes = n_nodes;
@@ -1163,7 +1233,7 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
     a.P = m->P; a.ldP = m->PNB * 16;
     a.efeat = g->efeat; a.omega = m->omega; a.beta = m->beta;
     a.kv_b = m->kv_b; a.KFC = m->KFC; a.KVNB = m->KVNB;
-    a.b_k = m->b_k; a.b_v = m->b_v; a.c_q = m->c_q;
+    a.pbias = m->pbias;
     a.out_b = m->out_b; a.OC = m->OC; a.ONB = m->ONB; a.b_o = m->b_o;
     a.mem_new = mem_new; a.h = h;
     const dim3 grid(cdiv(R, a.RT)), block(64 * kMaxWaves);
