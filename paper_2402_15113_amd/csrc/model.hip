@@ -18,228 +18,293 @@ constexpr int kAttMaxRB = 5;   // 16-row slot blocks per workgroup
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf(-x)); }
 
 // ------------------------------------------------------------------ GRU
-// Workgroup (blockIdx.x, blockIdx.y) owns 16 node-set rows and one 16-wide
-// block of hidden units; its kGruKS wavefronts split the reduction (k) range.
-// The rows' GRU inputs [mail || phi(mail_ts - mem_ts) | mem] are staged in LDS
-// with the row loads of the block in flight together; each wave accumulates
-// partial gate pre-activations for its k-chunks (r and z over [x | h]; n split
-// into its x part and its h part, which the reset gate scales) with the next
-// chunk's weights prefetched; the partials are summed in a fixed wave order
-// (deterministic) and the gates applied.  The hb = 0 workgroups also reset the
-// latest-message slots of their rows (consumed next by k_latest) and write the
-// new memory timestamps.
-constexpr int kGruKS = 4;
+// The work is nrb x MB equal tasks (16-row block rb, 16-wide hidden block hb).
+// Persistent grid of kGruGrid workgroups: workgroup w takes a contiguous range
+// of tasks (ranges are dealt so that the ranges of one XCD are adjacent, and
+// the tasks of one row block mostly meet in one L2) and walks it in rounds of
+// at most 4 tasks spanning at most 2 row blocks:
+//   the rows' GRU inputs [mail || phi(mail_ts - mem_ts) | mem] are staged in
+//   LDS with all their loads in flight together; task j of the round goes to
+//   wavefronts j and j + 4, which split the reduction (k) range in two halves
+//   and stream the weights of their half, two chunks ahead of the multiply;
+//   each accumulates r and z over [x | h] and n in its x part and its h part
+//   (which the reset gate scales); the upper half's partial sums go through
+//   LDS to the lower half, which applies the gates.
+// The hb = 0 tasks also reset the latest-message slots of their rows
+// (consumed next by k_latest) and write the new memory timestamps.
+constexpr int kGruWaves = 8;
+constexpr int kGruGrid = 256;
+constexpr int kGruRows = 32;   // rows staged per round (2 row blocks)
 
-// k-chunks [cb, ce) of one part (x or h) of the GRU: three gate accumulators,
-// weights double-buffered in registers (sets A and B alternate, no copies).
-// `cofs` is the part's first chunk in the LDS row.
-__device__ __forceinline__ void gru_part(const f4 *__restrict__ w, int64_t gs, int64_t kstep,
-                                         int hb, int lane, const float *arow, int cb, int ce,
-                                         int cofs, f4 &ar, f4 &az, f4 &an)
+struct GruArgs {
+    const int32_t *n_nodes;
+    const float *mem, *mail;
+    const double *mem_ts, *mail_ts;
+    const int32_t *ver;
+    const f4 *bx, *bh;
+    const float *bias;
+    const double *omega, *beta;
+    int M, D_m, D_t, KXC, KHC, MB;
+    float *mem_new;
+    double *new_mem_ts;
+    int32_t *win;
+};
+
+// The weights of k-chunk c (chunks [0, KXC) are the x part, the rest the h
+// part) for hidden block hb: gates r, z, n.
+struct GruW {
+    const f4 *bx, *bh;
+    int64_t kstep, gx, gh;
+    int KXC, last;   // last: the highest chunk that may be loaded
+
+    __device__ __forceinline__ void load(int c, int hb, int lane, f4 (&w)[3]) const
+    {
+        c = c < last ? c : last;
+        const bool x = c < KXC;
+        const f4 *p = (x ? bx + (int64_t)c * kstep : bh + (int64_t)(c - KXC) * kstep) +
+                      (int64_t)hb * kWave + lane;
+        const int64_t gs = x ? gx : gh;
+        w[0] = p[0];
+        w[1] = p[gs];
+        w[2] = p[2 * gs];
+    }
+};
+
+__device__ __forceinline__ void gru_mma(const float *arow, int c, int KXC, const f4 (&w)[3],
+                                        f4 &ar, f4 &az, f4 &anx, f4 &anh)
 {
-    if (cb >= ce)
-        return;
-    const f4 *pw = w + (int64_t)(cb - cofs) * kstep + (int64_t)hb * kWave + lane;
-    f4 a0 = pw[0], a1 = pw[gs], a2 = pw[2 * gs];
-    keep_loaded(a0);
-    keep_loaded(a1);
-    keep_loaded(a2);
-    int c = cb;
-    for (; c + 1 < ce; c += 2) {
-        const f4 *q = pw + kstep;
-        const f4 b0 = q[0], b1 = q[gs], b2 = q[2 * gs];
-        issue_fence();
-        {
-            const f4 a = *reinterpret_cast<const f4 *>(arow + c * 16);
-            ar = mfma_k16(a, a0, ar);
-            az = mfma_k16(a, a1, az);
-            an = mfma_k16(a, a2, an);
-        }
-        pw += 2 * kstep;
-        a0 = pw[0];
-        a1 = pw[gs];
-        a2 = pw[2 * gs];
-        issue_fence();
-        {
-            const f4 a = *reinterpret_cast<const f4 *>(arow + (c + 1) * 16);
-            ar = mfma_k16(a, b0, ar);
-            az = mfma_k16(a, b1, az);
-            an = mfma_k16(a, b2, an);
-        }
-    }
-    if (c < ce) {
-        const f4 a = *reinterpret_cast<const f4 *>(arow + c * 16);
-        ar = mfma_k16(a, a0, ar);
-        az = mfma_k16(a, a1, az);
-        an = mfma_k16(a, a2, an);
-    }
+    const f4 a = *reinterpret_cast<const f4 *>(arow + c * 16);
+    ar = mfma_k16(a, w[0], ar);
+    az = mfma_k16(a, w[1], az);
+    if (c < KXC)
+        anx = mfma_k16(a, w[2], anx);
+    else
+        anh = mfma_k16(a, w[2], anh);
 }
 
-__global__ __launch_bounds__(64 * kGruKS) void k_gru(
-    const int32_t *__restrict__ n_nodes, const float *__restrict__ mem,
-    const double *__restrict__ mem_ts, const float *__restrict__ mail,
-    const double *__restrict__ mail_ts, const int32_t *__restrict__ ver,
-    const f4 *__restrict__ bx, const f4 *__restrict__ bh, const float *__restrict__ bias,
-    const double *__restrict__ omega, const double *__restrict__ beta, int M, int D_m, int D_t,
-    int KXC, int KHC, int MB, float *__restrict__ mem_new, double *__restrict__ new_mem_ts,
-    int32_t *__restrict__ win)
-{
-    // LDS: A [16][SA] | partial sums [KS][4][64] f4 | omega, beta [D_t] fp64
-    extern __shared__ float lds[];
-    __shared__ int s_has[16];
-    const int n = *n_nodes;
-    const int KX = KXC * 16, KH = KHC * 16;
-    const int SA = KX + KH + 4;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-    f4 *red = reinterpret_cast<f4 *>(lds + 16 * SA);
-    double *s_om = reinterpret_cast<double *>(lds + 16 * SA + kGruKS * 4 * kWave * 4);
-    double *s_be = s_om + D_t;
-    if (n <= 0)
-        return;
-    for (int d = tid; d < D_t; d += blockDim.x) {
-        s_om[d] = omega[d];
-        s_be[d] = beta[d];
-    }
-    const int KC = KXC + KHC;
-    const int c0 = (wave * KC) / kGruKS, c1 = ((wave + 1) * KC) / kGruKS;
-    const float *arow = lds + (lane & 15) * SA + 4 * (lane >> 4);
-    const int64_t gx = (int64_t)KXC * MB * kWave;   // stride between gates in bx
-    const int64_t gh = (int64_t)KHC * MB * kWave;
-    const int64_t kstep = (int64_t)MB * kWave;
-    const bool al =
-        ((reinterpret_cast<uintptr_t>(mail) | reinterpret_cast<uintptr_t>(mem)) & 15) == 0 &&
-        (D_m & 3) == 0 && (M & 3) == 0;   // 16-byte rows: vector loads
-    const int padx = KX - D_m - D_t, padh = KH - M;
+// Rows of one round held in registers between their load and their LDS
+// store: wave w takes rows w + 8 i.
+template <int W, int CM, int CH>
+struct GruRows {
+    static constexpr int RR = kGruRows / kGruWaves;
+    WaveRows<W, RR, CM> xm;
+    WaveRows<W, RR, CH> xh;
+    int64_t offm[RR], offh[RR];
+    int lr[RR], vv[RR];
+    double mt[RR], lt[RR];
 
-    // Tiles (row block r, hidden block hb).  Workgroup w runs on XCD w % 8, and
-    // the XCD x workgroups share the row blocks r = x (mod 8), so the MB tiles
-    // that stage the same 16 rows meet in one L2.  Within an XCD the tiles go
-    // in row-block-major order; the first one past the node set ends the loop.
-    const int nx = gridDim.x >= 8 ? 8 : 1;
-    const int xcd = blockIdx.x % nx, slot = blockIdx.x / nx;
-    const int per_xcd = (gridDim.x - xcd + nx - 1) / nx;   // workgroups on this XCD
-    for (int k = slot;; k += per_xcd) {
-        const int rl = k / MB;                  // the XCD's rl-th row block
-        const int hb = k - rl * MB;
-        const int row0 = (rl * nx + xcd) * 16;
-        if (row0 >= n)
-            break;
-        const int nvalid = min(16, n - row0);
-        __syncthreads();   // the previous tile is done with LDS
-        {
-            // wave w stages rows w, w + 4, w + 8, w + 12 of the tile: one round of
-            // loads for their versions, times, mail and memory (branch-free: rows
-            // past the node set read the tile's first row and drop it); the time
-            // codes are computed while the rows are in flight
-            int64_t offm[4], offh[4];
-            int lr[4];
-            bool has[4];
-            double dts[4], nts_[4];
+    __device__ __forceinline__ void load(const GruArgs &g, int row0, int nrows, int wave,
+                                         int lane)
+    {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = wave + 4 * i;
-                const bool live = r < nvalid;
-                const int p = row0 + (live ? r : 0);
-                const int v = ver[p];
-                const double mt = mem_ts[p], lt = mail_ts[p];
-                lr[i] = r;
-                has[i] = live && v >= 0;
-                dts[i] = lt - mt;
-                nts_[i] = has[i] ? lt : mt;
-                offm[i] = live ? (int64_t)p * D_m : -1;
-                offh[i] = live ? (int64_t)p * M : -1;
-            }
-            auto finish_rows = [&]() {
-                for (int d = lane; d < D_t; d += kWave) {
-                    const double om = s_om[d], be = s_be[d];
+        for (int i = 0; i < RR; ++i) {
+            const int r = wave + kGruWaves * i;
+            const bool live = r < nrows;
+            const int p = row0 + (live ? r : 0);   // branch-free: dead rows read the first row
+            lr[i] = r;
+            vv[i] = g.ver[p];
+            mt[i] = g.mem_ts[p];
+            lt[i] = g.mail_ts[p];
+            offm[i] = live ? (int64_t)p * g.D_m : -1;
+            offh[i] = live ? (int64_t)p * g.M : -1;
+        }
+        xm.load(g.mail, offm, g.D_m, lane);
+        xh.load(g.mem, offh, g.M, lane);
+    }
+
+    __device__ __forceinline__ void store(const GruArgs &g, float *A, int *s_has, double *s_nts,
+                                          int SA, int KX, const double *s_om,
+                                          const double *s_be, int nrows, int lane) const
+    {
+        const int D_m = g.D_m, D_t = g.D_t, M = g.M;
+        bool has[RR];
+        double dt[RR];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        lds[lr[i] * SA + D_m + d] = has[i] ? time_enc(om, be, dts[i]) : 0.f;
-                }
+        for (int i = 0; i < RR; ++i) {
+            has[i] = lr[i] < nrows && vv[i] >= 0;
+            dt[i] = lt[i] - mt[i];
+        }
+        for (int d = lane; d < D_t; d += kWave) {
+            const double om = s_om[d], be = s_be[d];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    float *row = lds + lr[i] * SA;
-                    for (int k = lane; k < padx; k += kWave)
-                        row[D_m + D_t + k] = 0.f;
-                    for (int k = lane; k < padh; k += kWave)
-                        row[KX + M + k] = 0.f;
-                    if (lane == 0) {
-                        s_has[lr[i]] = has[i];
-                        if (hb == 0 && lr[i] < nvalid) {
-                            win[row0 + lr[i]] = -1;
-                            if (new_mem_ts)
-                                new_mem_ts[row0 + lr[i]] = nts_[i];
-                        }
-                    }
-                }
-            };
-            if (al) {
-                WaveRows<4, 4, 2> xm;
-                WaveRows<4, 4, 1> xh;
-                xm.load(mail, offm, D_m, lane);
-                xh.load(mem, offh, M, lane);
-                finish_rows();
-                xm.store(lds, SA, 0, lr, offm, D_m, lane);
-                xh.store(lds, SA, KX, lr, offh, M, lane);
-            } else {
-                WaveRows<1, 4, 8> xm;
-                WaveRows<1, 4, 2> xh;
-                xm.load(mail, offm, D_m, lane);
-                xh.load(mem, offh, M, lane);
-                finish_rows();
-                xm.store(lds, SA, 0, lr, offm, D_m, lane);
-                xh.store(lds, SA, KX, lr, offh, M, lane);
+            for (int i = 0; i < RR; ++i)
+                A[lr[i] * SA + D_m + d] = has[i] ? time_enc(om, be, dt[i]) : 0.f;
+        }
+        const int padx = KX - D_m - D_t, padh = SA - 4 - KX - M;
+#pragma unroll
+        for (int i = 0; i < RR; ++i) {
+            float *row = A + lr[i] * SA;
+            for (int k = lane; k < padx; k += kWave)
+                row[D_m + D_t + k] = 0.f;
+            for (int k = lane; k < padh; k += kWave)
+                row[KX + M + k] = 0.f;
+            if (lane == 0) {
+                s_has[lr[i]] = has[i];
+                s_nts[lr[i]] = has[i] ? lt[i] : mt[i];
             }
         }
+        xm.store(A, SA, 0, lr, offm, D_m, lane);
+        xh.store(A, SA, KX, lr, offh, M, lane);
+    }
+};
+
+template <int W, int CM, int CH>
+__device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_has,
+                                         double *s_nts)
+{
+    const int n = *g.n_nodes;
+    const int M = g.M, MB = g.MB, D_t = g.D_t, KXC = g.KXC, KHC = g.KHC;
+    const int KC = KXC + KHC;
+    const int KX = KXC * 16, SA = KC * 16 + 4;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    float *A = lds;                                              // [kGruRows][SA]
+    f4 *red = reinterpret_cast<f4 *>(lds + kGruRows * SA);       // [4 tasks][4][64]
+    double *s_om = reinterpret_cast<double *>(lds + kGruRows * SA + 4 * 4 * kWave * 4);
+    double *s_be = s_om + D_t;
+
+    // this workgroup's task range: range c = (w % 8) * (G / 8) + w / 8, so the
+    // ranges of one XCD are adjacent
+    const int64_t T = (int64_t)((n + 15) >> 4) * MB;
+    const int G = gridDim.x;
+    const int c = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    const int64_t t0 = T * c / G, t1 = T * (c + 1) / G;
+    if (t0 >= t1)
+        return;
+
+    GruW gw;
+    gw.bx = g.bx;
+    gw.bh = g.bh;
+    gw.kstep = (int64_t)MB * kWave;
+    gw.gx = (int64_t)KXC * gw.kstep;
+    gw.gh = (int64_t)KHC * gw.kstep;
+    gw.KXC = KXC;
+    const int j = wave & 3, half = wave >> 2;
+    const int kc0 = half ? KC / 2 : 0, kc1 = half ? KC : KC / 2;
+    gw.last = kc1 - 1;
+    const float *arow0 = A + (lane & 15) * SA + 4 * (lane >> 4);
+    const int MP = MB * 16;
+    GruRows<W, CM, CH> rows;
+
+    // round geometry: tasks [t, te), rows [row0, row0 + nrows)
+    auto round_end = [&](int64_t t) {
+        const int64_t rb_a = t / MB;
+        return std::min<int64_t>(std::min<int64_t>(t + 4, t1), (rb_a + 2) * MB);
+    };
+    auto round_rows = [&](int64_t t, int64_t te) {
+        const int rb_a = (int)(t / MB);
+        return std::min(kGruRows, std::min<int>(n - rb_a * 16,
+                                                (int)(((te - 1) / MB - rb_a + 1) * 16)));
+    };
+
+    // the first round's rows go out before the time-encoding constants are
+    // set up
+    int64_t t = t0;
+    int64_t te = round_end(t);
+    rows.load(g, (int)(t / MB) * 16, round_rows(t, te), wave, lane);
+    for (int d = tid; d < D_t; d += blockDim.x) {
+        s_om[d] = g.omega[d];
+        s_be[d] = g.beta[d];
+    }
+    for (;;) {
+        const int rb_a = (int)(t / MB);
+        const int row0 = rb_a * 16;
+        const int nrows = round_rows(t, te);
+        const int64_t tj = t + j;
+        const bool live = tj < te;
+        const int rb = (int)(tj / MB), hb = live ? (int)(tj - (int64_t)rb * MB) : 0;
+        const int lrow0 = (rb - rb_a) * 16;
+        // biases and the first two weight chunks load while the rows are staged
+        const int col = hb * 16 + (lane & 15);
+        const int colc = col < M ? col : 0;
+        const float b_r = g.bias[colc], b_z = g.bias[MP + colc];
+        const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
+        f4 w0[3], w1[3], w2[3];
+        gw.load(kc0, hb, lane, w0);
+        gw.load(kc0 + 1, hb, lane, w1);
+        __syncthreads();   // s_om is written; the previous round is done with LDS
+        rows.store(g, A, s_has, s_nts, SA, KX, s_om, s_be, nrows, lane);
         __syncthreads();
 
         f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-        // x part chunks [c0, min(c1, KXC)), then h part chunks.  Each part is a
-        // two-set register ping-pong: the weights of chunk c + 1 are loaded while
-        // chunk c is multiplied, then the set of chunk c is refilled with chunk
-        // c + 2 (the packed weights carry padding chunks past the end).
-        {
-            const int xe = c1 < KXC ? c1 : KXC;
-            const int hs = c0 > KXC ? c0 : KXC;
-            gru_part(bx, gx, kstep, hb, lane, arow, c0, xe, 0, ar, az, anx);
-            gru_part(bh, gh, kstep, hb, lane, arow, hs, c1, KXC, ar, az, anh);
-        }
-        red[(wave * 4 + 0) * kWave + lane] = ar;
-        red[(wave * 4 + 1) * kWave + lane] = az;
-        red[(wave * 4 + 2) * kWave + lane] = anx;
-        red[(wave * 4 + 3) * kWave + lane] = anh;
-        __syncthreads();
-
-        // epilogue: thread (v, lane) finishes output element v of lane's 4
-        {
-            const int v = wave;   // kGruKS == 4 waves cover the 4 values of a lane
-            const int col = hb * 16 + (lane & 15);
-            const int rr = 4 * (lane >> 4) + v;
-            const int p = row0 + rr;
-            if (col < M && rr < nvalid) {
-                float gsum[4];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float acc = 0.f;
-                    for (int w = 0; w < kGruKS; ++w)
-                        acc += red[(w * 4 + q) * kWave + lane][v];
-                    gsum[q] = acc;
-                }
-                const int MP = MB * 16;
-                const float h = lds[rr * SA + KX + col];
-                float o = h;
-                if (s_has[rr]) {
-                    const float r = sigmoidf_(gsum[0] + bias[col]);
-                    const float z = sigmoidf_(gsum[1] + bias[MP + col]);
-                    const float nn =
-                        tanhf(gsum[2] + bias[2 * MP + col] + r * (gsum[3] + bias[3 * MP + col]));
-                    o = (1.0f - z) * nn + z * h;
-                }
-                mem_new[(int64_t)p * M + col] = o;
+        if (live) {
+            // three weight sets rotate: chunk c + 2 loads while chunk c multiplies
+            const float *arow = arow0 + lrow0 * SA;
+            for (int cc = kc0; cc < kc1; cc += 3) {
+                gw.load(cc + 2, hb, lane, w2);
+                issue_fence();
+                gru_mma(arow, cc, KXC, w0, ar, az, anx, anh);
+                gw.load(cc + 3, hb, lane, w0);
+                issue_fence();
+                if (cc + 1 < kc1)
+                    gru_mma(arow, cc + 1, KXC, w1, ar, az, anx, anh);
+                gw.load(cc + 4, hb, lane, w1);
+                issue_fence();
+                if (cc + 2 < kc1)
+                    gru_mma(arow, cc + 2, KXC, w2, ar, az, anx, anh);
+            }
+            if (half) {
+                red[(j * 4 + 0) * kWave + lane] = ar;
+                red[(j * 4 + 1) * kWave + lane] = az;
+                red[(j * 4 + 2) * kWave + lane] = anx;
+                red[(j * 4 + 3) * kWave + lane] = anh;
             }
         }
+        const int64_t tn = te;
+        const int64_t ten = tn < t1 ? round_end(tn) : tn;
+        if (tn < t1)   // the next round's rows, in flight during the epilogue
+            rows.load(g, (int)(tn / MB) * 16, round_rows(tn, ten), wave, lane);
+        __syncthreads();
+        if (live && !half) {
+            // lane holds values v = 0..3 of rows 4 (lane / 16) + v, column hb 16 + lane % 16
+            ar += red[(j * 4 + 0) * kWave + lane];
+            az += red[(j * 4 + 1) * kWave + lane];
+            anx += red[(j * 4 + 2) * kWave + lane];
+            anh += red[(j * 4 + 3) * kWave + lane];
+            if (col < M) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int lr = lrow0 + 4 * (lane >> 4) + v;
+                    const int p = row0 + lr;
+                    if (p < n) {
+                        const float h = A[lr * SA + KX + col];
+                        float o = h;
+                        if (s_has[lr]) {
+                            const float r = sigmoidf_(ar[v] + b_r);
+                            const float z = sigmoidf_(az[v] + b_z);
+                            const float nn = tanhf(anx[v] + b_nx + r * (anh[v] + b_nh));
+                            o = (1.0f - z) * nn + z * h;
+                        }
+                        g.mem_new[(int64_t)p * M + col] = o;
+                    }
+                }
+            }
+            if (hb == 0 && lane < 16 && row0 + lrow0 + lane < n) {
+                const int p = row0 + lrow0 + lane;
+                g.win[p] = -1;
+                if (g.new_mem_ts)
+                    g.new_mem_ts[p] = s_nts[lrow0 + lane];
+            }
+        }
+        if (tn >= t1)
+            break;
+        t = tn;
+        te = ten;
     }
+}
+
+__global__ __launch_bounds__(64 * kGruWaves) void k_gru(GruArgs g)
+{
+    extern __shared__ float lds[];
+    __shared__ int s_has[kGruRows];
+    __shared__ double s_nts[kGruRows];
+    const bool al = ((reinterpret_cast<uintptr_t>(g.mail) | reinterpret_cast<uintptr_t>(g.mem)) &
+                     15) == 0 &&
+                    (g.D_m & 3) == 0 && (g.M & 3) == 0;   // 16-byte rows: vector loads
+    if (al)
+        gru_body<4, 2, 1>(g, lds, s_has, s_nts);   // D_m <= 512, M <= 256
+    else
+        gru_body<1, 8, 2>(g, lds, s_has, s_nts);
 }
 
 // Latest-message reduce.  Candidate c = 2 (e - first) + role is the message
@@ -906,19 +971,10 @@ int waves_for(int blocks) { return blocks < kMaxWaves ? (blocks < 1 ? 1 : blocks
 
 size_t gru_lds(const tgm_model *m)
 {
-    return sizeof(float) * (16 * ((m->KXC + m->KHC) * 16 + 4) + kGruKS * 4 * kWave * 4) +
+    return sizeof(float) * (kGruRows * ((m->KXC + m->KHC) * 16 + 4) + 4 * 4 * kWave * 4) +
            2 * sizeof(double) * m->D_t;
 }
 
-// Persistent grid of k_gru: the tiles of the largest node set, capped at the
-// workgroups that fit on the device at once.
-int gru_grid(const tgm_model *m, int cap)
-{
-    const int64_t tiles = cdiv(cap, 16) * m->MB;
-    const int per_cu = (int)std::max<size_t>(1, (160 * 1024) / gru_lds(m));
-    const int64_t resident = 256LL * std::min(per_cu, 8);
-    return (int)std::max<int64_t>(1, std::min(tiles, resident));
-}
 size_t proj_lds(const tgm_model *m) { return sizeof(float) * 16 * (m->PC * 16 + 4); }
 
 int attn_roots(const tgm_model *m, int *RBa)
@@ -1144,10 +1200,14 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
         return TGM_EORDER;   // the slot still holds an uncommitted write set
     hipStream_t s = as_stream(stream);
     if (cap > 0) {
-        TGM_LAUNCH(k_gru, dim3(gru_grid(m, cap)), dim3(64 * kGruKS), gru_lds(m), s, n_nodes, mem,
-                           mem_ts, mail, mail_ts, ver, m->gru_bx, m->gru_bh, m->gru_bias,
-                           m->omega, m->beta, m->M, m->D_m, m->D_t, m->KXC, m->KHC, m->MB,
-                           mem_new, new_mem_ts, st->win);
+        GruArgs ga;
+        ga.n_nodes = n_nodes; ga.mem = mem; ga.mail = mail; ga.mem_ts = mem_ts;
+        ga.mail_ts = mail_ts; ga.ver = ver; ga.bx = m->gru_bx; ga.bh = m->gru_bh;
+        ga.bias = m->gru_bias; ga.omega = m->omega; ga.beta = m->beta; ga.M = m->M;
+        ga.D_m = m->D_m; ga.D_t = m->D_t; ga.KXC = m->KXC; ga.KHC = m->KHC; ga.MB = m->MB;
+        ga.mem_new = mem_new; ga.new_mem_ts = new_mem_ts; ga.win = st->win;
+        // persistent: the node set's tasks are split over kGruGrid workgroups
+        TGM_LAUNCH(k_gru, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
     }
     const int n_cand = 2 * b;
     const size_t base = (size_t)(iter % slots) * st->ring_rows();
