@@ -97,21 +97,25 @@ def work_model(wl, rows):
     f, d = 4, 8
     return {
         # per node with mail: the three gates over [x | h]
+        # (plus the batch's latest-message reduce: 2b positions, 2b 64-bit atomics)
         "k_gru": dict(flops=n_mail * 2 * 3 * M * (D_x + M),
-                      bytes=n_U * (M * f + d + d + 4) + n_mail * D_m * f + n_U * M * f),
+                      bytes=n_U * (M * f + d + d + 4) + n_mail * D_m * f + n_U * M * f
+                      + 2 * b * (4 + 8)),
         # per valid slot: [efeat || phi] -> [K | V] and the two head dot products;
         # per root: the output projection
         "k_attn": dict(flops=slots * (2 * (D_e + D_t) * 2 * M + 4 * M) + R * 2 * (2 * M) * M,
                        bytes=slots * (D_e * f + 4 + 4 + d) + R * (M * f + 4 + d + 4) + R * M * f),
         "k_node_proj": dict(flops=n_U * 2 * M * 3 * M, bytes=n_U * (M * f + 3 * M * f)),
         # roots in, offsets, the sampled records, outputs
-        "k_sample": dict(flops=0, bytes=R * (4 + d + 16) + slots * 16 + R * nb * (4 + 4 + d) + R * 4),
-        "k_node_set": dict(flops=0, bytes=R * 4 * 2 + R * nb * 4 * 2 + n_U * 4),
+        "k_sample_batch": dict(flops=0, bytes=b * (3 * 4 + d) + R * (4 + d + 16) + slots * 16
+                               + R * nb * (4 + 4 + d) + R * 4),
+        # node set: ids in, one stamp per id; then the stamps, ids in, positions out
+        "k_ns_mark": dict(flops=0, bytes=R * (nb + 1) * 4 * 2),
+        "k_ns_pos": dict(flops=0, bytes=wl.N * 4 + R * (nb + 1) * 4 * 2 + n_U * 4),
         "k_gather_state": dict(flops=0, bytes=2 * n_U * ((M + D_m) * f + d + d + 4) + n_U * 4),
         "k_commit": dict(flops=0, bytes=2 * n_win * ((M + D_m) * f + d + d) + 2 * b * 4),
         "k_stage": dict(flops=0, bytes=n_win * (2 * M * f + D_e * f + (M + D_m) * f + 3 * d)
                         + 2 * b * 12),
-        "k_latest": dict(flops=0, bytes=2 * b * 8),
         "k_batch_roots": dict(flops=0, bytes=b * (3 * 4 + d) + 3 * b * (4 + d)),
     }
 

@@ -100,7 +100,10 @@ struct tgm_state {
     int64_t committed_through = -1;   // all writes <= this are in the tables
     int64_t staged_through = -1;      // last iteration whose update was issued
     int64_t last_fetch = INT64_MIN;
-    int32_t *win = nullptr;           // [N] latest candidate per node-set position
+    // [N] latest candidate per node-set position, as the key (tag << 32) | c
+    // of the update call that wrote it (tags start at 1, so zero is stale)
+    uint64_t *win = nullptr;
+    uint32_t win_tag = 0;             // tag of the last update call
     size_t ring_rows() const { return 2 * (size_t)max_batch; }
 };
 

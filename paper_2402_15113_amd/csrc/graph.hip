@@ -195,10 +195,11 @@ __global__ __launch_bounds__(256) void k_sample_batch(
 // of U and maps its slice of roots and neighbours to their positions.  The
 // bitmap is rebuilt per workgroup because it is small (N/8 bytes) and L2-hot;
 // that replaces a grid-wide barrier.
-constexpr int kNsThreads = 256;
+constexpr int kNsThreads = 1024;
 constexpr int kNsWaves = kNsThreads / kWave;
-constexpr int kNsIds = 8;                          // ids per thread in k_ns_pos
+constexpr int kNsIds = 2;                          // ids per thread in k_ns_pos
 constexpr int kNsIdsPerBlock = kNsThreads * kNsIds;
+constexpr int kNsScan = 8;                         // stamp loads in flight per thread
 constexpr int kNsMaxWords = 1 << 13;               // 2^19 node ids
 
 __global__ __launch_bounds__(256) void k_fill_i32(int32_t *__restrict__ p, int32_t n, int32_t v)
@@ -243,17 +244,18 @@ __global__ __launch_bounds__(kNsThreads) void k_ns_pos(
         x[u] = k < R ? root[k] : (k < total ? nbr[k - R] : -1);
     }
 
-    // 1. membership words, four 64-id loads in flight per wave
-    for (int w0 = wave; w0 < NW; w0 += 4 * kNsWaves) {
-        int32_t f[4];
+    // 1. membership words: kNsScan coalesced stamp loads in flight per thread,
+    // then one ballot per 64 ids (wave w of round u covers word 16 u + w)
+    for (int base = 0; base < NW * kWave; base += kNsScan * kNsThreads) {
+        int32_t f[kNsScan];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int id = (w0 + u * kNsWaves) * kWave + lane;
+        for (int u = 0; u < kNsScan; ++u) {
+            const int id = base + u * kNsThreads + tid;
             f[u] = id < N ? stamp[id] : 0;
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int w = w0 + u * kNsWaves;
+        for (int u = 0; u < kNsScan; ++u) {
+            const int w = (base >> 6) + u * kNsWaves + wave;
             const uint64_t m = __ballot(f[u] == epoch);
             if (w < NW && lane == 0)
                 ns_mask[w] = m;

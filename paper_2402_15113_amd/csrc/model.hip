@@ -30,8 +30,8 @@ __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf
 //   each accumulates r and z over [x | h] and n in its x part and its h part
 //   (which the reset gate scales); the upper half's partial sums go through
 //   LDS to the lower half, which applies the gates.
-// The hb = 0 tasks also reset the latest-message slots of their rows
-// (consumed next by k_latest) and write the new memory timestamps.
+// The hb = 0 tasks also write the new memory timestamps.  The same launch
+// runs the batch's latest-message reduce (latest_reduce) first.
 constexpr int kGruWaves = 8;
 constexpr int kGruGrid = 256;
 constexpr int kGruRows = 32;   // rows staged per round (2 row blocks)
@@ -47,7 +47,11 @@ struct GruArgs {
     int M, D_m, D_t, KXC, KHC, MB;
     float *mem_new;
     double *new_mem_ts;
-    int32_t *win;
+    // latest-message reduce of the batch (see latest_reduce)
+    int32_t n_cand;
+    const int32_t *src_pos, *dst_pos;
+    uint64_t *win;
+    uint64_t tag;   // (update tag) << 32
 };
 
 // The weights of k-chunk c (chunks [0, KXC) are the x part, the rest the h
@@ -148,11 +152,44 @@ struct GruRows {
     }
 };
 
+// Latest-message reduce.  Candidate c = 2 (e - first) + role is the message
+// of event first + c/2 to its source (role 0) or destination (role 1).  The
+// stream is sorted by (t, e), so the candidate order is the (t, e, role)
+// order and the latest message of a node is its largest c: an integer max,
+// exact and order-independent.  The slot of a node holds the 64-bit key
+// (tag << 32) | c, with a tag that grows with every update call, so a max
+// over keys needs no reset between calls: a key of an older call is smaller
+// than any key of this one.  Candidates of one wavefront that hit the same
+// node are first reduced with lane shuffles (the wave's candidates are
+// consecutive, so a node's last lane in the wave holds its wave maximum); only
+// that lane issues the atomic.  Thread c of the grid takes candidate c.
+__device__ __forceinline__ void latest_reduce(const GruArgs &g, int n)
+{
+    const int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (c - (threadIdx.x & (kWave - 1)) >= g.n_cand)
+        return;   // the whole wave is past the candidates
+    const int lane = threadIdx.x & (kWave - 1);
+    int p = c < g.n_cand ? ((c & 1) ? g.dst_pos[c >> 1] : g.src_pos[c >> 1]) : -1;
+    const bool live = p >= 0 && p < n;   // positions outside the node set are dropped
+    if (!live)
+        p = -1 - lane;
+    // is there a later lane in this wave with the same position?
+    bool later = false;
+    for (int o = 1; o < kWave; ++o) {
+        const int q = __shfl(p, (lane + o) & (kWave - 1), kWave);
+        later |= (lane + o < kWave) && q == p;
+    }
+    if (live && !later)
+        atomicMax(reinterpret_cast<unsigned long long *>(g.win + p),
+                  (unsigned long long)(g.tag | (uint64_t)c));
+}
+
 template <int W, int CM, int CH>
 __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_has,
                                          double *s_nts)
 {
     const int n = *g.n_nodes;
+    latest_reduce(g, n);
     const int M = g.M, MB = g.MB, D_t = g.D_t, KXC = g.KXC, KHC = g.KHC;
     const int KC = KXC + KHC;
     const int KX = KXC * 16, SA = KC * 16 + 4;
@@ -279,12 +316,8 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
                     }
                 }
             }
-            if (hb == 0 && lane < 16 && row0 + lrow0 + lane < n) {
-                const int p = row0 + lrow0 + lane;
-                g.win[p] = -1;
-                if (g.new_mem_ts)
-                    g.new_mem_ts[p] = s_nts[lrow0 + lane];
-            }
+            if (hb == 0 && g.new_mem_ts && lane < 16 && row0 + lrow0 + lane < n)
+                g.new_mem_ts[row0 + lrow0 + lane] = s_nts[lrow0 + lane];
         }
         if (tn >= t1)
             break;
@@ -307,36 +340,6 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru(GruArgs g)
         gru_body<1, 8, 2>(g, lds, s_has, s_nts);
 }
 
-// Latest-message reduce.  Candidate c = 2 (e - first) + role is the message
-// of event first + c/2 to its source (role 0) or destination (role 1).  The
-// stream is sorted by (t, e), so the candidate order is the (t, e, role)
-// order and the latest message of a node is its largest c: an integer max,
-// exact and order-independent.  Candidates of one wavefront that hit the same
-// node are first reduced with lane shuffles (the wave's candidates are
-// consecutive, so a node's last lane in the wave holds its wave maximum); only
-// that lane issues the atomic.
-__global__ __launch_bounds__(256) void k_latest(int32_t n_cand, const int32_t *__restrict__ n_nodes,
-                                                const int32_t *__restrict__ src_pos,
-                                                const int32_t *__restrict__ dst_pos,
-                                                int32_t *__restrict__ win)
-{
-    const int c = blockIdx.x * blockDim.x + threadIdx.x;
-    const int lane = threadIdx.x & 63;
-    const int n = *n_nodes;
-    int p = c < n_cand ? ((c & 1) ? dst_pos[c >> 1] : src_pos[c >> 1]) : -1;
-    const bool live = p >= 0 && p < n;   // positions outside the node set are dropped
-    if (!live)
-        p = -1 - lane;
-    // is there a later lane in this wave with the same position?
-    bool later = false;
-    for (int o = 1; o < kWave; ++o) {
-        const int q = __shfl(p, (lane + o) & 63, kWave);
-        later |= (lane + o < kWave) && q == p;
-    }
-    if (live && !later)
-        atomicMax(&win[p], c);
-}
-
 // Stage the write set of iteration i, and commit an older one, in one launch.
 // Wavefronts c < n_cand each take one candidate of iteration i: the winning
 // candidate of its node writes the node's new memory, its message
@@ -351,7 +354,9 @@ struct StageArgs {
     int64_t first, iter, c_iter;
     int M, D_m, D_e;
     bool direct;
-    const int32_t *n_nodes, *src, *dst, *src_pos, *dst_pos, *win, *ver;
+    const int32_t *n_nodes, *src, *dst, *src_pos, *dst_pos, *ver;
+    const uint64_t *win;
+    uint64_t tag;   // (update tag) << 32
     const double *t, *mem_ts, *mail_ts;
     const float *efeat, *mem_new;
     // destination ring slot of iteration i
@@ -391,7 +396,7 @@ __global__ __launch_bounds__(256) void k_stage(StageArgs g)
     const int n = *g.n_nodes;
     const int p = role ? g.dst_pos[k] : g.src_pos[k];
     const int q = role ? g.src_pos[k] : g.dst_pos[k];
-    if (p < 0 || p >= n || q < 0 || q >= n || g.win[p] != c) {
+    if (p < 0 || p >= n || q < 0 || q >= n || g.win[p] != (g.tag | (uint64_t)c)) {
         if (lane == 0 && !g.direct)
             g.r_flag[c] = 0;
         return;
@@ -421,14 +426,22 @@ __global__ __launch_bounds__(256) void k_stage(StageArgs g)
     }
 }
 
+__global__ void k_fill_u64(uint64_t *__restrict__ p, int32_t n)
+{
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < n)
+        p[k] = 0;
+}
+
 __global__ void k_winner_out(const int32_t *__restrict__ n_nodes, int32_t cap, int64_t first,
-                             const int32_t *__restrict__ win, int64_t *__restrict__ winner)
+                             const uint64_t *__restrict__ win, uint64_t tag,
+                             int64_t *__restrict__ winner)
 {
     const int p = blockIdx.x * blockDim.x + threadIdx.x;
     if (p >= cap || p >= *n_nodes)
         return;
-    const int32_t c = win[p];
-    winner[p] = c >= 0 ? 2 * first + c : -1;
+    const uint64_t key = win[p];
+    winner[p] = (key >> 32) == (tag >> 32) ? 2 * first + (int64_t)(key & 0xffffffffu) : -1;
 }
 
 // ------------------------------------------------------------------ embed
@@ -1199,17 +1212,24 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
     if (iter - slots > st->committed_through)
         return TGM_EORDER;   // the slot still holds an uncommitted write set
     hipStream_t s = as_stream(stream);
+    if (st->win_tag == UINT32_MAX) {   // keys restart from zero
+        TGM_LAUNCH(k_fill_u64, dim3(cdiv(st->N, 256)), dim3(256), 0, s, st->win, st->N);
+        st->win_tag = 0;
+    }
+    const uint64_t tag = (uint64_t)(++st->win_tag) << 32;
+    const int n_cand = 2 * b;
     if (cap > 0) {
         GruArgs ga;
         ga.n_nodes = n_nodes; ga.mem = mem; ga.mail = mail; ga.mem_ts = mem_ts;
         ga.mail_ts = mail_ts; ga.ver = ver; ga.bx = m->gru_bx; ga.bh = m->gru_bh;
         ga.bias = m->gru_bias; ga.omega = m->omega; ga.beta = m->beta; ga.M = m->M;
         ga.D_m = m->D_m; ga.D_t = m->D_t; ga.KXC = m->KXC; ga.KHC = m->KHC; ga.MB = m->MB;
-        ga.mem_new = mem_new; ga.new_mem_ts = new_mem_ts; ga.win = st->win;
+        ga.mem_new = mem_new; ga.new_mem_ts = new_mem_ts;
+        ga.n_cand = n_cand; ga.src_pos = src_pos; ga.dst_pos = dst_pos; ga.win = st->win;
+        ga.tag = tag;
         // persistent: the node set's tasks are split over kGruGrid workgroups
         TGM_LAUNCH(k_gru, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
     }
-    const int n_cand = 2 * b;
     const size_t base = (size_t)(iter % slots) * st->ring_rows();
     // the write set of iteration iter - s is committed by this launch when it
     // is the next one due (s = 0: the current write set goes to the tables)
@@ -1219,10 +1239,6 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
     const bool fuse = !direct && cj >= 0 && cj == st->committed_through + 1 && cs.staged &&
                       cs.iter == cj;
     const int n_commit = fuse ? 2 * cs.b : 0;
-    if (n_cand > 0) {
-        TGM_LAUNCH(k_latest, dim3(cdiv(n_cand, 256)), dim3(256), 0, s, n_cand, n_nodes,
-                   src_pos, dst_pos, st->win);
-    }
     if (n_cand + n_commit > 0) {
         const size_t cbase = (size_t)(((cj % slots) + slots) % slots) * st->ring_rows();
         StageArgs a;
@@ -1230,7 +1246,7 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
         a.first = first_event; a.iter = iter; a.c_iter = cj;
         a.M = m->M; a.D_m = m->D_m; a.D_e = m->D_e; a.direct = direct;
         a.n_nodes = n_nodes; a.src = g->src; a.dst = g->dst; a.src_pos = src_pos;
-        a.dst_pos = dst_pos; a.win = st->win; a.ver = ver;
+        a.dst_pos = dst_pos; a.win = st->win; a.tag = tag; a.ver = ver;
         a.t = g->t; a.mem_ts = mem_ts; a.mail_ts = mail_ts; a.efeat = g->efeat;
         a.mem_new = mem_new;
         a.r_flag = st->r_flag + base; a.r_node = st->r_node + base;
@@ -1245,7 +1261,7 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
     }
     if (winner && cap > 0) {
         TGM_LAUNCH(k_winner_out, dim3(cdiv(cap, 256)), dim3(256), 0, s, n_nodes, cap,
-                           first_event, st->win, winner);
+                   first_event, st->win, tag, winner);
     }
     if (fuse) {
         st->ring[cj % slots].staged = false;

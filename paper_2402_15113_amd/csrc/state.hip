@@ -8,7 +8,8 @@ namespace {
 
 __global__ void k_state_init(int32_t N, int32_t M, int32_t D_m, float *__restrict__ mem,
                              double *__restrict__ mem_ts, float *__restrict__ mail,
-                             double *__restrict__ mail_ts, int32_t *__restrict__ ver)
+                             double *__restrict__ mail_ts, int32_t *__restrict__ ver,
+                             uint64_t *__restrict__ win)
 {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t t0 = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -20,6 +21,7 @@ __global__ void k_state_init(int32_t N, int32_t M, int32_t D_m, float *__restric
         mem_ts[k] = 0.0;
         mail_ts[k] = 0.0;
         ver[k] = -1;
+        win[k] = 0;
     }
 }
 
@@ -100,8 +102,9 @@ extern "C" tgm_status_t tgm_state_reset(tgm_state_t st, void *stream)
     if (!st)
         return TGM_EINVAL;
     hipLaunchKernelGGL(k_state_init, dim3(1024), dim3(256), 0, as_stream(stream), st->N, st->M,
-                       st->D_m, st->mem, st->mem_ts, st->mail, st->mail_ts, st->ver);
+                       st->D_m, st->mem, st->mem_ts, st->mail, st->mail_ts, st->ver, st->win);
     TGM_LAUNCHED();
+    st->win_tag = 0;
     for (auto &sl : st->ring)
         sl = tgm_state::Slot();
     st->committed_through = -1;
@@ -155,7 +158,7 @@ extern "C" tgm_status_t tgm_state_create(int32_t N, int32_t M, int32_t D_m, int3
               hipMalloc(&st->r_mail, sizeof(float) * (rows * D_m + 1)) == hipSuccess &&
               hipMalloc(&st->r_mem_ts, sizeof(double) * rows) == hipSuccess &&
               hipMalloc(&st->r_mail_ts, sizeof(double) * rows) == hipSuccess &&
-              hipMalloc(&st->win, sizeof(int32_t) * N) == hipSuccess;
+              hipMalloc(&st->win, sizeof(uint64_t) * N) == hipSuccess;
     if (!ok) {
         tgm_state_destroy(st);
         return TGM_ENOMEM;
