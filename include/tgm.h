@@ -118,6 +118,16 @@ tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t R, const i
                           int32_t nb, int32_t *nodes, int32_t *n_nodes, int32_t cap,
                           int32_t *root_pos, int32_t *nbr_pos, void *stream);
 
+/* tgm_sample_batch followed by tgm_node_set over its outputs, with the node
+ * marks made by the sampler itself (one launch fewer): same outputs as the
+ * two calls (root, root_ts, nbr, eid, nts, cnt; nodes, *n_nodes, root_pos
+ * [3b], nbr_pos [3b x nb]); cap >= min(N, 3b (nb + 1)).  Uses the graph's
+ * scratch like tgm_node_set. */
+tgm_status_t tgm_sample_nodes(tgm_graph_t g, int64_t first_event, int32_t b, int32_t nb,
+                              int32_t *root, double *root_ts, int32_t *nbr, int32_t *eid,
+                              double *nts, int32_t *cnt, int32_t *nodes, int32_t *n_nodes,
+                              int32_t cap, int32_t *root_pos, int32_t *nbr_pos, void *stream);
+
 /* ------------------------------------------------------------------------
  * Node memory and mailbox (Sec. 2: node memory s_v; Sec. 3.1, Eq. 2: reads
  * of stale memory).  Per node: mem [M] fp32, mem_ts fp64 (time of the last

@@ -109,10 +109,14 @@ __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
                                            const AdjRec *__restrict__ adj, int r, int32_t v,
                                            double tq, int32_t N, int32_t nb,
                                            int32_t *__restrict__ nbr, int32_t *__restrict__ eid,
-                                           double *__restrict__ nts, int32_t *__restrict__ cnt)
+                                           double *__restrict__ nts, int32_t *__restrict__ cnt,
+                                           int32_t *__restrict__ stamp = nullptr,
+                                           int32_t epoch = 0)
 {
     const int lane = threadIdx.x & 63;
     const bool ok = v >= 0 && v < N;   // an id out of range samples nothing
+    if (stamp && ok && lane == 0)      // node-set mark of the root (see k_ns_mark)
+        stamp[v] = epoch;
     const int64_t base = ok ? off[v] : 0;
     int64_t lo = base, hi = ok ? off[v + 1] : 0;
     while (hi - lo > kWave) {
@@ -137,6 +141,8 @@ __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
             nbr[o] = a.nbr;
             eid[o] = a.eid;
             nts[o] = a.ts;
+            if (stamp)   // adjacency ids are in [0, N): checked at graph creation
+                stamp[a.nbr] = epoch;
         } else {
             nbr[o] = -1;
             eid[o] = -1;
@@ -169,7 +175,8 @@ __global__ __launch_bounds__(256) void k_sample_batch(
     const int32_t *__restrict__ src, const int32_t *__restrict__ dst,
     const int32_t *__restrict__ neg, const double *__restrict__ t, int32_t N, int32_t nb,
     int32_t *__restrict__ root, double *__restrict__ root_ts, int32_t *__restrict__ nbr,
-    int32_t *__restrict__ eid, double *__restrict__ nts, int32_t *__restrict__ cnt)
+    int32_t *__restrict__ eid, double *__restrict__ nts, int32_t *__restrict__ cnt,
+    int32_t *__restrict__ stamp, int32_t epoch)
 {
     const int r = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
     if (r >= 3 * b)
@@ -182,7 +189,7 @@ __global__ __launch_bounds__(256) void k_sample_batch(
         root[r] = v;
         root_ts[r] = tq;
     }
-    sample_one(off, adj, r, v, tq, N, nb, nbr, eid, nts, cnt);
+    sample_one(off, adj, r, v, tq, N, nb, nbr, eid, nts, cnt, stamp, epoch);
 }
 
 // ------------------------------------------------------------ node set
@@ -486,14 +493,15 @@ extern "C" tgm_status_t tgm_sample_batch(tgm_graph_t g, int64_t first_event, int
     const int per_block = 256 / kWave;
     TGM_LAUNCH(k_sample_batch, dim3(cdiv(3 * (int64_t)b, per_block)), dim3(256), 0,
                as_stream(stream), g->off, g->adj, first_event, b, g->src, g->dst, g->neg, g->t,
-               g->N, nb, root, root_ts, nbr, eid, nts, cnt);
+               g->N, nb, root, root_ts, nbr, eid, nts, cnt, nullptr, 0);
     return TGM_OK;
 }
 
-extern "C" tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t R,
-                                     const int32_t *nbr, int32_t nb, int32_t *nodes,
-                                     int32_t *n_nodes, int32_t cap, int32_t *root_pos,
-                                     int32_t *nbr_pos, void *stream)
+namespace {
+
+tgm_status_t ns_check(tgm_graph_t g, int32_t R, int32_t nb, const int32_t *root,
+                      const int32_t *nbr, const int32_t *nodes, const int32_t *n_nodes,
+                      int32_t cap, const int32_t *root_pos, const int32_t *nbr_pos)
 {
     if (!g || R < 0 || nb < 0 || !n_nodes || (int64_t)R * (nb + 1) > INT32_MAX)
         return TGM_EINVAL;
@@ -502,9 +510,28 @@ extern "C" tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t
         return TGM_ESIZE;
     if ((R > 0 && (!root || !nodes || !root_pos)) || ((int64_t)R * nb > 0 && (!nbr || !nbr_pos)))
         return TGM_EINVAL;
-    const int NW = (g->N + 63) >> 6;
-    if (NW > kNsMaxWords)
+    if (((g->N + 63) >> 6) > kNsMaxWords)
         return TGM_EINVAL;
+    return TGM_OK;
+}
+
+// The epoch of a new node set (stamps of older sets never equal it).
+tgm_status_t ns_next_epoch(tgm_graph_t g, hipStream_t s, int32_t *epoch)
+{
+    if (g->ns_epoch == INT32_MAX) {   // stamps restart from zero
+        TGM_LAUNCH(k_fill_i32, dim3(cdiv(g->N, 256)), dim3(256), 0, s, g->ns_stamp, g->N, 0);
+        g->ns_epoch = 0;
+    }
+    *epoch = ++g->ns_epoch;
+    return TGM_OK;
+}
+
+// Ranking of the ids stamped with `epoch`: U, its size and the positions.
+tgm_status_t ns_rank(tgm_graph_t g, const int32_t *root, int32_t R, const int32_t *nbr,
+                     int32_t nb, int32_t *nodes, int32_t *n_nodes, int32_t *root_pos,
+                     int32_t *nbr_pos, int32_t epoch, hipStream_t s)
+{
+    const int NW = (g->N + 63) >> 6;
     const size_t lds = (sizeof(uint64_t) + sizeof(uint32_t)) * NW;
     static bool lds_opt_in = false;
     if (!lds_opt_in) {
@@ -513,17 +540,57 @@ extern "C" tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t
                                     (int)((sizeof(uint64_t) + sizeof(uint32_t)) * kNsMaxWords)));
         lds_opt_in = true;
     }
+    const int32_t total = (int32_t)((int64_t)R * (nb + 1));
+    TGM_LAUNCH(k_ns_pos, dim3((unsigned)std::max<int64_t>(1, cdiv(total, kNsIdsPerBlock))),
+               dim3(kNsThreads), lds, s, g->N, g->ns_stamp, epoch, root, R, nbr, total, nodes,
+               n_nodes, root_pos, nbr_pos);
+    return TGM_OK;
+}
+
+}  // namespace
+
+extern "C" tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t R,
+                                     const int32_t *nbr, int32_t nb, int32_t *nodes,
+                                     int32_t *n_nodes, int32_t cap, int32_t *root_pos,
+                                     int32_t *nbr_pos, void *stream)
+{
+    tgm_status_t st = ns_check(g, R, nb, root, nbr, nodes, n_nodes, cap, root_pos, nbr_pos);
+    if (st != TGM_OK)
+        return st;
     hipStream_t s = as_stream(stream);
-    if (g->ns_epoch == INT32_MAX) {   // stamps restart from zero
-        TGM_LAUNCH(k_fill_i32, dim3(cdiv(g->N, 256)), dim3(256), 0, s, g->ns_stamp, g->N, 0);
-        g->ns_epoch = 0;
-    }
-    const int32_t epoch = ++g->ns_epoch;
+    int32_t epoch = 0;
+    if ((st = ns_next_epoch(g, s, &epoch)) != TGM_OK)
+        return st;
     const int32_t total = (int32_t)((int64_t)R * (nb + 1));
     if (total > 0)
         TGM_LAUNCH(k_ns_mark, dim3(cdiv(total, 256)), dim3(256), 0, s, g->N, root, R, nbr, total,
                    g->ns_stamp, epoch);
-    TGM_LAUNCH(k_ns_pos, dim3((unsigned)std::max<int64_t>(1, cdiv(total, kNsIdsPerBlock))), dim3(kNsThreads), lds, s,
-               g->N, g->ns_stamp, epoch, root, R, nbr, total, nodes, n_nodes, root_pos, nbr_pos);
-    return TGM_OK;
+    return ns_rank(g, root, R, nbr, nb, nodes, n_nodes, root_pos, nbr_pos, epoch, s);
+}
+
+extern "C" tgm_status_t tgm_sample_nodes(tgm_graph_t g, int64_t first_event, int32_t b,
+                                         int32_t nb, int32_t *root, double *root_ts,
+                                         int32_t *nbr, int32_t *eid, double *nts, int32_t *cnt,
+                                         int32_t *nodes, int32_t *n_nodes, int32_t cap,
+                                         int32_t *root_pos, int32_t *nbr_pos, void *stream)
+{
+    if (!g || b < 0 || first_event < 0 || first_event + b > g->E || nb < 1 || nb > kWave)
+        return TGM_EINVAL;
+    if (b > 0 && (!root || !root_ts || !nbr || !eid || !nts || !cnt))
+        return TGM_EINVAL;
+    const int32_t R = 3 * b;
+    tgm_status_t st = ns_check(g, R, nb, root, nbr, nodes, n_nodes, cap, root_pos, nbr_pos);
+    if (st != TGM_OK)
+        return st;
+    hipStream_t s = as_stream(stream);
+    int32_t epoch = 0;
+    if ((st = ns_next_epoch(g, s, &epoch)) != TGM_OK)
+        return st;
+    if (b > 0) {   // the sampler stamps every root and neighbour it writes
+        const int per_block = 256 / kWave;
+        TGM_LAUNCH(k_sample_batch, dim3(cdiv(3 * (int64_t)b, per_block)), dim3(256), 0, s, g->off,
+                   g->adj, first_event, b, g->src, g->dst, g->neg, g->t, g->N, nb, root,
+                   root_ts, nbr, eid, nts, cnt, g->ns_stamp, epoch);
+    }
+    return ns_rank(g, root, R, nbr, nb, nodes, n_nodes, root_pos, nbr_pos, epoch, s);
 }

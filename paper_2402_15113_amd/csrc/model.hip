@@ -448,100 +448,114 @@ __global__ void k_winner_out(const int32_t *__restrict__ n_nodes, int32_t cap, i
 // Node projections P[p] = s'_p [W_q^s; W_k^s; W_v^s]^T: the memory part of the
 // query, key and value projections depends only on the node, so it is
 // computed once per node of the set instead of once per slot.
+constexpr int kProjMaxPC = 8;   // k-chunks of the node projection (K = M <= 128)
+
+// Persistent over 16-row tiles (launched with 4..8 waves); wave w owns column
+// blocks w, w + nw, w + 2nw (a block past the last is a copy of w: it stores
+// the same values) and keeps all their weights in registers, loaded once
+// while the first tile's rows are in flight; the next tile's rows load while
+// a tile multiplies.  Three independent accumulators per wave.
+template <int W, int C>
+__device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ mem_new, int M,
+                                               int PC, const f4 *__restrict__ pb, int PNB,
+                                               const float *__restrict__ pbias,
+                                               float *__restrict__ P, float *lds)
+{
+    const int K = PC * 16, SA = K + 4, ldP = PNB * 16;
+    const int nw = blockDim.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
+    const bool has_cb = wave < PNB;
+    const int cb0 = has_cb ? wave : 0;
+    const int cb1 = wave + nw < PNB ? wave + nw : cb0;
+    const int cb2 = wave + 2 * nw < PNB ? wave + 2 * nw : cb0;
+    const float *arow = lds + (lane & 15) * SA + 4 * (lane >> 4);
+
+    // rows of tile row0: wave w takes rows w + nw i (nw >= 4)
+    int64_t off[4];
+    int lr[4];
+    auto rows_of = [&](int row0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = wave + nw * i;
+            lr[i] = r < 16 ? r : -1;
+            off[i] = (r < 16 && row0 + r < n) ? (int64_t)(row0 + r) * M : -1;
+        }
+    };
+    int row0 = blockIdx.x * 16;
+    WaveRows<W, 4, C> x;
+    rows_of(row0);
+    x.load(mem_new, off, M, lane);
+    f4 w[kProjMaxPC][3];
+    const int64_t kstep = (int64_t)PNB * kWave;
+#pragma unroll
+    for (int kc = 0; kc < kProjMaxPC; ++kc) {   // chunks past PC reload chunk 0, unused
+        const f4 *p = pb + (int64_t)(kc < PC ? kc : 0) * kstep + lane;
+        w[kc][0] = p[(int64_t)cb0 * kWave];
+        w[kc][1] = p[(int64_t)cb1 * kWave];
+        w[kc][2] = p[(int64_t)cb2 * kWave];
+    }
+    const float e0 = pbias[cb0 * 16 + (lane & 15)], e1 = pbias[cb1 * 16 + (lane & 15)],
+                e2 = pbias[cb2 * 16 + (lane & 15)];
+    for (;;) {
+        __syncthreads();   // the previous tile is done with LDS
+        x.store(lds, SA, 0, lr, off, M, lane);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (lr[i] >= 0)
+                for (int k = M + lane; k < K; k += kWave)
+                    lds[lr[i] * SA + k] = 0.f;
+        __syncthreads();
+        const int next = row0 + gridDim.x * 16;
+        if (next < n) {
+            rows_of(next);
+            x.load(mem_new, off, M, lane);
+        }
+        if (has_cb) {
+            f4 c0 = {0, 0, 0, 0}, c1 = c0, c2 = c0;
+#pragma unroll
+            for (int kc = 0; kc < kProjMaxPC; ++kc) {
+                if (kc < PC) {
+                    const f4 a = *reinterpret_cast<const f4 *>(arow + kc * 16);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        c0 = mfma_16x16x4(a[j], w[kc][0][j], c0);
+                        c1 = mfma_16x16x4(a[j], w[kc][1][j], c1);
+                        c2 = mfma_16x16x4(a[j], w[kc][2][j], c2);
+                    }
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int r = row0 + 4 * (lane >> 4) + v;
+                if (r < n) {
+                    float *out = P + (int64_t)r * ldP + (lane & 15);
+                    out[cb0 * 16] = c0[v] + e0;
+                    out[cb1 * 16] = c1[v] + e1;
+                    out[cb2 * 16] = c2[v] + e2;
+                }
+            }
+        }
+        if (next >= n)
+            break;
+        row0 = next;
+    }
+}
+
 __global__ __launch_bounds__(512) void k_node_proj(const int32_t *__restrict__ n_nodes,
                                                    const float *__restrict__ mem_new, int M,
                                                    int PC, const f4 *__restrict__ pb, int PNB,
                                                    const float *__restrict__ pbias,
                                                    float *__restrict__ P)
 {
-    // persistent over 16-row tiles (launched with 4..8 waves); wave w owns
-    // column blocks w, w + nw, w + 2nw
-    // (a block past the last is a copy of w: it stores the same values), three
-    // independent accumulators fed from double-buffered weight registers
     extern __shared__ float lds[];
     const int n = *n_nodes;
-    const int K = PC * 16, SA = K + 4, ldP = PNB * 16;
-    const int nw = blockDim.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
-    const int cb0 = wave;
-    const int cb1 = wave + nw < PNB ? wave + nw : wave;
-    const int cb2 = wave + 2 * nw < PNB ? wave + 2 * nw : wave;
-    const int64_t o1 = (int64_t)(cb1 - cb0) * kWave, o2 = (int64_t)(cb2 - cb0) * kWave;
-    const int64_t kstep = (int64_t)PNB * kWave;
-    const float *arow = lds + (lane & 15) * SA + 4 * (lane >> 4);
-    for (int row0 = blockIdx.x * 16; row0 < n; row0 += gridDim.x * 16) {
-        __syncthreads();   // the previous tile is done with LDS
-        {
-            int64_t off[4];
-            int lr[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {   // wave w stages rows w + nw i (nw >= 4)
-                const int r = wave + nw * i;
-                lr[i] = r < 16 ? r : -1;
-                off[i] = (r < 16 && row0 + r < n) ? (int64_t)(row0 + r) * M : -1;
-            }
-            if ((M & 3) == 0 && (reinterpret_cast<uintptr_t>(mem_new) & 15) == 0) {
-                WaveRows<4, 4, 1> x;
-                x.load(mem_new, off, M, lane);
-                x.store(lds, SA, 0, lr, off, M, lane);
-            } else {
-                WaveRows<1, 4, 2> x;
-                x.load(mem_new, off, M, lane);
-                x.store(lds, SA, 0, lr, off, M, lane);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (lr[i] >= 0)
-                    for (int k = M + lane; k < K; k += kWave)
-                        lds[lr[i] * SA + k] = 0.f;
-        }
-        __syncthreads();
-        if (cb0 >= PNB)
-            continue;
-        f4 c0 = {0, 0, 0, 0}, c1 = c0, c2 = c0;
-        const f4 *p = pb + (int64_t)cb0 * kWave + lane;
-        f4 x0 = p[0], x1 = p[o1], x2 = p[o2];
-        keep_loaded(x0);
-        keep_loaded(x1);
-        keep_loaded(x2);
-        auto mma = [&](int kc, const f4 w0, const f4 w1, const f4 w2) {
-            const f4 a = *reinterpret_cast<const f4 *>(arow + kc * 16);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                c0 = mfma_16x16x4(a[j], w0[j], c0);
-                c1 = mfma_16x16x4(a[j], w1[j], c1);
-                c2 = mfma_16x16x4(a[j], w2[j], c2);
-            }
-        };
-        int kc = 0;
-        for (; kc + 1 < PC; kc += 2) {   // weights carry padding chunks past the end
-            const f4 *q = p + kstep;
-            const f4 y0 = q[0], y1 = q[o1], y2 = q[o2];
-            issue_fence();
-            mma(kc, x0, x1, x2);
-            p += 2 * kstep;
-            x0 = p[0];
-            x1 = p[o1];
-            x2 = p[o2];
-            issue_fence();
-            mma(kc + 1, y0, y1, y2);
-        }
-        if (kc < PC)
-            mma(kc, x0, x1, x2);
-        const float e0 = pbias[cb0 * 16 + (lane & 15)], e1 = pbias[cb1 * 16 + (lane & 15)],
-                    e2 = pbias[cb2 * 16 + (lane & 15)];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int r = row0 + 4 * (lane >> 4) + v;
-            if (r < n) {
-                float *out = P + (int64_t)r * ldP + (lane & 15);
-                out[cb0 * 16] = c0[v] + e0;
-                out[cb1 * 16] = c1[v] + e1;
-                out[cb2 * 16] = c2[v] + e2;
-            }
-        }
-    }
+    if ((int)blockIdx.x * 16 >= n)
+        return;
+    if ((M & 3) == 0 && (reinterpret_cast<uintptr_t>(mem_new) & 15) == 0)
+        node_proj_body<4, 1>(n, mem_new, M, PC, pb, PNB, pbias, P, lds);
+    else
+        node_proj_body<1, 2>(n, mem_new, M, PC, pb, PNB, pbias, P, lds);
 }
 
 struct AttnArgs {

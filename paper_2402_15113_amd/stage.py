@@ -2,7 +2,7 @@
 
 ``Stage`` owns the library handles and every per-batch device buffer
 (allocated once, through torch), and issues, for iteration i, the calls
-tgm_sample_batch (roots + sampling) -> tgm_node_set -> tgm_fetch_memory ->
+tgm_sample_nodes (roots + sampling + node set) -> tgm_fetch_memory ->
 tgm_update_memory -> tgm_embed on one stream.  It holds no arithmetic of the
 method: all of it runs in the library's kernels.
 """
@@ -81,10 +81,9 @@ class Stage:
         b = hi - lo
         R = 3 * b
         nb, cap, st = self.nb, self.cap, self.stream
-        tgm.tgm_sample_batch(self.g, lo, b, nb, self.root, self.root_ts, self.nbr, self.eid,
-                             self.nts, self.cnt, stream=st)
-        tgm.tgm_node_set(self.g, self.root, R, self.nbr, nb, self.nodes, self.n_nodes, cap,
-                         self.root_pos, self.nbr_pos, stream=st)
+        tgm.tgm_sample_nodes(self.g, lo, b, nb, self.root, self.root_ts, self.nbr, self.eid,
+                             self.nts, self.cnt, self.nodes, self.n_nodes, cap, self.root_pos,
+                             self.nbr_pos, stream=st)
         tgm.tgm_fetch_memory(self.st, i, self.nodes, self.n_nodes, cap, self.f_mem,
                              self.f_mem_ts, self.f_mail, self.f_mail_ts, self.f_ver, stream=st)
         tgm.tgm_update_memory(self.st, self.m, self.g, i, self.nodes, self.n_nodes, cap,

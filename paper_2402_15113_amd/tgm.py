@@ -20,7 +20,7 @@ TGM_OK, TGM_EINVAL, TGM_ERANGE, TGM_EORDER, TGM_ESIZE, TGM_EDEVICE, TGM_ENOMEM =
 # Every exported symbol of include/tgm.h
 SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_create",
            "tgm_graph_destroy", "tgm_graph_info", "tgm_batch_roots", "tgm_sample", "tgm_sample_batch",
-           "tgm_node_set", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
+           "tgm_node_set", "tgm_sample_nodes", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
            "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
@@ -72,6 +72,7 @@ def lib():
             "tgm_sample": [V, P, P, I32, I32, P, P, P, P, V],
             "tgm_sample_batch": [V, I64, I32, I32, P, P, P, P, P, P, V],
             "tgm_node_set": [V, P, I32, P, I32, P, P, I32, P, P, V],
+            "tgm_sample_nodes": [V, I64, I32, I32, P, P, P, P, P, P, P, P, I32, P, P, V],
             "tgm_state_create": [I32, I32, I32, I32, I32, V, C.POINTER(V)],
             "tgm_state_destroy": [V],
             "tgm_state_reset": [V, V],
@@ -189,6 +190,13 @@ def tgm_node_set(g, root, R, nbr, nb, nodes, n_nodes, cap, root_pos, nbr_pos, st
     _check("tgm_node_set", lib().tgm_node_set(g, _p(root), R, _p(nbr), nb, _p(nodes),
                                               _p(n_nodes), cap, _p(root_pos), _p(nbr_pos),
                                               _s(stream)))
+
+
+def tgm_sample_nodes(g, first_event, b, nb, root, root_ts, nbr, eid, nts, cnt, nodes, n_nodes, cap,
+                     root_pos, nbr_pos, stream=None):
+    _check("tgm_sample_nodes", lib().tgm_sample_nodes(
+        g, first_event, b, nb, _p(root), _p(root_ts), _p(nbr), _p(eid), _p(nts), _p(cnt),
+        _p(nodes), _p(n_nodes), cap, _p(root_pos), _p(nbr_pos), _s(stream)))
 
 
 # ------------------------------------------------------------------ state

@@ -313,6 +313,42 @@ def test_sample_batch_equals_roots_then_sample():
     st.close()
 
 
+def test_sample_nodes_equals_sample_batch_then_node_set():
+    """tgm_sample_nodes (sampler-made node marks) == tgm_sample_batch followed
+    by tgm_node_set, bit for bit, including on a graph with a self-loop-heavy,
+    tie-heavy stream."""
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    for wl in (make_workload("wiki", E=40_000), make_workload("lastfm", E=60_000)):
+        w = make_weights(wl.M, wl.D_e, wl.D_t)
+        st = from_workload(wl, w)
+        dev, nb, cap = st.dev, wl.nb, st.cap
+        for i in (0, 3, wl.n_iters - 1):
+            lo, hi = wl.batch(i)
+            b = hi - lo
+            R = 3 * b
+            print(f"[parity] sample_nodes {wl.name} iter {i} b={b}", flush=True)
+            tgm.tgm_sample_nodes(st.g, lo, b, nb, st.root, st.root_ts, st.nbr, st.eid, st.nts,
+                                 st.cnt, st.nodes, st.n_nodes, cap, st.root_pos, st.nbr_pos)
+            z = lambda shape, dt: torch.full(shape, -7, dtype=dt, device=dev)
+            root2, rts2 = z((R,), torch.int32), z((R,), torch.float64)
+            nbr2, eid2 = z((R, nb), torch.int32), z((R, nb), torch.int32)
+            nts2, cnt2 = z((R, nb), torch.float64), z((R,), torch.int32)
+            nodes2, n2 = z((cap,), torch.int32), z((1,), torch.int32)
+            rp2, np2 = z((R,), torch.int32), z((R, nb), torch.int32)
+            tgm.tgm_sample_batch(st.g, lo, b, nb, root2, rts2, nbr2, eid2, nts2, cnt2)
+            tgm.tgm_node_set(st.g, root2, R, nbr2, nb, nodes2, n2, cap, rp2, np2)
+            torch.cuda.synchronize()
+            n = int(n2.item())
+            assert int(st.n_nodes.item()) == n
+            for a, c in ((st.root[:R], root2), (st.root_ts[:R], rts2), (st.nbr[:R], nbr2),
+                         (st.eid[:R], eid2), (st.nts[:R], nts2), (st.cnt[:R], cnt2),
+                         (st.nodes[:n], nodes2[:n]), (st.root_pos[:R], rp2),
+                         (st.nbr_pos[:R], np2)):
+                assert torch.equal(a, c)
+        st.close()
+
+
 @pytest.mark.parametrize("s", [1, 3])
 def test_fetch_ahead_order(orc, s):
     """With s >= 1 the fetch of iteration i+1 may be issued before the update of
