@@ -43,6 +43,7 @@ def log(*a):
 
 
 def source_hash(*names):
+    """Hash of the named kernel sources under paper_2402_15113_amd/csrc."""
     h = hashlib.sha256()
     for n in names:
         with open(os.path.join(ROOT, "paper_2402_15113_amd", "csrc", n), "rb") as f:
@@ -120,6 +121,64 @@ def work_model(wl, rows):
     }
 
 
+CSRC = ("common.h", "api.hip", "graph.hip", "state.hip", "model.hip")
+
+
+def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
+    """HBM traffic per launch of every stage kernel from two counter runs.
+
+    FETCH_SIZE and WRITE_SIZE are read in KiB per dispatch; each is scaled by
+    what it reads for the plain copy of copy_mib MiB (a kernel that moves
+    exactly that many bytes each way), so the figures are calibrated HBM
+    bytes.  The result is keyed to a hash of the kernel sources: once those
+    change, the bench reports traffic as unmeasured again."""
+    import csv
+    import re
+    assert copy_mib > 0, "--copy-probe-mib must give the size of the calibration copy"
+
+    def per_kernel(path, counter):
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            m = re.search(r"(k_[a-z0-9_]+)(<\d+>)?\(", name)
+            key = m.group(1) if m else ("copy" if "copy" in name.lower() else name[:40])
+            vals.setdefault(key, []).append(float(r["Counter_Value"]))
+        return vals
+
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    kib = copy_mib * 1024.0
+    # the calibration copy is the largest copy dispatch of the run
+    f_copy = max(fetch.get("copy", [0.0])) / kib
+    w_copy = max(write.get("copy", [0.0])) / kib
+    assert f_copy > 0 and w_copy > 0, "no copy dispatch in the counter files"
+    src_hash = source_hash(*CSRC)
+    out_dir = os.path.join(ROOT, "profiles")
+    rows = []
+    for k in sorted(set(fetch) & set(write)):
+        if not k.startswith("k_") or len(fetch[k]) < 2:   # per-step kernels only
+            continue
+        fk = sum(fetch[k]) / len(fetch[k])
+        wk = sum(write[k]) / len(write[k])
+        hbm = (fk / f_copy + wk / w_copy) * 1024.0
+        rows.append((k, len(fetch[k]), fk, wk, hbm))
+        rec = {"kernel": k, "workload": workload, "sources": list(CSRC),
+               "source_hash": src_hash, "dispatches": len(fetch[k]),
+               "fetch_kib_per_launch": fk, "write_kib_per_launch": wk,
+               "copy_factor": {"fetch": f_copy, "write": w_copy, "copy_mib": copy_mib},
+               "hbm_bytes_per_launch": hbm}
+        with open(os.path.join(out_dir, f"{k}_{workload}_pmc.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+    print(f"calibration copy of {copy_mib} MiB: FETCH_SIZE x{f_copy:.4f}, "
+          f"WRITE_SIZE x{w_copy:.4f}")
+    print("| kernel | dispatches | FETCH KiB | WRITE KiB | HBM MB / launch |")
+    print("|---|---|---|---|---|")
+    for k, n, fk, wk, hbm in rows:
+        print(f"| {k} | {n} | {fk:.1f} | {wk:.1f} | {hbm / 1e6:.3f} |")
+
+
 def cpu_baseline(wl, w, W, seconds):
     import oracle
     oracle.build(force=False)
@@ -154,10 +213,21 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB before pass 1 (the "
+                         "calibration kernel of the FETCH_SIZE / WRITE_SIZE counters)")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU: turn two rocprofv3 --pmc counter_collection.csv files (one "
+                         "FETCH_SIZE run, one WRITE_SIZE run, both with --copy-probe-mib) "
+                         "into profiles/<kernel>_<workload>_pmc.json")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_probe_mib,
+                    args.workload)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(see the sharding notes in DESIGN.md); use --gpus 1", file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the stage has no multi-GPU path; "
+              "use --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -174,6 +244,14 @@ def main():
     stage = from_workload(wl, w)
     stage.want_winner = False
     n_it = wl.n_iters
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
 
     # pass 1: timed
