@@ -7,6 +7,9 @@ Floating point (fetched memory and mail, updated memory s', embeddings h,
 committed tables): |gpu - oracle| <= 1e-5 + 1e-4 |oracle| element-wise
 (fp32 vs fp64).
 """
+import dataclasses
+import time
+
 import numpy as np
 import pytest
 
@@ -14,7 +17,8 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-from workloads import custom_workload, make_weights, make_workload  # noqa: E402
+from workloads import (CONFIGS, FEAT_CHUNK, custom_workload, edge_feature_rows,  # noqa: E402
+                       make_weights, make_workload)
 
 ATOL, RTOL = 1e-5, 1e-4
 
@@ -83,9 +87,18 @@ def compare_state(gs, os_):
     close("mail", gs["mail"], os_["mail"])
 
 
-def run_pair(orc, wl, w, n_iters=None, s=None, first=0, init=None, check_every=1):
-    from paper_2402_15113_amd.stage import from_workload
-    st = from_workload(wl, w, s=s)
+def run_pair(orc, wl, w, n_iters=None, s=None, first=0, init=None, check_every=1,
+             gpu_efeat=None):
+    """Run the GPU stage and the oracle side by side over iterations
+    first .. first + n_iters - 1 and compare every check_every-th step, then the
+    flushed tables.  gpu_efeat (a device tensor) replaces wl.efeat on the GPU
+    side only; it must hold the same values wherever either side reads."""
+    from paper_2402_15113_amd.stage import Stage, from_workload
+    if gpu_efeat is None:
+        st = from_workload(wl, w, s=s)
+    else:
+        st = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, gpu_efeat, w, M=wl.M, D_t=wl.D_t,
+                   H=wl.H, nb=wl.nb, B=wl.B, s=wl.s if s is None else s)
     o = orc.Oracle(wl, w, s=s)
     if init is not None:
         st.load_state(first, **init)
@@ -185,6 +198,141 @@ def test_mid_run_window_from_synthetic_state(orc):
                 mail_ts=np.minimum(mem_ts + np.floor(r.exponential(3600, N)), wl.t[lo - 1]),
                 ver=np.where(r.random(N) < 0.9, r.integers(0, j - 2, N), -1).astype(np.int32))
     run_pair(orc, wl, w, n_iters=16, first=j, init=init)
+
+
+# ------------------------------------------------------------------ GDELT-shaped
+# The full stream has 191,290,882 events and a 142 GB edge-feature table.  It
+# is generated once per session without features; the tests below read only
+# the feature rows they need (the rows of the events the oracle's sampler picks
+# and of the batch events), which both sides receive as a zero table with
+# those rows filled.
+_GDELT = {}
+
+
+def gdelt_stream():
+    if "wl" not in _GDELT:
+        print("[parity] generating the GDELT-shaped stream (191,290,882 events)", flush=True)
+        t0 = time.time()
+        _GDELT["wl"] = make_workload("gdelt", with_features=False)
+        print(f"[parity] generated in {time.time() - t0:.0f} s", flush=True)
+    return _GDELT["wl"]
+
+
+def gdelt_prefix(E):
+    """The first E events (all a batch < E / B can see: sampling is strictly
+    earlier and events are time-sorted)."""
+    full = gdelt_stream()
+    return dataclasses.replace(full, src=full.src[:E], dst=full.dst[:E], t=full.t[:E],
+                               neg=full.neg[:E])
+
+
+def window_rows(orc, wl, first, n):
+    """Feature rows read by batches first .. first + n - 1: the batch events and
+    the events the oracle's sampler picks for their roots."""
+    roots, rts = [], []
+    for i in range(first, first + n):
+        a, b = wl.batch(i)
+        roots += [wl.src[a:b], wl.dst[a:b], wl.neg[a:b]]
+        rts += [wl.t[a:b]] * 3
+    _, eid, _, _ = orc.sample(wl.N, wl.src, wl.dst, wl.t, np.concatenate(roots),
+                              np.concatenate(rts), wl.nb)
+    lo, hi = wl.batch(first)[0], wl.batch(first + n - 1)[1]
+    return np.unique(np.concatenate([eid[eid >= 0].ravel().astype(np.int64),
+                                     np.arange(lo, hi, dtype=np.int64)]))
+
+
+def sparse_features(wl, rows):
+    """Host table [E x D_e] that is zero except `rows` (untouched pages stay
+    unallocated), and the same table on the device."""
+    from concurrent.futures import ThreadPoolExecutor
+    E_full = CONFIGS[wl.name]["E"]
+    host = np.zeros((wl.E, wl.D_e), dtype=np.float32)
+
+    def fill(c):
+        lo = int(c) * FEAT_CHUNK
+        hi = min(lo + FEAT_CHUNK, wl.E)
+        sel = rows[(rows >= lo) & (rows < hi)]
+        host[sel] = edge_feature_rows(wl.seed, E_full, wl.D_e, lo, hi)[sel - lo]
+
+    with ThreadPoolExecutor(8) as ex:
+        list(ex.map(fill, np.unique(rows // FEAT_CHUNK)))
+    dev = torch.zeros((wl.E, wl.D_e), dtype=torch.float32, device="cuda")
+    dev[torch.from_numpy(rows).cuda()] = torch.from_numpy(host[rows]).cuda()
+    return host, dev
+
+
+def synthetic_state(wl, j, seed):
+    """A seeded memory state standing in for the one iteration j would see."""
+    r = np.random.default_rng(seed)
+    N, M, D_m = wl.N, wl.M, wl.D_m
+    lo, _ = wl.batch(j)
+    mem_ts = np.floor(r.uniform(0, wl.t[lo - 1], N))
+    return dict(mem=r.uniform(-1, 1, (N, M)).astype(np.float32).astype(np.float64),
+                mem_ts=mem_ts,
+                mail=r.standard_normal((N, D_m)).astype(np.float32).astype(np.float64),
+                mail_ts=np.minimum(mem_ts + np.floor(r.exponential(3600, N)), wl.t[lo - 1]),
+                ver=np.where(r.random(N) < 0.9, r.integers(0, j - 2, N), -1).astype(np.int32))
+
+
+def test_gdelt_first_batches(orc):
+    """GDELT-shaped stream at full model size (D_e 186, B 4000, s 4): the first
+    4 batches from the initial state."""
+    wl = gdelt_prefix(4 * 4000)
+    wl = dataclasses.replace(wl, efeat=edge_feature_rows(wl.seed, CONFIGS["gdelt"]["E"],
+                                                          wl.D_e, 0, wl.E))
+    w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random")
+    run_pair(orc, wl, w, n_iters=4)
+
+
+def test_gdelt_mid_run_window(orc):
+    """GDELT-shaped stream, batches 20,000 .. 20,003 on the real graph of their
+    first 80,016,000 events (80 M-event history, 59.5 GB feature table on the
+    device), both sides started from the same seeded synthetic state."""
+    j, n = 20_000, 4
+    wl = gdelt_prefix((j + n) * 4000)
+    rows = window_rows(orc, wl, j, n)
+    print(f"[parity] gdelt window: {len(rows)} feature rows", flush=True)
+    host, dev = sparse_features(wl, rows)
+    wl = dataclasses.replace(wl, efeat=host)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    run_pair(orc, wl, w, n_iters=n, first=j, init=synthetic_state(wl, j, 11), gpu_efeat=dev)
+    del dev
+    torch.cuda.empty_cache()
+
+
+def test_gdelt_sampler_full_graph(orc):
+    """The whole GDELT-shaped graph (191 M events, 382 M adjacency records): the
+    sampler at a random sample of (node, time) roots against the oracle's."""
+    from paper_2402_15113_amd import tgm
+    wl = gdelt_stream()
+    dev = torch.device("cuda:0")
+    T = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+    src, dst, t, neg = (T(wl.src, torch.int32), T(wl.dst, torch.int32), T(wl.t, torch.float64),
+                        T(wl.neg, torch.int32))
+    g = tgm.tgm_graph_create(wl.N, src, dst, t, neg, None)
+    r = np.random.default_rng(5)
+    R, nb = 8192, 10
+    deg = np.bincount(np.concatenate([wl.src[:1 << 24], wl.dst[:1 << 24]]), minlength=wl.N)
+    hot = np.argsort(deg)[-50:]
+    root = np.where(r.random(R) < 0.5, r.choice(hot, R), r.integers(0, wl.N, R)).astype(np.int32)
+    rts = np.where(r.random(R) < 0.5, wl.t[r.integers(0, wl.E, R)],
+                   r.uniform(-5, wl.t[-1] + 5, R))
+    nbr, eid, nts, cnt = (torch.empty((R, nb), dtype=torch.int32, device=dev),
+                          torch.empty((R, nb), dtype=torch.int32, device=dev),
+                          torch.empty((R, nb), dtype=torch.float64, device=dev),
+                          torch.empty(R, dtype=torch.int32, device=dev))
+    tgm.tgm_sample(g, T(root, torch.int32), T(rts, torch.float64), R, nb, nbr, eid, nts, cnt)
+    torch.cuda.synchronize()
+    onbr, oeid, onts, ocnt = orc.sample(wl.N, wl.src, wl.dst, wl.t, root, rts, nb)
+    exact("cnt", cnt.cpu().numpy(), ocnt)
+    exact("nbr", nbr.cpu().numpy(), onbr)
+    exact("eid", eid.cpu().numpy(), oeid)
+    exact("nts", nts.cpu().numpy(), onts)
+    _, _, _, n_adj = tgm.tgm_graph_info(g)
+    assert n_adj == 2 * wl.E - int((wl.src == wl.dst).sum())
+    tgm.tgm_graph_destroy(g)
+    del src, dst, t, neg
+    torch.cuda.empty_cache()
 
 
 def test_sampler_full_size_sampled_roots(orc):

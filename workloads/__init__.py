@@ -20,15 +20,17 @@ from __future__ import annotations
 
 import hashlib
 import math
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["Workload", "Weights", "CONFIGS", "make_workload", "make_weights",
+__all__ = ["Workload", "Weights", "CONFIGS", "FEAT_CHUNK", "make_workload", "make_weights",
            "edge_feature_rows", "config_names"]
 
 # Rows per independently keyed chunk of the edge-feature stream.
-_FEAT_CHUNK = 1 << 16
+FEAT_CHUNK = 1 << 16
+_FEAT_CHUNK = FEAT_CHUNK
 
 
 def _key(seed: int, name: str, chunk: int = 0) -> np.ndarray:
@@ -118,20 +120,40 @@ def config_names() -> list[str]:
     return list(CONFIGS)
 
 
+def _inverse_cdf(c: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """min(#{k : c[k] <= u}, n - 1) for every u (c non-decreasing, c[-1] == 1):
+    the inverse-CDF draw, as searchsorted(c, u, side='right'), run over blocks
+    of u on several threads (searchsorted releases the GIL; the result does not
+    depend on the split)."""
+    from concurrent.futures import ThreadPoolExecutor
+    n = len(c)
+    out = np.empty(len(u), dtype=np.int64)
+    step = 1 << 22
+
+    def block(lo):
+        out[lo:lo + step] = np.searchsorted(c, u[lo:lo + step], side="right")
+
+    if len(u) <= step:
+        block(0)
+    else:
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            list(ex.map(block, range(0, len(u), step)))
+    np.minimum(out, n - 1, out=out)
+    return out
+
+
 def _bounded_zipf(rng: np.random.Generator, n: int, a: float, size: int) -> np.ndarray:
     """Ranks 0..n-1 with P(rank k) proportional to (k+1)^-a."""
     w = np.arange(1, n + 1, dtype=np.float64) ** (-a)
     c = np.cumsum(w)
     c /= c[-1]
-    u = rng.random(size)
-    return np.minimum(np.searchsorted(c, u, side="right"), n - 1).astype(np.int64)
+    return _inverse_cdf(c, rng.random(size))
 
 
 def _weighted_choice(rng: np.random.Generator, w: np.ndarray, size: int) -> np.ndarray:
     c = np.cumsum(w.astype(np.float64))
     c /= c[-1]
-    u = rng.random(size)
-    return np.minimum(np.searchsorted(c, u, side="right"), len(w) - 1).astype(np.int64)
+    return _inverse_cdf(c, rng.random(size))
 
 
 def _sorted_int_seconds(rng: np.random.Generator, E: int, span: int) -> np.ndarray:
