@@ -51,28 +51,46 @@ def source_hash(*names):
     return h.hexdigest()[:16]
 
 
-def run_steps(stage, first_step, K, n_iters):
-    """Enqueue K steps starting at global step `first_step` (epochs wrap)."""
-    from paper_2402_15113_amd import tgm
-    for k in range(first_step, first_step + K):
-        i = k % n_iters
-        if i == 0 and k > 0:
-            tgm.tgm_state_reset(stage.st, stream=stage.stream)
-        stage.step(i)
+class Schedule:
+    """Which iteration global step k runs, and the state a pass starts from.
+
+    Full workloads run their batches 0, 1, ... and start each epoch from the
+    initial state (a reset inside the timed region when the steps wrap).  A
+    window run (GDELT-shaped) runs batches first, first + 1, ... from a loaded
+    state and never wraps within a pass."""
+
+    def __init__(self, stage, n_iters, first=0, init=None):
+        self.stage, self.first, self.init = stage, first, init
+        self.n = n_iters - first
+
+    def restart(self):
+        from paper_2402_15113_amd import tgm
+        if self.init is None:
+            tgm.tgm_state_reset(self.stage.st, stream=self.stage.stream)
+        else:
+            self.stage.load_state(self.first, **self.init)
+
+    def run(self, k0, K):
+        """Enqueue K steps starting at global step k0."""
+        for k in range(k0, k0 + K):
+            if k % self.n == 0 and k > 0:
+                self.restart()
+            self.stage.step(self.first + k % self.n)
+
+    def events(self, wl, k0, K):
+        return sum(wl.batch(self.first + k % self.n)[1] - wl.batch(self.first + k % self.n)[0]
+                   for k in range(k0, k0 + K))
 
 
-def account(stage, W, K, n_iters):
+def account(sched, W, K):
     """Per-step sizes of the timed steps, read back from an untimed replay."""
     import torch
-    from paper_2402_15113_amd import tgm
-    tgm.tgm_state_reset(stage.st, stream=stage.stream)
+    stage = sched.stage
+    sched.restart()
     stage.want_winner = True
     rows = []
     for k in range(W + K):
-        i = k % n_iters
-        if i == 0 and k > 0:
-            tgm.tgm_state_reset(stage.st, stream=stage.stream)
-        stage.step(i)
+        sched.run(k, 1)
         if k >= W:
             torch.cuda.synchronize()
             b = stage.last[1]
@@ -83,6 +101,57 @@ def account(stage, W, K, n_iters):
                              n_win=int((stage.winner[:n] >= 0).sum().item())))
     stage.want_winner = False
     return rows
+
+
+def window_setup(name, first, L, w):
+    """Stage for batches first .. first + L - 1 of a large stream: the graph of
+    every event up to the window's end, a device feature table that holds the
+    generator's rows from the oldest event the window samples onwards (zero
+    below: never read), and a seeded synthetic memory state at `first`."""
+    import dataclasses
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import torch
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import Stage
+    from workloads import CONFIGS, FEAT_CHUNK, edge_feature_rows, make_workload
+
+    full = make_workload(name, with_features=False)
+    E_end = min(full.E, (first + L) * full.B)
+    wl = dataclasses.replace(full, src=full.src[:E_end], dst=full.dst[:E_end],
+                             t=full.t[:E_end], neg=full.neg[:E_end])
+    efeat = torch.zeros((E_end, wl.D_e), dtype=torch.float32, device="cuda")
+    stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
+                  nb=wl.nb, B=wl.B, s=wl.s)
+    lo_row = first * wl.B
+    for i in range(first, first + L):   # the oldest event any window batch samples
+        a, b = wl.batch(i)
+        tgm.tgm_sample_batch(stage.g, a, b - a, wl.nb, stage.root, stage.root_ts, stage.nbr,
+                             stage.eid, stage.nts, stage.cnt, stream=stage.stream)
+        e = stage.eid[:3 * (b - a)]
+        lo_row = min(lo_row, int(torch.where(e >= 0, e, E_end).min().item()))
+    E_full = CONFIGS[name]["E"]
+
+    def rows(c):
+        a = max(lo_row, c * FEAT_CHUNK)
+        b = min(E_end, (c + 1) * FEAT_CHUNK)
+        return a, edge_feature_rows(wl.seed, E_full, wl.D_e, a, b)
+
+    with ThreadPoolExecutor(8) as ex:
+        for a, blk in ex.map(rows, range(lo_row // FEAT_CHUNK, (E_end - 1) // FEAT_CHUNK + 1)):
+            efeat[a:a + len(blk)] = torch.from_numpy(blk).to("cuda")
+    stage._efeat_keep = efeat
+    r = np.random.default_rng(11)
+    N, M, D_m = wl.N, wl.M, wl.D_m
+    t0 = wl.t[lo_row - 1] if lo_row > 0 else 0.0
+    mem_ts = np.floor(r.uniform(0, t0, N))
+    init = dict(mem=r.uniform(-1, 1, (N, M)), mem_ts=mem_ts, mail=r.standard_normal((N, D_m)),
+                mail_ts=np.minimum(mem_ts + np.floor(r.exponential(3600, N)), t0),
+                ver=np.where(r.random(N) < 0.9, r.integers(0, first - 2, N), -1))
+    log(f"window: batches {first}..{first + L - 1}, graph of {E_end} events, feature rows "
+        f"[{lo_row}, {E_end}) filled ({(E_end - lo_row) * wl.D_e * 4 / 1e9:.2f} GB)")
+    return wl, stage, init
 
 
 def work_model(wl, rows):
@@ -209,7 +278,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="wiki", help="wiki (default), tiny, reddit, lastfm")
+    ap.add_argument("--workload", default="wiki",
+                    help="wiki (default), tiny, reddit, lastfm; gdelt runs a window of batches "
+                         "starting at --first from a synthetic state")
+    ap.add_argument("--first", type=int, default=20_000, help="first batch of a gdelt window")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
@@ -238,12 +310,21 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     tgm.lib()
     K, W = args.steps, args.warmup
-    wl = make_workload(args.workload)
-    w = make_weights(wl.M, wl.D_e, wl.D_t)
-    log(f"workload {wl.name}: N={wl.N} E={wl.E} B={wl.B} s={wl.s} iters/epoch={wl.n_iters}")
-    stage = from_workload(wl, w)
+    window = args.workload == "gdelt"
+    if window:
+        from workloads import CONFIGS
+        c = CONFIGS["gdelt"]
+        w = make_weights(c["M"], c["D_e"], c["D_t"])
+        wl, stage, init = window_setup("gdelt", args.first, W + K, w)
+        sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
+        sched.restart()
+    else:
+        wl = make_workload(args.workload)
+        w = make_weights(wl.M, wl.D_e, wl.D_t)
+        stage = from_workload(wl, w)
+        sched = Schedule(stage, wl.n_iters)
+    log(f"workload {wl.name}: N={wl.N} E={wl.E} B={wl.B} s={wl.s} iters={wl.n_iters}")
     stage.want_winner = False
-    n_it = wl.n_iters
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -255,13 +336,13 @@ def main():
     torch.cuda.synchronize()
 
     # pass 1: timed
-    run_steps(stage, 0, W, n_it)
+    sched.run(0, W)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run_steps(stage, W, K, n_it)
+    sched.run(W, K)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    events = sum(min(wl.E, (k % n_it + 1) * wl.B) - (k % n_it) * wl.B for k in range(W, W + K))
+    events = sched.events(wl, W, K)
     value = events / dt
     log(f"timed: {K} steps, {events} events, {dt * 1e3:.2f} ms -> {value:,.0f} events/s")
 
@@ -275,13 +356,13 @@ def main():
 
     if not args.no_profile:
         # pass 2: per-kernel durations (HIP events on the launch stream)
-        tgm.tgm_state_reset(stage.st, stream=stage.stream)
-        run_steps(stage, 0, W, n_it)
+        sched.restart()
+        sched.run(0, W)
         torch.cuda.synchronize()
         tgm.tgm_profile_reset()
         tgm.tgm_profile_enable(True)
         tp = time.perf_counter()
-        run_steps(stage, W, K, n_it)
+        sched.run(W, K)
         torch.cuda.synchronize()
         tp = time.perf_counter() - tp
         tgm.tgm_profile_enable(False)
@@ -291,7 +372,7 @@ def main():
             n0, m0 = prof.get(base, (0, 0.0))
             prof[base] = (n0 + launches, m0 + ms)
         # pass 3: algorithmic work per launch
-        rows = account(stage, W, K, n_it)
+        rows = account(sched, W, K)
         work = work_model(wl, rows)
         kernels = {}
         for name, (launches, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
@@ -326,7 +407,10 @@ def main():
             f"{out['roofline']['unit']} ({100 * achieved / peak:.1f}% of peak)")
     stage.close()
 
-    if not args.no_cpu_baseline:
+    if window:
+        out["config"]["window"] = f"batches {args.first}..{args.first + W + K - 1} from a seeded " \
+                                  "synthetic memory state"
+    if not args.no_cpu_baseline and not window:
         log(f"oracle baseline ({args.cpu_seconds:.0f} s budget)")
         out["cpu_baseline"] = cpu_baseline(wl, w, W, args.cpu_seconds)
     print(json.dumps(out), flush=True)

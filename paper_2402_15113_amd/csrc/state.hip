@@ -1,5 +1,7 @@
 // Node memory / mailbox tables, the staleness-bounded write-back ring, and
 // the versioned fetch.
+#include <algorithm>
+
 #include "common.h"
 
 using namespace tgm;
@@ -240,7 +242,7 @@ extern "C" tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int
     if (cap == 0)
         return TGM_OK;
     TGM_LAUNCH(k_gather_state, dim3(cdiv(cap, 4)), dim3(256), 0, s, nodes, n_nodes,
-                       st->M, st->D_m, st->mem, st->mem_ts, st->mail, st->mail_ts, st->ver, mem,
-                       mem_ts, mail, mail_ts, ver);
+               st->M, st->D_m, st->mem, st->mem_ts, st->mail, st->mail_ts, st->ver, mem,
+               mem_ts, mail, mail_ts, ver);
     return TGM_OK;
 }
