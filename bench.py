@@ -12,8 +12,12 @@ the initial memory state (a reset inside the timed region).
 
 Passes:
   1. warm-up, then K timed steps bracketed by device synchronisation -> value;
-  2. the same steps again with the library's per-kernel HIP-event timing on
-     -> average launch duration per kernel (the roofline's denominator);
+     the steps are pipelined over two streams (Stage.run: the sample, node
+     set and fetch of batch i+1 run beside the update and embedding of batch
+     i, which staleness s >= 1 allows);
+  2. the same steps again, one after another on one stream, with the
+     library's per-kernel HIP-event timing on -> average launch duration per
+     kernel (the roofline's denominator);
   3. an untimed replay that reads back each step's sizes (valid slots, node
      set, nodes with mail) -> algorithmic flops and bytes per launch;
   4. the fp64 oracle on the host cores for a bounded sample of the same
@@ -70,12 +74,22 @@ class Schedule:
         else:
             self.stage.load_state(self.first, **self.init)
 
-    def run(self, k0, K):
-        """Enqueue K steps starting at global step k0."""
-        for k in range(k0, k0 + K):
+    def run(self, k0, K, pipelined=True):
+        """Enqueue K steps starting at global step k0: pipelined (prefetch of
+        step k+1 on a second stream beside step k, ``Stage.run``) or one step
+        after another on one stream (``Stage.step``)."""
+        k = k0
+        while k < k0 + K:
             if k % self.n == 0 and k > 0:
                 self.restart()
-            self.stage.step(self.first + k % self.n)
+            seg = min(k0 + K - k, self.n - k % self.n)
+            i = self.first + k % self.n
+            if pipelined:
+                self.stage.run(i, seg)
+            else:
+                for j in range(seg):
+                    self.stage.step(i + j)
+            k += seg
 
     def events(self, wl, k0, K):
         return sum(wl.batch(self.first + k % self.n)[1] - wl.batch(self.first + k % self.n)[0]
@@ -90,7 +104,7 @@ def account(sched, W, K):
     stage.want_winner = True
     rows = []
     for k in range(W + K):
-        sched.run(k, 1)
+        sched.run(k, 1, pipelined=False)
         if k >= W:
             torch.cuda.synchronize()
             b = stage.last[1]
@@ -352,17 +366,19 @@ def main():
            "config": {"workload": f"{wl.name}-shaped synthetic stream", "nodes": wl.N,
                       "events": wl.E, "edge_feat": wl.D_e, "memory": wl.M, "time_enc": wl.D_t,
                       "heads": wl.H, "global_batch": wl.B, "neighbours": wl.nb,
-                      "staleness": wl.s, "graph": wl.meta.get("graph", "")}}
+                      "staleness": wl.s, "graph": wl.meta.get("graph", ""),
+                      "pipeline": "two streams: sample + node set + fetch of batch i+1 beside "
+                                  "update + embed of batch i"}}
 
     if not args.no_profile:
         # pass 2: per-kernel durations (HIP events on the launch stream)
         sched.restart()
-        sched.run(0, W)
+        sched.run(0, W, pipelined=False)
         torch.cuda.synchronize()
         tgm.tgm_profile_reset()
         tgm.tgm_profile_enable(True)
         tp = time.perf_counter()
-        sched.run(W, K)
+        sched.run(W, K, pipelined=False)
         torch.cuda.synchronize()
         tp = time.perf_counter() - tp
         tgm.tgm_profile_enable(False)

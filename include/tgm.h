@@ -14,6 +14,8 @@
  *   tgm_update_memory  GRU memory update of U, latest-message reduce,
  *                      staged write-back of the batch's endpoints
  *   tgm_embed          time-encoded multi-head attention embedding of roots
+ *   tgm_stage_run      all of it for a range of iterations, sampling a chunk
+ *                      of iterations ahead on a second stream
  *
  * Conventions shared by every call:
  *  - All array arguments are DEVICE pointers unless marked "host".  Arrays are
@@ -31,7 +33,10 @@
  *    their destroy call.  Per-batch calls allocate nothing.  Arrays passed to
  *    tgm_graph_create are BORROWED: they must stay alive and unchanged until
  *    the graph is destroyed.
- *  - A handle must not be used from two streams or threads at once.
+ *  - A handle must not be used from two threads at once.  Calls on one
+ *    handle must be stream-ordered, except that tgm_sample_nodes and
+ *    tgm_node_set (which touch only the graph's event arrays and node-set
+ *    scratch) may run on another stream beside the state and model calls.
  */
 #ifndef TGM_H
 #define TGM_H
@@ -241,6 +246,48 @@ tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
                        const int32_t *eid, const double *nts, const int32_t *cnt,
                        const float *mem_new, const int32_t *n_nodes, int32_t cap, float *h,
                        void *stream);
+
+/* ------------------------------------------------------------------------
+ * Pipelined executor.  Runs iterations i0 .. i0+n-1 of the stage (the batch of
+ * iteration i is events [iB, min(E, (i+1)B))).  The sample and node set of an
+ * iteration depend on the event stream only (Sec. 3.1: MSPipe prefetches
+ * them), so they run a chunk of nsb/2 iterations ahead on prefetch_stream,
+ * into sample buffer set (i - i0) % nsb; the fetch, update and embedding of
+ * each iteration run in order on `stream` with one set of fetch buffers.
+ * The streams synchronise once per chunk.  The prefetch stream starts after
+ * everything issued before on `stream`, and `stream` ends after the last
+ * embedding.  Results equal those of issuing tgm_sample_nodes,
+ * tgm_fetch_memory, tgm_update_memory and tgm_embed per iteration in order
+ * on one stream.  nsb >= 2 and even; nb, cap as for the calls above;
+ * mem_new [cap x M], new_mem_ts [cap] (may be NULL), winner [cap] (may be
+ * NULL) and h [3B x M] hold the last iteration's outputs.  The two streams
+ * must differ.  Errors of the underlying calls are returned as they occur
+ * (the iterations before stay enqueued). */
+typedef struct {
+    int32_t *root;      /* [3B] */
+    double *root_ts;    /* [3B] */
+    int32_t *nbr, *eid; /* [3B x nb] */
+    double *nts;        /* [3B x nb] */
+    int32_t *cnt;       /* [3B] */
+    int32_t *nodes;     /* [cap] */
+    int32_t *n_nodes;   /* [1] */
+    int32_t *root_pos;  /* [3B] */
+    int32_t *nbr_pos;   /* [3B x nb] */
+} tgm_sample_buffers;
+
+typedef struct {
+    float *mem;         /* [cap x M] */
+    double *mem_ts;     /* [cap] */
+    float *mail;        /* [cap x D_m] */
+    double *mail_ts;    /* [cap] */
+    int32_t *ver;       /* [cap] */
+} tgm_fetch_buffers;
+
+tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t i0, int64_t n,
+                           int32_t B, int32_t nb, int32_t cap, const tgm_sample_buffers *sb,
+                           int32_t nsb, const tgm_fetch_buffers *fb, float *mem_new,
+                           double *new_mem_ts, int64_t *winner, float *h, void *stream,
+                           void *prefetch_stream);
 
 /* ------------------------------------------------------------------------
  * Per-kernel timing.  When enabled, every kernel the library launches is

@@ -1,10 +1,18 @@
 """Runs the per-batch memory-module stage through libtgm.
 
 ``Stage`` owns the library handles and every per-batch device buffer
-(allocated once, through torch), and issues, for iteration i, the calls
-tgm_sample_nodes (roots + sampling + node set) -> tgm_fetch_memory ->
-tgm_update_memory -> tgm_embed on one stream.  It holds no arithmetic of the
-method: all of it runs in the library's kernels.
+(allocated once, through torch).  Iteration i is tgm_sample_nodes (roots,
+sampling, node set), tgm_fetch_memory (state as of iteration i-1-s),
+tgm_update_memory (GRU, latest-message reduce, staged write-back) and
+tgm_embed.
+
+``step(i)`` issues the four calls on one stream.  ``run(i0, n)`` hands
+iterations i0 .. i0+n-1 to the library's pipelined executor
+(tgm_stage_run): the sample and node set, which depend on the event stream
+only, run a chunk of iterations ahead on a second stream (the prefetch of
+Sec. 3.1), into sample buffer set (i - i0) % nsb.  Results are identical to
+``step`` (tested).  The class holds no arithmetic of the method: all of it
+runs in the library's kernels.
 """
 from __future__ import annotations
 
@@ -12,6 +20,25 @@ import numpy as np
 import torch
 
 from . import tgm
+
+# sample and node-set buffers of one batch (``Stage.<name>`` reads the set of
+# the last iteration)
+_SAMPLE_BUFFERS = ("root", "root_ts", "nbr", "eid", "nts", "cnt", "nodes", "n_nodes", "root_pos",
+                   "nbr_pos")
+_SETS = 16   # sample buffer sets of the pipelined executor: chunks of 8 iterations
+
+
+class _Sample:
+    """Sample and node-set buffers of one batch."""
+
+    def __init__(self, dev, R, nb, cap):
+        i32, f64 = torch.int32, torch.float64
+        z = lambda shape, dt: torch.zeros(shape, dtype=dt, device=dev)
+        self.root, self.root_ts = z(R, i32), z(R, f64)
+        self.nbr, self.eid, self.nts = z((R, nb), i32), z((R, nb), i32), z((R, nb), f64)
+        self.cnt = z(R, i32)
+        self.nodes, self.n_nodes = z(cap, i32), z(1, i32)
+        self.root_pos, self.nbr_pos = z(R, i32), z((R, nb), i32)
 
 
 class Stage:
@@ -22,6 +49,7 @@ class Stage:
         dev = torch.device(device)
         self.dev = dev
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
+        self.pre_stream = torch.cuda.Stream(dev)   # default priority
         T = lambda a, dt: a.to(dev, dt).contiguous() if torch.is_tensor(a) else \
             torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
         self.src = T(src, torch.int32)
@@ -41,29 +69,31 @@ class Stage:
                                       stream=st)
         self.st = tgm.tgm_state_create(self.N, M, self.D_m, s, B, stream=st)
         self.m = tgm.tgm_model_create(M, self.D_e, D_t, H, nb, self.cap, R, weights, stream=st)
-        i32, f64, f32 = torch.int32, torch.float64, torch.float32
+        self.sets = [_Sample(dev, R, nb, self.cap) for _ in range(_SETS)]
         z = lambda shape, dt: torch.zeros(shape, dtype=dt, device=dev)
         cap = self.cap
-        self.root, self.root_ts = z(R, i32), z(R, f64)
-        self.nbr, self.eid, self.nts = z((R, nb), i32), z((R, nb), i32), z((R, nb), f64)
-        self.cnt = z(R, i32)
-        self.nodes, self.n_nodes = z(cap, i32), z(1, i32)
-        self.root_pos, self.nbr_pos = z(R, i32), z((R, nb), i32)
-        self.f_mem, self.f_mem_ts = z((cap, M), f32), z(cap, f64)
-        self.f_mail, self.f_mail_ts = z((cap, self.D_m), f32), z(cap, f64)
-        self.f_ver = z(cap, i32)
-        self.mem_new, self.new_mem_ts = z((cap, M), f32), z(cap, f64)
-        self.winner = z(cap, torch.int64)
-        self.h = z((R, M), f32)
+        self.f_mem, self.f_mem_ts = z((cap, M), torch.float32), z(cap, torch.float64)
+        self.f_mail, self.f_mail_ts = z((cap, self.D_m), torch.float32), z(cap, torch.float64)
+        self.f_ver = z(cap, torch.int32)
+        self.mem_new, self.new_mem_ts = z((self.cap, M), torch.float32), z(self.cap, torch.float64)
+        self.winner = z(self.cap, torch.int64)
+        self.h = z((R, M), torch.float32)
         self.want_winner = True
-        self.last = None
+        self.last = None      # (iteration, batch size) of the last issued iteration
+        self._set = 0         # its sample buffer set
+        self._bufs = None
+
+    def __getattr__(self, name):
+        if name in _SAMPLE_BUFFERS and "sets" in self.__dict__:
+            return getattr(self.sets[self.__dict__.get("_set", 0)], name)
+        raise AttributeError(name)
 
     def close(self):
         for fn, h in ((tgm.tgm_model_destroy, "m"), (tgm.tgm_state_destroy, "st"),
                       (tgm.tgm_graph_destroy, "g")):
-            if getattr(self, h, None) is not None:
-                fn(getattr(self, h))
-                setattr(self, h, None)
+            if self.__dict__.get(h) is not None:
+                fn(self.__dict__[h])
+                self.__dict__[h] = None
 
     def __del__(self):
         try:
@@ -76,37 +106,57 @@ class Stage:
         return lo, min(self.E, lo + self.B)
 
     def step(self, i: int):
-        """Enqueue iteration i (no synchronisation)."""
+        """Enqueue iteration i on the main stream (no synchronisation)."""
         lo, hi = self.batch(i)
-        b = hi - lo
-        R = 3 * b
-        nb, cap, st = self.nb, self.cap, self.stream
-        tgm.tgm_sample_nodes(self.g, lo, b, nb, self.root, self.root_ts, self.nbr, self.eid,
-                             self.nts, self.cnt, self.nodes, self.n_nodes, cap, self.root_pos,
-                             self.nbr_pos, stream=st)
-        tgm.tgm_fetch_memory(self.st, i, self.nodes, self.n_nodes, cap, self.f_mem,
-                             self.f_mem_ts, self.f_mail, self.f_mail_ts, self.f_ver, stream=st)
-        tgm.tgm_update_memory(self.st, self.m, self.g, i, self.nodes, self.n_nodes, cap,
+        n = hi - lo
+        b, st = self.sets[0], self.stream
+        tgm.tgm_sample_nodes(self.g, lo, n, self.nb, b.root, b.root_ts, b.nbr, b.eid, b.nts,
+                             b.cnt, b.nodes, b.n_nodes, self.cap, b.root_pos, b.nbr_pos, stream=st)
+        tgm.tgm_fetch_memory(self.st, i, b.nodes, b.n_nodes, self.cap, self.f_mem, self.f_mem_ts,
+                             self.f_mail, self.f_mail_ts, self.f_ver, stream=st)
+        tgm.tgm_update_memory(self.st, self.m, self.g, i, b.nodes, b.n_nodes, self.cap,
                               self.f_mem, self.f_mem_ts, self.f_mail, self.f_mail_ts, self.f_ver,
-                              lo, b, self.root_pos[:b], self.root_pos[b:2 * b], self.mem_new,
+                              lo, n, b.root_pos[:n], b.root_pos[n:2 * n], self.mem_new,
                               self.new_mem_ts, self.winner if self.want_winner else None,
                               stream=st)
-        tgm.tgm_embed(self.m, self.g, R, nb, self.root_pos, self.root_ts, self.nbr_pos,
-                      self.eid, self.nts, self.cnt, self.mem_new, self.n_nodes, cap, self.h,
-                      stream=st)
-        self.last = (i, b)
+        tgm.tgm_embed(self.m, self.g, 3 * n, self.nb, b.root_pos, b.root_ts, b.nbr_pos, b.eid,
+                      b.nts, b.cnt, self.mem_new, b.n_nodes, self.cap, self.h, stream=st)
+        self.last, self._set = (i, n), 0
 
+    def run(self, i0: int, n: int):
+        """Enqueue iterations i0 .. i0+n-1 through the library's pipelined
+        executor (tgm_stage_run).  Ordered after everything issued before on
+        the main stream; the main stream ends after the last iteration."""
+        if n <= 0:
+            return
+        if self._bufs is None:
+            sb = (tgm.SampleBuffers * len(self.sets))(
+                *[tgm.buffers(tgm.SampleBuffers, **vars(b)) for b in self.sets])
+            fb = tgm.buffers(tgm.FetchBuffers, mem=self.f_mem, mem_ts=self.f_mem_ts,
+                             mail=self.f_mail, mail_ts=self.f_mail_ts, ver=self.f_ver)
+            self._bufs = (sb, fb)
+        sb, fb = self._bufs
+        tgm.tgm_stage_run(self.g, self.st, self.m, i0, n, self.B, self.nb, self.cap, sb, fb,
+                          self.mem_new, self.new_mem_ts,
+                          self.winner if self.want_winner else None, self.h, self.stream,
+                          self.pre_stream)
+        last = i0 + n - 1
+        lo, hi = self.batch(last)
+        self.last, self._set = (last, hi - lo), (n - 1) % len(self.sets)
+
+    # ------------------------------------------------------------ read-back
     def outputs(self):
         """Host copies of the last iteration's outputs (synchronises)."""
         torch.cuda.synchronize(self.dev)
         i, b = self.last
-        R, nb = 3 * b, self.nb
-        n = int(self.n_nodes.item())
+        s = self.sets[self._set]
+        R = 3 * b
+        n = int(s.n_nodes.item())
         c = lambda x: x.cpu().numpy()
-        return dict(iter=i, b=b, R=R, n_U=n, root=c(self.root[:R]), root_ts=c(self.root_ts[:R]),
-                    nbr=c(self.nbr[:R]), eid=c(self.eid[:R]), nts=c(self.nts[:R]),
-                    cnt=c(self.cnt[:R]), U=c(self.nodes[:n]), root_pos=c(self.root_pos[:R]),
-                    nbr_pos=c(self.nbr_pos[:R]), f_mem=c(self.f_mem[:n]),
+        return dict(iter=i, b=b, R=R, n_U=n, root=c(s.root[:R]), root_ts=c(s.root_ts[:R]),
+                    nbr=c(s.nbr[:R]), eid=c(s.eid[:R]), nts=c(s.nts[:R]),
+                    cnt=c(s.cnt[:R]), U=c(s.nodes[:n]), root_pos=c(s.root_pos[:R]),
+                    nbr_pos=c(s.nbr_pos[:R]), f_mem=c(self.f_mem[:n]),
                     f_mem_ts=c(self.f_mem_ts[:n]), f_mail=c(self.f_mail[:n]),
                     f_mail_ts=c(self.f_mail_ts[:n]), f_ver=c(self.f_ver[:n]),
                     s_new=c(self.mem_new[:n]), new_mem_ts=c(self.new_mem_ts[:n]),

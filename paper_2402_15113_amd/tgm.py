@@ -23,6 +23,7 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_
            "tgm_node_set", "tgm_sample_nodes", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
            "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
+           "tgm_stage_run",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
 
@@ -30,6 +31,15 @@ class TgmError(RuntimeError):
     def __init__(self, fn, code):
         self.code = code
         super().__init__(f"{fn}: {status_str(code)} ({code})")
+
+
+class SampleBuffers(C.Structure):
+    _fields_ = [(name, C.c_void_p) for name in (
+        "root", "root_ts", "nbr", "eid", "nts", "cnt", "nodes", "n_nodes", "root_pos", "nbr_pos")]
+
+
+class FetchBuffers(C.Structure):
+    _fields_ = [(name, C.c_void_p) for name in ("mem", "mem_ts", "mail", "mail_ts", "ver")]
 
 
 class ModelDesc(C.Structure):
@@ -85,6 +95,8 @@ def lib():
             "tgm_update_memory": [V, V, V, I64, P, P, I32, P, P, P, P, P, I64, I32, P, P, P, P, P,
                                   V],
             "tgm_embed": [V, V, I32, I32, P, P, P, P, P, P, P, P, I32, P, V],
+            "tgm_stage_run": [V, V, V, I64, I64, I32, I32, I32, C.POINTER(SampleBuffers), I32,
+                              C.POINTER(FetchBuffers), P, P, P, P, V, V],
         }
         sig["tgm_profile_enable"] = [I32]
         sig["tgm_profile_reset"] = []
@@ -233,6 +245,19 @@ def tgm_fetch_memory(st, it, nodes, n_nodes, cap, mem, mem_ts, mail, mail_ts, ve
     _check("tgm_fetch_memory", lib().tgm_fetch_memory(st, it, _p(nodes), _p(n_nodes), cap,
                                                       _p(mem), _p(mem_ts), _p(mail), _p(mail_ts),
                                                       _p(ver), _s(stream)))
+
+
+def buffers(struct, **tensors):
+    """A SampleBuffers / FetchBuffers holding the device pointers of the named tensors."""
+    return struct(*[tensors[f].data_ptr() for f, _ in struct._fields_])
+
+
+def tgm_stage_run(g, st, m, i0, n, B, nb, cap, sample_bufs, fetch_bufs, mem_new, new_mem_ts,
+                  winner, h, stream, prefetch_stream):
+    """sample_bufs: a (SampleBuffers * nsb) array; fetch_bufs: a FetchBuffers."""
+    _check("tgm_stage_run", lib().tgm_stage_run(
+        g, st, m, i0, n, B, nb, cap, sample_bufs, len(sample_bufs), C.byref(fetch_bufs),
+        _p(mem_new), _p(new_mem_ts), _p(winner), _p(h), _s(stream), _s(prefetch_stream)))
 
 
 # ------------------------------------------------------------------ model

@@ -200,6 +200,53 @@ def test_mid_run_window_from_synthetic_state(orc):
     run_pair(orc, wl, w, n_iters=16, first=j, init=init)
 
 
+@pytest.mark.parametrize("name,s,E", [("tiny", 0, None), ("tiny", 2, None), ("wiki", 1, 36_000),
+                                      ("lastfm", 2, 60_000)])
+def test_pipelined_run(orc, name, s, E):
+    """Stage.run (prefetch of i+1 on a second stream beside compute(i)) against
+    the oracle: the last iteration's outputs and the flushed tables."""
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload(name, E=E, s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w)
+    o = orc.Oracle(wl, w)
+    n = wl.n_iters
+    print(f"[parity] pipelined {name} s={s} iters 0..{n - 1}", flush=True)
+    st.run(0, n)
+    for i in range(n):
+        r = o.step(want="all" if i == n - 1 else "light")
+    compare_step(st.outputs(), r)
+    st.flush()
+    o.flush()
+    compare_state(st.state(), o.state())
+    st.close()
+
+
+def test_pipelined_equals_sequential():
+    """Stage.run and Stage.step give bit-identical results (the same kernels;
+    only the streams differ), including across a run split in two."""
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("wiki", E=30_000)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    n = wl.n_iters
+    a = from_workload(wl, w)
+    a.run(0, 20)
+    a.run(20, n - 20)
+    b = from_workload(wl, w)
+    for i in range(n):
+        b.step(i)
+    oa, ob = a.outputs(), b.outputs()
+    for k in oa:
+        assert np.array_equal(np.asarray(oa[k]), np.asarray(ob[k])), k
+    a.flush()
+    b.flush()
+    sa, sb = a.state(), b.state()
+    for k in sa:
+        assert np.array_equal(sa[k], sb[k]), k
+    a.close()
+    b.close()
+
+
 # ------------------------------------------------------------------ GDELT-shaped
 # The full stream has 191,290,882 events and a 142 GB edge-feature table.  It
 # is generated once per session without features; the tests below read only
