@@ -253,8 +253,10 @@ tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
  * iteration depend on the event stream only (Sec. 3.1: MSPipe prefetches
  * them), so they run a chunk of nsb/2 iterations ahead on prefetch_stream,
  * into sample buffer set (i - i0) % nsb; the fetch, update and embedding of
- * each iteration run in order on `stream` with one set of fetch buffers.
- * The streams synchronise once per chunk.  The prefetch stream starts after
+ * each iteration run in order on `stream` with one set of fetch buffers, in
+ * three launches per iteration (the staging of a write set shares a launch
+ * with the node projections, and the attention with the next fetch's
+ * gather).  The streams synchronise once per chunk.  The prefetch stream starts after
  * everything issued before on `stream`, and `stream` ends after the last
  * embedding.  Results equal those of issuing tgm_sample_nodes,
  * tgm_fetch_memory, tgm_update_memory and tgm_embed per iteration in order

@@ -27,6 +27,13 @@ void record_error(hipError_t e);
         }                                              \
     } while (0)
 
+#define TGM_TRY_STATUS(call)                           \
+    do {                                               \
+        const tgm_status_t st_ = (call);               \
+        if (st_ != TGM_OK)                             \
+            return st_;                                \
+    } while (0)
+
 #define TGM_LAUNCHED()                                 \
     do {                                               \
         hipError_t e_ = hipGetLastError();             \
@@ -226,6 +233,32 @@ __device__ __forceinline__ void wave_copy_row(float *__restrict__ dst,
     }
 }
 
+// One fetch's gather: rows nodes[0 .. min(*n_nodes, cap)) of the committed
+// tables into the caller's buffers (see tgm_fetch_memory).
+struct GatherPlan {
+    const int32_t *nodes = nullptr, *n_nodes = nullptr;
+    int32_t cap = 0, M = 0, D_m = 0;
+    const float *mem = nullptr, *mail = nullptr;
+    const double *mem_ts = nullptr, *mail_ts = nullptr;
+    const int32_t *ver = nullptr;
+    float *o_mem = nullptr, *o_mail = nullptr;
+    double *o_mem_ts = nullptr, *o_mail_ts = nullptr;
+    int32_t *o_ver = nullptr;
+};
+
+// Row p of a gather, copied by one wavefront.
+__device__ __forceinline__ void gather_row(const GatherPlan &g, int p, int lane)
+{
+    const int32_t v = g.nodes[p];
+    wave_copy_row(g.o_mem + (int64_t)p * g.M, g.mem + (int64_t)v * g.M, g.M, lane);
+    wave_copy_row(g.o_mail + (int64_t)p * g.D_m, g.mail + (int64_t)v * g.D_m, g.D_m, lane);
+    if (lane == 0) {
+        g.o_mem_ts[p] = g.mem_ts[v];
+        g.o_mail_ts[p] = g.mail_ts[v];
+        g.o_ver[p] = g.ver[v];
+    }
+}
+
 // Block-wide gather of `rows` rows of `n` floats into LDS: row r of the
 // destination (stride `lds_stride` floats, starting at column `col0`) is
 // src[off[r] .. off[r] + n), or zeros when off[r] < 0.  `off` lives in LDS.
@@ -340,5 +373,27 @@ __device__ __forceinline__ void stage_rows(float *__restrict__ lds, int lds_stri
 std::vector<float> pack_b(const float *W, int n_out, int ldw, int c0, int K, int KC, int NB);
 
 tgm_status_t upload(void *dst, const void *src, size_t bytes);
+
+// Host side of tgm_fetch_memory: argument and protocol checks, the commits
+// the fetch needs (enqueued on s), and the gather to run, in *plan.
+tgm_status_t fetch_plan(tgm_state_t st, int64_t iter, const int32_t *nodes,
+                        const int32_t *n_nodes, int32_t cap, float *mem, double *mem_ts,
+                        float *mail, double *mail_ts, int32_t *ver, hipStream_t s,
+                        GatherPlan *plan);
+// The gather of a plan as its own launch.
+tgm_status_t launch_gather(const GatherPlan &plan, hipStream_t s);
+
+// The compute of iteration `iter` for the pipelined executor, with the fetch
+// of iteration iter + 1 into the same fetch buffers when next_sb (its sample
+// buffers) is given, in three launches on s: the GRU (with the
+// latest-message reduce); the staging of the write set fused with the node
+// projections; the attention fused with the next fetch's gather, which needs
+// only the staging's commits.  Same results as tgm_update_memory and
+// tgm_embed of iter followed by tgm_fetch_memory of iter + 1.
+tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
+                               const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
+                               int32_t cap, int64_t first_event, int32_t b, int32_t nb,
+                               float *mem_new, double *new_mem_ts, int64_t *winner, float *h,
+                               const tgm_sample_buffers *next_sb, hipStream_t s);
 
 }  // namespace tgm

@@ -12,6 +12,7 @@ using namespace tgm;
 namespace {
 
 constexpr int kMaxWaves = 8;
+constexpr int kCUs = 256;      // compute units of an MI355X
 constexpr int kAttMaxCB = 2;   // K|V column blocks per wave
 constexpr int kAttMaxRB = 5;   // 16-row slot blocks per workgroup
 
@@ -373,10 +374,9 @@ struct StageArgs {
     int32_t *t_ver;
 };
 
-__global__ __launch_bounds__(256) void k_stage(StageArgs g)
+// Wavefront work item c of a staging launch (see StageArgs).
+__device__ __forceinline__ void stage_wave(const StageArgs &g, int c, int lane)
 {
-    const int c = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
-    const int lane = threadIdx.x & 63;
     const int M = g.M, D_m = g.D_m, D_e = g.D_e;
     if (c >= g.n_cand) {
         const int k = c - g.n_cand;
@@ -426,6 +426,12 @@ __global__ __launch_bounds__(256) void k_stage(StageArgs g)
     }
 }
 
+__global__ __launch_bounds__(256) void k_stage(StageArgs g)
+{
+    stage_wave(g, (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6),
+               threadIdx.x & 63);
+}
+
 __global__ void k_fill_u64(uint64_t *__restrict__ p, int32_t n)
 {
     const int k = blockIdx.x * blockDim.x + threadIdx.x;
@@ -459,7 +465,8 @@ template <int W, int C>
 __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ mem_new, int M,
                                                int PC, const f4 *__restrict__ pb, int PNB,
                                                const float *__restrict__ pbias,
-                                               float *__restrict__ P, float *lds)
+                                               float *__restrict__ P, float *lds, int bid,
+                                               int nblk)
 {
     const int K = PC * 16, SA = K + 4, ldP = PNB * 16;
     const int nw = blockDim.x >> 6;
@@ -482,7 +489,7 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
             off[i] = (r < 16 && row0 + r < n) ? (int64_t)(row0 + r) * M : -1;
         }
     };
-    int row0 = blockIdx.x * 16;
+    int row0 = bid * 16;
     WaveRows<W, 4, C> x;
     rows_of(row0);
     x.load(mem_new, off, M, lane);
@@ -506,7 +513,7 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
                 for (int k = M + lane; k < K; k += kWave)
                     lds[lr[i] * SA + k] = 0.f;
         __syncthreads();
-        const int next = row0 + gridDim.x * 16;
+        const int next = row0 + nblk * 16;
         if (next < n) {
             rows_of(next);
             x.load(mem_new, off, M, lane);
@@ -542,20 +549,44 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
     }
 }
 
-__global__ __launch_bounds__(512) void k_node_proj(const int32_t *__restrict__ n_nodes,
-                                                   const float *__restrict__ mem_new, int M,
-                                                   int PC, const f4 *__restrict__ pb, int PNB,
-                                                   const float *__restrict__ pbias,
-                                                   float *__restrict__ P)
+struct ProjArgs {
+    const int32_t *n_nodes;
+    const float *mem_new;
+    int M, PC, PNB;
+    const f4 *pb;
+    const float *pbias;
+    float *P;
+};
+
+// Block bid of nblk node-projection blocks.
+__device__ __forceinline__ void node_proj_block(const ProjArgs &a, float *lds, int bid, int nblk)
+{
+    const int n = *a.n_nodes;
+    if (bid * 16 >= n)
+        return;
+    if ((a.M & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mem_new) & 15) == 0)
+        node_proj_body<4, 1>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.pbias, a.P, lds, bid, nblk);
+    else
+        node_proj_body<1, 2>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.pbias, a.P, lds, bid, nblk);
+}
+
+__global__ __launch_bounds__(512) void k_node_proj(ProjArgs a)
 {
     extern __shared__ float lds[];
-    const int n = *n_nodes;
-    if ((int)blockIdx.x * 16 >= n)
+    node_proj_block(a, lds, blockIdx.x, gridDim.x);
+}
+
+// The staging of a write set and the node projections in one launch: blocks
+// [0, n_proj) project, the rest stage (one wavefront per staging item).
+__global__ __launch_bounds__(512) void k_stage_proj(StageArgs sa, ProjArgs pa, int n_proj)
+{
+    extern __shared__ float lds[];
+    if ((int)blockIdx.x < n_proj) {
+        node_proj_block(pa, lds, blockIdx.x, n_proj);
         return;
-    if ((M & 3) == 0 && (reinterpret_cast<uintptr_t>(mem_new) & 15) == 0)
-        node_proj_body<4, 1>(n, mem_new, M, PC, pb, PNB, pbias, P, lds);
-    else
-        node_proj_body<1, 2>(n, mem_new, M, PC, pb, PNB, pbias, P, lds);
+    }
+    const int waves = blockDim.x >> 6;
+    stage_wave(sa, ((int)blockIdx.x - n_proj) * waves + (int)(threadIdx.x >> 6), threadIdx.x & 63);
 }
 
 struct AttnArgs {
@@ -597,16 +628,15 @@ constexpr int kAttMaxOC = 16;   // 16-wide k-chunks of the output projection (2M
 constexpr int kAttPre = 6;      // time-code k-chunks whose weights are preloaded
 
 template <int RB>   // 16-row slot blocks per workgroup (3..5)
-__global__ __launch_bounds__(512) void k_attn(AttnArgs g)
+__device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bid)
 {
-    extern __shared__ float lds[];
     __shared__ int s_np[kAttMaxSlots];         // neighbour's node-set position, -1 if none
     __shared__ int64_t s_qoff[kAttMaxSlots], s_voff[kAttMaxSlots];
     __shared__ int s_cnt[kAttMaxSlots];
     __shared__ int64_t s_eoff[kAttMaxSlots];   // edge-feature row offset, -1 if none
     __shared__ double s_dt[kAttMaxSlots];      // t_root - t_slot
     __shared__ int s_ok[kAttMaxSlots];         // slot holds a sampled neighbour
-    const int r0 = blockIdx.x * g.RT;
+    const int r0 = bid * g.RT;
     const int nroots = min(g.RT, g.R - r0);
     if (nroots <= 0)
         return;
@@ -971,6 +1001,31 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs g)
     }
 }
 
+template <int RB>
+__global__ __launch_bounds__(512) void k_attn(AttnArgs g)
+{
+    extern __shared__ float lds[];
+    attn_block<RB>(g, lds, blockIdx.x);
+}
+
+// The attention and the gather of the next iteration's fetch in one launch:
+// blocks [0, n_attn) embed; the rest (dispatched after them, on the CUs the
+// attention leaves free) gather one node row per wavefront.
+template <int RB>
+__global__ __launch_bounds__(512) void k_attn_gather(AttnArgs g, int n_attn, GatherPlan gp)
+{
+    extern __shared__ float lds[];
+    if ((int)blockIdx.x < n_attn) {
+        attn_block<RB>(g, lds, blockIdx.x);
+        return;
+    }
+    const int waves = blockDim.x >> 6;
+    const int n = min(*gp.n_nodes, gp.cap);
+    const int stride = ((int)gridDim.x - n_attn) * waves;
+    for (int p = ((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6); p < n; p += stride)
+        gather_row(gp, p, threadIdx.x & 63);
+}
+
 // q bias folded at creation: c_q = W_q^t phi(0) + b_q with phi(0)_d = cos(beta_d).
 __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, const float *b_q,
                               const double *__restrict__ beta, float *c_q)   // may alias b_q
@@ -986,12 +1041,14 @@ __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, con
 
 bool attn_lds_opt_in(int bytes)
 {
-    return hipFuncSetAttribute((const void *)k_attn<3>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               bytes) == hipSuccess &&
-           hipFuncSetAttribute((const void *)k_attn<4>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               bytes) == hipSuccess &&
-           hipFuncSetAttribute((const void *)k_attn<5>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               bytes) == hipSuccess;
+    const void *fn[] = {(const void *)k_attn<3>, (const void *)k_attn<4>, (const void *)k_attn<5>,
+                        (const void *)k_attn_gather<3>, (const void *)k_attn_gather<4>,
+                        (const void *)k_attn_gather<5>};
+    for (const void *f : fn)
+        if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) !=
+            hipSuccess)
+            return false;
+    return true;
 }
 
 int waves_for(int blocks) { return blocks < kMaxWaves ? (blocks < 1 ? 1 : blocks) : kMaxWaves; }
@@ -1197,16 +1254,19 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     return TGM_OK;
 }
 
-extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_graph_t g,
-                                          int64_t iter, const int32_t *nodes,
-                                          const int32_t *n_nodes, int32_t cap, const float *mem,
-                                          const double *mem_ts, const float *mail,
-                                          const double *mail_ts, const int32_t *ver,
-                                          int64_t first_event, int32_t b, const int32_t *src_pos,
-                                          const int32_t *dst_pos, float *mem_new,
-                                          double *new_mem_ts, int64_t *winner, void *stream)
+namespace {
+
+// Host side of tgm_update_memory: the checks, the GRU launch (with the
+// latest-message reduce) on s, the staging launch's arguments (*sa, *n_items
+// wavefront items) and the protocol bookkeeping.  *tag is the call's key tag.
+tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
+                          const int32_t *n_nodes, int32_t cap, const float *mem,
+                          const double *mem_ts, const float *mail, const double *mail_ts,
+                          const int32_t *ver, int64_t first_event, int32_t b,
+                          const int32_t *src_pos, const int32_t *dst_pos, float *mem_new,
+                          double *new_mem_ts, hipStream_t s, StageArgs *sa, int *n_items,
+                          uint64_t *tag_out)
 {
-    (void)nodes;
     if (!st || !m || !g || !n_nodes || cap < 0 || b < 0 || first_event < 0 ||
         first_event + b > g->E)
         return TGM_EINVAL;
@@ -1225,7 +1285,6 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
     const int slots = st->s + 1;
     if (iter - slots > st->committed_through)
         return TGM_EORDER;   // the slot still holds an uncommitted write set
-    hipStream_t s = as_stream(stream);
     if (st->win_tag == UINT32_MAX) {   // keys restart from zero
         TGM_LAUNCH(k_fill_u64, dim3(cdiv(st->N, 256)), dim3(256), 0, s, st->win, st->N);
         st->win_tag = 0;
@@ -1245,38 +1304,34 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
         TGM_LAUNCH(k_gru, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
     }
     const size_t base = (size_t)(iter % slots) * st->ring_rows();
-    // the write set of iteration iter - s is committed by this launch when it
-    // is the next one due (s = 0: the current write set goes to the tables)
+    // the write set of iteration iter - s is committed by the staging launch
+    // when it is the next one due (s = 0: the current write set goes to the
+    // tables)
     const bool direct = st->s == 0;
     const int64_t cj = iter - st->s;
     const tgm_state::Slot &cs = st->ring[((cj % slots) + slots) % slots];
     const bool fuse = !direct && cj >= 0 && cj == st->committed_through + 1 && cs.staged &&
                       cs.iter == cj;
     const int n_commit = fuse ? 2 * cs.b : 0;
-    if (n_cand + n_commit > 0) {
-        const size_t cbase = (size_t)(((cj % slots) + slots) % slots) * st->ring_rows();
-        StageArgs a;
-        a.n_cand = n_cand; a.n_commit = n_commit;
-        a.first = first_event; a.iter = iter; a.c_iter = cj;
-        a.M = m->M; a.D_m = m->D_m; a.D_e = m->D_e; a.direct = direct;
-        a.n_nodes = n_nodes; a.src = g->src; a.dst = g->dst; a.src_pos = src_pos;
-        a.dst_pos = dst_pos; a.win = st->win; a.tag = tag; a.ver = ver;
-        a.t = g->t; a.mem_ts = mem_ts; a.mail_ts = mail_ts; a.efeat = g->efeat;
-        a.mem_new = mem_new;
-        a.r_flag = st->r_flag + base; a.r_node = st->r_node + base;
-        a.r_mem = st->r_mem + base * st->M; a.r_mail = st->r_mail + base * st->D_m;
-        a.r_mem_ts = st->r_mem_ts + base; a.r_mail_ts = st->r_mail_ts + base;
-        a.c_flag = st->r_flag + cbase; a.c_node = st->r_node + cbase;
-        a.c_mem = st->r_mem + cbase * st->M; a.c_mail = st->r_mail + cbase * st->D_m;
-        a.c_mem_ts = st->r_mem_ts + cbase; a.c_mail_ts = st->r_mail_ts + cbase;
-        a.mem = st->mem; a.mail = st->mail; a.t_mem_ts = st->mem_ts; a.t_mail_ts = st->mail_ts;
-        a.t_ver = st->ver;
-        TGM_LAUNCH(k_stage, dim3(cdiv(n_cand + n_commit, 4)), dim3(256), 0, s, a);
-    }
-    if (winner && cap > 0) {
-        TGM_LAUNCH(k_winner_out, dim3(cdiv(cap, 256)), dim3(256), 0, s, n_nodes, cap,
-                   first_event, st->win, tag, winner);
-    }
+    const size_t cbase = (size_t)(((cj % slots) + slots) % slots) * st->ring_rows();
+    StageArgs &a = *sa;
+    a.n_cand = n_cand; a.n_commit = n_commit;
+    a.first = first_event; a.iter = iter; a.c_iter = cj;
+    a.M = m->M; a.D_m = m->D_m; a.D_e = m->D_e; a.direct = direct;
+    a.n_nodes = n_nodes; a.src = g->src; a.dst = g->dst; a.src_pos = src_pos;
+    a.dst_pos = dst_pos; a.win = st->win; a.tag = tag; a.ver = ver;
+    a.t = g->t; a.mem_ts = mem_ts; a.mail_ts = mail_ts; a.efeat = g->efeat;
+    a.mem_new = mem_new;
+    a.r_flag = st->r_flag + base; a.r_node = st->r_node + base;
+    a.r_mem = st->r_mem + base * st->M; a.r_mail = st->r_mail + base * st->D_m;
+    a.r_mem_ts = st->r_mem_ts + base; a.r_mail_ts = st->r_mail_ts + base;
+    a.c_flag = st->r_flag + cbase; a.c_node = st->r_node + cbase;
+    a.c_mem = st->r_mem + cbase * st->M; a.c_mail = st->r_mail + cbase * st->D_m;
+    a.c_mem_ts = st->r_mem_ts + cbase; a.c_mail_ts = st->r_mail_ts + cbase;
+    a.mem = st->mem; a.mail = st->mail; a.t_mem_ts = st->mem_ts; a.t_mail_ts = st->mail_ts;
+    a.t_ver = st->ver;
+    *n_items = n_cand + n_commit;
+    *tag_out = tag;
     if (fuse) {
         st->ring[cj % slots].staged = false;
         st->committed_through = cj;
@@ -1293,11 +1348,21 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
     return TGM_OK;
 }
 
-extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
-                                  const int32_t *root_pos, const double *root_ts,
-                                  const int32_t *nbr_pos, const int32_t *eid, const double *nts,
-                                  const int32_t *cnt, const float *mem_new,
-                                  const int32_t *n_nodes, int32_t cap, float *h, void *stream)
+tgm_status_t update_winner(tgm_state_t st, const int32_t *n_nodes, int32_t cap,
+                           int64_t first_event, uint64_t tag, int64_t *winner, hipStream_t s)
+{
+    if (winner && cap > 0)
+        TGM_LAUNCH(k_winner_out, dim3(cdiv(cap, 256)), dim3(256), 0, s, n_nodes, cap,
+                   first_event, st->win, tag, winner);
+    return TGM_OK;
+}
+
+// Checks of tgm_embed and the arguments of its two launches.
+tgm_status_t embed_plan(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
+                        const int32_t *root_pos, const double *root_ts, const int32_t *nbr_pos,
+                        const int32_t *eid, const double *nts, const int32_t *cnt,
+                        const float *mem_new, const int32_t *n_nodes, int32_t cap, float *h,
+                        ProjArgs *pa, int *proj_grid, int *proj_waves, AttnArgs *aa)
 {
     if (!m || !g || R < 0 || nb != m->nb || !n_nodes || cap < 0 || g->D_e != m->D_e)
         return TGM_EINVAL;
@@ -1307,14 +1372,13 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
         return TGM_OK;
     if (!root_pos || !root_ts || !nbr_pos || !eid || !nts || !cnt || !mem_new || !h || cap == 0)
         return TGM_EINVAL;
-    hipStream_t s = as_stream(stream);
-    // persistent grid: at most the tiles of the largest node set, at most two
-    // workgroups per CU; every wave owns up to three column blocks
-    const int proj_waves = std::max<int>(4, std::min<int>(kMaxWaves, (int)cdiv(m->PNB, 3)));
-    const int proj_grid = (int)std::min<int64_t>(cdiv(cap, 16), 512);
-    TGM_LAUNCH(k_node_proj, dim3(proj_grid), dim3(64 * proj_waves), proj_lds(m), s, n_nodes,
-               mem_new, m->M, m->PC, m->proj_b, m->PNB, m->pbias, m->P);
-    AttnArgs a;
+    // persistent grid: at most the tiles of the largest node set; every wave
+    // owns up to three column blocks
+    *proj_waves = std::max<int>(4, std::min<int>(kMaxWaves, (int)cdiv(m->PNB, 3)));
+    *proj_grid = (int)std::min<int64_t>(cdiv(cap, 16), 512);
+    pa->n_nodes = n_nodes; pa->mem_new = mem_new; pa->M = m->M; pa->PC = m->PC;
+    pa->PNB = m->PNB; pa->pb = m->proj_b; pa->pbias = m->pbias; pa->P = m->P;
+    AttnArgs &a = *aa;
     a.R = R; a.nb = nb; a.RT = attn_roots(m, &a.RBa); a.M = m->M; a.H = m->H;
     a.E = g->E; a.n_nodes = n_nodes;
     a.D_e = m->D_e; a.D_t = m->D_t;
@@ -1326,13 +1390,128 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
     a.pbias = m->pbias;
     a.out_b = m->out_b; a.OC = m->OC; a.ONB = m->ONB; a.b_o = m->b_o;
     a.mem_new = mem_new; a.h = h;
-    const dim3 grid(cdiv(R, a.RT)), block(64 * kMaxWaves);
+    return a.RBa >= 3 && a.RBa <= 5 ? TGM_OK : TGM_EINVAL;
+}
+
+// The attention launch, with the gather of `next` in the same launch when
+// given (extra blocks after the attention's).
+tgm_status_t launch_attn(const tgm_model *m, const AttnArgs &a, const GatherPlan *next,
+                         hipStream_t s)
+{
+    const int n_attn = (int)cdiv(a.R, a.RT);
+    const dim3 block(64 * kMaxWaves);
     const size_t lds = attn_lds(m);
+    // the gather rides along only when the attention leaves CUs free (its
+    // blocks are dispatched after the attention's and hold one CU each: they
+    // carry the attention's LDS size); otherwise it is its own launch
+    if (next && next->cap > 0 && n_attn + 8 > kCUs) {
+        TGM_TRY_STATUS(launch_gather(*next, s));
+        next = nullptr;
+    }
+    if (next && next->cap > 0) {
+        const int n_gather = kCUs - n_attn;
+        const dim3 grid(n_attn + n_gather);
+        switch (a.RBa) {
+        case 3: TGM_LAUNCH(k_attn_gather<3>, grid, block, lds, s, a, n_attn, *next); break;
+        case 4: TGM_LAUNCH(k_attn_gather<4>, grid, block, lds, s, a, n_attn, *next); break;
+        default: TGM_LAUNCH(k_attn_gather<5>, grid, block, lds, s, a, n_attn, *next); break;
+        }
+        return TGM_OK;
+    }
+    const dim3 grid(n_attn);
     switch (a.RBa) {
     case 3: TGM_LAUNCH(k_attn<3>, grid, block, lds, s, a); break;
     case 4: TGM_LAUNCH(k_attn<4>, grid, block, lds, s, a); break;
-    case 5: TGM_LAUNCH(k_attn<5>, grid, block, lds, s, a); break;
-    default: return TGM_EINVAL;
+    default: TGM_LAUNCH(k_attn<5>, grid, block, lds, s, a); break;
     }
     return TGM_OK;
+}
+
+}  // namespace
+
+extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_graph_t g,
+                                          int64_t iter, const int32_t *nodes,
+                                          const int32_t *n_nodes, int32_t cap, const float *mem,
+                                          const double *mem_ts, const float *mail,
+                                          const double *mail_ts, const int32_t *ver,
+                                          int64_t first_event, int32_t b, const int32_t *src_pos,
+                                          const int32_t *dst_pos, float *mem_new,
+                                          double *new_mem_ts, int64_t *winner, void *stream)
+{
+    (void)nodes;
+    const hipStream_t s = as_stream(stream);
+    StageArgs sa;
+    int n_items = 0;
+    uint64_t tag = 0;
+    tgm_status_t rc = update_begin(st, m, g, iter, n_nodes, cap, mem, mem_ts, mail, mail_ts, ver,
+                                   first_event, b, src_pos, dst_pos, mem_new, new_mem_ts, s, &sa,
+                                   &n_items, &tag);
+    if (rc != TGM_OK)
+        return rc;
+    if (n_items > 0)
+        TGM_LAUNCH(k_stage, dim3(cdiv(n_items, 4)), dim3(256), 0, s, sa);
+    return update_winner(st, n_nodes, cap, first_event, tag, winner, s);
+}
+
+extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
+                                  const int32_t *root_pos, const double *root_ts,
+                                  const int32_t *nbr_pos, const int32_t *eid, const double *nts,
+                                  const int32_t *cnt, const float *mem_new,
+                                  const int32_t *n_nodes, int32_t cap, float *h, void *stream)
+{
+    const hipStream_t s = as_stream(stream);
+    ProjArgs pa;
+    AttnArgs aa;
+    int proj_grid = 0, proj_waves = 0;
+    const tgm_status_t rc = embed_plan(m, g, R, nb, root_pos, root_ts, nbr_pos, eid, nts, cnt,
+                                       mem_new, n_nodes, cap, h, &pa, &proj_grid, &proj_waves,
+                                       &aa);
+    if (rc != TGM_OK || R == 0)
+        return rc;
+    TGM_LAUNCH(k_node_proj, dim3(proj_grid), dim3(64 * proj_waves), proj_lds(m), s, pa);
+    return launch_attn(m, aa, nullptr, s);
+}
+
+tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
+                                    const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
+                                    int32_t cap, int64_t first_event, int32_t b, int32_t nb,
+                                    float *mem_new, double *new_mem_ts, int64_t *winner,
+                                    float *h, const tgm_sample_buffers *next_sb, hipStream_t s)
+{
+    StageArgs sa;
+    int n_items = 0;
+    uint64_t tag = 0;
+    tgm_status_t rc = update_begin(st, m, g, iter, sb.n_nodes, cap, fb.mem, fb.mem_ts, fb.mail,
+                                   fb.mail_ts, fb.ver, first_event, b, sb.root_pos,
+                                   sb.root_pos + b, mem_new, new_mem_ts, s, &sa, &n_items, &tag);
+    if (rc != TGM_OK)
+        return rc;
+    ProjArgs pa;
+    AttnArgs aa;
+    int proj_grid = 0, proj_waves = 0;
+    const int32_t R = 3 * b;
+    rc = embed_plan(m, g, R, nb, sb.root_pos, sb.root_ts, sb.nbr_pos, sb.eid, sb.nts, sb.cnt,
+                    mem_new, sb.n_nodes, cap, h, &pa, &proj_grid, &proj_waves, &aa);
+    if (rc != TGM_OK)
+        return rc;
+    // the fetch of iteration iter + 1, planned after this update's protocol
+    // step (so the commit it needs is the one this staging launch makes)
+    GatherPlan next_plan;
+    const GatherPlan *next = nullptr;
+    if (next_sb) {
+        rc = fetch_plan(st, iter + 1, next_sb->nodes, next_sb->n_nodes, cap, fb.mem, fb.mem_ts,
+                        fb.mail, fb.mail_ts, fb.ver, s, &next_plan);
+        if (rc != TGM_OK)
+            return rc;
+        next = &next_plan;
+    }
+    // staging items ride in blocks after the projection's
+    const int n_stage_blocks = (int)cdiv(n_items, proj_waves);
+    if (R > 0 || n_items > 0)
+        TGM_LAUNCH(k_stage_proj, dim3((R > 0 ? proj_grid : 0) + n_stage_blocks),
+                   dim3(64 * proj_waves), proj_lds(m), s, sa, pa, R > 0 ? proj_grid : 0);
+    TGM_TRY_STATUS(update_winner(st, sb.n_nodes, cap, first_event, tag, winner, s));
+    if (R > 0)
+        return launch_attn(m, aa, next, s);
+    return next ? launch_gather(*next, s) : TGM_OK;
 }

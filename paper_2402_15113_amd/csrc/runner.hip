@@ -1,7 +1,9 @@
 // Pipelined executor of the stage.  The sample and node set of an iteration
 // depend on the event stream only, so they run a chunk of iterations ahead on
-// a second stream; the fetch, update and embedding run in iteration order on
-// the main stream (each update commits the write set the next fetch needs).
+// a second stream.  On the main stream each iteration is three launches: the
+// GRU; the staging of its write set fused with the node projections; the
+// attention fused with the gather of the next iteration's fetch (which needs
+// only the staging's commits and runs on the CUs the attention leaves free).
 // Cross-stream waits are host calls of several microseconds each, so the
 // streams synchronise once per chunk, not once per iteration.
 #include <hip/hip_runtime.h>
@@ -29,13 +31,6 @@ struct Events {
     }
 };
 
-#define TGM_TRY(call)                      \
-    do {                                   \
-        const tgm_status_t st_ = (call);   \
-        if (st_ != TGM_OK)                 \
-            return st_;                    \
-    } while (0)
-
 }  // namespace
 
 extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m,
@@ -59,15 +54,20 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     Events ev;   // 0-1: sampled chunk by parity, 2-3: computed chunk by parity, 4: start
     if (!ev.create())
         return TGM_EDEVICE;
-    const int64_t K = nsb / 2;                 // iterations per chunk
+    const int64_t K = nsb / 2;   // iterations per chunk
     const int64_t nch = (n + K - 1) / K;
+    auto batch = [&](int64_t k, int64_t *lo) {   // the k-th iteration of the run
+        *lo = (i0 + k) * B;
+        return (int32_t)std::min<int64_t>(B, g->E - *lo);
+    };
     auto sample_chunk = [&](int64_t c) -> tgm_status_t {
         for (int64_t k = c * K; k < std::min(n, (c + 1) * K); ++k) {
-            const int64_t lo = (i0 + k) * B;
-            const int32_t b = (int32_t)std::min<int64_t>(B, g->E - lo);
+            int64_t lo = 0;
+            const int32_t b = batch(k, &lo);
             const tgm_sample_buffers &s = sb[k % nsb];
-            TGM_TRY(tgm_sample_nodes(g, lo, b, nb, s.root, s.root_ts, s.nbr, s.eid, s.nts, s.cnt,
-                                     s.nodes, s.n_nodes, cap, s.root_pos, s.nbr_pos, pre));
+            TGM_TRY_STATUS(tgm_sample_nodes(g, lo, b, nb, s.root, s.root_ts, s.nbr, s.eid, s.nts,
+                                            s.cnt, s.nodes, s.n_nodes, cap, s.root_pos,
+                                            s.nbr_pos, pre));
         }
         TGM_HIP(hipEventRecord(ev.e[c & 1], pre));
         return TGM_OK;
@@ -75,25 +75,30 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     // the prefetch stream starts after everything issued before on the main one
     TGM_HIP(hipEventRecord(ev.e[4], main));
     TGM_HIP(hipStreamWaitEvent(pre, ev.e[4], 0));
-    TGM_TRY(sample_chunk(0));
+    TGM_TRY_STATUS(sample_chunk(0));
+    TGM_HIP(hipStreamWaitEvent(main, ev.e[0], 0));
+    {   // the first iteration's fetch on its own
+        GatherPlan plan;
+        TGM_TRY_STATUS(fetch_plan(st, i0, sb[0].nodes, sb[0].n_nodes, cap, fb->mem, fb->mem_ts,
+                                  fb->mail, fb->mail_ts, fb->ver, main, &plan));
+        TGM_TRY_STATUS(launch_gather(plan, main));
+    }
     for (int64_t c = 0; c < nch; ++c) {
         if (c + 1 < nch) {
             if (c >= 1)   // chunk c-1, the last user of these sample sets, is computed
                 TGM_HIP(hipStreamWaitEvent(pre, ev.e[2 + ((c - 1) & 1)], 0));
-            TGM_TRY(sample_chunk(c + 1));
+            TGM_TRY_STATUS(sample_chunk(c + 1));
         }
-        TGM_HIP(hipStreamWaitEvent(main, ev.e[c & 1], 0));
-        for (int64_t k = c * K; k < std::min(n, (c + 1) * K); ++k) {
-            const int64_t i = i0 + k, lo = i * B;
-            const int32_t b = (int32_t)std::min<int64_t>(B, g->E - lo);
-            const tgm_sample_buffers &s = sb[k % nsb];
-            TGM_TRY(tgm_fetch_memory(st, i, s.nodes, s.n_nodes, cap, fb->mem, fb->mem_ts,
-                                     fb->mail, fb->mail_ts, fb->ver, main));
-            TGM_TRY(tgm_update_memory(st, m, g, i, s.nodes, s.n_nodes, cap, fb->mem, fb->mem_ts,
-                                      fb->mail, fb->mail_ts, fb->ver, lo, b, s.root_pos,
-                                      s.root_pos + b, mem_new, new_mem_ts, winner, main));
-            TGM_TRY(tgm_embed(m, g, 3 * b, nb, s.root_pos, s.root_ts, s.nbr_pos, s.eid, s.nts,
-                              s.cnt, mem_new, s.n_nodes, cap, h, main));
+        const int64_t kend = std::min(n, (c + 1) * K);
+        for (int64_t k = c * K; k < kend; ++k) {
+            int64_t lo = 0;
+            const int32_t b = batch(k, &lo);
+            const bool more = k + 1 < n;
+            if (more && k + 1 == kend)   // the next iteration's samples are the next chunk's
+                TGM_HIP(hipStreamWaitEvent(main, ev.e[(c + 1) & 1], 0));
+            TGM_TRY_STATUS(compute_iteration(st, m, g, i0 + k, sb[k % nsb], *fb, cap, lo, b, nb,
+                                             mem_new, new_mem_ts, winner, h,
+                                             more ? &sb[(k + 1) % nsb] : nullptr, main));
         }
         TGM_HIP(hipEventRecord(ev.e[2 + (c & 1)], main));
     }

@@ -52,25 +52,12 @@ __global__ __launch_bounds__(256) void k_commit(
 }
 
 // Gather the committed rows of the node set: one wavefront per node.
-__global__ __launch_bounds__(256) void k_gather_state(
-    const int32_t *__restrict__ nodes, const int32_t *__restrict__ n_nodes, int32_t M,
-    int32_t D_m, const float *__restrict__ mem, const double *__restrict__ mem_ts,
-    const float *__restrict__ mail, const double *__restrict__ mail_ts,
-    const int32_t *__restrict__ ver, float *__restrict__ o_mem, double *__restrict__ o_mem_ts,
-    float *__restrict__ o_mail, double *__restrict__ o_mail_ts, int32_t *__restrict__ o_ver)
+__global__ __launch_bounds__(256) void k_gather_state(GatherPlan g)
 {
     const int p = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
-    const int lane = threadIdx.x & 63;
-    if (p >= *n_nodes)
+    if (p >= min(*g.n_nodes, g.cap))
         return;
-    const int32_t v = nodes[p];
-    wave_copy_row(o_mem + (int64_t)p * M, mem + (int64_t)v * M, M, lane);
-    wave_copy_row(o_mail + (int64_t)p * D_m, mail + (int64_t)v * D_m, D_m, lane);
-    if (lane == 0) {
-        o_mem_ts[p] = mem_ts[v];
-        o_mail_ts[p] = mail_ts[v];
-        o_ver[p] = ver[v];
-    }
+    gather_row(g, p, threadIdx.x & 63);
 }
 
 tgm_status_t commit_through(tgm_state *st, int64_t target, hipStream_t s)
@@ -218,10 +205,10 @@ extern "C" tgm_status_t tgm_state_load(tgm_state_t st, int64_t iter, const float
     return TGM_OK;
 }
 
-extern "C" tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int32_t *nodes,
-                                         const int32_t *n_nodes, int32_t cap, float *mem,
-                                         double *mem_ts, float *mail, double *mail_ts,
-                                         int32_t *ver, void *stream)
+tgm_status_t tgm::fetch_plan(tgm_state_t st, int64_t iter, const int32_t *nodes,
+                             const int32_t *n_nodes, int32_t cap, float *mem, double *mem_ts,
+                             float *mail, double *mail_ts, int32_t *ver, hipStream_t s,
+                             GatherPlan *plan)
 {
     if (!st || iter < 0 || cap < 0 || !n_nodes)
         return TGM_EINVAL;
@@ -234,15 +221,35 @@ extern "C" tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int
     const int64_t target = iter - 1 - st->s;
     if (target > st->staged_through)
         return TGM_EORDER;
-    hipStream_t s = as_stream(stream);
     tgm_status_t rc = commit_through(st, target, s);
     if (rc != TGM_OK)
         return rc;
     st->last_fetch = iter;
-    if (cap == 0)
-        return TGM_OK;
-    TGM_LAUNCH(k_gather_state, dim3(cdiv(cap, 4)), dim3(256), 0, s, nodes, n_nodes,
-               st->M, st->D_m, st->mem, st->mem_ts, st->mail, st->mail_ts, st->ver, mem,
-               mem_ts, mail, mail_ts, ver);
+    GatherPlan p;
+    p.nodes = nodes; p.n_nodes = n_nodes; p.cap = cap; p.M = st->M; p.D_m = st->D_m;
+    p.mem = st->mem; p.mail = st->mail; p.mem_ts = st->mem_ts; p.mail_ts = st->mail_ts;
+    p.ver = st->ver;
+    p.o_mem = mem; p.o_mail = mail; p.o_mem_ts = mem_ts; p.o_mail_ts = mail_ts; p.o_ver = ver;
+    *plan = p;
     return TGM_OK;
+}
+
+tgm_status_t tgm::launch_gather(const GatherPlan &plan, hipStream_t s)
+{
+    if (plan.cap == 0)
+        return TGM_OK;
+    TGM_LAUNCH(k_gather_state, dim3(cdiv(plan.cap, 4)), dim3(256), 0, s, plan);
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int32_t *nodes,
+                                         const int32_t *n_nodes, int32_t cap, float *mem,
+                                         double *mem_ts, float *mail, double *mail_ts,
+                                         int32_t *ver, void *stream)
+{
+    GatherPlan plan;
+    const hipStream_t s = as_stream(stream);
+    const tgm_status_t rc =
+        fetch_plan(st, iter, nodes, n_nodes, cap, mem, mem_ts, mail, mail_ts, ver, s, &plan);
+    return rc != TGM_OK ? rc : launch_gather(plan, s);
 }
