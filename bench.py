@@ -15,9 +15,9 @@ Passes:
      the steps are pipelined over two streams (Stage.run: the sample, node
      set and fetch of batch i+1 run beside the update and embedding of batch
      i, which staleness s >= 1 allows);
-  2. the same steps again, one after another on one stream, with the
-     library's per-kernel HIP-event timing on -> average launch duration per
-     kernel (the roofline's denominator);
+  2. the same pipelined steps again with the library's per-kernel HIP-event
+     timing on (events on each kernel's own stream) -> average launch
+     duration per kernel (the roofline's denominator);
   3. an untimed replay that reads back each step's sizes (valid slots, node
      set, nodes with mail) -> algorithmic flops and bytes per launch;
   4. the fp64 oracle on the host cores for a bounded sample of the same
@@ -179,7 +179,7 @@ def work_model(wl, rows):
     slots, R, n_U, n_mail, n_win, b = (avg("slots"), avg("R"), avg("n_U"), avg("n_mail"),
                                        avg("n_win"), avg("b"))
     f, d = 4, 8
-    return {
+    k = {
         # per node with mail: the three gates over [x | h]
         # (plus the batch's latest-message reduce: 2b positions, 2b 64-bit atomics)
         "k_gru": dict(flops=n_mail * 2 * 3 * M * (D_x + M),
@@ -202,6 +202,13 @@ def work_model(wl, rows):
                         + 2 * b * 12),
         "k_batch_roots": dict(flops=0, bytes=b * (3 * 4 + d) + 3 * b * (4 + d)),
     }
+    # the executor's fused launches: staging + node projection; attention +
+    # the next iteration's gather
+    k["k_stage_proj"] = dict(flops=k["k_node_proj"]["flops"],
+                             bytes=k["k_node_proj"]["bytes"] + k["k_stage"]["bytes"])
+    k["k_attn_gather"] = dict(flops=k["k_attn"]["flops"],
+                              bytes=k["k_attn"]["bytes"] + k["k_gather_state"]["bytes"])
+    return k
 
 
 CSRC = ("common.h", "api.hip", "graph.hip", "state.hip", "model.hip")
@@ -373,12 +380,12 @@ def main():
     if not args.no_profile:
         # pass 2: per-kernel durations (HIP events on the launch stream)
         sched.restart()
-        sched.run(0, W, pipelined=False)
+        sched.run(0, W)
         torch.cuda.synchronize()
         tgm.tgm_profile_reset()
         tgm.tgm_profile_enable(True)
         tp = time.perf_counter()
-        sched.run(W, K, pipelined=False)
+        sched.run(W, K)
         torch.cuda.synchronize()
         tp = time.perf_counter() - tp
         tgm.tgm_profile_enable(False)
