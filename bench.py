@@ -208,10 +208,14 @@ def work_model(wl, rows):
                              bytes=k["k_node_proj"]["bytes"] + k["k_stage"]["bytes"])
     k["k_attn_gather"] = dict(flops=k["k_attn"]["flops"],
                               bytes=k["k_attn"]["bytes"] + k["k_gather_state"]["bytes"])
+    # the attention with the query folded into the key weights computes the
+    # same embedding: the same algorithmic work
+    k["k_attn_fold"] = dict(k["k_attn"])
+    k["k_attn_fold_gather"] = dict(k["k_attn_gather"])
     return k
 
 
-CSRC = ("common.h", "api.hip", "graph.hip", "state.hip", "model.hip")
+CSRC = ("common.h", "api.hip", "graph.hip", "state.hip", "model.hip", "runner.hip")
 
 
 def pmc_summary(fetch_csv, write_csv, copy_mib, workload):

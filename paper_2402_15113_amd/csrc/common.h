@@ -131,6 +131,11 @@ struct tgm_model {
     int32_t KFC = 0, KVNB = 0;           // chunks of D_e + D_t, 16-col blocks of 2M
     tgm::f4 *kv_b = nullptr;
     float *pbias = nullptr;   // [PNB*16] bias of the node projection: c_q | b_k | b_v | 0
+    // attention with the query folded into the key weights (when the shapes fit)
+    bool fold = false;
+    int32_t VNB = 0, DC = 0;             // 16-col blocks of M, 16-wide chunks of M
+    tgm::f4 *v_b = nullptr;              // [KFC(+pad)][VNB][64]: V part of the slot weights
+    tgm::f4 *uk_a = nullptr;             // [DC][KFC][64]: W_k^t as A fragments
     // output projection
     int32_t OC = 0, ONB = 0;             // chunks of 2M, 16-col blocks of M
     tgm::f4 *out_b = nullptr;
@@ -201,6 +206,34 @@ __device__ __forceinline__ void keep_loaded(const f4 &a) { asm volatile("" ::"v"
 // Keeps the scheduler from moving instructions across this point (used right
 // after the prefetch loads so they are issued before the iteration's MFMAs).
 __device__ __forceinline__ void issue_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Reductions over one 16-lane DPP row (lanes 16i .. 16i + 15) with row-local
+// DPP moves: swaps inside quads (quad_perm [1,0,3,2], then [2,3,0,1]), then the
+// half-row and row mirrors.  Each step combines a lane with its partner's equal
+// partial (a+b and b+a round alike), so every lane of the row ends with the
+// same value.  Only the row's own lanes are read: other rows may be inactive.
+template <int CTRL>
+__device__ __forceinline__ float dpp_row(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+__device__ __forceinline__ float row16_max(float v)
+{
+    v = fmaxf(v, dpp_row<kDppXor1>(v));
+    v = fmaxf(v, dpp_row<kDppXor2>(v));
+    v = fmaxf(v, dpp_row<kDppHalfMirror>(v));
+    return fmaxf(v, dpp_row<kDppMirror>(v));
+}
+
+__device__ __forceinline__ float row16_sum(float v)
+{
+    v += dpp_row<kDppXor1>(v);
+    v += dpp_row<kDppXor2>(v);
+    v += dpp_row<kDppHalfMirror>(v);
+    return v + dpp_row<kDppMirror>(v);
+}
 
 __device__ __forceinline__ float wave_sum(float v)
 {

@@ -602,6 +602,8 @@ struct AttnArgs {
     const f4 *kv_b;
     int KFC, KVNB;
     const float *pbias;   // c_q | b_k | b_v: the rows of P carry it already
+    const f4 *v_b, *uk_a;     // folded attention: V weights, W_k^t fragments
+    int VNB, DC;              // 16-col blocks of M, 16-wide chunks of M
     const f4 *out_b;
     int OC, ONB;
     const float *b_o;
@@ -619,8 +621,9 @@ struct AttnArgs {
 //     accumulators start from the neighbour's node projection plus the bias,
 //     and the (row block, column block) tiles are dealt out evenly over the
 //     waves; K and V go back to LDS;
-//  4. scores (one thread per (root, head, slot)), softmax (one thread per
-//     (root, head)) and the weighted sum of V (one thread per output);
+//  4. scores, softmax and the weighted sum of V: for nb <= 16 two 16-lane rows
+//     per (root, head) with row-local DPP reductions; otherwise one thread per
+//     score, one wave per softmax and one thread per output;
 //  5. the output projection ReLU(W_o [a || s'_v] + b_o) as a second MFMA GEMM
 //     whose weights were fetched before step 4.
 constexpr int kAttMaxSlots = kAttMaxRB * 16;
@@ -650,47 +653,14 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
     float *A = lds;                                   // [RA][SA], then K|V [RA][SKV]
     float *Q = lds + RA * (SA > SKV ? SA : SKV);      // [RT][M]
     float *AO = Q + g.RT * M;                         // [ORB*16][SAO]: [a || s'_v]
-    float *S = AO + ORB * 16 * SAO;                   // [RT*H*nb] scores, then weights
+    float *S = AO + ORB * 16 * SAO;   // scores, then weights: [RT*H*nb], or [RT*H][16] for nb <= 16
     // [D_t] fp64 frequencies and phases, at an 8-byte aligned float offset
-    double *s_om = reinterpret_cast<double *>(lds + (((S - lds) + RA * H + 1) & ~(int64_t)1));
+    double *s_om = reinterpret_cast<double *>(
+        lds + (((S - lds) + H * max(RA, g.RT * 16) + 1) & ~(int64_t)1));
     double *s_be = s_om + D_t;
     const int nw = blockDim.x >> 6;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
-
-    // 1. metadata of the roots and of the slots (one round of loads, issued
-    // together), and the time-encoding constants
-    for (int r = tid; r < ORB * 16; r += blockDim.x) {
-        const int pv = r < nroots ? g.root_pos[r0 + r] : -1;
-        const bool ok = pv >= 0 && pv < n;
-        s_qoff[r] = ok ? (int64_t)pv * g.ldP : -1;
-        s_voff[r] = ok ? (int64_t)pv * M : -1;
-        s_cnt[r] = r < nroots ? g.cnt[r0 + r] : 0;
-    }
-    for (int sr = tid; sr < RA; sr += blockDim.x) {
-        const int r = sr / nb, j = sr - r * nb;
-        int c = 0, q = -1;
-        int64_t e = -1;
-        double t_root = 0.0, t_slot = 0.0;
-        if (r < nroots) {
-            const int64_t sl = (int64_t)(r0 + r) * nb + j;
-            c = g.cnt[r0 + r];
-            e = g.eid[sl];
-            q = g.nbr_pos[sl];
-            t_root = g.root_ts[r0 + r];
-            t_slot = g.nts[sl];
-        }
-        const bool ok = j < c;
-        s_ok[sr] = ok;
-        s_dt[sr] = t_root - t_slot;
-        s_eoff[sr] = (ok && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
-        s_np[sr] = (ok && q >= 0 && q < n) ? q : -1;
-    }
-    for (int d = tid; d < D_t; d += blockDim.x) {
-        s_om[d] = g.omega[d];
-        s_be[d] = g.beta[d];
-    }
-    __syncthreads();
 
     // GEMM tiles of this wave: column blocks cb0 = wave and cb1 = wave + nw
     // (cb1 = cb0 when past the last block: the copy computes and stores the same
@@ -699,10 +669,12 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
     const int cb0 = wave, cb1 = wave + nw < g.KVNB ? wave + nw : wave;
     const bool has_tiles = cb0 < g.KVNB;
 
-    // 2. every load of the slot rows, in the order it is consumed (a wave's
-    // loads complete in issue order): the weights of the chunks made of time
-    // codes only, the edge-feature rows, the accumulator seeds P[nbr][M + col];
-    // the time codes are computed while they are in flight
+    // A wave's loads complete in issue order, so they are issued in the order
+    // they are consumed: the weights of the chunks made of time codes only
+    // (they do not depend on the batch: issued first, they arrive with the
+    // metadata), the metadata, the edge-feature rows (consumed after the
+    // time-code chunks), then, once the GEMM runs, the query and s'_v rows and
+    // the accumulator seeds (consumed at its end).
     const int P1 = min(D_t / 16, kAttPre);   // k-chunks of time codes only
     const int64_t kstep = (int64_t)g.KVNB * kWave;
     const f4 *p0 = g.kv_b + (int64_t)(has_tiles ? cb0 : 0) * kWave + lane;
@@ -713,26 +685,63 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
         bpre[kc][0] = p0[kc * kstep];
         bpre[kc][1] = p0[kc * kstep + o1];
     }
-    issue_fence();   // every weight load goes out before the row loads
-    // query rows (the node projection carries the folded bias c_q; a root
-    // without a position gets c_q alone) and s'_v rows: two vectors per thread
-    // now (branch-free), stored after the GEMM; the rest after the GEMM
-    const bool qv4 = (M & 3) == 0 && (reinterpret_cast<uintptr_t>(g.mem_new) & 15) == 0;
-    const int M4 = qv4 ? M >> 2 : 0, M4c = qv4 ? M >> 2 : 1;
-    const int nq4 = nroots * M4, nv4 = ORB * 16 * M4;
-    f4 qreg[2], vreg[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int i = tid + u * blockDim.x;
-        const int rq = i < nq4 ? i / M4c : 0, cq = i < nq4 ? i - rq * M4c : 0;
-        const int rv = i < nv4 ? i / M4c : 0, cv = i < nv4 ? i - rv * M4c : 0;
-        const int64_t oq = s_qoff[rq], ov = s_voff[rv];
-        qreg[u] = *reinterpret_cast<const f4 *>(oq >= 0 && qv4 ? g.P + oq + 4 * cq
-                                                               : g.pbias + 4 * cq);
-        vreg[u] = *reinterpret_cast<const f4 *>(ov >= 0 && qv4 ? g.mem_new + ov + 4 * cv
-                                                               : g.mem_new);
+    issue_fence();
+
+    // 1. metadata of the roots and of the slots and the time-encoding constants
+    // in one round of loads (branch-free: indices clamped, results masked; the
+    // launch has at least ORB * 16 and RA threads), and the zero parts of the
+    // output projection's input: columns [0, M) of rows without a root, the
+    // padding [2M, ..)
+    {
+        const int rr = min(tid, nroots - 1);
+        const int sr = min(tid, RA - 1);
+        const int r = sr / nb, j = sr - r * nb;
+        const int rc = min(r, nroots - 1);
+        const int64_t sl = (int64_t)(r0 + rc) * nb + j;
+        const int dd = min(tid, max(D_t - 1, 0));
+        const int pv = g.root_pos[r0 + rr];
+        const int c_root = g.cnt[r0 + rr];
+        const int c_slot = g.cnt[r0 + rc];
+        const int64_t e = g.eid[sl];
+        const int q = g.nbr_pos[sl];
+        const double t_root = g.root_ts[r0 + rc];
+        const double t_slot = g.nts[sl];
+        const double om = g.omega[dd], be = g.beta[dd];
+        if (tid < ORB * 16) {
+            const bool ok = tid < nroots && pv >= 0 && pv < n;
+            s_qoff[tid] = ok ? (int64_t)pv * g.ldP : -1;
+            s_voff[tid] = ok ? (int64_t)pv * M : -1;
+            s_cnt[tid] = tid < nroots ? c_root : 0;
+        }
+        if (tid < RA) {
+            const bool ok = r < nroots && j < c_slot;
+            s_ok[sr] = ok;
+            s_dt[sr] = r < nroots ? t_root - t_slot : 0.0;
+            s_eoff[sr] = (ok && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
+            s_np[sr] = (ok && q >= 0 && q < n) ? q : -1;
+        }
+        if (tid < D_t) {
+            s_om[tid] = om;
+            s_be[tid] = be;
+        }
+        for (int d = tid + blockDim.x; d < D_t; d += blockDim.x) {
+            s_om[d] = g.omega[d];
+            s_be[d] = g.beta[d];
+        }
     }
-    // wave w stages slot rows w + kMaxWaves i (the launch has kMaxWaves waves)
+    {
+        const int w2 = g.OC * 16 - M;
+        for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
+            const int r = idx / w2, c = idx - r * w2;
+            if (c >= M || r >= nroots)
+                AO[r * SAO + (c < M ? c : M + c)] = 0.f;
+        }
+    }
+    __syncthreads();
+
+    // 2. the edge-feature rows of the slots (to registers; wave w stages slot
+    // rows w + kMaxWaves i, the launch has kMaxWaves waves), then the time codes
+    // phi(t_root - t_slot) in columns [0, D_t) while they are in flight
     constexpr int RPW = 2 * RB;   // RB * 16 / kMaxWaves
     int64_t eoff[RPW];
     int lr[RPW];
@@ -755,23 +764,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
         eoffv[i] = vec_e ? eoff[i] : -1;
     WaveRows<4, RPW, 1> xf;
     xf.load(vec_e ? g.efeat : g.P, eoffv, D_e, lane);
-    // seeds: the neighbour's row of P (node projection plus bias), or the bias
-    // alone for a slot without a neighbour; columns past 2M read column 0
-    f4 seed[2][RB];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int c = (i ? cb1 : cb0) * 16 + (lane & 15);
-        const int col = M + (c < 2 * M ? c : 0);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int np = s_np[rb * 16 + 4 * (lane >> 4) + v];
-                seed[i][rb][v] = *(np >= 0 ? g.P + (int64_t)np * g.ldP + col : g.pbias + col);
-            }
-    }
-    // time codes phi(t_root - t_slot) in columns [0, D_t) (the RPW rows of a
-    // column are independent chains) and the zero padding past D_t + D_e
+    issue_fence();
+    // (the RPW rows of a column are independent chains) and the zero padding
+    // past D_t + D_e
     for (int d = lane; d < D_t; d += kWave) {
         const double om = s_om[d], be = s_be[d];
 #pragma unroll
@@ -810,9 +805,47 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
             }                                                                               \
         }                                                                                   \
     }
+    if (has_tiles && P1 > 0)
+        TGM_ATT_MMA(0, bpre[0][0], bpre[0][1])
+    issue_fence();
+    // query rows (the node projection carries the folded bias c_q; a root
+    // without a position gets c_q alone) and s'_v rows: two vectors per thread
+    // (branch-free), stored before the second part of the GEMM; the rest after
+    // the GEMM
+    const bool qv4 = (M & 3) == 0 && (reinterpret_cast<uintptr_t>(g.mem_new) & 15) == 0;
+    const int M4 = qv4 ? M >> 2 : 0, M4c = qv4 ? M >> 2 : 1;
+    const int nq4 = nroots * M4, nv4 = ORB * 16 * M4;
+    f4 qreg[2], vreg[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        const int rq = i < nq4 ? i / M4c : 0, cq = i < nq4 ? i - rq * M4c : 0;
+        const int rv = i < nv4 ? i / M4c : 0, cv = i < nv4 ? i - rv * M4c : 0;
+        const int64_t oq = s_qoff[rq], ov = s_voff[rv];
+        qreg[u] = *reinterpret_cast<const f4 *>(oq >= 0 && qv4 ? g.P + oq + 4 * cq
+                                                               : g.pbias + 4 * cq);
+        vreg[u] = *reinterpret_cast<const f4 *>(ov >= 0 && qv4 ? g.mem_new + ov + 4 * cv
+                                                               : g.mem_new);
+    }
+    // seeds: the neighbour's row of P (node projection plus bias), or the bias
+    // alone for a slot without a neighbour; columns past 2M read column 0
+    f4 seed[2][RB];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int c = (i ? cb1 : cb0) * 16 + (lane & 15);
+        const int col = M + (c < 2 * M ? c : 0);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int np = s_np[rb * 16 + 4 * (lane >> 4) + v];
+                seed[i][rb][v] = *(np >= 0 ? g.P + (int64_t)np * g.ldP + col : g.pbias + col);
+            }
+    }
+    issue_fence();
     if (has_tiles) {
 #pragma unroll
-        for (int kc = 0; kc < kAttPre; ++kc)
+        for (int kc = 1; kc < kAttPre; ++kc)
             if (kc < P1)
                 TGM_ATT_MMA(kc, bpre[kc][0], bpre[kc][1])
     }
@@ -821,6 +854,33 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
     // (no chunk read so far touches them)
     const f4 *pk = p0 + P1 * kstep;
     f4 x0 = pk[0], x1 = pk[o1];
+    // the output projection's weights, used in step 5 (unconditional: the
+    // packed weights hold kAttMaxOC chunks, zero past OC; waves beyond ONB
+    // load the last block and compute nothing)
+    f4 ob[kAttMaxOC];
+    const int ocb = wave;
+    const float bo = g.b_o[min(ocb * 16 + (lane & 15), M - 1)];
+    {
+        const f4 *ob0 = g.out_b + (int64_t)min(ocb, g.ONB - 1) * kWave + lane;
+#pragma unroll
+        for (int kc = 0; kc < kAttMaxOC; ++kc)
+            ob[kc] = ob0[(int64_t)kc * g.ONB * kWave];
+    }
+    issue_fence();
+    // the query rows and the [. || s'_v] rows of the output projection's input
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        if (i < nq4) {
+            const int r = i / M4c, c = i - r * M4c;
+            *reinterpret_cast<f4 *>(Q + r * M + 4 * c) = qreg[u];
+        }
+        if (i < nv4) {
+            const int r = i / M4c, c = i - r * M4c;
+            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
+                s_voff[r] >= 0 ? vreg[u] : f4{0, 0, 0, 0};
+        }
+    }
     if (vec_e) {
         xf.store(A, SA, D_t, lr, eoffv, D_e, lane);
     } else if (D_e > 0) {   // unaligned or empty edge features: plain copies
@@ -855,35 +915,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
             for (int rb = 0; rb < RB; ++rb)
                 acc[i][rb] += seed[i][rb];
     }
-    __syncthreads();   // every read of the slot rows is done
-
-    float *KV = A;
-    if (has_tiles) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int col = (i ? cb1 : cb0) * 16 + (lane & 15);
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-                for (int v = 0; v < 4; ++v)
-                    KV[(rb * 16 + 4 * (lane >> 4) + v) * SKV + col] = acc[i][rb][v];
-        }
-    }
-    // the query rows and the [. || s'_v] rows of the output projection's input
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-        const int i = tid + u * blockDim.x;
-        if (i < nq4) {
-            const int r = i / M4c, c = i - r * M4c;
-            *reinterpret_cast<f4 *>(Q + r * M + 4 * c) = qreg[u];
-        }
-        if (i < nv4) {
-            const int r = i / M4c, c = i - r * M4c;
-            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
-                s_voff[r] >= 0 ? vreg[u] : f4{0, 0, 0, 0};
-        }
-    }
-    if (qv4) {   // vectors past the first two per thread
+    // query and s'_v vectors past the first two per thread (none of this
+    // touches the slot rows)
+    if (qv4) {
         for (int i = tid + 2 * blockDim.x; i < max(nq4, nv4); i += blockDim.x) {
             const int r = i / M4c, c = i - r * M4c;
             if (i < nq4)
@@ -903,98 +937,168 @@ __device__ __forceinline__ void attn_block(const AttnArgs &g, float *lds, int bi
             AO[r * SAO + M + k] = s_voff[r] >= 0 ? g.mem_new[s_voff[r] + k] : 0.f;
         }
     }
-    {
-        // AO: columns [0, M) of rows without a root and the padding [2M, ..)
-        const int w2 = g.OC * 16 - M;
-        for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
-            const int r = idx / w2, c = idx - r * w2;
-            if (c >= M || r >= nroots)
-                AO[r * SAO + (c < M ? c : M + c)] = 0.f;
+    __syncthreads();   // every read of the slot rows is done
+
+    // K|V over the slot rows
+    float *KV = A;
+    if (has_tiles) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int col = (i ? cb1 : cb0) * 16 + (lane & 15);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    KV[(rb * 16 + 4 * (lane >> 4) + v) * SKV + col] = acc[i][rb][v];
         }
     }
-    // the output projection's weights: fetched now, used in step 5
-    f4 ob[kAttMaxOC];
-    const int ocb = wave;   // waves beyond ONB have no output column block
-#pragma unroll
-    for (int kc = 0; kc < kAttMaxOC; ++kc)
-        ob[kc] = (ocb < g.ONB && kc < g.OC)
-                     ? g.out_b[((int64_t)kc * g.ONB + ocb) * kWave + lane]
-                     : f4{0, 0, 0, 0};
     __syncthreads();
 
-    // 4. attention: scores (one thread per (root, head, slot)), softmax (one
-    // wave per (root, head): lane j holds slot j, reductions over lanes) and
-    // the weighted sum of V (one thread per output)
+    // 4. attention
     const int d_h = M / H;
     const float scale = 1.0f / sqrtf((float)d_h);
-    const int nsc = nroots * H * nb;
-    for (int idx = tid; idx < nsc; idx += blockDim.x) {
-        const int r = idx / (H * nb), rem = idx - r * (H * nb);
-        const int eta = rem / nb, j = rem - eta * nb;
-        float sc = -INFINITY;
-        if (j < s_cnt[r]) {
+    if (nb <= 16) {
+        // two 16-lane rows per (root, head), h = bit 4 of the lane: lane j of
+        // both rows scores slot j over alternate pairs of the head's dimensions
+        // and a swap of the rows adds the halves (in one order on both); the
+        // softmax reductions stay inside the row (DPP); the row with h = 0
+        // writes the 16 weights (zero past c) to S, and both rows read them
+        // back (same wave: LDS is in order) for the weighted sum of V, whose
+        // d_h outputs they share
+        const int j = lane & 15, h = (lane >> 4) & 1;
+        const int npair = nroots * H;
+        const bool pairs = (d_h & 1) == 0;   // 8-byte aligned dimension pairs
+        for (int pr = wave * 2 + (lane >> 5); pr < npair; pr += nw * 2) {
+            const int r = pr / H, eta = pr - r * H;
+            const int c = s_cnt[r];
             const float *qr = Q + r * M + eta * d_h;
-            const float *kr = KV + (r * nb + j) * SKV + eta * d_h;
-            float dot = 0.f;
-            for (int d = 0; d < d_h; ++d)
-                dot += qr[d] * kr[d];
-            sc = dot * scale;
+            const float *kr = KV + (r * nb + min(j, nb - 1)) * SKV + eta * d_h;
+            float d0 = 0.f, d1 = 0.f;
+            if (pairs) {
+                int d = 2 * h;
+                for (; d + 13 < d_h; d += 16) {   // four pairs, loads issued together
+                    float2 q2[4], k2[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        q2[t] = *reinterpret_cast<const float2 *>(qr + d + 4 * t);
+                        k2[t] = *reinterpret_cast<const float2 *>(kr + d + 4 * t);
+                    }
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        d0 += q2[t].x * k2[t].x;
+                        d1 += q2[t].y * k2[t].y;
+                    }
+                }
+                for (; d < d_h; d += 4) {
+                    const float2 q2 = *reinterpret_cast<const float2 *>(qr + d);
+                    const float2 k2 = *reinterpret_cast<const float2 *>(kr + d);
+                    d0 += q2.x * k2.x;
+                    d1 += q2.y * k2.y;
+                }
+            } else {
+                for (int d = h; d < d_h; d += 2)
+                    d0 += qr[d] * kr[d];
+            }
+            const float part = d0 + d1;
+            const float other = __shfl_xor(part, 16, kWave);
+            const float dot = h ? other + part : part + other;
+            const float sc = j < c ? dot * scale : -INFINITY;
+            const float mx = row16_max(sc);
+            const float e = j < c ? expf(sc - mx) : 0.f;
+            const float den = row16_sum(e);
+            float *al = S + pr * 16;
+            if (h == 0)
+                al[j] = j < c ? e / den : 0.f;
+            float alv[16];
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj)
+                alv[jj] = al[jj];
+            const float *vr = KV + r * nb * SKV + M + eta * d_h;
+            float *ar = AO + r * SAO + eta * d_h;
+            for (int k = j + 16 * h; k < d_h; k += 32) {
+                float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+                for (int jj = 0; jj < 16; jj += 2) {
+                    a0 += alv[jj] * vr[min(jj, nb - 1) * SKV + k];
+                    a1 += alv[jj + 1] * vr[min(jj + 1, nb - 1) * SKV + k];
+                }
+                ar[k] = a0 + a1;   // 0 when the root has no neighbours
+            }
         }
-        S[idx] = sc;
-    }
-    __syncthreads();
-    for (int pr = wave; pr < nroots * H; pr += nw) {
-        const int c = s_cnt[pr / H];
-        float *sr = S + pr * nb;
-        const float sc = lane < c ? sr[lane] : -INFINITY;
-        float mx = sc;
+    } else {
+        // scores (one thread per (root, head, slot)), softmax (one wave per
+        // (root, head): lane j holds slot j, reductions over lanes) and the
+        // weighted sum of V (one thread per output)
+        const int nsc = nroots * H * nb;
+        for (int idx = tid; idx < nsc; idx += blockDim.x) {
+            const int r = idx / (H * nb), rem = idx - r * (H * nb);
+            const int eta = rem / nb, j = rem - eta * nb;
+            float sc = -INFINITY;
+            if (j < s_cnt[r]) {
+                const float *qr = Q + r * M + eta * d_h;
+                const float *kr = KV + (r * nb + j) * SKV + eta * d_h;
+                float dot = 0.f;
+                for (int d = 0; d < d_h; ++d)
+                    dot += qr[d] * kr[d];
+                sc = dot * scale;
+            }
+            S[idx] = sc;
+        }
+        __syncthreads();
+        for (int pr = wave; pr < nroots * H; pr += nw) {
+            const int c = s_cnt[pr / H];
+            float *sr = S + pr * nb;
+            const float sc = lane < c ? sr[lane] : -INFINITY;
+            float mx = sc;
 #pragma unroll
-        for (int o = kWave / 2; o >= 1; o >>= 1)
-            mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
-        const float e = lane < c ? expf(sc - mx) : 0.f;
-        float den = e;
+            for (int o = kWave / 2; o >= 1; o >>= 1)
+                mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+            const float e = lane < c ? expf(sc - mx) : 0.f;
+            float den = e;
 #pragma unroll
-        for (int o = kWave / 2; o >= 1; o >>= 1)
-            den += __shfl_xor(den, o, kWave);
-        if (lane < c)
-            sr[lane] = e / den;
-    }
-    __syncthreads();
-    for (int idx = tid; idx < nroots * M; idx += blockDim.x) {
-        const int r = idx / M, k = idx - r * M;
-        const int eta = k / d_h;
-        const float *al = S + (r * H + eta) * nb;
-        const int c = s_cnt[r];
-        float a = 0.f;
-        for (int j = 0; j < c; ++j)
-            a += al[j] * KV[(r * nb + j) * SKV + M + k];
-        AO[r * SAO + k] = a;   // 0 when the root has no neighbours
+            for (int o = kWave / 2; o >= 1; o >>= 1)
+                den += __shfl_xor(den, o, kWave);
+            if (lane < c)
+                sr[lane] = e / den;
+        }
+        __syncthreads();
+        for (int idx = tid; idx < nroots * M; idx += blockDim.x) {
+            const int r = idx / M, k = idx - r * M;
+            const int eta = k / d_h;
+            const float *al = S + (r * H + eta) * nb;
+            const int c = s_cnt[r];
+            float a = 0.f;
+            for (int j = 0; j < c; ++j)
+                a += al[j] * KV[(r * nb + j) * SKV + M + k];
+            AO[r * SAO + k] = a;   // 0 when the root has no neighbours
+        }
     }
     __syncthreads();
 
-    // 5. h = ReLU(W_o [a || s'_v] + b_o), two accumulators over alternate chunks
+    // 5. h = ReLU(W_o [a || s'_v] + b_o): the row block's fragments first (chunks
+    // past OC re-read the last one against zero weights), then four accumulators
+    // over the chunks
     if (ocb < g.ONB) {
         const float *orow = AO + (lane & 15) * SAO + 4 * (lane >> 4);
         const int col = ocb * 16 + (lane & 15);
+        const int OC = g.OC;
         for (int orb = 0; orb < ORB; ++orb) {
-            f4 ac0 = {0, 0, 0, 0}, ac1 = ac0;
+            f4 af[kAttMaxOC];
 #pragma unroll
-            for (int kc = 0; kc < kAttMaxOC; kc += 2) {
-                if (kc < g.OC)
-                    ac0 = mfma_k16(*reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + kc * 16),
-                                   ob[kc], ac0);
-                if (kc + 1 < g.OC)
-                    ac1 = mfma_k16(
-                        *reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + (kc + 1) * 16),
-                        ob[kc + 1], ac1);
-            }
+            for (int kc = 0; kc < kAttMaxOC; ++kc)
+                af[kc] = *reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + min(kc, OC - 1) * 16);
+            f4 ac[4] = {{0, 0, 0, 0}, {0, 0, 0, 0}, {0, 0, 0, 0}, {0, 0, 0, 0}};
+#pragma unroll
+            for (int kc = 0; kc < kAttMaxOC; ++kc)
+                if (kc < OC)
+                    ac[kc & 3] = mfma_k16(af[kc], ob[kc], ac[kc & 3]);
             if (col < M) {
-                const float bo = g.b_o[col];
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int r = orb * 16 + 4 * (lane >> 4) + v;
                     if (r < nroots)
-                        g.h[(int64_t)(r0 + r) * M + col] = fmaxf(ac0[v] + ac1[v] + bo, 0.f);
+                        g.h[(int64_t)(r0 + r) * M + col] =
+                            fmaxf((ac[0][v] + ac[1][v]) + (ac[2][v] + ac[3][v]) + bo, 0.f);
                 }
             }
         }
@@ -1026,6 +1130,508 @@ __global__ __launch_bounds__(512) void k_attn_gather(AttnArgs g, int n_attn, Gat
         gather_row(gp, p, threadIdx.x & 63);
 }
 
+// ---------------------------------------------------------------------------
+// Attention with the query folded into the key weights.  Each score is
+//   q_r,eta . K_s,eta = sum_k a_s[k] U[k][(r, eta)] + seedK_s,eta . q_r,eta
+// with a_s = [phi || efeat] the slot row, seedK_s the neighbour's key part of
+// P (node projection plus b_k) and U[k][(r, eta)] = sum_{d in head eta}
+// W_k[d][k] q_r[d] (Sec. 4's attention restated by associativity).  K itself
+// is never formed: the per-slot GEMM produces V (VNB column blocks) and one
+// block of 16 score columns (n = r * H + eta, RT * H <= 16) instead of the
+// 2M columns of K | V.  Roles of the kMaxWaves wavefronts:
+//   * wave w < VNB: V column block w over all RB row blocks;
+//   * wave VNB (the score wave): the score block, first the seedK . q part
+//     (K = M, operands straight from P), then [phi || efeat] x U;
+//   * waves on SIMDs (wave % 4) other than the score wave's: the U GEMM
+//     (KFC row blocks of 16 k, K = M, weights W_k^t preloaded).
+// A wave's loads complete in issue order, so each issues what it consumes
+// first before the edge-feature rows (the slow, HBM-bound loads).
+constexpr int kAttUT = 3;   // U tiles per wavefront
+constexpr int kAttDC = 7;   // 16-wide chunks of M (M <= 112)
+constexpr int kAttFoldOC = 2 * kAttDC;   // 16-wide chunks of [a || s'_v]
+
+template <int RB>   // 16-row slot blocks per workgroup (3..5)
+__device__ __forceinline__ void attn_fold_block(const AttnArgs &g, float *lds, int bid)
+{
+    __shared__ int s_np[kAttMaxSlots];         // neighbour's node-set position, -1 if none
+    __shared__ int64_t s_qoff[kAttMaxSlots], s_voff[kAttMaxSlots];
+    __shared__ int s_cnt[kAttMaxSlots];
+    __shared__ int64_t s_eoff[kAttMaxSlots];   // edge-feature row offset, -1 if none
+    __shared__ double s_dt[kAttMaxSlots];      // t_root - t_slot
+    __shared__ int s_ok[kAttMaxSlots];         // slot holds a sampled neighbour
+    const int r0 = bid * g.RT;
+    const int nroots = min(g.RT, g.R - r0);
+    if (nroots <= 0)
+        return;
+    const int M = g.M, nb = g.nb, D_e = g.D_e, D_t = g.D_t, H = g.H;
+    const int n = *g.n_nodes;   // positions and event ids are bounds-checked
+    const int KFC = g.KFC, VNB = g.VNB, DC = g.DC;
+    const int RA = RB * 16;
+    const int KF = KFC * 16, SA = KF + 4, SV = VNB * 16 + 4;
+    const int ORB = (g.RT + 15) / 16;
+    const int SAO = g.OC * 16 + 4;
+    const int d_h = M / H;
+    float *A = lds;                                             // [RA][SA], then V [RA][SV]
+    f4 *U = reinterpret_cast<f4 *>(A + RA * SA);                // [KFC][64] B fragments
+    float *AO = reinterpret_cast<float *>(U + KFC * kWave);     // [ORB*16][SAO]: [a || s'_v]
+    float *S = AO + ORB * 16 * SAO;                             // [RA][H] scores
+    float *Wt = S + RA * H;                                     // [RT*H][16] weights
+    double *s_om = reinterpret_cast<double *>(
+        lds + (((Wt - lds) + g.RT * H * 16 + 1) & ~(int64_t)1));
+    double *s_be = s_om + D_t;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
+    const bool is_v = wave < VNB, is_s = wave == VNB;
+    int ui = -1, NU = 0;   // this wave's index among the U waves, their number
+    for (int w = 0; w < kMaxWaves; ++w)
+        if ((w & 3) != (VNB & 3)) {
+            if (w == wave)
+                ui = NU;
+            ++NU;
+        }
+
+    // 0. the W_k^t fragments of this wave's U tiles (they do not depend on the
+    // batch; indices clamped).  Loads issued inside a role's branch are only
+    // waited for inside it, before any later load is: the wait counts stay
+    // exact on every path.
+    f4 ua[kAttUT][kAttDC];
+    if (ui >= 0) {
+#pragma unroll
+        for (int t = 0; t < kAttUT; ++t) {
+            const int kb = min(ui + NU * t, KFC - 1);
+#pragma unroll
+            for (int dc = 0; dc < kAttDC; ++dc)
+                ua[t][dc] = g.uk_a[((int64_t)min(dc, DC - 1) * KFC + kb) * kWave + lane];
+        }
+    }
+    issue_fence();
+
+    // 1. metadata of the roots and of the slots and the time-encoding constants
+    // in one round of loads (branch-free: indices clamped, results masked; the
+    // launch has at least ORB * 16 and RA threads), and the zero parts of the
+    // output projection's input: columns [0, M) of rows without a root, the
+    // padding [2M, ..)
+    {
+        const int rr = min(tid, nroots - 1);
+        const int sr = min(tid, RA - 1);
+        const int r = sr / nb, j = sr - r * nb;
+        const int rc = min(r, nroots - 1);
+        const int64_t sl = (int64_t)(r0 + rc) * nb + j;
+        const int dd = min(tid, max(D_t - 1, 0));
+        const int pv_ = g.root_pos[r0 + rr];
+        const int c_root = g.cnt[r0 + rr];
+        const int c_slot = g.cnt[r0 + rc];
+        const int64_t e = g.eid[sl];
+        const int q = g.nbr_pos[sl];
+        const double t_root = g.root_ts[r0 + rc];
+        const double t_slot = g.nts[sl];
+        const double om = g.omega[dd], be = g.beta[dd];
+        if (tid < ORB * 16) {
+            const bool ok = tid < nroots && pv_ >= 0 && pv_ < n;
+            s_qoff[tid] = ok ? (int64_t)pv_ * g.ldP : -1;
+            s_voff[tid] = ok ? (int64_t)pv_ * M : -1;
+            s_cnt[tid] = tid < nroots ? c_root : 0;
+        }
+        if (tid < RA) {
+            const bool ok = r < nroots && j < c_slot;
+            s_ok[sr] = ok;
+            s_dt[sr] = r < nroots ? t_root - t_slot : 0.0;
+            s_eoff[sr] = (ok && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
+            s_np[sr] = (ok && q >= 0 && q < n) ? q : -1;
+        }
+        if (tid < D_t) {
+            s_om[tid] = om;
+            s_be[tid] = be;
+        }
+        for (int d = tid + blockDim.x; d < D_t; d += blockDim.x) {
+            s_om[d] = g.omega[d];
+            s_be[d] = g.beta[d];
+        }
+        const int w2 = g.OC * 16 - M;
+        for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
+            const int rw = idx / w2, c = idx - rw * w2;
+            if (c >= M || rw >= nroots)
+                AO[rw * SAO + (c < M ? c : M + c)] = 0.f;
+        }
+    }
+    __syncthreads();
+
+    // 2. query fragments (every wave: the B operand of the U GEMM and of the
+    // score wave's seed part): lane l holds q_r[d] of column n = l % 16
+    // (r = n / H, eta = n % H) for d = 16 dc + 4 (l / 16) + j, zero outside
+    // head eta, past M and for a column without a root; a root without a
+    // position has the folded bias c_q as its query
+    const int cn = lane & 15, cr = cn / H, ceta = cn - cr * H;
+    f4 bq[kAttDC];
+    {
+        const int64_t qo = cr < nroots ? s_qoff[cr] : -1;
+        const float *qrow = qo >= 0 ? g.P + qo : g.pbias;
+#pragma unroll
+        for (int dc = 0; dc < kAttDC; ++dc)
+            bq[dc] = *reinterpret_cast<const f4 *>(qrow + min(16 * dc + 4 * (lane >> 4), M - 4));
+    }
+    issue_fence();
+    // the score wave's seed part: K = M over the neighbours' key rows of P (or
+    // b_k for a slot without one), A fragments double-buffered per row block
+    f4 acc[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+        acc[rb] = f4{0, 0, 0, 0};
+    // (masked where first used, after the loads that must not wait for it)
+    auto mask_q = [&]() {
+        const int lo = ceta * d_h, hi = cr < nroots ? lo + d_h : lo;
+#pragma unroll
+        for (int dc = 0; dc < kAttDC; ++dc)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int d = 16 * dc + 4 * (lane >> 4) + j;
+                if (!(d >= lo && d < hi))
+                    bq[dc][j] = 0.f;
+            }
+    };
+    constexpr int RPW = 2 * RB;   // slot rows staged per wave (RB * 16 / kMaxWaves)
+    int64_t eoff[RPW];
+    int lr[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+        lr[i] = wave + kMaxWaves * i;
+        eoff[i] = s_eoff[lr[i]];
+    }
+    const bool vec_e = D_e > 0 && g.E > 0 && (reinterpret_cast<uintptr_t>(g.efeat) & 15) == 0 &&
+                       (D_e & 3) == 0 && (D_t & 3) == 0;
+    int64_t eoffv[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i)
+        eoffv[i] = vec_e ? eoff[i] : -1;
+    WaveRows<4, RPW, 1> xf;
+    const int P1 = min(D_t / 16, kAttPre);   // k-chunks of time codes only
+    const int64_t vstep = (int64_t)VNB * kWave;
+    const f4 *pv = g.v_b + (int64_t)(is_v ? wave : 0) * kWave + lane;
+    f4 bpre[kAttPre];
+    if (is_s) {
+        auto seed_row = [&](int rb, f4 (&a)[kAttDC]) {
+            const int np = s_np[rb * 16 + (lane & 15)];
+            const float *row = (np >= 0 ? g.P + (int64_t)np * g.ldP : g.pbias) + M;
+#pragma unroll
+            for (int dc = 0; dc < kAttDC; ++dc)
+                a[dc] = *reinterpret_cast<const f4 *>(row + min(16 * dc + 4 * (lane >> 4), M - 4));
+        };
+        f4 sa[2][kAttDC];
+        seed_row(0, sa[0]);
+        mask_q();
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            if (rb + 1 < RB)
+                seed_row(rb + 1, sa[(rb + 1) & 1]);
+            issue_fence();
+#pragma unroll
+            for (int dc = 0; dc < kAttDC; ++dc)   // bq is zero past M
+                acc[rb] = mfma_k16(sa[rb & 1][dc], bq[dc], acc[rb]);
+        }
+    } else if (ui >= 0) {
+        mask_q();
+        {   // U tiles kb = ui + NU t: U[16 kb .. +16][n] -> LDS
+            f4 au[kAttUT];
+#pragma unroll
+            for (int t = 0; t < kAttUT; ++t)
+                au[t] = f4{0, 0, 0, 0};
+#pragma unroll
+            for (int dc = 0; dc < kAttDC; ++dc)   // bq is zero past M
+#pragma unroll
+                for (int t = 0; t < kAttUT; ++t)
+                    au[t] = mfma_k16(ua[t][dc], bq[dc], au[t]);
+#pragma unroll
+            for (int t = 0; t < kAttUT; ++t) {
+                const int kb = ui + NU * t;
+                if (kb < KFC)
+                    U[kb * kWave + lane] = au[t];
+            }
+        }
+    }
+    // then the loads consumed in step 3 (after the fragments above, whose waits
+    // they would otherwise join): the V weights of the chunks made of time
+    // codes only, and the edge-feature rows
+    if (is_v) {
+#pragma unroll
+        for (int kc = 0; kc < kAttPre; ++kc)   // chunks past P1 are loaded and unused
+            bpre[kc] = pv[kc * vstep];
+    }
+    xf.load(vec_e ? g.efeat : g.P, eoffv, D_e, lane);
+    issue_fence();
+    // time codes phi(t_root - t_slot) in columns [0, D_t) (the RPW rows of a
+    // column are independent chains) and the zero padding past D_t + D_e
+    {
+        double dts[RPW];
+        bool oks[RPW];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            dts[i] = s_dt[lr[i]];
+            oks[i] = s_ok[lr[i]] != 0;
+        }
+        for (int d = lane; d < D_t; d += kWave) {
+            const double om = s_om[d], be = s_be[d];
+#pragma unroll
+            for (int i = 0; i < RPW; ++i)
+                A[lr[i] * SA + d] = oks[i] ? time_enc(om, be, dts[i]) : 0.f;
+        }
+    }
+    for (int k = D_t + D_e + lane; k < KF; k += kWave)
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+            A[lr[i] * SA + k] = 0.f;
+    __syncthreads();
+
+    // 3. the per-slot GEMM over [phi || efeat]: the time-code chunks first (V
+    // weights in registers, U in LDS: no wait on the rows in flight), then the
+    // edge-feature rows go to LDS and the remaining chunks follow
+    const float *arow = A + (lane & 15) * SA + 4 * (lane >> 4);
+// one k-chunk against the B fragment b: the RB A fragments, then the MFMAs
+#define TGM_FOLD_MMA(KC, B)                                                                 \
+    {                                                                                       \
+        f4 a_[RB];                                                                          \
+        _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                                   \
+            a_[rb] = *reinterpret_cast<const f4 *>(arow + rb * 16 * SA + (KC) * 16);        \
+        _Pragma("unroll") for (int j = 0; j < 4; ++j)                                       \
+        {                                                                                   \
+            _Pragma("unroll") for (int rb = 0; rb < RB; ++rb)                               \
+                acc[rb] = mfma_16x16x4(a_[rb][j], (B)[j], acc[rb]);                          \
+        }                                                                                   \
+    }
+    if (is_v && P1 > 0) {
+        TGM_FOLD_MMA(0, bpre[0])
+    } else if (is_s && P1 > 0) {
+        const f4 ub = U[lane];
+        TGM_FOLD_MMA(0, ub)
+    }
+    issue_fence();
+    // s'_v rows of the output projection's input (two vectors per thread,
+    // branch-free; the rest after the GEMM) and the V seeds: the neighbour's
+    // value row of P, or b_v alone for a slot without a neighbour
+    const bool v4 = (M & 3) == 0 && (reinterpret_cast<uintptr_t>(g.mem_new) & 15) == 0;
+    const int M4 = v4 ? M >> 2 : 0, M4c = v4 ? M >> 2 : 1;
+    const int nv4 = ORB * 16 * M4;
+    f4 vreg[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        const int rv = i < nv4 ? i / M4c : 0, cv = i < nv4 ? i - rv * M4c : 0;
+        const int64_t ov = s_voff[rv];
+        vreg[u] = *reinterpret_cast<const f4 *>(ov >= 0 && v4 ? g.mem_new + ov + 4 * cv
+                                                              : g.mem_new);
+    }
+    f4 seed[RB];
+    {
+        const int c = (is_v ? wave : 0) * 16 + (lane & 15);
+        const int col = 2 * M + (c < M ? c : 0);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int np = s_np[rb * 16 + 4 * (lane >> 4) + v];
+                seed[rb][v] = *(np >= 0 ? g.P + (int64_t)np * g.ldP + col : g.pbias + col);
+            }
+    }
+    issue_fence();
+    if (is_v) {
+#pragma unroll
+        for (int kc = 1; kc < kAttPre; ++kc)
+            if (kc < P1)
+                TGM_FOLD_MMA(kc, bpre[kc])
+    } else if (is_s) {
+        for (int kc = 1; kc < P1; ++kc) {
+            const f4 ub = U[kc * kWave + lane];
+            TGM_FOLD_MMA(kc, ub)
+        }
+    }
+    // the V weights of chunk P1 (the packed weights carry two zero chunks past
+    // the end), the edge-feature rows to columns [D_t, D_t + D_e) and the s'_v
+    // rows, then the output projection's weights (unconditional: the packed
+    // weights hold kAttMaxOC >= kAttFoldOC chunks, zero past OC; waves beyond
+    // ONB load the last block and compute nothing)
+    const f4 *pk = pv + P1 * vstep;
+    f4 x = pk[0];
+    if (vec_e) {
+        xf.store(A, SA, D_t, lr, eoffv, D_e, lane);
+    } else if (D_e > 0) {   // unaligned edge features: plain copies
+        for (int i = 0; i < RPW; ++i)
+            for (int k = lane; k < D_e; k += kWave)
+                A[lr[i] * SA + D_t + k] = eoff[i] >= 0 ? g.efeat[eoff[i] + k] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const int i = tid + u * blockDim.x;
+        if (i < nv4) {
+            const int r = i / M4c, c = i - r * M4c;
+            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
+                s_voff[r] >= 0 ? vreg[u] : f4{0, 0, 0, 0};
+        }
+    }
+    f4 ob[kAttFoldOC];
+    const int ocb = wave;
+    const float bo = g.b_o[min(ocb * 16 + (lane & 15), M - 1)];
+    {
+        const f4 *ob0 = g.out_b + (int64_t)min(ocb, g.ONB - 1) * kWave + lane;
+#pragma unroll
+        for (int kc = 0; kc < kAttFoldOC; ++kc)
+            ob[kc] = ob0[(int64_t)kc * g.ONB * kWave];
+    }
+    issue_fence();
+    __syncthreads();
+    if (is_v) {
+        // two register sets of weights alternate (chunk kc + 1 loads while kc
+        // multiplies)
+        int kc = P1;
+        for (; kc + 1 < KFC; kc += 2) {
+            const f4 y = pk[vstep];
+            issue_fence();
+            TGM_FOLD_MMA(kc, x)
+            pk += 2 * vstep;
+            x = pk[0];
+            issue_fence();
+            TGM_FOLD_MMA(kc + 1, y)
+        }
+        if (kc < KFC)
+            TGM_FOLD_MMA(kc, x)
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+            acc[rb] += seed[rb];
+    } else if (is_s) {
+#pragma unroll 2
+        for (int kc = P1; kc < KFC; ++kc) {
+            const f4 ub = U[kc * kWave + lane];
+            TGM_FOLD_MMA(kc, ub)
+        }
+    }
+#undef TGM_FOLD_MMA
+    // s'_v vectors past the first two per thread (none of this touches the
+    // slot rows)
+    if (v4) {
+        for (int i = tid + 2 * blockDim.x; i < nv4; i += blockDim.x) {
+            const int r = i / M4c, c = i - r * M4c;
+            *reinterpret_cast<f4 *>(AO + r * SAO + M + 4 * c) =
+                s_voff[r] >= 0 ? *reinterpret_cast<const f4 *>(g.mem_new + s_voff[r] + 4 * c)
+                               : f4{0, 0, 0, 0};
+        }
+    } else {
+        for (int i = tid; i < ORB * 16 * M; i += blockDim.x) {
+            const int r = i / M, k = i - r * M;
+            AO[r * SAO + M + k] = s_voff[r] >= 0 ? g.mem_new[s_voff[r] + k] : 0.f;
+        }
+    }
+    __syncthreads();   // every read of the slot rows is done
+
+    // V over the slot rows; the score wave keeps score (s, eta) of slot s's own
+    // root r(s) = s / nb, held by the lane of column n = r(s) * H + eta
+    float *Vs = A;
+    const float scale = 1.0f / sqrtf((float)d_h);
+    if (is_v) {
+        const int col = wave * 16 + (lane & 15);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                Vs[(rb * 16 + 4 * (lane >> 4) + v) * SV + col] = acc[rb][v];
+    } else if (is_s) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int s = rb * 16 + 4 * (lane >> 4) + v;
+                if (s / nb == cr && cr < nroots)
+                    S[s * H + ceta] = acc[rb][v] * scale;
+            }
+    }
+    __syncthreads();
+
+    // 4. softmax and the weighted sum of V: two 16-lane rows per (root, head),
+    // h = bit 4 of the lane; lane j holds slot j's score, the reductions stay
+    // inside the row (DPP); the row with h = 0 writes the 16 weights (zero past
+    // c) and both rows read them back (same wave: LDS is in order) and share
+    // the head's d_h outputs
+    {
+        const int nw = blockDim.x >> 6;
+        const int j = lane & 15, h = (lane >> 4) & 1;
+        const int npair = nroots * H;
+        for (int pr = wave * 2 + (lane >> 5); pr < npair; pr += nw * 2) {
+            const int r = pr / H, eta = pr - r * H;
+            const int c = s_cnt[r];
+            const float sc = j < c ? S[(r * nb + min(j, nb - 1)) * H + eta] : -INFINITY;
+            const float mx = row16_max(sc);
+            const float e = j < c ? expf(sc - mx) : 0.f;
+            const float den = row16_sum(e);
+            float *al = Wt + pr * 16;
+            if (h == 0)
+                al[j] = j < c ? e / den : 0.f;
+            float alv[16];
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj)
+                alv[jj] = al[jj];
+            const float *vr = Vs + r * nb * SV + eta * d_h;
+            float *ar = AO + r * SAO + eta * d_h;
+            for (int k = j + 16 * h; k < d_h; k += 32) {
+                float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+                for (int jj = 0; jj < 16; jj += 2) {
+                    a0 += alv[jj] * vr[min(jj, nb - 1) * SV + k];
+                    a1 += alv[jj + 1] * vr[min(jj + 1, nb - 1) * SV + k];
+                }
+                ar[k] = a0 + a1;   // 0 when the root has no neighbours
+            }
+        }
+    }
+    __syncthreads();
+
+    // 5. h = ReLU(W_o [a || s'_v] + b_o): the row block's fragments first (chunks
+    // past OC re-read the last one against zero weights), then four accumulators
+    if (ocb < g.ONB) {
+        const float *orow = AO + (lane & 15) * SAO + 4 * (lane >> 4);
+        const int col = ocb * 16 + (lane & 15);
+        const int OC = g.OC;
+        for (int orb = 0; orb < ORB; ++orb) {
+            f4 af[kAttFoldOC];
+#pragma unroll
+            for (int kc = 0; kc < kAttFoldOC; ++kc)
+                af[kc] = *reinterpret_cast<const f4 *>(orow + orb * 16 * SAO + min(kc, OC - 1) * 16);
+            f4 ac[4] = {{0, 0, 0, 0}, {0, 0, 0, 0}, {0, 0, 0, 0}, {0, 0, 0, 0}};
+#pragma unroll
+            for (int kc = 0; kc < kAttFoldOC; ++kc)
+                if (kc < OC)
+                    ac[kc & 3] = mfma_k16(af[kc], ob[kc], ac[kc & 3]);
+            if (col < M) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int r = orb * 16 + 4 * (lane >> 4) + v;
+                    if (r < nroots)
+                        g.h[(int64_t)(r0 + r) * M + col] =
+                            fmaxf((ac[0][v] + ac[1][v]) + (ac[2][v] + ac[3][v]) + bo, 0.f);
+                }
+            }
+        }
+    }
+}
+
+template <int RB>
+__global__ __launch_bounds__(512) void k_attn_fold(AttnArgs g)
+{
+    extern __shared__ float lds[];
+    attn_fold_block<RB>(g, lds, blockIdx.x);
+}
+
+template <int RB>
+__global__ __launch_bounds__(512) void k_attn_fold_gather(AttnArgs g, int n_attn, GatherPlan gp)
+{
+    extern __shared__ float lds[];
+    if ((int)blockIdx.x < n_attn) {
+        attn_fold_block<RB>(g, lds, blockIdx.x);
+        return;
+    }
+    const int waves = blockDim.x >> 6;
+    const int nn = min(*gp.n_nodes, gp.cap);
+    const int stride = ((int)gridDim.x - n_attn) * waves;
+    for (int p = ((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6); p < nn; p += stride)
+        gather_row(gp, p, threadIdx.x & 63);
+}
+
 // q bias folded at creation: c_q = W_q^t phi(0) + b_q with phi(0)_d = cos(beta_d).
 __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, const float *b_q,
                               const double *__restrict__ beta, float *c_q)   // may alias b_q
@@ -1039,13 +1645,23 @@ __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, con
     c_q[k] = (float)acc;
 }
 
-bool attn_lds_opt_in(int bytes)
+bool attn_lds_opt_in(int bytes, int fold_bytes)
 {
     const void *fn[] = {(const void *)k_attn<3>, (const void *)k_attn<4>, (const void *)k_attn<5>,
                         (const void *)k_attn_gather<3>, (const void *)k_attn_gather<4>,
                         (const void *)k_attn_gather<5>};
     for (const void *f : fn)
         if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) !=
+            hipSuccess)
+            return false;
+    if (fold_bytes <= 0)
+        return true;
+    const void *ff[] = {(const void *)k_attn_fold<3>, (const void *)k_attn_fold<4>,
+                        (const void *)k_attn_fold<5>, (const void *)k_attn_fold_gather<3>,
+                        (const void *)k_attn_fold_gather<4>,
+                        (const void *)k_attn_fold_gather<5>};
+    for (const void *f : ff)
+        if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, fold_bytes) !=
             hipSuccess)
             return false;
     return true;
@@ -1082,8 +1698,37 @@ size_t attn_lds(const tgm_model *m)
     const int ORB = (RT + 15) / 16;
     const size_t before_s = (size_t)RA * (SA > SKV ? SA : SKV) + (size_t)RT * m->M +
                             (size_t)ORB * 16 * (m->OC * 16 + 4);
-    const size_t om = (before_s + (size_t)RA * m->H + 1) & ~(size_t)1;   // as in k_attn
+    const size_t om =
+        (before_s + (size_t)m->H * std::max(RA, 16 * RT) + 1) & ~(size_t)1;   // as in k_attn
     return sizeof(float) * om + 2 * sizeof(double) * m->D_t;
+}
+
+// LDS of k_attn_fold (the layout in attn_fold_block)
+size_t attn_fold_lds(const tgm_model *m)
+{
+    int RBa;
+    const int RT = attn_roots(m, &RBa);
+    const size_t RA = (size_t)RBa * 16, SA = (size_t)m->KFC * 16 + 4;
+    const size_t ORB = (size_t)(RT + 15) / 16, SAO = (size_t)m->OC * 16 + 4;
+    const size_t fl = RA * SA + (size_t)m->KFC * kWave * 4 + ORB * 16 * SAO + RA * m->H +
+                      (size_t)RT * m->H * 16;
+    return sizeof(float) * ((fl + 1) & ~(size_t)1) + 2 * sizeof(double) * m->D_t;
+}
+
+// Shapes the folded attention handles: rows of 16 lanes hold a root's slots,
+// one 16-column score block (RT * H <= 16), V blocks and the score wave within
+// kMaxWaves, the U tiles within kAttUT per U wave, V within the slot-row region
+bool attn_fold_fits(const tgm_model *m)
+{
+    int RBa;
+    const int RT = attn_roots(m, &RBa);
+    const int DC = (int)cdiv(m->M, 16);
+    int nu = 0;
+    for (int w = 0; w < kMaxWaves; ++w)
+        nu += (w & 3) != (DC & 3);
+    return m->nb <= 16 && m->M % 4 == 0 && DC <= kAttDC && DC + 1 <= kMaxWaves &&
+           RT * m->H <= 16 && m->KFC <= kAttUT * nu && DC <= m->KFC &&
+           attn_fold_lds(m) <= 160 * 1024;
 }
 
 }  // namespace
@@ -1102,6 +1747,8 @@ extern "C" tgm_status_t tgm_model_destroy(tgm_model_t m)
     hipFree(m->proj_b);
     hipFree(m->P);
     hipFree(m->kv_b);
+    hipFree(m->v_b);
+    hipFree(m->uk_a);
     hipFree(m->pbias);
     hipFree(m->out_b);
     hipFree(m->b_o);
@@ -1141,6 +1788,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     m->KVNB = (int)cdiv(2 * M, 16);
     m->OC = (int)cdiv(2 * M, 16);
     m->ONB = (int)cdiv(M, 16);
+    m->VNB = m->DC = (int)cdiv(M, 16);
+    m->fold = attn_fold_fits(m);
 
     // GRU operands
     const int D_x = m->D_x, MP = m->MB * 16;
@@ -1180,6 +1829,17 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             wkv[(size_t)(M + n) * KF + k] = w->W_v[(size_t)n * Dkv + src];
         }
     auto kvb = pack_b(wkv.data(), 2 * M, KF, 0, KF, m->KFC, m->KVNB);
+    // folded attention: the V rows alone, and W_k^t [KF x M] as A fragments
+    std::vector<float> vb, uka;
+    if (m->fold) {
+        vb = pack_b(wkv.data() + (size_t)M * (KF > 0 ? KF : 1), M, KF, 0, KF, m->KFC, m->VNB);
+        vb.resize((size_t)std::max(m->KFC + 2, kAttPre) * m->VNB * kWave * 4, 0.f);
+        std::vector<float> wkt((size_t)(KF > 0 ? KF : 1) * M, 0.f);
+        for (int d = 0; d < M; ++d)
+            for (int k = 0; k < KF; ++k)
+                wkt[(size_t)k * M + d] = wkv[(size_t)d * KF + k];
+        uka = pack_b(wkt.data(), KF, M, 0, M, m->DC, m->KFC);
+    }
     auto ob = pack_b(w->W_o, M, 2 * M, 0, 2 * M, m->OC, m->ONB);
     // two zero k-chunks past the end of every packed operand: the kernels
     // load chunks kc + 1 and kc + 2 while multiplying chunk kc
@@ -1188,7 +1848,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     pb.resize(pb.size() + 2 * (size_t)m->PNB * kWave * 4, 0.f);
     // (and at least kAttPre chunks: k_attn preloads that many)
     kvb.resize((size_t)std::max(m->KFC + 2, kAttPre) * m->KVNB * kWave * 4, 0.f);
-    ob.resize(ob.size() + 2 * (size_t)m->ONB * kWave * 4, 0.f);
+    // (k_attn loads kAttMaxOC chunks)
+    ob.resize((size_t)std::max(m->OC + 2, kAttMaxOC) * m->ONB * kWave * 4, 0.f);
 
     float *wq_dev = nullptr;
     tgm_status_t st = TGM_OK;
@@ -1203,6 +1864,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             !alloc((void **)&m->proj_b, pb.size() * 4) ||
             !alloc((void **)&m->P, sizeof(float) * (size_t)d->max_nodes * m->PNB * 16) ||
             !alloc((void **)&m->kv_b, kvb.size() * 4) ||
+            (m->fold && (!alloc((void **)&m->v_b, vb.size() * 4) ||
+                         !alloc((void **)&m->uk_a, uka.size() * 4))) ||
             !alloc((void **)&m->pbias, sizeof(float) * m->PNB * 16) ||
             !alloc((void **)&m->out_b, ob.size() * 4) || !alloc((void **)&m->b_o, 4 * M) ||
             !alloc((void **)&wq_dev, sizeof(float) * (size_t)M * Dq)) {
@@ -1218,6 +1881,10 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
         }
         if ((st = upload(m->proj_b, pb.data(), pb.size() * 4)) != TGM_OK) break;
         if ((st = upload(m->kv_b, kvb.data(), kvb.size() * 4)) != TGM_OK) break;
+        if (m->fold) {
+            if ((st = upload(m->v_b, vb.data(), vb.size() * 4)) != TGM_OK) break;
+            if ((st = upload(m->uk_a, uka.data(), uka.size() * 4)) != TGM_OK) break;
+        }
         {   // b_q (folded into c_q in place below), b_k, b_v, zero padding
             std::vector<float> pbias((size_t)m->PNB * 16, 0.f);
             std::copy(w->b_q, w->b_q + M, pbias.begin());
@@ -1240,7 +1907,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             hipFuncSetAttribute((const void *)k_node_proj,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)proj_lds(m)) != hipSuccess ||
-            !attn_lds_opt_in((int)attn_lds(m))) {
+            !attn_lds_opt_in((int)attn_lds(m), m->fold ? (int)attn_fold_lds(m) : 0)) {
             st = TGM_EINVAL;   // dimensions beyond the LDS of one workgroup
             break;
         }
@@ -1388,6 +2055,7 @@ tgm_status_t embed_plan(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
     a.efeat = g->efeat; a.omega = m->omega; a.beta = m->beta;
     a.kv_b = m->kv_b; a.KFC = m->KFC; a.KVNB = m->KVNB;
     a.pbias = m->pbias;
+    a.v_b = m->v_b; a.uk_a = m->uk_a; a.VNB = m->VNB; a.DC = m->DC;
     a.out_b = m->out_b; a.OC = m->OC; a.ONB = m->ONB; a.b_o = m->b_o;
     a.mem_new = mem_new; a.h = h;
     return a.RBa >= 3 && a.RBa <= 5 ? TGM_OK : TGM_EINVAL;
@@ -1400,7 +2068,7 @@ tgm_status_t launch_attn(const tgm_model *m, const AttnArgs &a, const GatherPlan
 {
     const int n_attn = (int)cdiv(a.R, a.RT);
     const dim3 block(64 * kMaxWaves);
-    const size_t lds = attn_lds(m);
+    const size_t lds = m->fold ? attn_fold_lds(m) : attn_lds(m);
     // the gather rides along only when the attention leaves CUs free (its
     // blocks are dispatched after the attention's and hold one CU each: they
     // carry the attention's LDS size); otherwise it is its own launch
@@ -1411,6 +2079,14 @@ tgm_status_t launch_attn(const tgm_model *m, const AttnArgs &a, const GatherPlan
     if (next && next->cap > 0) {
         const int n_gather = kCUs - n_attn;
         const dim3 grid(n_attn + n_gather);
+        if (m->fold) {
+            switch (a.RBa) {
+            case 3: TGM_LAUNCH(k_attn_fold_gather<3>, grid, block, lds, s, a, n_attn, *next); break;
+            case 4: TGM_LAUNCH(k_attn_fold_gather<4>, grid, block, lds, s, a, n_attn, *next); break;
+            default: TGM_LAUNCH(k_attn_fold_gather<5>, grid, block, lds, s, a, n_attn, *next); break;
+            }
+            return TGM_OK;
+        }
         switch (a.RBa) {
         case 3: TGM_LAUNCH(k_attn_gather<3>, grid, block, lds, s, a, n_attn, *next); break;
         case 4: TGM_LAUNCH(k_attn_gather<4>, grid, block, lds, s, a, n_attn, *next); break;
@@ -1419,6 +2095,14 @@ tgm_status_t launch_attn(const tgm_model *m, const AttnArgs &a, const GatherPlan
         return TGM_OK;
     }
     const dim3 grid(n_attn);
+    if (m->fold) {
+        switch (a.RBa) {
+        case 3: TGM_LAUNCH(k_attn_fold<3>, grid, block, lds, s, a); break;
+        case 4: TGM_LAUNCH(k_attn_fold<4>, grid, block, lds, s, a); break;
+        default: TGM_LAUNCH(k_attn_fold<5>, grid, block, lds, s, a); break;
+        }
+        return TGM_OK;
+    }
     switch (a.RBa) {
     case 3: TGM_LAUNCH(k_attn<3>, grid, block, lds, s, a); break;
     case 4: TGM_LAUNCH(k_attn<4>, grid, block, lds, s, a); break;
