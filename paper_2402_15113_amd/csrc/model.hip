@@ -1207,17 +1207,19 @@ __device__ __forceinline__ void attn_fold_block(const AttnArgs &g, float *lds, i
     issue_fence();
 
     // 1. metadata of the roots and of the slots and the time-encoding constants
-    // in one round of loads (branch-free: indices clamped, results masked; the
-    // launch has at least ORB * 16 and RA threads), and the zero parts of the
-    // output projection's input: columns [0, M) of rows without a root, the
-    // padding [2M, ..)
-    {
-        const int rr = min(tid, nroots - 1);
-        const int sr = min(tid, RA - 1);
+    // in one round of loads, by the two waves on the score wave's SIMD (the U
+    // waves' weight loads stay in flight meanwhile; branch-free: indices
+    // clamped, results masked; RA and ORB * 16 are at most 128), and the zero
+    // parts of the output projection's input: columns [0, M) of rows without a
+    // root, the padding [2M, ..)
+    if (ui < 0) {
+        const int mt = (wave > 3 ? 64 : 0) + lane;   // 0 .. 127
+        const int rr = min(mt, nroots - 1);
+        const int sr = min(mt, RA - 1);
         const int r = sr / nb, j = sr - r * nb;
         const int rc = min(r, nroots - 1);
         const int64_t sl = (int64_t)(r0 + rc) * nb + j;
-        const int dd = min(tid, max(D_t - 1, 0));
+        const int dd = min(mt, max(D_t - 1, 0));
         const int pv_ = g.root_pos[r0 + rr];
         const int c_root = g.cnt[r0 + rr];
         const int c_slot = g.cnt[r0 + rc];
@@ -1226,27 +1228,29 @@ __device__ __forceinline__ void attn_fold_block(const AttnArgs &g, float *lds, i
         const double t_root = g.root_ts[r0 + rc];
         const double t_slot = g.nts[sl];
         const double om = g.omega[dd], be = g.beta[dd];
-        if (tid < ORB * 16) {
-            const bool ok = tid < nroots && pv_ >= 0 && pv_ < n;
-            s_qoff[tid] = ok ? (int64_t)pv_ * g.ldP : -1;
-            s_voff[tid] = ok ? (int64_t)pv_ * M : -1;
-            s_cnt[tid] = tid < nroots ? c_root : 0;
+        if (mt < ORB * 16) {
+            const bool ok = mt < nroots && pv_ >= 0 && pv_ < n;
+            s_qoff[mt] = ok ? (int64_t)pv_ * g.ldP : -1;
+            s_voff[mt] = ok ? (int64_t)pv_ * M : -1;
+            s_cnt[mt] = mt < nroots ? c_root : 0;
         }
-        if (tid < RA) {
+        if (mt < RA) {
             const bool ok = r < nroots && j < c_slot;
             s_ok[sr] = ok;
             s_dt[sr] = r < nroots ? t_root - t_slot : 0.0;
             s_eoff[sr] = (ok && D_e > 0 && e >= 0 && e < g.E) ? e * D_e : -1;
             s_np[sr] = (ok && q >= 0 && q < n) ? q : -1;
         }
-        if (tid < D_t) {
-            s_om[tid] = om;
-            s_be[tid] = be;
+        if (mt < D_t) {
+            s_om[mt] = om;
+            s_be[mt] = be;
         }
-        for (int d = tid + blockDim.x; d < D_t; d += blockDim.x) {
+        for (int d = mt + 128; d < D_t; d += 128) {
             s_om[d] = g.omega[d];
             s_be[d] = g.beta[d];
         }
+    }
+    {
         const int w2 = g.OC * 16 - M;
         for (int idx = tid; idx < ORB * 16 * w2; idx += blockDim.x) {
             const int rw = idx / w2, c = idx - rw * w2;
@@ -1272,7 +1276,7 @@ __device__ __forceinline__ void attn_fold_block(const AttnArgs &g, float *lds, i
     }
     issue_fence();
     // the score wave's seed part: K = M over the neighbours' key rows of P (or
-    // b_k for a slot without one), A fragments double-buffered per row block
+    // b_k for a slot without one)
     f4 acc[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
@@ -1308,59 +1312,11 @@ __device__ __forceinline__ void attn_fold_block(const AttnArgs &g, float *lds, i
     const int64_t vstep = (int64_t)VNB * kWave;
     const f4 *pv = g.v_b + (int64_t)(is_v ? wave : 0) * kWave + lane;
     f4 bpre[kAttPre];
-    if (is_s) {
-        auto seed_row = [&](int rb, f4 (&a)[kAttDC]) {
-            const int np = s_np[rb * 16 + (lane & 15)];
-            const float *row = (np >= 0 ? g.P + (int64_t)np * g.ldP : g.pbias) + M;
-#pragma unroll
-            for (int dc = 0; dc < kAttDC; ++dc)
-                a[dc] = *reinterpret_cast<const f4 *>(row + min(16 * dc + 4 * (lane >> 4), M - 4));
-        };
-        f4 sa[2][kAttDC];
-        seed_row(0, sa[0]);
-        mask_q();
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-            if (rb + 1 < RB)
-                seed_row(rb + 1, sa[(rb + 1) & 1]);
-            issue_fence();
-#pragma unroll
-            for (int dc = 0; dc < kAttDC; ++dc)   // bq is zero past M
-                acc[rb] = mfma_k16(sa[rb & 1][dc], bq[dc], acc[rb]);
-        }
-    } else if (ui >= 0) {
-        mask_q();
-        {   // U tiles kb = ui + NU t: U[16 kb .. +16][n] -> LDS
-            f4 au[kAttUT];
-#pragma unroll
-            for (int t = 0; t < kAttUT; ++t)
-                au[t] = f4{0, 0, 0, 0};
-#pragma unroll
-            for (int dc = 0; dc < kAttDC; ++dc)   // bq is zero past M
-#pragma unroll
-                for (int t = 0; t < kAttUT; ++t)
-                    au[t] = mfma_k16(ua[t][dc], bq[dc], au[t]);
-#pragma unroll
-            for (int t = 0; t < kAttUT; ++t) {
-                const int kb = ui + NU * t;
-                if (kb < KFC)
-                    U[kb * kWave + lane] = au[t];
-            }
-        }
-    }
-    // then the loads consumed in step 3 (after the fragments above, whose waits
-    // they would otherwise join): the V weights of the chunks made of time
-    // codes only, and the edge-feature rows
-    if (is_v) {
-#pragma unroll
-        for (int kc = 0; kc < kAttPre; ++kc)   // chunks past P1 are loaded and unused
-            bpre[kc] = pv[kc * vstep];
-    }
-    xf.load(vec_e ? g.efeat : g.P, eoffv, D_e, lane);
-    issue_fence();
-    // time codes phi(t_root - t_slot) in columns [0, D_t) (the RPW rows of a
-    // column are independent chains) and the zero padding past D_t + D_e
-    {
+    // the time codes phi(t_root - t_slot) in columns [0, D_t), computed while
+    // the P rows are in flight (the RPW rows of a column are independent
+    // chains), and the zero padding past D_t + D_e; inlined into each role's
+    // branch below, so that role-specific registers never share live ranges
+    auto time_codes = [&]() {
         double dts[RPW];
         bool oks[RPW];
 #pragma unroll
@@ -1374,11 +1330,63 @@ __device__ __forceinline__ void attn_fold_block(const AttnArgs &g, float *lds, i
             for (int i = 0; i < RPW; ++i)
                 A[lr[i] * SA + d] = oks[i] ? time_enc(om, be, dts[i]) : 0.f;
         }
-    }
-    for (int k = D_t + D_e + lane; k < KF; k += kWave)
+        for (int k = D_t + D_e + lane; k < KF; k += kWave)
 #pragma unroll
-        for (int i = 0; i < RPW; ++i)
-            A[lr[i] * SA + k] = 0.f;
+            for (int i = 0; i < RPW; ++i)
+                A[lr[i] * SA + k] = 0.f;
+    };
+    if (is_s) {
+        // the neighbours' key rows: every row's loads in flight together
+        f4 sa[RB][kAttDC];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            const int np = s_np[rb * 16 + (lane & 15)];
+            const float *row = (np >= 0 ? g.P + (int64_t)np * g.ldP : g.pbias) + M;
+#pragma unroll
+            for (int dc = 0; dc < kAttDC; ++dc)
+                sa[rb][dc] =
+                    *reinterpret_cast<const f4 *>(row + min(16 * dc + 4 * (lane >> 4), M - 4));
+        }
+        issue_fence();
+        time_codes();
+        mask_q();
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int dc = 0; dc < kAttDC; ++dc)   // bq is zero past M
+                acc[rb] = mfma_k16(sa[rb][dc], bq[dc], acc[rb]);
+    } else if (ui >= 0) {
+        time_codes();
+        mask_q();
+        // U tiles kb = ui + NU t: U[16 kb .. +16][n] -> LDS
+        f4 au[kAttUT];
+#pragma unroll
+        for (int t = 0; t < kAttUT; ++t)
+            au[t] = f4{0, 0, 0, 0};
+#pragma unroll
+        for (int dc = 0; dc < kAttDC; ++dc)   // bq is zero past M
+#pragma unroll
+            for (int t = 0; t < kAttUT; ++t)
+                au[t] = mfma_k16(ua[t][dc], bq[dc], au[t]);
+#pragma unroll
+        for (int t = 0; t < kAttUT; ++t) {
+            const int kb = ui + NU * t;
+            if (kb < KFC)
+                U[kb * kWave + lane] = au[t];
+        }
+    } else {
+        time_codes();
+    }
+    // then the loads consumed in step 3 (after the fragments above, whose waits
+    // they would otherwise join): the V weights of the chunks made of time
+    // codes only, and the edge-feature rows
+    if (is_v) {
+#pragma unroll
+        for (int kc = 0; kc < kAttPre; ++kc)   // chunks past P1 are loaded and unused
+            bpre[kc] = pv[kc * vstep];
+    }
+    xf.load(vec_e ? g.efeat : g.P, eoffv, D_e, lane);
+    issue_fence();
     __syncthreads();
 
     // 3. the per-slot GEMM over [phi || efeat]: the time-code chunks first (V
