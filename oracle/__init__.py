@@ -58,7 +58,9 @@ class _StepOut(C.Structure):
                 ("nts", _f64p), ("cnt", _i32p), ("U", _i32p), ("root_pos", _i32p),
                 ("nbr_pos", _i32p), ("f_mem", _f64p), ("f_mem_ts", _f64p), ("f_mail", _f64p),
                 ("f_mail_ts", _f64p), ("f_ver", _i32p), ("s_new", _f64p),
-                ("new_mem_ts", _f64p), ("h", _f64p), ("winner", _i64p)]
+                ("new_mem_ts", _f64p), ("h", _f64p), ("winner", _i64p),
+                ("m_mem", _f64p), ("m_stale", _i32p), ("m_omega", _i32p), ("m_gamma", C.c_double),
+                ("m_n_stale", C.c_int32), ("m_pad", C.c_int32)]
 
 
 def lib():
@@ -85,6 +87,10 @@ def lib():
         L.orc_next_iter.restype = C.c_int64
         L.orc_step.argtypes = [C.c_void_p, C.POINTER(_StepOut)]
         L.orc_step.restype = C.c_int
+        L.orc_set_mitigation.argtypes = [C.c_void_p, C.c_int, C.c_double, C.c_double, C.c_int]
+        L.orc_set_mitigation.restype = C.c_int
+        L.orc_quantile_nearest_rank.argtypes = [C.c_int, _f64p, C.c_double]
+        L.orc_quantile_nearest_rank.restype = C.c_double
         _lib = L
     return _lib
 
@@ -160,6 +166,13 @@ def sample(N, src, dst, t, root, root_ts, nb):
     return nbr, eid, nts, cnt
 
 
+def quantile_nearest_rank(x, p) -> float:
+    """The ceil(p n)-th smallest of the n values x (the staleness threshold of
+    the mitigation, Sec. 4.3)."""
+    x = _f64(x)
+    return float(lib().orc_quantile_nearest_rank(len(x), _p(x, _f64p), float(p)))
+
+
 # ---------------------------------------------------------------------------
 # Stateful driver
 # ---------------------------------------------------------------------------
@@ -188,13 +201,22 @@ class StepResult:
     new_mem_ts: np.ndarray
     h: np.ndarray
     winner: np.ndarray
+    # staleness mitigation (None when off): mitigated fetched memories, stale
+    # positions in U, their Omega as positions [n_stale x K] (-1 padded), gamma
+    m_mem: np.ndarray | None = None
+    m_stale: np.ndarray | None = None
+    m_omega: np.ndarray | None = None
+    m_gamma: float | None = None
 
 
 class Oracle:
     """Runs the stage iteration by iteration on a workload (``workloads.Workload``)."""
 
-    def __init__(self, wl, w, s: int | None = None):
+    def __init__(self, wl, w, s: int | None = None, mitigation: dict | None = None):
+        """``mitigation=dict(p=.., lam=.., K=..)`` enables the MSPipe-S step
+        (Sec. 4.3) between the fetch and the memory update."""
         self.wl = wl
+        self.mitigation = mitigation
         self.s = wl.s if s is None else s
         self.M, self.D_m, self.N, self.nb, self.B = wl.M, wl.D_m, wl.N, wl.nb, wl.B
         self._keep = []
@@ -223,6 +245,11 @@ class Oracle:
         if not h:
             raise ValueError("oracle: invalid description")
         self._h = h
+        if mitigation is not None:
+            rc = lib().orc_set_mitigation(h, 1, float(mitigation["p"]), float(mitigation["lam"]),
+                                          int(mitigation["K"]))
+            if rc != 0:
+                raise ValueError("oracle: invalid mitigation parameters")
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -248,6 +275,11 @@ class Oracle:
         if want == "all":
             arrs.update(f_mem=np.empty(N * M), f_mail=np.empty(N * D_m + 1),
                         s_new=np.empty(N * M), h=np.empty(R * M))
+        mit = self.mitigation
+        if mit is not None:
+            K = int(mit["K"])
+            arrs.update(m_mem=np.empty(N * M), m_stale=np.empty(N, np.int32),
+                        m_omega=np.empty(N * K, np.int32))
         for k, fld in _StepOut._fields_:
             if k in arrs:
                 setattr(o, k, _p(arrs[k], fld))
@@ -266,7 +298,11 @@ class Oracle:
             f_mem=g("f_mem", nU * M, (nU, M)), f_mem_ts=g("f_mem_ts", nU),
             f_mail=g("f_mail", nU * D_m, (nU, D_m)), f_mail_ts=g("f_mail_ts", nU),
             f_ver=g("f_ver", nU), s_new=g("s_new", nU * M, (nU, M)),
-            new_mem_ts=g("new_mem_ts", nU), h=g("h", R * M, (R, M)), winner=g("winner", nU))
+            new_mem_ts=g("new_mem_ts", nU), h=g("h", R * M, (R, M)), winner=g("winner", nU),
+            m_mem=g("m_mem", nU * M, (nU, M)), m_stale=g("m_stale", o.m_n_stale),
+            m_omega=(arrs["m_omega"][:o.m_n_stale * int(mit["K"])].reshape(-1, int(mit["K"]))
+                     if mit is not None else None),
+            m_gamma=o.m_gamma if mit is not None else None)
 
     def flush(self):
         lib().orc_flush(self._h)

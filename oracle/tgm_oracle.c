@@ -18,6 +18,10 @@
  *   2. most-recent-nb temporal neighbours of each root, strictly earlier events
  *      only (Sec. 5 training settings; Appendix D.1);
  *   3. node set U = sorted unique(roots + sampled neighbours) and its state;
+ *   3b. (optional, MSPipe-S, Sec. 4.3) staleness mitigation of the fetched
+ *      memories of nodes whose last update lies further back than the
+ *      p-quantile of the batch's gaps: a blend with the mean memory of the
+ *      most similar (common neighbours) fresher nodes;
  *   4. memory update s' = GRU(mail || phi(mail_ts - mem_ts), mem) for nodes
  *      with mail (mem() of Eq. 1; Delta-t as defined under Eq. 1);
  *   5. embedding h = emb(s'_v, s'_u | u in N(v)): one layer of multi-head
@@ -316,6 +320,162 @@ static int cmp_i32(const void *a, const void *b)
 }
 
 /* ------------------------------------------------------------------------- */
+/* Similarity-based staleness mitigation (MSPipe-S, Sec. 4.3).  Readings where
+ * the text is silent:
+ *   - the gap of a fetched node u is dt_u = T - mem_ts_u, T the time of the
+ *     batch's first event (the time since u's memory was last updated);
+ *   - gamma is the nearest-rank p-quantile of {dt_u : u in U}: the
+ *     ceil(p |U|)-th smallest gap;
+ *   - stale: dt_v > gamma; active: dt_u < gamma (then also fresher than any
+ *     stale v);
+ *   - the neighbours of a node are the distinct other endpoints of its nb
+ *     most recent events before T (the sampler's temporal neighbourhood);
+ *   - Omega(v) = the K active nodes with the most common neighbours (at least
+ *     one), ties to the fresher memory, then the smaller id;
+ *   - s_hat_v = lambda s_v + (1 - lambda) mean_{u in Omega(v)} s_u over the
+ *     fetched (unmitigated) memories; v keeps s_v when Omega(v) is empty.   */
+
+static int cmp_f64(const void *a, const void *b)
+{
+    double x = *(const double *)a, y = *(const double *)b;
+    return (x > y) - (x < y);
+}
+
+/* nearest-rank p-quantile of n values (n >= 1) */
+double orc_quantile_nearest_rank(int n, const double *x, double p)
+{
+    double *s = (double *)malloc(sizeof(double) * (size_t)n);
+    memcpy(s, x, sizeof(double) * (size_t)n);
+    qsort(s, (size_t)n, sizeof(double), cmp_f64);
+    long rank = (long)ceil(p * (double)n);
+    if (rank < 1)
+        rank = 1;
+    if (rank > n)
+        rank = n;
+    const double q = s[rank - 1];
+    free(s);
+    return q;
+}
+
+/* common elements of two sorted lists of distinct ids */
+static int common_count(const int32_t *a, int na, const int32_t *b, int nb_)
+{
+    int i = 0, j = 0, c = 0;
+    while (i < na && j < nb_) {
+        if (a[i] < b[j])
+            ++i;
+        else if (a[i] > b[j])
+            ++j;
+        else {
+            ++c; ++i; ++j;
+        }
+    }
+    return c;
+}
+
+typedef struct {
+    int sim;
+    double mts;
+    int32_t id, pos;
+} orc_cand;
+
+/* more common neighbours first, then the fresher memory, then the smaller id */
+static int cmp_cand(const void *a, const void *b)
+{
+    const orc_cand *x = (const orc_cand *)a, *y = (const orc_cand *)b;
+    if (x->sim != y->sim)
+        return x->sim > y->sim ? -1 : 1;
+    if (x->mts != y->mts)
+        return x->mts > y->mts ? -1 : 1;
+    return (x->id > y->id) - (x->id < y->id);
+}
+
+/* Mitigates the fetched rows fm [nU x M] of the nodes ids [nU] (with memory
+ * times fmts) in place.  Returns gamma; writes the stale positions (ascending)
+ * and their Omega positions when the pointers are given. */
+static double mitigate(const orc_adj *g, const int32_t *src, const int32_t *dst,
+                       const double *t, int nb, double T, int nU, const int32_t *ids,
+                       double *fm, const double *fmts, int M, double p, double lambda, int K,
+                       int32_t *stale_out, int32_t *omega_out, int *n_stale_out)
+{
+    double *dt = (double *)malloc(sizeof(double) * (size_t)nU);
+    for (int k = 0; k < nU; ++k)
+        dt[k] = T - fmts[k];
+    const double gamma = orc_quantile_nearest_rank(nU, dt, p);
+    /* neighbour sets: sorted distinct ids */
+    const int nbc = nb > 0 ? nb : 1;
+    int32_t *nset = (int32_t *)malloc(sizeof(int32_t) * (size_t)nU * nbc);
+    int *ncnt = (int *)malloc(sizeof(int) * (size_t)nU);
+    #pragma omp parallel for schedule(dynamic, 64)
+    for (int k = 0; k < nU; ++k) {
+        int32_t *nbr = nset + (size_t)k * nbc;
+        int32_t *eid = (int32_t *)malloc(sizeof(int32_t) * nbc);
+        double *nts = (double *)malloc(sizeof(double) * nbc);
+        int32_t c = 0;
+        sample_root(g, src, dst, t, ids[k], T, nb, nbr, eid, nts, &c);
+        qsort(nbr, (size_t)c, sizeof(int32_t), cmp_i32);
+        int d = 0;
+        for (int j = 0; j < c; ++j)
+            if (d == 0 || nbr[j] != nbr[d - 1])
+                nbr[d++] = nbr[j];
+        ncnt[k] = d;
+        free(eid);
+        free(nts);
+    }
+    int ns = 0;
+    int32_t *stale = (int32_t *)malloc(sizeof(int32_t) * (size_t)nU);
+    for (int k = 0; k < nU; ++k)
+        if (dt[k] > gamma)
+            stale[ns++] = k;
+    double *out = (double *)malloc(sizeof(double) * ((size_t)ns * M + 1));
+    int32_t *om = (int32_t *)malloc(sizeof(int32_t) * ((size_t)ns * (K > 0 ? K : 1) + 1));
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int q = 0; q < ns; ++q) {
+        const int v = stale[q];
+        orc_cand *cand = (orc_cand *)malloc(sizeof(orc_cand) * (size_t)nU);
+        int nc = 0;
+        for (int u = 0; u < nU; ++u) {
+            if (!(dt[u] < gamma))
+                continue;
+            const int sim = common_count(nset + (size_t)v * nbc, ncnt[v],
+                                         nset + (size_t)u * nbc, ncnt[u]);
+            if (sim > 0) {
+                cand[nc].sim = sim;
+                cand[nc].mts = fmts[u];
+                cand[nc].id = ids[u];
+                cand[nc].pos = u;
+                ++nc;
+            }
+        }
+        qsort(cand, (size_t)nc, sizeof(orc_cand), cmp_cand);
+        const int m = nc < K ? nc : K;
+        for (int j = 0; j < K; ++j)
+            om[(size_t)q * K + j] = j < m ? cand[j].pos : -1;
+        for (int d = 0; d < M; ++d) {
+            double x = fm[(size_t)v * M + d];
+            if (m > 0) {
+                double acc = 0.0;
+                for (int j = 0; j < m; ++j)
+                    acc += fm[(size_t)cand[j].pos * M + d];
+                x = lambda * x + (1.0 - lambda) * (acc / m);
+            }
+            out[(size_t)q * M + d] = x;
+        }
+        free(cand);
+    }
+    /* stale rows are never sources (sources are active), so order is free */
+    for (int q = 0; q < ns; ++q)
+        memcpy(fm + (size_t)stale[q] * M, out + (size_t)q * M, sizeof(double) * M);
+    if (stale_out)
+        memcpy(stale_out, stale, sizeof(int32_t) * (size_t)ns);
+    if (omega_out)
+        memcpy(omega_out, om, sizeof(int32_t) * (size_t)ns * K);
+    *n_stale_out = ns;
+    free(dt); free(nset); free(ncnt); free(stale); free(out); free(om);
+    return gamma;
+}
+
+/* ------------------------------------------------------------------------- */
 /* The stateful driver.                                                        */
 typedef struct {
     int64_t iter;
@@ -343,6 +503,9 @@ typedef struct {
     orc_wset *q;
     int nq, capq;
     int64_t next_iter;
+    /* staleness mitigation (off unless orc_set_mitigation enables it) */
+    int mit_on, mit_K;
+    double mit_p, mit_lambda;
 } orc_ctx;
 
 typedef struct {
@@ -373,6 +536,12 @@ typedef struct {
     double *s_new, *new_mem_ts;
     double *h;
     int64_t *winner;
+    /* staleness mitigation: mitigated rows [n_U x M], stale positions
+     * [n_stale], their Omega as positions [n_stale x K] (-1 padded), gamma */
+    double *m_mem;
+    int32_t *m_stale, *m_omega;
+    double m_gamma;
+    int32_t m_n_stale, m_pad;
 } orc_step_out;
 
 static double *widen(const float *x, size_t n)
@@ -514,6 +683,20 @@ void orc_get_state(void *p, double *mem, double *mem_ts, double *mail, double *m
 
 int64_t orc_next_iter(void *p) { return ((orc_ctx *)p)->next_iter; }
 
+/* Enables (on != 0) the staleness mitigation of step 3b with quantile p,
+ * blend weight lambda and at most K similar nodes. */
+int orc_set_mitigation(void *p, int on, double pq, double lambda, int K)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (on && (K < 1 || !(pq >= 0.0 && pq <= 1.0) || !(lambda >= 0.0 && lambda <= 1.0)))
+        return ORC_EINVAL;
+    c->mit_on = on != 0;
+    c->mit_p = pq;
+    c->mit_lambda = lambda;
+    c->mit_K = K;
+    return ORC_OK;
+}
+
 /* One iteration of the stage.  Returns ORC_EEND when the stream is exhausted. */
 int orc_step(void *p, orc_step_out *o)
 {
@@ -583,6 +766,18 @@ int orc_step(void *p, orc_step_out *o)
         fmts[k] = c->mem_ts[v];
         flts[k] = c->mail_ts[v];
         fver[k] = c->ver[v];
+    }
+
+    /* 3b. staleness mitigation of the fetched memories (when enabled); the
+     * fetched rows are reported as read, the mitigated ones separately */
+    double *fm_read = NULL, gamma = 0.0;
+    int n_stale = 0;
+    if (c->mit_on && nU > 0) {
+        fm_read = (double *)malloc(sizeof(double) * (size_t)nU * M);
+        memcpy(fm_read, fm, sizeof(double) * (size_t)nU * M);
+        gamma = mitigate(&c->adj, c->src, c->dst, c->t, nb, c->t[lo], nU, ids, fm, fmts, M,
+                         c->mit_p, c->mit_lambda, c->mit_K, o ? o->m_stale : NULL,
+                         o ? o->m_omega : NULL, &n_stale);
     }
 
     /* 4. memory update of every node in U that holds mail */
@@ -701,7 +896,10 @@ int orc_step(void *p, orc_step_out *o)
         if (o->nbr_pos)
             for (size_t k = 0; k < (size_t)R * nb; ++k)
                 o->nbr_pos[k] = nbr[k] >= 0 ? pos[nbr[k]] : -1;
-        if (o->f_mem) memcpy(o->f_mem, fm, sizeof(double) * (size_t)nU * M);
+        if (o->f_mem) memcpy(o->f_mem, fm_read ? fm_read : fm, sizeof(double) * (size_t)nU * M);
+        if (o->m_mem) memcpy(o->m_mem, fm, sizeof(double) * (size_t)nU * M);
+        o->m_gamma = gamma;
+        o->m_n_stale = n_stale;
         if (o->f_mem_ts) memcpy(o->f_mem_ts, fmts, sizeof(double) * nU);
         if (o->f_mail) memcpy(o->f_mail, fl, sizeof(double) * (size_t)nU * D_m);
         if (o->f_mail_ts) memcpy(o->f_mail_ts, flts, sizeof(double) * nU);
@@ -714,6 +912,7 @@ int orc_step(void *p, orc_step_out *o)
 
     free(root); free(rts); free(nbr); free(eid); free(nts); free(cnt); free(ids); free(pos);
     free(fm); free(fmts); free(fl); free(flts); free(fver); free(sn); free(nmts); free(h);
+    free(fm_read);
     free(win);
     c->next_iter = i + 1;
     return ORC_OK;
