@@ -60,6 +60,7 @@ typedef int32_t tgm_status_t;
 typedef struct tgm_graph *tgm_graph_t;
 typedef struct tgm_state *tgm_state_t;
 typedef struct tgm_model *tgm_model_t;
+typedef struct tgm_mitigator *tgm_mitigator_t;
 
 /* Static string for a status code. */
 const char *tgm_status_str(tgm_status_t status);
@@ -290,6 +291,50 @@ tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t
                            int32_t nsb, const tgm_fetch_buffers *fb, float *mem_new,
                            double *new_mem_ts, int64_t *winner, float *h, void *stream,
                            void *prefetch_stream);
+
+/* ------------------------------------------------------------------------
+ * Similarity-based staleness mitigation (MSPipe-S, Sec. 4.3), applied to the
+ * fetched memories of a batch between tgm_fetch_memory and
+ * tgm_update_memory.  For the fetched node set (positions p < *n_nodes):
+ *   gap      dt_p = T - mem_ts[p], T = the time of event first_event (the
+ *            batch's first event), formed in fp64;
+ *   gamma    the nearest-rank p-quantile of the gaps: the ceil(p n)-th
+ *            smallest, with the rank formed as ceil(p * n) in fp64;
+ *   stale    dt > gamma; active: dt < gamma;
+ *   N(u)     the distinct other endpoints of u's nb most recent events
+ *            strictly before T;
+ *   Omega(v) the K active nodes sharing the most neighbours with v (at least
+ *            one), ties to the larger mem_ts, then the smaller node id;
+ *   mem[v] = lambda mem[v] + (1 - lambda) mean_{u in Omega(v)} mem[u] for
+ *            every stale v with Omega(v) non-empty (fp32, the sum in Omega's
+ *            order); other rows are untouched.
+ * The mitigator owns its work space: the gaps, neighbour sets, gamma, the
+ * stale positions and Omega of the last call.  Calls on one mitigator must be
+ * stream-ordered.
+ */
+/* max_nodes >= any cap passed later; 1 <= nb <= 64 (the neighbour sets' nb);
+ * 1 <= K <= 16.  Errors: TGM_EINVAL, TGM_ENOMEM. */
+tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int32_t K,
+                                  tgm_mitigator_t *out);
+tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt);
+/* nodes [cap] and n_nodes [1] as from tgm_sample_nodes; mem [cap x M] (updated
+ * in place) and mem_ts [cap] as from tgm_fetch_memory; 0 <= p <= 1,
+ * 0 <= lambda <= 1.  Errors: TGM_EINVAL (null, dims, parameters), TGM_ERANGE
+ * (first_event outside the graph), TGM_ESIZE (cap above max_nodes). */
+tgm_status_t tgm_mitigate(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
+                          const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
+                          float *mem, const double *mem_ts, int32_t M, double p, float lambda,
+                          void *stream);
+/* Device copies of the last call's results (each pointer may be NULL): gamma
+ * [1], n_stale [1], stale [max_nodes] (positions, ascending; the first
+ * *n_stale are valid), omega [max_nodes x K] (positions, -1 padded; row q
+ * belongs to stale[q]). */
+tgm_status_t tgm_mitigator_read(tgm_mitigator_t mt, double *gamma, int32_t *n_stale,
+                                int32_t *stale, int32_t *omega, void *stream);
+/* Makes tgm_stage_run mitigate every fetch with mt, p and lambda (mt NULL:
+ * off, the default).  mt must stay alive while st uses it. */
+tgm_status_t tgm_state_set_mitigation(tgm_state_t st, tgm_mitigator_t mt, double p,
+                                      float lambda);
 
 /* ------------------------------------------------------------------------
  * Per-kernel timing.  When enabled, every kernel the library launches is

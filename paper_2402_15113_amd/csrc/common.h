@@ -111,6 +111,11 @@ struct tgm_state {
     // of the update call that wrote it (tags start at 1, so zero is stale)
     uint64_t *win = nullptr;
     uint32_t win_tag = 0;             // tag of the last update call
+    // staleness mitigation applied by the pipelined executor after each fetch
+    // (tgm_state_set_mitigation; off when mit is null)
+    struct tgm_mitigator *mit = nullptr;
+    double mit_p = 1.0;
+    float mit_lambda = 1.0f;
     size_t ring_rows() const { return 2 * (size_t)max_batch; }
 };
 
@@ -233,6 +238,34 @@ __device__ __forceinline__ float row16_sum(float v)
     v += dpp_row<kDppXor2>(v);
     v += dpp_row<kDppHalfMirror>(v);
     return v + dpp_row<kDppMirror>(v);
+}
+
+// One wavefront: the adjacency list of v is sorted by (t, e); returns p, the
+// first entry with ts >= tq, so that [*base, p) are v's strictly earlier
+// events.  A 64-ary search: each round lane l probes the last entry of the
+// l-th of 64 equal segments and the ballot's popcount names the segment that
+// holds p.  An id outside [0, N) has an empty list.
+__device__ __forceinline__ int64_t recent_end(const int64_t *__restrict__ off,
+                                              const AdjRec *__restrict__ adj, int32_t v,
+                                              double tq, int32_t N, int64_t *base)
+{
+    const int lane = threadIdx.x & 63;
+    const bool ok = v >= 0 && v < N;
+    *base = ok ? off[v] : 0;
+    int64_t lo = *base, hi = ok ? off[v + 1] : 0;
+    while (hi - lo > kWave) {
+        const int64_t step = (hi - lo + kWave - 1) / kWave;
+        const int64_t probe = lo + (int64_t)(lane + 1) * step - 1;
+        const bool below = probe < hi && adj[probe].ts < tq;
+        const int c = __popcll(__ballot(below));
+        const int64_t nlo = lo + (int64_t)c * step;
+        const int64_t nhi = nlo + step < hi ? nlo + step : hi;
+        lo = nlo;
+        hi = nhi;
+    }
+    const int64_t idx = lo + lane;
+    const bool below = idx < hi && adj[idx].ts < tq;
+    return lo + __popcll(__ballot(below));
 }
 
 __device__ __forceinline__ float wave_sum(float v)
@@ -428,5 +461,11 @@ tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int
                                int32_t cap, int64_t first_event, int32_t b, int32_t nb,
                                float *mem_new, double *new_mem_ts, int64_t *winner, float *h,
                                const tgm_sample_buffers *next_sb, hipStream_t s);
+
+// tgm_mitigate on stream s (three launches; see mitigate.hip).
+tgm_status_t mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
+                             const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
+                             float *mem, const double *mem_ts, int32_t M, double p, float lambda,
+                             hipStream_t s);
 
 }  // namespace tgm

@@ -99,12 +99,9 @@ __global__ void k_batch_roots(int64_t first, int32_t b, const int32_t *__restric
 }
 
 // ------------------------------------------------------------ sampler
-// One wavefront per root.  The root's adjacency list is sorted by (t, e);
-// the wavefront finds p = the first entry with ts >= tq by a 64-ary search
-// (each round, lane l probes the last entry of the l-th of 64 equal segments,
-// and the ballot's popcount names the segment holding p), then lanes
-// j < nb read entries p-1-j: the nb most recent strictly earlier events,
-// newest first.
+// One wavefront per root: recent_end() finds the end of the root's strictly
+// earlier events, then lanes j < nb read entries p-1-j: the nb most recent
+// strictly earlier events, newest first.
 __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
                                            const AdjRec *__restrict__ adj, int r, int32_t v,
                                            double tq, int32_t N, int32_t nb,
@@ -114,24 +111,10 @@ __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
                                            int32_t epoch = 0)
 {
     const int lane = threadIdx.x & 63;
-    const bool ok = v >= 0 && v < N;   // an id out of range samples nothing
-    if (stamp && ok && lane == 0)      // node-set mark of the root (see k_ns_mark)
+    if (stamp && v >= 0 && v < N && lane == 0)   // node-set mark of the root (see k_ns_mark)
         stamp[v] = epoch;
-    const int64_t base = ok ? off[v] : 0;
-    int64_t lo = base, hi = ok ? off[v + 1] : 0;
-    while (hi - lo > kWave) {
-        const int64_t step = (hi - lo + kWave - 1) / kWave;
-        const int64_t probe = lo + (int64_t)(lane + 1) * step - 1;
-        const bool below = probe < hi && adj[probe].ts < tq;
-        const int c = __popcll(__ballot(below));
-        const int64_t nlo = lo + (int64_t)c * step;
-        const int64_t nhi = nlo + step < hi ? nlo + step : hi;
-        lo = nlo;
-        hi = nhi;
-    }
-    const int64_t idx = lo + lane;
-    const bool below = idx < hi && adj[idx].ts < tq;
-    const int64_t p = lo + __popcll(__ballot(below));
+    int64_t base;
+    const int64_t p = recent_end(off, adj, v, tq, N, &base);
     const int64_t avail = p - base;
     const int c = avail < nb ? (int)avail : nb;
     if (lane < nb) {

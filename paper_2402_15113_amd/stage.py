@@ -43,9 +43,11 @@ class _Sample:
 
 class Stage:
     def __init__(self, N, src, dst, t, neg, efeat, weights, *, M, D_t, H, nb, B, s,
-                 device="cuda", stream=None):
+                 device="cuda", stream=None, mitigation=None):
         """src, dst, t, neg: numpy or torch arrays of the event stream; efeat
-        [E x D_e] fp32 or None; weights a ``workloads.Weights``."""
+        [E x D_e] fp32 or None; weights a ``workloads.Weights``;
+        ``mitigation=dict(p=.., lam=.., K=..)`` turns on the similarity-based
+        staleness mitigation (Sec. 4.3) of every fetch."""
         dev = torch.device(device)
         self.dev = dev
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
@@ -79,6 +81,11 @@ class Stage:
         self.winner = z(self.cap, torch.int64)
         self.h = z((R, M), torch.float32)
         self.want_winner = True
+        self.mit = None
+        self.mitigation = mitigation
+        if mitigation is not None:
+            self.mit = tgm.tgm_mitigator_create(self.cap, nb, int(mitigation["K"]))
+            tgm.tgm_state_set_mitigation(self.st, self.mit, mitigation["p"], mitigation["lam"])
         self.last = None      # (iteration, batch size) of the last issued iteration
         self._set = 0         # its sample buffer set
         self._bufs = None
@@ -90,7 +97,7 @@ class Stage:
 
     def close(self):
         for fn, h in ((tgm.tgm_model_destroy, "m"), (tgm.tgm_state_destroy, "st"),
-                      (tgm.tgm_graph_destroy, "g")):
+                      (tgm.tgm_mitigator_destroy, "mit"), (tgm.tgm_graph_destroy, "g")):
             if self.__dict__.get(h) is not None:
                 fn(self.__dict__[h])
                 self.__dict__[h] = None
@@ -114,6 +121,10 @@ class Stage:
                              b.cnt, b.nodes, b.n_nodes, self.cap, b.root_pos, b.nbr_pos, stream=st)
         tgm.tgm_fetch_memory(self.st, i, b.nodes, b.n_nodes, self.cap, self.f_mem, self.f_mem_ts,
                              self.f_mail, self.f_mail_ts, self.f_ver, stream=st)
+        if self.mit is not None:
+            mit = self.mitigation
+            tgm.tgm_mitigate(self.mit, self.g, lo, b.nodes, b.n_nodes, self.cap, self.f_mem,
+                             self.f_mem_ts, self.M, mit["p"], mit["lam"], stream=st)
         tgm.tgm_update_memory(self.st, self.m, self.g, i, b.nodes, b.n_nodes, self.cap,
                               self.f_mem, self.f_mem_ts, self.f_mail, self.f_mail_ts, self.f_ver,
                               lo, n, b.root_pos[:n], b.root_pos[n:2 * n], self.mem_new,
@@ -162,6 +173,21 @@ class Stage:
                     s_new=c(self.mem_new[:n]), new_mem_ts=c(self.new_mem_ts[:n]),
                     winner=c(self.winner[:n]), h=c(self.h[:R]))
 
+    def mitigation_result(self):
+        """Host copies of the last mitigation: gamma, stale positions, Omega
+        positions [n_stale x K] (synchronises)."""
+        K = int(self.mitigation["K"])
+        dev = self.dev
+        gamma = torch.zeros(1, dtype=torch.float64, device=dev)
+        ns = torch.zeros(1, dtype=torch.int32, device=dev)
+        stale = torch.zeros(self.cap, dtype=torch.int32, device=dev)
+        omega = torch.zeros(self.cap * K, dtype=torch.int32, device=dev)
+        tgm.tgm_mitigator_read(self.mit, gamma, ns, stale, omega, stream=self.stream)
+        torch.cuda.synchronize(dev)
+        n = int(ns.item())
+        return (float(gamma.item()), stale[:n].cpu().numpy(),
+                omega[:n * K].view(n, K).cpu().numpy())
+
     def flush(self):
         tgm.tgm_state_flush(self.st, stream=self.stream)
 
@@ -186,6 +212,7 @@ class Stage:
         torch.cuda.synchronize(dev)
 
 
-def from_workload(wl, w, *, s=None, device="cuda", stream=None) -> Stage:
+def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None) -> Stage:
     return Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, wl.efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
-                 nb=wl.nb, B=wl.B, s=wl.s if s is None else s, device=device, stream=stream)
+                 nb=wl.nb, B=wl.B, s=wl.s if s is None else s, device=device, stream=stream,
+                 mitigation=mitigation)

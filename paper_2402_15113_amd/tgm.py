@@ -23,7 +23,8 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_
            "tgm_node_set", "tgm_sample_nodes", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
            "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
-           "tgm_stage_run",
+           "tgm_stage_run", "tgm_mitigator_create", "tgm_mitigator_destroy", "tgm_mitigate",
+           "tgm_mitigator_read", "tgm_state_set_mitigation",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
 
@@ -97,6 +98,11 @@ def lib():
             "tgm_embed": [V, V, I32, I32, P, P, P, P, P, P, P, P, I32, P, V],
             "tgm_stage_run": [V, V, V, I64, I64, I32, I32, I32, C.POINTER(SampleBuffers), I32,
                               C.POINTER(FetchBuffers), P, P, P, P, V, V],
+            "tgm_mitigator_create": [I32, I32, I32, C.POINTER(V)],
+            "tgm_mitigator_destroy": [V],
+            "tgm_mitigate": [V, V, I64, P, P, I32, P, P, I32, C.c_double, C.c_float, V],
+            "tgm_mitigator_read": [V, P, P, P, P, V],
+            "tgm_state_set_mitigation": [V, V, C.c_double, C.c_float],
         }
         sig["tgm_profile_enable"] = [I32]
         sig["tgm_profile_reset"] = []
@@ -258,6 +264,33 @@ def tgm_stage_run(g, st, m, i0, n, B, nb, cap, sample_bufs, fetch_bufs, mem_new,
     _check("tgm_stage_run", lib().tgm_stage_run(
         g, st, m, i0, n, B, nb, cap, sample_bufs, len(sample_bufs), C.byref(fetch_bufs),
         _p(mem_new), _p(new_mem_ts), _p(winner), _p(h), _s(stream), _s(prefetch_stream)))
+
+
+# ------------------------------------------------------------- mitigation
+def tgm_mitigator_create(max_nodes, nb, K):
+    h = V()
+    _check("tgm_mitigator_create", lib().tgm_mitigator_create(max_nodes, nb, K, C.byref(h)))
+    return h
+
+
+def tgm_mitigator_destroy(mt):
+    _check("tgm_mitigator_destroy", lib().tgm_mitigator_destroy(mt))
+
+
+def tgm_mitigate(mt, g, first_event, nodes, n_nodes, cap, mem, mem_ts, M, p, lam, stream=None):
+    _check("tgm_mitigate", lib().tgm_mitigate(mt, g, first_event, _p(nodes), _p(n_nodes), cap,
+                                              _p(mem), _p(mem_ts), M, float(p), float(lam),
+                                              _s(stream)))
+
+
+def tgm_mitigator_read(mt, gamma, n_stale, stale, omega, stream=None):
+    _check("tgm_mitigator_read", lib().tgm_mitigator_read(mt, _p(gamma), _p(n_stale), _p(stale),
+                                                          _p(omega), _s(stream)))
+
+
+def tgm_state_set_mitigation(st, mt, p=1.0, lam=1.0):
+    _check("tgm_state_set_mitigation", lib().tgm_state_set_mitigation(st, mt, float(p),
+                                                                      float(lam)))
 
 
 # ------------------------------------------------------------------ model
