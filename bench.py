@@ -117,7 +117,7 @@ def account(sched, W, K):
     return rows
 
 
-def window_setup(name, first, L, w):
+def window_setup(name, first, L, w, mitigation=None):
     """Stage for batches first .. first + L - 1 of a large stream: the graph of
     every event up to the window's end, a device feature table that holds the
     generator's rows from the oldest event the window samples onwards (zero
@@ -137,7 +137,7 @@ def window_setup(name, first, L, w):
                              t=full.t[:E_end], neg=full.neg[:E_end])
     efeat = torch.zeros((E_end, wl.D_e), dtype=torch.float32, device="cuda")
     stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
-                  nb=wl.nb, B=wl.B, s=wl.s)
+                  nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation)
     lo_row = first * wl.B
     for i in range(first, first + L):   # the oldest event any window batch samples
         a, b = wl.batch(i)
@@ -208,6 +208,11 @@ def work_model(wl, rows):
                              bytes=k["k_node_proj"]["bytes"] + k["k_stage"]["bytes"])
     k["k_attn_gather"] = dict(flops=k["k_attn"]["flops"],
                               bytes=k["k_attn"]["bytes"] + k["k_gather_state"]["bytes"])
+    # staleness mitigation: per node a gap and a neighbour set; the threshold
+    # select reads the gaps 8 times; per stale node a probe of every node's set
+    k["k_mit_prep"] = dict(flops=0, bytes=n_U * (4 + 8 + 8 + nb * 16 + nb * 4 + 4))
+    k["k_mit_select"] = dict(flops=0, bytes=n_U * 8 * 9)
+    k["k_mit_omega"] = dict(flops=0, bytes=n_U * (8 + 4 + nb * 4))
     # the attention with the query folded into the key weights computes the
     # same embedding: the same algorithmic work
     k["k_attn_fold"] = dict(k["k_attn"])
@@ -307,6 +312,9 @@ def main():
                     help="wiki (default), tiny, reddit, lastfm; gdelt runs a window of batches "
                          "starting at --first from a synthetic state")
     ap.add_argument("--first", type=int, default=20_000, help="first batch of a gdelt window")
+    ap.add_argument("--mitigate", default=None, metavar="P,LAMBDA,K",
+                    help="similarity-based staleness mitigation on every fetch (MSPipe-S, "
+                         "off by default), e.g. 0.99,0.95,10")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
@@ -336,17 +344,21 @@ def main():
     tgm.lib()
     K, W = args.steps, args.warmup
     window = args.workload == "gdelt"
+    mit = None
+    if args.mitigate:
+        pq, lam, kk = args.mitigate.split(",")
+        mit = dict(p=float(pq), lam=float(lam), K=int(kk))
     if window:
         from workloads import CONFIGS
         c = CONFIGS["gdelt"]
         w = make_weights(c["M"], c["D_e"], c["D_t"])
-        wl, stage, init = window_setup("gdelt", args.first, W + K, w)
+        wl, stage, init = window_setup("gdelt", args.first, W + K, w, mit)
         sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
         sched.restart()
     else:
         wl = make_workload(args.workload)
         w = make_weights(wl.M, wl.D_e, wl.D_t)
-        stage = from_workload(wl, w)
+        stage = from_workload(wl, w, mitigation=mit)
         sched = Schedule(stage, wl.n_iters)
     log(f"workload {wl.name}: N={wl.N} E={wl.E} B={wl.B} s={wl.s} iters={wl.n_iters}")
     stage.want_winner = False
@@ -380,6 +392,8 @@ def main():
                       "staleness": wl.s, "graph": wl.meta.get("graph", ""),
                       "pipeline": "two streams: sample + node set + fetch of batch i+1 beside "
                                   "update + embed of batch i"}}
+    if mit is not None:
+        out["config"]["mitigation"] = dict(mit, kind="MSPipe-S similarity-based, every fetch")
 
     if not args.no_profile:
         # pass 2: per-kernel durations (HIP events on the launch stream)

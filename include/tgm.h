@@ -312,8 +312,9 @@ tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t
  * stale positions and Omega of the last call.  Calls on one mitigator must be
  * stream-ordered.
  */
-/* max_nodes >= any cap passed later; 1 <= nb <= 64 (the neighbour sets' nb);
- * 1 <= K <= 16.  Errors: TGM_EINVAL, TGM_ENOMEM. */
+/* max_nodes >= any cap passed later, at most 1 << 20; 1 <= nb <= 64 (the
+ * neighbour sets' nb); 1 <= K <= 16.  Errors: TGM_EINVAL, TGM_ENOMEM,
+ * TGM_EDEVICE. */
 tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int32_t K,
                                   tgm_mitigator_t *out);
 tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt);

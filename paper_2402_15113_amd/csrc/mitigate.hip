@@ -10,13 +10,20 @@
 //             one), then the fresher memory, then the smaller id;
 //   s_v      <- lambda s_v + (1 - lambda) mean_{u in Omega(v)} s_u  (in place;
 //             a stale row is never a source: sources are active).
-// Three launches: k_mit_prep (one wavefront per node: gap and sorted distinct
-// neighbour set), k_mit_select (one workgroup: a radix select of gamma over
-// the order-preserving 64-bit keys of the gaps, then the stale positions in
-// order), k_mit_omega (one workgroup per stale node: its neighbour set in an
-// LDS hash set, every active node probed against it, a per-thread top-K, a
-// wave-merge of the sorted lists, the blend).  Integer decisions only; the
-// gaps are formed exactly as the oracle forms them (one fp64 subtraction).
+// Three launches:
+//   k_mit_prep    one wavefront per node: its gap and its sorted distinct
+//                 neighbour set (padded with INT32_MAX);
+//   k_mit_select  one workgroup: gamma by a radix select over the
+//                 order-preserving 64-bit keys of the gaps (held in
+//                 registers, eight digit passes), then the stale positions
+//                 in order;
+//   k_mit_omega   one workgroup per stale node: its neighbour set in an LDS
+//                 hash set, every active node's set probed against it (rows
+//                 read as 16-byte vectors, several nodes in flight per
+//                 thread), a per-thread top-K, a wave-merge of the sorted
+//                 lists, and the blend.
+// Integer decisions only; the gaps are formed exactly as the oracle forms them
+// (one fp64 subtraction).
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -32,14 +39,26 @@ struct tgm_mitigator {
     int32_t *n_stale = nullptr;  // [1]
     int32_t *stale = nullptr;    // [cap] stale positions, ascending
     int32_t *omega = nullptr;    // [cap x K] Omega positions, -1 padded
+    int2 *part = nullptr;        // [kMitOmegaGrid x kMitMaxK] chunk top-K lists of k_mit_omega
+    int32_t *done = nullptr;     // [cap] finished chunks per stale node
 };
 
 namespace {
 
 constexpr int kMitMaxK = 16;
-constexpr int kMitHash = 256;          // LDS hash slots (>= 4 nb)
-constexpr int kMitThreads = 256;       // k_mit_omega
-constexpr int kMitSelThreads = 1024;   // k_mit_select
+constexpr int kMitThreads = 256;           // k_mit_omega
+constexpr int kMitSelThreads = 1024;       // k_mit_select
+constexpr int kMitSelRegs = 20;            // gaps per k_mit_select thread in registers
+constexpr int kMitHashBits = 10;
+constexpr int kMitHash = 1 << kMitHashBits;   // LDS hash slots (16 per possible id)
+constexpr int kMitPerThread = 4;           // nodes a k_mit_omega thread takes per round
+constexpr int kMitChunk = 1024;             // nodes of one k_mit_omega round (256 x 4)
+constexpr int kMitMaxChunks = 64;           // chunk lists of one stale node (64 x 16 entries)
+static_assert(kMitChunk == kMitThreads * kMitPerThread, "a round is one node per thread slot");
+static_assert(kMitMaxChunks * kMitMaxK <= kMitChunk, "the chunk lists fit the round entries");
+constexpr int kMitOmegaGrid = 1024;         // k_mit_omega workgroups
+
+constexpr int kMitMaxNodes = 1 << 20;
 
 // ---------------------------------------------------------------- prep
 // One wavefront per fetched node: its gap and its sorted distinct neighbour
@@ -79,9 +98,11 @@ __global__ __launch_bounds__(256) void k_mit_prep(const int64_t *__restrict__ of
     }
     if (lane < c && !dup)
         nset[(int64_t)p * nbp + less] = w;
-    const uint64_t firsts = __ballot(lane < c && !dup);
+    const int d = __popcll(__ballot(lane < c && !dup));
+    if (lane >= d && lane < nbp)
+        nset[(int64_t)p * nbp + lane] = INT32_MAX;   // padding: never an id
     if (lane == 0) {
-        ncnt[p] = __popcll(firsts);
+        ncnt[p] = d;
         dt[p] = T - mem_ts[p];
     }
 }
@@ -99,19 +120,68 @@ __device__ __forceinline__ double key_value(uint64_t k)
     return __longlong_as_double((long long)u);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront: shifts by 1, 2, 4
+// and 8 within each row of 16 lanes, then row 0's total into row 1 and row
+// 2's into row 3 (row_bcast:15), then rows 0-1's total into rows 2 and 3
+// (row_bcast:31).  Lanes without a source add 0.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
+{
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+    return v;
+}
+
+// Adds the keys of this round (one per thread; `in` marks those that count)
+// to the histogram of the digit (k >> sh) & dmask.  The bins of the wave's
+// first two remaining lanes take one atomic each (the leading digits of gaps
+// are few); the rest one per lane.
+__device__ __forceinline__ void hist_add(uint32_t *hist, uint64_t k, bool in, int sh,
+                                         uint32_t dmask)
+{
+    const int lane = threadIdx.x & 63;
+    const int bin = (int)((k >> sh) & dmask);
+    uint64_t act = __ballot(in);
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        if (act == 0)
+            break;
+        const int lead = __builtin_ctzll(act);
+        const int first = __builtin_amdgcn_readlane(bin, lead);
+        const uint64_t same = __ballot(in && bin == first);
+        if (lane == lead)
+            atomicAdd(&hist[first], (uint32_t)__popcll(same));
+        in = in && bin != first;
+        act &= ~same;
+    }
+    if (in)
+        atomicAdd(&hist[bin], 1u);
+}
+
 // One workgroup: gamma = the rank-th smallest gap (rank = ceil(pq n) in fp64,
-// clamped to [1, n]) by an 8-pass radix select on 8-bit digits, most
-// significant first; then the positions with dt > gamma, ascending.
+// clamped to [1, n]) by a radix select over the order-preserving 64-bit keys
+// of the gaps, most significant byte first (eight passes).  The keys stay in
+// registers (kMitSelRegs per thread; read again from global memory each pass
+// when n is larger).  A pass adds the digits of the keys that match the
+// prefix found so far to a 256-bin LDS histogram; after one barrier every
+// wave reads the whole histogram (four bins a lane), scans the lane sums with
+// DPP and finds the bin that holds the rank, so no second barrier is needed.
+// Three histogram buffers rotate: the one a pass clears was last read two
+// passes before, by waves that have all passed the barrier since.  Then the
+// positions with dt > gamma, ascending.
 __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
     const double *__restrict__ dt, const int32_t *__restrict__ n_nodes, int32_t cap, double pq,
-    double *__restrict__ gamma_out, int32_t *__restrict__ stale, int32_t *__restrict__ n_stale)
+    double *__restrict__ gamma_out, int32_t *__restrict__ stale, int32_t *__restrict__ n_stale,
+    int32_t *__restrict__ done)
 {
-    __shared__ uint32_t hist[256];
-    __shared__ uint64_t s_prefix;
-    __shared__ int s_krem;
-    __shared__ int s_wsum[kMitSelThreads / kWave];
+    constexpr int R = kMitSelRegs;
+    constexpr int T = kMitSelThreads;
+    __shared__ __align__(16) uint32_t hist[3][256];
+    __shared__ int s_wsum[2][T / kWave];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nw = blockDim.x >> 6;
     const int n = min(*n_nodes, cap);
     if (n <= 0) {
         if (tid == 0) {
@@ -120,87 +190,96 @@ __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
         }
         return;
     }
+    const bool in_regs = n <= R * T;
+    const int rounds = (n + T - 1) / T;
+    uint64_t kr[R];   // this thread's keys tid + j T (when in_regs)
+    if (in_regs) {
+        // every load issued before the first use; indices clamped to the
+        // buffer (cap), not to n, so they need not wait for the count
+        double x[R];
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+            x[j] = dt[min(tid + j * T, cap - 1)];
+#pragma unroll
+        for (int j = 0; j < R; ++j)
+            kr[j] = order_key(x[j]);
+    }
+    for (int i = tid; i < n; i += T)
+        done[i] = 0;   // k_mit_omega's per-stale-node chunk counts
+    if (tid < 256)
+        hist[0][tid] = 0;
     long long rank = (long long)ceil(pq * (double)n);
     rank = rank < 1 ? 1 : (rank > n ? n : rank);
-    int krem = (int)(rank - 1);
+    uint32_t krem = (uint32_t)(rank - 1);   // keys below the target among those matching
     uint64_t prefix = 0, mask = 0;
-    for (int pass = 7; pass >= 0; --pass) {
-        const int sh = 8 * pass;
-        for (int i = tid; i < 256; i += blockDim.x)
-            hist[i] = 0;
-        __syncthreads();
-        for (int i = tid; i < n; i += blockDim.x) {
-            const uint64_t k = order_key(dt[i]);
-            if ((k & mask) == prefix)
-                atomicAdd(&hist[(k >> sh) & 255], 1u);
-        }
-        __syncthreads();
-        if (wave == 0) {
-            // lane l holds bins 4l .. 4l + 3; a wave scan finds the bin of krem
-            uint32_t b[4];
-            uint32_t sum = 0;
+    for (int pass = 0; pass < 8; ++pass) {
+        const int sh = 56 - 8 * pass;
+        uint32_t *H = hist[pass % 3];
+        if (tid < 256)
+            hist[(pass + 1) % 3][tid] = 0;   // the next pass's buffer
+        if (pass == 0)
+            __syncthreads();   // hist[0] is clear
+        if (in_regs) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                b[j] = hist[4 * lane + j];
-                sum += b[j];
+            for (int j = 0; j < R; ++j) {
+                if (j < rounds)   // uniform
+                    hist_add(H, kr[j], tid + j * T < n && (kr[j] & mask) == prefix, sh, 255u);
             }
-            uint32_t incl = sum;
-#pragma unroll
-            for (int o = 1; o < kWave; o <<= 1) {
-                const uint32_t y = __shfl_up(incl, o, kWave);
-                if (lane >= o)
-                    incl += y;
-            }
-            const uint32_t excl = incl - sum;
-            if (excl <= (uint32_t)krem && (uint32_t)krem < incl) {
-                uint32_t cum = excl;
-                int bin = 4 * lane + 3;
-                bool found = false;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (!found) {
-                        if ((uint32_t)krem < cum + b[j]) {
-                            bin = 4 * lane + j;
-                            found = true;
-                        } else {
-                            cum += b[j];
-                        }
-                    }
-                }
-                s_prefix = prefix | ((uint64_t)bin << sh);
-                s_krem = krem - (int)cum;
+        } else {
+            for (int b0 = 0; b0 < n; b0 += T) {   // whole waves per round
+                const int i = b0 + tid;
+                const uint64_t k = i < n ? order_key(dt[i]) : 0;
+                hist_add(H, k, i < n && (k & mask) == prefix, sh, 255u);
             }
         }
         __syncthreads();
-        prefix = s_prefix;
-        krem = s_krem;
+        // every wave: lane l holds bins 4l .. 4l + 3
+        const uint4 c = reinterpret_cast<const uint4 *>(H)[lane];
+        const uint32_t a0 = c.x, a1 = a0 + c.y, a2 = a1 + c.z, sum = a2 + c.w;
+        const uint32_t incl = wave_incl_scan(sum);
+        const uint32_t excl = incl - sum;
+        // the one lane whose bins hold the rank
+        const int L = __builtin_ctzll(__ballot(excl <= krem && krem < incl));
+        const uint32_t r = krem - excl;   // meaningful on lane L
+        const uint32_t j = (r >= a0 ? 1u : 0u) + (r >= a1 ? 1u : 0u) + (r >= a2 ? 1u : 0u);
+        const uint32_t below = excl + (j == 0 ? 0u : (j == 1 ? a0 : (j == 2 ? a1 : a2)));
+        const uint32_t bin = (uint32_t)__builtin_amdgcn_readlane((int)(4 * lane + j), L);
+        krem -= (uint32_t)__builtin_amdgcn_readlane((int)below, L);
+        prefix |= (uint64_t)bin << sh;
         mask |= 255ull << sh;
-        __syncthreads();
     }
-    const double gamma = key_value(prefix);
-    // stale positions in order, one block of blockDim.x positions at a time
+    // stale positions in order (key > prefix  <=>  dt > gamma); the wave
+    // counts alternate between two buffers, one barrier a round
     int base = 0;
-    for (int b0 = 0; b0 < n; b0 += blockDim.x) {
-        const int i = b0 + tid;
-        const bool f = i < n && dt[i] > gamma;
+    for (int j = 0; j < rounds; ++j) {
+        const int i = tid + j * T;
+        uint64_t k = 0;
+        if (in_regs) {
+#pragma unroll
+            for (int jj = 0; jj < R; ++jj)
+                k = jj == j ? kr[jj] : k;
+        } else {
+            k = order_key(dt[min(i, n - 1)]);
+        }
+        const bool f = i < n && k > prefix;
         const uint64_t bal = __ballot(f);
         const int in_wave = __popcll(bal & ((1ull << lane) - 1));
+        int *ws = s_wsum[j & 1];
         if (lane == 0)
-            s_wsum[wave] = __popcll(bal);
+            ws[wave] = __popcll(bal);
         __syncthreads();
         int before = 0, total = 0;
-        for (int k = 0; k < nw; ++k) {
-            before += k < wave ? s_wsum[k] : 0;
-            total += s_wsum[k];
+        for (int w = 0; w < T / kWave; ++w) {
+            before += w < wave ? ws[w] : 0;
+            total += ws[w];
         }
         if (f)
             stale[base + before + in_wave] = i;
         base += total;
-        __syncthreads();
     }
     if (tid == 0) {
         *n_stale = base;
-        *gamma_out = gamma;
+        *gamma_out = key_value(prefix);
     }
 }
 
@@ -211,7 +290,11 @@ struct Cand {
     int32_t id, pos;
 };
 
-// more common neighbours, then the fresher memory, then the smaller id
+// more common neighbours, then the fresher memory, then the smaller id.  An
+// empty entry (similarity 0) loses to every candidate, so no separate "first
+// candidate" test is needed: the comparisons below use `better` alone (with a
+// short-circuit first-candidate test, the compiler kept the old position
+// while taking the other fields of a new best).
 __device__ __forceinline__ bool better(const Cand &a, const Cand &b)
 {
     if (a.sim != b.sim)
@@ -221,144 +304,271 @@ __device__ __forceinline__ bool better(const Cand &a, const Cand &b)
     return a.id < b.id;
 }
 
-__device__ __forceinline__ int hash_slot(int32_t w) { return (int)(((uint32_t)w * 2654435761u) >> 24); }
-
-__device__ __forceinline__ bool hash_has(const int32_t *hs, int32_t w)
+__device__ __forceinline__ int hash_slot(int32_t w)
 {
-    for (int k = 0, s = hash_slot(w); k < kMitHash; ++k, s = (s + 1) & (kMitHash - 1)) {
-        const int32_t x = hs[s];
-        if (x == w)
-            return true;
-        if (x < 0)
-            return false;
-    }
-    return false;
+    return (int)(((uint32_t)w * 2654435761u) >> (32 - kMitHashBits));
 }
 
-// One workgroup per stale node (blocks past the count exit).
+// Whether w (not in slot `from - 1`) is further along its probe sequence.
+__device__ __forceinline__ int hash_walk(const int32_t *hs, int32_t w, int from)
+{
+    for (int k = 1, s = from; k < kMitHash; ++k, s = (s + 1) & (kMitHash - 1)) {
+        const int32_t x = hs[s];
+        if (x == w)
+            return 1;
+        if (x < 0)
+            return 0;
+    }
+    return 0;
+}
+
+// Candidate lists in LDS: entry arrays of similarity (0 = end of a list),
+// memory time, id and position.
+struct Lists {
+    int *sim;
+    double *mts;
+    int32_t *id, *pos;
+};
+
+// Wave 0 merges nl sorted lists of the entry arrays (list l at l * stride, at
+// most len entries) and one more list at `xb` of xl entries into the best K.
+// Returns their count m on every lane; lane j < m holds the j-th in *mine.
+// Lane i owns lists 4i .. 4i + 3 (nl <= 256); lane 63 also the extra list.
+// Each round the wave takes its best head: a 6-step shuffle arg-best, whose
+// result every lane holds.
+__device__ int merge_lists(const Lists &L, int nl, int stride, int len, int xb, int xl, int K,
+                           Cand *mine)
+{
+    const int lane = threadIdx.x & 63;
+    int h[5] = {0, 0, 0, 0, 0};
+    int m = 0;
+    for (int r = 0; r < K; ++r) {
+        Cand best{0, 0.0, 0, -1};
+        int bi = -1;
+#pragma unroll
+        for (int i = 0; i < 5; ++i) {
+            const int l = 4 * lane + i;
+            const bool own = i < 4 ? (l < nl && h[i] < len) : (lane == 63 && h[4] < xl);
+            const int o = i < 4 ? l * stride + h[i] : xb + h[4];
+            if (own && L.sim[o] > 0) {
+                const Cand x{L.sim[o], L.mts[o], L.id[o], L.pos[o]};
+                if (better(x, best)) {   // best starts empty
+                    best = x;
+                    bi = i;
+                }
+            }
+        }
+        // the winner is unique (positions are distinct)
+        Cand wb = best;
+        int wl = bi >= 0 ? lane : -1;
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o >>= 1) {
+            Cand y;
+            y.sim = __shfl_xor(wb.sim, o, kWave);
+            y.mts = __shfl_xor(wb.mts, o, kWave);
+            y.id = __shfl_xor(wb.id, o, kWave);
+            y.pos = __shfl_xor(wb.pos, o, kWave);
+            const int yl = __shfl_xor(wl, o, kWave);
+            if (better(y, wb)) {   // an empty lane's entry has similarity 0
+                wb = y;
+                wl = yl;
+            }
+        }
+        if (wl < 0)
+            break;   // no candidate left anywhere (uniform)
+        if (lane == wl) {
+#pragma unroll
+            for (int i = 0; i < 5; ++i)
+                h[i] += i == bi ? 1 : 0;
+        }
+        if (lane == r)
+            *mine = wb;
+        m = r + 1;
+    }
+    return m;
+}
+
+// Work items (stale node q, chunk c of the node set), q-major, strided over a
+// fixed grid.  An item probes the neighbour set of every active node of its
+// chunk against the stale node's (an LDS hash set), 1024 nodes at a time
+// (kMitPerThread per thread, each thread keeping its best few sorted), and
+// merges the thread lists into a running top-K.  With one chunk that is
+// Omega; otherwise the chunk lists go to `part` and the last workgroup to
+// finish a chunk of q (a device counter, zeroed by k_mit_select) merges them.
+// The workgroup that holds Omega writes it and blends the stale row.  No
+// workgroup waits for another.
+template <int NBP>   // padded neighbour-set width: 4 (nb <= 4), 12 (<= 12) or 64
 __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
     const int32_t *__restrict__ nodes, const int32_t *__restrict__ n_nodes, int32_t cap,
     const double *__restrict__ dt, const double *__restrict__ mem_ts,
-    const int32_t *__restrict__ nset, const int32_t *__restrict__ ncnt, int32_t nbp,
+    const int32_t *__restrict__ nset, const int32_t *__restrict__ ncnt,
     const double *__restrict__ gamma_p, const int32_t *__restrict__ stale,
-    const int32_t *__restrict__ n_stale, int32_t K, float lambda, float *__restrict__ mem,
-    int32_t M, int32_t *__restrict__ omega)
+    const int32_t *__restrict__ n_stale, int2 *__restrict__ part,
+    int32_t *__restrict__ done, int32_t K, float lambda, float *__restrict__ mem, int32_t M,
+    int32_t *__restrict__ omega)
 {
+    typedef int __attribute__((ext_vector_type(4))) i4;
+    constexpr int P = kMitPerThread;
+    constexpr int U = NBP > 16 ? 1 : P;   // nodes in flight per thread
+    constexpr int kSub = kMitThreads * P;  // nodes per round
+    // entries: [0, kSub) thread lists (P each), then the running list
+    constexpr int kE = kSub + kMitMaxK;
     __shared__ int32_t hs[kMitHash];
-    // each thread's sorted list: similarity and position (mem_ts and the id
-    // are read back through the position)
-    __shared__ int c_sim[kMitThreads * kMitMaxK];
-    __shared__ int32_t c_pos[kMitThreads * kMitMaxK];
-    __shared__ int32_t r_pos[kMitMaxK];
-    __shared__ int s_m;
-    const int q = blockIdx.x;
-    if (q >= *n_stale)
-        return;
-    const int tid = threadIdx.x, lane = tid & 63;
+    __shared__ int e_sim[kE];
+    __shared__ double e_mts[kE];
+    __shared__ int32_t e_id[kE], e_pos[kE];
+    __shared__ int s_m, s_last;
+    const Lists L{e_sim, e_mts, e_id, e_pos};
+    const int RB = kSub;   // the running list
+    const int tid = threadIdx.x;
     const int n = min(*n_nodes, cap);
+    const int ns = *n_stale;
+    // chunks per stale node: one per 1024-node round, at most kMitMaxChunks,
+    // and no more items than kMitOmegaGrid unless every stale node is one item
+    const int nsub = (n + kSub - 1) / kSub;
+    int nce = min(min(nsub, kMitMaxChunks), max(1, kMitOmegaGrid / max(ns, 1)));
+    const int chunk = (nsub + nce - 1) / nce * kSub;
+    nce = (n + chunk - 1) / chunk;   // chunks that hold nodes
+    const int items = ns * nce;
     const double gamma = *gamma_p;
-    const int v = stale[q];
-    for (int i = tid; i < kMitHash; i += blockDim.x)
-        hs[i] = -1;
-    __syncthreads();
-    if (tid < ncnt[v]) {   // distinct ids: each is inserted once
-        const int32_t w = nset[(int64_t)v * nbp + tid];
-        for (int s = hash_slot(w);; s = (s + 1) & (kMitHash - 1))
-            if (atomicCAS(&hs[s], -1, w) == -1)
-                break;
-    }
-    __syncthreads();
-    // this thread's best K candidates, sorted best first (sim 0 = empty)
-    Cand top[kMitMaxK];
-#pragma unroll
-    for (int j = 0; j < kMitMaxK; ++j)
-        top[j] = Cand{0, 0.0, 0, -1};
-    for (int u = tid; u < n; u += blockDim.x) {
-        if (!(dt[u] < gamma))
-            continue;
-        const int c = ncnt[u];
-        int sim = 0;
-        for (int j = 0; j < c; ++j)
-            sim += hash_has(hs, nset[(int64_t)u * nbp + j]) ? 1 : 0;
-        if (sim == 0)
-            continue;
-        Cand x{sim, mem_ts[u], nodes[u], u};
-        // insertion into the sorted list: entries worse than x move down one
-#pragma unroll
-        for (int j = 0; j < kMitMaxK; ++j) {
-            if (j < K && (top[j].sim == 0 || better(x, top[j]))) {
-                const Cand y = top[j];
-                top[j] = x;
-                x = y;
-            }
+    const int KP = K < P ? K : P;   // per-thread list length
+    for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        const int q = item / nce, c = item % nce;
+        const int v = stale[q];
+        for (int i = tid; i < kMitHash; i += blockDim.x)
+            hs[i] = -1;
+        if (tid == 0)
+            s_m = 0;
+        __syncthreads();
+        if (tid < ncnt[v]) {   // distinct ids: each is inserted once
+            const int32_t w = nset[(int64_t)v * NBP + tid];
+            for (int sl = hash_slot(w);; sl = (sl + 1) & (kMitHash - 1))
+                if (atomicCAS(&hs[sl], -1, w) == -1)
+                    break;
         }
-    }
+        __syncthreads();
+        const int lo = c * chunk, hi = min(n, lo + chunk);
+        for (int sub = lo; sub < hi; sub += kSub) {
+            // this thread's best candidates among its P nodes, best first
+            Cand top[P];
 #pragma unroll
-    for (int j = 0; j < kMitMaxK; ++j) {
-        const int o = tid * kMitMaxK + j;
-        c_sim[o] = j < K ? top[j].sim : 0;
-        c_pos[o] = top[j].pos;
-    }
-    __syncthreads();
-    if (tid < kWave) {
-        // lane l merges the sorted lists of threads 4l .. 4l + 3 (heads h[i]);
-        // each round the wave takes its best head
-        int h[4] = {0, 0, 0, 0};
-        int m = 0;
-        for (int r = 0; r < K; ++r) {
-            Cand best{0, 0.0, 0, -1};
-            int bi = -1;
+            for (int j = 0; j < P; ++j)
+                top[j] = Cand{0, 0.0, 0, -1};
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int o = (4 * lane + i) * kMitMaxK + h[i];
-                if (h[i] < K && c_sim[o] > 0) {
-                    const int32_t ps = c_pos[o];
-                    const Cand x{c_sim[o], mem_ts[ps], nodes[ps], ps};
-                    if (bi < 0 || better(x, best)) {
-                        best = x;
-                        bi = i;
+            for (int x0 = 0; x0 < P; x0 += U) {
+                i4 row[U][NBP / 4];
+                double g[U];
+#pragma unroll
+                for (int x = 0; x < U; ++x) {
+                    const int u = min(sub + tid + (x0 + x) * kMitThreads, hi - 1);   // in range
+                    g[x] = dt[u];
+#pragma unroll
+                    for (int e = 0; e < NBP / 4; ++e)
+                        row[x][e] = reinterpret_cast<const i4 *>(nset + (int64_t)u * NBP)[e];
+                }
+#pragma unroll
+                for (int x = 0; x < U; ++x) {
+                    const int u = sub + tid + (x0 + x) * kMitThreads;
+                    // first probes of every id together; one that meets another
+                    // id walks on (rare: at most 64 of kMitHash slots are taken)
+                    int32_t y[NBP];
+#pragma unroll
+                    for (int e = 0; e < NBP; ++e)
+                        y[e] = hs[hash_slot(row[x][e / 4][e % 4])];
+                    int sim = 0;
+#pragma unroll
+                    for (int e = 0; e < NBP; ++e) {
+                        const int32_t w = row[x][e / 4][e % 4];
+                        if (w != INT32_MAX) {
+                            if (y[e] == w)
+                                ++sim;
+                            else if (y[e] >= 0)
+                                sim += hash_walk(hs, w, (hash_slot(w) + 1) & (kMitHash - 1));
+                        }
+                    }
+                    // active nodes only (v is not); a common neighbour at least
+                    if (u >= hi || !(g[x] < gamma) || sim == 0)
+                        continue;
+                    Cand z{sim, mem_ts[u], nodes[u], u};
+#pragma unroll
+                    for (int j = 0; j < P; ++j) {   // sorted insertion
+                        if (j < KP && better(z, top[j])) {   // empties lose
+                            const Cand t = top[j];
+                            top[j] = z;
+                            z = t;
+                        }
                     }
                 }
             }
-            // wave arg-best: the winner is unique (ids are distinct)
-            Cand wb = best;
-            int wl = bi >= 0 ? lane : -1;
 #pragma unroll
-            for (int o = kWave / 2; o >= 1; o >>= 1) {
-                Cand y;
-                y.sim = __shfl_xor(wb.sim, o, kWave);
-                y.mts = __shfl_xor(wb.mts, o, kWave);
-                y.id = __shfl_xor(wb.id, o, kWave);
-                y.pos = __shfl_xor(wb.pos, o, kWave);
-                const int yl = __shfl_xor(wl, o, kWave);
-                if (yl >= 0 && (wl < 0 || better(y, wb))) {
-                    wb = y;
-                    wl = yl;
-                }
+            for (int j = 0; j < P; ++j) {
+                const int o = tid * P + j;
+                e_sim[o] = j < KP ? top[j].sim : 0;
+                e_mts[o] = top[j].mts;
+                e_id[o] = top[j].id;
+                e_pos[o] = top[j].pos;
             }
-            if (wl < 0)
-                break;   // no candidate left anywhere (uniform)
-            if (lane == wl)
-                ++h[bi];
-            if (lane == 0)
-                r_pos[r] = wb.pos;
-            m = r + 1;
+            __syncthreads();
+            if (tid < kWave) {   // the new running list, written after the merge's reads
+                Cand w;
+                const int m = merge_lists(L, kMitThreads, P, P, RB, s_m, K, &w);
+                if (tid < m) {
+                    e_sim[RB + tid] = w.sim;
+                    e_mts[RB + tid] = w.mts;
+                    e_id[RB + tid] = w.id;
+                    e_pos[RB + tid] = w.pos;
+                }
+                if (tid == 0)
+                    s_m = m;
+            }
+            __syncthreads();
         }
-        if (lane == 0)
-            s_m = m;
-    }
-    __syncthreads();
-    const int m = s_m;
-    if (omega && tid < K)
-        omega[(int64_t)q * K + tid] = tid < m ? r_pos[tid] : -1;
-    if (m > 0) {
-        const float rest = 1.0f - lambda;
-        for (int c = tid; c < M; c += blockDim.x) {
-            float acc = 0.f;
-            for (int j = 0; j < m; ++j)
-                acc += mem[(int64_t)r_pos[j] * M + c];
-            mem[(int64_t)v * M + c] = lambda * mem[(int64_t)v * M + c] + rest * (acc / (float)m);
+        if (nce > 1) {
+            int2 *mine = part + ((int64_t)q * nce + c) * K;   // q nce < kMitOmegaGrid
+            if (tid < K)
+                mine[tid] = tid < s_m ? make_int2(e_sim[RB + tid], e_pos[RB + tid])
+                                      : make_int2(0, -1);
+            __threadfence();   // the list is visible device-wide before the count
+            __syncthreads();
+            if (tid == 0)
+                s_last = atomicAdd(&done[q], 1) == nce - 1;
+            __syncthreads();
+            if (!s_last)
+                continue;   // uniform: s_last is shared
+            __threadfence();   // the other chunks' lists are seen after the count
+            for (int i = tid; i < nce * K; i += blockDim.x) {
+                const int2 e = part[(int64_t)q * nce * K + i];
+                const int ps = e.y < 0 ? 0 : e.y;
+                e_sim[i] = e.x;
+                e_mts[i] = mem_ts[ps];
+                e_id[i] = nodes[ps];
+                e_pos[i] = e.y;
+            }
+            __syncthreads();
+            if (tid < kWave) {
+                Cand w;
+                const int m = merge_lists(L, nce, K, K, 0, 0, K, &w);
+                if (tid < m)
+                    e_pos[RB + tid] = w.pos;
+                if (tid == 0)
+                    s_m = m;
+            }
+            __syncthreads();
         }
+        const int m = s_m;
+        if (omega && tid < K)
+            omega[(int64_t)q * K + tid] = tid < m ? e_pos[RB + tid] : -1;
+        if (m > 0) {
+            const float rest = 1.0f - lambda;
+            for (int cc = tid; cc < M; cc += blockDim.x) {
+                float acc = 0.f;
+                for (int j = 0; j < m; ++j)
+                    acc += mem[(int64_t)e_pos[RB + j] * M + cc];
+                mem[(int64_t)v * M + cc] =
+                    lambda * mem[(int64_t)v * M + cc] + rest * (acc / (float)m);
+            }
+        }
+        __syncthreads();   // the entries and s_m are reused
     }
 }
 
@@ -366,18 +576,23 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
 
 // ======================================================================== API
 
+namespace {
+
+
+}  // namespace
+
 extern "C" tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int32_t K,
                                              tgm_mitigator_t *out)
 {
     if (!out)
         return TGM_EINVAL;
     *out = nullptr;
-    if (max_nodes <= 0 || nb < 1 || nb > 64 || K < 1 || K > kMitMaxK)
+    if (max_nodes <= 0 || max_nodes > kMitMaxNodes || nb < 1 || nb > 64 || K < 1 || K > kMitMaxK)
         return TGM_EINVAL;
     tgm_mitigator *mt = new tgm_mitigator();
     mt->cap = max_nodes;
     mt->nb = nb;
-    mt->nbp = round_up(nb, 4);
+    mt->nbp = nb <= 4 ? 4 : (nb <= 12 ? 12 : 64);   // the widths k_mit_omega reads
     mt->K = K;
     const size_t c = (size_t)max_nodes;
     if (hipMalloc((void **)&mt->dt, sizeof(double) * c) != hipSuccess ||
@@ -386,7 +601,9 @@ extern "C" tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int3
         hipMalloc((void **)&mt->gamma, sizeof(double)) != hipSuccess ||
         hipMalloc((void **)&mt->n_stale, sizeof(int32_t)) != hipSuccess ||
         hipMalloc((void **)&mt->stale, sizeof(int32_t) * c) != hipSuccess ||
-        hipMalloc((void **)&mt->omega, sizeof(int32_t) * c * K) != hipSuccess) {
+        hipMalloc((void **)&mt->omega, sizeof(int32_t) * c * K) != hipSuccess ||
+        hipMalloc((void **)&mt->part, sizeof(int2) * kMitOmegaGrid * kMitMaxK) != hipSuccess ||
+        hipMalloc((void **)&mt->done, sizeof(int32_t) * c) != hipSuccess) {
         tgm_mitigator_destroy(mt);
         return TGM_ENOMEM;
     }
@@ -405,6 +622,8 @@ extern "C" tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt)
     (void)hipFree(mt->n_stale);
     (void)hipFree(mt->stale);
     (void)hipFree(mt->omega);
+    (void)hipFree(mt->part);
+    (void)hipFree(mt->done);
     delete mt;
     return TGM_OK;
 }
@@ -427,13 +646,24 @@ tgm_status_t tgm::mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t fir
     TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->N,
                g->t, first_event, nodes, n_nodes, cap, mem_ts, mt->nb, mt->nbp, mt->dt,
                mt->nset, mt->ncnt);
-    TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, mt->dt, n_nodes, cap, p,
-               mt->gamma, mt->stale, mt->n_stale);
-    // at most n - ceil(p n) + 1 <= cap (1 - p) + 1 nodes are stale
-    const int64_t grid = std::min<int64_t>(cap, (int64_t)std::floor(cap * (1.0 - p)) + 1);
-    TGM_LAUNCH(k_mit_omega, dim3((unsigned)grid), dim3(kMitThreads), 0, s, nodes, n_nodes, cap,
-               mt->dt, mem_ts, mt->nset, mt->ncnt, mt->nbp, mt->gamma, mt->stale, mt->n_stale,
-               mt->K, lambda, mem, M, mt->omega);
+    TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, mt->dt, n_nodes,
+               cap, p, mt->gamma, mt->stale, mt->n_stale, mt->done);
+    // at most n - ceil(p n) + 1 <= cap (1 - p) + 1 nodes are stale, each in
+    // at most ceil(cap / kMitChunk) items; a fixed grid strides over the items
+    const int64_t slots = std::min<int64_t>(cap, (int64_t)std::floor(cap * (1.0 - p)) + 1);
+    const dim3 grid((unsigned)std::min<int64_t>(slots * cdiv(cap, kMitChunk), kMitOmegaGrid));
+    if (mt->nbp == 4)
+        TGM_LAUNCH(k_mit_omega<4>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mt->dt,
+                   mem_ts, mt->nset, mt->ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
+                   mt->done, mt->K, lambda, mem, M, mt->omega);
+    else if (mt->nbp == 12)
+        TGM_LAUNCH(k_mit_omega<12>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mt->dt,
+                   mem_ts, mt->nset, mt->ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
+                   mt->done, mt->K, lambda, mem, M, mt->omega);
+    else
+        TGM_LAUNCH(k_mit_omega<64>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mt->dt,
+                   mem_ts, mt->nset, mt->ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
+                   mt->done, mt->K, lambda, mem, M, mt->omega);
     return TGM_OK;
 }
 

@@ -74,7 +74,8 @@ def test_mitigation_tiny_full_run(orc, s, mit):
     (0, {}, dict(p=0.6, lam=0.5, K=3)),
     (1, dict(nb=1, s=0), dict(p=0.3, lam=0.0, K=2)),
     (2, dict(D_e=0, s=3), dict(p=0.0, lam=0.9, K=5)),   # p = 0: gamma is the smallest gap
-    (3, dict(nb=12, B=5), dict(p=1.0, lam=0.5, K=4))])  # p = 1: nothing is stale
+    (3, dict(nb=12, B=5), dict(p=1.0, lam=0.5, K=4)),   # p = 1: nothing is stale
+    (4, dict(nb=20, s=1), dict(p=0.5, lam=0.25, K=16))])   # the widest neighbour sets
 def test_mitigation_tie_heavy(orc, seed, kw, mit):
     # integer times over a short span: many equal gaps, equal memory times and
     # equal common-neighbour counts
