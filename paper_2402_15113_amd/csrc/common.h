@@ -460,12 +460,22 @@ tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int
                                const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
                                int32_t cap, int64_t first_event, int32_t b, int32_t nb,
                                float *mem_new, double *new_mem_ts, int64_t *winner, float *h,
-                               const tgm_sample_buffers *next_sb, hipStream_t s);
+                               const tgm_sample_buffers *next_sb, int32_t mit_slot,
+                               hipStream_t s);
 
-// tgm_mitigate on stream s (three launches; see mitigate.hip).
+// The mitigation of tgm_mitigate in two parts.  mitigate_prep_launch writes
+// the neighbour sets of a node set into slot `slot` (it needs the graph and
+// the node set only); mitigate_launch selects the stale nodes and blends their
+// fetched memories with the sets of that slot.  Slot 0 belongs to
+// tgm_mitigate; mitigate_reserve makes slots 0 .. nslots - 1 (it may allocate,
+// and drops the contents of existing slots).
+tgm_status_t mitigate_reserve(tgm_mitigator_t mt, int32_t nslots);
+tgm_status_t mitigate_prep_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
+                                  const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
+                                  int32_t slot, hipStream_t s);
 tgm_status_t mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
                              const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
                              float *mem, const double *mem_ts, int32_t M, double p, float lambda,
-                             hipStream_t s);
+                             int32_t slot, hipStream_t s);
 
 }  // namespace tgm

@@ -11,19 +11,21 @@
 //   s_v      <- lambda s_v + (1 - lambda) mean_{u in Omega(v)} s_u  (in place;
 //             a stale row is never a source: sources are active).
 // Three launches:
-//   k_mit_prep    one wavefront per node: its gap and its sorted distinct
-//                 neighbour set (padded with INT32_MAX);
+//   k_mit_prep    one wavefront per node: its sorted distinct neighbour set
+//                 (padded with INT32_MAX).  It depends on the graph and the
+//                 node set only, so the pipelined executor runs it on its
+//                 sampling stream, into one slot per sample buffer set;
 //   k_mit_select  one workgroup: gamma by a radix select over the
 //                 order-preserving 64-bit keys of the gaps (held in
 //                 registers, eight digit passes), then the stale positions
 //                 in order;
-//   k_mit_omega   one workgroup per stale node: its neighbour set in an LDS
-//                 hash set, every active node's set probed against it (rows
-//                 read as 16-byte vectors, several nodes in flight per
-//                 thread), a per-thread top-K, a wave-merge of the sorted
-//                 lists, and the blend.
-// Integer decisions only; the gaps are formed exactly as the oracle forms them
-// (one fp64 subtraction).
+//   k_mit_omega   work items (stale node, chunk of the node set) over a
+//                 fixed grid: the stale node's neighbour set in an LDS hash
+//                 set, every active node's set of the chunk probed against it,
+//                 per-thread sorted lists merged into the top-K, chunk lists
+//                 merged by the last workgroup of the node, and the blend.
+// Integer decisions only; each gap is formed where it is used, by the one fp64
+// subtraction the oracle makes.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -32,9 +34,9 @@ using namespace tgm;
 
 struct tgm_mitigator {
     int32_t cap = 0, nb = 0, nbp = 0, K = 0;
-    double *dt = nullptr;        // [cap] gaps
-    int32_t *nset = nullptr;     // [cap x nbp] sorted distinct neighbour ids
-    int32_t *ncnt = nullptr;     // [cap]
+    int32_t nslots = 0;          // neighbour-set slots (0: tgm_mitigate; 1..: the executor's)
+    int32_t *nset = nullptr;     // [nslots x cap x nbp] sorted distinct neighbour ids
+    int32_t *ncnt = nullptr;     // [nslots x cap]
     double *gamma = nullptr;     // [1]
     int32_t *n_stale = nullptr;  // [1]
     int32_t *stale = nullptr;    // [cap] stale positions, ascending
@@ -61,17 +63,16 @@ constexpr int kMitOmegaGrid = 1024;         // k_mit_omega workgroups
 constexpr int kMitMaxNodes = 1 << 20;
 
 // ---------------------------------------------------------------- prep
-// One wavefront per fetched node: its gap and its sorted distinct neighbour
-// set.  Lane j < c holds the j-th most recent neighbour; duplicates and ranks
-// come from a loop over the c lanes with readlane (c <= nb <= 64).
+// One wavefront per fetched node: its sorted distinct neighbour set before T,
+// the time of event `first`.  Lane j < c holds the j-th most recent
+// neighbour; duplicates and ranks come from a loop over the c lanes with
+// readlane (c <= nb <= 64).
 __global__ __launch_bounds__(256) void k_mit_prep(const int64_t *__restrict__ off,
                                                   const AdjRec *__restrict__ adj, int32_t N,
                                                   const double *__restrict__ t, int64_t first,
                                                   const int32_t *__restrict__ nodes,
                                                   const int32_t *__restrict__ n_nodes,
-                                                  int32_t cap, const double *__restrict__ mem_ts,
-                                                  int32_t nb, int32_t nbp,
-                                                  double *__restrict__ dt,
+                                                  int32_t cap, int32_t nb, int32_t nbp,
                                                   int32_t *__restrict__ nset,
                                                   int32_t *__restrict__ ncnt)
 {
@@ -101,10 +102,8 @@ __global__ __launch_bounds__(256) void k_mit_prep(const int64_t *__restrict__ of
     const int d = __popcll(__ballot(lane < c && !dup));
     if (lane >= d && lane < nbp)
         nset[(int64_t)p * nbp + lane] = INT32_MAX;   // padding: never an id
-    if (lane == 0) {
+    if (lane == 0)
         ncnt[p] = d;
-        dt[p] = T - mem_ts[p];
-    }
 }
 
 // ---------------------------------------------------------------- select
@@ -173,9 +172,9 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint64_t k, bool in, in
 // passes before, by waves that have all passed the barrier since.  Then the
 // positions with dt > gamma, ascending.
 __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
-    const double *__restrict__ dt, const int32_t *__restrict__ n_nodes, int32_t cap, double pq,
-    double *__restrict__ gamma_out, int32_t *__restrict__ stale, int32_t *__restrict__ n_stale,
-    int32_t *__restrict__ done)
+    const double *__restrict__ t, int64_t first, const double *__restrict__ mem_ts,
+    const int32_t *__restrict__ n_nodes, int32_t cap, double pq, double *__restrict__ gamma_out,
+    int32_t *__restrict__ stale, int32_t *__restrict__ n_stale, int32_t *__restrict__ done)
 {
     constexpr int R = kMitSelRegs;
     constexpr int T = kMitSelThreads;
@@ -190,19 +189,22 @@ __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
         }
         return;
     }
+    const double T0 = t[first];
+    auto gap = [&](int i) { return T0 - mem_ts[i]; };
     const bool in_regs = n <= R * T;
     const int rounds = (n + T - 1) / T;
     uint64_t kr[R];   // this thread's keys tid + j T (when in_regs)
     if (in_regs) {
         // every load issued before the first use; indices clamped to the
-        // buffer (cap), not to n, so they need not wait for the count
+        // buffer (cap), not to n, so they need not wait for the count (mem_ts
+        // holds cap entries)
         double x[R];
 #pragma unroll
         for (int j = 0; j < R; ++j)
-            x[j] = dt[min(tid + j * T, cap - 1)];
+            x[j] = mem_ts[min(tid + j * T, cap - 1)];
 #pragma unroll
         for (int j = 0; j < R; ++j)
-            kr[j] = order_key(x[j]);
+            kr[j] = order_key(T0 - x[j]);
     }
     for (int i = tid; i < n; i += T)
         done[i] = 0;   // k_mit_omega's per-stale-node chunk counts
@@ -228,7 +230,7 @@ __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
         } else {
             for (int b0 = 0; b0 < n; b0 += T) {   // whole waves per round
                 const int i = b0 + tid;
-                const uint64_t k = i < n ? order_key(dt[i]) : 0;
+                const uint64_t k = i < n ? order_key(gap(i)) : 0;
                 hist_add(H, k, i < n && (k & mask) == prefix, sh, 255u);
             }
         }
@@ -259,7 +261,7 @@ __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
             for (int jj = 0; jj < R; ++jj)
                 k = jj == j ? kr[jj] : k;
         } else {
-            k = order_key(dt[min(i, n - 1)]);
+            k = order_key(gap(min(i, n - 1)));
         }
         const bool f = i < n && k > prefix;
         const uint64_t bal = __ballot(f);
@@ -400,7 +402,7 @@ __device__ int merge_lists(const Lists &L, int nl, int stride, int len, int xb, 
 template <int NBP>   // padded neighbour-set width: 4 (nb <= 4), 12 (<= 12) or 64
 __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
     const int32_t *__restrict__ nodes, const int32_t *__restrict__ n_nodes, int32_t cap,
-    const double *__restrict__ dt, const double *__restrict__ mem_ts,
+    const double *__restrict__ t, int64_t first, const double *__restrict__ mem_ts,
     const int32_t *__restrict__ nset, const int32_t *__restrict__ ncnt,
     const double *__restrict__ gamma_p, const int32_t *__restrict__ stale,
     const int32_t *__restrict__ n_stale, int2 *__restrict__ part,
@@ -431,6 +433,7 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
     nce = (n + chunk - 1) / chunk;   // chunks that hold nodes
     const int items = ns * nce;
     const double gamma = *gamma_p;
+    const double T0 = t[first];
     const int KP = K < P ? K : P;   // per-thread list length
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         const int q = item / nce, c = item % nce;
@@ -461,7 +464,7 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
 #pragma unroll
                 for (int x = 0; x < U; ++x) {
                     const int u = min(sub + tid + (x0 + x) * kMitThreads, hi - 1);   // in range
-                    g[x] = dt[u];
+                    g[x] = T0 - mem_ts[u];   // the gap
 #pragma unroll
                     for (int e = 0; e < NBP / 4; ++e)
                         row[x][e] = reinterpret_cast<const i4 *>(nset + (int64_t)u * NBP)[e];
@@ -595,15 +598,13 @@ extern "C" tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int3
     mt->nbp = nb <= 4 ? 4 : (nb <= 12 ? 12 : 64);   // the widths k_mit_omega reads
     mt->K = K;
     const size_t c = (size_t)max_nodes;
-    if (hipMalloc((void **)&mt->dt, sizeof(double) * c) != hipSuccess ||
-        hipMalloc((void **)&mt->nset, sizeof(int32_t) * c * mt->nbp) != hipSuccess ||
-        hipMalloc((void **)&mt->ncnt, sizeof(int32_t) * c) != hipSuccess ||
-        hipMalloc((void **)&mt->gamma, sizeof(double)) != hipSuccess ||
+    if (hipMalloc((void **)&mt->gamma, sizeof(double)) != hipSuccess ||
         hipMalloc((void **)&mt->n_stale, sizeof(int32_t)) != hipSuccess ||
         hipMalloc((void **)&mt->stale, sizeof(int32_t) * c) != hipSuccess ||
         hipMalloc((void **)&mt->omega, sizeof(int32_t) * c * K) != hipSuccess ||
         hipMalloc((void **)&mt->part, sizeof(int2) * kMitOmegaGrid * kMitMaxK) != hipSuccess ||
-        hipMalloc((void **)&mt->done, sizeof(int32_t) * c) != hipSuccess) {
+        hipMalloc((void **)&mt->done, sizeof(int32_t) * c) != hipSuccess ||
+        tgm::mitigate_reserve(mt, 1) != TGM_OK) {
         tgm_mitigator_destroy(mt);
         return TGM_ENOMEM;
     }
@@ -615,7 +616,6 @@ extern "C" tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt)
 {
     if (!mt)
         return TGM_EINVAL;
-    (void)hipFree(mt->dt);
     (void)hipFree(mt->nset);
     (void)hipFree(mt->ncnt);
     (void)hipFree(mt->gamma);
@@ -628,12 +628,54 @@ extern "C" tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt)
     return TGM_OK;
 }
 
+tgm_status_t tgm::mitigate_reserve(tgm_mitigator_t mt, int32_t nslots)
+{
+    if (!mt || nslots < 1)
+        return TGM_EINVAL;
+    if (nslots <= mt->nslots)
+        return TGM_OK;
+    // the sets of earlier calls need not survive: a run fills its slots first
+    if (mt->nslots > 0 && hipDeviceSynchronize() != hipSuccess)
+        return TGM_EDEVICE;
+    (void)hipFree(mt->nset);
+    (void)hipFree(mt->ncnt);
+    mt->nset = nullptr;
+    mt->ncnt = nullptr;
+    mt->nslots = 0;
+    const size_t c = (size_t)mt->cap * nslots;
+    if (hipMalloc((void **)&mt->nset, sizeof(int32_t) * c * mt->nbp) != hipSuccess ||
+        hipMalloc((void **)&mt->ncnt, sizeof(int32_t) * c) != hipSuccess)
+        return TGM_ENOMEM;
+    mt->nslots = nslots;
+    return TGM_OK;
+}
+
+tgm_status_t tgm::mitigate_prep_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
+                                       const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
+                                       int32_t slot, hipStream_t s)
+{
+    if (!mt || !g || !nodes || !n_nodes || cap < 0 || slot < 0 || slot >= mt->nslots)
+        return TGM_EINVAL;
+    if (first_event < 0 || first_event >= g->E)
+        return TGM_ERANGE;
+    if (cap > mt->cap)
+        return TGM_ESIZE;
+    if (cap == 0)
+        return TGM_OK;
+    const int64_t o = (int64_t)slot * mt->cap;
+    TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->N,
+               g->t, first_event, nodes, n_nodes, cap, mt->nb, mt->nbp, mt->nset + o * mt->nbp,
+               mt->ncnt + o);
+    return TGM_OK;
+}
+
 tgm_status_t tgm::mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
                                   const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
                                   float *mem, const double *mem_ts, int32_t M, double p,
-                                  float lambda, hipStream_t s)
+                                  float lambda, int32_t slot, hipStream_t s)
 {
-    if (!mt || !g || !nodes || !n_nodes || !mem || !mem_ts || M <= 0 || cap < 0)
+    if (!mt || !g || !nodes || !n_nodes || !mem || !mem_ts || M <= 0 || cap < 0 || slot < 0 ||
+        slot >= mt->nslots)
         return TGM_EINVAL;
     if (!(p >= 0.0 && p <= 1.0) || !(lambda >= 0.0f && lambda <= 1.0f))
         return TGM_EINVAL;
@@ -643,26 +685,25 @@ tgm_status_t tgm::mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t fir
         return TGM_ESIZE;
     if (cap == 0)
         return TGM_OK;
-    TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->N,
-               g->t, first_event, nodes, n_nodes, cap, mem_ts, mt->nb, mt->nbp, mt->dt,
-               mt->nset, mt->ncnt);
-    TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, mt->dt, n_nodes,
-               cap, p, mt->gamma, mt->stale, mt->n_stale, mt->done);
+    const int64_t o = (int64_t)slot * mt->cap;
+    const int32_t *nset = mt->nset + o * mt->nbp, *ncnt = mt->ncnt + o;
+    TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, g->t, first_event, mem_ts,
+               n_nodes, cap, p, mt->gamma, mt->stale, mt->n_stale, mt->done);
     // at most n - ceil(p n) + 1 <= cap (1 - p) + 1 nodes are stale, each in
     // at most ceil(cap / kMitChunk) items; a fixed grid strides over the items
     const int64_t slots = std::min<int64_t>(cap, (int64_t)std::floor(cap * (1.0 - p)) + 1);
     const dim3 grid((unsigned)std::min<int64_t>(slots * cdiv(cap, kMitChunk), kMitOmegaGrid));
     if (mt->nbp == 4)
-        TGM_LAUNCH(k_mit_omega<4>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mt->dt,
-                   mem_ts, mt->nset, mt->ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
+        TGM_LAUNCH(k_mit_omega<4>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
+                   first_event, mem_ts, nset, ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
                    mt->done, mt->K, lambda, mem, M, mt->omega);
     else if (mt->nbp == 12)
-        TGM_LAUNCH(k_mit_omega<12>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mt->dt,
-                   mem_ts, mt->nset, mt->ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
+        TGM_LAUNCH(k_mit_omega<12>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
+                   first_event, mem_ts, nset, ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
                    mt->done, mt->K, lambda, mem, M, mt->omega);
     else
-        TGM_LAUNCH(k_mit_omega<64>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mt->dt,
-                   mem_ts, mt->nset, mt->ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
+        TGM_LAUNCH(k_mit_omega<64>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
+                   first_event, mem_ts, nset, ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
                    mt->done, mt->K, lambda, mem, M, mt->omega);
     return TGM_OK;
 }
@@ -672,8 +713,15 @@ extern "C" tgm_status_t tgm_mitigate(tgm_mitigator_t mt, tgm_graph_t g, int64_t 
                                      float *mem, const double *mem_ts, int32_t M, double p,
                                      float lambda, void *stream)
 {
+    // slot 0: the neighbour sets of this call
+    if (!mem || !mem_ts || M <= 0)
+        return TGM_EINVAL;
+    if (!(p >= 0.0 && p <= 1.0) || !(lambda >= 0.0f && lambda <= 1.0f))
+        return TGM_EINVAL;
+    TGM_TRY_STATUS(tgm::mitigate_prep_launch(mt, g, first_event, nodes, n_nodes, cap, 0,
+                                             as_stream(stream)));
     return tgm::mitigate_launch(mt, g, first_event, nodes, n_nodes, cap, mem, mem_ts, M, p,
-                                lambda, as_stream(stream));
+                                lambda, 0, as_stream(stream));
 }
 
 extern "C" tgm_status_t tgm_mitigator_read(tgm_mitigator_t mt, double *gamma, int32_t *n_stale,

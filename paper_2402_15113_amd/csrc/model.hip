@@ -2168,11 +2168,13 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
                                     const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
                                     int32_t cap, int64_t first_event, int32_t b, int32_t nb,
                                     float *mem_new, double *new_mem_ts, int64_t *winner,
-                                    float *h, const tgm_sample_buffers *next_sb, hipStream_t s)
+                                    float *h, const tgm_sample_buffers *next_sb,
+                                    int32_t mit_slot, hipStream_t s)
 {
     if (st && st->mit)   // the mitigation of this iteration's fetched memories
         TGM_TRY_STATUS(mitigate_launch(st->mit, g, first_event, sb.nodes, sb.n_nodes, cap,
-                                       fb.mem, fb.mem_ts, st->M, st->mit_p, st->mit_lambda, s));
+                                       fb.mem, fb.mem_ts, st->M, st->mit_p, st->mit_lambda,
+                                       mit_slot, s));
     StageArgs sa;
     int n_items = 0;
     uint64_t tag = 0;

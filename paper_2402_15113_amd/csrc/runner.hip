@@ -1,6 +1,7 @@
 // Pipelined executor of the stage.  The sample and node set of an iteration
-// depend on the event stream only, so they run a chunk of iterations ahead on
-// a second stream.  On the main stream each iteration is three launches: the
+// (and, with staleness mitigation on, the node set's neighbour sets) depend on
+// the event stream only, so they run a chunk of iterations ahead on a second
+// stream.  On the main stream each iteration is three launches: the
 // GRU; the staging of its write set fused with the node projections; the
 // attention fused with the gather of the next iteration's fetch (which needs
 // only the staging's commits and runs on the CUs the attention leaves free).
@@ -60,6 +61,10 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
         *lo = (i0 + k) * B;
         return (int32_t)std::min<int64_t>(B, g->E - *lo);
     };
+    // with mitigation on, the neighbour sets of each node set are built beside
+    // the sample, into mitigator slot 1 + (k % nsb)
+    if (st->mit)
+        TGM_TRY_STATUS(mitigate_reserve(st->mit, 1 + nsb));
     auto sample_chunk = [&](int64_t c) -> tgm_status_t {
         for (int64_t k = c * K; k < std::min(n, (c + 1) * K); ++k) {
             int64_t lo = 0;
@@ -68,6 +73,9 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             TGM_TRY_STATUS(tgm_sample_nodes(g, lo, b, nb, s.root, s.root_ts, s.nbr, s.eid, s.nts,
                                             s.cnt, s.nodes, s.n_nodes, cap, s.root_pos,
                                             s.nbr_pos, pre));
+            if (st->mit)
+                TGM_TRY_STATUS(mitigate_prep_launch(st->mit, g, lo, s.nodes, s.n_nodes, cap,
+                                                    (int32_t)(1 + k % nsb), pre));
         }
         TGM_HIP(hipEventRecord(ev.e[c & 1], pre));
         return TGM_OK;
@@ -98,7 +106,8 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
                 TGM_HIP(hipStreamWaitEvent(main, ev.e[(c + 1) & 1], 0));
             TGM_TRY_STATUS(compute_iteration(st, m, g, i0 + k, sb[k % nsb], *fb, cap, lo, b, nb,
                                              mem_new, new_mem_ts, winner, h,
-                                             more ? &sb[(k + 1) % nsb] : nullptr, main));
+                                             more ? &sb[(k + 1) % nsb] : nullptr,
+                                             (int32_t)(1 + k % nsb), main));
         }
         TGM_HIP(hipEventRecord(ev.e[2 + (c & 1)], main));
     }
