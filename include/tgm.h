@@ -308,9 +308,12 @@ tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t
  *   mem[v] = lambda mem[v] + (1 - lambda) mean_{u in Omega(v)} mem[u] for
  *            every stale v with Omega(v) non-empty (fp32, the sum in Omega's
  *            order); other rows are untouched.
- * The mitigator owns its work space: the gaps, neighbour sets, gamma, the
- * stale positions and Omega of the last call.  Calls on one mitigator must be
- * stream-ordered.
+ * The mitigator owns its work space: the neighbour sets, gamma, the stale
+ * positions and Omega of the last call.  Calls on one mitigator must be
+ * stream-ordered.  Under tgm_stage_run the neighbour sets of each iteration
+ * are built on the prefetch stream beside its sample (the first run with a
+ * mitigator set may allocate one set per sample buffer set, after a device
+ * synchronisation); the threshold and the blend run on the main stream.
  */
 /* max_nodes >= any cap passed later, at most 1 << 20; 1 <= nb <= 64 (the
  * neighbour sets' nb); 1 <= K <= 16.  Errors: TGM_EINVAL, TGM_ENOMEM,

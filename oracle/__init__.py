@@ -60,7 +60,7 @@ class _StepOut(C.Structure):
                 ("f_mail_ts", _f64p), ("f_ver", _i32p), ("s_new", _f64p),
                 ("new_mem_ts", _f64p), ("h", _f64p), ("winner", _i64p),
                 ("m_mem", _f64p), ("m_stale", _i32p), ("m_omega", _i32p), ("m_gamma", C.c_double),
-                ("m_n_stale", C.c_int32), ("m_pad", C.c_int32)]
+                ("m_n_stale", C.c_int32), ("m_pad", C.c_int32), ("x_mem", _f64p)]
 
 
 def lib():
@@ -207,6 +207,9 @@ class StepResult:
     m_stale: np.ndarray | None = None
     m_omega: np.ndarray | None = None
     m_gamma: float | None = None
+    # the exact memories of U: committed state plus every write set of
+    # iterations <= i-1 (what a fetch without staleness would read here)
+    x_mem: np.ndarray | None = None
 
 
 class Oracle:
@@ -274,7 +277,7 @@ class Oracle:
                     winner=np.empty(N, np.int64))
         if want == "all":
             arrs.update(f_mem=np.empty(N * M), f_mail=np.empty(N * D_m + 1),
-                        s_new=np.empty(N * M), h=np.empty(R * M))
+                        s_new=np.empty(N * M), h=np.empty(R * M), x_mem=np.empty(N * M))
         mit = self.mitigation
         if mit is not None:
             K = int(mit["K"])
@@ -302,7 +305,8 @@ class Oracle:
             m_mem=g("m_mem", nU * M, (nU, M)), m_stale=g("m_stale", o.m_n_stale),
             m_omega=(arrs["m_omega"][:o.m_n_stale * int(mit["K"])].reshape(-1, int(mit["K"]))
                      if mit is not None else None),
-            m_gamma=o.m_gamma if mit is not None else None)
+            m_gamma=o.m_gamma if mit is not None else None,
+            x_mem=g("x_mem", nU * M, (nU, M)))
 
     def flush(self):
         lib().orc_flush(self._h)

@@ -542,6 +542,11 @@ typedef struct {
     int32_t *m_stale, *m_omega;
     double m_gamma;
     int32_t m_n_stale, m_pad;
+    /* the exact memories of U [n_U x M]: the committed state with every write
+     * set of iterations <= i-1 applied, i.e. what a fetch without staleness
+     * would read at this point of the run (for the staleness error of Sec. 4.3
+     * and App. C.3) */
+    double *x_mem;
 } orc_step_out;
 
 static double *widen(const float *x, size_t n)
@@ -898,6 +903,16 @@ int orc_step(void *p, orc_step_out *o)
                 o->nbr_pos[k] = nbr[k] >= 0 ? pos[nbr[k]] : -1;
         if (o->f_mem) memcpy(o->f_mem, fm_read ? fm_read : fm, sizeof(double) * (size_t)nU * M);
         if (o->m_mem) memcpy(o->m_mem, fm, sizeof(double) * (size_t)nU * M);
+        if (o->x_mem)
+            for (int k = 0; k < nU; ++k) {
+                /* the newest queued write of the node, else the committed row */
+                const double *row = c->mem + (size_t)ids[k] * M;
+                for (int q = 0; q < c->nq && c->q[q].iter < i; ++q)   /* not W_i */
+                    for (int j = 0; j < c->q[q].n; ++j)
+                        if (c->q[q].node[j] == ids[k])
+                            row = c->q[q].mem + (size_t)j * M;
+                memcpy(o->x_mem + (size_t)k * M, row, sizeof(double) * M);
+            }
         o->m_gamma = gamma;
         o->m_n_stale = n_stale;
         if (o->f_mem_ts) memcpy(o->f_mem_ts, fmts, sizeof(double) * nU);
