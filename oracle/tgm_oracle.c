@@ -903,16 +903,18 @@ int orc_step(void *p, orc_step_out *o)
                 o->nbr_pos[k] = nbr[k] >= 0 ? pos[nbr[k]] : -1;
         if (o->f_mem) memcpy(o->f_mem, fm_read ? fm_read : fm, sizeof(double) * (size_t)nU * M);
         if (o->m_mem) memcpy(o->m_mem, fm, sizeof(double) * (size_t)nU * M);
-        if (o->x_mem)
-            for (int k = 0; k < nU; ++k) {
-                /* the newest queued write of the node, else the committed row */
-                const double *row = c->mem + (size_t)ids[k] * M;
-                for (int q = 0; q < c->nq && c->q[q].iter < i; ++q)   /* not W_i */
-                    for (int j = 0; j < c->q[q].n; ++j)
-                        if (c->q[q].node[j] == ids[k])
-                            row = c->q[q].mem + (size_t)j * M;
-                memcpy(o->x_mem + (size_t)k * M, row, sizeof(double) * M);
-            }
+        if (o->x_mem) {
+            /* the committed rows, then the queued write sets of iterations
+             * before i in order (a later write wins) */
+            for (int k = 0; k < nU; ++k)
+                memcpy(o->x_mem + (size_t)k * M, c->mem + (size_t)ids[k] * M,
+                       sizeof(double) * M);
+            for (int q = 0; q < c->nq && c->q[q].iter < i; ++q)   /* not W_i */
+                for (int j = 0; j < c->q[q].n; ++j)
+                    if (pos[c->q[q].node[j]] >= 0)
+                        memcpy(o->x_mem + (size_t)pos[c->q[q].node[j]] * M,
+                               c->q[q].mem + (size_t)j * M, sizeof(double) * M);
+        }
         o->m_gamma = gamma;
         o->m_n_stale = n_stale;
         if (o->f_mem_ts) memcpy(o->f_mem_ts, fmts, sizeof(double) * nU);
