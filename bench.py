@@ -97,13 +97,20 @@ class Schedule:
 
 
 def account(sched, W, K):
-    """Per-step sizes of the timed steps, read back from an untimed replay."""
+    """Per-step sizes of the timed steps, read back from an untimed replay on
+    the sequential path (one call per stage), and the per-kernel durations of
+    that replay's timed steps (HIP events)."""
     import torch
+    from paper_2402_15113_amd import tgm
     stage = sched.stage
     sched.restart()
     stage.want_winner = True
     rows = []
     for k in range(W + K):
+        if k == W:
+            torch.cuda.synchronize()
+            tgm.tgm_profile_reset()
+            tgm.tgm_profile_enable(True)
         sched.run(k, 1, pipelined=False)
         if k >= W:
             torch.cuda.synchronize()
@@ -113,8 +120,10 @@ def account(sched, W, K):
             rows.append(dict(b=b, R=R, slots=int(stage.cnt[:R].sum().item()), n_U=n,
                              n_mail=int((stage.f_ver[:n] >= 0).sum().item()),
                              n_win=int((stage.winner[:n] >= 0).sum().item())))
+    tgm.tgm_profile_enable(False)
+    seq = tgm.tgm_profile_read()
     stage.want_winner = False
-    return rows
+    return rows, seq
 
 
 def window_setup(name, first, L, w, mitigation=None):
@@ -412,8 +421,8 @@ def main():
             base = name.split("<")[0]   # template instances count as their kernel
             n0, m0 = prof.get(base, (0, 0.0))
             prof[base] = (n0 + launches, m0 + ms)
-        # pass 3: algorithmic work per launch
-        rows = account(sched, W, K)
+        # pass 3: algorithmic work per launch, and the sequential stage times
+        rows, seq = account(sched, W, K)
         work = work_model(wl, rows)
         kernels = {}
         for name, (launches, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
@@ -441,6 +450,11 @@ def main():
                            "algorithmic_per_launch": work.get(dom),
                            "avg_launch_us": dk["avg_us"]}
         out["kernels"] = kernels
+        # the minimal staleness (Sec. 3.2) for the stage times measured on the
+        # sequential replay (the paper profiles a few iterations, App. D.1)
+        from paper_2402_15113_amd.stage import minimal_staleness, stage_durations_us
+        out["staleness_bound"] = dict(minimal_staleness(stage_durations_us(seq, K)),
+                                      s_config=wl.s)
         out["profiled_ms_per_step"] = tp * 1e3 / K
         out["per_step"] = {k: sum(r[k] for r in rows) / len(rows)
                            for k in ("R", "slots", "n_U", "n_mail", "n_win")}

@@ -341,6 +341,31 @@ tgm_status_t tgm_state_set_mitigation(tgm_state_t st, tgm_mitigator_t mt, double
                                       float lambda);
 
 /* ------------------------------------------------------------------------
+ * Minimal-staleness bound (Sec. 3.2, Eq. 3 and Eq. 4, constraints C1-C3).
+ * Host code; touches no device.
+ *
+ * tau [5]: the durations of the stages 1 sample, 2 feature fetch, 3 memory
+ * fetch, 4 compute, 5 memory update (any time unit, each >= 0).  For
+ * iterations i = 1..n the start times b_i^(j) and end times
+ * e_i^(j) = b_i^(j) + tau^(j) follow Eq. 3: b_i^(1) = e_{i-1}^(1);
+ * b_i^(2) = max(e_i^(1), e_{i-1}^(3)); b_i^(j) = max(e_i^(j-1), e_{i-1}^(j))
+ * for j = 3..5; every stage of "iteration 0" ends at 0.  Then k_i is the
+ * smallest k with 1 <= k < min(i, k_max) such that the memory fetch, started
+ * once the update of iteration i - k is done (C1: at
+ * max(b_i^(3), e_{i-k}^(5))), ends by b_i^(4) (C2:
+ * e_{i-k}^(5) <= b_i^(4) - tau^(3)).  An empty range (i <= 1 or k_max <= 1)
+ * is a warm-up iteration: k_i = 0, no wait.  If no k in the range meets C2,
+ * k_i = min(i, k_max) - 1 and the fetch stalls the compute stage.
+ *
+ * Outputs (host arrays, iteration i at index i - 1): k [n]; fetch_start [n],
+ * stall [n] (the compute stage's delay, 0 when stall-free), b [n x 5] and
+ * e [n x 5] (stage j at column j - 1) may be NULL.  Errors: TGM_EINVAL (null
+ * tau or k, n < 0, k_max < 1, a negative or NaN duration).
+ */
+tgm_status_t tgm_min_staleness(const double *tau, int64_t n, int32_t k_max, int32_t *k,
+                               double *fetch_start, double *stall, double *b, double *e);
+
+/* ------------------------------------------------------------------------
  * Per-kernel timing.  When enabled, every kernel the library launches is
  * bracketed by two HIP events recorded on its own stream; tgm_profile_get
  * synchronises those events and reports, per kernel name, the number of

@@ -216,3 +216,40 @@ def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None)
     return Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, wl.efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
                  nb=wl.nb, B=wl.B, s=wl.s if s is None else s, device=device, stream=stream,
                  mitigation=mitigation)
+
+
+# ------------------------------------------------------- staleness bound
+# The paper's five stages (Sec. 3.2) as this library's kernels on the
+# sequential path (one call per stage).  Edge features are read inside the
+# attention kernel, so the feature fetch has no kernel of its own; the
+# mitigation belongs to the memory fetch (Sec. 4.3).
+STAGE_KERNELS = {1: ("k_sample_batch", "k_ns_mark", "k_ns_pos"), 2: (),
+                 3: ("k_gather_state", "k_mit_prep", "k_mit_select", "k_mit_omega"),
+                 4: ("k_gru", "k_node_proj", "k_attn_fold", "k_attn"),
+                 5: ("k_stage", "k_commit")}
+
+
+def stage_durations_us(profile: dict, iters: int) -> list:
+    """Per-iteration durations (µs) of the five stages from a per-kernel
+    profile ({kernel: (launches, total ms)}, template instances folded into
+    their kernel) taken over `iters` sequential steps."""
+    folded = {}
+    for name, (launches, ms) in profile.items():
+        base = name.split("<")[0]
+        n0, m0 = folded.get(base, (0, 0.0))
+        folded[base] = (n0 + launches, m0 + ms)
+    return [sum(folded.get(k, (0, 0.0))[1] for k in STAGE_KERNELS[j]) * 1e3 / iters
+            for j in range(1, 6)]
+
+
+def minimal_staleness(tau_us, k_max: int = 16, n: int = 64) -> dict:
+    """The minimal staleness of Sec. 3.2 (Eq. 3-4, C1-C3) for the stage
+    durations tau_us, by the library's host solver, in steady state (the last
+    of n iterations).  The paper's k corresponds to s = k - 1 here: a fetch at
+    iteration i reads the write sets of iterations up to i - 1 - s."""
+    k, _, stall, _, _ = tgm.tgm_min_staleness(list(tau_us), n, k_max)
+    return {"tau_us": dict(zip(("sample", "feature_fetch", "memory_fetch", "compute",
+                                "memory_update"), (float(t) for t in tau_us))),
+            "k_min": int(k[-1]), "s_equivalent": int(k[-1]) - 1,
+            "stall_free": bool(stall[-1] == 0.0), "k_max": k_max}
+

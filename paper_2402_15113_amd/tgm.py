@@ -24,7 +24,7 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_
            "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
            "tgm_stage_run", "tgm_mitigator_create", "tgm_mitigator_destroy", "tgm_mitigate",
-           "tgm_mitigator_read", "tgm_state_set_mitigation",
+           "tgm_mitigator_read", "tgm_state_set_mitigation", "tgm_min_staleness",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
 
@@ -103,6 +103,7 @@ def lib():
             "tgm_mitigate": [V, V, I64, P, P, I32, P, P, I32, C.c_double, C.c_float, V],
             "tgm_mitigator_read": [V, P, P, P, P, V],
             "tgm_state_set_mitigation": [V, V, C.c_double, C.c_float],
+            "tgm_min_staleness": [P, I64, I32, P, P, P, P, P],
         }
         sig["tgm_profile_enable"] = [I32]
         sig["tgm_profile_reset"] = []
@@ -291,6 +292,24 @@ def tgm_mitigator_read(mt, gamma, n_stale, stale, omega, stream=None):
 def tgm_state_set_mitigation(st, mt, p=1.0, lam=1.0):
     _check("tgm_state_set_mitigation", lib().tgm_state_set_mitigation(st, mt, float(p),
                                                                       float(lam)))
+
+
+# ------------------------------------------------------------- staleness bound
+def tgm_min_staleness(tau, n, k_max):
+    """Host solver of the minimal-staleness bound: returns (k, fetch_start,
+    stall, b, e) for iterations 1..n as numpy arrays (b, e: [n x 5])."""
+    import numpy as np
+    t = np.ascontiguousarray(tau, dtype=np.float64)
+    if t.shape != (5,):
+        raise ValueError("tau holds the five stage durations")
+    n = int(n)
+    k = np.zeros(max(n, 1), np.int32)
+    fs, st = np.zeros(max(n, 1)), np.zeros(max(n, 1))
+    b, e = np.zeros((max(n, 1), 5)), np.zeros((max(n, 1), 5))
+    _check("tgm_min_staleness", lib().tgm_min_staleness(
+        t.ctypes.data, n, int(k_max), k.ctypes.data, fs.ctypes.data, st.ctypes.data,
+        b.ctypes.data, e.ctypes.data))
+    return k[:n], fs[:n], st[:n], b[:n], e[:n]
 
 
 # ------------------------------------------------------------------ model
