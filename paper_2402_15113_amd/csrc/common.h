@@ -299,6 +299,48 @@ __device__ __forceinline__ void wave_copy_row(float *__restrict__ dst,
     }
 }
 
+// Two rows copied by one wavefront with every load issued before the first
+// store (lane l holds elements l + 64 u; clamped indices keep the loads
+// unconditional and in range; n1 >= 1, n2 >= 0).  The rows must fit U1 and
+// U2 chunks of 64 elements.
+template <int U1, int U2>
+__device__ __forceinline__ void copy2_rows_regs(float *__restrict__ d1,
+                                                const float *__restrict__ s1, int n1,
+                                                float *__restrict__ d2,
+                                                const float *__restrict__ s2, int n2, int lane)
+{
+    float a[U1], b[U2];
+#pragma unroll
+    for (int u = 0; u < U1; ++u)
+        a[u] = s1[min(lane + kWave * u, n1 - 1)];
+#pragma unroll
+    for (int u = 0; u < U2; ++u)
+        b[u] = n2 > 0 ? s2[min(lane + kWave * u, n2 - 1)] : 0.f;
+#pragma unroll
+    for (int u = 0; u < U1; ++u)
+        if (lane + kWave * u < n1)
+            d1[lane + kWave * u] = a[u];
+#pragma unroll
+    for (int u = 0; u < U2; ++u)
+        if (lane + kWave * u < n2)
+            d2[lane + kWave * u] = b[u];
+}
+
+// Copies rows (s1 -> d1, n1 floats) and (s2 -> d2, n2 floats) with one
+// wavefront: loads first when the rows are short enough, else row by row.
+__device__ __forceinline__ void wave_copy_2rows(float *d1, const float *s1, int n1, float *d2,
+                                                const float *s2, int n2, int lane)
+{
+    if (n1 <= 2 * kWave && n2 <= 8 * kWave) {
+        copy2_rows_regs<2, 8>(d1, s1, n1, d2, s2, n2, lane);
+    } else if (n1 <= 4 * kWave && n2 <= 16 * kWave) {
+        copy2_rows_regs<4, 16>(d1, s1, n1, d2, s2, n2, lane);
+    } else {
+        wave_copy_row(d1, s1, n1, lane);
+        wave_copy_row(d2, s2, n2, lane);
+    }
+}
+
 // One fetch's gather: rows nodes[0 .. min(*n_nodes, cap)) of the committed
 // tables into the caller's buffers (see tgm_fetch_memory).
 struct GatherPlan {
@@ -312,16 +354,131 @@ struct GatherPlan {
     int32_t *o_ver = nullptr;
 };
 
-// Row p of a gather, copied by one wavefront.
-__device__ __forceinline__ void gather_row(const GatherPlan &g, int p, int lane)
+// Row p of a gather, copied by one wavefront.  Every load of the node's two
+// rows and three scalars is issued before the first store: one wavefront
+// keeps up to 2.5 KB in flight, which the HBM latency needs (with a load and
+// its store per round trip, a node's rows took several round trips).  Lane l
+// holds elements l + 64 u of a row (4-byte loads, 256 contiguous bytes per
+// instruction); indices past the row are clamped to its last element, so
+// every load is unconditional and in range.  UM and UD bound the 64-element
+// chunks of the two rows.
+template <int UM, int UD>
+__device__ __forceinline__ void gather_row_regs(const GatherPlan &g, int p, int lane)
 {
     const int32_t v = g.nodes[p];
-    wave_copy_row(g.o_mem + (int64_t)p * g.M, g.mem + (int64_t)v * g.M, g.M, lane);
-    wave_copy_row(g.o_mail + (int64_t)p * g.D_m, g.mail + (int64_t)v * g.D_m, g.D_m, lane);
+    const int M = g.M, D = g.D_m;
+    const float *sm = g.mem + (int64_t)v * M, *sd = g.mail + (int64_t)v * D;
+    float a[UM], b[UD];
+#pragma unroll
+    for (int u = 0; u < UM; ++u)
+        a[u] = sm[min(lane + kWave * u, M - 1)];
+#pragma unroll
+    for (int u = 0; u < UD; ++u)
+        b[u] = D > 0 ? sd[min(lane + kWave * u, D - 1)] : 0.f;
+    double mts = 0.0, lts = 0.0;
+    int32_t ver = 0;
     if (lane == 0) {
-        g.o_mem_ts[p] = g.mem_ts[v];
-        g.o_mail_ts[p] = g.mail_ts[v];
-        g.o_ver[p] = g.ver[v];
+        mts = g.mem_ts[v];
+        lts = g.mail_ts[v];
+        ver = g.ver[v];
+    }
+    float *dm = g.o_mem + (int64_t)p * M, *dd = g.o_mail + (int64_t)p * D;
+#pragma unroll
+    for (int u = 0; u < UM; ++u)
+        if (lane + kWave * u < M)
+            dm[lane + kWave * u] = a[u];
+#pragma unroll
+    for (int u = 0; u < UD; ++u)
+        if (lane + kWave * u < D)
+            dd[lane + kWave * u] = b[u];
+    if (lane == 0) {
+        g.o_mem_ts[p] = mts;
+        g.o_mail_ts[p] = lts;
+        g.o_ver[p] = ver;
+    }
+}
+
+__device__ __forceinline__ void gather_row(const GatherPlan &g, int p, int lane);
+
+// Rows p0 .. p0 + NPW - 1 (those below n) of a gather, copied by one
+// wavefront: lane j < NPW loads node id j, then every row load of the NPW
+// nodes is issued (up to 10 KB in flight) before the first store.  Positions
+// past n reuse the last node's rows for their (discarded) loads.
+constexpr int kGatherNPW = 4;   // nodes per wavefront
+
+template <int UM, int UD>
+__device__ __forceinline__ void gather_rows_regs(const GatherPlan &g, int p0, int n, int lane)
+{
+    constexpr int NPW = kGatherNPW;
+    const int M = g.M, D = g.D_m;
+    const int32_t vid = g.nodes[min(p0 + (lane < NPW ? lane : 0), n - 1)];
+    float a[NPW][UM], b[NPW][UD];
+#pragma unroll
+    for (int j = 0; j < NPW; ++j) {
+        const int32_t v = __builtin_amdgcn_readlane(vid, j);
+        const float *sm = g.mem + (int64_t)v * M, *sd = g.mail + (int64_t)v * D;
+#pragma unroll
+        for (int u = 0; u < UM; ++u)
+            a[j][u] = sm[min(lane + kWave * u, M - 1)];
+#pragma unroll
+        for (int u = 0; u < UD; ++u)
+            b[j][u] = D > 0 ? sd[min(lane + kWave * u, D - 1)] : 0.f;
+    }
+    double mts = 0.0, lts = 0.0;
+    int32_t ver = 0;
+    if (lane < NPW) {
+        mts = g.mem_ts[vid];
+        lts = g.mail_ts[vid];
+        ver = g.ver[vid];
+    }
+#pragma unroll
+    for (int j = 0; j < NPW; ++j) {
+        const int p = p0 + j;
+        if (p >= n)
+            break;   // uniform
+        float *dm = g.o_mem + (int64_t)p * M, *dd = g.o_mail + (int64_t)p * D;
+#pragma unroll
+        for (int u = 0; u < UM; ++u)
+            if (lane + kWave * u < M)
+                dm[lane + kWave * u] = a[j][u];
+#pragma unroll
+        for (int u = 0; u < UD; ++u)
+            if (lane + kWave * u < D)
+                dd[lane + kWave * u] = b[j][u];
+    }
+    if (lane < NPW && p0 + lane < n) {
+        g.o_mem_ts[p0 + lane] = mts;
+        g.o_mail_ts[p0 + lane] = lts;
+        g.o_ver[p0 + lane] = ver;
+    }
+}
+
+// Rows p0 .. p0 + kGatherNPW - 1 (those below n) of a gather by one wavefront.
+__device__ __forceinline__ void gather_rows(const GatherPlan &g, int p0, int n, int lane)
+{
+    if (g.M <= 2 * kWave && g.D_m <= 8 * kWave) {
+        gather_rows_regs<2, 8>(g, p0, n, lane);
+    } else {
+        for (int j = 0; j < kGatherNPW && p0 + j < n; ++j)
+            gather_row(g, p0 + j, lane);
+    }
+}
+
+__device__ __forceinline__ void gather_row(const GatherPlan &g, int p, int lane)
+{
+    if (g.M <= 2 * kWave && g.D_m <= 8 * kWave) {
+        gather_row_regs<2, 8>(g, p, lane);
+    } else if (g.M <= 4 * kWave && g.D_m <= 16 * kWave) {
+        gather_row_regs<4, 16>(g, p, lane);
+    } else {
+        const int32_t v = g.nodes[p];
+        wave_copy_row(g.o_mem + (int64_t)p * g.M, g.mem + (int64_t)v * g.M, g.M, lane);
+        wave_copy_row(g.o_mail + (int64_t)p * g.D_m, g.mail + (int64_t)v * g.D_m, g.D_m, lane);
+        if (lane == 0) {
+            g.o_mem_ts[p] = g.mem_ts[v];
+            g.o_mail_ts[p] = g.mail_ts[v];
+            g.o_ver[p] = g.ver[v];
+        }
     }
 }
 

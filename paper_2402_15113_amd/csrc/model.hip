@@ -383,11 +383,16 @@ __device__ __forceinline__ void stage_wave(const StageArgs &g, int c, int lane)
         if (k >= g.n_commit || !g.c_flag[k])
             return;
         const int32_t v = g.c_node[k];
-        wave_copy_row(g.mem + (int64_t)v * M, g.c_mem + (int64_t)k * M, M, lane);
-        wave_copy_row(g.mail + (int64_t)v * D_m, g.c_mail + (int64_t)k * D_m, D_m, lane);
+        double mts = 0.0, lts = 0.0;
         if (lane == 0) {
-            g.t_mem_ts[v] = g.c_mem_ts[k];
-            g.t_mail_ts[v] = g.c_mail_ts[k];
+            mts = g.c_mem_ts[k];
+            lts = g.c_mail_ts[k];
+        }
+        wave_copy_2rows(g.mem + (int64_t)v * M, g.c_mem + (int64_t)k * M, M,
+                        g.mail + (int64_t)v * D_m, g.c_mail + (int64_t)k * D_m, D_m, lane);
+        if (lane == 0) {
+            g.t_mem_ts[v] = mts;
+            g.t_mail_ts[v] = lts;
             g.t_ver[v] = (int32_t)g.c_iter;
         }
         return;
@@ -406,11 +411,37 @@ __device__ __forceinline__ void stage_wave(const StageArgs &g, int c, int lane)
     const float *sp = g.mem_new + (int64_t)p * M;
     float *dm = g.direct ? g.mem + (int64_t)w * M : g.r_mem + (int64_t)c * M;
     float *ml = g.direct ? g.mail + (int64_t)w * D_m : g.r_mail + (int64_t)c * D_m;
-    wave_copy_row(dm, sp, M, lane);
-    wave_copy_row(ml, sp, M, lane);
-    wave_copy_row(ml + M, g.mem_new + (int64_t)q * M, M, lane);
-    if (D_e > 0)
-        wave_copy_row(ml + 2 * M, g.efeat + e * D_e, D_e, lane);
+    if (M <= 2 * kWave && D_e <= 4 * kWave) {
+        // every load before the first store: s'_p, s'_q and the feature row
+        // (lane l holds elements l + 64 u, clamped indices)
+        const float *sq = g.mem_new + (int64_t)q * M, *fe = g.efeat + e * D_e;
+        float a[2], bq[2], f[4];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            a[u] = sp[min(lane + kWave * u, M - 1)];
+            bq[u] = sq[min(lane + kWave * u, M - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            f[u] = D_e > 0 ? fe[min(lane + kWave * u, D_e - 1)] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            if (lane + kWave * u < M) {
+                dm[lane + kWave * u] = a[u];
+                ml[lane + kWave * u] = a[u];
+                ml[M + lane + kWave * u] = bq[u];
+            }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (lane + kWave * u < D_e)
+                ml[2 * M + lane + kWave * u] = f[u];
+    } else {
+        wave_copy_row(dm, sp, M, lane);
+        wave_copy_row(ml, sp, M, lane);
+        wave_copy_row(ml + M, g.mem_new + (int64_t)q * M, M, lane);
+        if (D_e > 0)
+            wave_copy_row(ml + 2 * M, g.efeat + e * D_e, D_e, lane);
+    }
     if (lane == 0) {
         const double mts = g.ver[p] >= 0 ? g.mail_ts[p] : g.mem_ts[p];
         if (g.direct) {
@@ -1125,9 +1156,10 @@ __global__ __launch_bounds__(512) void k_attn_gather(AttnArgs g, int n_attn, Gat
     }
     const int waves = blockDim.x >> 6;
     const int n = min(*gp.n_nodes, gp.cap);
-    const int stride = ((int)gridDim.x - n_attn) * waves;
-    for (int p = ((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6); p < n; p += stride)
-        gather_row(gp, p, threadIdx.x & 63);
+    const int stride = ((int)gridDim.x - n_attn) * waves * kGatherNPW;
+    for (int p = (((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
+         p < n; p += stride)
+        gather_rows(gp, p, n, threadIdx.x & 63);
 }
 
 // ---------------------------------------------------------------------------
@@ -1635,9 +1667,10 @@ __global__ __launch_bounds__(512) void k_attn_fold_gather(AttnArgs g, int n_attn
     }
     const int waves = blockDim.x >> 6;
     const int nn = min(*gp.n_nodes, gp.cap);
-    const int stride = ((int)gridDim.x - n_attn) * waves;
-    for (int p = ((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6); p < nn; p += stride)
-        gather_row(gp, p, threadIdx.x & 63);
+    const int stride = ((int)gridDim.x - n_attn) * waves * kGatherNPW;
+    for (int p = (((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
+         p < nn; p += stride)
+        gather_rows(gp, p, nn, threadIdx.x & 63);
 }
 
 // q bias folded at creation: c_q = W_q^t phi(0) + b_q with phi(0)_d = cos(beta_d).

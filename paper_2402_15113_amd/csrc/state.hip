@@ -42,22 +42,29 @@ __global__ __launch_bounds__(256) void k_commit(
     if (c >= n_cand || !flag[c])
         return;
     const int32_t v = node[c];
-    wave_copy_row(mem + (int64_t)v * M, r_mem + (int64_t)c * M, M, lane);
-    wave_copy_row(mail + (int64_t)v * D_m, r_mail + (int64_t)c * D_m, D_m, lane);
+    double mts = 0.0, lts = 0.0;
     if (lane == 0) {
-        mem_ts[v] = r_mem_ts[c];
-        mail_ts[v] = r_mail_ts[c];
+        mts = r_mem_ts[c];
+        lts = r_mail_ts[c];
+    }
+    wave_copy_2rows(mem + (int64_t)v * M, r_mem + (int64_t)c * M, M,
+                    mail + (int64_t)v * D_m, r_mail + (int64_t)c * D_m, D_m, lane);
+    if (lane == 0) {
+        mem_ts[v] = mts;
+        mail_ts[v] = lts;
         ver[v] = (int32_t)iter;
     }
 }
 
-// Gather the committed rows of the node set: one wavefront per node.
+// Gather the committed rows of the node set: one wavefront per kGatherNPW
+// consecutive nodes.
 __global__ __launch_bounds__(256) void k_gather_state(GatherPlan g)
 {
-    const int p = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
-    if (p >= min(*g.n_nodes, g.cap))
+    const int p0 = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6) * kGatherNPW;
+    const int n = min(*g.n_nodes, g.cap);
+    if (p0 >= n)
         return;
-    gather_row(g, p, threadIdx.x & 63);
+    gather_rows(g, p0, n, threadIdx.x & 63);
 }
 
 tgm_status_t commit_through(tgm_state *st, int64_t target, hipStream_t s)
@@ -238,7 +245,7 @@ tgm_status_t tgm::launch_gather(const GatherPlan &plan, hipStream_t s)
 {
     if (plan.cap == 0)
         return TGM_OK;
-    TGM_LAUNCH(k_gather_state, dim3(cdiv(plan.cap, 4)), dim3(256), 0, s, plan);
+    TGM_LAUNCH(k_gather_state, dim3(cdiv(plan.cap, 4 * kGatherNPW)), dim3(256), 0, s, plan);
     return TGM_OK;
 }
 
