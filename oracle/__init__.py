@@ -48,7 +48,10 @@ class _Desc(C.Structure):
                 ("W_ih", _f32p), ("W_hh", _f32p), ("b_ih", _f32p), ("b_hh", _f32p),
                 ("omega", _f64p), ("beta", _f64p),
                 ("W_q", _f32p), ("b_q", _f32p), ("W_k", _f32p), ("b_k", _f32p),
-                ("W_v", _f32p), ("b_v", _f32p), ("W_o", _f32p), ("b_o", _f32p)]
+                ("W_v", _f32p), ("b_v", _f32p), ("W_o", _f32p), ("b_o", _f32p),
+                ("kind", C.c_int), ("w_t", _f32p)]
+
+KINDS = {"tgn": 0, "jodie": 1}
 
 
 class _StepOut(C.Structure):
@@ -89,6 +92,8 @@ def lib():
         L.orc_step.restype = C.c_int
         L.orc_set_mitigation.argtypes = [C.c_void_p, C.c_int, C.c_double, C.c_double, C.c_int]
         L.orc_set_mitigation.restype = C.c_int
+        L.orc_rnn_cell.argtypes = [C.c_int, C.c_int] + [_f64p] * 7
+        L.orc_time_projection.argtypes = [C.c_int, _f64p, _f64p, C.c_double, C.c_double, _f64p]
         L.orc_quantile_nearest_rank.argtypes = [C.c_int, _f64p, C.c_double]
         L.orc_quantile_nearest_rank.restype = C.c_double
         _lib = L
@@ -115,6 +120,25 @@ def time_encode(omega, beta, dt) -> np.ndarray:
     out = np.empty(len(omega))
     lib().orc_time_encode(len(omega), _p(omega, _f64p), _p(beta, _f64p), float(dt),
                           _p(out, _f64p))
+    return out
+
+
+def rnn_cell(W_ih, W_hh, b_ih, b_hh, x, h) -> np.ndarray:
+    W_ih, W_hh, b_ih, b_hh, x, h = map(_f64, (W_ih, W_hh, b_ih, b_hh, x, h))
+    M = h.shape[0]
+    D_x = x.shape[0]
+    assert W_ih.shape == (M, D_x) and W_hh.shape == (M, M)
+    out = np.empty(M)
+    lib().orc_rnn_cell(M, D_x, *(_p(a, _f64p) for a in (W_ih, W_hh, b_ih, b_hh, x, h)),
+                       _p(out, _f64p))
+    return out
+
+
+def time_projection(w_t, s, ts, tq) -> np.ndarray:
+    w_t, s = _f64(w_t), _f64(s)
+    out = np.empty(len(s))
+    lib().orc_time_projection(len(s), _p(w_t, _f64p), _p(s, _f64p), float(ts), float(tq),
+                              _p(out, _f64p))
     return out
 
 
@@ -239,8 +263,11 @@ class Oracle:
         d.D_e, d.M, d.D_t, d.H, d.nb, d.B, d.s = (wl.D_e, wl.M, wl.D_t, wl.H, wl.nb, wl.B,
                                                   self.s)
         for name in ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v",
-                     "W_o", "b_o"):
-            setattr(d, name, _p(keep(getattr(w, name), np.float32), _f32p))
+                     "W_o", "b_o", "w_t"):
+            a = getattr(w, name, None)
+            setattr(d, name, _p(keep(a, np.float32), _f32p) if a is not None else
+                    C.cast(None, _f32p))
+        d.kind = KINDS[getattr(w, "kind", "tgn")]
         d.omega = _p(keep(w.omega, np.float64), _f64p)
         d.beta = _p(keep(w.beta, np.float64), _f64p)
         self._desc = d

@@ -23,10 +23,12 @@
  *      p-quantile of the batch's gaps: a blend with the mean memory of the
  *      most similar (common neighbours) fresher nodes;
  *   4. memory update s' = GRU(mail || phi(mail_ts - mem_ts), mem) for nodes
- *      with mail (mem() of Eq. 1; Delta-t as defined under Eq. 1);
+ *      with mail (mem() of Eq. 1; Delta-t as defined under Eq. 1); for the
+ *      JODIE model family an RNN cell takes the GRU's place;
  *   5. embedding h = emb(s'_v, s'_u | u in N(v)): one layer of multi-head
  *      scaled dot-product attention with a cosine time encoding (emb() of
- *      Eq. 1, "a single layer GAT");
+ *      Eq. 1, "a single layer GAT"); for JODIE the time projection
+ *      h = s'_v * (1 + w_t (t - ts'_v)) of the node's memory instead;
  *   6. messages m = msg(s'_v, s'_u, y_uv(t)) as identity concatenation (msg()
  *      of Eq. 1);
  *   7. latest-message reduce: one message per node, the one with the largest
@@ -46,6 +48,10 @@
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
 #define ORC_EEND (-2)
+
+/* model families (Sec. 5 trains TGN, JODIE and APAN) */
+#define ORC_TGN 0
+#define ORC_JODIE 1
 
 /* ------------------------------------------------------------------------- */
 /* Time encoding: phi(dt)_d = cos(omega_d * dt + beta_d), the cosine functional
@@ -95,6 +101,37 @@ void orc_gru_cell(int M, int D_x, const double *W_ih, const double *W_hh,
         double n = tanh(in_ + r * hn);
         out[j] = (1.0 - z) * n + z * h[j];
     }
+}
+
+/* JODIE's memory updater: an RNN cell (Elman) on the same input as the GRU,
+ *   h' = tanh(W_ih x + b_ih + W_hh h + b_hh),  W_ih [M x D_x], W_hh [M x M].
+ * JODIE (Kumar et al. 2019) updates a node from its interactions with two
+ * mutually recursive RNNs; the recursion runs through the message, which holds
+ * the other endpoint's memory. */
+void orc_rnn_cell(int M, int D_x, const double *W_ih, const double *W_hh,
+                  const double *b_ih, const double *b_hh,
+                  const double *x, const double *h, double *out)
+{
+    for (int j = 0; j < M; ++j) {
+        double a = b_ih[j], u = b_hh[j];
+        const double *w = W_ih + (size_t)j * D_x;
+        for (int k = 0; k < D_x; ++k)
+            a += w[k] * x[k];
+        const double *v = W_hh + (size_t)j * M;
+        for (int k = 0; k < M; ++k)
+            u += v[k] * h[k];
+        out[j] = tanh(a + u);
+    }
+}
+
+/* JODIE's embedding, the time projection of a node's memory to the query
+ * time tq: h = s * (1 + w_t * (tq - ts)), ts the memory's time. */
+void orc_time_projection(int M, const double *w_t, const double *s, double ts, double tq,
+                         double *out)
+{
+    const double d = tq - ts;
+    for (int j = 0; j < M; ++j)
+        out[j] = s[j] * (1.0 + w_t[j] * d);
 }
 
 /* y[rows] = W[rows x cols] * x[cols] + b[rows] */
@@ -506,6 +543,9 @@ typedef struct {
     /* staleness mitigation (off unless orc_set_mitigation enables it) */
     int mit_on, mit_K;
     double mit_p, mit_lambda;
+    /* model family and JODIE's projection vector */
+    int kind;
+    double *w_t;
 } orc_ctx;
 
 typedef struct {
@@ -518,6 +558,10 @@ typedef struct {
     const float *W_ih, *W_hh, *b_ih, *b_hh;
     const double *omega, *beta;
     const float *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+    /* ORC_TGN (the fields above) or ORC_JODIE: W_ih [M x D_x], W_hh [M x M],
+     * b_ih, b_hh [M], w_t [M]; the attention weights are not read */
+    int kind;
+    const float *w_t;
 } orc_desc;
 
 /* Per-iteration outputs; every pointer may be NULL.  Capacities: R = 3B roots,
@@ -568,7 +612,8 @@ static double *copyd(const double *x, size_t n)
 void *orc_create(const orc_desc *d)
 {
     if (!d || d->N <= 0 || d->E < 0 || d->M <= 0 || d->H <= 0 || d->M % d->H != 0 ||
-        d->nb < 0 || d->B <= 0 || d->s < 0 || d->D_t < 0 || d->D_e < 0)
+        d->nb < 0 || d->B <= 0 || d->s < 0 || d->D_t < 0 || d->D_e < 0 ||
+        (d->kind != ORC_TGN && d->kind != ORC_JODIE) || (d->kind == ORC_JODIE && !d->w_t))
         return NULL;
     orc_ctx *c = (orc_ctx *)calloc(1, sizeof(orc_ctx));
     c->N = d->N; c->E = d->E;
@@ -578,20 +623,26 @@ void *orc_create(const orc_desc *d)
     c->D_m = 2 * d->M + d->D_e;
     c->D_x = c->D_m + d->D_t;
     const int M = c->M, D_x = c->D_x, D_t = c->D_t, D_e = c->D_e;
-    c->W_ih = widen(d->W_ih, (size_t)3 * M * D_x);
-    c->W_hh = widen(d->W_hh, (size_t)3 * M * M);
-    c->b_ih = widen(d->b_ih, (size_t)3 * M);
-    c->b_hh = widen(d->b_hh, (size_t)3 * M);
+    c->kind = d->kind;
+    const int G = c->kind == ORC_JODIE ? 1 : 3;   /* gate row blocks of the updater */
+    c->W_ih = widen(d->W_ih, (size_t)G * M * D_x);
+    c->W_hh = widen(d->W_hh, (size_t)G * M * M);
+    c->b_ih = widen(d->b_ih, (size_t)G * M);
+    c->b_hh = widen(d->b_hh, (size_t)G * M);
     c->omega = copyd(d->omega, (size_t)D_t);
     c->beta = copyd(d->beta, (size_t)D_t);
-    c->W_q = widen(d->W_q, (size_t)M * (M + D_t));
-    c->b_q = widen(d->b_q, (size_t)M);
-    c->W_k = widen(d->W_k, (size_t)M * (M + D_e + D_t));
-    c->b_k = widen(d->b_k, (size_t)M);
-    c->W_v = widen(d->W_v, (size_t)M * (M + D_e + D_t));
-    c->b_v = widen(d->b_v, (size_t)M);
-    c->W_o = widen(d->W_o, (size_t)M * (2 * M));
-    c->b_o = widen(d->b_o, (size_t)M);
+    if (c->kind == ORC_TGN) {
+        c->W_q = widen(d->W_q, (size_t)M * (M + D_t));
+        c->b_q = widen(d->b_q, (size_t)M);
+        c->W_k = widen(d->W_k, (size_t)M * (M + D_e + D_t));
+        c->b_k = widen(d->b_k, (size_t)M);
+        c->W_v = widen(d->W_v, (size_t)M * (M + D_e + D_t));
+        c->b_v = widen(d->b_v, (size_t)M);
+        c->W_o = widen(d->W_o, (size_t)M * (2 * M));
+        c->b_o = widen(d->b_o, (size_t)M);
+    } else {
+        c->w_t = widen(d->w_t, (size_t)M);
+    }
     if (build_adj(&c->adj, c->N, c->E, c->src, c->dst) != ORC_OK)
         return NULL;
     c->mem = (double *)calloc((size_t)c->N * M, sizeof(double));
@@ -619,7 +670,7 @@ void orc_destroy(void *p)
         return;
     free(c->W_ih); free(c->W_hh); free(c->b_ih); free(c->b_hh); free(c->omega); free(c->beta);
     free(c->W_q); free(c->b_q); free(c->W_k); free(c->b_k); free(c->W_v); free(c->b_v);
-    free(c->W_o); free(c->b_o);
+    free(c->W_o); free(c->b_o); free(c->w_t);
     free_adj(&c->adj);
     free(c->mem); free(c->mem_ts); free(c->mail); free(c->mail_ts); free(c->ver);
     for (int k = 0; k < c->nq; ++k)
@@ -794,8 +845,12 @@ int orc_step(void *p, orc_step_out *o)
             double *x = (double *)malloc(sizeof(double) * D_x);
             memcpy(x, fl + (size_t)k * D_m, sizeof(double) * D_m);
             orc_time_encode(D_t, c->omega, c->beta, flts[k] - fmts[k], x + D_m);
-            orc_gru_cell(M, D_x, c->W_ih, c->W_hh, c->b_ih, c->b_hh, x, fm + (size_t)k * M,
-                         sn + (size_t)k * M);
+            if (c->kind == ORC_JODIE)
+                orc_rnn_cell(M, D_x, c->W_ih, c->W_hh, c->b_ih, c->b_hh, x, fm + (size_t)k * M,
+                             sn + (size_t)k * M);
+            else
+                orc_gru_cell(M, D_x, c->W_ih, c->W_hh, c->b_ih, c->b_hh, x, fm + (size_t)k * M,
+                             sn + (size_t)k * M);
             nmts[k] = flts[k];
             free(x);
         } else {
@@ -810,6 +865,12 @@ int orc_step(void *p, orc_step_out *o)
                      c->W_v, c->b_v, c->W_o, c->b_o};
     #pragma omp parallel for schedule(dynamic, 8)
     for (int r = 0; r < R; ++r) {
+        if (c->kind == ORC_JODIE) {
+            const int pr = pos[root[r]];
+            orc_time_projection(M, c->w_t, sn + (size_t)pr * M, nmts[pr], rts[r],
+                                h + (size_t)r * M);
+            continue;
+        }
         const int cr = cnt[r];
         const double **pu = (const double **)malloc(sizeof(void *) * (nb > 0 ? nb : 1));
         const double **pf = (const double **)malloc(sizeof(void *) * (nb > 0 ? nb : 1));

@@ -85,21 +85,26 @@ class Workload:
 
 @dataclass
 class Weights:
-    """Model parameters, row-major.  fp32 except the time encoding (fp64)."""
-    W_ih: np.ndarray  # [3M, D_x]  gate order r, z, n
-    W_hh: np.ndarray  # [3M, M]
-    b_ih: np.ndarray  # [3M]
-    b_hh: np.ndarray  # [3M]
+    """Model parameters, row-major.  fp32 except the time encoding (fp64).
+    TGN: a GRU updater and attention.  JODIE: an RNN updater ([M, D_x] and
+    [M, M] weights, [M] biases) and the time projection w_t [M]; no attention
+    weights."""
+    W_ih: np.ndarray  # [3M, D_x]  gate order r, z, n   (JODIE: [M, D_x])
+    W_hh: np.ndarray  # [3M, M]                        (JODIE: [M, M])
+    b_ih: np.ndarray  # [3M]                           (JODIE: [M])
+    b_hh: np.ndarray  # [3M]                           (JODIE: [M])
     omega: np.ndarray  # float64[D_t]
     beta: np.ndarray   # float64[D_t]
-    W_q: np.ndarray   # [d_a, M + D_t]
-    b_q: np.ndarray
-    W_k: np.ndarray   # [d_a, M + D_e + D_t]
-    b_k: np.ndarray
-    W_v: np.ndarray   # [d_a, M + D_e + D_t]
-    b_v: np.ndarray
-    W_o: np.ndarray   # [M, d_a + M]
-    b_o: np.ndarray   # [M]
+    W_q: np.ndarray | None = None   # [d_a, M + D_t]
+    b_q: np.ndarray | None = None
+    W_k: np.ndarray | None = None   # [d_a, M + D_e + D_t]
+    b_k: np.ndarray | None = None
+    W_v: np.ndarray | None = None   # [d_a, M + D_e + D_t]
+    b_v: np.ndarray | None = None
+    W_o: np.ndarray | None = None   # [M, d_a + M]
+    b_o: np.ndarray | None = None   # [M]
+    kind: str = "tgn"               # "tgn" or "jodie"
+    w_t: np.ndarray | None = None   # [M] JODIE's time projection
 
 
 # ---------------------------------------------------------------------------
@@ -297,10 +302,12 @@ def _uniform(rng, shape, fan_in):
 
 
 def make_weights(M: int, D_e: int, D_t: int, *, seed: int = 0,
-                 beta: str = "zero") -> Weights:
+                 beta: str = "zero", model: str = "tgn") -> Weights:
     """U(+-1/sqrt(fan_in)) fp32 weights; time-encoding frequencies
     omega_d = 10^(-9 d / (D_t - 1)) and phases beta (zero, or U(0, 2pi) when
-    ``beta='random'``) in fp64."""
+    ``beta='random'``) in fp64.  ``model='jodie'``: an RNN updater and a time
+    projection w_t ~ U(+-1/sqrt(M)) scaled by 1e-5 per time unit (the
+    streams' gaps reach 1e6)."""
     D_m = 2 * M + D_e
     D_x = D_m + D_t
     d_a = M
@@ -314,6 +321,16 @@ def make_weights(M: int, D_e: int, D_t: int, *, seed: int = 0,
         b = r("beta").uniform(0.0, 2.0 * math.pi, size=D_t)
     else:
         raise ValueError(beta)
+    if model == "jodie":
+        return Weights(
+            W_ih=_uniform(r("W_ih1"), (M, D_x), D_x),
+            W_hh=_uniform(r("W_hh1"), (M, M), M),
+            b_ih=_uniform(r("b_ih1"), (M,), M),
+            b_hh=_uniform(r("b_hh1"), (M,), M),
+            omega=omega, beta=b, kind="jodie",
+            w_t=(_uniform(r("w_t"), (M,), M) * np.float32(1e-5)).astype(np.float32))
+    if model != "tgn":
+        raise ValueError(model)
     return Weights(
         W_ih=_uniform(r("W_ih"), (3 * M, D_x), D_x),
         W_hh=_uniform(r("W_hh"), (3 * M, M), M),
