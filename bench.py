@@ -177,11 +177,13 @@ def window_setup(name, first, L, w, mitigation=None):
     return wl, stage, init
 
 
-def work_model(wl, rows):
+def work_model(wl, rows, model="tgn"):
     """Algorithmic flops / bytes per launch of each kernel (averaged over the
     timed steps).  Counts only useful work: valid slots, nodes with mail,
-    winning messages; no tile padding."""
+    winning messages; no tile padding.  model: "tgn" (GRU, three gates) or
+    "jodie" (RNN cell, one gate)."""
     M, D_e, D_t, D_m, nb = wl.M, wl.D_e, wl.D_t, wl.D_m, wl.nb
+    gates = 1 if model == "jodie" else 3
     D_x = D_m + D_t
     n = len(rows)
     avg = lambda key: sum(r[key] for r in rows) / n
@@ -191,7 +193,7 @@ def work_model(wl, rows):
     k = {
         # per node with mail: the three gates over [x | h]
         # (plus the batch's latest-message reduce: 2b positions, 2b 64-bit atomics)
-        "k_gru": dict(flops=n_mail * 2 * 3 * M * (D_x + M),
+        "k_gru": dict(flops=n_mail * 2 * gates * M * (D_x + M),
                       bytes=n_U * (M * f + d + d + 4) + n_mail * D_m * f + n_U * M * f
                       + 2 * b * (4 + 8)),
         # per valid slot: [efeat || phi] -> [K | V] and the two head dot products;
@@ -217,6 +219,11 @@ def work_model(wl, rows):
                              bytes=k["k_node_proj"]["bytes"] + k["k_stage"]["bytes"])
     k["k_attn_gather"] = dict(flops=k["k_attn"]["flops"],
                               bytes=k["k_attn"]["bytes"] + k["k_gather_state"]["bytes"])
+    # JODIE's time projection: per root its memory row, time and position in,
+    # the embedding out; with the next fetch's gather in the executor
+    k["k_tproj"] = dict(flops=R * 3 * M, bytes=R * (2 * M * f + 4 + d + d) + M * f)
+    k["k_tproj_gather"] = dict(flops=k["k_tproj"]["flops"],
+                               bytes=k["k_tproj"]["bytes"] + k["k_gather_state"]["bytes"])
     # staleness mitigation: per node a gap and a neighbour set; the threshold
     # select reads the gaps 8 times; per stale node a probe of every node's set
     k["k_mit_prep"] = dict(flops=0, bytes=n_U * (4 + 8 + 8 + nb * 16 + nb * 4 + 4))
@@ -321,6 +328,9 @@ def main():
                     help="wiki (default), tiny, reddit, lastfm; gdelt runs a window of batches "
                          "starting at --first from a synthetic state")
     ap.add_argument("--first", type=int, default=20_000, help="first batch of a gdelt window")
+    ap.add_argument("--model", default="tgn", choices=("tgn", "jodie"),
+                    help="model family: tgn (GRU memory, attention; default) or jodie (RNN "
+                         "memory, time projection)")
     ap.add_argument("--mitigate", default=None, metavar="P,LAMBDA,K",
                     help="similarity-based staleness mitigation on every fetch (MSPipe-S, "
                          "off by default), e.g. 0.99,0.95,10")
@@ -360,13 +370,13 @@ def main():
     if window:
         from workloads import CONFIGS
         c = CONFIGS["gdelt"]
-        w = make_weights(c["M"], c["D_e"], c["D_t"])
+        w = make_weights(c["M"], c["D_e"], c["D_t"], model=args.model)
         wl, stage, init = window_setup("gdelt", args.first, W + K, w, mit)
         sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
         sched.restart()
     else:
         wl = make_workload(args.workload)
-        w = make_weights(wl.M, wl.D_e, wl.D_t)
+        w = make_weights(wl.M, wl.D_e, wl.D_t, model=args.model)
         stage = from_workload(wl, w, mitigation=mit)
         sched = Schedule(stage, wl.n_iters)
     log(f"workload {wl.name}: N={wl.N} E={wl.E} B={wl.B} s={wl.s} iters={wl.n_iters}")
@@ -403,6 +413,8 @@ def main():
                                   "update + embed of batch i"}}
     if mit is not None:
         out["config"]["mitigation"] = dict(mit, kind="MSPipe-S similarity-based, every fetch")
+    if args.model != "tgn":
+        out["config"]["model_family"] = "JODIE: RNN memory updater, time-projection embedding"
 
     if not args.no_profile:
         # pass 2: per-kernel durations (HIP events on the launch stream)
@@ -423,7 +435,7 @@ def main():
             prof[base] = (n0 + launches, m0 + ms)
         # pass 3: algorithmic work per launch, and the sequential stage times
         rows, seq = account(sched, W, K)
-        work = work_model(wl, rows)
+        work = work_model(wl, rows, args.model)
         kernels = {}
         for name, (launches, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
             avg_s = ms / launches * 1e-3

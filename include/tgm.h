@@ -191,15 +191,28 @@ tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int32_t *nodes
  * D_e <= 256, and the attention tile of 80 slots x (D_e + D_t) fp32 must fit
  * the 160 KB of LDS of a workgroup (D_e + D_t <= 384); else TGM_EINVAL.
  */
+/* Model families (Sec. 5 trains TGN, JODIE and APAN):
+ *   TGM_MODEL_TGN    the GRU updater and the attention embedding above;
+ *   TGM_MODEL_JODIE  an RNN updater, mem' = tanh(W_ih x + b_ih + W_hh mem + b_hh)
+ *     on the same input x = [mail || phi(mail_ts - mem_ts)], with W_ih
+ *     [M x D_x], W_hh [M x M], b_ih, b_hh [M]; the embedding is the time
+ *     projection h = s' * (1 + w_t (t - ts')) of tgm_embed_projection, w_t [M]
+ *     (JODIE's projection of a node's memory to the query time).  The
+ *     attention weights and H are not read (H must still divide M). */
+#define TGM_MODEL_TGN 0
+#define TGM_MODEL_JODIE 1
+
 typedef struct {
     int32_t M, D_e, D_t, H, nb;
     int32_t max_nodes, max_roots;
+    int32_t kind;   /* TGM_MODEL_TGN or TGM_MODEL_JODIE */
 } tgm_model_desc;
 
 typedef struct {
     const float *W_ih, *W_hh, *b_ih, *b_hh;
     const double *omega, *beta;
     const float *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+    const float *w_t;   /* TGM_MODEL_JODIE: [M] */
 } tgm_weights;
 
 tgm_status_t tgm_model_create(const tgm_model_desc *desc, const tgm_weights *w, void *stream,
@@ -209,7 +222,8 @@ tgm_status_t tgm_model_destroy(tgm_model_t m);
 /* Memory update of iteration `iter` (Eq. 1 with the stale reads of Eq. 2;
  * Alg. 1's update_mem):
  *  - for every node p < *n_nodes of the fetched set with ver[p] >= 0:
- *      mem_new[p] = GRU([mail[p] || phi(mail_ts[p] - mem_ts[p])], mem[p]),
+ *      mem_new[p] = GRU([mail[p] || phi(mail_ts[p] - mem_ts[p])], mem[p])
+ *        (the RNN cell for TGM_MODEL_JODIE models),
  *      new_mem_ts[p] = mail_ts[p]  (Delta-t as defined under Eq. 1);
  *    otherwise mem_new[p] = mem[p], new_mem_ts[p] = mem_ts[p];
  *  - messages of the b positive events [first_event, first_event + b)
@@ -247,6 +261,19 @@ tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
                        const int32_t *eid, const double *nts, const int32_t *cnt,
                        const float *mem_new, const int32_t *n_nodes, int32_t cap, float *h,
                        void *stream);
+
+/* JODIE's embedding (TGM_MODEL_JODIE models; TGN models: TGM_EINVAL): the
+ * time projection of each root's updated memory to its query time,
+ *   h[r] = mem_new[p] * (1 + w_t * (root_ts[r] - new_mem_ts[p])),
+ *   p = root_pos[r], formed in fp64 and stored as fp32.
+ * root_pos [R] and root_ts [R] as from tgm_sample_nodes; mem_new [cap x M]
+ * and new_mem_ts [cap] as from tgm_update_memory.  Output h [R x M].  Errors:
+ * TGM_EINVAL (null, dims, model family), TGM_ESIZE (R above max_roots or cap
+ * above max_nodes). */
+tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int32_t *root_pos,
+                                  const double *root_ts, const float *mem_new,
+                                  const double *new_mem_ts, const int32_t *n_nodes, int32_t cap,
+                                  float *h, void *stream);
 
 /* ------------------------------------------------------------------------
  * Pipelined executor.  Runs iterations i0 .. i0+n-1 of the stage (the batch of

@@ -145,6 +145,11 @@ struct tgm_model {
     int32_t OC = 0, ONB = 0;             // chunks of 2M, 16-col blocks of M
     tgm::f4 *out_b = nullptr;
     float *b_o = nullptr;
+    // model family; JODIE's time projection and a [max_nodes] buffer of new
+    // memory times for the executor when its caller passes none
+    int32_t kind = TGM_MODEL_TGN;
+    float *w_t = nullptr;
+    double *nts = nullptr;
 };
 
 namespace tgm {

@@ -62,6 +62,9 @@ struct GruW {
     int64_t kstep, gx, gh;
     int KXC, last;   // last: the highest chunk that may be loaded
 
+    // G = 3 gates (GRU: r, z, n) or 1 (the RNN cell: its single gate sits in
+    // w[2], where the GRU keeps n)
+    template <int G>
     __device__ __forceinline__ void load(int c, int hb, int lane, f4 (&w)[3]) const
     {
         c = c < last ? c : last;
@@ -69,18 +72,25 @@ struct GruW {
         const f4 *p = (x ? bx + (int64_t)c * kstep : bh + (int64_t)(c - KXC) * kstep) +
                       (int64_t)hb * kWave + lane;
         const int64_t gs = x ? gx : gh;
-        w[0] = p[0];
-        w[1] = p[gs];
-        w[2] = p[2 * gs];
+        if (G == 3) {
+            w[0] = p[0];
+            w[1] = p[gs];
+            w[2] = p[2 * gs];
+        } else {
+            w[2] = p[0];
+        }
     }
 };
 
+template <int G>
 __device__ __forceinline__ void gru_mma(const float *arow, int c, int KXC, const f4 (&w)[3],
                                         f4 &ar, f4 &az, f4 &anx, f4 &anh)
 {
     const f4 a = *reinterpret_cast<const f4 *>(arow + c * 16);
-    ar = mfma_k16(a, w[0], ar);
-    az = mfma_k16(a, w[1], az);
+    if (G == 3) {
+        ar = mfma_k16(a, w[0], ar);
+        az = mfma_k16(a, w[1], az);
+    }
     if (c < KXC)
         anx = mfma_k16(a, w[2], anx);
     else
@@ -185,7 +195,7 @@ __device__ __forceinline__ void latest_reduce(const GruArgs &g, int n)
                   (unsigned long long)(g.tag | (uint64_t)c));
 }
 
-template <int W, int CM, int CH>
+template <int W, int CM, int CH, int NG>
 __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_has,
                                          double *s_nts)
 {
@@ -258,8 +268,8 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
         const float b_r = g.bias[colc], b_z = g.bias[MP + colc];
         const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
         f4 w0[3], w1[3], w2[3];
-        gw.load(kc0, hb, lane, w0);
-        gw.load(kc0 + 1, hb, lane, w1);
+        gw.load<NG>(kc0, hb, lane, w0);
+        gw.load<NG>(kc0 + 1, hb, lane, w1);
         __syncthreads();   // s_om is written; the previous round is done with LDS
         rows.store(g, A, s_has, s_nts, SA, KX, s_om, s_be, nrows, lane);
         __syncthreads();
@@ -269,17 +279,17 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
             // three weight sets rotate: chunk c + 2 loads while chunk c multiplies
             const float *arow = arow0 + lrow0 * SA;
             for (int cc = kc0; cc < kc1; cc += 3) {
-                gw.load(cc + 2, hb, lane, w2);
+                gw.load<NG>(cc + 2, hb, lane, w2);
                 issue_fence();
-                gru_mma(arow, cc, KXC, w0, ar, az, anx, anh);
-                gw.load(cc + 3, hb, lane, w0);
+                gru_mma<NG>(arow, cc, KXC, w0, ar, az, anx, anh);
+                gw.load<NG>(cc + 3, hb, lane, w0);
                 issue_fence();
                 if (cc + 1 < kc1)
-                    gru_mma(arow, cc + 1, KXC, w1, ar, az, anx, anh);
-                gw.load(cc + 4, hb, lane, w1);
+                    gru_mma<NG>(arow, cc + 1, KXC, w1, ar, az, anx, anh);
+                gw.load<NG>(cc + 4, hb, lane, w1);
                 issue_fence();
                 if (cc + 2 < kc1)
-                    gru_mma(arow, cc + 2, KXC, w2, ar, az, anx, anh);
+                    gru_mma<NG>(arow, cc + 2, KXC, w2, ar, az, anx, anh);
             }
             if (half) {
                 red[(j * 4 + 0) * kWave + lane] = ar;
@@ -308,10 +318,14 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
                         const float h = A[lr * SA + KX + col];
                         float o = h;
                         if (s_has[lr]) {
-                            const float r = sigmoidf_(ar[v] + b_r);
-                            const float z = sigmoidf_(az[v] + b_z);
-                            const float nn = tanhf(anx[v] + b_nx + r * (anh[v] + b_nh));
-                            o = (1.0f - z) * nn + z * h;
+                            if (NG == 3) {
+                                const float r = sigmoidf_(ar[v] + b_r);
+                                const float z = sigmoidf_(az[v] + b_z);
+                                const float nn = tanhf(anx[v] + b_nx + r * (anh[v] + b_nh));
+                                o = (1.0f - z) * nn + z * h;
+                            } else {   // the RNN cell
+                                o = tanhf((anx[v] + b_nx) + (anh[v] + b_nh));
+                            }
                         }
                         g.mem_new[(int64_t)p * M + col] = o;
                     }
@@ -327,6 +341,8 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
     }
 }
 
+// NG = 3: the GRU cell; NG = 1: the RNN cell (JODIE), same pipeline.
+template <int NG>
 __global__ __launch_bounds__(64 * kGruWaves) void k_gru(GruArgs g)
 {
     extern __shared__ float lds[];
@@ -336,9 +352,57 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru(GruArgs g)
                      15) == 0 &&
                     (g.D_m & 3) == 0 && (g.M & 3) == 0;   // 16-byte rows: vector loads
     if (al)
-        gru_body<4, 2, 1>(g, lds, s_has, s_nts);   // D_m <= 512, M <= 256
+        gru_body<4, 2, 1, NG>(g, lds, s_has, s_nts);   // D_m <= 512, M <= 256
     else
-        gru_body<1, 8, 2>(g, lds, s_has, s_nts);
+        gru_body<1, 8, 2, NG>(g, lds, s_has, s_nts);
+}
+
+// JODIE's embedding: the time projection h[r] = s'[p] * (1 + w_t (t_r - ts'[p]))
+// of root r's updated memory (p = root_pos[r]), in fp64, one thread per
+// element of h.  A position outside the node set yields a zero row.
+struct TprojArgs {
+    int32_t R = 0, M = 0;
+    const int32_t *root_pos = nullptr, *n_nodes = nullptr;
+    const double *root_ts = nullptr, *nts = nullptr;
+    const float *mem_new = nullptr, *w_t = nullptr;
+    float *h = nullptr;
+};
+
+__device__ __forceinline__ void tproj_elem(const TprojArgs &a, int64_t i, int n)
+{
+    const int r = (int)(i / a.M), c = (int)(i - (int64_t)r * a.M);
+    const int p = a.root_pos[r];
+    float o = 0.f;
+    if (p >= 0 && p < n) {
+        const double d = a.root_ts[r] - a.nts[p];
+        o = (float)((double)a.mem_new[(int64_t)p * a.M + c] * (1.0 + (double)a.w_t[c] * d));
+    }
+    a.h[i] = o;
+}
+
+__global__ __launch_bounds__(256) void k_tproj(TprojArgs a)
+{
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (i < (int64_t)a.R * a.M)
+        tproj_elem(a, i, *a.n_nodes);
+}
+
+// The projection and the gather of the next fetch in one launch: blocks
+// below n_tp project, the rest gather (kGatherNPW nodes per wavefront).
+__global__ __launch_bounds__(256) void k_tproj_gather(TprojArgs a, int n_tp, GatherPlan gp)
+{
+    if ((int)blockIdx.x < n_tp) {
+        const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+        if (i < (int64_t)a.R * a.M)
+            tproj_elem(a, i, *a.n_nodes);
+        return;
+    }
+    const int waves = blockDim.x >> 6;
+    const int n = min(*gp.n_nodes, gp.cap);
+    const int stride = ((int)gridDim.x - n_tp) * waves * kGatherNPW;
+    for (int p = (((int)blockIdx.x - n_tp) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
+         p < n; p += stride)
+        gather_rows(gp, p, n, threadIdx.x & 63);
 }
 
 // Stage the write set of iteration i, and commit an older one, in one launch.
@@ -1776,6 +1840,49 @@ bool attn_fold_fits(const tgm_model *m)
 
 // ======================================================================== API
 
+namespace {
+
+// The JODIE part of tgm_model_create: the RNN cell's operands in the GRU
+// kernel's layout (one gate block, in the slot of the GRU's n gate, and its
+// biases b_ih, b_hh in the n slots), the time encoding, the time projection
+// and the executor's buffer of new memory times.
+tgm_status_t create_jodie(tgm_model *m, const tgm_model_desc *d, const tgm_weights *w)
+{
+    const int M = m->M, D_x = m->D_x, D_t = m->D_t, MP = m->MB * 16;
+    auto bx = pack_b(w->W_ih, M, D_x, 0, D_x, m->KXC, m->MB);
+    auto bh = pack_b(w->W_hh, M, M, 0, M, m->KHC, m->MB);
+    bx.resize(bx.size() + 2 * (size_t)m->MB * kWave * 4, 0.f);   // two zero chunks past the end
+    bh.resize(bh.size() + 2 * (size_t)m->MB * kWave * 4, 0.f);
+    std::vector<float> bias(4 * (size_t)MP, 0.f);
+    for (int k = 0; k < M; ++k) {
+        bias[2 * MP + k] = w->b_ih[k];
+        bias[3 * MP + k] = w->b_hh[k];
+    }
+    auto alloc = [](void **p, size_t bytes) {
+        return hipMalloc(p, bytes ? bytes : 16) == hipSuccess;
+    };
+    if (!alloc((void **)&m->gru_bx, bx.size() * 4) || !alloc((void **)&m->gru_bh, bh.size() * 4) ||
+        !alloc((void **)&m->gru_bias, bias.size() * 4) ||
+        !alloc((void **)&m->omega, sizeof(double) * D_t) ||
+        !alloc((void **)&m->beta, sizeof(double) * D_t) || !alloc((void **)&m->w_t, 4 * M) ||
+        !alloc((void **)&m->nts, sizeof(double) * (size_t)d->max_nodes))
+        return TGM_ENOMEM;
+    TGM_TRY_STATUS(upload(m->gru_bx, bx.data(), bx.size() * 4));
+    TGM_TRY_STATUS(upload(m->gru_bh, bh.data(), bh.size() * 4));
+    TGM_TRY_STATUS(upload(m->gru_bias, bias.data(), bias.size() * 4));
+    if (D_t > 0) {
+        TGM_TRY_STATUS(upload(m->omega, w->omega, sizeof(double) * D_t));
+        TGM_TRY_STATUS(upload(m->beta, w->beta, sizeof(double) * D_t));
+    }
+    TGM_TRY_STATUS(upload(m->w_t, w->w_t, 4 * M));
+    if (hipFuncSetAttribute((const void *)k_gru<1>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)gru_lds(m)) != hipSuccess)
+        return TGM_EINVAL;
+    return TGM_OK;
+}
+
+}  // namespace
+
 extern "C" tgm_status_t tgm_model_destroy(tgm_model_t m)
 {
     if (!m)
@@ -1793,6 +1900,8 @@ extern "C" tgm_status_t tgm_model_destroy(tgm_model_t m)
     hipFree(m->pbias);
     hipFree(m->out_b);
     hipFree(m->b_o);
+    hipFree(m->w_t);
+    hipFree(m->nts);
     delete m;
     return TGM_OK;
 }
@@ -1811,8 +1920,11 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
         d->max_nodes <= 0 || d->max_roots < 0 || 2 * M > 16 * kMaxWaves * kAttMaxCB ||
         D_e > 256)
         return TGM_EINVAL;
-    if (!w->W_ih || !w->W_hh || !w->b_ih || !w->b_hh || (D_t > 0 && (!w->omega || !w->beta)) ||
-        !w->W_q || !w->b_q || !w->W_k || !w->b_k || !w->W_v || !w->b_v || !w->W_o || !w->b_o)
+    if (!w->W_ih || !w->W_hh || !w->b_ih || !w->b_hh || (D_t > 0 && (!w->omega || !w->beta)))
+        return TGM_EINVAL;
+    if (d->kind == TGM_MODEL_JODIE ? !w->w_t
+                                   : (!w->W_q || !w->b_q || !w->W_k || !w->b_k || !w->W_v ||
+                                      !w->b_v || !w->W_o || !w->b_o))
         return TGM_EINVAL;
     hipStream_t s = as_stream(stream);
     tgm_model *m = new tgm_model();
@@ -1830,6 +1942,20 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     m->OC = (int)cdiv(2 * M, 16);
     m->ONB = (int)cdiv(M, 16);
     m->VNB = m->DC = (int)cdiv(M, 16);
+    m->kind = d->kind;
+    if (d->kind == TGM_MODEL_JODIE) {
+        const tgm_status_t st = create_jodie(m, d, w);
+        if (st != TGM_OK) {
+            tgm_model_destroy(m);
+            return st;
+        }
+        *out = m;
+        return TGM_OK;
+    }
+    if (d->kind != TGM_MODEL_TGN) {
+        tgm_model_destroy(m);
+        return TGM_EINVAL;
+    }
     m->fold = attn_fold_fits(m);
 
     // GRU operands
@@ -1943,7 +2069,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             break;
         }
         // large LDS footprints need an explicit opt-in
-        if (hipFuncSetAttribute((const void *)k_gru, hipFuncAttributeMaxDynamicSharedMemorySize,
+        if (hipFuncSetAttribute((const void *)k_gru<3>, hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)gru_lds(m)) != hipSuccess ||
             hipFuncSetAttribute((const void *)k_node_proj,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -2009,7 +2135,10 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
         ga.n_cand = n_cand; ga.src_pos = src_pos; ga.dst_pos = dst_pos; ga.win = st->win;
         ga.tag = tag;
         // persistent: the node set's tasks are split over kGruGrid workgroups
-        TGM_LAUNCH(k_gru, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
+        if (m->kind == TGM_MODEL_JODIE)
+            TGM_LAUNCH(k_gru<1>, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
+        else
+            TGM_LAUNCH(k_gru<3>, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
     }
     const size_t base = (size_t)(iter % slots) * st->ring_rows();
     // the write set of iteration iter - s is committed by the staging launch
@@ -2072,7 +2201,8 @@ tgm_status_t embed_plan(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
                         const float *mem_new, const int32_t *n_nodes, int32_t cap, float *h,
                         ProjArgs *pa, int *proj_grid, int *proj_waves, AttnArgs *aa)
 {
-    if (!m || !g || R < 0 || nb != m->nb || !n_nodes || cap < 0 || g->D_e != m->D_e)
+    if (!m || !g || R < 0 || nb != m->nb || !n_nodes || cap < 0 || g->D_e != m->D_e ||
+        m->kind != TGM_MODEL_TGN)
         return TGM_EINVAL;
     if (R > m->max_roots || cap > m->max_nodes)
         return TGM_ESIZE;
@@ -2197,6 +2327,38 @@ extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32
     return launch_attn(m, aa, nullptr, s);
 }
 
+namespace {
+
+tgm_status_t tproj_plan(tgm_model_t m, int32_t R, const int32_t *root_pos,
+                        const double *root_ts, const float *mem_new, const double *new_mem_ts,
+                        const int32_t *n_nodes, int32_t cap, float *h, TprojArgs *a)
+{
+    if (!m || m->kind != TGM_MODEL_JODIE || R < 0 || cap < 0 || !n_nodes)
+        return TGM_EINVAL;
+    if (R > m->max_roots || cap > m->max_nodes)
+        return TGM_ESIZE;
+    if (R > 0 && (!root_pos || !root_ts || !mem_new || !new_mem_ts || !h || cap == 0))
+        return TGM_EINVAL;
+    a->R = R; a->M = m->M; a->root_pos = root_pos; a->n_nodes = n_nodes;
+    a->root_ts = root_ts; a->nts = new_mem_ts; a->mem_new = mem_new; a->w_t = m->w_t; a->h = h;
+    return TGM_OK;
+}
+
+}  // namespace
+
+extern "C" tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int32_t *root_pos,
+                                             const double *root_ts, const float *mem_new,
+                                             const double *new_mem_ts, const int32_t *n_nodes,
+                                             int32_t cap, float *h, void *stream)
+{
+    TprojArgs a;
+    TGM_TRY_STATUS(tproj_plan(m, R, root_pos, root_ts, mem_new, new_mem_ts, n_nodes, cap, h, &a));
+    if (R > 0)
+        TGM_LAUNCH(k_tproj, dim3((unsigned)cdiv((int64_t)R * m->M, 256)), dim3(256), 0,
+                   as_stream(stream), a);
+    return TGM_OK;
+}
+
 tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
                                     const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
                                     int32_t cap, int64_t first_event, int32_t b, int32_t nb,
@@ -2211,11 +2373,40 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     StageArgs sa;
     int n_items = 0;
     uint64_t tag = 0;
+    const bool jodie = m && m->kind == TGM_MODEL_JODIE;
+    // JODIE's projection reads the new memory times: the model's buffer
+    // stands in when the caller keeps none
+    double *nts = jodie && !new_mem_ts ? m->nts : new_mem_ts;
     tgm_status_t rc = update_begin(st, m, g, iter, sb.n_nodes, cap, fb.mem, fb.mem_ts, fb.mail,
                                    fb.mail_ts, fb.ver, first_event, b, sb.root_pos,
-                                   sb.root_pos + b, mem_new, new_mem_ts, s, &sa, &n_items, &tag);
+                                   sb.root_pos + b, mem_new, nts, s, &sa, &n_items, &tag);
     if (rc != TGM_OK)
         return rc;
+    if (jodie) {
+        // RNN, staging, then the projection with the next fetch's gather
+        TprojArgs ta;
+        const int32_t R = 3 * b;
+        TGM_TRY_STATUS(tproj_plan(m, R, sb.root_pos, sb.root_ts, mem_new, nts, sb.n_nodes, cap,
+                                  h, &ta));
+        GatherPlan next_plan;
+        bool has_next = false;
+        if (next_sb) {
+            TGM_TRY_STATUS(fetch_plan(st, iter + 1, next_sb->nodes, next_sb->n_nodes, cap,
+                                      fb.mem, fb.mem_ts, fb.mail, fb.mail_ts, fb.ver, s,
+                                      &next_plan));
+            has_next = next_plan.cap > 0;
+        }
+        if (n_items > 0)
+            TGM_LAUNCH(k_stage, dim3((unsigned)cdiv(n_items, 4)), dim3(256), 0, s, sa);
+        TGM_TRY_STATUS(update_winner(st, sb.n_nodes, cap, first_event, tag, winner, s));
+        const int n_tp = (int)cdiv((int64_t)R * m->M, 256);
+        if (has_next)
+            TGM_LAUNCH(k_tproj_gather, dim3((unsigned)(n_tp + kCUs)), dim3(256), 0, s, ta, n_tp,
+                       next_plan);
+        else if (R > 0)
+            TGM_LAUNCH(k_tproj, dim3((unsigned)n_tp), dim3(256), 0, s, ta);
+        return TGM_OK;
+    }
     ProjArgs pa;
     AttnArgs aa;
     int proj_grid = 0, proj_waves = 0;

@@ -70,6 +70,7 @@ class Stage:
         self.g = tgm.tgm_graph_create(self.N, self.src, self.dst, self.t, self.neg, self.efeat,
                                       stream=st)
         self.st = tgm.tgm_state_create(self.N, M, self.D_m, s, B, stream=st)
+        self.kind = getattr(weights, "kind", "tgn")   # "tgn" or "jodie"
         self.m = tgm.tgm_model_create(M, self.D_e, D_t, H, nb, self.cap, R, weights, stream=st)
         self.sets = [_Sample(dev, R, nb, self.cap) for _ in range(_SETS)]
         z = lambda shape, dt: torch.zeros(shape, dtype=dt, device=dev)
@@ -130,8 +131,13 @@ class Stage:
                               lo, n, b.root_pos[:n], b.root_pos[n:2 * n], self.mem_new,
                               self.new_mem_ts, self.winner if self.want_winner else None,
                               stream=st)
-        tgm.tgm_embed(self.m, self.g, 3 * n, self.nb, b.root_pos, b.root_ts, b.nbr_pos, b.eid,
-                      b.nts, b.cnt, self.mem_new, b.n_nodes, self.cap, self.h, stream=st)
+        if self.kind == "jodie":
+            tgm.tgm_embed_projection(self.m, 3 * n, b.root_pos, b.root_ts, self.mem_new,
+                                     self.new_mem_ts, b.n_nodes, self.cap, self.h, stream=st)
+        else:
+            tgm.tgm_embed(self.m, self.g, 3 * n, self.nb, b.root_pos, b.root_ts, b.nbr_pos,
+                          b.eid, b.nts, b.cnt, self.mem_new, b.n_nodes, self.cap, self.h,
+                          stream=st)
         self.last, self._set = (i, n), 0
 
     def run(self, i0: int, n: int):
@@ -225,7 +231,7 @@ def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None)
 # mitigation belongs to the memory fetch (Sec. 4.3).
 STAGE_KERNELS = {1: ("k_sample_batch", "k_ns_mark", "k_ns_pos"), 2: (),
                  3: ("k_gather_state", "k_mit_prep", "k_mit_select", "k_mit_omega"),
-                 4: ("k_gru", "k_node_proj", "k_attn_fold", "k_attn"),
+                 4: ("k_gru", "k_node_proj", "k_attn_fold", "k_attn", "k_tproj"),
                  5: ("k_stage", "k_commit")}
 
 

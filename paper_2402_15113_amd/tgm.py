@@ -25,6 +25,7 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
            "tgm_stage_run", "tgm_mitigator_create", "tgm_mitigator_destroy", "tgm_mitigate",
            "tgm_mitigator_read", "tgm_state_set_mitigation", "tgm_min_staleness",
+           "tgm_embed_projection",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
 
@@ -45,7 +46,12 @@ class FetchBuffers(C.Structure):
 
 class ModelDesc(C.Structure):
     _fields_ = [("M", C.c_int32), ("D_e", C.c_int32), ("D_t", C.c_int32), ("H", C.c_int32),
-                ("nb", C.c_int32), ("max_nodes", C.c_int32), ("max_roots", C.c_int32)]
+                ("nb", C.c_int32), ("max_nodes", C.c_int32), ("max_roots", C.c_int32),
+                ("kind", C.c_int32)]
+
+
+TGM_MODEL_TGN, TGM_MODEL_JODIE = 0, 1
+MODEL_KINDS = {"tgn": TGM_MODEL_TGN, "jodie": TGM_MODEL_JODIE}
 
 
 _fp = C.POINTER(C.c_float)
@@ -56,7 +62,7 @@ class Weights(C.Structure):
     _fields_ = [("W_ih", _fp), ("W_hh", _fp), ("b_ih", _fp), ("b_hh", _fp),
                 ("omega", _dp), ("beta", _dp),
                 ("W_q", _fp), ("b_q", _fp), ("W_k", _fp), ("b_k", _fp), ("W_v", _fp),
-                ("b_v", _fp), ("W_o", _fp), ("b_o", _fp)]
+                ("b_v", _fp), ("W_o", _fp), ("b_o", _fp), ("w_t", _fp)]
 
 
 _lib = None
@@ -104,6 +110,7 @@ def lib():
             "tgm_mitigator_read": [V, P, P, P, P, V],
             "tgm_state_set_mitigation": [V, V, C.c_double, C.c_float],
             "tgm_min_staleness": [P, I64, I32, P, P, P, P, P],
+            "tgm_embed_projection": [V, I32, P, P, P, P, P, I32, P, V],
         }
         sig["tgm_profile_enable"] = [I32]
         sig["tgm_profile_reset"] = []
@@ -315,17 +322,21 @@ def tgm_min_staleness(tau, n, k_max):
 # ------------------------------------------------------------------ model
 def tgm_model_create(M, D_e, D_t, H, nb, max_nodes, max_roots, w, stream=None):
     """``w`` holds numpy weights (fp32; omega and beta fp64), see workloads.Weights."""
-    d = ModelDesc(M, D_e, D_t, H, nb, max_nodes, max_roots)
+    kind = MODEL_KINDS[getattr(w, "kind", "tgn")]
+    d = ModelDesc(M, D_e, D_t, H, nb, max_nodes, max_roots, kind)
     keep = {}
 
     def arr(name, dt):
-        a = np.ascontiguousarray(getattr(w, name), dtype=dt)
+        v = getattr(w, name, None)
+        if v is None:
+            return None
+        a = np.ascontiguousarray(v, dtype=dt)
         keep[name] = a
         return a.ctypes.data_as(_fp if dt == np.float32 else _dp)
 
     ws = Weights()
     for name in ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v",
-                 "W_o", "b_o"):
+                 "W_o", "b_o", "w_t"):
         setattr(ws, name, arr(name, np.float32))
     ws.omega = arr("omega", np.float64)
     ws.beta = arr("beta", np.float64)
@@ -346,6 +357,13 @@ def tgm_update_memory(st, m, g, it, nodes, n_nodes, cap, mem, mem_ts, mail, mail
         st, m, g, it, _p(nodes), _p(n_nodes), cap, _p(mem), _p(mem_ts), _p(mail), _p(mail_ts),
         _p(ver), first_event, b, _p(src_pos), _p(dst_pos), _p(mem_new), _p(new_mem_ts),
         _p(winner), _s(stream)))
+
+
+def tgm_embed_projection(m, R, root_pos, root_ts, mem_new, new_mem_ts, n_nodes, cap, h,
+                         stream=None):
+    _check("tgm_embed_projection", lib().tgm_embed_projection(
+        m, R, _p(root_pos), _p(root_ts), _p(mem_new), _p(new_mem_ts), _p(n_nodes), cap, _p(h),
+        _s(stream)))
 
 
 def tgm_embed(m, g, R, nb, root_pos, root_ts, nbr_pos, eid, nts, cnt, mem_new, n_nodes, cap, h,
