@@ -104,3 +104,25 @@ def test_model_family_argument_errors():
     torch.cuda.synchronize()
     j.close()
     t.close()
+
+
+def test_jodie_with_mitigation_pipelined_equals_sequential(orc):
+    """The mitigation acts on fetched memories, so it composes with either
+    family: the executor and Stage.step agree bit for bit, and the sequential
+    run matches the oracle."""
+    from paper_2402_15113_amd.stage import from_workload
+    from test_gpu_mitigation import run_mitigated
+    wl = make_workload("tiny", s=2)
+    w = _w(wl)
+    mit = dict(p=0.8, lam=0.9, K=4)
+    assert run_mitigated(orc, wl, w, mit) > 0
+    a, b = from_workload(wl, w, mitigation=mit), from_workload(wl, w, mitigation=mit)
+    n = wl.n_iters
+    a.run(0, n)
+    for i in range(n):
+        b.step(i)
+    oa, ob = a.outputs(), b.outputs()
+    for k in oa:
+        assert np.array_equal(np.asarray(oa[k]), np.asarray(ob[k])), k
+    a.close()
+    b.close()
