@@ -284,11 +284,12 @@ tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int32_t *root_
  * each iteration run in order on `stream` with one set of fetch buffers, in
  * three launches per iteration (the staging of a write set shares a launch
  * with the node projections, and the attention with the next fetch's
- * gather).  The streams synchronise once per chunk.  The prefetch stream starts after
- * everything issued before on `stream`, and `stream` ends after the last
- * embedding.  Results equal those of issuing tgm_sample_nodes,
- * tgm_fetch_memory, tgm_update_memory and tgm_embed per iteration in order
- * on one stream.  nsb >= 2 and even; nb, cap as for the calls above;
+ * gather; for JODIE models: the update, the staging, and the projection with
+ * the next fetch's gather).  The streams synchronise once per chunk.  The
+ * prefetch stream starts after everything issued before on `stream`, and
+ * `stream` ends after the last embedding.  Results equal those of issuing
+ * tgm_sample_nodes, tgm_fetch_memory, tgm_update_memory and tgm_embed (or
+ * tgm_embed_projection) per iteration in order on one stream.  nsb >= 2 and even; nb, cap as for the calls above;
  * mem_new [cap x M], new_mem_ts [cap] (may be NULL), winner [cap] (may be
  * NULL) and h [3B x M] hold the last iteration's outputs.  The two streams
  * must differ.  Errors of the underlying calls are returned as they occur
