@@ -212,6 +212,8 @@ def work_model(wl, rows, model="tgn"):
         "k_stage": dict(flops=0, bytes=n_win * (2 * M * f + D_e * f + (M + D_m) * f + 3 * d)
                         + 2 * b * 12),
         "k_batch_roots": dict(flops=0, bytes=b * (3 * 4 + d) + 3 * b * (4 + d)),
+        # the executor's latest-message reduce: 2b positions in, 2b 64-bit atomics
+        "k_latest": dict(flops=0, bytes=2 * b * (4 + 8)),
     }
     # the executor's fused launches: staging + node projection; attention +
     # the next iteration's gather

@@ -111,6 +111,12 @@ struct tgm_state {
     // of the update call that wrote it (tags start at 1, so zero is stale)
     uint64_t *win = nullptr;
     uint32_t win_tag = 0;             // tag of the last update call
+    // the pipelined executor's latest-message reduce, run beside each sample
+    // on the prefetch stream: one [xwin_cap] key array per sample buffer set,
+    // keyed with a tag that grows with every reduced iteration
+    uint64_t *xwin = nullptr;
+    int32_t xwin_slots = 0, xwin_cap = 0;
+    uint32_t xwin_tag = 0;
     // staleness mitigation applied by the pipelined executor after each fetch
     // (tgm_state_set_mitigation; off when mit is null)
     struct tgm_mitigator *mit = nullptr;
@@ -623,7 +629,18 @@ tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int
                                int32_t cap, int64_t first_event, int32_t b, int32_t nb,
                                float *mem_new, double *new_mem_ts, int64_t *winner, float *h,
                                const tgm_sample_buffers *next_sb, int32_t mit_slot,
-                               hipStream_t s);
+                               uint64_t *xwin, uint64_t xtag, hipStream_t s);
+
+// The executor's latest-message reduce of an iteration, on the prefetch
+// stream beside its sample: exec_latest_reserve makes nslots key arrays of
+// cap entries (it may allocate; contents of existing arrays are dropped);
+// exec_latest_launch reduces the 2b candidates of the batch into array `slot`
+// under a fresh tag and returns the array and the tag, which
+// compute_iteration's staging then reads.
+tgm_status_t exec_latest_reserve(tgm_state_t st, int32_t nslots, int32_t cap);
+tgm_status_t exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b, const int32_t *src_pos,
+                                const int32_t *dst_pos, const int32_t *n_nodes, hipStream_t s,
+                                uint64_t **win, uint64_t *tag);
 
 // The mitigation of tgm_mitigate in two parts.  mitigate_prep_launch writes
 // the neighbour sets of a node set into slot `slot` (it needs the graph and

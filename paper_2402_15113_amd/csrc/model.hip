@@ -195,6 +195,13 @@ __device__ __forceinline__ void latest_reduce(const GruArgs &g, int n)
                   (unsigned long long)(g.tag | (uint64_t)c));
 }
 
+// The latest-message reduce on its own (the executor runs it on the prefetch
+// stream): only the reduce fields of g are read.
+__global__ __launch_bounds__(256) void k_latest(GruArgs g)
+{
+    latest_reduce(g, *g.n_nodes);
+}
+
 template <int W, int CM, int CH, int NG>
 __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_has,
                                          double *s_nts)
@@ -2099,7 +2106,7 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
                           const int32_t *ver, int64_t first_event, int32_t b,
                           const int32_t *src_pos, const int32_t *dst_pos, float *mem_new,
                           double *new_mem_ts, hipStream_t s, StageArgs *sa, int *n_items,
-                          uint64_t *tag_out)
+                          uint64_t *tag_out, uint64_t *ext_win = nullptr, uint64_t ext_tag = 0)
 {
     if (!st || !m || !g || !n_nodes || cap < 0 || b < 0 || first_event < 0 ||
         first_event + b > g->E)
@@ -2119,11 +2126,17 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
     const int slots = st->s + 1;
     if (iter - slots > st->committed_through)
         return TGM_EORDER;   // the slot still holds an uncommitted write set
-    if (st->win_tag == UINT32_MAX) {   // keys restart from zero
-        TGM_LAUNCH(k_fill_u64, dim3(cdiv(st->N, 256)), dim3(256), 0, s, st->win, st->N);
-        st->win_tag = 0;
+    // the keys of this update's latest-message reduce: the state's array, or
+    // one the executor reduced already (ext_win; the GRU then skips the reduce)
+    uint64_t *win = ext_win ? ext_win : st->win;
+    uint64_t tag = ext_tag;
+    if (!ext_win) {
+        if (st->win_tag == UINT32_MAX) {   // keys restart from zero
+            TGM_LAUNCH(k_fill_u64, dim3(cdiv(st->N, 256)), dim3(256), 0, s, st->win, st->N);
+            st->win_tag = 0;
+        }
+        tag = (uint64_t)(++st->win_tag) << 32;
     }
-    const uint64_t tag = (uint64_t)(++st->win_tag) << 32;
     const int n_cand = 2 * b;
     if (cap > 0) {
         GruArgs ga;
@@ -2132,8 +2145,8 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
         ga.bias = m->gru_bias; ga.omega = m->omega; ga.beta = m->beta; ga.M = m->M;
         ga.D_m = m->D_m; ga.D_t = m->D_t; ga.KXC = m->KXC; ga.KHC = m->KHC; ga.MB = m->MB;
         ga.mem_new = mem_new; ga.new_mem_ts = new_mem_ts;
-        ga.n_cand = n_cand; ga.src_pos = src_pos; ga.dst_pos = dst_pos; ga.win = st->win;
-        ga.tag = tag;
+        ga.n_cand = ext_win ? 0 : n_cand; ga.src_pos = src_pos; ga.dst_pos = dst_pos;
+        ga.win = win; ga.tag = tag;
         // persistent: the node set's tasks are split over kGruGrid workgroups
         if (m->kind == TGM_MODEL_JODIE)
             TGM_LAUNCH(k_gru<1>, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
@@ -2156,7 +2169,7 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
     a.first = first_event; a.iter = iter; a.c_iter = cj;
     a.M = m->M; a.D_m = m->D_m; a.D_e = m->D_e; a.direct = direct;
     a.n_nodes = n_nodes; a.src = g->src; a.dst = g->dst; a.src_pos = src_pos;
-    a.dst_pos = dst_pos; a.win = st->win; a.tag = tag; a.ver = ver;
+    a.dst_pos = dst_pos; a.win = win; a.tag = tag; a.ver = ver;
     a.t = g->t; a.mem_ts = mem_ts; a.mail_ts = mail_ts; a.efeat = g->efeat;
     a.mem_new = mem_new;
     a.r_flag = st->r_flag + base; a.r_node = st->r_node + base;
@@ -2185,12 +2198,12 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
     return TGM_OK;
 }
 
-tgm_status_t update_winner(tgm_state_t st, const int32_t *n_nodes, int32_t cap,
+tgm_status_t update_winner(const uint64_t *win, const int32_t *n_nodes, int32_t cap,
                            int64_t first_event, uint64_t tag, int64_t *winner, hipStream_t s)
 {
     if (winner && cap > 0)
         TGM_LAUNCH(k_winner_out, dim3(cdiv(cap, 256)), dim3(256), 0, s, n_nodes, cap,
-                   first_event, st->win, tag, winner);
+                   first_event, win, tag, winner);
     return TGM_OK;
 }
 
@@ -2305,7 +2318,7 @@ extern "C" tgm_status_t tgm_update_memory(tgm_state_t st, tgm_model_t m, tgm_gra
         return rc;
     if (n_items > 0)
         TGM_LAUNCH(k_stage, dim3(cdiv(n_items, 4)), dim3(256), 0, s, sa);
-    return update_winner(st, n_nodes, cap, first_event, tag, winner, s);
+    return update_winner(st->win, n_nodes, cap, first_event, tag, winner, s);
 }
 
 extern "C" tgm_status_t tgm_embed(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
@@ -2364,7 +2377,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
                                     int32_t cap, int64_t first_event, int32_t b, int32_t nb,
                                     float *mem_new, double *new_mem_ts, int64_t *winner,
                                     float *h, const tgm_sample_buffers *next_sb,
-                                    int32_t mit_slot, hipStream_t s)
+                                    int32_t mit_slot, uint64_t *xwin, uint64_t xtag,
+                                    hipStream_t s)
 {
     if (st && st->mit)   // the mitigation of this iteration's fetched memories
         TGM_TRY_STATUS(mitigate_launch(st->mit, g, first_event, sb.nodes, sb.n_nodes, cap,
@@ -2379,7 +2393,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     double *nts = jodie && !new_mem_ts ? m->nts : new_mem_ts;
     tgm_status_t rc = update_begin(st, m, g, iter, sb.n_nodes, cap, fb.mem, fb.mem_ts, fb.mail,
                                    fb.mail_ts, fb.ver, first_event, b, sb.root_pos,
-                                   sb.root_pos + b, mem_new, nts, s, &sa, &n_items, &tag);
+                                   sb.root_pos + b, mem_new, nts, s, &sa, &n_items, &tag,
+                                   xwin, xtag);
     if (rc != TGM_OK)
         return rc;
     if (jodie) {
@@ -2398,7 +2413,7 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
         }
         if (n_items > 0)
             TGM_LAUNCH(k_stage, dim3((unsigned)cdiv(n_items, 4)), dim3(256), 0, s, sa);
-        TGM_TRY_STATUS(update_winner(st, sb.n_nodes, cap, first_event, tag, winner, s));
+        TGM_TRY_STATUS(update_winner(sa.win, sb.n_nodes, cap, first_event, tag, winner, s));
         const int n_tp = (int)cdiv((int64_t)R * m->M, 256);
         if (has_next)
             TGM_LAUNCH(k_tproj_gather, dim3((unsigned)(n_tp + kCUs)), dim3(256), 0, s, ta, n_tp,
@@ -2431,8 +2446,62 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     if (R > 0 || n_items > 0)
         TGM_LAUNCH(k_stage_proj, dim3((R > 0 ? proj_grid : 0) + n_stage_blocks),
                    dim3(64 * proj_waves), proj_lds(m), s, sa, pa, R > 0 ? proj_grid : 0);
-    TGM_TRY_STATUS(update_winner(st, sb.n_nodes, cap, first_event, tag, winner, s));
+    TGM_TRY_STATUS(update_winner(sa.win, sb.n_nodes, cap, first_event, tag, winner, s));
     if (R > 0)
         return launch_attn(m, aa, next, s);
     return next ? launch_gather(*next, s) : TGM_OK;
+}
+
+tgm_status_t tgm::exec_latest_reserve(tgm_state_t st, int32_t nslots, int32_t cap)
+{
+    if (!st || nslots < 1 || cap < 0)
+        return TGM_EINVAL;
+    if (nslots <= st->xwin_slots && cap <= st->xwin_cap)
+        return TGM_OK;
+    if (st->xwin && hipDeviceSynchronize() != hipSuccess)
+        return TGM_EDEVICE;
+    (void)hipFree(st->xwin);
+    st->xwin = nullptr;
+    st->xwin_slots = st->xwin_cap = 0;
+    const int32_t c = std::max(cap, 1);
+    const size_t bytes = sizeof(uint64_t) * (size_t)nslots * c;
+    if (hipMalloc((void **)&st->xwin, bytes) != hipSuccess)
+        return TGM_ENOMEM;
+    // zero keys are older than every tag; a synchronous clear (set-up only)
+    if (hipMemset(st->xwin, 0, bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
+        return TGM_EDEVICE;
+    st->xwin_slots = nslots;
+    st->xwin_cap = c;
+    st->xwin_tag = 0;
+    return TGM_OK;
+}
+
+tgm_status_t tgm::exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b,
+                                     const int32_t *src_pos, const int32_t *dst_pos,
+                                     const int32_t *n_nodes, hipStream_t s, uint64_t **win,
+                                     uint64_t *tag)
+{
+    if (!st || slot < 0 || slot >= st->xwin_slots || b < 0 || !n_nodes || !win || !tag)
+        return TGM_EINVAL;
+    if (st->xwin_tag == UINT32_MAX) {   // keys restart from zero in every array
+        const int64_t n = (int64_t)st->xwin_slots * st->xwin_cap;
+        TGM_LAUNCH(k_fill_u64, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, st->xwin, (int32_t)n);
+        st->xwin_tag = 0;
+    }
+    *tag = (uint64_t)(++st->xwin_tag) << 32;
+    *win = st->xwin + (size_t)slot * st->xwin_cap;
+    const int n_cand = 2 * b;
+    if (n_cand == 0)
+        return TGM_OK;
+    if (!src_pos || !dst_pos)
+        return TGM_EINVAL;
+    GruArgs ga;
+    ga.n_nodes = n_nodes;
+    ga.n_cand = n_cand;
+    ga.src_pos = src_pos;
+    ga.dst_pos = dst_pos;
+    ga.win = *win;
+    ga.tag = *tag;
+    TGM_LAUNCH(k_latest, dim3((unsigned)cdiv(n_cand, 256)), dim3(256), 0, s, ga);
+    return TGM_OK;
 }

@@ -9,6 +9,8 @@
 // streams synchronise once per chunk, not once per iteration.
 #include <hip/hip_runtime.h>
 
+#include <vector>
+
 #include "common.h"
 
 using namespace tgm;
@@ -65,6 +67,11 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     // the sample, into mitigator slot 1 + (k % nsb)
     if (st->mit)
         TGM_TRY_STATUS(mitigate_reserve(st->mit, 1 + nsb));
+    // the latest-message reduce of each batch also runs beside its sample,
+    // into key array k % nsb (so the update's GRU launch skips it)
+    TGM_TRY_STATUS(exec_latest_reserve(st, nsb, cap));
+    std::vector<uint64_t *> xwin(nsb, nullptr);
+    std::vector<uint64_t> xtag(nsb, 0);
     auto sample_chunk = [&](int64_t c) -> tgm_status_t {
         for (int64_t k = c * K; k < std::min(n, (c + 1) * K); ++k) {
             int64_t lo = 0;
@@ -76,6 +83,9 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             if (st->mit)
                 TGM_TRY_STATUS(mitigate_prep_launch(st->mit, g, lo, s.nodes, s.n_nodes, cap,
                                                     (int32_t)(1 + k % nsb), pre));
+            TGM_TRY_STATUS(exec_latest_launch(st, (int32_t)(k % nsb), b, s.root_pos,
+                                              s.root_pos + b, s.n_nodes, pre, &xwin[k % nsb],
+                                              &xtag[k % nsb]));
         }
         TGM_HIP(hipEventRecord(ev.e[c & 1], pre));
         return TGM_OK;
@@ -107,7 +117,8 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             TGM_TRY_STATUS(compute_iteration(st, m, g, i0 + k, sb[k % nsb], *fb, cap, lo, b, nb,
                                              mem_new, new_mem_ts, winner, h,
                                              more ? &sb[(k + 1) % nsb] : nullptr,
-                                             (int32_t)(1 + k % nsb), main));
+                                             (int32_t)(1 + k % nsb), xwin[k % nsb],
+                                             xtag[k % nsb], main));
         }
         TGM_HIP(hipEventRecord(ev.e[2 + (c & 1)], main));
     }

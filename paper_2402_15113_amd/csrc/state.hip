@@ -125,6 +125,7 @@ extern "C" tgm_status_t tgm_state_destroy(tgm_state_t st)
     hipFree(st->r_mem_ts);
     hipFree(st->r_mail_ts);
     hipFree(st->win);
+    hipFree(st->xwin);
     delete st;
     return TGM_OK;
 }
