@@ -126,7 +126,7 @@ def account(sched, W, K):
     return rows, seq
 
 
-def window_setup(name, first, L, w, mitigation=None):
+def window_setup(name, first, L, w, mitigation=None, s=None):
     """Stage for batches first .. first + L - 1 of a large stream: the graph of
     every event up to the window's end, a device feature table that holds the
     generator's rows from the oldest event the window samples onwards (zero
@@ -140,7 +140,7 @@ def window_setup(name, first, L, w, mitigation=None):
     from paper_2402_15113_amd.stage import Stage
     from workloads import CONFIGS, FEAT_CHUNK, edge_feature_rows, make_workload
 
-    full = make_workload(name, with_features=False)
+    full = make_workload(name, with_features=False, s=s)
     E_end = min(full.E, (first + L) * full.B)
     wl = dataclasses.replace(full, src=full.src[:E_end], dst=full.dst[:E_end],
                              t=full.t[:E_end], neg=full.neg[:E_end])
@@ -336,6 +336,10 @@ def main():
     ap.add_argument("--mitigate", default=None, metavar="P,LAMBDA,K",
                     help="similarity-based staleness mitigation on every fetch (MSPipe-S, "
                          "off by default), e.g. 0.99,0.95,10")
+    ap.add_argument("--staleness", default="config", metavar="config|auto|S",
+                    help="s of the run: the workload's (config), a number, or auto: the "
+                         "minimal staleness (Sec. 3.2) solved from stage times profiled on a "
+                         "calibration stage of its own before the run")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
@@ -369,18 +373,35 @@ def main():
     if args.mitigate:
         pq, lam, kk = args.mitigate.split(",")
         mit = dict(p=float(pq), lam=float(lam), K=int(kk))
-    if window:
-        from workloads import CONFIGS
-        c = CONFIGS["gdelt"]
-        w = make_weights(c["M"], c["D_e"], c["D_t"], model=args.model)
-        wl, stage, init = window_setup("gdelt", args.first, W + K, w, mit)
-        sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
+    def build(s):
+        if window:
+            from workloads import CONFIGS
+            c = CONFIGS["gdelt"]
+            w = make_weights(c["M"], c["D_e"], c["D_t"], model=args.model)
+            wl, stage, init = window_setup("gdelt", args.first, W + K, w, mit, s=s)
+            sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
+        else:
+            wl = make_workload(args.workload, s=s)
+            w = make_weights(wl.M, wl.D_e, wl.D_t, model=args.model)
+            stage = from_workload(wl, w, mitigation=mit)
+            sched = Schedule(stage, wl.n_iters)
         sched.restart()
+        return wl, w, stage, sched
+
+    calib = None
+    if args.staleness == "auto":
+        # the paper's procedure: profile a few iterations, solve for k, run
+        # with it (the calibration stage is discarded: its steps moved its state)
+        from paper_2402_15113_amd.stage import calibrate_staleness
+        wl, w, stage, sched = build(None)
+        calib = calibrate_staleness(stage, first=sched.first)
+        stage.close()
+        del stage, sched
+        log(f"calibrated staleness: k_min {calib['k_min']} -> s {calib['s']} "
+            f"(tau us {calib['tau_us']})")
+        wl, w, stage, sched = build(calib["s"])
     else:
-        wl = make_workload(args.workload)
-        w = make_weights(wl.M, wl.D_e, wl.D_t, model=args.model)
-        stage = from_workload(wl, w, mitigation=mit)
-        sched = Schedule(stage, wl.n_iters)
+        wl, w, stage, sched = build(None if args.staleness == "config" else int(args.staleness))
     log(f"workload {wl.name}: N={wl.N} E={wl.E} B={wl.B} s={wl.s} iters={wl.n_iters}")
     stage.want_winner = False
     if args.copy_probe_mib > 0:
@@ -413,6 +434,10 @@ def main():
                       "staleness": wl.s, "graph": wl.meta.get("graph", ""),
                       "pipeline": "two streams: sample + node set + fetch of batch i+1 beside "
                                   "update + embed of batch i"}}
+    out["config"]["staleness_source"] = {"config": "workload", "auto": "minimal-staleness bound"}.get(
+        args.staleness, "argument")
+    if calib is not None:
+        out["staleness_calibration"] = calib
     if mit is not None:
         out["config"]["mitigation"] = dict(mit, kind="MSPipe-S similarity-based, every fetch")
     if args.model != "tgn":

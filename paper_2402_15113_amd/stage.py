@@ -259,3 +259,29 @@ def minimal_staleness(tau_us, k_max: int = 16, n: int = 64) -> dict:
             "k_min": int(k[-1]), "s_equivalent": int(k[-1]) - 1,
             "stall_free": bool(stall[-1] == 0.0), "k_max": k_max}
 
+
+
+def calibrate_staleness(stage: Stage, first: int = 0, *, warm: int = 3, iters: int = 12,
+                        k_max: int = 16) -> dict:
+    """The online half of the bound (Sec. 3.2; App. D.1 profiles a few
+    iterations before training): `warm` untimed sequential steps of `stage`
+    from batch `first` on, then `iters` profiled ones, their kernel durations
+    mapped to the five stages, and the steady-state minimal staleness solved
+    from them.  Adds "s", the staleness this library's state takes for it
+    (k_min - 1).  The steps advance the stage's state, so the run that uses
+    the result is built afresh with that s: calibrate on a stage of its own."""
+    for i in range(first, first + warm):
+        stage.step(i)
+    torch.cuda.synchronize()
+    tgm.tgm_profile_reset()
+    tgm.tgm_profile_enable(True)
+    try:
+        for i in range(first + warm, first + warm + iters):
+            stage.step(i)
+        torch.cuda.synchronize()
+    finally:
+        tgm.tgm_profile_enable(False)
+    res = minimal_staleness(stage_durations_us(tgm.tgm_profile_read(), iters), k_max=k_max)
+    res["s"] = max(res["k_min"] - 1, 0)
+    res["calibration"] = {"first": first, "warm": warm, "iters": iters}
+    return res

@@ -44,3 +44,23 @@ def test_bound_from_measured_stage_times(mitigation):
     assert res["k_min"] == ref[-1][0] >= 1
     assert res["stall_free"] == (ref[-1][2] == 0.0)
     st.close()
+
+
+def test_calibrated_staleness_drives_the_run(orc):
+    """The online schedule: the bound solved from a calibration stage's
+    profiled steps sets the s of a fresh run, which matches the oracle at that
+    s (and the pipelined executor runs it as well)."""
+    from paper_2402_15113_amd.stage import calibrate_staleness, from_workload
+    from test_gpu_parity import run_pair
+    wl = make_workload("tiny", E=8000)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    cal_stage = from_workload(wl, w)
+    cal = calibrate_staleness(cal_stage)
+    cal_stage.close()
+    print("calibrated:", cal, flush=True)
+    assert cal["s"] == cal["k_min"] - 1 >= 0
+    assert cal["calibration"] == {"first": 0, "warm": 3, "iters": 12}
+    assert min_staleness([cal["tau_us"][k] for k in ("sample", "feature_fetch", "memory_fetch",
+                                                     "compute", "memory_update")],
+                         64, 16)[-1][0] == cal["k_min"]
+    run_pair(orc, make_workload("tiny", E=8000, s=cal["s"]), w, s=cal["s"])
