@@ -165,6 +165,25 @@ tgm_status_t tgm_state_read(tgm_state_t st, float *mem, double *mem_ts, float *m
 tgm_status_t tgm_state_load(tgm_state_t st, int64_t iter, const float *mem, const double *mem_ts,
                             const float *mail, const double *mail_ts, const int32_t *ver,
                             void *stream);
+/* Checkpoint and resume of the whole versioned state (Alg. 1's state between
+ * iterations): the committed tables, the staged write sets that no fetch has
+ * needed yet (up to s + 1 of them) and the protocol counters, so that a run
+ * resumed from a checkpoint gives bit for bit the results of the run that
+ * was not interrupted.  The checkpoint is a HOST buffer of
+ * tgm_state_checkpoint_bytes bytes (owned by the caller; a self-describing
+ * layout with a magic number and format version).  tgm_state_save orders
+ * its copies after the work already on `stream` and returns once they are
+ * done; no other stream may be writing the state meanwhile.
+ * tgm_state_restore loads a checkpoint into a state created with the same
+ * N, M, D_m, s and max_batch (else TGM_EINVAL; a bad magic, format or
+ * counters that the protocol cannot reach also give TGM_EINVAL) and returns
+ * once the tables are on the device.  A buffer shorter than the checkpoint
+ * gives TGM_ESIZE.  The next call continues the protocol where the saved
+ * state was: a fetch of last_fetch or later, or the update after the last
+ * staged one. */
+tgm_status_t tgm_state_checkpoint_bytes(tgm_state_t st, size_t *bytes);
+tgm_status_t tgm_state_save(tgm_state_t st, void *buf, size_t bytes, void *stream);
+tgm_status_t tgm_state_restore(tgm_state_t st, const void *buf, size_t bytes, void *stream);
 
 /* Memory fetch of iteration `iter` (Alg. 1's fetch_memory, after its wait
  * until the update of iteration iter-k is done, with k = s + 1).  First commits

@@ -261,3 +261,144 @@ extern "C" tgm_status_t tgm_fetch_memory(tgm_state_t st, int64_t iter, const int
         fetch_plan(st, iter, nodes, n_nodes, cap, mem, mem_ts, mail, mail_ts, ver, s, &plan);
     return rc != TGM_OK ? rc : launch_gather(plan, s);
 }
+
+// ============================================================== checkpoints
+//
+// A checkpoint is the whole versioned state: the committed tables, the ring
+// of staged write sets (the s pending updates a fetch has not needed yet) and
+// the protocol counters.  Layout (host bytes, every section 8-byte aligned):
+//   int64 header[kCkptHeader]: magic, format, N, M, D_m, s, max_batch,
+//         committed_through, staged_through, last_fetch, slots (= s + 1)
+//   int64 slot[slots][3]: iteration, b, staged
+//   mem [N x M] f32, mem_ts [N] f64, mail [N x D_m] f32, mail_ts [N] f64,
+//   ver [N] i32, then the ring rows (slots x 2 max_batch rows): r_flag i32,
+//   r_node i32, r_mem [x M] f32, r_mail [x D_m] f32, r_mem_ts f64,
+//   r_mail_ts f64.
+// The latest-message keys (win, xwin) are not part of it: they are scratch of
+// one update call, filtered by a tag that only grows in the state they live in.
+
+namespace {
+
+constexpr int64_t kCkptMagic = 0x74676d2d636b7074LL;   // "tgm-ckpt"
+constexpr int64_t kCkptFormat = 1;
+constexpr int kCkptHeader = 11;
+
+struct CkptSection {
+    void *dev;
+    size_t bytes;
+};
+
+size_t align8(size_t x) { return (x + 7) & ~(size_t)7; }
+
+// the device arrays of a state in checkpoint order
+std::vector<CkptSection> ckpt_sections(const tgm_state *st)
+{
+    const size_t N = st->N, M = st->M, Dm = st->D_m;
+    const size_t rows = (size_t)(st->s + 1) * st->ring_rows();
+    return {{st->mem, sizeof(float) * N * M},       {st->mem_ts, sizeof(double) * N},
+            {st->mail, sizeof(float) * N * Dm},     {st->mail_ts, sizeof(double) * N},
+            {st->ver, sizeof(int32_t) * N},         {st->r_flag, sizeof(int32_t) * rows},
+            {st->r_node, sizeof(int32_t) * rows},   {st->r_mem, sizeof(float) * rows * M},
+            {st->r_mail, sizeof(float) * rows * Dm}, {st->r_mem_ts, sizeof(double) * rows},
+            {st->r_mail_ts, sizeof(double) * rows}};
+}
+
+size_t ckpt_meta_bytes(const tgm_state *st)
+{
+    return sizeof(int64_t) * (kCkptHeader + 3 * (size_t)(st->s + 1));
+}
+
+size_t ckpt_bytes(const tgm_state *st)
+{
+    size_t b = ckpt_meta_bytes(st);
+    for (const CkptSection &c : ckpt_sections(st))
+        b += align8(c.bytes);
+    return b;
+}
+
+}  // namespace
+
+extern "C" tgm_status_t tgm_state_checkpoint_bytes(tgm_state_t st, size_t *bytes)
+{
+    if (!st || !bytes)
+        return TGM_EINVAL;
+    *bytes = ckpt_bytes(st);
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_state_save(tgm_state_t st, void *buf, size_t bytes, void *stream)
+{
+    if (!st || !buf)
+        return TGM_EINVAL;
+    if (bytes < ckpt_bytes(st))
+        return TGM_ESIZE;
+    hipStream_t s = as_stream(stream);
+    char *p = static_cast<char *>(buf);
+    int64_t *h = reinterpret_cast<int64_t *>(p);
+    const int64_t head[kCkptHeader] = {kCkptMagic,          kCkptFormat,        st->N,
+                                       st->M,               st->D_m,            st->s,
+                                       st->max_batch,       st->committed_through,
+                                       st->staged_through,  st->last_fetch,     st->s + 1};
+    for (int k = 0; k < kCkptHeader; ++k)
+        h[k] = head[k];
+    for (int j = 0; j <= st->s; ++j) {
+        h[kCkptHeader + 3 * j] = st->ring[j].iter;
+        h[kCkptHeader + 3 * j + 1] = st->ring[j].b;
+        h[kCkptHeader + 3 * j + 2] = st->ring[j].staged ? 1 : 0;
+    }
+    p += ckpt_meta_bytes(st);
+    for (const CkptSection &c : ckpt_sections(st)) {
+        if (c.bytes)
+            TGM_HIP(hipMemcpyAsync(p, c.dev, c.bytes, hipMemcpyDeviceToHost, s));
+        p += align8(c.bytes);
+    }
+    TGM_HIP(hipStreamSynchronize(s));
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_state_restore(tgm_state_t st, const void *buf, size_t bytes,
+                                          void *stream)
+{
+    if (!st || !buf)
+        return TGM_EINVAL;
+    if (bytes < sizeof(int64_t) * kCkptHeader)
+        return TGM_ESIZE;
+    const int64_t *h = static_cast<const int64_t *>(buf);
+    if (h[0] != kCkptMagic || h[1] != kCkptFormat || h[2] != st->N || h[3] != st->M ||
+        h[4] != st->D_m || h[5] != st->s || h[6] != st->max_batch || h[10] != st->s + 1)
+        return TGM_EINVAL;
+    if (bytes < ckpt_bytes(st))
+        return TGM_ESIZE;
+    // the counters must describe a state the protocol can reach
+    const int64_t committed = h[7], staged = h[8], last_fetch = h[9];
+    if (committed < -1 || staged < committed || staged - committed > st->s + 1)
+        return TGM_EINVAL;
+    std::vector<tgm_state::Slot> ring(st->s + 1);
+    for (int j = 0; j <= st->s; ++j) {
+        const int64_t it = h[kCkptHeader + 3 * j], b = h[kCkptHeader + 3 * j + 1],
+                      on = h[kCkptHeader + 3 * j + 2];
+        if (b < 0 || b > st->max_batch || (on != 0 && on != 1))
+            return TGM_EINVAL;
+        ring[j].iter = it;
+        ring[j].b = (int32_t)b;
+        ring[j].staged = on == 1;
+    }
+    for (int64_t j = committed + 1; j <= staged; ++j) {
+        const tgm_state::Slot &sl = ring[j % (st->s + 1)];
+        if (!sl.staged || sl.iter != j)
+            return TGM_EINVAL;
+    }
+    hipStream_t s = as_stream(stream);
+    const char *p = static_cast<const char *>(buf) + ckpt_meta_bytes(st);
+    for (const CkptSection &c : ckpt_sections(st)) {
+        if (c.bytes)
+            TGM_HIP(hipMemcpyAsync(c.dev, p, c.bytes, hipMemcpyHostToDevice, s));
+        p += align8(c.bytes);
+    }
+    TGM_HIP(hipStreamSynchronize(s));
+    st->ring = ring;
+    st->committed_through = committed;
+    st->staged_through = staged;
+    st->last_fetch = last_fetch;
+    return TGM_OK;
+}

@@ -218,6 +218,19 @@ class Stage:
         torch.cuda.synchronize(dev)
 
 
+    def save_checkpoint(self):
+        """The versioned state's checkpoint (host uint8 array: committed
+        tables, staged write sets, protocol counters) after the work issued
+        so far on the stage's stream."""
+        return tgm.tgm_state_save(self.st, stream=self.stream)
+
+    def restore_checkpoint(self, buf):
+        """Continue from a checkpoint of a stage with the same N, M, D_m, s
+        and batch size: the next step or run takes the iteration after the
+        checkpoint's last update."""
+        tgm.tgm_state_restore(self.st, buf, stream=self.stream)
+
+
 def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None) -> Stage:
     return Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, wl.efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
                  nb=wl.nb, B=wl.B, s=wl.s if s is None else s, device=device, stream=stream,

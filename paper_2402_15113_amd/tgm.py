@@ -21,7 +21,8 @@ TGM_OK, TGM_EINVAL, TGM_ERANGE, TGM_EORDER, TGM_ESIZE, TGM_EDEVICE, TGM_ENOMEM =
 SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_create",
            "tgm_graph_destroy", "tgm_graph_info", "tgm_batch_roots", "tgm_sample", "tgm_sample_batch",
            "tgm_node_set", "tgm_sample_nodes", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
-           "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_fetch_memory",
+           "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_state_checkpoint_bytes",
+           "tgm_state_save", "tgm_state_restore", "tgm_fetch_memory",
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
            "tgm_stage_run", "tgm_mitigator_create", "tgm_mitigator_destroy", "tgm_mitigate",
            "tgm_mitigator_read", "tgm_state_set_mitigation", "tgm_min_staleness",
@@ -96,6 +97,9 @@ def lib():
             "tgm_state_flush": [V, V],
             "tgm_state_read": [V, P, P, P, P, P, V],
             "tgm_state_load": [V, I64, P, P, P, P, P, V],
+            "tgm_state_checkpoint_bytes": [V, C.POINTER(C.c_size_t)],
+            "tgm_state_save": [V, P, C.c_size_t, V],
+            "tgm_state_restore": [V, P, C.c_size_t, V],
             "tgm_fetch_memory": [V, I64, P, P, I32, P, P, P, P, P, V],
             "tgm_model_create": [C.POINTER(ModelDesc), C.POINTER(Weights), V, C.POINTER(V)],
             "tgm_model_destroy": [V],
@@ -253,6 +257,30 @@ def tgm_state_read(st, mem, mem_ts, mail, mail_ts, ver, stream=None):
 def tgm_state_load(st, it, mem, mem_ts, mail, mail_ts, ver, stream=None):
     _check("tgm_state_load", lib().tgm_state_load(st, it, _p(mem), _p(mem_ts), _p(mail),
                                                   _p(mail_ts), _p(ver), _s(stream)))
+
+
+def tgm_state_checkpoint_bytes(st) -> int:
+    n = C.c_size_t(0)
+    _check("tgm_state_checkpoint_bytes", lib().tgm_state_checkpoint_bytes(st, C.byref(n)))
+    return n.value
+
+
+def tgm_state_save(st, stream=None, nbytes=None):
+    """The state's checkpoint as a host uint8 array (after the work already on
+    `stream`; returns once it is copied)."""
+    import numpy as np
+    n = tgm_state_checkpoint_bytes(st) if nbytes is None else nbytes
+    buf = np.zeros(n, dtype=np.uint8)
+    _check("tgm_state_save", lib().tgm_state_save(st, buf.ctypes.data, n, _s(stream)))
+    return buf
+
+
+def tgm_state_restore(st, buf, stream=None):
+    """Load a checkpoint (a contiguous host uint8 array) into st."""
+    import numpy as np
+    buf = np.ascontiguousarray(buf, dtype=np.uint8)
+    _check("tgm_state_restore", lib().tgm_state_restore(st, buf.ctypes.data, buf.nbytes,
+                                                        _s(stream)))
 
 
 def tgm_fetch_memory(st, it, nodes, n_nodes, cap, mem, mem_ts, mail, mail_ts, ver, stream=None):

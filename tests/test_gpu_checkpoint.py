@@ -1,0 +1,121 @@
+"""Checkpoint and resume of the versioned state (tgm_state_save /
+tgm_state_restore): a run stopped after iteration k-1, saved, and resumed in
+a fresh state from the checkpoint gives bit for bit the outputs and final
+tables of the run that was not stopped (which the parity tests compare with
+the oracle).  With s > 0 the checkpoint holds staged write sets that no fetch
+has needed yet, so the resumed run commits them itself."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from workloads import make_weights, make_workload  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2402_15113_amd import tgm
+    tgm.lib()
+
+
+def _same(a, b):
+    assert a.keys() == b.keys()
+    for k in a:
+        assert np.array_equal(np.asarray(a[k]), np.asarray(b[k])), k
+
+
+@pytest.mark.parametrize("s,k", [(0, 7), (2, 9), (3, 1)])
+def test_resume_equals_uninterrupted_sequential(s, k):
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=6000, s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    n = wl.n_iters
+    print(f"[ckpt] tiny s={s} stop after {k}, iters {n}", flush=True)
+    a = from_workload(wl, w)
+    want = []
+    for i in range(n):
+        a.step(i)
+        if i >= k:
+            want.append(a.outputs())
+    a.flush()
+    final = a.state()
+    a.close()
+    b = from_workload(wl, w)
+    for i in range(k):
+        b.step(i)
+    ck = b.save_checkpoint()
+    b.close()
+    c = from_workload(wl, w)
+    c.restore_checkpoint(ck)
+    for i in range(k, n):
+        c.step(i)
+        _same(c.outputs(), want[i - k])
+    c.flush()
+    _same(c.state(), final)
+    c.close()
+
+
+@pytest.mark.parametrize("name,s,E,k", [("tiny", 2, None, 13), ("wiki", 1, 30_000, 24)])
+def test_resume_equals_uninterrupted_pipelined(name, s, E, k):
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload(name, E=E, s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    n = wl.n_iters
+    print(f"[ckpt] pipelined {name} s={s} stop after {k}, iters {n}", flush=True)
+    a = from_workload(wl, w)
+    a.run(0, n)
+    out = a.outputs()
+    a.flush()
+    final = a.state()
+    a.close()
+    b = from_workload(wl, w)
+    b.run(0, k)
+    ck = b.save_checkpoint()
+    b.close()
+    c = from_workload(wl, w)
+    c.restore_checkpoint(ck)
+    c.run(k, n - k)
+    _same(c.outputs(), out)
+    c.flush()
+    _same(c.state(), final)
+    c.close()
+
+
+def test_checkpoint_argument_errors():
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=3000, s=1)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    a = from_workload(wl, w)
+    for i in range(4):
+        a.step(i)
+    ck = a.save_checkpoint()
+    assert ck.nbytes == tgm.tgm_state_checkpoint_bytes(a.st)
+
+    def code(fn):
+        with pytest.raises(tgm.TgmError) as e:
+            fn()
+        return e.value.code
+
+    assert code(lambda: tgm.tgm_state_save(a.st, stream=a.stream, nbytes=ck.nbytes - 8)) == \
+        tgm.TGM_ESIZE
+    assert code(lambda: a.restore_checkpoint(ck[:-8])) == tgm.TGM_ESIZE
+    bad = ck.copy()
+    bad[0] ^= 1                                   # magic
+    assert code(lambda: a.restore_checkpoint(bad)) == tgm.TGM_EINVAL
+    bad = ck.copy().view(np.int64)
+    bad[8] = bad[7] - 1                           # staged before committed
+    assert code(lambda: a.restore_checkpoint(bad.view(np.uint8))) == tgm.TGM_EINVAL
+    other = from_workload(wl, w, s=2)             # another staleness
+    assert code(lambda: other.restore_checkpoint(ck)) == tgm.TGM_EINVAL
+    other.close()
+    # a failed restore leaves the state as it was: the run continues
+    a.step(4)
+    a.restore_checkpoint(ck)                      # and a good one rewinds it
+    a.step(4)
+    torch.cuda.synchronize()
+    a.close()
