@@ -558,15 +558,17 @@ __global__ void k_winner_out(const int32_t *__restrict__ n_nodes, int32_t cap, i
 // computed once per node of the set instead of once per slot.
 constexpr int kProjMaxPC = 8;   // k-chunks of the node projection (K = M <= 128)
 
-// Persistent over 16-row tiles (launched with 4..8 waves); wave w owns column
-// blocks w, w + nw, w + 2nw (a block past the last is a copy of w: it stores
-// the same values) and keeps all their weights in registers, loaded once
-// while the first tile's rows are in flight; the next tile's rows load while
-// a tile multiplies.  Three independent accumulators per wave.
+// Persistent over 16-row tiles.  The PNB column blocks are split into CS
+// contiguous groups of at most nw blocks (launched with nw = 4..8 waves):
+// workgroup b takes group b % CS of tiles b / CS, b / CS + nblk / CS, ...,
+// so a node set of few tiles still spreads over CS times as many CUs.  Wave w
+// owns block w of its group and keeps that block's weights in registers,
+// loaded once while the first tile's rows are in flight; the next tile's rows
+// load while a tile multiplies.  Two accumulators alternate over the k steps.
 template <int W, int C>
 __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ mem_new, int M,
                                                int PC, const f4 *__restrict__ pb, int PNB,
-                                               const float *__restrict__ pbias,
+                                               int CS, const float *__restrict__ pbias,
                                                float *__restrict__ P, float *lds, int bid,
                                                int nblk)
 {
@@ -574,10 +576,10 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
     const int nw = blockDim.x >> 6;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
-    const bool has_cb = wave < PNB;
-    const int cb0 = has_cb ? wave : 0;
-    const int cb1 = wave + nw < PNB ? wave + nw : cb0;
-    const int cb2 = wave + 2 * nw < PNB ? wave + 2 * nw : cb0;
+    const int per = (PNB + CS - 1) / CS;
+    const int lo = (bid % CS) * per, hi = min(PNB, lo + per);
+    const bool has_cb = lo + wave < hi;
+    const int cb = has_cb ? lo + wave : lo;
     const float *arow = lds + (lane & 15) * SA + 4 * (lane >> 4);
 
     // rows of tile row0: wave w takes rows w + nw i (nw >= 4)
@@ -591,21 +593,17 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
             off[i] = (r < 16 && row0 + r < n) ? (int64_t)(row0 + r) * M : -1;
         }
     };
-    int row0 = bid * 16;
+    const int tstep = (nblk / CS) * 16;
+    int row0 = (bid / CS) * 16;
     WaveRows<W, 4, C> x;
     rows_of(row0);
     x.load(mem_new, off, M, lane);
-    f4 w[kProjMaxPC][3];
+    f4 w[kProjMaxPC];
     const int64_t kstep = (int64_t)PNB * kWave;
 #pragma unroll
-    for (int kc = 0; kc < kProjMaxPC; ++kc) {   // chunks past PC reload chunk 0, unused
-        const f4 *p = pb + (int64_t)(kc < PC ? kc : 0) * kstep + lane;
-        w[kc][0] = p[(int64_t)cb0 * kWave];
-        w[kc][1] = p[(int64_t)cb1 * kWave];
-        w[kc][2] = p[(int64_t)cb2 * kWave];
-    }
-    const float e0 = pbias[cb0 * 16 + (lane & 15)], e1 = pbias[cb1 * 16 + (lane & 15)],
-                e2 = pbias[cb2 * 16 + (lane & 15)];
+    for (int kc = 0; kc < kProjMaxPC; ++kc)   // chunks past PC reload chunk 0, unused
+        w[kc] = pb[(int64_t)(kc < PC ? kc : 0) * kstep + (int64_t)cb * kWave + lane];
+    const float e0 = pbias[cb * 16 + (lane & 15)];
     for (;;) {
         __syncthreads();   // the previous tile is done with LDS
         x.store(lds, SA, 0, lr, off, M, lane);
@@ -615,34 +613,28 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
                 for (int k = M + lane; k < K; k += kWave)
                     lds[lr[i] * SA + k] = 0.f;
         __syncthreads();
-        const int next = row0 + nblk * 16;
+        const int next = row0 + tstep;
         if (next < n) {
             rows_of(next);
             x.load(mem_new, off, M, lane);
         }
         if (has_cb) {
-            f4 c0 = {0, 0, 0, 0}, c1 = c0, c2 = c0;
+            f4 c0 = {0, 0, 0, 0}, c1 = c0;
 #pragma unroll
             for (int kc = 0; kc < kProjMaxPC; ++kc) {
                 if (kc < PC) {
                     const f4 a = *reinterpret_cast<const f4 *>(arow + kc * 16);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        c0 = mfma_16x16x4(a[j], w[kc][0][j], c0);
-                        c1 = mfma_16x16x4(a[j], w[kc][1][j], c1);
-                        c2 = mfma_16x16x4(a[j], w[kc][2][j], c2);
-                    }
+                    c0 = mfma_16x16x4(a[0], w[kc][0], c0);
+                    c1 = mfma_16x16x4(a[1], w[kc][1], c1);
+                    c0 = mfma_16x16x4(a[2], w[kc][2], c0);
+                    c1 = mfma_16x16x4(a[3], w[kc][3], c1);
                 }
             }
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int r = row0 + 4 * (lane >> 4) + v;
-                if (r < n) {
-                    float *out = P + (int64_t)r * ldP + (lane & 15);
-                    out[cb0 * 16] = c0[v] + e0;
-                    out[cb1 * 16] = c1[v] + e1;
-                    out[cb2 * 16] = c2[v] + e2;
-                }
+                if (r < n)
+                    P[(int64_t)r * ldP + cb * 16 + (lane & 15)] = (c0[v] + c1[v]) + e0;
             }
         }
         if (next >= n)
@@ -654,7 +646,7 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
 struct ProjArgs {
     const int32_t *n_nodes;
     const float *mem_new;
-    int M, PC, PNB;
+    int M, PC, PNB, CS;   // CS: column groups of the node projection
     const f4 *pb;
     const float *pbias;
     float *P;
@@ -664,12 +656,14 @@ struct ProjArgs {
 __device__ __forceinline__ void node_proj_block(const ProjArgs &a, float *lds, int bid, int nblk)
 {
     const int n = *a.n_nodes;
-    if (bid * 16 >= n)
+    if ((bid / a.CS) * 16 >= n || bid >= (nblk / a.CS) * a.CS)
         return;
     if ((a.M & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mem_new) & 15) == 0)
-        node_proj_body<4, 1>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.pbias, a.P, lds, bid, nblk);
+        node_proj_body<4, 1>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias, a.P, lds, bid,
+                             nblk);
     else
-        node_proj_body<1, 2>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.pbias, a.P, lds, bid, nblk);
+        node_proj_body<1, 2>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias, a.P, lds, bid,
+                             nblk);
 }
 
 __global__ __launch_bounds__(512) void k_node_proj(ProjArgs a)
@@ -2225,8 +2219,12 @@ tgm_status_t embed_plan(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
         return TGM_EINVAL;
     // persistent grid: at most the tiles of the largest node set; every wave
     // owns up to three column blocks
-    *proj_waves = std::max<int>(4, std::min<int>(kMaxWaves, (int)cdiv(m->PNB, 3)));
-    *proj_grid = (int)std::min<int64_t>(cdiv(cap, 16), 512);
+    // column groups of at most kMaxWaves blocks, one block per wave; a grid of
+    // up to 512 workgroups, a multiple of the group count
+    const int CS = (int)cdiv(m->PNB, kMaxWaves);
+    *proj_waves = std::max<int>(4, (int)cdiv(m->PNB, CS));
+    *proj_grid = (int)std::min<int64_t>(cdiv(cap, 16) * CS, 512 / CS * CS);
+    pa->CS = CS;
     pa->n_nodes = n_nodes; pa->mem_new = mem_new; pa->M = m->M; pa->PC = m->PC;
     pa->PNB = m->PNB; pa->pb = m->proj_b; pa->pbias = m->pbias; pa->P = m->P;
     AttnArgs &a = *aa;
