@@ -28,14 +28,20 @@ def _same(a, b):
         assert np.array_equal(np.asarray(a[k]), np.asarray(b[k])), k
 
 
-@pytest.mark.parametrize("s,k", [(0, 7), (2, 9), (3, 1)])
-def test_resume_equals_uninterrupted_sequential(s, k):
+@pytest.mark.parametrize("s,k,model,mit", [(0, 7, "tgn", None), (2, 9, "tgn", None),
+                                           (3, 1, "tgn", None), (2, 11, "jodie", None),
+                                           (1, 10, "tgn", dict(p=0.7, lam=0.9, K=4))])
+def test_resume_equals_uninterrupted_sequential(s, k, model, mit):
     from paper_2402_15113_amd.stage import from_workload
     wl = make_workload("tiny", E=6000, s=s)
-    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, model=model)
     n = wl.n_iters
-    print(f"[ckpt] tiny s={s} stop after {k}, iters {n}", flush=True)
-    a = from_workload(wl, w)
+    print(f"[ckpt] tiny s={s} {model} mitigation={mit} stop after {k}, iters {n}", flush=True)
+
+    def from_workload_(wl, w):
+        return from_workload(wl, w, mitigation=mit)
+
+    a = from_workload_(wl, w)
     want = []
     for i in range(n):
         a.step(i)
@@ -44,12 +50,12 @@ def test_resume_equals_uninterrupted_sequential(s, k):
     a.flush()
     final = a.state()
     a.close()
-    b = from_workload(wl, w)
+    b = from_workload_(wl, w)
     for i in range(k):
         b.step(i)
     ck = b.save_checkpoint()
     b.close()
-    c = from_workload(wl, w)
+    c = from_workload_(wl, w)
     c.restore_checkpoint(ck)
     for i in range(k, n):
         c.step(i)
