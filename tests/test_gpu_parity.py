@@ -159,6 +159,22 @@ def test_tie_heavy_edge_cases(orc, seed, kw):
     run_pair(orc, wl, w)
 
 
+@pytest.mark.parametrize("seed,kw", [
+    (20, dict(M=128, H=2, D_e=256, D_t=128, nb=10, B=9)),   # the documented maxima
+    (21, dict(M=112, H=2, D_e=96, D_t=16, nb=16, B=6)),     # largest folded shape
+    (25, dict(M=112, H=7, D_e=40, D_t=16, nb=16, B=6)),     # 5 roots x 7 heads > 16: unfolded
+    (22, dict(M=16, H=1, D_e=1, D_t=1, nb=17, B=4)),        # smallest dims, nb past 16
+    (23, dict(M=64, H=4, D_e=0, D_t=100, nb=2, B=13, s=0)),
+    (24, dict(M=100, H=2, D_e=172, D_t=100, nb=10, B=8, s=2))])
+def test_shape_limits(orc, seed, kw):
+    """Shapes at the limits the model header states (M <= 128, D_e <= 256,
+    D_e + D_t <= 384, nb <= 64), the boundary of the folded attention (nb <=
+    16, M <= 112) and the smallest dims."""
+    wl = tie_heavy(seed, N=29, E=240, **kw)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, seed=seed, beta="random")
+    run_pair(orc, wl, w)
+
+
 def test_wiki_full_run(orc):
     """The bench workload (WIKI-shaped, B = 600, s = 1), every batch."""
     wl = make_workload("wiki")
