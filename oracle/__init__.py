@@ -86,6 +86,9 @@ def lib():
         L.orc_flush.argtypes = [C.c_void_p]
         L.orc_set_state.argtypes = [C.c_void_p, C.c_int64, _f64p, _f64p, _f64p, _f64p, _i32p]
         L.orc_get_state.argtypes = [C.c_void_p, _f64p, _f64p, _f64p, _f64p, _i32p]
+        L.orc_push_wset.argtypes = [C.c_void_p, C.c_int64, C.c_int, _i32p, _f64p, _f64p, _f64p,
+                                    _f64p]
+        L.orc_push_wset.restype = C.c_int
         L.orc_next_iter.argtypes = [C.c_void_p]
         L.orc_next_iter.restype = C.c_int64
         L.orc_step.argtypes = [C.c_void_p, C.POINTER(_StepOut)]
@@ -348,8 +351,18 @@ class Oracle:
                             _p(mail_ts, _f64p), _p(ver, _i32p))
         return dict(mem=mem, mem_ts=mem_ts, mail=mail, mail_ts=mail_ts, ver=ver)
 
-    def set_state(self, it, mem, mem_ts, mail, mail_ts, ver):
+    def set_state(self, it, mem, mem_ts, mail, mail_ts, ver, pending=()):
+        """Committed tables at iteration `it`, then the pending write sets of
+        a saved state: (iteration, node, mem, mem_ts, mail, mail_ts) each, in
+        iteration order (Eq. 2: a read at i applies those of iteration
+        <= i-1-s)."""
         mem, mem_ts, mail, mail_ts = map(_f64, (mem, mem_ts, mail, mail_ts))
         ver = np.ascontiguousarray(ver, dtype=np.int32)
         lib().orc_set_state(self._h, int(it), _p(mem, _f64p), _p(mem_ts, _f64p),
                             _p(mail, _f64p), _p(mail_ts, _f64p), _p(ver, _i32p))
+        for j, node, wm, wmt, wl, wlt in pending:
+            node = np.ascontiguousarray(node, dtype=np.int32)
+            wm, wmt, wl, wlt = map(_f64, (wm, wmt, wl, wlt))
+            assert lib().orc_push_wset(self._h, int(j), len(node), _p(node, _i32p),
+                                       _p(wm, _f64p), _p(wmt, _f64p), _p(wl, _f64p),
+                                       _p(wlt, _f64p)) == 0

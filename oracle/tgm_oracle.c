@@ -726,6 +726,43 @@ void orc_set_state(void *p, int64_t it, const double *mem, const double *mem_ts,
     c->next_iter = it;
 }
 
+/* Queue a write set of iteration `it` behind the queued ones (after
+ * orc_set_state: the pending updates of a saved state, which the snapshot of
+ * iteration i applies once it <= i-1-s, Eq. 2).  Rows: node [n], mem [n x M],
+ * mem_ts [n], mail [n x D_m], mail_ts [n]; iterations must grow.  Returns 0,
+ * or -1 for an iteration not after the last queued one. */
+int orc_push_wset(void *p, int64_t it, int n, const int32_t *node, const double *mem,
+                  const double *mem_ts, const double *mail, const double *mail_ts)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (n < 0 || (c->nq > 0 && c->q[c->nq - 1].iter >= it))
+        return -1;
+    const int M = c->M, D_m = c->D_m;
+    orc_wset W;
+    memset(&W, 0, sizeof(W));
+    W.iter = it;
+    W.n = n;
+    W.node = (int32_t *)malloc(sizeof(int32_t) * (n ? n : 1));
+    W.mem = (double *)malloc(sizeof(double) * ((size_t)n * M + 1));
+    W.mem_ts = (double *)malloc(sizeof(double) * (n ? n : 1));
+    W.mail = (double *)malloc(sizeof(double) * ((size_t)n * D_m + 1));
+    W.mail_ts = (double *)malloc(sizeof(double) * (n ? n : 1));
+    if (n) {
+        memcpy(W.node, node, sizeof(int32_t) * (size_t)n);
+        memcpy(W.mem, mem, sizeof(double) * (size_t)n * M);
+        memcpy(W.mem_ts, mem_ts, sizeof(double) * (size_t)n);
+        if (D_m)
+            memcpy(W.mail, mail, sizeof(double) * (size_t)n * D_m);
+        memcpy(W.mail_ts, mail_ts, sizeof(double) * (size_t)n);
+    }
+    if (c->nq == c->capq) {
+        c->capq *= 2;
+        c->q = (orc_wset *)realloc(c->q, sizeof(orc_wset) * (size_t)c->capq);
+    }
+    c->q[c->nq++] = W;
+    return 0;
+}
+
 void orc_get_state(void *p, double *mem, double *mem_ts, double *mail, double *mail_ts,
                    int32_t *ver)
 {

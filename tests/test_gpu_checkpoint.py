@@ -125,3 +125,31 @@ def test_checkpoint_argument_errors():
     a.step(4)
     torch.cuda.synchronize()
     a.close()
+
+
+@pytest.mark.parametrize("name,s,E,j,n", [("tiny", 2, 6000, 15, 12), ("wiki", 3, 40_000, 40, 12)])
+def test_oracle_resumes_from_gpu_checkpoint(orc, name, s, E, j, n):
+    """A parity window that starts mid-run from a GPU checkpoint: the GPU
+    runs iterations 0..j-1, its checkpoint (committed tables and the pending
+    write sets) seeds the oracle, and both run iterations j..j+n-1."""
+    from ckpt_format import parse
+    from paper_2402_15113_amd.stage import from_workload
+    from test_gpu_parity import compare_state, compare_step
+    wl = make_workload(name, E=E, s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w)
+    st.run(0, j)
+    ck = parse(st.save_checkpoint())
+    print(f"[ckpt] {name} s={s}: resume at {ck['next_iter']} with "
+          f"{len(ck['pending'])} pending write sets", flush=True)
+    assert ck["next_iter"] == j and len(ck["pending"]) == s
+    o = orc.Oracle(wl, w)
+    o.set_state(j, ck["mem"], ck["mem_ts"], ck["mail"], ck["mail_ts"], ck["ver"],
+                pending=ck["pending"])
+    for i in range(j, j + n):
+        st.step(i)
+        compare_step(st.outputs(), o.step(want="all"))
+    st.flush()
+    o.flush()
+    compare_state(st.state(), o.state())
+    st.close()
