@@ -23,11 +23,12 @@ __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf
 // Persistent grid of kGruGrid workgroups: workgroup w takes a contiguous range
 // of tasks (ranges are dealt so that the ranges of one XCD are adjacent, and
 // the tasks of one row block mostly meet in one L2) and walks it in rounds of
-// at most 4 tasks spanning at most 2 row blocks:
+// at most 4 kGruSlots tasks spanning at most 2 row blocks:
 //   the rows' GRU inputs [mail || phi(mail_ts - mem_ts) | mem] are staged in
-//   LDS with all their loads in flight together; task j of the round goes to
-//   wavefronts j and j + 4, which split the reduction (k) range in two halves
-//   and stream the weights of their half, two chunks ahead of the multiply;
+//   LDS with all their loads in flight together; tasks j and j + 4 q of the
+//   round go to wavefronts j and j + 4, which split the reduction (k) range in
+//   two halves and stream the weights of their half for each of their tasks,
+//   two chunks ahead of the multiply (longer ranges take fewer rounds);
 //   each accumulates r and z over [x | h] and n in its x part and its h part
 //   (which the reset gate scales); the upper half's partial sums go through
 //   LDS to the lower half, which applies the gates.
@@ -36,6 +37,7 @@ __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf
 constexpr int kGruWaves = 8;
 constexpr int kGruGrid = 256;
 constexpr int kGruRows = 32;   // rows staged per round (2 row blocks)
+constexpr int kGruSlots = 2;   // tasks per wave pair and round (rounds of 4 kGruSlots tasks)
 
 struct GruArgs {
     const int32_t *n_nodes;
@@ -213,9 +215,10 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
     const int KX = KXC * 16, SA = KC * 16 + 4;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    constexpr int S = kGruSlots;
     float *A = lds;                                              // [kGruRows][SA]
-    f4 *red = reinterpret_cast<f4 *>(lds + kGruRows * SA);       // [4 tasks][4][64]
-    double *s_om = reinterpret_cast<double *>(lds + kGruRows * SA + 4 * 4 * kWave * 4);
+    f4 *red = reinterpret_cast<f4 *>(lds + kGruRows * SA);       // [4 S tasks][4][64]
+    double *s_om = reinterpret_cast<double *>(red + 4 * S * 4 * kWave);
     double *s_be = s_om + D_t;
 
     // this workgroup's task range: range c = (w % 8) * (G / 8) + w / 8, so the
@@ -244,7 +247,7 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
     // round geometry: tasks [t, te), rows [row0, row0 + nrows)
     auto round_end = [&](int64_t t) {
         const int64_t rb_a = t / MB;
-        return std::min<int64_t>(std::min<int64_t>(t + 4, t1), (rb_a + 2) * MB);
+        return std::min<int64_t>(std::min<int64_t>(t + 4 * S, t1), (rb_a + 2) * MB);
     };
     auto round_rows = [&](int64_t t, int64_t te) {
         const int rb_a = (int)(t / MB);
@@ -265,44 +268,80 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
         const int rb_a = (int)(t / MB);
         const int row0 = rb_a * 16;
         const int nrows = round_rows(t, te);
-        const int64_t tj = t + j;
-        const bool live = tj < te;
-        const int rb = (int)(tj / MB), hb = live ? (int)(tj - (int64_t)rb * MB) : 0;
-        const int lrow0 = (rb - rb_a) * 16;
-        // biases and the first two weight chunks load while the rows are staged
-        const int col = hb * 16 + (lane & 15);
-        const int colc = col < M ? col : 0;
-        const float b_r = g.bias[colc], b_z = g.bias[MP + colc];
-        const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
-        f4 w0[3], w1[3], w2[3];
-        gw.load<NG>(kc0, hb, lane, w0);
-        gw.load<NG>(kc0 + 1, hb, lane, w1);
+        // slot q of this wave pair: task t + j + 4 q of the round
+        bool live[S];
+        int hb[S], lrow0[S];
+#pragma unroll
+        for (int q = 0; q < S; ++q) {
+            const int64_t tj = t + j + 4 * q;
+            live[q] = tj < te;
+            const int rb = live[q] ? (int)(tj / MB) : rb_a;
+            hb[q] = live[q] ? (int)(tj - (int64_t)rb * MB) : 0;
+            lrow0[q] = (rb - rb_a) * 16;
+        }
+        // the first two weight chunks load while the rows are staged
+        f4 w0[S][3], w1[S][3], w2[S][3];
+#pragma unroll
+        for (int q = 0; q < S; ++q)
+            if (live[q]) {
+                gw.load<NG>(kc0, hb[q], lane, w0[q]);
+                gw.load<NG>(kc0 + 1, hb[q], lane, w1[q]);
+            }
         __syncthreads();   // s_om is written; the previous round is done with LDS
         rows.store(g, A, s_has, s_nts, SA, KX, s_om, s_be, nrows, lane);
         __syncthreads();
 
-        f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
-        if (live) {
-            // three weight sets rotate: chunk c + 2 loads while chunk c multiplies
-            const float *arow = arow0 + lrow0 * SA;
+        f4 ar[S], az[S], anx[S], anh[S];
+#pragma unroll
+        for (int q = 0; q < S; ++q)
+            ar[q] = az[q] = anx[q] = anh[q] = f4{0, 0, 0, 0};
+        if (live[0]) {
+            // three weight sets rotate: chunk c + 2 loads while chunk c
+            // multiplies; each chunk serves the wave's live slots
             for (int cc = kc0; cc < kc1; cc += 3) {
-                gw.load<NG>(cc + 2, hb, lane, w2);
+#pragma unroll
+                for (int q = 0; q < S; ++q)
+                    if (live[q])
+                        gw.load<NG>(cc + 2, hb[q], lane, w2[q]);
                 issue_fence();
-                gru_mma<NG>(arow, cc, KXC, w0, ar, az, anx, anh);
-                gw.load<NG>(cc + 3, hb, lane, w0);
+#pragma unroll
+                for (int q = 0; q < S; ++q)
+                    if (live[q])
+                        gru_mma<NG>(arow0 + lrow0[q] * SA, cc, KXC, w0[q], ar[q], az[q], anx[q],
+                                    anh[q]);
+#pragma unroll
+                for (int q = 0; q < S; ++q)
+                    if (live[q])
+                        gw.load<NG>(cc + 3, hb[q], lane, w0[q]);
                 issue_fence();
                 if (cc + 1 < kc1)
-                    gru_mma<NG>(arow, cc + 1, KXC, w1, ar, az, anx, anh);
-                gw.load<NG>(cc + 4, hb, lane, w1);
+#pragma unroll
+                    for (int q = 0; q < S; ++q)
+                        if (live[q])
+                            gru_mma<NG>(arow0 + lrow0[q] * SA, cc + 1, KXC, w1[q], ar[q], az[q],
+                                        anx[q], anh[q]);
+#pragma unroll
+                for (int q = 0; q < S; ++q)
+                    if (live[q])
+                        gw.load<NG>(cc + 4, hb[q], lane, w1[q]);
                 issue_fence();
                 if (cc + 2 < kc1)
-                    gru_mma<NG>(arow, cc + 2, KXC, w2, ar, az, anx, anh);
+#pragma unroll
+                    for (int q = 0; q < S; ++q)
+                        if (live[q])
+                            gru_mma<NG>(arow0 + lrow0[q] * SA, cc + 2, KXC, w2[q], ar[q], az[q],
+                                        anx[q], anh[q]);
             }
             if (half) {
-                red[(j * 4 + 0) * kWave + lane] = ar;
-                red[(j * 4 + 1) * kWave + lane] = az;
-                red[(j * 4 + 2) * kWave + lane] = anx;
-                red[(j * 4 + 3) * kWave + lane] = anh;
+#pragma unroll
+                for (int q = 0; q < S; ++q)
+                    if (live[q]) {
+                        f4 *rw = red + ((j + 4 * q) * 4) * kWave + lane;
+                        rw[0] = ar[q];
+                        rw[kWave] = az[q];
+                        rw[2 * kWave] = anx[q];
+                        rw[3 * kWave] = anh[q];
+                    }
             }
         }
         const int64_t tn = te;
@@ -310,36 +349,45 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
         if (tn < t1)   // the next round's rows, in flight during the epilogue
             rows.load(g, (int)(tn / MB) * 16, round_rows(tn, ten), wave, lane);
         __syncthreads();
-        if (live && !half) {
-            // lane holds values v = 0..3 of rows 4 (lane / 16) + v, column hb 16 + lane % 16
-            ar += red[(j * 4 + 0) * kWave + lane];
-            az += red[(j * 4 + 1) * kWave + lane];
-            anx += red[(j * 4 + 2) * kWave + lane];
-            anh += red[(j * 4 + 3) * kWave + lane];
-            if (col < M) {
+        if (!half) {
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int lr = lrow0 + 4 * (lane >> 4) + v;
-                    const int p = row0 + lr;
-                    if (p < n) {
-                        const float h = A[lr * SA + KX + col];
-                        float o = h;
-                        if (s_has[lr]) {
-                            if (NG == 3) {
-                                const float r = sigmoidf_(ar[v] + b_r);
-                                const float z = sigmoidf_(az[v] + b_z);
-                                const float nn = tanhf(anx[v] + b_nx + r * (anh[v] + b_nh));
-                                o = (1.0f - z) * nn + z * h;
-                            } else {   // the RNN cell
-                                o = tanhf((anx[v] + b_nx) + (anh[v] + b_nh));
+            for (int q = 0; q < S; ++q) {
+                if (!live[q])
+                    continue;
+                // lane holds values v = 0..3 of rows 4 (lane / 16) + v, column
+                // hb 16 + lane % 16
+                const f4 *rq = red + ((j + 4 * q) * 4) * kWave + lane;
+                const f4 sr = ar[q] + rq[0], sz = az[q] + rq[kWave];
+                const f4 snx = anx[q] + rq[2 * kWave], snh = anh[q] + rq[3 * kWave];
+                const int col = hb[q] * 16 + (lane & 15);
+                const int colc = col < M ? col : 0;
+                const float b_r = g.bias[colc], b_z = g.bias[MP + colc];
+                const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
+                if (col < M) {
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int lr = lrow0[q] + 4 * (lane >> 4) + v;
+                        const int p = row0 + lr;
+                        if (p < n) {
+                            const float h = A[lr * SA + KX + col];
+                            float o = h;
+                            if (s_has[lr]) {
+                                if (NG == 3) {
+                                    const float r = sigmoidf_(sr[v] + b_r);
+                                    const float z = sigmoidf_(sz[v] + b_z);
+                                    const float nn = tanhf(snx[v] + b_nx + r * (snh[v] + b_nh));
+                                    o = (1.0f - z) * nn + z * h;
+                                } else {   // the RNN cell
+                                    o = tanhf((snx[v] + b_nx) + (snh[v] + b_nh));
+                                }
                             }
+                            g.mem_new[(int64_t)p * M + col] = o;
                         }
-                        g.mem_new[(int64_t)p * M + col] = o;
                     }
                 }
+                if (hb[q] == 0 && g.new_mem_ts && lane < 16 && row0 + lrow0[q] + lane < n)
+                    g.new_mem_ts[row0 + lrow0[q] + lane] = s_nts[lrow0[q] + lane];
             }
-            if (hb == 0 && g.new_mem_ts && lane < 16 && row0 + lrow0 + lane < n)
-                g.new_mem_ts[row0 + lrow0 + lane] = s_nts[lrow0 + lane];
         }
         if (tn >= t1)
             break;
@@ -1777,7 +1825,8 @@ int waves_for(int blocks) { return blocks < kMaxWaves ? (blocks < 1 ? 1 : blocks
 
 size_t gru_lds(const tgm_model *m)
 {
-    return sizeof(float) * (kGruRows * ((m->KXC + m->KHC) * 16 + 4) + 4 * 4 * kWave * 4) +
+    return sizeof(float) * (kGruRows * ((m->KXC + m->KHC) * 16 + 4) +
+                            4 * kGruSlots * 4 * kWave * 4) +
            2 * sizeof(double) * m->D_t;
 }
 
