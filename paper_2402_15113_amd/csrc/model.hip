@@ -2300,15 +2300,17 @@ tgm_status_t launch_attn(const tgm_model *m, const AttnArgs &a, const GatherPlan
     const int n_attn = (int)cdiv(a.R, a.RT);
     const dim3 block(64 * kMaxWaves);
     const size_t lds = m->fold ? attn_fold_lds(m) : attn_lds(m);
-    // the gather rides along only when the attention leaves CUs free (its
-    // blocks are dispatched after the attention's and hold one CU each: they
-    // carry the attention's LDS size); otherwise it is its own launch
-    if (next && next->cap > 0 && n_attn + 8 > kCUs) {
+    // the gather rides along when the attention's last round of blocks
+    // leaves CUs free: its blocks are dispatched after the attention's, hold
+    // one CU each (they carry the attention's LDS size) and fill that round;
+    // otherwise it is its own launch
+    const int spare = (kCUs - n_attn % kCUs) % kCUs;
+    if (next && next->cap > 0 && spare < 8) {
         TGM_TRY_STATUS(launch_gather(*next, s));
         next = nullptr;
     }
     if (next && next->cap > 0) {
-        const int n_gather = kCUs - n_attn;
+        const int n_gather = spare;
         const dim3 grid(n_attn + n_gather);
         if (m->fold) {
             switch (a.RBa) {
