@@ -442,21 +442,24 @@ __global__ __launch_bounds__(256) void k_tproj(TprojArgs a)
         tproj_elem(a, i, *a.n_nodes);
 }
 
-// The projection and the gather of the next fetch in one launch: blocks
-// below n_tp project, the rest gather (kGatherNPW nodes per wavefront).
+// The projection and the gather of the next fetch in one launch: the last
+// n_tp blocks project, the others gather (kGatherNPW nodes per wavefront).
 __global__ __launch_bounds__(256) void k_tproj_gather(TprojArgs a, int n_tp, GatherPlan gp)
 {
-    if ((int)blockIdx.x < n_tp) {
-        const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    // the gather's blocks come first: their row copies are the longer chains,
+    // and the projection's small blocks fill the CUs around them
+    const int n_gather = (int)gridDim.x - n_tp;
+    if ((int)blockIdx.x >= n_gather) {
+        const int64_t i = (blockIdx.x - n_gather) * (int64_t)blockDim.x + threadIdx.x;
         if (i < (int64_t)a.R * a.M)
             tproj_elem(a, i, *a.n_nodes);
         return;
     }
     const int waves = blockDim.x >> 6;
     const int n = min(*gp.n_nodes, gp.cap);
-    const int stride = ((int)gridDim.x - n_tp) * waves * kGatherNPW;
-    for (int p = (((int)blockIdx.x - n_tp) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
-         p < n; p += stride)
+    const int stride = n_gather * waves * kGatherNPW;
+    for (int p = ((int)blockIdx.x * waves + (int)(threadIdx.x >> 6)) * kGatherNPW; p < n;
+         p += stride)
         gather_rows(gp, p, n, threadIdx.x & 63);
 }
 
