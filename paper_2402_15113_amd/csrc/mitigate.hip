@@ -324,6 +324,49 @@ __device__ __forceinline__ int hash_walk(const int32_t *hs, int32_t w, int from)
     return 0;
 }
 
+// One step of the wave arg-best: the candidate that DPP control CTRL brings
+// in (rows ROWS only; a lane with no source sees its own) replaces the lane's
+// when better.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void best_step(Cand &b, int &bl)
+{
+    const long long m = __double_as_longlong(b.mts);
+    const int mlo = (int)m, mhi = (int)(m >> 32);
+    Cand y;
+    y.sim = __builtin_amdgcn_update_dpp(b.sim, b.sim, CTRL, ROWS, 0xF, false);
+    const int lo = __builtin_amdgcn_update_dpp(mlo, mlo, CTRL, ROWS, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(mhi, mhi, CTRL, ROWS, 0xF, false);
+    y.mts = __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+    y.id = __builtin_amdgcn_update_dpp(b.id, b.id, CTRL, ROWS, 0xF, false);
+    y.pos = __builtin_amdgcn_update_dpp(b.pos, b.pos, CTRL, ROWS, 0xF, false);
+    const int yl = __builtin_amdgcn_update_dpp(bl, bl, CTRL, ROWS, 0xF, false);
+    if (better(y, b)) {
+        b = y;
+        bl = yl;
+    }
+}
+
+// The wave's best candidate and its lane, on every lane: a running best
+// within each row of 16 lanes (shifts by 1, 2, 4, 8), the rows joined into
+// lane 63 by the two row broadcasts, then read from lane 63.
+__device__ __forceinline__ void wave_best(Cand &b, int &bl)
+{
+    best_step<0x111, 0xF>(b, bl);
+    best_step<0x112, 0xF>(b, bl);
+    best_step<0x114, 0xF>(b, bl);
+    best_step<0x118, 0xF>(b, bl);
+    best_step<0x142, 0xA>(b, bl);
+    best_step<0x143, 0xC>(b, bl);
+    const long long m = __double_as_longlong(b.mts);
+    const int lo = __builtin_amdgcn_readlane((int)m, 63);
+    const int hi = __builtin_amdgcn_readlane((int)(m >> 32), 63);
+    b.mts = __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+    b.sim = __builtin_amdgcn_readlane(b.sim, 63);
+    b.id = __builtin_amdgcn_readlane(b.id, 63);
+    b.pos = __builtin_amdgcn_readlane(b.pos, 63);
+    bl = __builtin_amdgcn_readlane(bl, 63);
+}
+
 // Candidate lists in LDS: entry arrays of similarity (0 = end of a list),
 // memory time, id and position.
 struct Lists {
@@ -332,13 +375,14 @@ struct Lists {
     int32_t *id, *pos;
 };
 
-// Wave 0 merges nl sorted lists of the entry arrays (list l at l * stride, at
-// most len entries) and one more list at `xb` of xl entries into the best K.
-// Returns their count m on every lane; lane j < m holds the j-th in *mine.
-// Lane i owns lists 4i .. 4i + 3 (nl <= 256); lane 63 also the extra list.
-// Each round the wave takes its best head: a 6-step shuffle arg-best, whose
-// result every lane holds.
-__device__ int merge_lists(const Lists &L, int nl, int stride, int len, int xb, int xl, int K,
+// Wave 0 merges nl sorted lists of the entry arrays (entry h of list l at
+// l * ls + h * es, at most len entries) and one more list at `xb` of xl
+// entries into the best K.  Returns their count m on every lane; lane j < m
+// holds the j-th in *mine.  Lane i owns lists i, i + 64, i + 128 and i + 192
+// (nl <= 256), so the heads of neighbouring lanes sit side by side when the
+// lists are interleaved (es = the list count); lane 63 also owns the extra
+// list.  Each round the wave takes its best head with the DPP arg-best.
+__device__ int merge_lists(const Lists &L, int nl, int ls, int es, int len, int xb, int xl, int K,
                            Cand *mine)
 {
     const int lane = threadIdx.x & 63;
@@ -349,9 +393,9 @@ __device__ int merge_lists(const Lists &L, int nl, int stride, int len, int xb, 
         int bi = -1;
 #pragma unroll
         for (int i = 0; i < 5; ++i) {
-            const int l = 4 * lane + i;
+            const int l = lane + kWave * i;
             const bool own = i < 4 ? (l < nl && h[i] < len) : (lane == 63 && h[4] < xl);
-            const int o = i < 4 ? l * stride + h[i] : xb + h[4];
+            const int o = i < 4 ? l * ls + h[i] * es : xb + h[4];
             if (own && L.sim[o] > 0) {
                 const Cand x{L.sim[o], L.mts[o], L.id[o], L.pos[o]};
                 if (better(x, best)) {   // best starts empty
@@ -363,19 +407,7 @@ __device__ int merge_lists(const Lists &L, int nl, int stride, int len, int xb, 
         // the winner is unique (positions are distinct)
         Cand wb = best;
         int wl = bi >= 0 ? lane : -1;
-#pragma unroll
-        for (int o = kWave / 2; o >= 1; o >>= 1) {
-            Cand y;
-            y.sim = __shfl_xor(wb.sim, o, kWave);
-            y.mts = __shfl_xor(wb.mts, o, kWave);
-            y.id = __shfl_xor(wb.id, o, kWave);
-            y.pos = __shfl_xor(wb.pos, o, kWave);
-            const int yl = __shfl_xor(wl, o, kWave);
-            if (better(y, wb)) {   // an empty lane's entry has similarity 0
-                wb = y;
-                wl = yl;
-            }
-        }
+        wave_best(wb, wl);   // an empty lane's entry has similarity 0
         if (wl < 0)
             break;   // no candidate left anywhere (uniform)
         if (lane == wl) {
@@ -505,7 +537,7 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
             }
 #pragma unroll
             for (int j = 0; j < P; ++j) {
-                const int o = tid * P + j;
+                const int o = j * kMitThreads + tid;   // entry j of every list together
                 e_sim[o] = j < KP ? top[j].sim : 0;
                 e_mts[o] = top[j].mts;
                 e_id[o] = top[j].id;
@@ -514,7 +546,7 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
             __syncthreads();
             if (tid < kWave) {   // the new running list, written after the merge's reads
                 Cand w;
-                const int m = merge_lists(L, kMitThreads, P, P, RB, s_m, K, &w);
+                const int m = merge_lists(L, kMitThreads, 1, kMitThreads, P, RB, s_m, K, &w);
                 if (tid < m) {
                     e_sim[RB + tid] = w.sim;
                     e_mts[RB + tid] = w.mts;
@@ -550,7 +582,7 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
             __syncthreads();
             if (tid < kWave) {
                 Cand w;
-                const int m = merge_lists(L, nce, K, K, 0, 0, K, &w);
+                const int m = merge_lists(L, nce, K, 1, K, 0, 0, K, &w);
                 if (tid < m)
                     e_pos[RB + tid] = w.pos;
                 if (tid == 0)
