@@ -30,7 +30,10 @@
  *    the device surface after the caller synchronises, through
  *    tgm_last_device_error().
  *  - Handles own the device memory they allocate at creation and free it in
- *    their destroy call.  Per-batch calls allocate nothing.  Arrays passed to
+ *    their destroy call (tgm_state_set_mitigation also allocates the
+ *    executor's neighbour-set slots in the mitigator).  Per-batch calls,
+ *    tgm_stage_run included, allocate nothing and never synchronise the
+ *    device (tgm_alloc_count counts every allocation).  Arrays passed to
  *    tgm_graph_create are BORROWED: they must stay alive and unchanged until
  *    the graph is destroyed.
  *  - A handle must not be used from two threads at once.  Calls on one
@@ -47,6 +50,9 @@
 #ifdef __cplusplus
 extern "C" {
 #endif
+
+/* Largest number of sample buffer sets tgm_stage_run takes (its nsb). */
+#define TGM_MAX_SAMPLE_SETS 16
 
 typedef int32_t tgm_status_t;
 #define TGM_OK 0
@@ -69,6 +75,12 @@ const char *tgm_status_str(tgm_status_t status);
 tgm_status_t tgm_last_device_error(void);
 /* ABI version: major * 100 + minor. */
 int32_t tgm_version(void);
+/* *count (host) = the number of device allocations the library has made in
+ * this process so far.  Every allocation happens in a create call or in
+ * tgm_state_set_mitigation; a caller can read the count before and after any
+ * other call to check that it allocated nothing.  TGM_EINVAL if count is
+ * NULL. */
+tgm_status_t tgm_alloc_count(int64_t *count);
 
 /* ------------------------------------------------------------------------
  * Event graph (Sec. 2: the event set y_uv(t) of a dynamic graph).
@@ -92,7 +104,7 @@ tgm_status_t tgm_graph_info(tgm_graph_t g, int32_t *N, int64_t *E, int32_t *D_e,
 /* Roots of the batch of events [first_event, first_event + b): the training
  * samples of an iteration are its events, each with a source, a destination
  * and one negative destination (Sec. 5, training settings: equal numbers of
- * positive and negative pairs; Appendix E: three nodes per sample).
+ * positive and negative pairs; App. E.6: three nodes per sample).
  * Output root[3b] = src[batch] ++ dst[batch] ++ neg[batch], root_ts[3b] = the
  * event time, repeated three times. */
 tgm_status_t tgm_batch_roots(tgm_graph_t g, int64_t first_event, int32_t b, int32_t *root,
@@ -115,8 +127,11 @@ tgm_status_t tgm_sample_batch(tgm_graph_t g, int64_t first_event, int32_t b, int
                               int32_t *root, double *root_ts, int32_t *nbr, int32_t *eid,
                               double *nts, int32_t *cnt, void *stream);
 
-/* Node set of the subgraph: U = sorted unique(root[0..R) and every valid
- * nbr).  nodes [cap] receives U, *n_nodes (device int32) its size, root_pos
+/* Node set of the subgraph (Sec. 2, Eq. 1: emb() of a root reads the memory of
+ * the root and of its 1-hop temporal neighbours N(v), so an iteration fetches
+ * and updates the memory of every node of the sampled subgraph; App. E.6
+ * sizes that subgraph at the roots plus nb neighbours each):
+ * U = sorted unique(root[0..R) and every valid nbr).  nodes [cap] receives U, *n_nodes (device int32) its size, root_pos
  * [R] and nbr_pos [R x nb] the position in U of every root and neighbour (-1
  * for empty slots).  cap must be >= min(N, R * (nb + 1)).  Uses the graph's
  * scratch: calls on one graph must be stream-ordered. */
@@ -124,7 +139,10 @@ tgm_status_t tgm_node_set(tgm_graph_t g, const int32_t *root, int32_t R, const i
                           int32_t nb, int32_t *nodes, int32_t *n_nodes, int32_t cap,
                           int32_t *root_pos, int32_t *nbr_pos, void *stream);
 
-/* tgm_sample_batch followed by tgm_node_set over its outputs, with the node
+/* The sampling of an iteration's subgraph and its node set (Sec. 3.1: the
+ * sample stage of the pipeline, which depends on the event stream only; Sec. 5
+ * and App. D.1 for the sampler; Eq. 1 for the node set, as above):
+ * tgm_sample_batch followed by tgm_node_set over its outputs, with the node
  * marks made by the sampler itself (one launch fewer): same outputs as the
  * two calls (root, root_ts, nbr, eid, nts, cnt; nodes, *n_nodes, root_pos
  * [3b], nbr_pos [3b x nb]); cap >= min(N, 3b (nb + 1)).  Uses the graph's
@@ -308,11 +326,17 @@ tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int32_t *root_
  * prefetch stream starts after everything issued before on `stream`, and
  * `stream` ends after the last embedding.  Results equal those of issuing
  * tgm_sample_nodes, tgm_fetch_memory, tgm_update_memory and tgm_embed (or
- * tgm_embed_projection) per iteration in order on one stream.  nsb >= 2 and even; nb, cap as for the calls above;
- * mem_new [cap x M], new_mem_ts [cap] (may be NULL), winner [cap] (may be
- * NULL) and h [3B x M] hold the last iteration's outputs.  The two streams
- * must differ.  Errors of the underlying calls are returned as they occur
- * (the iterations before stay enqueued). */
+ * tgm_embed_projection) per iteration in order on one stream.
+ * 2 <= nsb <= TGM_MAX_SAMPLE_SETS and even (TGM_EINVAL if odd or below 2,
+ * TGM_ESIZE if above); nb, cap as for the calls above; mem_new [cap x M],
+ * new_mem_ts [cap] (may be NULL), winner [cap] (may be NULL) and h [3B x M]
+ * hold the last iteration's outputs.  Optional per-iteration copies (NULL:
+ * none): h_trace [n x 3B x M] receives every iteration's embeddings (rows
+ * past 3b of a partial last batch untouched), s_trace [n x cap x M] every
+ * iteration's new memories mem_new (rows past its node-set size untouched).
+ * The two streams must differ.  The call allocates nothing and does not
+ * synchronise the host with the device.  Errors of the underlying calls are
+ * returned as they occur (the iterations before stay enqueued). */
 typedef struct {
     int32_t *root;      /* [3B] */
     double *root_ts;    /* [3B] */
@@ -336,11 +360,11 @@ typedef struct {
 tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t i0, int64_t n,
                            int32_t B, int32_t nb, int32_t cap, const tgm_sample_buffers *sb,
                            int32_t nsb, const tgm_fetch_buffers *fb, float *mem_new,
-                           double *new_mem_ts, int64_t *winner, float *h, void *stream,
-                           void *prefetch_stream);
+                           double *new_mem_ts, int64_t *winner, float *h, float *h_trace,
+                           float *s_trace, void *stream, void *prefetch_stream);
 
 /* ------------------------------------------------------------------------
- * Similarity-based staleness mitigation (MSPipe-S, Sec. 4.3), applied to the
+ * Similarity-based staleness mitigation (MSPipe-S, Sec. 3.3), applied to the
  * fetched memories of a batch between tgm_fetch_memory and
  * tgm_update_memory.  For the fetched node set (positions p < *n_nodes):
  *   gap      dt_p = T - mem_ts[p], T = the time of event first_event (the
@@ -358,9 +382,9 @@ tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t
  * The mitigator owns its work space: the neighbour sets, gamma, the stale
  * positions and Omega of the last call.  Calls on one mitigator must be
  * stream-ordered.  Under tgm_stage_run the neighbour sets of each iteration
- * are built on the prefetch stream beside its sample (the first run with a
- * mitigator set may allocate one set per sample buffer set, after a device
- * synchronisation); the threshold and the blend run on the main stream.
+ * are built on the prefetch stream beside its sample, in one of the
+ * TGM_MAX_SAMPLE_SETS slots that tgm_state_set_mitigation makes; the
+ * threshold and the blend run on the main stream.
  */
 /* max_nodes >= any cap passed later, at most 1 << 20; 1 <= nb <= 64 (the
  * neighbour sets' nb); 1 <= K <= 16.  Errors: TGM_EINVAL, TGM_ENOMEM,
@@ -383,7 +407,10 @@ tgm_status_t tgm_mitigate(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event
 tgm_status_t tgm_mitigator_read(tgm_mitigator_t mt, double *gamma, int32_t *n_stale,
                                 int32_t *stale, int32_t *omega, void *stream);
 /* Makes tgm_stage_run mitigate every fetch with mt, p and lambda (mt NULL:
- * off, the default).  mt must stay alive while st uses it. */
+ * off, the default).  mt must stay alive while st uses it.  A set-up call:
+ * the first call with a mitigator allocates its executor slots (one
+ * neighbour-set table per sample buffer set) after synchronising the device.
+ * Errors: TGM_EINVAL, TGM_ENOMEM, TGM_EDEVICE. */
 tgm_status_t tgm_state_set_mitigation(tgm_state_t st, tgm_mitigator_t mt, double p,
                                       float lambda);
 

@@ -195,7 +195,7 @@ def sample(N, src, dst, t, root, root_ts, nb):
 
 def quantile_nearest_rank(x, p) -> float:
     """The ceil(p n)-th smallest of the n values x (the staleness threshold of
-    the mitigation, Sec. 4.3)."""
+    the mitigation, Sec. 3.3)."""
     x = _f64(x)
     return float(lib().orc_quantile_nearest_rank(len(x), _p(x, _f64p), float(p)))
 
@@ -244,7 +244,7 @@ class Oracle:
 
     def __init__(self, wl, w, s: int | None = None, mitigation: dict | None = None):
         """``mitigation=dict(p=.., lam=.., K=..)`` enables the MSPipe-S step
-        (Sec. 4.3) between the fetch and the memory update."""
+        (Sec. 3.3) between the fetch and the memory update."""
         self.wl = wl
         self.mitigation = mitigation
         self.s = wl.s if s is None else s

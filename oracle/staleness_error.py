@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE: runs the fp64 oracle only (no GPU code).
 
-Sec. 4.3 (error reduction) and App. C.3 compare, per iteration i, the
+Sec. 5.5 (error reduction) and App. E.2 compare, per iteration i, the
 Frobenius distance between the memories a stale fetch returns and the exact
 memories, ||s~ - s||_F, with the distance after the similarity-based
 mitigation, ||s^ - s||_F.  The exact memories are those a fetch without

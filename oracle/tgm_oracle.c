@@ -18,7 +18,7 @@
  *   2. most-recent-nb temporal neighbours of each root, strictly earlier events
  *      only (Sec. 5 training settings; Appendix D.1);
  *   3. node set U = sorted unique(roots + sampled neighbours) and its state;
- *   3b. (optional, MSPipe-S, Sec. 4.3) staleness mitigation of the fetched
+ *   3b. (optional, MSPipe-S, Sec. 3.3) staleness mitigation of the fetched
  *      memories of nodes whose last update lies further back than the
  *      p-quantile of the batch's gaps: a blend with the mean memory of the
  *      most similar (common neighbours) fresher nodes;
@@ -357,7 +357,7 @@ static int cmp_i32(const void *a, const void *b)
 }
 
 /* ------------------------------------------------------------------------- */
-/* Similarity-based staleness mitigation (MSPipe-S, Sec. 4.3).  Readings where
+/* Similarity-based staleness mitigation (MSPipe-S, Sec. 3.3).  Readings where
  * the text is silent:
  *   - the gap of a fetched node u is dt_u = T - mem_ts_u, T the time of the
  *     batch's first event (the time since u's memory was last updated);
@@ -588,8 +588,8 @@ typedef struct {
     int32_t m_n_stale, m_pad;
     /* the exact memories of U [n_U x M]: the committed state with every write
      * set of iterations <= i-1 applied, i.e. what a fetch without staleness
-     * would read at this point of the run (for the staleness error of Sec. 4.3
-     * and App. C.3) */
+     * would read at this point of the run (for the staleness error of Sec. 5.5
+     * and App. E.2) */
     double *x_mem;
 } orc_step_out;
 

@@ -72,6 +72,9 @@ void prof_end(int id, hipStream_t s)
 }
 
 static std::atomic<int> g_device_error{hipSuccess};
+static std::atomic<int64_t> g_allocs{0};
+
+void count_alloc() { g_allocs.fetch_add(1, std::memory_order_relaxed); }
 
 void record_error(hipError_t e)
 {
@@ -133,6 +136,14 @@ extern "C" tgm_status_t tgm_last_device_error(void)
 }
 
 extern "C" int32_t tgm_version(void) { return 100; }
+
+extern "C" tgm_status_t tgm_alloc_count(int64_t *count)
+{
+    if (!count)
+        return TGM_EINVAL;
+    *count = tgm::g_allocs.load(std::memory_order_relaxed);
+    return TGM_OK;
+}
 
 extern "C" tgm_status_t tgm_profile_enable(int32_t on)
 {

@@ -45,6 +45,16 @@ void record_error(hipError_t e);
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Every device allocation of the library goes through dev_malloc, which counts
+// it (tgm_alloc_count), so a caller can check that a call allocated nothing.
+void count_alloc();
+template <class T>
+inline hipError_t dev_malloc(T **p, size_t bytes)
+{
+    count_alloc();
+    return hipMalloc((void **)p, bytes);
+}
+
 // Per-kernel timing (tgm_profile_*): prof_begin returns -1 when disabled.
 int prof_begin(const char *kernel, hipStream_t s);
 void prof_end(int id, hipStream_t s);
@@ -117,6 +127,9 @@ struct tgm_state {
     uint64_t *xwin = nullptr;
     int32_t xwin_slots = 0, xwin_cap = 0;
     uint32_t xwin_tag = 0;
+    // the executor's cross-stream events (sampled chunk and computed chunk by
+    // parity, start), made at creation so that a run creates nothing
+    hipEvent_t run_ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
     // staleness mitigation applied by the pipelined executor after each fetch
     // (tgm_state_set_mitigation; off when mit is null)
     struct tgm_mitigator *mit = nullptr;
@@ -632,12 +645,10 @@ tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int
                                uint64_t *xwin, uint64_t xtag, hipStream_t s);
 
 // The executor's latest-message reduce of an iteration, on the prefetch
-// stream beside its sample: exec_latest_reserve makes nslots key arrays of
-// cap entries (it may allocate; contents of existing arrays are dropped);
-// exec_latest_launch reduces the 2b candidates of the batch into array `slot`
-// under a fresh tag and returns the array and the tag, which
-// compute_iteration's staging then reads.
-tgm_status_t exec_latest_reserve(tgm_state_t st, int32_t nslots, int32_t cap);
+// stream beside its sample: exec_latest_launch reduces the 2b candidates of
+// the batch into key array `slot` (one of the TGM_MAX_SAMPLE_SETS arrays of N
+// entries made with the state) under a fresh tag and returns the array and
+// the tag, which compute_iteration's staging then reads.
 tgm_status_t exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b, const int32_t *src_pos,
                                 const int32_t *dst_pos, const int32_t *n_nodes, hipStream_t s,
                                 uint64_t **win, uint64_t *tag);
@@ -649,6 +660,7 @@ tgm_status_t exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b, const i
 // tgm_mitigate; mitigate_reserve makes slots 0 .. nslots - 1 (it may allocate,
 // and drops the contents of existing slots).
 tgm_status_t mitigate_reserve(tgm_mitigator_t mt, int32_t nslots);
+int32_t mitigate_slots(tgm_mitigator_t mt);
 tgm_status_t mitigate_prep_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
                                   const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
                                   int32_t slot, hipStream_t s);

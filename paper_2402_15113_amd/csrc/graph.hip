@@ -350,9 +350,9 @@ extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *sr
         st = code;
     };
     do {
-        if (hipMalloc(&g->off, sizeof(int64_t) * (N + 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
-        if (hipMalloc(&bad, sizeof(int32_t) * 2) != hipSuccess) { fail(TGM_ENOMEM); break; }
-        if (hipMalloc(&g->ns_stamp, sizeof(int32_t) * N) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (dev_malloc(&g->off, sizeof(int64_t) * (N + 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (dev_malloc(&bad, sizeof(int32_t) * 2) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (dev_malloc(&g->ns_stamp, sizeof(int32_t) * N) != hipSuccess) { fail(TGM_ENOMEM); break; }
         if (hipMemsetAsync(g->ns_stamp, 0, sizeof(int32_t) * N, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         if (hipMemsetAsync(bad, 0, sizeof(int32_t) * 2, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         if (E == 0) {
@@ -367,10 +367,10 @@ extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *sr
             hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         if (hbad[0] || hbad[1]) { fail(TGM_ERANGE); break; }
 
-        if (hipMalloc(&key, sizeof(int32_t) * n2) != hipSuccess ||
-            hipMalloc(&val, sizeof(int32_t) * n2) != hipSuccess ||
-            hipMalloc(&key2, sizeof(int32_t) * n2) != hipSuccess ||
-            hipMalloc(&val2, sizeof(int32_t) * n2) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (dev_malloc(&key, sizeof(int32_t) * n2) != hipSuccess ||
+            dev_malloc(&val, sizeof(int32_t) * n2) != hipSuccess ||
+            dev_malloc(&key2, sizeof(int32_t) * n2) != hipSuccess ||
+            dev_malloc(&val2, sizeof(int32_t) * n2) != hipSuccess) { fail(TGM_ENOMEM); break; }
         hipLaunchKernelGGL(k_incidences, dim3(grid_for(E, 256)), dim3(256), 0, s, E, N, src, dst,
                            key, val);
         int bits = 1;
@@ -379,7 +379,7 @@ extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *sr
         // LSD radix sort is stable: within a node, incidences keep event order
         if (hipcub::DeviceRadixSort::SortPairs(nullptr, tmp_bytes, key, key2, val, val2, (int)n2,
                                                0, bits, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
-        if (hipMalloc(&tmp, tmp_bytes) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (dev_malloc(&tmp, tmp_bytes) != hipSuccess) { fail(TGM_ENOMEM); break; }
         if (hipcub::DeviceRadixSort::SortPairs(tmp, tmp_bytes, key, key2, val, val2, (int)n2, 0,
                                                bits, s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         hipLaunchKernelGGL(k_offsets, dim3(grid_for(n2 + 1, 256)), dim3(256), 0, s, n2, N, key2,
@@ -389,7 +389,7 @@ extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *sr
                 hipSuccess ||
             hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         g->n_adj = n_adj;
-        if (hipMalloc(&g->adj, sizeof(AdjRec) * (n_adj > 0 ? n_adj : 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (dev_malloc(&g->adj, sizeof(AdjRec) * (n_adj > 0 ? n_adj : 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
         if (n_adj > 0)
             hipLaunchKernelGGL(k_adj_records, dim3(grid_for(n_adj, 256)), dim3(256), 0, s, n_adj,
                                key2, val2, src, dst, t, g->adj);

@@ -1,4 +1,4 @@
-// Similarity-based staleness mitigation (MSPipe-S, Sec. 4.3) of the fetched
+// Similarity-based staleness mitigation (MSPipe-S, Sec. 3.3) of the fetched
 // memories of a batch, between the fetch and the memory update.  For the
 // fetched node set U (positions p < n, memory times mem_ts):
 //   gap       dt_p = T - mem_ts_p, T the time of the batch's first event;
@@ -630,12 +630,12 @@ extern "C" tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int3
     mt->nbp = nb <= 4 ? 4 : (nb <= 12 ? 12 : 64);   // the widths k_mit_omega reads
     mt->K = K;
     const size_t c = (size_t)max_nodes;
-    if (hipMalloc((void **)&mt->gamma, sizeof(double)) != hipSuccess ||
-        hipMalloc((void **)&mt->n_stale, sizeof(int32_t)) != hipSuccess ||
-        hipMalloc((void **)&mt->stale, sizeof(int32_t) * c) != hipSuccess ||
-        hipMalloc((void **)&mt->omega, sizeof(int32_t) * c * K) != hipSuccess ||
-        hipMalloc((void **)&mt->part, sizeof(int2) * kMitOmegaGrid * kMitMaxK) != hipSuccess ||
-        hipMalloc((void **)&mt->done, sizeof(int32_t) * c) != hipSuccess ||
+    if (dev_malloc((void **)&mt->gamma, sizeof(double)) != hipSuccess ||
+        dev_malloc((void **)&mt->n_stale, sizeof(int32_t)) != hipSuccess ||
+        dev_malloc((void **)&mt->stale, sizeof(int32_t) * c) != hipSuccess ||
+        dev_malloc((void **)&mt->omega, sizeof(int32_t) * c * K) != hipSuccess ||
+        dev_malloc((void **)&mt->part, sizeof(int2) * kMitOmegaGrid * kMitMaxK) != hipSuccess ||
+        dev_malloc((void **)&mt->done, sizeof(int32_t) * c) != hipSuccess ||
         tgm::mitigate_reserve(mt, 1) != TGM_OK) {
         tgm_mitigator_destroy(mt);
         return TGM_ENOMEM;
@@ -660,6 +660,8 @@ extern "C" tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt)
     return TGM_OK;
 }
 
+int32_t tgm::mitigate_slots(tgm_mitigator_t mt) { return mt ? mt->nslots : 0; }
+
 tgm_status_t tgm::mitigate_reserve(tgm_mitigator_t mt, int32_t nslots)
 {
     if (!mt || nslots < 1)
@@ -675,8 +677,8 @@ tgm_status_t tgm::mitigate_reserve(tgm_mitigator_t mt, int32_t nslots)
     mt->ncnt = nullptr;
     mt->nslots = 0;
     const size_t c = (size_t)mt->cap * nslots;
-    if (hipMalloc((void **)&mt->nset, sizeof(int32_t) * c * mt->nbp) != hipSuccess ||
-        hipMalloc((void **)&mt->ncnt, sizeof(int32_t) * c) != hipSuccess)
+    if (dev_malloc((void **)&mt->nset, sizeof(int32_t) * c * mt->nbp) != hipSuccess ||
+        dev_malloc((void **)&mt->ncnt, sizeof(int32_t) * c) != hipSuccess)
         return TGM_ENOMEM;
     mt->nslots = nslots;
     return TGM_OK;
@@ -781,6 +783,10 @@ extern "C" tgm_status_t tgm_state_set_mitigation(tgm_state_t st, tgm_mitigator_t
 {
     if (!st || (mt && (!(p >= 0.0 && p <= 1.0) || !(lambda >= 0.0f && lambda <= 1.0f))))
         return TGM_EINVAL;
+    // the executor's neighbour-set slots (one per sample buffer set), made
+    // here so that a run allocates nothing
+    if (mt)
+        TGM_TRY_STATUS(tgm::mitigate_reserve(mt, 1 + TGM_MAX_SAMPLE_SETS));
     st->mit = mt;
     st->mit_p = p;
     st->mit_lambda = lambda;

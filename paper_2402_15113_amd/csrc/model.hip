@@ -1283,7 +1283,7 @@ __global__ __launch_bounds__(512) void k_attn_gather(AttnArgs g, int n_attn, Gat
 //   q_r,eta . K_s,eta = sum_k a_s[k] U[k][(r, eta)] + seedK_s,eta . q_r,eta
 // with a_s = [phi || efeat] the slot row, seedK_s the neighbour's key part of
 // P (node projection plus b_k) and U[k][(r, eta)] = sum_{d in head eta}
-// W_k[d][k] q_r[d] (Sec. 4's attention restated by associativity).  K itself
+// W_k[d][k] q_r[d] (Eq. 1's emb() restated by associativity).  K itself
 // is never formed: the per-slot GEMM produces V (VNB column blocks) and one
 // block of 16 score columns (n = r * H + eta, RT * H <= 16) instead of the
 // 2M columns of K | V.  Roles of the kMaxWaves wavefronts:
@@ -1912,7 +1912,7 @@ tgm_status_t create_jodie(tgm_model *m, const tgm_model_desc *d, const tgm_weigh
         bias[3 * MP + k] = w->b_hh[k];
     }
     auto alloc = [](void **p, size_t bytes) {
-        return hipMalloc(p, bytes ? bytes : 16) == hipSuccess;
+        return dev_malloc(p, bytes ? bytes : 16) == hipSuccess;
     };
     if (!alloc((void **)&m->gru_bx, bx.size() * 4) || !alloc((void **)&m->gru_bh, bh.size() * 4) ||
         !alloc((void **)&m->gru_bias, bias.size() * 4) ||
@@ -2075,7 +2075,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     tgm_status_t st = TGM_OK;
     do {
         auto alloc = [&](void **p, size_t bytes) {
-            return hipMalloc(p, bytes ? bytes : 16) == hipSuccess;
+            return dev_malloc(p, bytes ? bytes : 16) == hipSuccess;
         };
         if (!alloc((void **)&m->gru_bx, bx.size() * 4) || !alloc((void **)&m->gru_bh, bh.size() * 4) ||
             !alloc((void **)&m->gru_bias, bias.size() * 4) ||
@@ -2502,30 +2502,6 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     if (R > 0)
         return launch_attn(m, aa, next, s);
     return next ? launch_gather(*next, s) : TGM_OK;
-}
-
-tgm_status_t tgm::exec_latest_reserve(tgm_state_t st, int32_t nslots, int32_t cap)
-{
-    if (!st || nslots < 1 || cap < 0)
-        return TGM_EINVAL;
-    if (nslots <= st->xwin_slots && cap <= st->xwin_cap)
-        return TGM_OK;
-    if (st->xwin && hipDeviceSynchronize() != hipSuccess)
-        return TGM_EDEVICE;
-    (void)hipFree(st->xwin);
-    st->xwin = nullptr;
-    st->xwin_slots = st->xwin_cap = 0;
-    const int32_t c = std::max(cap, 1);
-    const size_t bytes = sizeof(uint64_t) * (size_t)nslots * c;
-    if (hipMalloc((void **)&st->xwin, bytes) != hipSuccess)
-        return TGM_ENOMEM;
-    // zero keys are older than every tag; a synchronous clear (set-up only)
-    if (hipMemset(st->xwin, 0, bytes) != hipSuccess || hipDeviceSynchronize() != hipSuccess)
-        return TGM_EDEVICE;
-    st->xwin_slots = nslots;
-    st->xwin_cap = c;
-    st->xwin_tag = 0;
-    return TGM_OK;
 }
 
 tgm_status_t tgm::exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b,

@@ -15,38 +15,20 @@
 
 using namespace tgm;
 
-namespace {
-
-struct Events {
-    hipEvent_t e[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
-    ~Events()
-    {
-        for (hipEvent_t x : e)
-            if (x)
-                hipEventDestroy(x);
-    }
-    bool create()
-    {
-        for (hipEvent_t &x : e)
-            if (hipEventCreateWithFlags(&x, hipEventDisableTiming) != hipSuccess)
-                return false;
-        return true;
-    }
-};
-
-}  // namespace
-
 extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m,
                                       int64_t i0, int64_t n, int32_t B, int32_t nb, int32_t cap,
                                       const tgm_sample_buffers *sb, int32_t nsb,
                                       const tgm_fetch_buffers *fb, float *mem_new,
                                       double *new_mem_ts, int64_t *winner, float *h,
-                                      void *stream, void *prefetch_stream)
+                                      float *h_trace, float *s_trace, void *stream,
+                                      void *prefetch_stream)
 {
     if (!g || !st || !m || !sb || !fb || i0 < 0 || n < 0 || B < 1 || !mem_new || !h)
         return TGM_EINVAL;
     if (nsb < 2 || (nsb & 1))
         return TGM_EINVAL;
+    if (nsb > st->xwin_slots || (st->mit && mitigate_slots(st->mit) < 1 + nsb))
+        return TGM_ESIZE;
     if (n == 0)
         return TGM_OK;
     if ((i0 + n - 1) * (int64_t)B >= g->E)
@@ -54,9 +36,8 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     hipStream_t main = as_stream(stream), pre = as_stream(prefetch_stream);
     if (main == pre)
         return TGM_EINVAL;
-    Events ev;   // 0-1: sampled chunk by parity, 2-3: computed chunk by parity, 4: start
-    if (!ev.create())
-        return TGM_EDEVICE;
+    // events 0-1: sampled chunk by parity, 2-3: computed chunk by parity, 4: start
+    hipEvent_t *const ev = st->run_ev;
     const int64_t K = nsb / 2;   // iterations per chunk
     const int64_t nch = (n + K - 1) / K;
     auto batch = [&](int64_t k, int64_t *lo) {   // the k-th iteration of the run
@@ -64,12 +45,9 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
         return (int32_t)std::min<int64_t>(B, g->E - *lo);
     };
     // with mitigation on, the neighbour sets of each node set are built beside
-    // the sample, into mitigator slot 1 + (k % nsb)
-    if (st->mit)
-        TGM_TRY_STATUS(mitigate_reserve(st->mit, 1 + nsb));
-    // the latest-message reduce of each batch also runs beside its sample,
-    // into key array k % nsb (so the update's GRU launch skips it)
-    TGM_TRY_STATUS(exec_latest_reserve(st, nsb, cap));
+    // the sample, into mitigator slot 1 + (k % nsb); the latest-message reduce
+    // of each batch also runs beside its sample, into key array k % nsb (so
+    // the update's GRU launch skips it)
     std::vector<uint64_t *> xwin(nsb, nullptr);
     std::vector<uint64_t> xtag(nsb, 0);
     auto sample_chunk = [&](int64_t c) -> tgm_status_t {
@@ -87,14 +65,14 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
                                               s.root_pos + b, s.n_nodes, pre, &xwin[k % nsb],
                                               &xtag[k % nsb]));
         }
-        TGM_HIP(hipEventRecord(ev.e[c & 1], pre));
+        TGM_HIP(hipEventRecord(ev[c & 1], pre));
         return TGM_OK;
     };
     // the prefetch stream starts after everything issued before on the main one
-    TGM_HIP(hipEventRecord(ev.e[4], main));
-    TGM_HIP(hipStreamWaitEvent(pre, ev.e[4], 0));
+    TGM_HIP(hipEventRecord(ev[4], main));
+    TGM_HIP(hipStreamWaitEvent(pre, ev[4], 0));
     TGM_TRY_STATUS(sample_chunk(0));
-    TGM_HIP(hipStreamWaitEvent(main, ev.e[0], 0));
+    TGM_HIP(hipStreamWaitEvent(main, ev[0], 0));
     {   // the first iteration's fetch on its own
         GatherPlan plan;
         TGM_TRY_STATUS(fetch_plan(st, i0, sb[0].nodes, sb[0].n_nodes, cap, fb->mem, fb->mem_ts,
@@ -104,7 +82,7 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     for (int64_t c = 0; c < nch; ++c) {
         if (c + 1 < nch) {
             if (c >= 1)   // chunk c-1, the last user of these sample sets, is computed
-                TGM_HIP(hipStreamWaitEvent(pre, ev.e[2 + ((c - 1) & 1)], 0));
+                TGM_HIP(hipStreamWaitEvent(pre, ev[2 + ((c - 1) & 1)], 0));
             TGM_TRY_STATUS(sample_chunk(c + 1));
         }
         const int64_t kend = std::min(n, (c + 1) * K);
@@ -113,14 +91,23 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             const int32_t b = batch(k, &lo);
             const bool more = k + 1 < n;
             if (more && k + 1 == kend)   // the next iteration's samples are the next chunk's
-                TGM_HIP(hipStreamWaitEvent(main, ev.e[(c + 1) & 1], 0));
+                TGM_HIP(hipStreamWaitEvent(main, ev[(c + 1) & 1], 0));
             TGM_TRY_STATUS(compute_iteration(st, m, g, i0 + k, sb[k % nsb], *fb, cap, lo, b, nb,
                                              mem_new, new_mem_ts, winner, h,
                                              more ? &sb[(k + 1) % nsb] : nullptr,
                                              (int32_t)(1 + k % nsb), xwin[k % nsb],
                                              xtag[k % nsb], main));
+            // per-iteration copies of the embeddings and new memories
+            if (h_trace && b > 0)
+                TGM_HIP(hipMemcpyAsync(h_trace + (size_t)k * 3 * B * m->M, h,
+                                       sizeof(float) * 3 * (size_t)b * m->M,
+                                       hipMemcpyDeviceToDevice, main));
+            if (s_trace)
+                TGM_HIP(hipMemcpyAsync(s_trace + (size_t)k * cap * m->M, mem_new,
+                                       sizeof(float) * (size_t)cap * m->M,
+                                       hipMemcpyDeviceToDevice, main));
         }
-        TGM_HIP(hipEventRecord(ev.e[2 + (c & 1)], main));
+        TGM_HIP(hipEventRecord(ev[2 + (c & 1)], main));
     }
     // the events may be destroyed now: the waits already enqueued keep the
     // state they captured

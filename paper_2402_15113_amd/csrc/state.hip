@@ -126,6 +126,9 @@ extern "C" tgm_status_t tgm_state_destroy(tgm_state_t st)
     hipFree(st->r_mail_ts);
     hipFree(st->win);
     hipFree(st->xwin);
+    for (hipEvent_t e : st->run_ev)
+        if (e)
+            hipEventDestroy(e);
     delete st;
     return TGM_OK;
 }
@@ -144,21 +147,38 @@ extern "C" tgm_status_t tgm_state_create(int32_t N, int32_t M, int32_t D_m, int3
     st->max_batch = max_batch;
     st->ring.resize(s + 1);
     const size_t rows = (size_t)(s + 1) * st->ring_rows();
-    bool ok = hipMalloc(&st->mem, sizeof(float) * N * (size_t)M) == hipSuccess &&
-              hipMalloc(&st->mem_ts, sizeof(double) * N) == hipSuccess &&
-              hipMalloc(&st->mail, sizeof(float) * (N * (size_t)D_m + 1)) == hipSuccess &&
-              hipMalloc(&st->mail_ts, sizeof(double) * N) == hipSuccess &&
-              hipMalloc(&st->ver, sizeof(int32_t) * N) == hipSuccess &&
-              hipMalloc(&st->r_flag, sizeof(int32_t) * rows) == hipSuccess &&
-              hipMalloc(&st->r_node, sizeof(int32_t) * rows) == hipSuccess &&
-              hipMalloc(&st->r_mem, sizeof(float) * rows * M) == hipSuccess &&
-              hipMalloc(&st->r_mail, sizeof(float) * (rows * D_m + 1)) == hipSuccess &&
-              hipMalloc(&st->r_mem_ts, sizeof(double) * rows) == hipSuccess &&
-              hipMalloc(&st->r_mail_ts, sizeof(double) * rows) == hipSuccess &&
-              hipMalloc(&st->win, sizeof(uint64_t) * N) == hipSuccess;
+    bool ok = dev_malloc(&st->mem, sizeof(float) * N * (size_t)M) == hipSuccess &&
+              dev_malloc(&st->mem_ts, sizeof(double) * N) == hipSuccess &&
+              dev_malloc(&st->mail, sizeof(float) * (N * (size_t)D_m + 1)) == hipSuccess &&
+              dev_malloc(&st->mail_ts, sizeof(double) * N) == hipSuccess &&
+              dev_malloc(&st->ver, sizeof(int32_t) * N) == hipSuccess &&
+              dev_malloc(&st->r_flag, sizeof(int32_t) * rows) == hipSuccess &&
+              dev_malloc(&st->r_node, sizeof(int32_t) * rows) == hipSuccess &&
+              dev_malloc(&st->r_mem, sizeof(float) * rows * M) == hipSuccess &&
+              dev_malloc(&st->r_mail, sizeof(float) * (rows * D_m + 1)) == hipSuccess &&
+              dev_malloc(&st->r_mem_ts, sizeof(double) * rows) == hipSuccess &&
+              dev_malloc(&st->r_mail_ts, sizeof(double) * rows) == hipSuccess &&
+              dev_malloc(&st->win, sizeof(uint64_t) * N) == hipSuccess &&
+              dev_malloc(&st->xwin, sizeof(uint64_t) * N * (size_t)TGM_MAX_SAMPLE_SETS) ==
+                  hipSuccess;
     if (!ok) {
         tgm_state_destroy(st);
         return TGM_ENOMEM;
+    }
+    // the executor's latest-message key arrays: one per sample buffer set,
+    // indexed by node-set position (< N); zero keys are older than every tag
+    st->xwin_slots = TGM_MAX_SAMPLE_SETS;
+    st->xwin_cap = N;
+    st->xwin_tag = 0;
+    for (hipEvent_t &e : st->run_ev)
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+            tgm_state_destroy(st);
+            return TGM_EDEVICE;
+        }
+    if (hipMemsetAsync(st->xwin, 0, sizeof(uint64_t) * N * (size_t)TGM_MAX_SAMPLE_SETS,
+                       as_stream(stream)) != hipSuccess) {
+        tgm_state_destroy(st);
+        return TGM_EDEVICE;
     }
     tgm_status_t rc = tgm_state_reset(st, stream);
     if (rc != TGM_OK) {

@@ -47,7 +47,7 @@ class Stage:
         """src, dst, t, neg: numpy or torch arrays of the event stream; efeat
         [E x D_e] fp32 or None; weights a ``workloads.Weights``;
         ``mitigation=dict(p=.., lam=.., K=..)`` turns on the similarity-based
-        staleness mitigation (Sec. 4.3) of every fetch."""
+        staleness mitigation (Sec. 3.3) of every fetch."""
         dev = torch.device(device)
         self.dev = dev
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
@@ -140,12 +140,14 @@ class Stage:
                           stream=st)
         self.last, self._set = (i, n), 0
 
-    def run(self, i0: int, n: int):
+    def run(self, i0: int, n: int, trace: bool = False):
         """Enqueue iterations i0 .. i0+n-1 through the library's pipelined
         executor (tgm_stage_run).  Ordered after everything issued before on
-        the main stream; the main stream ends after the last iteration."""
+        the main stream; the main stream ends after the last iteration.  With
+        trace=True returns device tensors (h [n x 3B x M], s_new [n x cap x M])
+        holding every iteration's embeddings and new memories."""
         if n <= 0:
-            return
+            return None
         if self._bufs is None:
             sb = (tgm.SampleBuffers * len(self.sets))(
                 *[tgm.buffers(tgm.SampleBuffers, **vars(b)) for b in self.sets])
@@ -153,13 +155,18 @@ class Stage:
                              mail=self.f_mail, mail_ts=self.f_mail_ts, ver=self.f_ver)
             self._bufs = (sb, fb)
         sb, fb = self._bufs
+        h_tr = s_tr = None
+        if trace:
+            h_tr = torch.zeros((n, 3 * self.B, self.M), dtype=torch.float32, device=self.dev)
+            s_tr = torch.zeros((n, self.cap, self.M), dtype=torch.float32, device=self.dev)
         tgm.tgm_stage_run(self.g, self.st, self.m, i0, n, self.B, self.nb, self.cap, sb, fb,
                           self.mem_new, self.new_mem_ts,
                           self.winner if self.want_winner else None, self.h, self.stream,
-                          self.pre_stream)
+                          self.pre_stream, h_trace=h_tr, s_trace=s_tr)
         last = i0 + n - 1
         lo, hi = self.batch(last)
         self.last, self._set = (last, hi - lo), (n - 1) % len(self.sets)
+        return (h_tr, s_tr) if trace else None
 
     # ------------------------------------------------------------ read-back
     def outputs(self):
@@ -241,7 +248,7 @@ def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None)
 # The paper's five stages (Sec. 3.2) as this library's kernels on the
 # sequential path (one call per stage).  Edge features are read inside the
 # attention kernel, so the feature fetch has no kernel of its own; the
-# mitigation belongs to the memory fetch (Sec. 4.3).
+# mitigation belongs to the memory fetch (Sec. 3.3).
 STAGE_KERNELS = {1: ("k_sample_batch", "k_ns_mark", "k_ns_pos"), 2: (),
                  3: ("k_gather_state", "k_mit_prep", "k_mit_select", "k_mit_omega"),
                  4: ("k_gru", "k_node_proj", "k_attn_fold", "k_attn", "k_tproj"),

@@ -18,7 +18,8 @@ TGM_OK, TGM_EINVAL, TGM_ERANGE, TGM_EORDER, TGM_ESIZE, TGM_EDEVICE, TGM_ENOMEM =
     0, -1, -2, -3, -4, -5, -6
 
 # Every exported symbol of include/tgm.h
-SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_graph_create",
+SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_alloc_count",
+           "tgm_graph_create",
            "tgm_graph_destroy", "tgm_graph_info", "tgm_batch_roots", "tgm_sample", "tgm_sample_batch",
            "tgm_node_set", "tgm_sample_nodes", "tgm_state_create", "tgm_state_destroy", "tgm_state_reset",
            "tgm_state_flush", "tgm_state_read", "tgm_state_load", "tgm_state_checkpoint_bytes",
@@ -107,7 +108,8 @@ def lib():
                                   V],
             "tgm_embed": [V, V, I32, I32, P, P, P, P, P, P, P, P, I32, P, V],
             "tgm_stage_run": [V, V, V, I64, I64, I32, I32, I32, C.POINTER(SampleBuffers), I32,
-                              C.POINTER(FetchBuffers), P, P, P, P, V, V],
+                              C.POINTER(FetchBuffers), P, P, P, P, P, P, V, V],
+            "tgm_alloc_count": [C.POINTER(I64)],
             "tgm_mitigator_create": [I32, I32, I32, C.POINTER(V)],
             "tgm_mitigator_destroy": [V],
             "tgm_mitigate": [V, V, I64, P, P, I32, P, P, I32, C.c_double, C.c_float, V],
@@ -295,11 +297,21 @@ def buffers(struct, **tensors):
 
 
 def tgm_stage_run(g, st, m, i0, n, B, nb, cap, sample_bufs, fetch_bufs, mem_new, new_mem_ts,
-                  winner, h, stream, prefetch_stream):
-    """sample_bufs: a (SampleBuffers * nsb) array; fetch_bufs: a FetchBuffers."""
+                  winner, h, stream, prefetch_stream, h_trace=None, s_trace=None):
+    """sample_bufs: a (SampleBuffers * nsb) array; fetch_bufs: a FetchBuffers;
+    h_trace [n x 3B x M] and s_trace [n x cap x M] optional per-iteration
+    copies of h and mem_new."""
     _check("tgm_stage_run", lib().tgm_stage_run(
         g, st, m, i0, n, B, nb, cap, sample_bufs, len(sample_bufs), C.byref(fetch_bufs),
-        _p(mem_new), _p(new_mem_ts), _p(winner), _p(h), _s(stream), _s(prefetch_stream)))
+        _p(mem_new), _p(new_mem_ts), _p(winner), _p(h), _p(h_trace), _p(s_trace), _s(stream),
+        _s(prefetch_stream)))
+
+
+def alloc_count() -> int:
+    """Device allocations the library has made in this process so far."""
+    c = I64()
+    _check("tgm_alloc_count", lib().tgm_alloc_count(C.byref(c)))
+    return int(c.value)
 
 
 # ------------------------------------------------------------- mitigation

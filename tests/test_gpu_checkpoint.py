@@ -128,24 +128,49 @@ def test_checkpoint_argument_errors():
 
 
 @pytest.mark.parametrize("name,s,E,j,n", [("tiny", 2, 6000, 15, 12), ("wiki", 3, 40_000, 40, 12)])
-def test_oracle_resumes_from_gpu_checkpoint(orc, name, s, E, j, n):
-    """A parity window that starts mid-run from a GPU checkpoint: the GPU
-    runs iterations 0..j-1, its checkpoint (committed tables and the pending
-    write sets) seeds the oracle, and both run iterations j..j+n-1."""
+def test_window_resumed_from_gpu_checkpoint(orc, name, s, E, j, n):
+    """A parity window that starts mid-run from a GPU checkpoint: the GPU runs
+    iterations 0..j-1 (pipelined), saves, and a fresh state restored from the
+    checkpoint runs j..j+n-1.  The oracle runs 0..j+n-1 on its own (it takes
+    no input from the GPU) and every step of the window is compared.  The
+    checkpoint's content is checked too: its committed tables with its pending
+    write sets applied in order equal the tables of a separate oracle run
+    through j-1 and flushed."""
     from ckpt_format import parse
     from paper_2402_15113_amd.stage import from_workload
-    from test_gpu_parity import compare_state, compare_step
+    from test_gpu_parity import close, compare_state, compare_step, exact
     wl = make_workload(name, E=E, s=s)
     w = make_weights(wl.M, wl.D_e, wl.D_t)
-    st = from_workload(wl, w)
-    st.run(0, j)
-    ck = parse(st.save_checkpoint())
+    a = from_workload(wl, w)
+    a.run(0, j)
+    raw = a.save_checkpoint()
+    a.close()
+    ck = parse(raw)
     print(f"[ckpt] {name} s={s}: resume at {ck['next_iter']} with "
           f"{len(ck['pending'])} pending write sets", flush=True)
     assert ck["next_iter"] == j and len(ck["pending"]) == s
+    # the checkpoint's tables, flushed by hand, against the oracle's
+    mem, mem_ts, mail, mail_ts, ver = (ck[k].copy() for k in ("mem", "mem_ts", "mail",
+                                                               "mail_ts", "ver"))
+    for it, node, wm, wmt, wml, wmlt in ck["pending"]:
+        mem[node], mem_ts[node], mail[node], mail_ts[node], ver[node] = wm, wmt, wml, wmlt, it
+    ref = orc.Oracle(wl, w)
+    for i in range(j):
+        ref.step(want="light")
+    ref.flush()
+    rs = ref.state()
+    exact("ver", ver, rs["ver"])
+    exact("mem_ts", mem_ts, rs["mem_ts"])
+    exact("mail_ts", mail_ts, rs["mail_ts"])
+    close("mem", mem, rs["mem"])
+    close("mail", mail, rs["mail"])
+    del ref
+    # the resumed run against an oracle that ran from the start
+    st = from_workload(wl, w)
+    st.restore_checkpoint(raw)
     o = orc.Oracle(wl, w)
-    o.set_state(j, ck["mem"], ck["mem_ts"], ck["mail"], ck["mail_ts"], ck["ver"],
-                pending=ck["pending"])
+    for i in range(j):
+        o.step(want="light")
     for i in range(j, j + n):
         st.step(i)
         compare_step(st.outputs(), o.step(want="all"))

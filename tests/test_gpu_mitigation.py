@@ -1,4 +1,4 @@
-"""GPU staleness mitigation (MSPipe-S, Sec. 4.3) through the C ABI against the
+"""GPU staleness mitigation (MSPipe-S, Sec. 3.3) through the C ABI against the
 fp64 oracle, which applies the same readings.
 
 Bit-exact: gamma, the stale positions and their Omega (positions in the node

@@ -185,17 +185,18 @@ def test_wiki_full_run(orc):
 
 def test_lastfm_no_edge_features_window(orc):
     """LastFM-shaped: D_e = 0, heavy repetition (latest-message reduce and
-    write-set conflicts), B = 2000, s = 2: first 24 batches."""
+    write-set conflicts), B = 2000, s = 2: first 64 batches."""
     wl = make_workload("lastfm")
     w = make_weights(wl.M, wl.D_e, wl.D_t)
-    run_pair(orc, wl, w, n_iters=24)
+    run_pair(orc, wl, w, n_iters=64)
 
 
 @pytest.mark.parametrize("s", [1, 2, 4])
 def test_reddit_window(orc, s):
+    """REDDIT-shaped, first 32 batches."""
     wl = make_workload("reddit", s=s)
     w = make_weights(wl.M, wl.D_e, wl.D_t)
-    run_pair(orc, wl, w, n_iters=16)
+    run_pair(orc, wl, w, n_iters=32)
 
 
 def test_mid_run_window_from_synthetic_state(orc):

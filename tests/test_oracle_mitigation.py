@@ -1,4 +1,4 @@
-"""Pins for the oracle's staleness mitigation (MSPipe-S, Sec. 4.3).
+"""Pins for the oracle's staleness mitigation (MSPipe-S, Sec. 3.3).
 
 * gamma          -- numpy's inverted-CDF quantile (the nearest-rank definition);
 * stale set, Omega and the blended rows -- re-derived by brute force in Python
@@ -175,3 +175,37 @@ def test_update_consumes_mitigated_memory(tiny_mitigated):
                 np.testing.assert_array_equal(r.s_new[v], r.m_mem[v])
                 n += 1
     assert n > 0
+
+
+def test_update_of_stale_node_with_mail_reads_blended_memory(orc):
+    """Sec. 3.3's second equation: the memory update of a stale node takes the
+    blended memory as its previous state.  For every stale node with mail the
+    oracle's s' must equal an independent fp64 GRU (torch's GRUCell, with the
+    input [mail || cos(omega (mail_ts - mem_ts) + beta)] formed here in numpy)
+    of the blended row, and differ from the same GRU of the row as fetched."""
+    torch = pytest.importorskip("torch")
+    wl = make_workload("tiny", E=6000, s=2)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random")
+    res = _run(orc, wl, w, 2, dict(p=0.9, lam=0.5, K=4), 30)
+    M = wl.M
+    cell = torch.nn.GRUCell(wl.D_m + wl.D_t, M).double()
+    with torch.no_grad():
+        cell.weight_ih.copy_(torch.from_numpy(np.asarray(w.W_ih, np.float64)))
+        cell.weight_hh.copy_(torch.from_numpy(np.asarray(w.W_hh, np.float64)))
+        cell.bias_ih.copy_(torch.from_numpy(np.asarray(w.b_ih, np.float64)))
+        cell.bias_hh.copy_(torch.from_numpy(np.asarray(w.b_hh, np.float64)))
+    omega, beta = np.asarray(w.omega, np.float64), np.asarray(w.beta, np.float64)
+    n = 0
+    for r in res:
+        for v in r.m_stale:
+            if r.f_ver[v] < 0 or np.array_equal(r.m_mem[v], r.f_mem[v]):
+                continue
+            phi = np.cos(omega * (r.f_mail_ts[v] - r.f_mem_ts[v]) + beta)
+            x = torch.from_numpy(np.concatenate([r.f_mail[v], phi]))[None]
+            with torch.no_grad():
+                blended = cell(x, torch.from_numpy(r.m_mem[v].copy())[None])[0].numpy()
+                fetched = cell(x, torch.from_numpy(r.f_mem[v].copy())[None])[0].numpy()
+            np.testing.assert_allclose(r.s_new[v], blended, rtol=0, atol=1e-12)
+            assert np.abs(r.s_new[v] - fetched).max() > 1e-6
+            n += 1
+    assert n > 20

@@ -1,5 +1,5 @@
 """Pins for the oracle's exact memories (``x_mem``) and the staleness-error
-measurement of MSPipe-S (Sec. 4.3, App. C.3).
+measurement of MSPipe-S (Sec. 3.3, App. E.2).
 
 * s = 0: a fetch is never stale, so the exact memories equal the fetched ones
   bit for bit (closed form);
