@@ -32,6 +32,26 @@ def _gpu():
     tgm.lib()
 
 
+def projection_close(name, g, r, w):
+    """JODIE's embedding h = s' * f with f = 1 + w_t (t - ts') formed exactly in
+    fp64 (reading R27): an error e in s' reaches h as |f| e, so h is held to
+    the s' tolerance scaled by |f| (1e-5 |f| + 1e-4 |h|).  f can reach ~80 on
+    the GDELT-shaped stream, where memory times lag the query by up to 2.5
+    years."""
+    from test_gpu_parity import ATOL, RTOL
+    f = 1.0 + np.asarray(w.w_t, np.float64)[None, :] * \
+        (r.root_ts - r.new_mem_ts[r.root_pos])[:, None]
+    g = np.asarray(g, np.float64)
+    err = np.abs(g - r.h)
+    tol = ATOL * np.maximum(1.0, np.abs(f)) + RTOL * np.abs(r.h)
+    bad = err > tol
+    if bad.any():
+        k = np.unravel_index(np.argmax(err - tol), err.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())}/{bad.size} outside tolerance; worst at "
+                             f"{k}: gpu {g[k]!r} oracle {r.h[k]!r} f {f[k]!r}")
+    return float(err.max()) if err.size else 0.0
+
+
 def traced_pair(orc, wl, w, first, n, *, s=None, init=None, gpu_efeat=None, skip_to=None,
                 mitigation=None):
     """GPU: the executor over iterations first .. first+n-1 (from the state
@@ -63,8 +83,11 @@ def traced_pair(orc, wl, w, first, n, *, s=None, init=None, gpu_efeat=None, skip
         k = i - skip_to
         h = h_tr[k, :r.R].cpu().numpy()
         sn = s_tr[k, :r.n_U].cpu().numpy()
-        worst["h"] = max(worst["h"], close(f"h[{i}]", h, r.h))
         worst["s_new"] = max(worst["s_new"], close(f"s_new[{i}]", sn, r.s_new))
+        if getattr(w, "kind", "tgn") == "jodie":
+            worst["h"] = max(worst["h"], projection_close(f"h[{i}]", h, r, w))
+        else:
+            worst["h"] = max(worst["h"], close(f"h[{i}]", h, r.h))
     del h_tr, s_tr
     st.flush()
     o.flush()
