@@ -400,6 +400,27 @@ tgm_status_t tgm_mitigate(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event
                           const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
                           float *mem, const double *mem_ts, int32_t M, double p, float lambda,
                           void *stream);
+/* The mitigation of tgm_mitigate without a mitigator handle, for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same computation and results as
+ * tgm_mitigate with a mitigator of the same nb and K.  Its work space (the
+ * neighbour sets, gamma, the stale list, Omega, the chunk lists and counters)
+ * lives in a fixed array of TGM_MITIGATE_NOALLOC_BYTES bytes that the library
+ * holds on every GPU it runs on until the process ends; the call allocates
+ * nothing.  The first call on a device looks that device's array up (the
+ * calling thread's current device must be the stream's device).  All calls on
+ * one GPU share the array and it keeps the last call's contents: calls that
+ * overlap on one GPU (other streams, other threads) race; calls ordered on
+ * one stream do not.  Each call clears what it needs at zero itself.  Limits:
+ * cap <= TGM_MITIGATE_NOALLOC_MAX_NODES (else TGM_ESIZE); 1 <= nb <= 64 and
+ * 1 <= K <= 16 (else TGM_EINVAL).  Other arguments and errors as for
+ * tgm_mitigate. */
+#define TGM_MITIGATE_NOALLOC_MAX_NODES 32768
+#define TGM_MITIGATE_NOALLOC_BYTES (12u << 20)
+tgm_status_t tgm_mitigate_noalloc(tgm_graph_t g, int64_t first_event, const int32_t *nodes,
+                                  const int32_t *n_nodes, int32_t cap, float *mem,
+                                  const double *mem_ts, int32_t M, int32_t nb, int32_t K,
+                                  double p, float lambda, void *stream);
 /* Device copies of the last call's results (each pointer may be NULL): gamma
  * [1], n_stale [1], stale [max_nodes] (positions, ascending; the first
  * *n_stale are valid), omega [max_nodes x K] (positions, -1 padded; row q

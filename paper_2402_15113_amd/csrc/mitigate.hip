@@ -28,6 +28,8 @@
 // subtraction the oracle makes.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "common.h"
 
 using namespace tgm;
@@ -61,6 +63,9 @@ static_assert(kMitMaxChunks * kMitMaxK <= kMitChunk, "the chunk lists fit the ro
 constexpr int kMitOmegaGrid = 1024;         // k_mit_omega workgroups
 
 constexpr int kMitMaxNodes = 1 << 20;
+static_assert(TGM_MITIGATE_NOALLOC_MAX_NODES * (64 + 1 + 1 + 16 + 1) * 4 +
+                  kMitOmegaGrid * kMitMaxK * 8 + 9 * 256 <= TGM_MITIGATE_NOALLOC_BYTES,
+              "the no-allocation work space fits its largest call");
 
 // ---------------------------------------------------------------- prep
 // One wavefront per fetched node: its sorted distinct neighbour set before T,
@@ -684,6 +689,76 @@ tgm_status_t tgm::mitigate_reserve(tgm_mitigator_t mt, int32_t nslots)
     return TGM_OK;
 }
 
+namespace {
+
+// The work space one mitigation reads and writes: a mitigator's (one of its
+// neighbour-set slots), or the fixed per-device array of
+// tgm_mitigate_noalloc.
+struct MitWork {
+    int32_t nb = 0, nbp = 0, K = 0;
+    int32_t *nset = nullptr, *ncnt = nullptr;   // [cap x nbp], [cap]
+    double *gamma = nullptr;
+    int32_t *n_stale = nullptr, *stale = nullptr, *omega = nullptr, *done = nullptr;
+    int2 *part = nullptr;
+};
+
+MitWork work_of(const tgm_mitigator *mt, int32_t slot)
+{
+    MitWork w;
+    const int64_t o = (int64_t)slot * mt->cap;
+    w.nb = mt->nb;
+    w.nbp = mt->nbp;
+    w.K = mt->K;
+    w.nset = mt->nset + o * mt->nbp;
+    w.ncnt = mt->ncnt + o;
+    w.gamma = mt->gamma;
+    w.n_stale = mt->n_stale;
+    w.stale = mt->stale;
+    w.omega = mt->omega;
+    w.done = mt->done;
+    w.part = mt->part;
+    return w;
+}
+
+tgm_status_t prep_launch(const MitWork &w, tgm_graph_t g, int64_t first_event,
+                         const int32_t *nodes, const int32_t *n_nodes, int32_t cap, hipStream_t s)
+{
+    if (cap == 0)
+        return TGM_OK;
+    TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->N,
+               g->t, first_event, nodes, n_nodes, cap, w.nb, w.nbp, w.nset, w.ncnt);
+    return TGM_OK;
+}
+
+tgm_status_t blend_launch(const MitWork &w, tgm_graph_t g, int64_t first_event,
+                          const int32_t *nodes, const int32_t *n_nodes, int32_t cap, float *mem,
+                          const double *mem_ts, int32_t M, double p, float lambda, hipStream_t s)
+{
+    if (cap == 0)
+        return TGM_OK;
+    TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, g->t, first_event, mem_ts,
+               n_nodes, cap, p, w.gamma, w.stale, w.n_stale, w.done);
+    // at most n - ceil(p n) + 1 <= cap (1 - p) + 1 nodes are stale, each in
+    // at most ceil(cap / kMitChunk) items; a fixed grid strides over the items
+    const int64_t slots = std::min<int64_t>(cap, (int64_t)std::floor(cap * (1.0 - p)) + 1);
+    const dim3 grid((unsigned)std::min<int64_t>(slots * cdiv(cap, kMitChunk), kMitOmegaGrid));
+    if (w.nbp == 4)
+        TGM_LAUNCH(k_mit_omega<4>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
+                   first_event, mem_ts, w.nset, w.ncnt, w.gamma, w.stale, w.n_stale, w.part,
+                   w.done, w.K, lambda, mem, M, w.omega);
+    else if (w.nbp == 12)
+        TGM_LAUNCH(k_mit_omega<12>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
+                   first_event, mem_ts, w.nset, w.ncnt, w.gamma, w.stale, w.n_stale, w.part,
+                   w.done, w.K, lambda, mem, M, w.omega);
+    else
+        TGM_LAUNCH(k_mit_omega<64>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
+                   first_event, mem_ts, w.nset, w.ncnt, w.gamma, w.stale, w.n_stale, w.part,
+                   w.done, w.K, lambda, mem, M, w.omega);
+    return TGM_OK;
+}
+
+}  // namespace
+
 tgm_status_t tgm::mitigate_prep_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
                                        const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
                                        int32_t slot, hipStream_t s)
@@ -694,13 +769,7 @@ tgm_status_t tgm::mitigate_prep_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_
         return TGM_ERANGE;
     if (cap > mt->cap)
         return TGM_ESIZE;
-    if (cap == 0)
-        return TGM_OK;
-    const int64_t o = (int64_t)slot * mt->cap;
-    TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->N,
-               g->t, first_event, nodes, n_nodes, cap, mt->nb, mt->nbp, mt->nset + o * mt->nbp,
-               mt->ncnt + o);
-    return TGM_OK;
+    return prep_launch(work_of(mt, slot), g, first_event, nodes, n_nodes, cap, s);
 }
 
 tgm_status_t tgm::mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
@@ -717,29 +786,8 @@ tgm_status_t tgm::mitigate_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t fir
         return TGM_ERANGE;
     if (cap > mt->cap)
         return TGM_ESIZE;
-    if (cap == 0)
-        return TGM_OK;
-    const int64_t o = (int64_t)slot * mt->cap;
-    const int32_t *nset = mt->nset + o * mt->nbp, *ncnt = mt->ncnt + o;
-    TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, g->t, first_event, mem_ts,
-               n_nodes, cap, p, mt->gamma, mt->stale, mt->n_stale, mt->done);
-    // at most n - ceil(p n) + 1 <= cap (1 - p) + 1 nodes are stale, each in
-    // at most ceil(cap / kMitChunk) items; a fixed grid strides over the items
-    const int64_t slots = std::min<int64_t>(cap, (int64_t)std::floor(cap * (1.0 - p)) + 1);
-    const dim3 grid((unsigned)std::min<int64_t>(slots * cdiv(cap, kMitChunk), kMitOmegaGrid));
-    if (mt->nbp == 4)
-        TGM_LAUNCH(k_mit_omega<4>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
-                   first_event, mem_ts, nset, ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
-                   mt->done, mt->K, lambda, mem, M, mt->omega);
-    else if (mt->nbp == 12)
-        TGM_LAUNCH(k_mit_omega<12>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
-                   first_event, mem_ts, nset, ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
-                   mt->done, mt->K, lambda, mem, M, mt->omega);
-    else
-        TGM_LAUNCH(k_mit_omega<64>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
-                   first_event, mem_ts, nset, ncnt, mt->gamma, mt->stale, mt->n_stale, mt->part,
-                   mt->done, mt->K, lambda, mem, M, mt->omega);
-    return TGM_OK;
+    return blend_launch(work_of(mt, slot), g, first_event, nodes, n_nodes, cap, mem, mem_ts, M,
+                        p, lambda, s);
 }
 
 extern "C" tgm_status_t tgm_mitigate(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
@@ -756,6 +804,118 @@ extern "C" tgm_status_t tgm_mitigate(tgm_mitigator_t mt, tgm_graph_t g, int64_t 
                                              as_stream(stream)));
     return tgm::mitigate_launch(mt, g, first_event, nodes, n_nodes, cap, mem, mem_ts, M, p,
                                 lambda, 0, as_stream(stream));
+}
+
+// ------------------------------------------------- the allocation-free variant
+// tgm_mitigate_noalloc keeps its work space in this array.  Each GPU the
+// library runs on holds its own copy until the process ends.  Host code never
+// passes the array's name to a kernel or a copy (on the host it is a stand-in,
+// not a device address): it looks up each device's address once, with that
+// device current, and uses that.
+namespace {
+
+constexpr int32_t kNoallocMaxNodes = TGM_MITIGATE_NOALLOC_MAX_NODES;
+constexpr size_t kNoallocBytes = TGM_MITIGATE_NOALLOC_BYTES;
+constexpr int kMaxDevices = 64;
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The work space of one call, carved from the array in this order.
+size_t noalloc_layout(int32_t cap, int32_t nbp, int32_t K, char *base, MitWork *w)
+{
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        char *p = base ? base + o : nullptr;
+        o = align256(o + bytes);
+        return p;
+    };
+    const size_t c = (size_t)cap;
+    void *nset = take(sizeof(int32_t) * c * nbp);
+    void *ncnt = take(sizeof(int32_t) * c);
+    void *gamma = take(sizeof(double));
+    void *n_stale = take(sizeof(int32_t));
+    void *stale = take(sizeof(int32_t) * c);
+    void *omega = take(sizeof(int32_t) * c * K);
+    void *part = take(sizeof(int2) * kMitOmegaGrid * kMitMaxK);
+    void *done = take(sizeof(int32_t) * c);
+    if (w) {
+        w->nset = (int32_t *)nset;
+        w->ncnt = (int32_t *)ncnt;
+        w->gamma = (double *)gamma;
+        w->n_stale = (int32_t *)n_stale;
+        w->stale = (int32_t *)stale;
+        w->omega = (int32_t *)omega;
+        w->part = (int2 *)part;
+        w->done = (int32_t *)done;
+    }
+    return o;
+}
+
+}  // namespace
+
+static __device__ __align__(256) char scratch[TGM_MITIGATE_NOALLOC_BYTES];
+
+namespace {
+
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, looked up on the first call on
+// that device (hipGetSymbolAddress, with the device current) and kept.
+tgm_status_t static_scratch_ptr(char **out)
+{
+    int dev = -1;
+    TGM_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices)
+        return TGM_EDEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            record_error(e != hipSuccess ? e : hipErrorInvalidSymbol);
+            return TGM_EDEVICE;
+        }
+        g_scratch_ptr[dev] = (char *)p;
+    }
+    *out = g_scratch_ptr[dev];
+    return TGM_OK;
+}
+
+}  // namespace
+
+extern "C" tgm_status_t tgm_mitigate_noalloc(tgm_graph_t g, int64_t first_event,
+                                             const int32_t *nodes, const int32_t *n_nodes,
+                                             int32_t cap, float *mem, const double *mem_ts,
+                                             int32_t M, int32_t nb, int32_t K, double p,
+                                             float lambda, void *stream)
+{
+    if (!g || !nodes || !n_nodes || !mem || !mem_ts || M <= 0 || cap < 0)
+        return TGM_EINVAL;
+    if (nb < 1 || nb > 64 || K < 1 || K > kMitMaxK)
+        return TGM_EINVAL;
+    if (!(p >= 0.0 && p <= 1.0) || !(lambda >= 0.0f && lambda <= 1.0f))
+        return TGM_EINVAL;
+    if (first_event < 0 || first_event >= g->E)
+        return TGM_ERANGE;
+    if (cap > kNoallocMaxNodes)
+        return TGM_ESIZE;
+    MitWork w;
+    w.nb = nb;
+    w.nbp = nb <= 4 ? 4 : (nb <= 12 ? 12 : 64);
+    w.K = K;
+    if (noalloc_layout(cap, w.nbp, K, nullptr, nullptr) > kNoallocBytes)
+        return TGM_ESIZE;
+    if (cap == 0)
+        return TGM_OK;
+    char *base = nullptr;
+    TGM_TRY_STATUS(static_scratch_ptr(&base));
+    noalloc_layout(cap, w.nbp, K, base, &w);
+    // k_mit_select clears the per-stale-node counters k_mit_omega needs at
+    // zero; everything else is written before it is read within the call
+    hipStream_t s = as_stream(stream);
+    TGM_TRY_STATUS(prep_launch(w, g, first_event, nodes, n_nodes, cap, s));
+    return blend_launch(w, g, first_event, nodes, n_nodes, cap, mem, mem_ts, M, p, lambda, s);
 }
 
 extern "C" tgm_status_t tgm_mitigator_read(tgm_mitigator_t mt, double *gamma, int32_t *n_stale,

@@ -16,6 +16,8 @@ LIB_PATH = os.path.join(HERE, "libtgm.so")
 
 TGM_OK, TGM_EINVAL, TGM_ERANGE, TGM_EORDER, TGM_ESIZE, TGM_EDEVICE, TGM_ENOMEM = \
     0, -1, -2, -3, -4, -5, -6
+MAX_SAMPLE_SETS = 16                     # TGM_MAX_SAMPLE_SETS
+MITIGATE_NOALLOC_MAX_NODES = 32768       # TGM_MITIGATE_NOALLOC_MAX_NODES
 
 # Every exported symbol of include/tgm.h
 SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_alloc_count",
@@ -27,6 +29,7 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_alloc_
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
            "tgm_stage_run", "tgm_mitigator_create", "tgm_mitigator_destroy", "tgm_mitigate",
            "tgm_mitigator_read", "tgm_state_set_mitigation", "tgm_min_staleness",
+           "tgm_mitigate_noalloc",
            "tgm_embed_projection",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
@@ -113,6 +116,8 @@ def lib():
             "tgm_mitigator_create": [I32, I32, I32, C.POINTER(V)],
             "tgm_mitigator_destroy": [V],
             "tgm_mitigate": [V, V, I64, P, P, I32, P, P, I32, C.c_double, C.c_float, V],
+            "tgm_mitigate_noalloc": [V, I64, P, P, I32, P, P, I32, I32, I32, C.c_double,
+                                     C.c_float, V],
             "tgm_mitigator_read": [V, P, P, P, P, V],
             "tgm_state_set_mitigation": [V, V, C.c_double, C.c_float],
             "tgm_min_staleness": [P, I64, I32, P, P, P, P, P],
@@ -329,6 +334,13 @@ def tgm_mitigate(mt, g, first_event, nodes, n_nodes, cap, mem, mem_ts, M, p, lam
     _check("tgm_mitigate", lib().tgm_mitigate(mt, g, first_event, _p(nodes), _p(n_nodes), cap,
                                               _p(mem), _p(mem_ts), M, float(p), float(lam),
                                               _s(stream)))
+
+
+def tgm_mitigate_noalloc(g, first_event, nodes, n_nodes, cap, mem, mem_ts, M, nb, K, p, lam,
+                         stream=None):
+    _check("tgm_mitigate_noalloc", lib().tgm_mitigate_noalloc(
+        g, first_event, _p(nodes), _p(n_nodes), cap, _p(mem), _p(mem_ts), M, nb, K, float(p),
+        float(lam), _s(stream)))
 
 
 def tgm_mitigator_read(mt, gamma, n_stale, stale, omega, stream=None):

@@ -63,3 +63,20 @@ def test_null_handles_rejected_without_device(libtgm):
     assert L.tgm_graph_create(0, 0, None, None, None, None, None, 0, None, None) == tgm.TGM_EINVAL
     out = ctypes.c_void_p()
     assert L.tgm_state_create(10, 0, 4, 0, 5, None, ctypes.byref(out)) == tgm.TGM_EINVAL
+
+
+def test_binding_constants_match_the_header():
+    from paper_2402_15113_amd import tgm
+    text = open(HEADER).read()
+    defs = dict(re.findall(r"#define\s+(TGM_\w+)\s+\(?(-?\d+)", text))
+    assert int(defs["TGM_MAX_SAMPLE_SETS"]) == tgm.MAX_SAMPLE_SETS
+    assert int(defs["TGM_MITIGATE_NOALLOC_MAX_NODES"]) == tgm.MITIGATE_NOALLOC_MAX_NODES
+    for name in ("TGM_OK", "TGM_EINVAL", "TGM_ERANGE", "TGM_EORDER", "TGM_ESIZE", "TGM_EDEVICE",
+                 "TGM_ENOMEM"):
+        assert int(defs[name]) == getattr(tgm, name), name
+
+
+def test_alloc_count_without_device(libtgm):
+    from paper_2402_15113_amd import tgm
+    assert tgm.lib().tgm_alloc_count(None) == tgm.TGM_EINVAL
+    assert tgm.alloc_count() >= 0
