@@ -4,11 +4,18 @@
 One step = one batch through the whole stage (roots, most-recent-k sampling,
 node set, versioned fetch, GRU memory update + latest-message reduce + staged
 write-back, time-encoded attention embedding), with every input resident in
-HBM before the timed region starts.  Workload: the WIKI-shaped synthetic
-stream (9,227 nodes, 157,474 events, edge features 172, memory 100, time
-encoding 100, 2 heads, batch 600, 10 neighbours, staleness 1).  When the
-requested steps run past the stream's last batch, the next epoch starts from
-the initial memory state (a reset inside the timed region).
+HBM before the timed region starts.
+
+Default workload: the GDELT-shaped synthetic stream (16,682 nodes,
+191,290,882 events, edge features 186, memory 100, time encoding 100, 2
+heads, batch 4,000, 10 neighbours, staleness 4).  The graph holds every event
+and the device edge-feature table has a row for every event (142.3 GB of
+fp32).  The GPU first runs batches 0 .. first-1 from the initial state
+(untimed, default first = 20,000: an 80 M-event history); from that state
+(a checkpoint that restarts every pass) the window runs W warm-up batches
+and K timed batches.  Every feature row is filled from the generator.  `--workload wiki|reddit|lastfm|tiny`
+runs a whole small stream instead (the next epoch starts from the initial
+state when the steps run past its last batch).
 
 Passes:
   1. warm-up, then K timed steps bracketed by device synchronisation -> value;
@@ -21,7 +28,7 @@ Passes:
   3. an untimed replay that reads back each step's sizes (valid slots, node
      set, nodes with mail) -> algorithmic flops and bytes per launch;
   4. the fp64 oracle on the host cores for a bounded sample of the same
-     batches -> cpu_baseline.
+     workload (one thread, then every core) -> cpu_baseline.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -71,6 +78,8 @@ class Schedule:
         from paper_2402_15113_amd import tgm
         if self.init is None:
             tgm.tgm_state_reset(self.stage.st, stream=self.stage.stream)
+        elif "checkpoint" in self.init:
+            self.stage.restore_checkpoint(self.init["checkpoint"])
         else:
             self.stage.load_state(self.first, **self.init)
 
@@ -126,55 +135,110 @@ def account(sched, W, K):
     return rows, seq
 
 
-def window_setup(name, first, L, w, mitigation=None, s=None):
-    """Stage for batches first .. first + L - 1 of a large stream: the graph of
-    every event up to the window's end, a device feature table that holds the
-    generator's rows from the oldest event the window samples onwards (zero
-    below: never read), and a seeded synthetic memory state at `first`."""
-    import dataclasses
-    from concurrent.futures import ThreadPoolExecutor
-
+def synthetic_state(wl, first, t0, seed=11):
+    """A seeded memory state standing in for the one batch `first` would see:
+    memory U(-1, 1), mail N(0, 1), memory times before t0, mail times after
+    them, 90% of the nodes with mail."""
     import numpy as np
+    r = np.random.default_rng(seed)
+    N, M, D_m = wl.N, wl.M, wl.D_m
+    mem_ts = np.floor(r.uniform(0, t0, N))
+    return dict(mem=r.uniform(-1, 1, (N, M)), mem_ts=mem_ts, mail=r.standard_normal((N, D_m)),
+                mail_ts=np.minimum(mem_ts + np.floor(r.exponential(3600, N)), t0),
+                ver=np.where(r.random(N) < 0.9, r.integers(0, first - 2, N), -1))
+
+
+def oldest_sampled_row(stage, wl, first, L):
+    """The oldest event any root of batches first .. first + L - 1 samples."""
     import torch
     from paper_2402_15113_amd import tgm
-    from paper_2402_15113_amd.stage import Stage
-    from workloads import CONFIGS, FEAT_CHUNK, edge_feature_rows, make_workload
-
-    full = make_workload(name, with_features=False, s=s)
-    E_end = min(full.E, (first + L) * full.B)
-    wl = dataclasses.replace(full, src=full.src[:E_end], dst=full.dst[:E_end],
-                             t=full.t[:E_end], neg=full.neg[:E_end])
-    efeat = torch.zeros((E_end, wl.D_e), dtype=torch.float32, device="cuda")
-    stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
-                  nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation)
     lo_row = first * wl.B
-    for i in range(first, first + L):   # the oldest event any window batch samples
+    for i in range(first, first + L):
         a, b = wl.batch(i)
         tgm.tgm_sample_batch(stage.g, a, b - a, wl.nb, stage.root, stage.root_ts, stage.nbr,
                              stage.eid, stage.nts, stage.cnt, stream=stage.stream)
         e = stage.eid[:3 * (b - a)]
-        lo_row = min(lo_row, int(torch.where(e >= 0, e, E_end).min().item()))
-    E_full = CONFIGS[name]["E"]
+        lo_row = min(lo_row, int(torch.where(e >= 0, e, wl.E).min().item()))
+    return lo_row
+
+
+def fill_features(efeat, wl, lo, hi, threads):
+    """Rows [lo, hi) of the device table from the generator, chunk by chunk
+    (generated on host threads, copied in order)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import torch
+    from workloads import CONFIGS, FEAT_CHUNK, edge_feature_rows
+    E_full = CONFIGS[wl.name]["E"]
 
     def rows(c):
-        a = max(lo_row, c * FEAT_CHUNK)
-        b = min(E_end, (c + 1) * FEAT_CHUNK)
+        a = max(lo, c * FEAT_CHUNK)
+        b = min(hi, (c + 1) * FEAT_CHUNK)
         return a, edge_feature_rows(wl.seed, E_full, wl.D_e, a, b)
 
-    with ThreadPoolExecutor(8) as ex:
-        for a, blk in ex.map(rows, range(lo_row // FEAT_CHUNK, (E_end - 1) // FEAT_CHUNK + 1)):
-            efeat[a:a + len(blk)] = torch.from_numpy(blk).to("cuda")
+    t0 = last = time.perf_counter()
+    chunks = range(lo // FEAT_CHUNK, (hi - 1) // FEAT_CHUNK + 1) if hi > lo else range(0)
+    with ThreadPoolExecutor(threads) as ex:
+        for a, blk in ex.map(rows, chunks):
+            efeat[a:a + len(blk)].copy_(torch.from_numpy(blk))
+            if time.perf_counter() - last > 15:
+                last = time.perf_counter()
+                log(f"  feature rows filled through {a + len(blk):,} of [{lo:,}, {hi:,})")
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0
+
+
+def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu"):
+    """Stage over the whole stream of a large workload for the window of
+    batches first .. first + L - 1.
+
+    The graph holds every event of the stream, and the device edge-feature
+    table has a row for every event (E x D_e fp32, 142 GB for the GDELT-shaped
+    stream).  Rows a run can read are filled from the generator; the rest are
+    never read (sampling is strictly earlier and no batch after the window
+    runs) and stay unwritten.  The memory state at `first`:
+      state="gpu"        the GPU runs batches 0 .. first - 1 from the initial
+                         state (untimed); its checkpoint restarts every pass;
+                         every row is filled;
+      state="synthetic"  a seeded synthetic state; rows from the oldest event
+                         the window samples to its end are filled."""
+    import torch
+    from paper_2402_15113_amd.stage import Stage
+    from workloads import make_workload
+
+    tg = time.perf_counter()
+    wl = make_workload(name, with_features=False, s=s)
+    log(f"stream of {wl.E:,} events generated in {time.perf_counter() - tg:.1f} s")
+    E_end = min(wl.E, (first + L) * wl.B)
+    efeat = torch.empty((wl.E, wl.D_e), dtype=torch.float32, device="cuda")
+    stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
+                  nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation)
     stage._efeat_keep = efeat
-    r = np.random.default_rng(11)
-    N, M, D_m = wl.N, wl.M, wl.D_m
-    t0 = wl.t[lo_row - 1] if lo_row > 0 else 0.0
-    mem_ts = np.floor(r.uniform(0, t0, N))
-    init = dict(mem=r.uniform(-1, 1, (N, M)), mem_ts=mem_ts, mail=r.standard_normal((N, D_m)),
-                mail_ts=np.minimum(mem_ts + np.floor(r.exponential(3600, N)), t0),
-                ver=np.where(r.random(N) < 0.9, r.integers(0, first - 2, N), -1))
-    log(f"window: batches {first}..{first + L - 1}, graph of {E_end} events, feature rows "
-        f"[{lo_row}, {E_end}) filled ({(E_end - lo_row) * wl.D_e * 4 / 1e9:.2f} GB)")
-    return wl, stage, init
+    if state == "gpu":
+        lo_row, hi_row = 0, wl.E
+    else:
+        lo_row, hi_row = oldest_sampled_row(stage, wl, first, L), E_end
+    threads = max(1, min(16, os.cpu_count() or 1))
+    t_fill = fill_features(efeat, wl, lo_row, hi_row, threads)
+    log(f"feature rows [{lo_row:,}, {hi_row:,}) of {wl.E:,} filled "
+        f"({(hi_row - lo_row) * wl.D_e * 4 / 1e9:.1f} GB of {wl.E * wl.D_e * 4 / 1e9:.1f} GB) "
+        f"in {t_fill:.1f} s ({threads} threads)")
+    meta = {"edge_table": {"rows": wl.E, "bytes": wl.E * wl.D_e * 4, "resident": "HBM",
+                           "rows_filled": [lo_row, hi_row]}}
+    if hi_row - lo_row < wl.E:
+        meta["edge_table"]["rows_not_filled"] = "never read by the batches that run"
+    if state == "gpu":
+        tp = time.perf_counter()
+        stage.want_winner = False
+        stage.run(0, first)
+        torch.cuda.synchronize()
+        init = {"checkpoint": stage.save_checkpoint()}
+        log(f"state: GPU ran batches 0..{first - 1} in {time.perf_counter() - tp:.1f} s")
+        meta["state"] = f"GPU run of batches 0..{first - 1} from the initial state"
+    else:
+        init = synthetic_state(wl, first, wl.t[lo_row - 1] if lo_row > 0 else 0.0)
+        meta["state"] = f"seeded synthetic memory state at batch {first}"
+    return wl, stage, init, meta
 
 
 def work_model(wl, rows, model="tgn"):
@@ -296,29 +360,116 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
         print(f"| {k} | {n} | {fk:.1f} | {wk:.1f} | {hbm / 1e6:.3f} |")
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_timed(make, seconds, max_batches, threads):
+    """Runs the oracle made by make() (construction untimed) batch by batch
+    for up to `seconds` (at least one batch, at most max_batches) with
+    `threads` OpenMP threads; returns (events/s, threads used, batches,
+    events, seconds)."""
+    import oracle
+    used = oracle.set_threads(threads)
+    o = make()
+    events, nb, t0 = 0, 0, time.perf_counter()
+    while nb < max_batches and (nb == 0 or time.perf_counter() - t0 < seconds):
+        r = o.step(want="all")
+        if r is None:
+            break
+        events += r.b
+        nb += 1
+    dt = time.perf_counter() - t0
+    return events / dt, used, nb, events, dt
+
+
 def cpu_baseline(wl, w, W, seconds):
+    """The fp64 oracle over the same stream from batch W on (the state it
+    reaches after W batches is built untimed): single-threaded (the primary
+    figure), then on every host core."""
     import oracle
     oracle.build(force=False)
-    o = oracle.Oracle(wl, w)
-    for _ in range(W):                       # state before the timed batches
-        if o.step(want="light") is None:
-            break
-    events, t0, nb_done, epochs = 0, time.perf_counter(), 0, 0
-    first = o.next_iter
-    while time.perf_counter() - t0 < seconds:
-        r = o.step(want="all")
-        if r is None:                        # next epoch from the initial state
-            o = oracle.Oracle(wl, w)
-            epochs += 1
-            continue
-        events += r.b
-        nb_done += 1
-    dt = time.perf_counter() - t0
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": events / dt, "unit": "events/s", "cores": threads, "kind": "oracle",
-            "sample": f"fp64 oracle on the same stream: {nb_done} batches from batch {first} "
-                      f"({epochs} epoch restarts), {events} events in {dt:.1f} s, "
-                      f"OpenMP over nodes/roots"}
+
+    def make():
+        o = oracle.Oracle(wl, w)
+        for _ in range(W):
+            o.step(want="light")
+        return o
+
+    all_threads = oracle.set_threads(0)
+    v1, c1, n1, e1, t1 = oracle_timed(make, 0.6 * seconds, wl.n_iters - W, 1)
+    va, ca, na, ea, ta = oracle_timed(make, 0.4 * seconds, wl.n_iters - W, all_threads)
+    return {"value": v1, "unit": "events/s", "cores": c1, "kind": "oracle",
+            "sample": f"fp64 oracle on the same stream: batches {W}..{W + n1 - 1} ({e1} events) "
+                      f"in {t1:.1f} s on one thread",
+            "all_cores": {"value": va, "cores": ca,
+                          "sample": f"batches {W}..{W + na - 1} ({ea} events) in {ta:.1f} s"},
+            "cpu_model": cpu_model()}
+
+
+def cpu_baseline_window(wl, w, first, seconds, mitigation=None):
+    """The fp64 oracle on a bounded sample of the same window: batches first,
+    first + 1, ... from the seeded synthetic state at `first` (the oracle takes
+    no input from the GPU), on the graph of the events through the sample's
+    end, with the feature rows those batches read; single-threaded (the
+    primary figure), then on every host core."""
+    import dataclasses
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import oracle
+    from workloads import CONFIGS, FEAT_CHUNK, edge_feature_rows
+    oracle.build(force=False)
+    nmax = 24
+    E_end = min(wl.E, (first + nmax) * wl.B)
+    pre = dataclasses.replace(wl, src=wl.src[:E_end], dst=wl.dst[:E_end], t=wl.t[:E_end],
+                              neg=wl.neg[:E_end])
+    roots, rts = [], []
+    for i in range(first, first + nmax):
+        a, b = pre.batch(i)
+        roots += [pre.src[a:b], pre.dst[a:b], pre.neg[a:b]]
+        rts += [pre.t[a:b]] * 3
+    _, eid, _, _ = oracle.sample(pre.N, pre.src, pre.dst, pre.t, np.concatenate(roots),
+                                 np.concatenate(rts), pre.nb)
+    lo = first * pre.B
+    rows = np.unique(np.concatenate([eid[eid >= 0].ravel().astype(np.int64),
+                                     np.arange(lo, E_end, dtype=np.int64)]))
+    host = np.zeros((E_end, pre.D_e), dtype=np.float32)   # untouched pages stay unallocated
+    E_full = CONFIGS[pre.name]["E"]
+
+    def fill(c):
+        a = int(c) * FEAT_CHUNK
+        b = min(a + FEAT_CHUNK, E_end)
+        sel = rows[(rows >= a) & (rows < b)]
+        host[sel] = edge_feature_rows(pre.seed, E_full, pre.D_e, a, b)[sel - a]
+
+    with ThreadPoolExecutor(8) as ex:
+        list(ex.map(fill, np.unique(rows // FEAT_CHUNK)))
+    pre = dataclasses.replace(pre, efeat=host)
+    lo_row = int(rows.min())
+    init = synthetic_state(pre, first, pre.t[lo_row - 1] if lo_row > 0 else 0.0)
+
+    def make():
+        o = oracle.Oracle(pre, w, mitigation=mitigation)
+        o.set_state(first, **init)
+        return o
+
+    all_threads = oracle.set_threads(0)
+    v1, c1, n1, e1, t1 = oracle_timed(make, 0.6 * seconds, 2, 1)
+    va, ca, na, ea, ta = oracle_timed(make, 0.4 * seconds, nmax, all_threads)
+    return {"value": v1, "unit": "events/s", "cores": c1, "kind": "oracle",
+            "sample": f"fp64 oracle, batches {first}..{first + n1 - 1} ({e1} events) of the same "
+                      f"stream from a seeded synthetic state, in {t1:.1f} s on one thread",
+            "all_cores": {"value": va, "cores": ca,
+                          "sample": f"batches {first}..{first + na - 1} ({ea} events) in "
+                                    f"{ta:.1f} s"},
+            "cpu_model": cpu_model()}
 
 
 def main():
@@ -326,10 +477,15 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="wiki",
-                    help="wiki (default), tiny, reddit, lastfm; gdelt runs a window of batches "
-                         "starting at --first from a synthetic state")
-    ap.add_argument("--first", type=int, default=20_000, help="first batch of a gdelt window")
+    ap.add_argument("--workload", default="gdelt",
+                    help="gdelt (default: the GDELT-shaped stream, 191,290,882 events, a window "
+                         "of batches from --first on), or a whole small stream: wiki, reddit, "
+                         "lastfm, tiny")
+    ap.add_argument("--first", type=int, default=20_000,
+                    help="gdelt: the batch the window starts at (warm-up steps first)")
+    ap.add_argument("--state", default="gpu", choices=("gpu", "synthetic"),
+                    help="gdelt: the memory state at --first: the GPU's own run of batches "
+                         "0..first-1 (default), or a seeded synthetic state (counter passes)")
     ap.add_argument("--model", default="tgn", choices=("tgn", "jodie"),
                     help="model family: tgn (GRU memory, attention; default) or jodie (RNN "
                          "memory, time projection)")
@@ -378,8 +534,10 @@ def main():
             from workloads import CONFIGS
             c = CONFIGS["gdelt"]
             w = make_weights(c["M"], c["D_e"], c["D_t"], model=args.model)
-            wl, stage, init = window_setup("gdelt", args.first, W + K, w, mit, s=s)
+            wl, stage, init, wmeta = window_setup("gdelt", args.first, W + K, w, mit, s=s,
+                                                  state=args.state)
             sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
+            sched.meta = wmeta
         else:
             wl = make_workload(args.workload, s=s)
             w = make_weights(wl.M, wl.D_e, wl.D_t, model=args.model)
@@ -502,11 +660,18 @@ def main():
     stage.close()
 
     if window:
-        out["config"]["window"] = f"batches {args.first}..{args.first + W + K - 1} from a seeded " \
-                                  "synthetic memory state"
-    if not args.no_cpu_baseline and not window:
+        out["config"]["window"] = {
+            "batches": [args.first, args.first + W + K - 1],
+            "timed_batches": [args.first + W, args.first + W + K - 1],
+            "state_at_first": sched.meta["state"]}
+        out["config"]["edge_table"] = sched.meta["edge_table"]
+    if not args.no_cpu_baseline:
         log(f"oracle baseline ({args.cpu_seconds:.0f} s budget)")
-        out["cpu_baseline"] = cpu_baseline(wl, w, W, args.cpu_seconds)
+        if window:
+            out["cpu_baseline"] = cpu_baseline_window(wl, w, args.first + W, args.cpu_seconds,
+                                                      mit)
+        else:
+            out["cpu_baseline"] = cpu_baseline(wl, w, W, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

@@ -316,8 +316,9 @@ tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int32_t *root_
  * Pipelined executor.  Runs iterations i0 .. i0+n-1 of the stage (the batch of
  * iteration i is events [iB, min(E, (i+1)B))).  The sample and node set of an
  * iteration depend on the event stream only (Sec. 3.1: MSPipe prefetches
- * them), so they run a chunk of nsb/2 iterations ahead on prefetch_stream,
- * into sample buffer set (i - i0) % nsb; the fetch, update and embedding of
+ * them), so they run ahead on prefetch_stream in chunks of 1, 2, 4, ... and
+ * then nsb/2 iterations (each chunk sampled while the one before it is
+ * computed), into sample buffer set (i - i0) % nsb; the fetch, update and embedding of
  * each iteration run in order on `stream` with one set of fetch buffers, in
  * three launches per iteration (the staging of a write set shares a launch
  * with the node projections, and the attention with the next fetch's

@@ -99,8 +99,16 @@ def lib():
         L.orc_time_projection.argtypes = [C.c_int, _f64p, _f64p, C.c_double, C.c_double, _f64p]
         L.orc_quantile_nearest_rank.argtypes = [C.c_int, _f64p, C.c_double]
         L.orc_quantile_nearest_rank.restype = C.c_double
+        L.orc_set_threads.argtypes = [C.c_int]
+        L.orc_set_threads.restype = C.c_int
         _lib = L
     return _lib
+
+
+def set_threads(n: int = 0) -> int:
+    """Threads of the oracle's OpenMP loops (n < 1: unchanged); returns the
+    count in use."""
+    return int(lib().orc_set_threads(int(n)))
 
 
 def _p(a, typ):

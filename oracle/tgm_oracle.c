@@ -44,6 +44,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
@@ -1031,4 +1034,19 @@ int orc_step(void *p, orc_step_out *o)
     free(win);
     c->next_iter = i + 1;
     return ORC_OK;
+}
+
+/* Thread count of the OpenMP loops (over independent nodes and roots; every
+ * sum has a fixed order, so results do not depend on it).  n < 1 leaves it
+ * unchanged.  Returns the count the next loops will use. */
+int orc_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
 }

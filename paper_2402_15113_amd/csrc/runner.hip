@@ -9,7 +9,6 @@
 // streams synchronise once per chunk, not once per iteration.
 #include <hip/hip_runtime.h>
 
-#include <vector>
 
 #include "common.h"
 
@@ -38,8 +37,22 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
         return TGM_EINVAL;
     // events 0-1: sampled chunk by parity, 2-3: computed chunk by parity, 4: start
     hipEvent_t *const ev = st->run_ev;
-    const int64_t K = nsb / 2;   // iterations per chunk
-    const int64_t nch = (n + K - 1) / K;
+    // Chunks of iterations: 1, 2, 4, ... then K = nsb / 2 each, so the main
+    // stream waits only for the first iteration's sample before it starts,
+    // and each chunk is sampled while the one before it is computed.  A chunk
+    // and the next hold at most nsb iterations together, so the sample sets a
+    // chunk fills were last read by chunks already computed.
+    const int64_t K = nsb / 2;
+    int64_t r = 0;   // ramp chunks: sizes 2^c < K
+    while ((int64_t(1) << r) < K)
+        ++r;
+    auto chunk_lo = [&](int64_t c) {
+        const int64_t lo = c <= r ? (int64_t(1) << c) - 1 : ((int64_t(1) << r) - 1) + (c - r) * K;
+        return std::min(lo, n);
+    };
+    int64_t nch = 0;
+    while (chunk_lo(nch) < n)
+        ++nch;
     auto batch = [&](int64_t k, int64_t *lo) {   // the k-th iteration of the run
         *lo = (i0 + k) * B;
         return (int32_t)std::min<int64_t>(B, g->E - *lo);
@@ -48,10 +61,10 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     // the sample, into mitigator slot 1 + (k % nsb); the latest-message reduce
     // of each batch also runs beside its sample, into key array k % nsb (so
     // the update's GRU launch skips it)
-    std::vector<uint64_t *> xwin(nsb, nullptr);
-    std::vector<uint64_t> xtag(nsb, 0);
+    uint64_t *xwin[TGM_MAX_SAMPLE_SETS] = {};
+    uint64_t xtag[TGM_MAX_SAMPLE_SETS] = {};
     auto sample_chunk = [&](int64_t c) -> tgm_status_t {
-        for (int64_t k = c * K; k < std::min(n, (c + 1) * K); ++k) {
+        for (int64_t k = chunk_lo(c); k < chunk_lo(c + 1); ++k) {
             int64_t lo = 0;
             const int32_t b = batch(k, &lo);
             const tgm_sample_buffers &s = sb[k % nsb];
@@ -85,8 +98,8 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
                 TGM_HIP(hipStreamWaitEvent(pre, ev[2 + ((c - 1) & 1)], 0));
             TGM_TRY_STATUS(sample_chunk(c + 1));
         }
-        const int64_t kend = std::min(n, (c + 1) * K);
-        for (int64_t k = c * K; k < kend; ++k) {
+        const int64_t kend = chunk_lo(c + 1);
+        for (int64_t k = chunk_lo(c); k < kend; ++k) {
             int64_t lo = 0;
             const int32_t b = batch(k, &lo);
             const bool more = k + 1 < n;

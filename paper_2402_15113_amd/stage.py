@@ -25,7 +25,7 @@ from . import tgm
 # the last iteration)
 _SAMPLE_BUFFERS = ("root", "root_ts", "nbr", "eid", "nts", "cnt", "nodes", "n_nodes", "root_pos",
                    "nbr_pos")
-_SETS = 16   # sample buffer sets of the pipelined executor: chunks of 8 iterations
+_SETS = 16   # sample buffer sets of the pipelined executor: chunks of up to 8 iterations
 
 
 class _Sample:
