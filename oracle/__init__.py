@@ -63,7 +63,13 @@ class _StepOut(C.Structure):
                 ("f_mail_ts", _f64p), ("f_ver", _i32p), ("s_new", _f64p),
                 ("new_mem_ts", _f64p), ("h", _f64p), ("winner", _i64p),
                 ("m_mem", _f64p), ("m_stale", _i32p), ("m_omega", _i32p), ("m_gamma", C.c_double),
-                ("m_n_stale", C.c_int32), ("m_pad", C.c_int32), ("x_mem", _f64p)]
+                ("m_n_stale", C.c_int32), ("m_pad", C.c_int32), ("x_mem", _f64p),
+                ("loss", C.c_double), ("grad", _f64p), ("params", _f64p)]
+
+OPTIMIZERS = {"sgd": 0, "adam": 1}
+# the parameter vector's tensors, in order (orc_param_sizes)
+PARAM_NAMES = ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v", "W_o",
+               "b_o", "W_src", "W_dst", "b_p", "w_out", "b_out")
 
 
 def lib():
@@ -99,6 +105,13 @@ def lib():
         L.orc_time_projection.argtypes = [C.c_int, _f64p, _f64p, C.c_double, C.c_double, _f64p]
         L.orc_quantile_nearest_rank.argtypes = [C.c_int, _f64p, C.c_double]
         L.orc_quantile_nearest_rank.restype = C.c_double
+        L.orc_set_training.argtypes = [C.c_void_p, C.c_int, C.c_double, C.c_double, C.c_double,
+                                       C.c_double, _f32p, _f32p, _f32p, _f32p, C.c_float]
+        L.orc_set_training.restype = C.c_int
+        L.orc_param_count.argtypes = [C.c_void_p]
+        L.orc_param_count.restype = C.c_int64
+        L.orc_param_sizes.argtypes = [C.c_void_p, _i64p]
+        L.orc_get_params.argtypes = [C.c_void_p, _f64p]
         L.orc_set_threads.argtypes = [C.c_int]
         L.orc_set_threads.restype = C.c_int
         _lib = L
@@ -245,14 +258,24 @@ class StepResult:
     # the exact memories of U: committed state plus every write set of
     # iterations <= i-1 (what a fetch without staleness would read here)
     x_mem: np.ndarray | None = None
+    # training (None when off): the loss, the gradient of the parameter
+    # vector and the parameters after the optimizer step
+    loss: float | None = None
+    grad: np.ndarray | None = None
+    params: np.ndarray | None = None
 
 
 class Oracle:
     """Runs the stage iteration by iteration on a workload (``workloads.Workload``)."""
 
-    def __init__(self, wl, w, s: int | None = None, mitigation: dict | None = None):
+    def __init__(self, wl, w, s: int | None = None, mitigation: dict | None = None,
+                 training: dict | None = None):
         """``mitigation=dict(p=.., lam=.., K=..)`` enables the MSPipe-S step
-        (Sec. 3.3) between the fetch and the memory update."""
+        (Sec. 3.3) between the fetch and the memory update.
+        ``training=dict(predictor=P, opt="sgd"|"adam", lr=.., beta1=..,
+        beta2=.., eps=..)`` adds the training step (link-prediction loss,
+        gradient, optimizer) after each iteration; P a
+        ``workloads.Predictor``."""
         self.wl = wl
         self.mitigation = mitigation
         self.s = wl.s if s is None else s
@@ -291,6 +314,19 @@ class Oracle:
                                           int(mitigation["K"]))
             if rc != 0:
                 raise ValueError("oracle: invalid mitigation parameters")
+        self.training = training
+        self.n_params = 0
+        if training is not None:
+            P = training["predictor"]
+            pw = [keep(getattr(P, k), np.float32) for k in ("W_src", "W_dst", "b_p", "w_out")]
+            rc = lib().orc_set_training(
+                h, OPTIMIZERS[training.get("opt", "adam")], float(training.get("lr", 1e-4)),
+                float(training.get("beta1", 0.9)), float(training.get("beta2", 0.999)),
+                float(training.get("eps", 1e-8)), *(_p(a, _f32p) for a in pw),
+                float(P.b_out))
+            if rc != 0:
+                raise ValueError("oracle: invalid training parameters")
+            self.n_params = int(lib().orc_param_count(h))
 
     def __del__(self):
         h = getattr(self, "_h", None)
@@ -321,6 +357,8 @@ class Oracle:
             K = int(mit["K"])
             arrs.update(m_mem=np.empty(N * M), m_stale=np.empty(N, np.int32),
                         m_omega=np.empty(N * K, np.int32))
+        if self.n_params:
+            arrs.update(grad=np.empty(self.n_params), params=np.empty(self.n_params))
         for k, fld in _StepOut._fields_:
             if k in arrs:
                 setattr(o, k, _p(arrs[k], fld))
@@ -344,10 +382,31 @@ class Oracle:
             m_omega=(arrs["m_omega"][:o.m_n_stale * int(mit["K"])].reshape(-1, int(mit["K"]))
                      if mit is not None else None),
             m_gamma=o.m_gamma if mit is not None else None,
-            x_mem=g("x_mem", nU * M, (nU, M)))
+            x_mem=g("x_mem", nU * M, (nU, M)),
+            loss=o.loss if self.n_params else None,
+            grad=arrs["grad"] if self.n_params else None,
+            params=arrs["params"] if self.n_params else None)
 
     def flush(self):
         lib().orc_flush(self._h)
+
+    def param_sizes(self) -> list:
+        sz = np.zeros(len(PARAM_NAMES), np.int64)
+        lib().orc_param_sizes(self._h, _p(sz, _i64p))
+        return [int(x) for x in sz]
+
+    def split(self, vec) -> dict:
+        """The tensors of a parameter vector, by name (flat)."""
+        out, o = {}, 0
+        for name, n in zip(PARAM_NAMES, self.param_sizes()):
+            out[name] = vec[o:o + n]
+            o += n
+        return out
+
+    def params(self) -> np.ndarray:
+        out = np.empty(self.n_params)
+        lib().orc_get_params(self._h, _p(out, _f64p))
+        return out
 
     def state(self):
         N, M, D_m = self.N, self.M, self.D_m

@@ -549,6 +549,15 @@ typedef struct {
     /* model family and JODIE's projection vector */
     int kind;
     double *w_t;
+    /* training (off unless orc_set_training enables it): every trained
+     * parameter in one vector theta (the weights above point into it), the
+     * link predictor's weights, the gradient of the last step, the optimizer's
+     * moments and step count */
+    int train_on, opt;
+    double lr, beta1, beta2, eps;
+    int64_t n_params, opt_steps;
+    double *theta, *grad, *m1, *m2;
+    double *W_src, *W_dst, *b_p, *w_out, *b_out;
 } orc_ctx;
 
 typedef struct {
@@ -594,6 +603,11 @@ typedef struct {
      * would read at this point of the run (for the staleness error of Sec. 5.5
      * and App. E.2) */
     double *x_mem;
+    /* training: the loss of the iteration, the gradient of every parameter
+     * [n_params] and the parameters after the optimizer step [n_params], in
+     * the order of orc_param_layout */
+    double loss;
+    double *grad, *params;
 } orc_step_out;
 
 static double *widen(const float *x, size_t n)
@@ -671,9 +685,14 @@ void orc_destroy(void *p)
     orc_ctx *c = (orc_ctx *)p;
     if (!c)
         return;
-    free(c->W_ih); free(c->W_hh); free(c->b_ih); free(c->b_hh); free(c->omega); free(c->beta);
-    free(c->W_q); free(c->b_q); free(c->W_k); free(c->b_k); free(c->W_v); free(c->b_v);
-    free(c->W_o); free(c->b_o); free(c->w_t);
+    if (c->train_on) {   /* the weights live in theta */
+        free(c->theta); free(c->grad); free(c->m1); free(c->m2);
+    } else {
+        free(c->W_ih); free(c->W_hh); free(c->b_ih); free(c->b_hh);
+        free(c->W_q); free(c->b_q); free(c->W_k); free(c->b_k); free(c->W_v); free(c->b_v);
+        free(c->W_o); free(c->b_o);
+    }
+    free(c->omega); free(c->beta); free(c->w_t);
     free_adj(&c->adj);
     free(c->mem); free(c->mem_ts); free(c->mail); free(c->mail_ts); free(c->ver);
     for (int k = 0; k < c->nq; ++k)
@@ -791,6 +810,413 @@ int orc_set_mitigation(void *p, int on, double pq, double lambda, int K)
     c->mit_lambda = lambda;
     c->mit_K = K;
     return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Training (the step after the stage: loss, gradient, optimizer).
+ *
+ * The training samples of an iteration are its b positive pairs (src, dst)
+ * and b negative pairs (src, neg) (Sec. 5, training settings: equal numbers of
+ * positive and negative pairs, link prediction).  Link predictor, a two-layer
+ * perceptron over the two endpoint embeddings (reading R28):
+ *   z = W_src h_u + W_dst h_v + b_p,   score(u, v) = w_out . ReLU(z) + b_out
+ * Loss, binary cross-entropy with the scores as logits (reading R29):
+ *   L = (1/b) sum_e [ softplus(-score(src_e, dst_e)) + softplus(score(src_e, neg_e)) ]
+ * The gradient flows through h into the attention's weights and the updated
+ * memories s', and through s' into the memory updater's weights for the
+ * nodes that hold mail.  The fetched memories and mails are inputs of the
+ * iteration, and the time encoding's omega and beta are not trained (reading
+ * R30).  The optimizer takes one step per iteration after the write set is
+ * staged (reading R31): SGD, theta -= lr g (the update of the convergence
+ * analysis of Sec. 4), or Adam with bias correction (the optimizer of the
+ * training settings, with its learning rate).
+ *
+ * Parameter vector order (orc_param_sizes): W_ih [3M x D_x], W_hh [3M x M],
+ * b_ih [3M], b_hh [3M], W_q [M x (M + D_t)], b_q [M], W_k [M x D_kv], b_k [M],
+ * W_v [M x D_kv], b_v [M], W_o [M x 2M], b_o [M], W_src [M x M], W_dst [M x M],
+ * b_p [M], w_out [M], b_out [1]; D_kv = M + D_e + D_t. */
+#define ORC_NPT 17
+#define ORC_SGD 0
+#define ORC_ADAM 1
+
+static void param_sizes(const orc_ctx *c, int64_t *sz)
+{
+    const int64_t M = c->M, D_x = c->D_x, D_q = c->M + c->D_t, D_kv = c->M + c->D_e + c->D_t;
+    const int64_t v[ORC_NPT] = {3 * M * D_x, 3 * M * M, 3 * M, 3 * M, M * D_q, M, M * D_kv, M,
+                                M * D_kv, M, M * 2 * M, M, M * M, M * M, M, M, 1};
+    memcpy(sz, v, sizeof(v));
+}
+
+/* views[k] = the k-th parameter tensor inside a vector of the layout above */
+static void param_views(const orc_ctx *c, double *base, double **views)
+{
+    int64_t sz[ORC_NPT];
+    param_sizes(c, sz);
+    for (int k = 0; k < ORC_NPT; ++k) {
+        views[k] = base;
+        base += sz[k];
+    }
+}
+
+void orc_param_sizes(void *p, int64_t *sizes)
+{
+    param_sizes((const orc_ctx *)p, sizes);
+}
+
+static double softplus(double x) { return x > 0.0 ? x + log1p(exp(-x)) : log1p(exp(x)); }
+
+/* Turns training on (TGN models): the predictor's weights (fp32, widened),
+ * the optimizer (ORC_SGD or ORC_ADAM) and its constants.  Returns 0, or -1. */
+int orc_set_training(void *p, int opt, double lr, double beta1, double beta2, double eps,
+                     const float *W_src, const float *W_dst, const float *b_p,
+                     const float *w_out, float b_out)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (c->kind != ORC_TGN || c->train_on || (opt != ORC_SGD && opt != ORC_ADAM) ||
+        !(lr >= 0.0) || !W_src || !W_dst || !b_p || !w_out)
+        return ORC_EINVAL;
+    int64_t sz[ORC_NPT], n = 0;
+    param_sizes(c, sz);
+    for (int k = 0; k < ORC_NPT; ++k)
+        n += sz[k];
+    c->n_params = n;
+    c->theta = (double *)malloc(sizeof(double) * (size_t)n);
+    c->grad = (double *)calloc((size_t)n, sizeof(double));
+    c->m1 = (double *)calloc((size_t)n, sizeof(double));
+    c->m2 = (double *)calloc((size_t)n, sizeof(double));
+    double *v[ORC_NPT];
+    param_views(c, c->theta, v);
+    double *old[12] = {c->W_ih, c->W_hh, c->b_ih, c->b_hh, c->W_q, c->b_q,
+                       c->W_k, c->b_k, c->W_v, c->b_v, c->W_o, c->b_o};
+    for (int k = 0; k < 12; ++k) {
+        memcpy(v[k], old[k], sizeof(double) * (size_t)sz[k]);
+        free(old[k]);
+    }
+    const int M = c->M;
+    for (int64_t k = 0; k < (int64_t)M * M; ++k) {
+        v[12][k] = W_src[k];
+        v[13][k] = W_dst[k];
+    }
+    for (int k = 0; k < M; ++k) {
+        v[14][k] = b_p[k];
+        v[15][k] = w_out[k];
+    }
+    v[16][0] = b_out;
+    c->W_ih = v[0]; c->W_hh = v[1]; c->b_ih = v[2]; c->b_hh = v[3];
+    c->W_q = v[4]; c->b_q = v[5]; c->W_k = v[6]; c->b_k = v[7];
+    c->W_v = v[8]; c->b_v = v[9]; c->W_o = v[10]; c->b_o = v[11];
+    c->W_src = v[12]; c->W_dst = v[13]; c->b_p = v[14]; c->w_out = v[15]; c->b_out = v[16];
+    c->train_on = 1;
+    c->opt = opt;
+    c->lr = lr;
+    c->beta1 = beta1;
+    c->beta2 = beta2;
+    c->eps = eps;
+    c->opt_steps = 0;
+    return ORC_OK;
+}
+
+int64_t orc_param_count(void *p) { return ((orc_ctx *)p)->n_params; }
+
+void orc_get_params(void *p, double *out)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (c->train_on)
+        memcpy(out, c->theta, sizeof(double) * (size_t)c->n_params);
+}
+
+/* Loss and gradient of one iteration (into c->grad), from the iteration's
+ * forward values: root and neighbour positions in the node set, the fetched
+ * rows (fm: after the mitigation when it is on), the updated memories sn
+ * [nU x M] and the embeddings h [R x M].  Intermediate values of the
+ * attention and the memory updater are recomputed here from the same inputs.
+ * Returns the loss. */
+static double train_gradient(orc_ctx *c, int b, int R, int nU, const int32_t *root_pos,
+                             const double *rts, const int32_t *nbr_pos, const int32_t *eid,
+                             const double *nts, const int32_t *cnt, const double *fm,
+                             const double *fmts, const double *fl, const double *flts,
+                             const int32_t *fver, const double *sn, const double *h)
+{
+    const int M = c->M, D_e = c->D_e, D_t = c->D_t, H = c->H, nb = c->nb;
+    const int D_x = c->D_x, D_m = c->D_m;
+    const int D_q = M + D_t, D_kv = M + D_e + D_t, d_h = M / H;
+    const int nbs = nb > 0 ? nb : 1;
+    double *g[ORC_NPT];
+    param_views(c, c->grad, g);
+    memset(c->grad, 0, sizeof(double) * (size_t)c->n_params);
+    double *gW_ih = g[0], *gW_hh = g[1], *gb_ih = g[2], *gb_hh = g[3];
+    double *gW_q = g[4], *gb_q = g[5], *gW_k = g[6], *gb_k = g[7], *gW_v = g[8], *gb_v = g[9];
+    double *gW_o = g[10], *gb_o = g[11], *gW_src = g[12], *gW_dst = g[13], *gb_p = g[14];
+    double *gw_out = g[15], *gb_out = g[16];
+
+    /* the link predictor and the loss, event by event */
+    double *dh = (double *)calloc((size_t)R * M + 1, sizeof(double));
+    double *zp = (double *)malloc(sizeof(double) * 4 * M);
+    double *zn = zp + M, *dzp = zn + M, *dzn = dzp + M;
+    double loss = 0.0;
+    for (int e = 0; e < b; ++e) {
+        const double *hs = h + (size_t)e * M, *hd = h + (size_t)(b + e) * M;
+        const double *hn = h + (size_t)(2 * b + e) * M;
+        double sp = c->b_out[0], sq = c->b_out[0];
+        for (int i = 0; i < M; ++i) {
+            double a = c->b_p[i], an = c->b_p[i];
+            for (int k = 0; k < M; ++k) {
+                a += c->W_src[(size_t)i * M + k] * hs[k] + c->W_dst[(size_t)i * M + k] * hd[k];
+                an += c->W_src[(size_t)i * M + k] * hs[k] + c->W_dst[(size_t)i * M + k] * hn[k];
+            }
+            zp[i] = a;
+            zn[i] = an;
+            sp += c->w_out[i] * (a > 0.0 ? a : 0.0);
+            sq += c->w_out[i] * (an > 0.0 ? an : 0.0);
+        }
+        loss += softplus(-sp) + softplus(sq);
+        const double dsp = (sigmoid(sp) - 1.0) / b, dsq = sigmoid(sq) / b;
+        gb_out[0] += dsp + dsq;
+        for (int i = 0; i < M; ++i) {
+            gw_out[i] += dsp * (zp[i] > 0.0 ? zp[i] : 0.0) + dsq * (zn[i] > 0.0 ? zn[i] : 0.0);
+            dzp[i] = zp[i] > 0.0 ? dsp * c->w_out[i] : 0.0;
+            dzn[i] = zn[i] > 0.0 ? dsq * c->w_out[i] : 0.0;
+            gb_p[i] += dzp[i] + dzn[i];
+            for (int k = 0; k < M; ++k) {
+                gW_src[(size_t)i * M + k] += (dzp[i] + dzn[i]) * hs[k];
+                gW_dst[(size_t)i * M + k] += dzp[i] * hd[k] + dzn[i] * hn[k];
+            }
+        }
+        for (int k = 0; k < M; ++k) {
+            double a = 0.0, ad = 0.0, an = 0.0;
+            for (int i = 0; i < M; ++i) {
+                a += c->W_src[(size_t)i * M + k] * (dzp[i] + dzn[i]);
+                ad += c->W_dst[(size_t)i * M + k] * dzp[i];
+                an += c->W_dst[(size_t)i * M + k] * dzn[i];
+            }
+            dh[(size_t)e * M + k] += a;
+            dh[(size_t)(b + e) * M + k] += ad;
+            dh[(size_t)(2 * b + e) * M + k] += an;
+        }
+    }
+    free(zp);
+
+    /* the attention, root by root: its forward values again, then the
+     * gradients of its inputs and of the slot-level projections */
+    const size_t RS = (size_t)R * nbs;
+    double *kap = (double *)calloc(RS * D_kv + 1, sizeof(double));
+    double *dK = (double *)calloc(RS * M + 1, sizeof(double));
+    double *dV = (double *)calloc(RS * M + 1, sizeof(double));
+    double *ds_slot = (double *)calloc(RS * M + 1, sizeof(double));
+    double *xq = (double *)malloc(sizeof(double) * ((size_t)R * D_q + 1));
+    double *dq = (double *)calloc((size_t)R * M + 1, sizeof(double));
+    double *xo = (double *)malloc(sizeof(double) * ((size_t)R * 2 * M + 1));
+    double *dzo = (double *)malloc(sizeof(double) * ((size_t)R * M + 1));
+    double *ds_root = (double *)malloc(sizeof(double) * ((size_t)R * M + 1));
+    const double scale = 1.0 / sqrt((double)d_h);
+    #pragma omp parallel for schedule(dynamic, 8)
+    for (int r = 0; r < R; ++r) {
+        const int cr = cnt[r];
+        const double *sv = sn + (size_t)root_pos[r] * M;
+        double *K = (double *)malloc(sizeof(double) * ((size_t)nbs * M * 2 + 4 * (size_t)M +
+                                                       (size_t)H * nbs + nbs));
+        double *V = K + (size_t)nbs * M;
+        double *q = V + (size_t)nbs * M, *o = q + M, *dxo = o + M;   /* dxo: [2M] */
+        double *al = dxo + 2 * M, *dal = al + (size_t)H * nbs;
+        double *xqr = xq + (size_t)r * D_q, *xor_ = xo + (size_t)r * 2 * M;
+        memcpy(xqr, sv, sizeof(double) * M);
+        orc_time_encode(D_t, c->omega, c->beta, 0.0, xqr + M);
+        matvec(M, D_q, c->W_q, c->b_q, xqr, q);
+        for (int j = 0; j < cr; ++j) {
+            const size_t sl = (size_t)r * nb + j;
+            double *kp = kap + sl * D_kv;
+            memcpy(kp, sn + (size_t)nbr_pos[sl] * M, sizeof(double) * M);
+            for (int d = 0; d < D_e; ++d)
+                kp[M + d] = (double)c->efeat[(size_t)eid[sl] * D_e + d];
+            orc_time_encode(D_t, c->omega, c->beta, rts[r] - nts[sl], kp + M + D_e);
+            matvec(M, D_kv, c->W_k, c->b_k, kp, K + (size_t)j * M);
+            matvec(M, D_kv, c->W_v, c->b_v, kp, V + (size_t)j * M);
+        }
+        for (int k = 0; k < M; ++k)
+            xor_[k] = 0.0;
+        for (int eta = 0; eta < H && cr > 0; ++eta) {
+            const int o0 = eta * d_h;
+            double mx = -INFINITY, den = 0.0;
+            for (int j = 0; j < cr; ++j) {
+                double dot = 0.0;
+                for (int k = 0; k < d_h; ++k)
+                    dot += q[o0 + k] * K[(size_t)j * M + o0 + k];
+                al[eta * nbs + j] = dot * scale;
+                if (al[eta * nbs + j] > mx)
+                    mx = al[eta * nbs + j];
+            }
+            for (int j = 0; j < cr; ++j) {
+                al[eta * nbs + j] = exp(al[eta * nbs + j] - mx);
+                den += al[eta * nbs + j];
+            }
+            for (int j = 0; j < cr; ++j) {
+                al[eta * nbs + j] /= den;
+                for (int k = 0; k < d_h; ++k)
+                    xor_[o0 + k] += al[eta * nbs + j] * V[(size_t)j * M + o0 + k];
+            }
+        }
+        memcpy(xor_ + M, sv, sizeof(double) * M);
+        matvec(M, 2 * M, c->W_o, c->b_o, xor_, o);
+        double *dzr = dzo + (size_t)r * M;
+        for (int i = 0; i < M; ++i)
+            dzr[i] = o[i] > 0.0 ? dh[(size_t)r * M + i] : 0.0;
+        for (int k = 0; k < 2 * M; ++k) {
+            double a = 0.0;
+            for (int i = 0; i < M; ++i)
+                a += c->W_o[(size_t)i * 2 * M + k] * dzr[i];
+            dxo[k] = a;
+        }
+        /* dxo[0, M): the gradient of the attention output a; [M, 2M): of s_v */
+        double *dqr = dq + (size_t)r * M;
+        for (int eta = 0; eta < H && cr > 0; ++eta) {
+            const int o0 = eta * d_h;
+            double sdot = 0.0;
+            for (int j = 0; j < cr; ++j) {
+                double a = 0.0;
+                for (int k = 0; k < d_h; ++k)
+                    a += dxo[o0 + k] * V[(size_t)j * M + o0 + k];
+                dal[j] = a;
+                sdot += al[eta * nbs + j] * a;
+            }
+            for (int j = 0; j < cr; ++j) {
+                const double aj = al[eta * nbs + j];
+                const double dsc = aj * (dal[j] - sdot);
+                const size_t sl = (size_t)r * nb + j;
+                for (int k = 0; k < d_h; ++k) {
+                    dV[sl * M + o0 + k] = aj * dxo[o0 + k];
+                    dK[sl * M + o0 + k] = dsc * q[o0 + k] * scale;
+                    dqr[o0 + k] += dsc * K[(size_t)j * M + o0 + k] * scale;
+                }
+            }
+        }
+        double *dsr = ds_root + (size_t)r * M;
+        for (int m = 0; m < M; ++m) {
+            double a = dxo[M + m];
+            for (int i = 0; i < M; ++i)
+                a += c->W_q[(size_t)i * D_q + m] * dqr[i];
+            dsr[m] = a;
+        }
+        for (int j = 0; j < cr; ++j) {
+            const size_t sl = (size_t)r * nb + j;
+            for (int m = 0; m < M; ++m) {
+                double a = 0.0;
+                for (int i = 0; i < M; ++i)
+                    a += c->W_k[(size_t)i * D_kv + m] * dK[sl * M + i] +
+                         c->W_v[(size_t)i * D_kv + m] * dV[sl * M + i];
+                ds_slot[sl * M + m] = a;
+            }
+        }
+        free(K);
+    }
+    /* the attention's weight gradients, one output row per thread */
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int i = 0; i < M; ++i) {
+        for (int r = 0; r < R; ++r) {
+            const double z = dzo[(size_t)r * M + i], d = dq[(size_t)r * M + i];
+            gb_o[i] += z;
+            gb_q[i] += d;
+            for (int k = 0; k < 2 * M; ++k)
+                gW_o[(size_t)i * 2 * M + k] += z * xo[(size_t)r * 2 * M + k];
+            for (int k = 0; k < D_q; ++k)
+                gW_q[(size_t)i * D_q + k] += d * xq[(size_t)r * D_q + k];
+            for (int j = 0; j < cnt[r]; ++j) {
+                const size_t sl = (size_t)r * nb + j;
+                const double dk = dK[sl * M + i], dv = dV[sl * M + i];
+                gb_k[i] += dk;
+                gb_v[i] += dv;
+                for (int k = 0; k < D_kv; ++k) {
+                    gW_k[(size_t)i * D_kv + k] += dk * kap[sl * D_kv + k];
+                    gW_v[(size_t)i * D_kv + k] += dv * kap[sl * D_kv + k];
+                }
+            }
+        }
+    }
+    /* the gradient of every updated memory: its roots, then its slots */
+    double *ds = (double *)calloc((size_t)nU * M + 1, sizeof(double));
+    for (int r = 0; r < R; ++r)
+        for (int m = 0; m < M; ++m)
+            ds[(size_t)root_pos[r] * M + m] += ds_root[(size_t)r * M + m];
+    for (int r = 0; r < R; ++r)
+        for (int j = 0; j < cnt[r]; ++j) {
+            const size_t sl = (size_t)r * nb + j;
+            for (int m = 0; m < M; ++m)
+                ds[(size_t)nbr_pos[sl] * M + m] += ds_slot[sl * M + m];
+        }
+    free(kap); free(dK); free(dV); free(ds_slot); free(xq); free(dq); free(xo); free(dzo);
+    free(ds_root); free(dh);
+
+    /* the memory updater (GRU), node by node for nodes with mail */
+    double *X = (double *)calloc((size_t)nU * D_x + 1, sizeof(double));
+    double *dGx = (double *)calloc((size_t)nU * 3 * M + 1, sizeof(double));
+    double *dGh = (double *)calloc((size_t)nU * 3 * M + 1, sizeof(double));
+    #pragma omp parallel for schedule(dynamic, 8)
+    for (int k = 0; k < nU; ++k) {
+        if (fver[k] < 0)
+            continue;
+        double *x = X + (size_t)k * D_x;
+        const double *hm = fm + (size_t)k * M;
+        memcpy(x, fl + (size_t)k * D_m, sizeof(double) * D_m);
+        orc_time_encode(D_t, c->omega, c->beta, flts[k] - fmts[k], x + D_m);
+        for (int j = 0; j < M; ++j) {
+            double ir = c->b_ih[j], iz = c->b_ih[M + j], in_ = c->b_ih[2 * M + j];
+            double hr = c->b_hh[j], hz = c->b_hh[M + j], hn = c->b_hh[2 * M + j];
+            for (int q = 0; q < D_x; ++q) {
+                ir += c->W_ih[(size_t)j * D_x + q] * x[q];
+                iz += c->W_ih[(size_t)(M + j) * D_x + q] * x[q];
+                in_ += c->W_ih[(size_t)(2 * M + j) * D_x + q] * x[q];
+            }
+            for (int q = 0; q < M; ++q) {
+                hr += c->W_hh[(size_t)j * M + q] * hm[q];
+                hz += c->W_hh[(size_t)(M + j) * M + q] * hm[q];
+                hn += c->W_hh[(size_t)(2 * M + j) * M + q] * hm[q];
+            }
+            const double r = sigmoid(ir + hr), z = sigmoid(iz + hz), n = tanh(in_ + r * hn);
+            const double d = ds[(size_t)k * M + j];
+            const double dn = d * (1.0 - z), dz = d * (hm[j] - n);
+            const double dan = dn * (1.0 - n * n);
+            const double dar = dan * hn * r * (1.0 - r), daz = dz * z * (1.0 - z);
+            double *gx = dGx + (size_t)k * 3 * M, *gh = dGh + (size_t)k * 3 * M;
+            gx[j] = dar; gx[M + j] = daz; gx[2 * M + j] = dan;
+            gh[j] = dar; gh[M + j] = daz; gh[2 * M + j] = dan * r;
+        }
+    }
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int i = 0; i < 3 * M; ++i) {
+        for (int k = 0; k < nU; ++k) {
+            if (fver[k] < 0)
+                continue;
+            const double gx = dGx[(size_t)k * 3 * M + i], gh = dGh[(size_t)k * 3 * M + i];
+            gb_ih[i] += gx;
+            gb_hh[i] += gh;
+            for (int q = 0; q < D_x; ++q)
+                gW_ih[(size_t)i * D_x + q] += gx * X[(size_t)k * D_x + q];
+            for (int q = 0; q < M; ++q)
+                gW_hh[(size_t)i * M + q] += gh * fm[(size_t)k * M + q];
+        }
+    }
+    free(X); free(dGx); free(dGh); free(ds);
+    return loss / b;
+}
+
+/* One optimizer step on theta with the gradient of the last iteration. */
+static void optimizer_step(orc_ctx *c)
+{
+    c->opt_steps++;
+    const int64_t n = c->n_params;
+    if (c->opt == ORC_SGD) {
+        for (int64_t k = 0; k < n; ++k)
+            c->theta[k] -= c->lr * c->grad[k];
+        return;
+    }
+    const double b1 = c->beta1, b2 = c->beta2;
+    const double c1 = 1.0 - pow(b1, (double)c->opt_steps), c2 = 1.0 - pow(b2, (double)c->opt_steps);
+    for (int64_t k = 0; k < n; ++k) {
+        const double g = c->grad[k];
+        c->m1[k] = b1 * c->m1[k] + (1.0 - b1) * g;
+        c->m2[k] = b2 * c->m2[k] + (1.0 - b2) * g * g;
+        const double mh = c->m1[k] / c1, vh = c->m2[k] / c2;
+        c->theta[k] -= c->lr * mh / (sqrt(vh) + c->eps);
+    }
 }
 
 /* One iteration of the stage.  Returns ORC_EEND when the stream is exhausted. */
@@ -987,8 +1413,30 @@ int orc_step(void *p, orc_step_out *o)
     }
     c->q[c->nq++] = W;
 
+    /* 9. training (when enabled): loss and gradient of this iteration, then
+     * the optimizer step (the next iteration runs with the new weights) */
+    double loss = 0.0;
+    if (c->train_on) {
+        int32_t *rp = (int32_t *)malloc(sizeof(int32_t) * R);
+        int32_t *np_ = (int32_t *)malloc(sizeof(int32_t) * (RS ? RS : 1));
+        for (int r = 0; r < R; ++r)
+            rp[r] = pos[root[r]];
+        for (size_t k = 0; k < (size_t)R * nb; ++k)
+            np_[k] = nbr[k] >= 0 ? pos[nbr[k]] : -1;
+        loss = train_gradient(c, b, R, nU, rp, rts, np_, eid, nts, cnt, fm, fmts, fl, flts,
+                              fver, sn, h);
+        optimizer_step(c);
+        free(rp);
+        free(np_);
+    }
+
     /* outputs */
     if (o) {
+        o->loss = loss;
+        if (c->train_on && o->grad)
+            memcpy(o->grad, c->grad, sizeof(double) * (size_t)c->n_params);
+        if (c->train_on && o->params)
+            memcpy(o->params, c->theta, sizeof(double) * (size_t)c->n_params);
         o->iter = i; o->b = b; o->R = R; o->n_U = nU;
         if (o->root) memcpy(o->root, root, sizeof(int32_t) * R);
         if (o->root_ts) memcpy(o->root_ts, rts, sizeof(double) * R);

@@ -25,8 +25,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["Workload", "Weights", "CONFIGS", "FEAT_CHUNK", "make_workload", "make_weights",
-           "edge_feature_rows", "config_names"]
+__all__ = ["Workload", "Weights", "Predictor", "CONFIGS", "FEAT_CHUNK", "make_workload",
+           "make_weights", "make_predictor", "edge_feature_rows", "config_names"]
 
 # Rows per independently keyed chunk of the edge-feature stream.
 FEAT_CHUNK = 1 << 16
@@ -294,6 +294,28 @@ def custom_workload(name, N, src, dst, t, neg, efeat, *, M, D_t, H, nb, B, s, se
                     neg=np.ascontiguousarray(neg, dtype=np.int32),
                     efeat=None if efeat is None else np.ascontiguousarray(efeat, dtype=np.float32),
                     D_e=D_e, M=M, D_t=D_t, H=H, nb=nb, B=B, s=s, seed=seed)
+
+
+@dataclass
+class Predictor:
+    """Link-predictor weights: z = W_src h_u + W_dst h_v + b_p,
+    score = w_out . ReLU(z) + b_out (fp32)."""
+    W_src: np.ndarray
+    W_dst: np.ndarray
+    b_p: np.ndarray
+    w_out: np.ndarray
+    b_out: float
+
+
+def make_predictor(M: int, *, seed: int = 0) -> Predictor:
+    """U(+-1/sqrt(fan_in)) fp32 predictor weights (fan_in 2M for the first
+    layer, which sees both endpoints, M for the output)."""
+    r = lambda n: _rng(seed, "p/" + n)
+    return Predictor(W_src=_uniform(r("W_src"), (M, M), 2 * M),
+                     W_dst=_uniform(r("W_dst"), (M, M), 2 * M),
+                     b_p=_uniform(r("b_p"), (M,), 2 * M),
+                     w_out=_uniform(r("w_out"), (M,), M),
+                     b_out=float(_uniform(r("b_out"), (1,), M)[0]))
 
 
 def _uniform(rng, shape, fan_in):
