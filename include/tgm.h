@@ -365,6 +365,86 @@ tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t m, int64_t
                            float *s_trace, void *stream, void *prefetch_stream);
 
 /* ------------------------------------------------------------------------
+ * Training step (the step that follows the stage in MTGNN training: Sec. 5,
+ * training settings, link prediction on equal numbers of positive and
+ * negative pairs, learning rate 1e-4; App. C.2, the embedding, the loss and
+ * the backward step).  TGN models only.
+ *
+ * The iteration's training samples are its b positive pairs (src_e, dst_e)
+ * and b negative pairs (src_e, neg_e), i.e. roots e, b + e and 2b + e.  The
+ * link predictor scores a pair from the two embeddings,
+ *   z = W_src h_u + W_dst h_v + b_p,  score(u, v) = w_out . ReLU(z) + b_out,
+ * and the loss is L = (1/b) sum_e [softplus(-score(src_e, dst_e)) +
+ * softplus(score(src_e, neg_e))] (binary cross-entropy on the scores).  The
+ * gradient of L reaches every weight of the attention (through h), of the
+ * memory updater (through the new memories s' of the nodes that hold mail)
+ * and of the predictor; the fetched memories and mails are inputs of the
+ * iteration, and omega and beta are not trained.  Then one optimizer step
+ * (SGD: theta -= lr g; Adam: the bias-corrected moments of Kingma and Ba) and
+ * the model's packed operands are rebuilt from the new weights, so the next
+ * iteration runs with them.
+ *
+ * Parameter vector (float, in this order): W_ih [3M x D_x], W_hh [3M x M],
+ * b_ih [3M], b_hh [3M], W_q [M x (M + D_t)], b_q [M], W_k [M x D_kv], b_k [M],
+ * W_v [M x D_kv], b_v [M], W_o [M x 2M], b_o [M], W_src [M x M],
+ * W_dst [M x M], b_p [M], w_out [M], b_out [1], with D_kv = M + D_e + D_t.
+ * Every reduction has a fixed order: results are bit-reproducible.
+ */
+typedef struct tgm_trainer *tgm_trainer_t;
+#define TGM_OPT_SGD 0
+#define TGM_OPT_ADAM 1
+#define TGM_N_PARAM_TENSORS 17
+
+typedef struct {
+    const float *W_src, *W_dst; /* host [M x M] */
+    const float *b_p, *w_out;   /* host [M] */
+    float b_out;
+} tgm_predictor;
+
+typedef struct {
+    int32_t kind;                 /* TGM_OPT_SGD or TGM_OPT_ADAM */
+    float lr, beta1, beta2, eps;  /* beta1, beta2, eps: Adam only */
+} tgm_optimizer;
+
+/* A trainer for model m (a TGN model, M <= 128), with the model's weights w
+ * (HOST arrays, the ones given to tgm_model_create) and the predictor's p
+ * copied into its device parameter vector; it owns the gradient, the
+ * optimizer's moments and the work space for batches of up to
+ * max_roots / 3 events and node sets of up to max_nodes rows (m's limits).
+ * The trainer rewrites m's operands after every step: m must not be used by
+ * another trainer.  Errors: TGM_EINVAL (null, JODIE model, parameters),
+ * TGM_ENOMEM, TGM_EDEVICE. */
+tgm_status_t tgm_trainer_create(tgm_model_t m, const tgm_weights *w, const tgm_predictor *p,
+                                const tgm_optimizer *opt, void *stream, tgm_trainer_t *out);
+tgm_status_t tgm_trainer_destroy(tgm_trainer_t tr);
+/* Host outputs (each may be NULL): the parameter count, the sizes of the
+ * TGM_N_PARAM_TENSORS tensors in vector order, the optimizer steps taken. */
+tgm_status_t tgm_trainer_info(tgm_trainer_t tr, int64_t *n_params, int64_t *sizes,
+                              int64_t *steps);
+/* Device copies (each may be NULL, ordered on `stream`): the parameter vector
+ * [n_params], the gradient of the last step [n_params], its loss [1]. */
+tgm_status_t tgm_trainer_read(tgm_trainer_t tr, float *params, float *grad, float *loss,
+                              void *stream);
+/* The training step of the iteration whose sample buffers sb (root_pos,
+ * root_ts, nbr_pos, eid, nts, cnt, n_nodes as from tgm_sample_nodes), fetch
+ * buffers fb (the rows as fetched, after the mitigation when it is on), new
+ * memories mem_new [cap x M] (tgm_update_memory) and embeddings h [3b x M]
+ * (tgm_embed) are given; b events; loss (device [1], may be NULL) receives
+ * the loss.  Stream-ordered; allocates nothing.  Errors: TGM_EINVAL,
+ * TGM_ESIZE (3b above max_roots or cap above max_nodes). */
+tgm_status_t tgm_train_step(tgm_trainer_t tr, tgm_model_t m, tgm_graph_t g, int32_t b,
+                            const tgm_sample_buffers *sb, const tgm_fetch_buffers *fb,
+                            const float *mem_new, const float *h, int32_t cap, float *loss,
+                            void *stream);
+/* Makes tgm_stage_run take the training step after every iteration (tr NULL:
+ * off, the default).  With loss_log (device, may be NULL) the loss of
+ * iteration i goes to loss_log[i % log_len].  In training mode the executor
+ * launches each next fetch after the training step (the step reads the
+ * iteration's fetch buffers), instead of in the attention launch. */
+tgm_status_t tgm_state_set_training(tgm_state_t st, tgm_trainer_t tr, float *loss_log,
+                                    int64_t log_len);
+
+/* ------------------------------------------------------------------------
  * Similarity-based staleness mitigation (MSPipe-S, Sec. 3.3), applied to the
  * fetched memories of a batch between tgm_fetch_memory and
  * tgm_update_memory.  For the fetched node set (positions p < *n_nodes):

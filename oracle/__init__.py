@@ -64,7 +64,8 @@ class _StepOut(C.Structure):
                 ("new_mem_ts", _f64p), ("h", _f64p), ("winner", _i64p),
                 ("m_mem", _f64p), ("m_stale", _i32p), ("m_omega", _i32p), ("m_gamma", C.c_double),
                 ("m_n_stale", C.c_int32), ("m_pad", C.c_int32), ("x_mem", _f64p),
-                ("loss", C.c_double), ("grad", _f64p), ("params", _f64p)]
+                ("loss", C.c_double), ("grad", _f64p), ("params", _f64p),
+                ("relu_margin", C.c_double)]
 
 OPTIMIZERS = {"sgd": 0, "adam": 1}
 # the parameter vector's tensors, in order (orc_param_sizes)
@@ -263,6 +264,8 @@ class StepResult:
     loss: float | None = None
     grad: np.ndarray | None = None
     params: np.ndarray | None = None
+    # the smallest |pre-activation| of the ReLUs on the gradient's path
+    relu_margin: float | None = None
 
 
 class Oracle:
@@ -385,7 +388,8 @@ class Oracle:
             x_mem=g("x_mem", nU * M, (nU, M)),
             loss=o.loss if self.n_params else None,
             grad=arrs["grad"] if self.n_params else None,
-            params=arrs["params"] if self.n_params else None)
+            params=arrs["params"] if self.n_params else None,
+            relu_margin=o.relu_margin if self.n_params else None)
 
     def flush(self):
         lib().orc_flush(self._h)

@@ -608,6 +608,10 @@ typedef struct {
      * the order of orc_param_layout */
     double loss;
     double *grad, *params;
+    /* the smallest |pre-activation| of the ReLUs the gradient passes (the
+     * predictor's z and the attention's output projection): the margin by
+     * which no branch of the backward is near its kink */
+    double relu_margin;
 } orc_step_out;
 
 static double *widen(const float *x, size_t n)
@@ -935,8 +939,10 @@ static double train_gradient(orc_ctx *c, int b, int R, int nU, const int32_t *ro
                              const double *rts, const int32_t *nbr_pos, const int32_t *eid,
                              const double *nts, const int32_t *cnt, const double *fm,
                              const double *fmts, const double *fl, const double *flts,
-                             const int32_t *fver, const double *sn, const double *h)
+                             const int32_t *fver, const double *sn, const double *h,
+                             double *margin_out)
 {
+    double margin = INFINITY;
     const int M = c->M, D_e = c->D_e, D_t = c->D_t, H = c->H, nb = c->nb;
     const int D_x = c->D_x, D_m = c->D_m;
     const int D_q = M + D_t, D_kv = M + D_e + D_t, d_h = M / H;
@@ -969,6 +975,8 @@ static double train_gradient(orc_ctx *c, int b, int R, int nU, const int32_t *ro
             sp += c->w_out[i] * (a > 0.0 ? a : 0.0);
             sq += c->w_out[i] * (an > 0.0 ? an : 0.0);
         }
+        for (int i = 0; i < M; ++i)
+            margin = fmin(margin, fmin(fabs(zp[i]), fabs(zn[i])));
         loss += softplus(-sp) + softplus(sq);
         const double dsp = (sigmoid(sp) - 1.0) / b, dsq = sigmoid(sq) / b;
         gb_out[0] += dsp + dsq;
@@ -1009,6 +1017,7 @@ static double train_gradient(orc_ctx *c, int b, int R, int nU, const int32_t *ro
     double *dzo = (double *)malloc(sizeof(double) * ((size_t)R * M + 1));
     double *ds_root = (double *)malloc(sizeof(double) * ((size_t)R * M + 1));
     const double scale = 1.0 / sqrt((double)d_h);
+    double *omarg = (double *)malloc(sizeof(double) * (R > 0 ? R : 1));
     #pragma omp parallel for schedule(dynamic, 8)
     for (int r = 0; r < R; ++r) {
         const int cr = cnt[r];
@@ -1058,8 +1067,11 @@ static double train_gradient(orc_ctx *c, int b, int R, int nU, const int32_t *ro
         memcpy(xor_ + M, sv, sizeof(double) * M);
         matvec(M, 2 * M, c->W_o, c->b_o, xor_, o);
         double *dzr = dzo + (size_t)r * M;
-        for (int i = 0; i < M; ++i)
+        omarg[r] = INFINITY;
+        for (int i = 0; i < M; ++i) {
             dzr[i] = o[i] > 0.0 ? dh[(size_t)r * M + i] : 0.0;
+            omarg[r] = fmin(omarg[r], fabs(o[i]));
+        }
         for (int k = 0; k < 2 * M; ++k) {
             double a = 0.0;
             for (int i = 0; i < M; ++i)
@@ -1108,6 +1120,10 @@ static double train_gradient(orc_ctx *c, int b, int R, int nU, const int32_t *ro
         }
         free(K);
     }
+    for (int r = 0; r < R; ++r)
+        margin = fmin(margin, omarg[r]);
+    free(omarg);
+    *margin_out = margin;
     /* the attention's weight gradients, one output row per thread */
     #pragma omp parallel for schedule(dynamic, 4)
     for (int i = 0; i < M; ++i) {
@@ -1415,7 +1431,7 @@ int orc_step(void *p, orc_step_out *o)
 
     /* 9. training (when enabled): loss and gradient of this iteration, then
      * the optimizer step (the next iteration runs with the new weights) */
-    double loss = 0.0;
+    double loss = 0.0, margin = INFINITY;
     if (c->train_on) {
         int32_t *rp = (int32_t *)malloc(sizeof(int32_t) * R);
         int32_t *np_ = (int32_t *)malloc(sizeof(int32_t) * (RS ? RS : 1));
@@ -1424,7 +1440,7 @@ int orc_step(void *p, orc_step_out *o)
         for (size_t k = 0; k < (size_t)R * nb; ++k)
             np_[k] = nbr[k] >= 0 ? pos[nbr[k]] : -1;
         loss = train_gradient(c, b, R, nU, rp, rts, np_, eid, nts, cnt, fm, fmts, fl, flts,
-                              fver, sn, h);
+                              fver, sn, h, &margin);
         optimizer_step(c);
         free(rp);
         free(np_);
@@ -1433,6 +1449,7 @@ int orc_step(void *p, orc_step_out *o)
     /* outputs */
     if (o) {
         o->loss = loss;
+        o->relu_margin = margin;
         if (c->train_on && o->grad)
             memcpy(o->grad, c->grad, sizeof(double) * (size_t)c->n_params);
         if (c->train_on && o->params)

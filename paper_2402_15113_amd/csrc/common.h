@@ -130,6 +130,11 @@ struct tgm_state {
     // the executor's cross-stream events (sampled chunk and computed chunk by
     // parity, start), made at creation so that a run creates nothing
     hipEvent_t run_ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+    // training step after every iteration of the executor (off when null):
+    // iteration i's loss goes to loss_log[i % loss_log_len] when a log is set
+    struct tgm_trainer *trainer = nullptr;
+    float *loss_log = nullptr;
+    int64_t loss_log_len = 0;
     // staleness mitigation applied by the pipelined executor after each fetch
     // (tgm_state_set_mitigation; off when mit is null)
     struct tgm_mitigator *mit = nullptr;
@@ -661,6 +666,21 @@ tgm_status_t exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b, const i
 // and drops the contents of existing slots).
 tgm_status_t mitigate_reserve(tgm_mitigator_t mt, int32_t nslots);
 int32_t mitigate_slots(tgm_mitigator_t mt);
+
+// The trained weights of a TGN model, plain row-major device arrays (the
+// layouts of tgm_weights).  model_repack rebuilds every packed operand the
+// model's kernels read from them (after an optimizer step).
+struct ModelParams {
+    const float *W_ih, *W_hh, *b_ih, *b_hh, *W_q, *b_q, *W_k, *b_k, *W_v, *b_v, *W_o, *b_o;
+};
+tgm_status_t model_repack(tgm_model_t m, const ModelParams &w, hipStream_t s);
+
+// The training step of one iteration (tgm_train_step) on stream s, from the
+// iteration's sample and fetch buffers, new memories and embeddings.
+tgm_status_t train_step_launch(tgm_trainer_t tr, tgm_model_t m, tgm_graph_t g, int32_t b,
+                               const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
+                               const float *mem_new, const float *h, int32_t cap, float *loss_out,
+                               hipStream_t s);
 tgm_status_t mitigate_prep_launch(tgm_mitigator_t mt, tgm_graph_t g, int64_t first_event,
                                   const int32_t *nodes, const int32_t *n_nodes, int32_t cap,
                                   int32_t slot, hipStream_t s);

@@ -2533,3 +2533,156 @@ tgm_status_t tgm::exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b,
     TGM_LAUNCH(k_latest, dim3((unsigned)cdiv(n_cand, 256)), dim3(256), 0, s, ga);
     return TGM_OK;
 }
+
+// ------------------------------------------------------------------ repack
+// After a training step the plain weights have changed: every operand the
+// kernels read in a packed layout is rebuilt from them on the device, in the
+// layouts tgm_model_create builds on the host (the zero padding past the data
+// chunks stays as it was).
+namespace {
+
+// Source of element (n, k) of a packed B operand: row n of up to three row
+// blocks of `rows` rows each (W[b], leading dimension ldw[b]); with perm_Dt
+// >= 0 the column k is read from the slot-row order [phi || efeat] of
+// columns of [s || efeat || phi]; with trans the roles of n and k swap.
+struct PackSrc {
+    const float *W[3];
+    int ldw[3];
+    int rows;
+    int perm_M, perm_De, perm_Dt;
+    int trans;
+};
+
+__device__ __forceinline__ float pack_src(const PackSrc &p, int n, int k)
+{
+    int r = n, c = k;
+    if (p.trans) {
+        r = k;
+        c = n;
+    }
+    const int blk = r / p.rows, rr = r - blk * p.rows;
+    if (p.perm_Dt >= 0)
+        c = c < p.perm_Dt ? p.perm_M + p.perm_De + c : p.perm_M + c - p.perm_Dt;
+    return p.W[blk][(int64_t)rr * p.ldw[blk] + c];
+}
+
+// out[((kc NB + nb) 64 + lane) 4 + j] = src(16 nb + lane % 16, 16 kc + 4 (lane / 16) + j),
+// zero outside [0, n_out) x [0, K): the layout of pack_b
+__global__ __launch_bounds__(256) void k_pack(PackSrc p, int n_out, int K, int KC, int NB,
+                                              float *__restrict__ out)
+{
+    const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (t >= (int64_t)KC * NB * kWave * 4)
+        return;
+    const int j = (int)(t & 3), lane = (int)((t >> 2) & 63);
+    const int64_t blk = t >> 8;
+    const int nb = (int)(blk % NB), kc = (int)(blk / NB);
+    const int k = 16 * kc + 4 * (lane >> 4) + j, n = 16 * nb + (lane & 15);
+    out[t] = (k < K && n < n_out) ? pack_src(p, n, k) : 0.f;
+}
+
+// GRU biases [4][MP]: b_ir + b_hr, b_iz + b_hz, b_in, b_hn (JODIE: 0, 0, b_ih, b_hh)
+__global__ void k_pack_gru_bias(int M, int MP, int gates, const float *__restrict__ b_ih,
+                                const float *__restrict__ b_hh, float *__restrict__ out)
+{
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= M)
+        return;
+    if (gates == 3) {
+        out[k] = b_ih[k] + b_hh[k];
+        out[MP + k] = b_ih[M + k] + b_hh[M + k];
+        out[2 * MP + k] = b_ih[2 * M + k];
+        out[3 * MP + k] = b_hh[2 * M + k];
+    } else {
+        out[2 * MP + k] = b_ih[k];
+        out[3 * MP + k] = b_hh[k];
+    }
+}
+
+__global__ void k_copy_f32(const float *__restrict__ src, float *__restrict__ dst, int n)
+{
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k < n)
+        dst[k] = src[k];
+}
+
+tgm_status_t pack_launch(const PackSrc &p, int n_out, int K, int KC, int NB, void *out,
+                         hipStream_t s)
+{
+    const int64_t n = (int64_t)KC * NB * kWave * 4;
+    if (n > 0)
+        TGM_LAUNCH(k_pack, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, s, p, n_out, K, KC, NB,
+                   (float *)out);
+    return TGM_OK;
+}
+
+PackSrc plain_src(const float *W, int ldw, int rows)
+{
+    PackSrc p{};
+    p.W[0] = p.W[1] = p.W[2] = W;
+    p.ldw[0] = p.ldw[1] = p.ldw[2] = ldw;
+    p.rows = rows > 0 ? rows : 1;
+    p.perm_Dt = -1;
+    return p;
+}
+
+}  // namespace
+
+tgm_status_t tgm::model_repack(tgm_model_t m, const ModelParams &w, hipStream_t s)
+{
+    if (!m || m->kind != TGM_MODEL_TGN)
+        return TGM_EINVAL;
+    const int M = m->M, D_e = m->D_e, D_t = m->D_t, D_x = m->D_x, MP = m->MB * 16;
+    const int Dq = M + D_t, Dkv = M + D_e + D_t, KF = D_e + D_t;
+    // GRU: one packed operand per gate, in gate order
+    const int64_t gx = (int64_t)m->KXC * m->MB * kWave * 4, gh = (int64_t)m->KHC * m->MB * kWave * 4;
+    for (int gte = 0; gte < 3; ++gte) {
+        TGM_TRY_STATUS(pack_launch(plain_src(w.W_ih + (int64_t)gte * M * D_x, D_x, M), M, D_x,
+                                   m->KXC, m->MB, (float *)m->gru_bx + gte * gx, s));
+        TGM_TRY_STATUS(pack_launch(plain_src(w.W_hh + (int64_t)gte * M * M, M, M), M, M, m->KHC,
+                                   m->MB, (float *)m->gru_bh + gte * gh, s));
+    }
+    TGM_LAUNCH(k_pack_gru_bias, dim3((unsigned)cdiv(M, 128)), dim3(128), 0, s, M, MP, 3, w.b_ih,
+               w.b_hh, m->gru_bias);
+    // node projections: rows of [W_q^s; W_k^s; W_v^s]
+    {
+        PackSrc p{};
+        p.W[0] = w.W_q;
+        p.W[1] = w.W_k;
+        p.W[2] = w.W_v;
+        p.ldw[0] = Dq;
+        p.ldw[1] = p.ldw[2] = Dkv;
+        p.rows = M;
+        p.perm_Dt = -1;
+        TGM_TRY_STATUS(pack_launch(p, 3 * M, M, m->PC, m->PNB, m->proj_b, s));
+    }
+    // per-slot part of [K | V] in the slot-row column order [phi || efeat]
+    PackSrc kv{};
+    kv.W[0] = w.W_k;
+    kv.W[1] = kv.W[2] = w.W_v;
+    kv.ldw[0] = kv.ldw[1] = kv.ldw[2] = Dkv;
+    kv.rows = M;
+    kv.perm_M = M;
+    kv.perm_De = D_e;
+    kv.perm_Dt = D_t;
+    if (KF > 0)
+        TGM_TRY_STATUS(pack_launch(kv, 2 * M, KF, m->KFC, m->KVNB, m->kv_b, s));
+    if (m->fold && KF > 0) {
+        PackSrc v = kv;
+        v.W[0] = w.W_v;
+        TGM_TRY_STATUS(pack_launch(v, M, KF, m->KFC, m->VNB, m->v_b, s));
+        PackSrc u = kv;   // W_k^t [KF x M]: element (kf, d) = W_k[d][perm(kf)]
+        u.trans = 1;
+        TGM_TRY_STATUS(pack_launch(u, KF, M, m->DC, m->KFC, m->uk_a, s));
+    }
+    TGM_TRY_STATUS(pack_launch(plain_src(w.W_o, 2 * M, M), M, 2 * M, m->OC, m->ONB, m->out_b, s));
+    // biases of the node projection: c_q = W_q^t phi(0) + b_q, then b_k, b_v
+    hipLaunchKernelGGL(k_fold_q_bias, dim3((unsigned)cdiv(M, 64)), dim3(64), 0, s, M, D_t, w.W_q,
+                       w.b_q, m->beta, m->pbias);
+    TGM_LAUNCHED();
+    TGM_LAUNCH(k_copy_f32, dim3((unsigned)cdiv(M, 128)), dim3(128), 0, s, w.b_k, m->pbias + M, M);
+    TGM_LAUNCH(k_copy_f32, dim3((unsigned)cdiv(M, 128)), dim3(128), 0, s, w.b_v,
+               m->pbias + 2 * M, M);
+    TGM_LAUNCH(k_copy_f32, dim3((unsigned)cdiv(M, 128)), dim3(128), 0, s, w.b_o, m->b_o, M);
+    return TGM_OK;
+}

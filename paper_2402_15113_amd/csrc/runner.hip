@@ -28,6 +28,9 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
         return TGM_EINVAL;
     if (nsb > st->xwin_slots || (st->mit && mitigate_slots(st->mit) < 1 + nsb))
         return TGM_ESIZE;
+    const bool train = st->trainer != nullptr;
+    if (train && m->kind != TGM_MODEL_TGN)
+        return TGM_EINVAL;
     if (n == 0)
         return TGM_OK;
     if ((i0 + n - 1) * (int64_t)B >= g->E)
@@ -105,11 +108,25 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             const bool more = k + 1 < n;
             if (more && k + 1 == kend)   // the next iteration's samples are the next chunk's
                 TGM_HIP(hipStreamWaitEvent(main, ev[(c + 1) & 1], 0));
+            // in training mode the next fetch waits for the training step,
+            // which reads this iteration's fetch buffers
+            const tgm_sample_buffers *next = more ? &sb[(k + 1) % nsb] : nullptr;
             TGM_TRY_STATUS(compute_iteration(st, m, g, i0 + k, sb[k % nsb], *fb, cap, lo, b, nb,
                                              mem_new, new_mem_ts, winner, h,
-                                             more ? &sb[(k + 1) % nsb] : nullptr,
-                                             (int32_t)(1 + k % nsb), xwin[k % nsb],
-                                             xtag[k % nsb], main));
+                                             train ? nullptr : next, (int32_t)(1 + k % nsb),
+                                             xwin[k % nsb], xtag[k % nsb], main));
+            if (train) {
+                float *lo_ = st->loss_log ? st->loss_log + (i0 + k) % st->loss_log_len : nullptr;
+                TGM_TRY_STATUS(train_step_launch(st->trainer, m, g, b, sb[k % nsb], *fb, mem_new,
+                                                 h, cap, lo_, main));
+                if (next) {
+                    GatherPlan plan;
+                    TGM_TRY_STATUS(fetch_plan(st, i0 + k + 1, next->nodes, next->n_nodes, cap,
+                                              fb->mem, fb->mem_ts, fb->mail, fb->mail_ts,
+                                              fb->ver, main, &plan));
+                    TGM_TRY_STATUS(launch_gather(plan, main));
+                }
+            }
             // per-iteration copies of the embeddings and new memories
             if (h_trace && b > 0)
                 TGM_HIP(hipMemcpyAsync(h_trace + (size_t)k * 3 * B * m->M, h,

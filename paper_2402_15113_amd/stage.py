@@ -43,11 +43,13 @@ class _Sample:
 
 class Stage:
     def __init__(self, N, src, dst, t, neg, efeat, weights, *, M, D_t, H, nb, B, s,
-                 device="cuda", stream=None, mitigation=None):
+                 device="cuda", stream=None, mitigation=None, training=None):
         """src, dst, t, neg: numpy or torch arrays of the event stream; efeat
         [E x D_e] fp32 or None; weights a ``workloads.Weights``;
         ``mitigation=dict(p=.., lam=.., K=..)`` turns on the similarity-based
-        staleness mitigation (Sec. 3.3) of every fetch."""
+        staleness mitigation (Sec. 3.3) of every fetch;
+        ``training=dict(predictor=P, opt="adam"|"sgd", lr=..)`` adds the
+        training step (loss, gradient, optimizer) after every iteration."""
         dev = torch.device(device)
         self.dev = dev
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
@@ -87,6 +89,16 @@ class Stage:
         if mitigation is not None:
             self.mit = tgm.tgm_mitigator_create(self.cap, nb, int(mitigation["K"]))
             tgm.tgm_state_set_mitigation(self.st, self.mit, mitigation["p"], mitigation["lam"])
+        self.tr = None
+        self.training = training
+        if training is not None:
+            kw = {k: training[k] for k in ("opt", "lr", "beta1", "beta2", "eps") if k in training}
+            self.tr = tgm.tgm_trainer_create(self.m, weights, training["predictor"], stream=st,
+                                             **kw)
+            self.n_params, self.param_sizes, _ = tgm.tgm_trainer_info(self.tr)
+            self.loss = z(1, torch.float32)
+            self.loss_log = z(self.n_iters, torch.float32)
+            tgm.tgm_state_set_training(self.st, self.tr, self.loss_log)
         self.last = None      # (iteration, batch size) of the last issued iteration
         self._set = 0         # its sample buffer set
         self._bufs = None
@@ -97,7 +109,8 @@ class Stage:
         raise AttributeError(name)
 
     def close(self):
-        for fn, h in ((tgm.tgm_model_destroy, "m"), (tgm.tgm_state_destroy, "st"),
+        for fn, h in ((tgm.tgm_trainer_destroy, "tr"), (tgm.tgm_model_destroy, "m"),
+                      (tgm.tgm_state_destroy, "st"),
                       (tgm.tgm_mitigator_destroy, "mit"), (tgm.tgm_graph_destroy, "g")):
             if self.__dict__.get(h) is not None:
                 fn(self.__dict__[h])
@@ -138,7 +151,30 @@ class Stage:
             tgm.tgm_embed(self.m, self.g, 3 * n, self.nb, b.root_pos, b.root_ts, b.nbr_pos,
                           b.eid, b.nts, b.cnt, self.mem_new, b.n_nodes, self.cap, self.h,
                           stream=st)
+        if self.tr is not None:
+            sb, fb = self._structs()
+            tgm.tgm_train_step(self.tr, self.m, self.g, n, sb[0], fb, self.mem_new, self.h,
+                               self.cap, loss=self.loss_log[i:i + 1], stream=st)
         self.last, self._set = (i, n), 0
+
+    def _structs(self):
+        if self._bufs is None:
+            sb = (tgm.SampleBuffers * len(self.sets))(
+                *[tgm.buffers(tgm.SampleBuffers, **vars(b)) for b in self.sets])
+            fb = tgm.buffers(tgm.FetchBuffers, mem=self.f_mem, mem_ts=self.f_mem_ts,
+                             mail=self.f_mail, mail_ts=self.f_mail_ts, ver=self.f_ver)
+            self._bufs = (sb, fb)
+        return self._bufs
+
+    def train_state(self):
+        """Host copies of the trainer's parameter vector, the gradient of the
+        last step and the per-iteration losses so far (synchronises)."""
+        params = torch.empty(self.n_params, dtype=torch.float32, device=self.dev)
+        grad = torch.empty_like(params)
+        tgm.tgm_trainer_read(self.tr, params, grad, stream=self.stream)
+        torch.cuda.synchronize(self.dev)
+        return dict(params=params.cpu().numpy(), grad=grad.cpu().numpy(),
+                    loss=self.loss_log.cpu().numpy())
 
     def run(self, i0: int, n: int, trace: bool = False):
         """Enqueue iterations i0 .. i0+n-1 through the library's pipelined
@@ -148,13 +184,7 @@ class Stage:
         holding every iteration's embeddings and new memories."""
         if n <= 0:
             return None
-        if self._bufs is None:
-            sb = (tgm.SampleBuffers * len(self.sets))(
-                *[tgm.buffers(tgm.SampleBuffers, **vars(b)) for b in self.sets])
-            fb = tgm.buffers(tgm.FetchBuffers, mem=self.f_mem, mem_ts=self.f_mem_ts,
-                             mail=self.f_mail, mail_ts=self.f_mail_ts, ver=self.f_ver)
-            self._bufs = (sb, fb)
-        sb, fb = self._bufs
+        sb, fb = self._structs()
         h_tr = s_tr = None
         if trace:
             h_tr = torch.zeros((n, 3 * self.B, self.M), dtype=torch.float32, device=self.dev)
@@ -238,10 +268,11 @@ class Stage:
         tgm.tgm_state_restore(self.st, buf, stream=self.stream)
 
 
-def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None) -> Stage:
+def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None,
+                  training=None) -> Stage:
     return Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, wl.efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
                  nb=wl.nb, B=wl.B, s=wl.s if s is None else s, device=device, stream=stream,
-                 mitigation=mitigation)
+                 mitigation=mitigation, training=training)
 
 
 # ------------------------------------------------------- staleness bound

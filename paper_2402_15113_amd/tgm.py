@@ -29,7 +29,8 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_alloc_
            "tgm_model_create", "tgm_model_destroy", "tgm_update_memory", "tgm_embed",
            "tgm_stage_run", "tgm_mitigator_create", "tgm_mitigator_destroy", "tgm_mitigate",
            "tgm_mitigator_read", "tgm_state_set_mitigation", "tgm_min_staleness",
-           "tgm_mitigate_noalloc",
+           "tgm_mitigate_noalloc", "tgm_trainer_create", "tgm_trainer_destroy",
+           "tgm_trainer_info", "tgm_trainer_read", "tgm_train_step", "tgm_state_set_training",
            "tgm_embed_projection",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
@@ -69,6 +70,20 @@ class Weights(C.Structure):
                 ("W_q", _fp), ("b_q", _fp), ("W_k", _fp), ("b_k", _fp), ("W_v", _fp),
                 ("b_v", _fp), ("W_o", _fp), ("b_o", _fp), ("w_t", _fp)]
 
+
+class Predictor(C.Structure):
+    _fields_ = [("W_src", _fp), ("W_dst", _fp), ("b_p", _fp), ("w_out", _fp),
+                ("b_out", C.c_float)]
+
+
+class Optimizer(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("lr", C.c_float), ("beta1", C.c_float),
+                ("beta2", C.c_float), ("eps", C.c_float)]
+
+
+TGM_OPT_SGD, TGM_OPT_ADAM = 0, 1
+OPTIMIZERS = {"sgd": TGM_OPT_SGD, "adam": TGM_OPT_ADAM}
+N_PARAM_TENSORS = 17   # TGM_N_PARAM_TENSORS
 
 _lib = None
 V, I32, I64, P = C.c_void_p, C.c_int32, C.c_int64, C.c_void_p
@@ -113,6 +128,14 @@ def lib():
             "tgm_stage_run": [V, V, V, I64, I64, I32, I32, I32, C.POINTER(SampleBuffers), I32,
                               C.POINTER(FetchBuffers), P, P, P, P, P, P, V, V],
             "tgm_alloc_count": [C.POINTER(I64)],
+            "tgm_trainer_create": [V, C.POINTER(Weights), C.POINTER(Predictor),
+                                   C.POINTER(Optimizer), V, C.POINTER(V)],
+            "tgm_trainer_destroy": [V],
+            "tgm_trainer_info": [V, C.POINTER(I64), C.POINTER(I64), C.POINTER(I64)],
+            "tgm_trainer_read": [V, P, P, P, V],
+            "tgm_train_step": [V, V, V, I32, C.POINTER(SampleBuffers), C.POINTER(FetchBuffers),
+                               P, P, I32, P, V],
+            "tgm_state_set_training": [V, V, P, I64],
             "tgm_mitigator_create": [I32, I32, I32, C.POINTER(V)],
             "tgm_mitigator_destroy": [V],
             "tgm_mitigate": [V, V, I64, P, P, I32, P, P, I32, C.c_double, C.c_float, V],
@@ -372,6 +395,70 @@ def tgm_min_staleness(tau, n, k_max):
 
 
 # ------------------------------------------------------------------ model
+def _weights_struct(w, keep):
+    def arr(name, dt):
+        v = getattr(w, name, None)
+        if v is None:
+            return None
+        a = np.ascontiguousarray(v, dtype=dt)
+        keep[name] = a
+        return a.ctypes.data_as(_fp if dt == np.float32 else _dp)
+
+    ws = Weights()
+    for name in ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v",
+                 "W_o", "b_o", "w_t"):
+        setattr(ws, name, arr(name, np.float32))
+    ws.omega = arr("omega", np.float64)
+    ws.beta = arr("beta", np.float64)
+    return ws
+
+
+def tgm_trainer_create(m, w, pred, opt="adam", lr=1e-4, beta1=0.9, beta2=0.999, eps=1e-8,
+                       stream=None):
+    """``w`` the model's numpy weights (workloads.Weights), ``pred`` a
+    workloads.Predictor."""
+    keep = {}
+    ws = _weights_struct(w, keep)
+    pa = {k: np.ascontiguousarray(getattr(pred, k), dtype=np.float32)
+          for k in ("W_src", "W_dst", "b_p", "w_out")}
+    ps = Predictor(*[pa[k].ctypes.data_as(_fp) for k in ("W_src", "W_dst", "b_p", "w_out")],
+                   float(pred.b_out))
+    os_ = Optimizer(OPTIMIZERS[opt], float(lr), float(beta1), float(beta2), float(eps))
+    h = V()
+    _check("tgm_trainer_create", lib().tgm_trainer_create(m, C.byref(ws), C.byref(ps),
+                                                          C.byref(os_), _s(stream), C.byref(h)))
+    return h
+
+
+def tgm_trainer_destroy(tr):
+    _check("tgm_trainer_destroy", lib().tgm_trainer_destroy(tr))
+
+
+def tgm_trainer_info(tr):
+    """(n_params, [sizes of the 17 tensors], optimizer steps taken)."""
+    n, st = I64(), I64()
+    sz = (I64 * N_PARAM_TENSORS)()
+    _check("tgm_trainer_info", lib().tgm_trainer_info(tr, C.byref(n), sz, C.byref(st)))
+    return int(n.value), [int(x) for x in sz], int(st.value)
+
+
+def tgm_trainer_read(tr, params=None, grad=None, loss=None, stream=None):
+    _check("tgm_trainer_read", lib().tgm_trainer_read(tr, _p(params), _p(grad), _p(loss),
+                                                      _s(stream)))
+
+
+def tgm_train_step(tr, m, g, b, sample_bufs, fetch_bufs, mem_new, h, cap, loss=None,
+                   stream=None):
+    _check("tgm_train_step", lib().tgm_train_step(tr, m, g, b, C.byref(sample_bufs),
+                                                  C.byref(fetch_bufs), _p(mem_new), _p(h), cap,
+                                                  _p(loss), _s(stream)))
+
+
+def tgm_state_set_training(st, tr, loss_log=None):
+    n = 0 if loss_log is None else int(loss_log.numel())
+    _check("tgm_state_set_training", lib().tgm_state_set_training(st, tr, _p(loss_log), n))
+
+
 def tgm_model_create(M, D_e, D_t, H, nb, max_nodes, max_roots, w, stream=None):
     """``w`` holds numpy weights (fp32; omega and beta fp64), see workloads.Weights."""
     kind = MODEL_KINDS[getattr(w, "kind", "tgn")]

@@ -1,0 +1,242 @@
+"""The training step on the GPU (tgm_train_step; tgm_stage_run with a
+trainer) against the fp64 oracle's, iteration by iteration: the loss, the
+gradient of every parameter, the parameters after the optimizer step, and
+the stage's own outputs, which after the first step run with the trained
+weights.
+
+Tolerances.  Forward values and parameters: 1e-5 + 1e-4 |oracle| (the
+stage's fp32-vs-fp64 bound).  Gradients, per tensor:
+* b_k's gradient is exactly zero (adding the same vector to every key of a
+  root shifts all its scores of a head by the same amount, which the softmax
+  ignores); the GPU's must stay below 1e-5 of the largest W_k gradient, and
+  the oracle's below 1e-12 of it;
+* the ReLU derivative jumps at zero: a pre-activation (the predictor's z or
+  the output projection's) within the fp32 error of zero (about 1e-7 here)
+  can take the other branch on the GPU.  Every element must satisfy
+  |g - o| <= 1e-4 |o| + 1e-4 max|o| (each element is a sum over slots, roots
+  or nodes that may cancel, so its error is bounded by the tensor's scale),
+  except in an iteration whose smallest |pre-activation| (the oracle reports
+  it) is below 1e-6: there one branch may differ, one term of each affected
+  sum with it, and the bound is ||g - o|| <= 1e-2 ||o|| (Frobenius).  At
+  least three quarters of the iterations of a run must pass element-wise.
+Adam runs use eps = 1e-6: Adam divides each step by the coordinate's own
+gradient scale, so with eps = 1e-8 a coordinate whose gradient lies within
+fp32 noise of zero could step by up to lr either way; with 1e-6, gradient
+noise of 1e-9 moves a parameter by at most lr / 1000.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+from workloads import make_predictor, make_weights, make_workload  # noqa: E402
+
+PARAM_NAMES = ("W_ih", "W_hh", "b_ih", "b_hh", "W_q", "b_q", "W_k", "b_k", "W_v", "b_v", "W_o",
+               "b_o", "W_src", "W_dst", "b_p", "w_out", "b_out")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2402_15113_amd import tgm
+    tgm.lib()
+
+
+def split(vec, sizes):
+    out, o = {}, 0
+    for name, n in zip(PARAM_NAMES, sizes):
+        out[name] = np.asarray(vec[o:o + n], np.float64)
+        o += n
+    return out
+
+
+RELU_TAU = 1e-6
+
+
+def grad_check(gg, og, margin, stats):
+    """gg, og: {name: flat gradient} of the GPU and the oracle."""
+    wk = np.abs(og["W_k"]).max()
+    assert np.abs(og["b_k"]).max() <= 1e-12 * wk, "oracle: b_k's gradient is not zero"
+    assert np.abs(gg["b_k"]).max() <= 1e-5 * wk, ("b_k", np.abs(gg["b_k"]).max(), wk)
+    strict = True
+    for k in PARAM_NAMES:
+        if k == "b_k":
+            continue
+        g, o = np.asarray(gg[k], np.float64), np.asarray(og[k], np.float64)
+        if not np.any(o) and not np.any(g):
+            continue
+        fro = float(np.linalg.norm(g - o) / max(np.linalg.norm(o), 1e-300))
+        stats[k] = max(stats.get(k, 0.0), fro)
+        err = np.abs(g - o)
+        tol = 1e-4 * np.abs(o) + 1e-4 * np.abs(o).max()
+        bad = err > tol
+        if not bad.any():
+            continue
+        j = int(np.argmax(err - tol))
+        msg = (f"grad {k}: {int(bad.sum())}/{bad.size} outside tolerance (margin {margin:.2e}); "
+               f"worst at {j}: gpu {g[j]!r} oracle {o[j]!r}; Frobenius {fro:.2e}")
+        assert margin < RELU_TAU, msg
+        assert fro <= 1e-2, msg
+        strict = False
+    key = "strict" if strict else "near_kink"
+    stats[key] = stats.get(key, 0) + 1
+
+
+def param_close(name, g, o):
+    from test_gpu_parity import close
+    close(name, g, o)
+
+
+def train_pair(orc, wl, w, P, n, *, s=None, opt="sgd", lr=1e-2, mitigation=None,
+               pipelined=False):
+    from paper_2402_15113_amd.stage import from_workload
+    from test_gpu_parity import close, compare_step
+    tr = dict(predictor=P, opt=opt, lr=lr, eps=1e-6)
+    st = from_workload(wl, w, s=s, mitigation=mitigation, training=tr)
+    o = orc.Oracle(wl, w, s=s, mitigation=mitigation, training=tr)
+    sizes = st.param_sizes
+    assert sizes == o.param_sizes()
+    stats = {}
+    print(f"[train] {wl.name} s={st.s} {opt} lr={lr} pipelined={pipelined} iters 0..{n - 1}",
+          flush=True)
+    if pipelined:
+        h_tr, s_tr = st.run(0, n, trace=True)
+        torch.cuda.synchronize()
+    for i in range(n):
+        if not pipelined:
+            st.step(i)
+        r = o.step()
+        if pipelined:
+            close(f"h[{i}]", h_tr[i, :r.R].cpu().numpy(), r.h)
+            close(f"s_new[{i}]", s_tr[i, :r.n_U].cpu().numpy(), r.s_new)
+            continue
+        # with the mitigation on, the fetch buffer holds the blended rows
+        compare_step(st.outputs(), r if mitigation is None else
+                     dataclasses.replace(r, f_mem=r.m_mem))
+        ts = st.train_state()
+        assert abs(ts["loss"][i] - r.loss) <= 1e-5 + 1e-4 * abs(r.loss), (i, ts["loss"][i],
+                                                                         r.loss)
+        gg, og = split(ts["grad"], sizes), o.split(r.grad)
+        grad_check(gg, og, r.relu_margin, stats)
+        gp, op = split(ts["params"], sizes), o.split(r.params)
+        for k in PARAM_NAMES:
+            param_close(f"param {k} [{i}]", gp[k], op[k])
+    ts = st.train_state()
+    losses = np.array([0.0] * n)
+    if pipelined:
+        o2 = orc.Oracle(wl, w, s=s, mitigation=mitigation, training=tr)
+        for i in range(n):
+            losses[i] = o2.step(want="light").loss
+        np.testing.assert_allclose(ts["loss"][:n], losses, rtol=1e-4, atol=1e-5)
+    gp, op = split(ts["params"], sizes), o.split(o.params())
+    for k in PARAM_NAMES:
+        param_close(f"final param {k}", gp[k], op[k])
+    st.flush()
+    o.flush()
+    from test_gpu_parity import compare_state
+    compare_state(st.state(), o.state())
+    st.close()
+    print(f"[train] iterations checked element-wise / near a kink, worst relative Frobenius "
+          f"error per tensor: {stats}", flush=True)
+    if not pipelined:
+        assert stats.get("strict", 0) >= 3 * stats.get("near_kink", 0), stats
+    return stats
+
+
+@pytest.mark.parametrize("s,opt,lr", [(0, "sgd", 1e-2), (2, "sgd", 1e-2), (2, "adam", 1e-4)])
+def test_train_tiny(orc, s, opt, lr):
+    wl = make_workload("tiny", E=6000, s=s)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random")
+    train_pair(orc, wl, w, make_predictor(wl.M, seed=1), wl.n_iters, s=s, opt=opt, lr=lr)
+
+
+def test_train_tie_heavy_odd_dims(orc):
+    from test_gpu_parity import tie_heavy
+    wl = tie_heavy(4, M=36, H=3, D_e=17, D_t=23, B=11, nb=10)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, seed=4, beta="random")
+    train_pair(orc, wl, w, make_predictor(wl.M, seed=2), wl.n_iters, s=wl.s)
+
+
+def test_train_lastfm_no_edge_features(orc):
+    wl = make_workload("lastfm", E=16 * 2000)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    train_pair(orc, wl, w, make_predictor(wl.M), 16, opt="adam", lr=1e-4)
+
+
+def test_train_wiki_window(orc):
+    wl = make_workload("wiki", E=24 * 600)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    train_pair(orc, wl, w, make_predictor(wl.M), 24, opt="sgd", lr=1e-2)
+
+
+def test_train_with_mitigation(orc):
+    wl = make_workload("tiny", E=6000, s=2)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    train_pair(orc, wl, w, make_predictor(wl.M), wl.n_iters, s=2,
+               mitigation=dict(p=0.8, lam=0.6, K=4))
+
+
+@pytest.mark.parametrize("name,E", [("tiny", 8000), ("wiki", 30_000)])
+def test_train_pipelined(orc, name, E):
+    """The executor with a trainer: every iteration's h and s' (which depend
+    on the weights trained so far), the loss log, the final parameters and
+    tables."""
+    wl = make_workload(name, E=E)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    train_pair(orc, wl, w, make_predictor(wl.M), wl.n_iters, opt="sgd", lr=1e-2, pipelined=True)
+
+
+def test_train_pipelined_equals_sequential():
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("wiki", E=20_000)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    tr = dict(predictor=make_predictor(wl.M), opt="adam", lr=1e-3)
+    a = from_workload(wl, w, training=tr)
+    a.run(0, wl.n_iters)
+    b = from_workload(wl, w, training=tr)
+    for i in range(wl.n_iters):
+        b.step(i)
+    ta, tb = a.train_state(), b.train_state()
+    for k in ta:
+        assert np.array_equal(ta[k], tb[k]), k
+    a.close()
+    b.close()
+
+
+def test_trainer_allocates_nothing_per_step():
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=4000, s=1)
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w, training=dict(predictor=make_predictor(wl.M)))
+    torch.cuda.synchronize()
+    before = tgm.alloc_count()
+    st.run(0, 8)
+    for i in range(8, 12):
+        st.step(i)
+    torch.cuda.synchronize()
+    assert tgm.alloc_count() == before
+    st.close()
+
+
+def test_trainer_argument_errors():
+    from paper_2402_15113_amd import tgm
+    from paper_2402_15113_amd.stage import from_workload
+    wl = make_workload("tiny", E=2000, s=1)
+    wj = make_weights(wl.M, wl.D_e, wl.D_t, model="jodie")
+    st = from_workload(wl, wj)
+    with pytest.raises(tgm.TgmError) as e:
+        tgm.tgm_trainer_create(st.m, wj, make_predictor(wl.M))
+    assert e.value.code == tgm.TGM_EINVAL
+    st.close()
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    st = from_workload(wl, w)
+    with pytest.raises(tgm.TgmError) as e:
+        tgm.tgm_trainer_create(st.m, w, make_predictor(wl.M), opt="adam", beta1=1.5)
+    assert e.value.code == tgm.TGM_EINVAL
+    st.close()

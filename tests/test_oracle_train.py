@@ -66,7 +66,8 @@ def _torch_iteration(wl, w, P, r):
     al = torch.softmax(sc, dim=1)
     al = torch.where(valid.any(dim=1)[:, None, None], al, torch.zeros_like(al))
     a = (al[..., None] * V.view(R, nb, H, dh)).sum(1).reshape(R, M)
-    h = torch.relu(torch.cat([a, sv], dim=1) @ prm["W_o"].T + prm["b_o"])
+    pre = torch.cat([a, sv], dim=1) @ prm["W_o"].T + prm["b_o"]
+    h = torch.relu(pre)
     b = r.b
     zp = h[:b] @ prm["W_src"].T + h[b:2 * b] @ prm["W_dst"].T + prm["b_p"]
     zn = h[:b] @ prm["W_src"].T + h[2 * b:] @ prm["W_dst"].T + prm["b_p"]
@@ -75,7 +76,7 @@ def _torch_iteration(wl, w, P, r):
     bce = torch.nn.functional.binary_cross_entropy_with_logits
     loss = bce(sp, torch.ones(b, dtype=torch.float64), reduction="sum") / b + \
         bce(sn, torch.zeros(b, dtype=torch.float64), reduction="sum") / b
-    return loss, prm, s_new, h
+    return loss, prm, s_new, h, pre
 
 
 @pytest.mark.parametrize("name,kw,s,first,mit", [
@@ -92,7 +93,7 @@ def test_gradient_equals_torch_autograd(orc, name, kw, s, first, mit):
     for _ in range(first):
         o.step(want="light")
     r = o.step()
-    loss, prm, s_new, h = _torch_iteration(wl, w, P, r)
+    loss, prm, s_new, h, _ = _torch_iteration(wl, w, P, r)
     np.testing.assert_allclose(s_new.detach().numpy(), r.s_new, rtol=0, atol=1e-12)
     np.testing.assert_allclose(h.detach().numpy(), r.h, rtol=0, atol=1e-12)
     assert abs(loss.item() - r.loss) < 1e-12
@@ -196,3 +197,23 @@ def test_sgd_and_adam_steps(orc):
         # the next iteration runs with the new weights
         r2 = o.step()
         assert not np.array_equal(r2.params, r.params)
+
+
+def test_relu_margin_is_the_smallest_pre_activation(orc):
+    """The reported margin equals the smallest |z| of the predictor and |o| of
+    the output projection, recomputed here from the torch forward."""
+    wl = make_workload("tiny", E=3000, s=1)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random")
+    P = make_predictor(wl.M, seed=3)
+    o = _oracle(orc, wl, w, P, s=1)
+    for _ in range(5):
+        o.step(want="light")
+    r = o.step()
+    _, prm, s_new, h, pre = _torch_iteration(wl, w, P, r)
+    b = r.b
+    with torch.no_grad():
+        hh = torch.tensor(r.h)
+        zp = hh[:b] @ prm["W_src"].T + hh[b:2 * b] @ prm["W_dst"].T + prm["b_p"]
+        zn = hh[:b] @ prm["W_src"].T + hh[2 * b:] @ prm["W_dst"].T + prm["b_p"]
+    m = min(zp.abs().min().item(), zn.abs().min().item(), pre.detach().abs().min().item())
+    assert abs(r.relu_margin - m) <= 1e-12 * max(m, 1e-300) + 1e-15
