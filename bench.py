@@ -188,7 +188,7 @@ def fill_features(efeat, wl, lo, hi, threads):
     return time.perf_counter() - t0
 
 
-def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu"):
+def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu", training=None):
     """Stage over the whole stream of a large workload for the window of
     batches first .. first + L - 1.
 
@@ -212,7 +212,7 @@ def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu"):
     E_end = min(wl.E, (first + L) * wl.B)
     efeat = torch.empty((wl.E, wl.D_e), dtype=torch.float32, device="cuda")
     stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
-                  nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation)
+                  nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation, training=training)
     stage._efeat_keep = efeat
     if state == "gpu":
         lo_row, hi_row = 0, wl.E
@@ -230,7 +230,11 @@ def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu"):
     if state == "gpu":
         tp = time.perf_counter()
         stage.want_winner = False
+        if training is not None:   # the state is the forward stage's; training starts at first
+            stage.set_training(False)
         stage.run(0, first)
+        if training is not None:
+            stage.set_training(True)
         torch.cuda.synchronize()
         init = {"checkpoint": stage.save_checkpoint()}
         log(f"state: GPU ran batches 0..{first - 1} in {time.perf_counter() - tp:.1f} s")
@@ -300,6 +304,36 @@ def work_model(wl, rows, model="tgn"):
     k["k_attn_fold"] = dict(k["k_attn"])
     k["k_attn_fold_gather"] = dict(k["k_attn_gather"])
     return k
+
+
+def train_work_model(wl, rows):
+    """Algorithmic flops per launch of the training step's GEMMs (k_gemm, all
+    shapes of one step averaged over its launches) and bytes of its
+    element-wise kernels.  Useful work only: valid slots (S), nodes with mail
+    (n_mail); the GEMMs also run over the empty slots and rows without mail,
+    which are zero."""
+    M, D_e, D_t, nb = wl.M, wl.D_e, wl.D_t, wl.nb
+    D_x, Dq, Dkv = wl.D_m + D_t, M + D_t, M + D_e + D_t
+    n = len(rows)
+    avg = lambda key: sum(r[key] for r in rows) / n
+    S, R, n_mail, b = avg("slots"), avg("R"), avg("n_mail"), avg("b")
+    f = 4
+    gemms = [  # (m, n, k) of every GEMM of one step
+        (b, M, M), (2 * b, M, M),                                  # predictor forward
+        (1, M, 2 * b), (1, 1, 2 * b), (1, M, b), (M, M, b), (M, M, 2 * b),
+        (b, M, M), (2 * b, M, M),                                  # predictor backward, dh
+        (R, M, Dq), (S, M, Dkv), (S, M, Dkv), (R, M, 2 * M),       # attention again
+        (M, 2 * M, R), (1, M, R), (R, 2 * M, M),                   # output projection
+        (M, Dkv, S), (M, Dkv, S), (1, M, S), (1, M, S), (M, Dq, R), (1, M, R),
+        (S, M, M), (S, M, M), (R, M, M),                           # dK, dV, dq; ds
+        (n_mail, 3 * M, D_x), (n_mail, 3 * M, M),                  # GRU gates again
+        (3 * M, D_x, n_mail), (3 * M, M, n_mail), (1, 3 * M, n_mail), (1, 3 * M, n_mail)]
+    flops = sum(2.0 * m_ * n_ * k_ for m_, n_, k_ in gemms)
+    byts = sum(f * (m_ * k_ + k_ * n_ + m_ * n_) for m_, n_, k_ in gemms)
+    L = len(gemms)
+    return {"k_gemm": dict(flops=flops / L, bytes=byts / L),
+            "k_att_rows": dict(flops=0, bytes=R * Dq * f * 2 + S * Dkv * f * 2),
+            "k_adam": dict(flops=0, bytes=0)}
 
 
 CSRC = ("common.h", "api.hip", "graph.hip", "state.hip", "model.hip", "runner.hip")
@@ -389,7 +423,7 @@ def oracle_timed(make, seconds, max_batches, threads):
     return events / dt, used, nb, events, dt
 
 
-def cpu_baseline(wl, w, W, seconds):
+def cpu_baseline(wl, w, W, seconds, training=None):
     """The fp64 oracle over the same stream from batch W on (the state it
     reaches after W batches is built untimed): single-threaded (the primary
     figure), then on every host core."""
@@ -397,7 +431,7 @@ def cpu_baseline(wl, w, W, seconds):
     oracle.build(force=False)
 
     def make():
-        o = oracle.Oracle(wl, w)
+        o = oracle.Oracle(wl, w, training=training)
         for _ in range(W):
             o.step(want="light")
         return o
@@ -413,7 +447,7 @@ def cpu_baseline(wl, w, W, seconds):
             "cpu_model": cpu_model()}
 
 
-def cpu_baseline_window(wl, w, first, seconds, mitigation=None):
+def cpu_baseline_window(wl, w, first, seconds, mitigation=None, training=None):
     """The fp64 oracle on a bounded sample of the same window: batches first,
     first + 1, ... from the seeded synthetic state at `first` (the oracle takes
     no input from the GPU), on the graph of the events through the sample's
@@ -456,7 +490,7 @@ def cpu_baseline_window(wl, w, first, seconds, mitigation=None):
     init = synthetic_state(pre, first, pre.t[lo_row - 1] if lo_row > 0 else 0.0)
 
     def make():
-        o = oracle.Oracle(pre, w, mitigation=mitigation)
+        o = oracle.Oracle(pre, w, mitigation=mitigation, training=training)
         o.set_state(first, **init)
         return o
 
@@ -496,6 +530,9 @@ def main():
                     help="s of the run: the workload's (config), a number, or auto: the "
                          "minimal staleness (Sec. 3.2) solved from stage times profiled on a "
                          "calibration stage of its own before the run")
+    ap.add_argument("--train", action="store_true",
+                    help="add the training step to every iteration (link-prediction loss, "
+                         "backward through attention and the GRU, Adam with lr 1e-4)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
@@ -529,19 +566,26 @@ def main():
     if args.mitigate:
         pq, lam, kk = args.mitigate.split(",")
         mit = dict(p=float(pq), lam=float(lam), K=int(kk))
+    training = None
+
     def build(s):
+        nonlocal training
+        if args.train:
+            from workloads import CONFIGS, make_predictor
+            training = dict(predictor=make_predictor(CONFIGS[args.workload]["M"]), opt="adam",
+                            lr=1e-4)
         if window:
             from workloads import CONFIGS
             c = CONFIGS["gdelt"]
             w = make_weights(c["M"], c["D_e"], c["D_t"], model=args.model)
             wl, stage, init, wmeta = window_setup("gdelt", args.first, W + K, w, mit, s=s,
-                                                  state=args.state)
+                                                  state=args.state, training=training)
             sched = Schedule(stage, args.first + W + K, first=args.first, init=init)
             sched.meta = wmeta
         else:
             wl = make_workload(args.workload, s=s)
             w = make_weights(wl.M, wl.D_e, wl.D_t, model=args.model)
-            stage = from_workload(wl, w, mitigation=mit)
+            stage = from_workload(wl, w, mitigation=mit, training=training)
             sched = Schedule(stage, wl.n_iters)
         sched.restart()
         return wl, w, stage, sched
@@ -600,6 +644,12 @@ def main():
         out["config"]["mitigation"] = dict(mit, kind="MSPipe-S similarity-based, every fetch")
     if args.model != "tgn":
         out["config"]["model_family"] = "JODIE: RNN memory updater, time-projection embedding"
+    if args.train:
+        out["metric"] = "training events/sec (stage + link-prediction loss + backward + Adam)"
+        out["config"]["training"] = {"predictor": "two-layer perceptron over the endpoint "
+                                                  "embeddings", "loss": "binary cross-entropy, "
+                                     "b positive and b negative pairs", "optimizer": "Adam",
+                                     "lr": 1e-4}
 
     if not args.no_profile:
         # pass 2: per-kernel durations (HIP events on the launch stream)
@@ -615,12 +665,14 @@ def main():
         tgm.tgm_profile_enable(False)
         prof = {}
         for name, (launches, ms) in tgm.tgm_profile_read().items():
-            base = name.split("<")[0]   # template instances count as their kernel
+            base = name.split("<")[0].lstrip("(")   # template instances count as their kernel
             n0, m0 = prof.get(base, (0, 0.0))
             prof[base] = (n0 + launches, m0 + ms)
         # pass 3: algorithmic work per launch, and the sequential stage times
         rows, seq = account(sched, W, K)
         work = work_model(wl, rows, args.model)
+        if args.train:
+            work.update(train_work_model(wl, rows))
         kernels = {}
         for name, (launches, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
             avg_s = ms / launches * 1e-3
@@ -669,9 +721,9 @@ def main():
         log(f"oracle baseline ({args.cpu_seconds:.0f} s budget)")
         if window:
             out["cpu_baseline"] = cpu_baseline_window(wl, w, args.first + W, args.cpu_seconds,
-                                                      mit)
+                                                      mit, training)
         else:
-            out["cpu_baseline"] = cpu_baseline(wl, w, W, args.cpu_seconds)
+            out["cpu_baseline"] = cpu_baseline(wl, w, W, args.cpu_seconds, training)
     print(json.dumps(out), flush=True)
 
 

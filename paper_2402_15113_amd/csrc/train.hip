@@ -463,27 +463,76 @@ __global__ __launch_bounds__(256) void k_ds_bounds(int64_t n, const uint64_t *__
         seg_end[p] = (int32_t)(i + 1);
 }
 
-// One wavefront per node p < n_nodes: ds[p] = the sum, in contributor order,
-// of dXq[r] + dXo[r][M:2M] over its roots and of dKm[sl] over its slots.
-__global__ __launch_bounds__(256) void k_ds(const int32_t *__restrict__ n_nodes, int32_t cap,
-                                            int M, int R, int64_t n_items,
-                                            const uint64_t *__restrict__ keys,
-                                            const int32_t *__restrict__ seg,
-                                            const int32_t *__restrict__ seg_end,
-                                            const float *__restrict__ dXq,
-                                            const float *__restrict__ dXo,
-                                            const float *__restrict__ dKm, float *__restrict__ ds)
+// The sum runs in fixed chunks of kDsChunk contributors so that nodes with
+// many contributors (hubs) spread over many wavefronts.  k_ds_chunks counts
+// each node's chunks and scans the counts (one workgroup: chunk_off[p] is the
+// first chunk of node p, chunk_off[cap] the total); k_ds_partial sums one
+// chunk per wavefront iteration (a grid-stride loop over the chunks); k_ds
+// adds each node's chunk sums in order.  ds[p] is, in contributor order, the
+// sum of dXq[r] + dXo[r][M:2M] over its roots and of dKm[sl] over its slots.
+constexpr int kDsChunk = 64;
+constexpr int kDsScanThreads = 1024;
+
+__global__ __launch_bounds__(kDsScanThreads) void k_ds_chunks(const int32_t *__restrict__ n_nodes,
+                                                              int32_t cap,
+                                                              const int32_t *__restrict__ seg,
+                                                              const int32_t *__restrict__ seg_end,
+                                                              int32_t *__restrict__ chunk_off)
 {
-    const int p = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
+    __shared__ int32_t s_sum[kDsScanThreads];
+    const int n = min(*n_nodes, cap), tid = threadIdx.x;
+    // each thread takes a contiguous run of nodes
+    const int per = (cap + kDsScanThreads - 1) / kDsScanThreads;
+    const int p0 = tid * per, p1 = min(cap, p0 + per);
+    auto chunks = [&](int p) {
+        return p < n ? (max(seg_end[p] - seg[p], 0) + kDsChunk - 1) / kDsChunk : 0;
+    };
+    int32_t local = 0;
+    for (int p = p0; p < p1; ++p)
+        local += chunks(p);
+    s_sum[tid] = local;
+    __syncthreads();
+    for (int o = 1; o < kDsScanThreads; o <<= 1) {   // inclusive scan (Hillis-Steele)
+        const int32_t v = tid >= o ? s_sum[tid - o] : 0;
+        __syncthreads();
+        s_sum[tid] += v;
+        __syncthreads();
+    }
+    int32_t run = s_sum[tid] - local;
+    for (int p = p0; p < p1; ++p) {
+        chunk_off[p] = run;
+        run += chunks(p);
+    }
+    if (tid == kDsScanThreads - 1)
+        chunk_off[cap] = s_sum[tid];
+}
+
+__global__ __launch_bounds__(256) void k_ds_partial(int32_t cap, int M, int R, int64_t n_items,
+                                                    const uint64_t *__restrict__ keys,
+                                                    const int32_t *__restrict__ seg,
+                                                    const int32_t *__restrict__ seg_end,
+                                                    const int32_t *__restrict__ chunk_off,
+                                                    const float *__restrict__ dXq,
+                                                    const float *__restrict__ dXo,
+                                                    const float *__restrict__ dKm,
+                                                    float *__restrict__ part)
+{
     const int lane = threadIdx.x & 63;
-    const int n = min(*n_nodes, cap);
-    if (p >= cap)
-        return;
-    float acc[2] = {0.f, 0.f};
-    if (p < n) {
-        // every node of the set is a root or a neighbour, so its segment was
-        // just written; the clamps keep a malformed node set in bounds
-        const int64_t i0 = max(seg[p], 0), i1 = min((int64_t)seg_end[p], n_items);
+    const int64_t nw = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    const int32_t total = chunk_off[cap];
+    for (int64_t t = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6; t < total; t += nw) {
+        int lo = 0, hi = cap;   // the node p with chunk_off[p] <= t < chunk_off[p + 1]
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (chunk_off[mid] <= t)
+                lo = mid;
+            else
+                hi = mid;
+        }
+        const int p = lo;
+        const int64_t i0 = max((int64_t)seg[p], (int64_t)0) + (t - chunk_off[p]) * kDsChunk;
+        const int64_t i1 = min(min((int64_t)seg_end[p], i0 + kDsChunk), n_items);
+        float acc[2] = {0.f, 0.f};
         for (int64_t i = i0; i < i1; ++i) {
             const int64_t c = (int64_t)(keys[i] & 0xffffffffu);
             if (c >= n_items)
@@ -497,7 +546,33 @@ __global__ __launch_bounds__(256) void k_ds(const int32_t *__restrict__ n_nodes,
                                 : dKm[(c - R) * M + k];
             }
         }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int k = lane + 64 * u;
+            if (k < M)
+                part[t * M + k] = acc[u];
+        }
     }
+}
+
+__global__ __launch_bounds__(256) void k_ds(const int32_t *__restrict__ n_nodes, int32_t cap,
+                                            int M, const int32_t *__restrict__ chunk_off,
+                                            const float *__restrict__ part, float *__restrict__ ds)
+{
+    const int p = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    if (p >= cap)
+        return;
+    const int n = min(*n_nodes, cap);
+    float acc[2] = {0.f, 0.f};
+    if (p < n)
+        for (int32_t t = chunk_off[p]; t < chunk_off[p + 1]; ++t)
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int k = lane + 64 * u;
+                if (k < M)
+                    acc[u] += part[(int64_t)t * M + k];
+            }
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
         const int k = lane + 64 * u;
@@ -640,7 +715,8 @@ struct tgm_trainer {
     float *X = nullptr, *Hm = nullptr, *Gx = nullptr, *Gh = nullptr, *dGx = nullptr,
           *dGh = nullptr;
     uint64_t *keys = nullptr, *keys_sorted = nullptr;
-    int32_t *seg = nullptr, *seg_end = nullptr;
+    int32_t *seg = nullptr, *seg_end = nullptr, *chunk_off = nullptr;
+    float *ds_part = nullptr;   // [(R + S) / kDsChunk + max_nodes] x M chunk sums
     void *sort_tmp = nullptr;
     size_t sort_bytes = 0;
     float *p(int k) const { return theta + off[k]; }
@@ -722,6 +798,8 @@ extern "C" tgm_status_t tgm_trainer_destroy(tgm_trainer_t tr)
     (void)hipFree(tr->keys_sorted);
     (void)hipFree(tr->seg);
     (void)hipFree(tr->seg_end);
+    (void)hipFree(tr->chunk_off);
+    (void)hipFree(tr->ds_part);
     (void)hipFree(tr->sort_tmp);
     delete tr;
     return TGM_OK;
@@ -825,6 +903,8 @@ extern "C" tgm_status_t tgm_trainer_create(tgm_model_t m, const tgm_weights *w,
     alloc(&tr->keys_sorted, n_items);
     alloc(&tr->seg, C);
     alloc(&tr->seg_end, C);
+    alloc(&tr->chunk_off, C + 1);
+    alloc(&tr->ds_part, (n_items / kDsChunk + C + 1) * M);
     if (st == TGM_OK) {
         size_t bytes = 0;
         if (hipcub::DeviceRadixSort::SortKeys(nullptr, bytes, tr->keys, tr->keys_sorted,
@@ -997,9 +1077,12 @@ tgm_status_t tgm::train_step_launch(tgm_trainer_t tr, tgm_model_t m, tgm_graph_t
                                               tr->keys_sorted, (int)n_items, 0, 64, s));
     TGM_LAUNCH(k_ds_bounds, dim3((unsigned)cdiv(n_items, 256)), dim3(256), 0, s, n_items,
                tr->keys_sorted, cap, tr->seg, tr->seg_end);
+    TGM_LAUNCH(k_ds_chunks, dim3(1), dim3(kDsScanThreads), 0, s, sb.n_nodes, cap, tr->seg,
+               tr->seg_end, tr->chunk_off);
+    TGM_LAUNCH(k_ds_partial, dim3(2048), dim3(256), 0, s, cap, M, R, n_items, tr->keys_sorted,
+               tr->seg, tr->seg_end, tr->chunk_off, tr->dXq, tr->dXo, tr->dKm, tr->ds_part);
     TGM_LAUNCH(k_ds, dim3((unsigned)cdiv((int64_t)cap * kWave, 256)), dim3(256), 0, s,
-               sb.n_nodes, cap, M, R, n_items, tr->keys_sorted, tr->seg, tr->seg_end, tr->dXq, tr->dXo,
-               tr->dKm, tr->ds);
+               sb.n_nodes, cap, M, tr->chunk_off, tr->ds_part, tr->ds);
 
     // memory updater (GRU) backward
     GruRowArgs gra{sb.n_nodes, cap, M, tr->D_m, tr->D_t, fb.mem, fb.mail, fb.mem_ts, fb.mail_ts,

@@ -151,11 +151,19 @@ class Stage:
             tgm.tgm_embed(self.m, self.g, 3 * n, self.nb, b.root_pos, b.root_ts, b.nbr_pos,
                           b.eid, b.nts, b.cnt, self.mem_new, b.n_nodes, self.cap, self.h,
                           stream=st)
-        if self.tr is not None:
+        if self.tr is not None and not getattr(self, "_train_off", False):
             sb, fb = self._structs()
             tgm.tgm_train_step(self.tr, self.m, self.g, n, sb[0], fb, self.mem_new, self.h,
                                self.cap, loss=self.loss_log[i:i + 1], stream=st)
         self.last, self._set = (i, n), 0
+
+    def set_training(self, on: bool):
+        """Turns the training step after every iteration on or off (a stage
+        made with ``training``)."""
+        assert self.tr is not None, "the stage was made without training"
+        self._train_off = not on
+        tgm.tgm_state_set_training(self.st, self.tr if on else None,
+                                   self.loss_log if on else None)
 
     def _structs(self):
         if self._bufs is None:
@@ -292,7 +300,7 @@ def stage_durations_us(profile: dict, iters: int) -> list:
     their kernel) taken over `iters` sequential steps."""
     folded = {}
     for name, (launches, ms) in profile.items():
-        base = name.split("<")[0]
+        base = name.split("<")[0].lstrip("(")
         n0, m0 = folded.get(base, (0, 0.0))
         folded[base] = (n0 + launches, m0 + ms)
     return [sum(folded.get(k, (0, 0.0))[1] for k in STAGE_KERNELS[j]) * 1e3 / iters
