@@ -49,9 +49,9 @@ class _Desc(C.Structure):
                 ("omega", _f64p), ("beta", _f64p),
                 ("W_q", _f32p), ("b_q", _f32p), ("W_k", _f32p), ("b_k", _f32p),
                 ("W_v", _f32p), ("b_v", _f32p), ("W_o", _f32p), ("b_o", _f32p),
-                ("kind", C.c_int), ("w_t", _f32p)]
+                ("kind", C.c_int), ("w_t", _f32p), ("K_mb", C.c_int), ("propagate", C.c_int)]
 
-KINDS = {"tgn": 0, "jodie": 1}
+KINDS = {"tgn": 0, "jodie": 1, "apan": 2}
 
 
 class _StepOut(C.Structure):
@@ -65,7 +65,8 @@ class _StepOut(C.Structure):
                 ("m_mem", _f64p), ("m_stale", _i32p), ("m_omega", _i32p), ("m_gamma", C.c_double),
                 ("m_n_stale", C.c_int32), ("m_pad", C.c_int32), ("x_mem", _f64p),
                 ("loss", C.c_double), ("grad", _f64p), ("params", _f64p),
-                ("relu_margin", C.c_double)]
+                ("relu_margin", C.c_double), ("f_mb", _f64p), ("f_mb_ts", _f64p),
+                ("f_mb_cnt", _i32p)]
 
 OPTIMIZERS = {"sgd": 0, "adam": 1}
 # the parameter vector's tensors, in order (orc_param_sizes)
@@ -113,6 +114,7 @@ def lib():
         L.orc_param_count.restype = C.c_int64
         L.orc_param_sizes.argtypes = [C.c_void_p, _i64p]
         L.orc_get_params.argtypes = [C.c_void_p, _f64p]
+        L.orc_get_mailbox.argtypes = [C.c_void_p, _f64p, _f64p, _i32p]
         L.orc_set_threads.argtypes = [C.c_int]
         L.orc_set_threads.restype = C.c_int
         _lib = L
@@ -266,6 +268,10 @@ class StepResult:
     params: np.ndarray | None = None
     # the smallest |pre-activation| of the ReLUs on the gradient's path
     relu_margin: float | None = None
+    # APAN: the fetched mailboxes, oldest mail first
+    f_mb: np.ndarray | None = None
+    f_mb_ts: np.ndarray | None = None
+    f_mb_cnt: np.ndarray | None = None
 
 
 class Oracle:
@@ -305,6 +311,9 @@ class Oracle:
             setattr(d, name, _p(keep(a, np.float32), _f32p) if a is not None else
                     C.cast(None, _f32p))
         d.kind = KINDS[getattr(w, "kind", "tgn")]
+        self.K_mb = int(getattr(w, "K_mb", 0) or 0)
+        d.K_mb = self.K_mb
+        d.propagate = 1 if getattr(w, "propagate", False) else 0
         d.omega = _p(keep(w.omega, np.float64), _f64p)
         d.beta = _p(keep(w.beta, np.float64), _f64p)
         self._desc = d
@@ -362,6 +371,10 @@ class Oracle:
                         m_omega=np.empty(N * K, np.int32))
         if self.n_params:
             arrs.update(grad=np.empty(self.n_params), params=np.empty(self.n_params))
+        Kmb = self.K_mb
+        if Kmb:
+            arrs.update(f_mb=np.empty(N * Kmb * D_m + 1), f_mb_ts=np.empty(N * Kmb),
+                        f_mb_cnt=np.empty(N, np.int32))
         for k, fld in _StepOut._fields_:
             if k in arrs:
                 setattr(o, k, _p(arrs[k], fld))
@@ -389,10 +402,21 @@ class Oracle:
             loss=o.loss if self.n_params else None,
             grad=arrs["grad"] if self.n_params else None,
             params=arrs["params"] if self.n_params else None,
-            relu_margin=o.relu_margin if self.n_params else None)
+            relu_margin=o.relu_margin if self.n_params else None,
+            f_mb=arrs["f_mb"][:nU * Kmb * D_m].reshape(nU, Kmb, D_m) if Kmb else None,
+            f_mb_ts=arrs["f_mb_ts"][:nU * Kmb].reshape(nU, Kmb) if Kmb else None,
+            f_mb_cnt=arrs["f_mb_cnt"][:nU] if Kmb else None)
 
     def flush(self):
         lib().orc_flush(self._h)
+
+    def mailbox(self):
+        """APAN: the committed mailboxes (rows [N x K_mb x D_m], times
+        [N x K_mb], counts [N]), oldest mail first."""
+        N, K, D_m = self.N, self.K_mb, self.D_m
+        mb, ts, cnt = np.empty(N * K * D_m + 1), np.empty(N * K), np.empty(N, np.int32)
+        lib().orc_get_mailbox(self._h, _p(mb, _f64p), _p(ts, _f64p), _p(cnt, _i32p))
+        return mb[:N * K * D_m].reshape(N, K, D_m), ts.reshape(N, K), cnt
 
     def param_sizes(self) -> list:
         sz = np.zeros(len(PARAM_NAMES), np.int64)

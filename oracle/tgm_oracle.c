@@ -55,6 +55,7 @@
 /* model families (Sec. 5 trains TGN, JODIE and APAN) */
 #define ORC_TGN 0
 #define ORC_JODIE 1
+#define ORC_APAN 2
 
 /* ------------------------------------------------------------------------- */
 /* Time encoding: phi(dt)_d = cos(omega_d * dt + beta_d), the cosine functional
@@ -522,6 +523,11 @@ typedef struct {
     int n;
     int32_t *node;
     double *mem, *mem_ts, *mail, *mail_ts;
+    /* APAN: the mails the iteration delivers, in delivery order (node,
+     * message [D_m], event time) */
+    int n_del;
+    int32_t *del_node;
+    double *del_mail, *del_t;
 } orc_wset;
 
 typedef struct {
@@ -549,6 +555,12 @@ typedef struct {
     /* model family and JODIE's projection vector */
     int kind;
     double *w_t;
+    /* APAN: every node's mailbox, its K_mb latest mails oldest first (rows
+     * [N x K_mb x D_m], times [N x K_mb], count [N]); whether each mail also
+     * goes to the sampled neighbours of its node */
+    int K_mb, propagate;
+    double *mb, *mb_ts;
+    int32_t *mb_cnt;
     /* training (off unless orc_set_training enables it): every trained
      * parameter in one vector theta (the weights above point into it), the
      * link predictor's weights, the gradient of the last step, the optimizer's
@@ -574,6 +586,9 @@ typedef struct {
      * b_ih, b_hh [M], w_t [M]; the attention weights are not read */
     int kind;
     const float *w_t;
+    /* ORC_APAN: mailbox size and propagation to neighbours; W_q [M x (M +
+     * D_t)], b_q, W_k [M x (D_m + D_t)], b_k of the mailbox attention */
+    int K_mb, propagate;
 } orc_desc;
 
 /* Per-iteration outputs; every pointer may be NULL.  Capacities: R = 3B roots,
@@ -612,6 +627,10 @@ typedef struct {
      * predictor's z and the attention's output projection): the margin by
      * which no branch of the backward is near its kink */
     double relu_margin;
+    /* APAN: the fetched mailboxes, oldest mail first: rows [n_U x K_mb x D_m],
+     * times [n_U x K_mb], counts [n_U] */
+    double *f_mb, *f_mb_ts;
+    int32_t *f_mb_cnt;
 } orc_step_out;
 
 static double *widen(const float *x, size_t n)
@@ -634,7 +653,8 @@ void *orc_create(const orc_desc *d)
 {
     if (!d || d->N <= 0 || d->E < 0 || d->M <= 0 || d->H <= 0 || d->M % d->H != 0 ||
         d->nb < 0 || d->B <= 0 || d->s < 0 || d->D_t < 0 || d->D_e < 0 ||
-        (d->kind != ORC_TGN && d->kind != ORC_JODIE) || (d->kind == ORC_JODIE && !d->w_t))
+        (d->kind != ORC_TGN && d->kind != ORC_JODIE && d->kind != ORC_APAN) ||
+        (d->kind == ORC_JODIE && !d->w_t) || (d->kind == ORC_APAN && d->K_mb < 1))
         return NULL;
     orc_ctx *c = (orc_ctx *)calloc(1, sizeof(orc_ctx));
     c->N = d->N; c->E = d->E;
@@ -661,6 +681,16 @@ void *orc_create(const orc_desc *d)
         c->b_v = widen(d->b_v, (size_t)M);
         c->W_o = widen(d->W_o, (size_t)M * (2 * M));
         c->b_o = widen(d->b_o, (size_t)M);
+    } else if (c->kind == ORC_APAN) {
+        c->W_q = widen(d->W_q, (size_t)M * (M + D_t));
+        c->b_q = widen(d->b_q, (size_t)M);
+        c->W_k = widen(d->W_k, (size_t)M * (c->D_m + D_t));
+        c->b_k = widen(d->b_k, (size_t)M);
+        c->K_mb = d->K_mb;
+        c->propagate = d->propagate != 0;
+        c->mb = (double *)calloc((size_t)c->N * d->K_mb * c->D_m + 1, sizeof(double));
+        c->mb_ts = (double *)calloc((size_t)c->N * d->K_mb, sizeof(double));
+        c->mb_cnt = (int32_t *)calloc((size_t)c->N, sizeof(int32_t));
     } else {
         c->w_t = widen(d->w_t, (size_t)M);
     }
@@ -681,6 +711,7 @@ void *orc_create(const orc_desc *d)
 static void free_wset(orc_wset *w)
 {
     free(w->node); free(w->mem); free(w->mem_ts); free(w->mail); free(w->mail_ts);
+    free(w->del_node); free(w->del_mail); free(w->del_t);
     memset(w, 0, sizeof(*w));
 }
 
@@ -697,6 +728,7 @@ void orc_destroy(void *p)
         free(c->W_o); free(c->b_o);
     }
     free(c->omega); free(c->beta); free(c->w_t);
+    free(c->mb); free(c->mb_ts); free(c->mb_cnt);
     free_adj(&c->adj);
     free(c->mem); free(c->mem_ts); free(c->mail); free(c->mail_ts); free(c->ver);
     for (int k = 0; k < c->nq; ++k)
@@ -717,6 +749,22 @@ static void apply_oldest(orc_ctx *c)
         c->mem_ts[v] = w->mem_ts[k];
         c->mail_ts[v] = w->mail_ts[k];
         c->ver[v] = (int32_t)w->iter;
+    }
+    /* APAN: each delivered mail joins its node's mailbox as the newest; a
+     * full mailbox drops its oldest */
+    const int K = c->K_mb;
+    for (int k = 0; k < w->n_del; ++k) {
+        const int v = w->del_node[k];
+        double *rows = c->mb + (size_t)v * K * D_m, *ts = c->mb_ts + (size_t)v * K;
+        if (c->mb_cnt[v] == K) {
+            memmove(rows, rows + D_m, sizeof(double) * (size_t)(K - 1) * D_m);
+            memmove(ts, ts + 1, sizeof(double) * (size_t)(K - 1));
+            c->mb_cnt[v]--;
+        }
+        memcpy(rows + (size_t)c->mb_cnt[v] * D_m, w->del_mail + (size_t)k * D_m,
+               sizeof(double) * D_m);
+        ts[c->mb_cnt[v]] = w->del_t[k];
+        c->mb_cnt[v]++;
     }
     free_wset(w);
     memmove(c->q, c->q + 1, sizeof(orc_wset) * (size_t)(c->nq - 1));
@@ -801,6 +849,19 @@ void orc_get_state(void *p, double *mem, double *mem_ts, double *mail, double *m
 }
 
 int64_t orc_next_iter(void *p) { return ((orc_ctx *)p)->next_iter; }
+
+/* APAN: the committed mailboxes, oldest mail first (rows [N x K_mb x D_m],
+ * times [N x K_mb], counts [N]; any pointer may be NULL). */
+void orc_get_mailbox(void *p, double *mb, double *mb_ts, int32_t *mb_cnt)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (c->kind != ORC_APAN)
+        return;
+    const size_t N = (size_t)c->N, K = (size_t)c->K_mb;
+    if (mb) memcpy(mb, c->mb, sizeof(double) * N * K * c->D_m);
+    if (mb_ts) memcpy(mb_ts, c->mb_ts, sizeof(double) * N * K);
+    if (mb_cnt) memcpy(mb_cnt, c->mb_cnt, sizeof(int32_t) * N);
+}
 
 /* Enables (on != 0) the staleness mitigation of step 3b with quantile p,
  * blend weight lambda and at most K similar nodes. */
@@ -1306,6 +1367,23 @@ int orc_step(void *p, orc_step_out *o)
         fver[k] = c->ver[v];
     }
 
+    /* APAN: the fetched mailboxes */
+    const int K = c->K_mb;
+    double *fmb = NULL, *fmbt = NULL;
+    int32_t *fmbc = NULL;
+    if (c->kind == ORC_APAN) {
+        fmb = (double *)malloc(sizeof(double) * ((size_t)nU * K * D_m + 1));
+        fmbt = (double *)malloc(sizeof(double) * ((size_t)nU * K + 1));
+        fmbc = (int32_t *)malloc(sizeof(int32_t) * (nU > 0 ? nU : 1));
+        for (int k = 0; k < nU; ++k) {
+            const int v = ids[k];
+            memcpy(fmb + (size_t)k * K * D_m, c->mb + (size_t)v * K * D_m,
+                   sizeof(double) * (size_t)K * D_m);
+            memcpy(fmbt + (size_t)k * K, c->mb_ts + (size_t)v * K, sizeof(double) * K);
+            fmbc[k] = c->mb_cnt[v];
+        }
+    }
+
     /* 3b. staleness mitigation of the fetched memories (when enabled); the
      * fetched rows are reported as read, the mitigated ones separately */
     double *fm_read = NULL, gamma = 0.0;
@@ -1321,6 +1399,59 @@ int orc_step(void *p, orc_step_out *o)
     /* 4. memory update of every node in U that holds mail */
     double *sn = (double *)malloc(sizeof(double) * (size_t)nU * M);
     double *nmts = (double *)malloc(sizeof(double) * nU);
+    if (c->kind == ORC_APAN) {
+        /* APAN's memory updater: the node's mailbox aggregated by attention
+         * (query from its memory, keys from each mail with the encoding of
+         * its age relative to the newest mail, the mails as values), then
+         * the GRU on [aggregate || phi(newest mail time - memory time)] */
+        const int D_mk = D_m + D_t;
+        const double scale = 1.0 / sqrt((double)M);
+        #pragma omp parallel for schedule(dynamic, 8)
+        for (int k = 0; k < nU; ++k) {
+            const int cntk = fmbc[k];
+            const double *hm = fm + (size_t)k * M;
+            if (cntk == 0) {
+                memcpy(sn + (size_t)k * M, hm, sizeof(double) * M);
+                nmts[k] = fmts[k];
+                continue;
+            }
+            const double *rows = fmb + (size_t)k * K * D_m, *ts = fmbt + (size_t)k * K;
+            const double tref = ts[cntk - 1];
+            double *buf = (double *)malloc(sizeof(double) * ((size_t)M + D_t + M + D_mk + M +
+                                                              K + D_x));
+            double *xq = buf, *q = xq + M + D_t, *kap = q + M, *kk = kap + D_mk, *sc = kk + M;
+            double *x = sc + K;
+            memcpy(xq, hm, sizeof(double) * M);
+            orc_time_encode(D_t, c->omega, c->beta, 0.0, xq + M);
+            matvec(M, M + D_t, c->W_q, c->b_q, xq, q);
+            double mx = -INFINITY;
+            for (int j = 0; j < cntk; ++j) {
+                memcpy(kap, rows + (size_t)j * D_m, sizeof(double) * D_m);
+                orc_time_encode(D_t, c->omega, c->beta, tref - ts[j], kap + D_m);
+                matvec(M, D_mk, c->W_k, c->b_k, kap, kk);
+                double dot = 0.0;
+                for (int i2 = 0; i2 < M; ++i2)
+                    dot += q[i2] * kk[i2];
+                sc[j] = dot * scale;
+                if (sc[j] > mx)
+                    mx = sc[j];
+            }
+            double den = 0.0;
+            for (int j = 0; j < cntk; ++j) {
+                sc[j] = exp(sc[j] - mx);
+                den += sc[j];
+            }
+            for (int d = 0; d < D_m; ++d)
+                x[d] = 0.0;
+            for (int j = 0; j < cntk; ++j)
+                for (int d = 0; d < D_m; ++d)
+                    x[d] += (sc[j] / den) * rows[(size_t)j * D_m + d];
+            orc_time_encode(D_t, c->omega, c->beta, tref - fmts[k], x + D_m);
+            orc_gru_cell(M, D_x, c->W_ih, c->W_hh, c->b_ih, c->b_hh, x, hm, sn + (size_t)k * M);
+            nmts[k] = tref;
+            free(buf);
+        }
+    } else {
     #pragma omp parallel for schedule(dynamic, 8)
     for (int k = 0; k < nU; ++k) {
         if (fver[k] >= 0) {
@@ -1340,6 +1471,7 @@ int orc_step(void *p, orc_step_out *o)
             nmts[k] = fmts[k];
         }
     }
+    }
 
     /* 5. embeddings of every root */
     double *h = (double *)malloc(sizeof(double) * (size_t)R * M);
@@ -1347,6 +1479,10 @@ int orc_step(void *p, orc_step_out *o)
                      c->W_v, c->b_v, c->W_o, c->b_o};
     #pragma omp parallel for schedule(dynamic, 8)
     for (int r = 0; r < R; ++r) {
+        if (c->kind == ORC_APAN) {   /* APAN's embedding: the updated memory */
+            memcpy(h + (size_t)r * M, sn + (size_t)pos[root[r]] * M, sizeof(double) * M);
+            continue;
+        }
         if (c->kind == ORC_JODIE) {
             const int pr = pos[root[r]];
             orc_time_projection(M, c->w_t, sn + (size_t)pr * M, nmts[pr], rts[r],
@@ -1423,6 +1559,35 @@ int orc_step(void *p, orc_step_out *o)
         W.mail_ts[w_] = c->t[e];
         ++w_;
     }
+    /* APAN: the mails of the batch, in (t, e, role) order, each to its node
+     * and (with propagation) then to the node's sampled neighbours at the
+     * event's time, in slot order */
+    if (c->kind == ORC_APAN) {
+        const int per = 1 + (c->propagate ? nb : 0);
+        W.del_node = (int32_t *)malloc(sizeof(int32_t) * ((size_t)2 * b * per + 1));
+        W.del_mail = (double *)malloc(sizeof(double) * ((size_t)2 * b * per * D_m + 1));
+        W.del_t = (double *)malloc(sizeof(double) * ((size_t)2 * b * per + 1));
+        int nd = 0;
+        for (int64_t e = lo; e < hi; ++e)
+            for (int role = 0; role < 2; ++role) {
+                const int v = role == 0 ? c->src[e] : c->dst[e];
+                const int other = role == 0 ? c->dst[e] : c->src[e];
+                const int r = role * b + (int)(e - lo);   /* v's root in this batch */
+                const int nrecv = 1 + (c->propagate ? cnt[r] : 0);
+                for (int hop = 0; hop < nrecv; ++hop) {
+                    const int w = hop == 0 ? v : nbr[(size_t)r * nb + hop - 1];
+                    double *ml = W.del_mail + (size_t)nd * D_m;
+                    memcpy(ml, sn + (size_t)pos[v] * M, sizeof(double) * M);
+                    memcpy(ml + M, sn + (size_t)pos[other] * M, sizeof(double) * M);
+                    for (int d = 0; d < D_e; ++d)
+                        ml[2 * M + d] = (double)c->efeat[(size_t)e * D_e + d];
+                    W.del_node[nd] = w;
+                    W.del_t[nd] = c->t[e];
+                    ++nd;
+                }
+            }
+        W.n_del = nd;
+    }
     if (c->nq == c->capq) {
         c->capq *= 2;
         c->q = (orc_wset *)realloc(c->q, sizeof(orc_wset) * (size_t)c->capq);
@@ -1450,6 +1615,12 @@ int orc_step(void *p, orc_step_out *o)
     if (o) {
         o->loss = loss;
         o->relu_margin = margin;
+        if (fmb && o->f_mb)
+            memcpy(o->f_mb, fmb, sizeof(double) * (size_t)nU * K * D_m);
+        if (fmbt && o->f_mb_ts)
+            memcpy(o->f_mb_ts, fmbt, sizeof(double) * (size_t)nU * K);
+        if (fmbc && o->f_mb_cnt)
+            memcpy(o->f_mb_cnt, fmbc, sizeof(int32_t) * (size_t)nU);
         if (c->train_on && o->grad)
             memcpy(o->grad, c->grad, sizeof(double) * (size_t)c->n_params);
         if (c->train_on && o->params)
@@ -1496,6 +1667,7 @@ int orc_step(void *p, orc_step_out *o)
     free(root); free(rts); free(nbr); free(eid); free(nts); free(cnt); free(ids); free(pos);
     free(fm); free(fmts); free(fl); free(flts); free(fver); free(sn); free(nmts); free(h);
     free(fm_read);
+    free(fmb); free(fmbt); free(fmbc);
     free(win);
     c->next_iter = i + 1;
     return ORC_OK;

@@ -88,7 +88,8 @@ class Weights:
     """Model parameters, row-major.  fp32 except the time encoding (fp64).
     TGN: a GRU updater and attention.  JODIE: an RNN updater ([M, D_x] and
     [M, M] weights, [M] biases) and the time projection w_t [M]; no attention
-    weights."""
+    weights.  APAN: the GRU updater, fed by an attention over the node's
+    mailbox (W_q [M, M + D_t], W_k [M, D_m + D_t] and their biases)."""
     W_ih: np.ndarray  # [3M, D_x]  gate order r, z, n   (JODIE: [M, D_x])
     W_hh: np.ndarray  # [3M, M]                        (JODIE: [M, M])
     b_ih: np.ndarray  # [3M]                           (JODIE: [M])
@@ -103,8 +104,10 @@ class Weights:
     b_v: np.ndarray | None = None
     W_o: np.ndarray | None = None   # [M, d_a + M]
     b_o: np.ndarray | None = None   # [M]
-    kind: str = "tgn"               # "tgn" or "jodie"
+    kind: str = "tgn"               # "tgn", "jodie" or "apan"
     w_t: np.ndarray | None = None   # [M] JODIE's time projection
+    K_mb: int = 0                   # APAN: mails per mailbox
+    propagate: bool = False         # APAN: mails also go to the sampled neighbours
 
 
 # ---------------------------------------------------------------------------
@@ -324,12 +327,15 @@ def _uniform(rng, shape, fan_in):
 
 
 def make_weights(M: int, D_e: int, D_t: int, *, seed: int = 0,
-                 beta: str = "zero", model: str = "tgn") -> Weights:
+                 beta: str = "zero", model: str = "tgn", K_mb: int = 10,
+                 propagate: bool = True) -> Weights:
     """U(+-1/sqrt(fan_in)) fp32 weights; time-encoding frequencies
     omega_d = 10^(-9 d / (D_t - 1)) and phases beta (zero, or U(0, 2pi) when
     ``beta='random'``) in fp64.  ``model='jodie'``: an RNN updater and a time
     projection w_t ~ U(+-1/sqrt(M)) scaled by 1e-5 per time unit (the
-    streams' gaps reach 1e6)."""
+    streams' gaps reach 1e6).  ``model='apan'``: the GRU and the mailbox
+    attention, K_mb mails per mailbox, mails propagated to the neighbours
+    when ``propagate``."""
     D_m = 2 * M + D_e
     D_x = D_m + D_t
     d_a = M
@@ -351,6 +357,19 @@ def make_weights(M: int, D_e: int, D_t: int, *, seed: int = 0,
             b_hh=_uniform(r("b_hh1"), (M,), M),
             omega=omega, beta=b, kind="jodie",
             w_t=(_uniform(r("w_t"), (M,), M) * np.float32(1e-5)).astype(np.float32))
+    if model == "apan":
+        D_mk = D_m + D_t
+        return Weights(
+            W_ih=_uniform(r("W_ih"), (3 * M, D_x), D_x),
+            W_hh=_uniform(r("W_hh"), (3 * M, M), M),
+            b_ih=_uniform(r("b_ih"), (3 * M,), M),
+            b_hh=_uniform(r("b_hh"), (3 * M,), M),
+            omega=omega, beta=b, kind="apan",
+            W_q=_uniform(r("W_q"), (d_a, M + D_t), M + D_t),
+            b_q=_uniform(r("b_q"), (d_a,), M + D_t),
+            W_k=_uniform(r("W_kmb"), (d_a, D_mk), D_mk),
+            b_k=_uniform(r("b_kmb"), (d_a,), D_mk),
+            K_mb=K_mb, propagate=propagate)
     if model != "tgn":
         raise ValueError(model)
     return Weights(
