@@ -445,6 +445,63 @@ tgm_status_t tgm_state_set_training(tgm_state_t st, tgm_trainer_t tr, float *los
                                     int64_t log_len);
 
 /* ------------------------------------------------------------------------
+ * APAN (Sec. 5 trains APAN; App. B: an RNN memory updater with an attention
+ * mechanism and asynchronous propagation).  A handle with its own state:
+ *   mailbox   per node the K_mb latest mails (the identity message
+ *             [s'_self || s'_other || efeat[e]] with its event time), oldest
+ *             first; a full mailbox drops its oldest;
+ *   propagation  the mail an event generates for its endpoint v goes to v
+ *             and (propagate != 0) to v's sampled neighbours at the event's
+ *             time (the nb most recent, as tgm_sample_nodes returns them for
+ *             root v), in (t, e, role, slot) order;
+ *   updater   for a node with mail: q = W_q [s || phi(0)] + b_q,
+ *             K_j = W_k [mail_j || phi(t_newest - t_j)] + b_k,
+ *             a = sum_j softmax_j(q . K_j / sqrt(M)) mail_j,
+ *             s' = GRU([a || phi(t_newest - mem_ts)], s), new_mem_ts = t_newest
+ *             (W_ih [3M x D_x], W_hh [3M x M], gates r, z, n as for TGN);
+ *             a node without mail keeps s;
+ *   embedding h = s' of each root;
+ *   write set of iteration i: the new memory of the batch's endpoints
+ *             (version i) and the iteration's mail deliveries, committed
+ *             before the fetch of iteration i + s + 1 (Eq. 2).
+ * Weights: W_ih, W_hh, b_ih, b_hh, W_q [M x (M + D_t)], b_q [M],
+ * W_k [M x (2M + D_e + D_t)], b_k [M], omega, beta of tgm_weights (HOST,
+ * copied); the other fields are not read.  Limits: M <= 128, D_e <= 256,
+ * 1 <= nb <= 64, 1 <= K_mb <= 16.
+ */
+typedef struct tgm_apan *tgm_apan_t;
+typedef struct {
+    int32_t N, M, D_e, D_t, nb;
+    int32_t K_mb, propagate;
+    int32_t s, max_batch, max_nodes;   /* staleness; events per batch; node-set rows */
+} tgm_apan_desc;
+tgm_status_t tgm_apan_create(const tgm_apan_desc *desc, const tgm_weights *w, void *stream,
+                             tgm_apan_t *out);
+tgm_status_t tgm_apan_destroy(tgm_apan_t a);
+/* Iteration `iter` (the batch [iter B, min(E, (iter + 1) B)), B = max_batch)
+ * from its sample and node set sb (tgm_sample_nodes of that batch with the
+ * same nb): commits the due write sets, fetches the node set's memories and
+ * mailboxes, updates them, writes mem_new [cap x M], new_mem_ts [cap] (may
+ * be NULL) and h [3b x M], and stages the write set.  Iterations are issued
+ * consecutively from 0 (else TGM_EORDER).  Errors: TGM_EINVAL, TGM_ESIZE
+ * (cap above max_nodes), TGM_ERANGE (iter past the stream). */
+tgm_status_t tgm_apan_step(tgm_apan_t a, tgm_graph_t g, int64_t iter,
+                           const tgm_sample_buffers *sb, int32_t cap, float *mem_new,
+                           double *new_mem_ts, float *h, void *stream);
+/* Commit every staged write set. */
+tgm_status_t tgm_apan_flush(tgm_apan_t a, void *stream);
+/* The committed tables (device, each may be NULL; mb and mb_ts together):
+ * mem [N x M], mem_ts [N], ver [N], mb [N x K_mb x D_m] and mb_ts
+ * [N x K_mb] oldest mail first (zero past the count), mb_cnt [N]. */
+tgm_status_t tgm_apan_read(tgm_apan_t a, float *mem, double *mem_ts, int32_t *ver, float *mb,
+                           double *mb_ts, int32_t *mb_cnt, void *stream);
+/* The last step's fetched rows (device, each may be NULL), in node-set order:
+ * mem [max_nodes x M], mem_ts, ver [max_nodes], mb [max_nodes x K_mb x D_m],
+ * mb_ts [max_nodes x K_mb] (oldest first), mb_cnt [max_nodes]. */
+tgm_status_t tgm_apan_fetched(tgm_apan_t a, float *mem, double *mem_ts, int32_t *ver, float *mb,
+                              double *mb_ts, int32_t *mb_cnt, void *stream);
+
+/* ------------------------------------------------------------------------
  * Similarity-based staleness mitigation (MSPipe-S, Sec. 3.3), applied to the
  * fetched memories of a batch between tgm_fetch_memory and
  * tgm_update_memory.  For the fetched node set (positions p < *n_nodes):

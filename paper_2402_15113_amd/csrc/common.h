@@ -675,6 +675,12 @@ struct ModelParams {
 };
 tgm_status_t model_repack(tgm_model_t m, const ModelParams &w, hipStream_t s);
 
+// C[m x n] = op(A) op(B) (+ bias[n]) (+ C when accumulate), fp32 MFMA, no
+// split of the reduction (the GEMM of the training step; op as there).
+tgm_status_t gemm_f32(bool ta, bool tb, int m, int n, int k, const float *A, int lda,
+                      const float *B, int ldb, float *C, int ldc, const float *bias,
+                      bool accumulate, hipStream_t s);
+
 // The training step of one iteration (tgm_train_step) on stream s, from the
 // iteration's sample and fetch buffers, new memories and embeddings.
 tgm_status_t train_step_launch(tgm_trainer_t tr, tgm_model_t m, tgm_graph_t g, int32_t b,

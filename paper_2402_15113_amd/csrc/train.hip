@@ -781,6 +781,39 @@ tgm_status_t colsum(const tgm_trainer *tr, int rows, int n, const float *X, int 
 
 }  // namespace
 
+tgm_status_t tgm::gemm_f32(bool ta, bool tb, int m, int n, int k, const float *A, int lda,
+                          const float *B, int ldb, float *C, int ldc, const float *bias,
+                          bool accumulate, hipStream_t s)
+{
+    if (m <= 0 || n <= 0)
+        return TGM_OK;
+    GemmArgs g;
+    g.m = m;
+    g.n = n;
+    g.k = k;
+    g.A = A;
+    g.lda = lda;
+    g.B = B;
+    g.ldb = ldb;
+    g.C = C;
+    g.ldc = ldc;
+    g.bias = bias;
+    g.accumulate = accumulate ? 1 : 0;
+    g.part = nullptr;
+    g.splits = 1;
+    g.kchunk = round_up((int32_t)std::max(k, 1), kGK);
+    const dim3 grid((unsigned)cdiv(n, kGT), (unsigned)cdiv(m, kGT), 1);
+    if (!ta && !tb)
+        TGM_LAUNCH((k_gemm<false, false>), grid, dim3(256), 0, s, g);
+    else if (!ta && tb)
+        TGM_LAUNCH((k_gemm<false, true>), grid, dim3(256), 0, s, g);
+    else if (ta && !tb)
+        TGM_LAUNCH((k_gemm<true, false>), grid, dim3(256), 0, s, g);
+    else
+        TGM_LAUNCH((k_gemm<true, true>), grid, dim3(256), 0, s, g);
+    return TGM_OK;
+}
+
 // ======================================================================== API
 
 extern "C" tgm_status_t tgm_trainer_destroy(tgm_trainer_t tr)

@@ -276,6 +276,99 @@ class Stage:
         tgm.tgm_state_restore(self.st, buf, stream=self.stream)
 
 
+class ApanStage:
+    """The APAN family through libtgm: tgm_sample_nodes, then tgm_apan_step
+    (fetch with the mailboxes, mailbox attention and GRU, identity
+    embedding, staged write set with the propagated mails) per iteration."""
+
+    def __init__(self, wl, w, *, s=None, device="cuda", stream=None):
+        dev = torch.device(device)
+        self.dev, self.wl = dev, wl
+        self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
+        T = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+        self.src, self.dst = T(wl.src, torch.int32), T(wl.dst, torch.int32)
+        self.t, self.neg = T(wl.t, torch.float64), T(wl.neg, torch.int32)
+        self.efeat = None if wl.efeat is None else T(wl.efeat, torch.float32)
+        self.N, self.M, self.nb, self.B = wl.N, wl.M, wl.nb, wl.B
+        self.s = wl.s if s is None else s
+        self.K = int(w.K_mb)
+        self.D_m = 2 * wl.M + wl.D_e
+        R = 3 * wl.B
+        self.cap = min(self.N, R * (self.nb + 1))
+        st = self.stream
+        self.g = tgm.tgm_graph_create(self.N, self.src, self.dst, self.t, self.neg, self.efeat,
+                                      stream=st)
+        self.a = tgm.tgm_apan_create(self.N, wl.M, wl.D_e, wl.D_t, self.nb, self.K, w.propagate,
+                                     self.s, wl.B, self.cap, w, stream=st)
+        self.sb = _Sample(dev, R, self.nb, self.cap)
+        self._sbs = tgm.buffers(tgm.SampleBuffers, **vars(self.sb))
+        z = lambda shape, dt: torch.zeros(shape, dtype=dt, device=dev)
+        self.mem_new, self.new_mem_ts = z((self.cap, wl.M), torch.float32), z(self.cap,
+                                                                              torch.float64)
+        self.h = z((R, wl.M), torch.float32)
+        self.last = None
+
+    def step(self, i: int):
+        lo = i * self.B
+        n = min(self.B, self.wl.E - lo)
+        b = self.sb
+        tgm.tgm_sample_nodes(self.g, lo, n, self.nb, b.root, b.root_ts, b.nbr, b.eid, b.nts,
+                             b.cnt, b.nodes, b.n_nodes, self.cap, b.root_pos, b.nbr_pos,
+                             stream=self.stream)
+        tgm.tgm_apan_step(self.a, self.g, i, self._sbs, self.cap, self.mem_new, self.new_mem_ts,
+                          self.h, stream=self.stream)
+        self.last = (i, n)
+
+    def outputs(self):
+        """Host copies of the last iteration's node set, fetched rows and
+        mailboxes (oldest first), new memories and embeddings (synchronises)."""
+        i, n = self.last
+        dev, C, M, K, D_m = self.dev, self.cap, self.M, self.K, self.D_m
+        e = lambda shape, dt: torch.empty(shape, dtype=dt, device=dev)
+        f_mem, f_ts, f_ver = e((C, M), torch.float32), e(C, torch.float64), e(C, torch.int32)
+        f_mb, f_mbt, f_cnt = e((C, K, D_m), torch.float32), e((C, K), torch.float64), \
+            e(C, torch.int32)
+        tgm.tgm_apan_fetched(self.a, f_mem, f_ts, f_ver, f_mb, f_mbt, f_cnt, stream=self.stream)
+        torch.cuda.synchronize(dev)
+        nU = int(self.sb.n_nodes.item())
+        R = 3 * n
+        c = lambda x: x.cpu().numpy()
+        return dict(iter=i, b=n, n_U=nU, U=c(self.sb.nodes[:nU]), root_pos=c(self.sb.root_pos[:R]),
+                    f_mem=c(f_mem[:nU]), f_mem_ts=c(f_ts[:nU]), f_ver=c(f_ver[:nU]),
+                    f_mb=c(f_mb[:nU]), f_mb_ts=c(f_mbt[:nU]), f_mb_cnt=c(f_cnt[:nU]),
+                    s_new=c(self.mem_new[:nU]), new_mem_ts=c(self.new_mem_ts[:nU]),
+                    h=c(self.h[:R]))
+
+    def flush(self):
+        tgm.tgm_apan_flush(self.a, stream=self.stream)
+
+    def state(self):
+        dev, N, M, K, D_m = self.dev, self.N, self.M, self.K, self.D_m
+        e = lambda shape, dt: torch.empty(shape, dtype=dt, device=dev)
+        mem, mem_ts, ver = e((N, M), torch.float32), e(N, torch.float64), e(N, torch.int32)
+        mb, mb_ts, cnt = e((N, K, D_m), torch.float32), e((N, K), torch.float64), \
+            e(N, torch.int32)
+        tgm.tgm_apan_read(self.a, mem, mem_ts, ver, mb, mb_ts, cnt, stream=self.stream)
+        torch.cuda.synchronize(dev)
+        c = lambda x: x.cpu().numpy()
+        return dict(mem=c(mem), mem_ts=c(mem_ts), ver=c(ver), mb=c(mb), mb_ts=c(mb_ts),
+                    mb_cnt=c(cnt))
+
+    def close(self):
+        if self.__dict__.get("a") is not None:
+            tgm.tgm_apan_destroy(self.a)
+            self.a = None
+        if self.__dict__.get("g") is not None:
+            tgm.tgm_graph_destroy(self.g)
+            self.g = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None,
                   training=None) -> Stage:
     return Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, wl.efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,

@@ -31,6 +31,8 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_alloc_
            "tgm_mitigator_read", "tgm_state_set_mitigation", "tgm_min_staleness",
            "tgm_mitigate_noalloc", "tgm_trainer_create", "tgm_trainer_destroy",
            "tgm_trainer_info", "tgm_trainer_read", "tgm_train_step", "tgm_state_set_training",
+           "tgm_apan_create", "tgm_apan_destroy", "tgm_apan_step", "tgm_apan_flush",
+           "tgm_apan_read", "tgm_apan_fetched",
            "tgm_embed_projection",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
 
@@ -69,6 +71,12 @@ class Weights(C.Structure):
                 ("omega", _dp), ("beta", _dp),
                 ("W_q", _fp), ("b_q", _fp), ("W_k", _fp), ("b_k", _fp), ("W_v", _fp),
                 ("b_v", _fp), ("W_o", _fp), ("b_o", _fp), ("w_t", _fp)]
+
+
+class ApanDesc(C.Structure):
+    _fields_ = [("N", C.c_int32), ("M", C.c_int32), ("D_e", C.c_int32), ("D_t", C.c_int32),
+                ("nb", C.c_int32), ("K_mb", C.c_int32), ("propagate", C.c_int32),
+                ("s", C.c_int32), ("max_batch", C.c_int32), ("max_nodes", C.c_int32)]
 
 
 class Predictor(C.Structure):
@@ -136,6 +144,12 @@ def lib():
             "tgm_train_step": [V, V, V, I32, C.POINTER(SampleBuffers), C.POINTER(FetchBuffers),
                                P, P, I32, P, V],
             "tgm_state_set_training": [V, V, P, I64],
+            "tgm_apan_create": [C.POINTER(ApanDesc), C.POINTER(Weights), V, C.POINTER(V)],
+            "tgm_apan_destroy": [V],
+            "tgm_apan_step": [V, V, I64, C.POINTER(SampleBuffers), I32, P, P, P, V],
+            "tgm_apan_flush": [V, V],
+            "tgm_apan_read": [V, P, P, P, P, P, P, V],
+            "tgm_apan_fetched": [V, P, P, P, P, P, P, V],
             "tgm_mitigator_create": [I32, I32, I32, C.POINTER(V)],
             "tgm_mitigator_destroy": [V],
             "tgm_mitigate": [V, V, I64, P, P, I32, P, P, I32, C.c_double, C.c_float, V],
@@ -428,6 +442,44 @@ def tgm_trainer_create(m, w, pred, opt="adam", lr=1e-4, beta1=0.9, beta2=0.999, 
     _check("tgm_trainer_create", lib().tgm_trainer_create(m, C.byref(ws), C.byref(ps),
                                                           C.byref(os_), _s(stream), C.byref(h)))
     return h
+
+
+def tgm_apan_create(N, M, D_e, D_t, nb, K_mb, propagate, s, max_batch, max_nodes, w,
+                    stream=None):
+    """``w`` the APAN weights (workloads.make_weights(model='apan'))."""
+    keep = {}
+    ws = _weights_struct(w, keep)
+    d = ApanDesc(N, M, D_e, D_t, nb, K_mb, 1 if propagate else 0, s, max_batch, max_nodes)
+    h = V()
+    _check("tgm_apan_create", lib().tgm_apan_create(C.byref(d), C.byref(ws), _s(stream),
+                                                    C.byref(h)))
+    return h
+
+
+def tgm_apan_destroy(a):
+    _check("tgm_apan_destroy", lib().tgm_apan_destroy(a))
+
+
+def tgm_apan_step(a, g, it, sample_bufs, cap, mem_new, new_mem_ts, h, stream=None):
+    _check("tgm_apan_step", lib().tgm_apan_step(a, g, it, C.byref(sample_bufs), cap,
+                                                _p(mem_new), _p(new_mem_ts), _p(h),
+                                                _s(stream)))
+
+
+def tgm_apan_flush(a, stream=None):
+    _check("tgm_apan_flush", lib().tgm_apan_flush(a, _s(stream)))
+
+
+def tgm_apan_read(a, mem=None, mem_ts=None, ver=None, mb=None, mb_ts=None, mb_cnt=None,
+                  stream=None):
+    _check("tgm_apan_read", lib().tgm_apan_read(a, _p(mem), _p(mem_ts), _p(ver), _p(mb),
+                                                _p(mb_ts), _p(mb_cnt), _s(stream)))
+
+
+def tgm_apan_fetched(a, mem=None, mem_ts=None, ver=None, mb=None, mb_ts=None, mb_cnt=None,
+                     stream=None):
+    _check("tgm_apan_fetched", lib().tgm_apan_fetched(a, _p(mem), _p(mem_ts), _p(ver), _p(mb),
+                                                      _p(mb_ts), _p(mb_cnt), _s(stream)))
 
 
 def tgm_trainer_destroy(tr):

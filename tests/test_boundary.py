@@ -18,7 +18,7 @@ CSRC = os.path.join(ROOT, "paper_2402_15113_amd", "csrc")
 
 # set-up functions that may allocate, create events or synchronise the device
 SETUP = {"tgm_graph_create", "tgm_state_create", "tgm_model_create", "create_jodie",
-         "tgm_trainer_create",
+         "tgm_trainer_create", "tgm_apan_create",
          "tgm_mitigator_create", "mitigate_reserve", "tgm_state_set_mitigation",
          "tgm_state_save", "tgm_state_restore", "tgm_state_load", "tgm_state_read",
          "upload", "tgm_profile_get", "tgm_profile_count", "fold_profile", "take_event",
