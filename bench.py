@@ -73,13 +73,15 @@ class Schedule:
     def __init__(self, stage, n_iters, first=0, init=None):
         self.stage, self.first, self.init = stage, first, init
         self.n = n_iters - first
+        self.apan = hasattr(stage, "counts")   # APAN: one stream, no pipelined executor
 
     def restart(self):
-        from paper_2402_15113_amd import tgm
         if self.init is None:
-            tgm.tgm_state_reset(self.stage.st, stream=self.stage.stream)
+            self.stage.reset()
         elif "checkpoint" in self.init:
             self.stage.restore_checkpoint(self.init["checkpoint"])
+        elif "apan" in self.init:   # APAN tables (device or host)
+            self.stage.load_state(self.first, *self.init["apan"])
         else:
             self.stage.load_state(self.first, **self.init)
 
@@ -93,7 +95,7 @@ class Schedule:
                 self.restart()
             seg = min(k0 + K - k, self.n - k % self.n)
             i = self.first + k % self.n
-            if pipelined:
+            if pipelined or self.apan:
                 self.stage.run(i, seg)
             else:
                 for j in range(seg):
@@ -132,6 +134,28 @@ def account(sched, W, K):
     tgm.tgm_profile_enable(False)
     seq = tgm.tgm_profile_read()
     stage.want_winner = False
+    return rows, seq
+
+
+def account_apan(sched, W, K):
+    """APAN: per-step sizes of the timed steps from an untimed replay (a
+    synchronisation after each step), and the per-kernel durations of its
+    timed steps."""
+    import torch
+    from paper_2402_15113_amd import tgm
+    stage = sched.stage
+    sched.restart()
+    rows = []
+    for k in range(W + K):
+        if k == W:
+            torch.cuda.synchronize()
+            tgm.tgm_profile_reset()
+            tgm.tgm_profile_enable(True)
+        sched.run(k, 1)
+        if k >= W:
+            rows.append(stage.counts())
+    tgm.tgm_profile_enable(False)
+    seq = tgm.tgm_profile_read()
     return rows, seq
 
 
@@ -203,16 +227,20 @@ def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu", traini
       state="synthetic"  a seeded synthetic state; rows from the oldest event
                          the window samples to its end are filled."""
     import torch
-    from paper_2402_15113_amd.stage import Stage
-    from workloads import make_workload
+    from paper_2402_15113_amd.stage import ApanStage, Stage
+    from workloads import make_workload, synthetic_mailbox
 
     tg = time.perf_counter()
     wl = make_workload(name, with_features=False, s=s)
     log(f"stream of {wl.E:,} events generated in {time.perf_counter() - tg:.1f} s")
     E_end = min(wl.E, (first + L) * wl.B)
     efeat = torch.empty((wl.E, wl.D_e), dtype=torch.float32, device="cuda")
-    stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
-                  nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation, training=training)
+    apan = w.K_mb > 0
+    if apan:
+        stage = ApanStage(wl, w, efeat=efeat)
+    else:
+        stage = Stage(wl.N, wl.src, wl.dst, wl.t, wl.neg, efeat, w, M=wl.M, D_t=wl.D_t, H=wl.H,
+                      nb=wl.nb, B=wl.B, s=wl.s, mitigation=mitigation, training=training)
     stage._efeat_keep = efeat
     if state == "gpu":
         lo_row, hi_row = 0, wl.E
@@ -227,7 +255,18 @@ def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu", traini
                            "rows_filled": [lo_row, hi_row]}}
     if hi_row - lo_row < wl.E:
         meta["edge_table"]["rows_not_filled"] = "never read by the batches that run"
-    if state == "gpu":
+    if state == "gpu" and apan:
+        # APAN's state at first: the GPU run of batches 0 .. first - 1 with
+        # every write set committed (a copy of the tables on the device)
+        tp = time.perf_counter()
+        stage.run(0, first)
+        stage.flush()
+        init = {"apan": stage.device_state()}
+        torch.cuda.synchronize()
+        log(f"state: GPU ran batches 0..{first - 1} in {time.perf_counter() - tp:.1f} s")
+        meta["state"] = (f"GPU run of batches 0..{first - 1} from the initial state, its write "
+                         f"sets committed")
+    elif state == "gpu":
         tp = time.perf_counter()
         stage.want_winner = False
         if training is not None:   # the state is the forward stage's; training starts at first
@@ -240,7 +279,11 @@ def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu", traini
         log(f"state: GPU ran batches 0..{first - 1} in {time.perf_counter() - tp:.1f} s")
         meta["state"] = f"GPU run of batches 0..{first - 1} from the initial state"
     else:
-        init = synthetic_state(wl, first, wl.t[lo_row - 1] if lo_row > 0 else 0.0)
+        t0 = wl.t[lo_row - 1] if lo_row > 0 else 0.0
+        init = synthetic_state(wl, first, t0)
+        if apan:
+            init = {"apan": (init["mem"], init["mem_ts"], init["ver"])
+                    + synthetic_mailbox(wl.N, w.K_mb, wl.D_m, t0, 12)}
         meta["state"] = f"seeded synthetic memory state at batch {first}"
     return wl, stage, init, meta
 
@@ -304,6 +347,47 @@ def work_model(wl, rows, model="tgn"):
     k["k_attn_fold"] = dict(k["k_attn"])
     k["k_attn_fold_gather"] = dict(k["k_attn_gather"])
     return k
+
+
+def apan_work_model(wl, K, rows):
+    """APAN: algorithmic flops / bytes per launch of each kernel (averaged
+    over the timed steps).  Useful work only: the node set's rows, its nodes
+    with mail (n_mail) and their mails (n_mails); the GEMMs count the rows of
+    nodes with mail (they also run over the rest of the node-set capacity)."""
+    M, D_e, D_t, D_m, nb = wl.M, wl.D_e, wl.D_t, wl.D_m, wl.nb
+    D_x = D_m + D_t
+    n = len(rows)
+    avg = lambda key: sum(r[key] for r in rows) / n
+    R, n_U, n_mail, n_mails, b = avg("R"), avg("n_U"), avg("n_mail"), avg("n_mails"), avg("b")
+    f, d = 4, 8
+    n_del = 2 * b * (nb + 1)   # delivery slots; at most K kept per node
+    gemms = [(n_mail, M, M + D_t), (n_mail, D_x, M), (n_mail, 3 * M, D_x), (n_mail, 3 * M, M)]
+    return {
+        # the node set's memories, times, versions, counts, heads; every mail
+        # and its time, in and out
+        "k_apan_gather": dict(flops=0, bytes=n_U * (2 * M * f + 2 * (d + 4) + 3 * 4)
+                              + n_mails * 2 * (D_m * f + d)),
+        "k_apan_query_rows": dict(flops=0, bytes=n_U * (M * f + (M + D_t) * f)),
+        "k_gemm": dict(flops=sum(2.0 * a * b_ * c for a, b_, c in gemms) / len(gemms),
+                       bytes=sum(f * (a * c + c * b_ + a * b_) for a, b_, c in gemms)
+                       / len(gemms)),
+        "k_apan_qb": dict(flops=n_U * 2 * M, bytes=n_U * (M + 1) * f),
+        # per mail: its row and time, the score over [mail || phi]; the weighted sum
+        "k_apan_attn": dict(flops=n_mails * (2 * D_x + 2 * D_m),
+                            bytes=n_mail * (2 * D_x * f + 2 * d + 4 + f)
+                            + n_mails * (D_m * f + d)),
+        "k_apan_gru": dict(flops=n_mail * 12 * M, bytes=n_U * (2 * M * f + 4)
+                           + n_mail * 6 * M * f),
+        "k_apan_embed": dict(flops=0, bytes=R * (2 * M * f + 4)),
+        "k_apan_stage_mem": dict(flops=0, bytes=2 * b * (2 * M * f + 4 + 4 + d + 4)),
+        "k_apan_keys": dict(flops=0, bytes=n_del * 8 + 2 * b * (4 + 4) + 2 * b * nb * 4),
+        "k_apan_bounds": dict(flops=0, bytes=n_del * 8),
+        # kept mails (at most K per node): two memory rows, the event's features
+        "k_apan_stage_mail": dict(flops=0, bytes=n_del * 8 + min(n_del, K * n_U)
+                                  * (2 * (2 * M + D_e) * f + 3 * 4 + d)),
+        "k_apan_commit_mem": dict(flops=0, bytes=2 * b * (2 * M * f + 2 * d + 4)),
+        "k_apan_commit_mail": dict(flops=0, bytes=min(n_del, K * n_U) * (2 * D_m * f + 2 * d)),
+    }
 
 
 def train_work_model(wl, rows):
@@ -489,9 +573,17 @@ def cpu_baseline_window(wl, w, first, seconds, mitigation=None, training=None):
     lo_row = int(rows.min())
     init = synthetic_state(pre, first, pre.t[lo_row - 1] if lo_row > 0 else 0.0)
 
+    box = None
+    if w.K_mb > 0:
+        from workloads import synthetic_mailbox
+        box = synthetic_mailbox(pre.N, w.K_mb, pre.D_m, pre.t[lo_row - 1] if lo_row > 0 else 0.0,
+                                12)
+
     def make():
         o = oracle.Oracle(pre, w, mitigation=mitigation, training=training)
         o.set_state(first, **init)
+        if box is not None:
+            o.set_mailbox(*box)
         return o
 
     all_threads = oracle.set_threads(0)
@@ -520,9 +612,11 @@ def main():
     ap.add_argument("--state", default="gpu", choices=("gpu", "synthetic"),
                     help="gdelt: the memory state at --first: the GPU's own run of batches "
                          "0..first-1 (default), or a seeded synthetic state (counter passes)")
-    ap.add_argument("--model", default="tgn", choices=("tgn", "jodie"),
-                    help="model family: tgn (GRU memory, attention; default) or jodie (RNN "
-                         "memory, time projection)")
+    ap.add_argument("--model", default="tgn", choices=("tgn", "jodie", "apan"),
+                    help="model family: tgn (GRU memory, attention; default), jodie (RNN "
+                         "memory, time projection) or apan (mailbox of the 10 latest mails "
+                         "with propagation to sampled neighbours, attention over the mailbox "
+                         "into the GRU)")
     ap.add_argument("--mitigate", default=None, metavar="P,LAMBDA,K",
                     help="similarity-based staleness mitigation on every fetch (MSPipe-S, "
                          "off by default), e.g. 0.99,0.95,10")
@@ -568,6 +662,12 @@ def main():
         mit = dict(p=float(pq), lam=float(lam), K=int(kk))
     training = None
 
+    apan = args.model == "apan"
+    if apan and (args.train or args.mitigate or args.staleness == "auto"):
+        print("--model apan runs the forward stage with a fixed staleness: no --train, "
+              "--mitigate or --staleness auto", file=sys.stderr)
+        sys.exit(2)
+
     def build(s):
         nonlocal training
         if args.train:
@@ -585,7 +685,11 @@ def main():
         else:
             wl = make_workload(args.workload, s=s)
             w = make_weights(wl.M, wl.D_e, wl.D_t, model=args.model)
-            stage = from_workload(wl, w, mitigation=mit, training=training)
+            if apan:
+                from paper_2402_15113_amd.stage import ApanStage
+                stage = ApanStage(wl, w)
+            else:
+                stage = from_workload(wl, w, mitigation=mit, training=training)
             sched = Schedule(stage, wl.n_iters)
         sched.restart()
         return wl, w, stage, sched
@@ -642,8 +746,15 @@ def main():
         out["staleness_calibration"] = calib
     if mit is not None:
         out["config"]["mitigation"] = dict(mit, kind="MSPipe-S similarity-based, every fetch")
-    if args.model != "tgn":
+    if args.model == "jodie":
         out["config"]["model_family"] = "JODIE: RNN memory updater, time-projection embedding"
+    elif apan:
+        out["config"]["model_family"] = (f"APAN: mailbox of the {w.K_mb} latest mails per node "
+                                         f"(propagated to the sampled neighbours), attention "
+                                         f"over the mailbox into the GRU, embedding = memory")
+        out["config"]["pipeline"] = ("one stream per batch: sample + node set, commit of due "
+                                     "write sets, fetch with mailboxes, attention, GRU, "
+                                     "embedding, staging of memories and mail deliveries")
     if args.train:
         out["metric"] = "training events/sec (stage + link-prediction loss + backward + Adam)"
         out["config"]["training"] = {"predictor": "two-layer perceptron over the endpoint "
@@ -669,8 +780,12 @@ def main():
             n0, m0 = prof.get(base, (0, 0.0))
             prof[base] = (n0 + launches, m0 + ms)
         # pass 3: algorithmic work per launch, and the sequential stage times
-        rows, seq = account(sched, W, K)
-        work = work_model(wl, rows, args.model)
+        if apan:
+            rows, seq = account_apan(sched, W, K)
+            work = apan_work_model(wl, w.K_mb, rows)
+        else:
+            rows, seq = account(sched, W, K)
+            work = work_model(wl, rows, args.model)
         if args.train:
             work.update(train_work_model(wl, rows))
         kernels = {}
@@ -702,11 +817,13 @@ def main():
         # the minimal staleness (Sec. 3.2) for the stage times measured on the
         # sequential replay (the paper profiles a few iterations, App. D.1)
         from paper_2402_15113_amd.stage import minimal_staleness, stage_durations_us
-        out["staleness_bound"] = dict(minimal_staleness(stage_durations_us(seq, K)),
-                                      s_config=wl.s)
+        if not apan:
+            out["staleness_bound"] = dict(minimal_staleness(stage_durations_us(seq, K)),
+                                          s_config=wl.s)
         out["profiled_ms_per_step"] = tp * 1e3 / K
         out["per_step"] = {k: sum(r[k] for r in rows) / len(rows)
-                           for k in ("R", "slots", "n_U", "n_mail", "n_win")}
+                           for k in (("R", "slots", "n_U", "n_mail", "n_mails") if apan else
+                                     ("R", "slots", "n_U", "n_mail", "n_win"))}
         log(f"dominant kernel {dom}: {dk['avg_us']:.1f} us, {achieved:.2f} "
             f"{out['roofline']['unit']} ({100 * achieved / peak:.1f}% of peak)")
     stage.close()

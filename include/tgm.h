@@ -495,6 +495,18 @@ tgm_status_t tgm_apan_flush(tgm_apan_t a, void *stream);
  * [N x K_mb] oldest mail first (zero past the count), mb_cnt [N]. */
 tgm_status_t tgm_apan_read(tgm_apan_t a, float *mem, double *mem_ts, int32_t *ver, float *mb,
                            double *mb_ts, int32_t *mb_cnt, void *stream);
+/* The initial state again (zero memories, versions -1, empty mailboxes);
+ * staged write sets are dropped and the next step is iteration 0. */
+tgm_status_t tgm_apan_reset(tgm_apan_t a, void *stream);
+/* Replace the committed tables (device, the layouts of tgm_apan_read; none
+ * may be NULL; counts outside [0, K_mb] are clamped, mails past a count are
+ * ignored) and restart the protocol at iteration `iter`: staged write sets
+ * are dropped, and the fetch of a step i >= iter sees the loaded tables plus
+ * the write sets of iterations iter .. i-1-s (Eq. 2).  The next step is
+ * iteration `iter`.  The copies are ordered on `stream`. */
+tgm_status_t tgm_apan_load(tgm_apan_t a, int64_t iter, const float *mem, const double *mem_ts,
+                           const int32_t *ver, const float *mb, const double *mb_ts,
+                           const int32_t *mb_cnt, void *stream);
 /* The last step's fetched rows (device, each may be NULL), in node-set order:
  * mem [max_nodes x M], mem_ts, ver [max_nodes], mb [max_nodes x K_mb x D_m],
  * mb_ts [max_nodes x K_mb] (oldest first), mb_cnt [max_nodes]. */

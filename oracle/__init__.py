@@ -115,6 +115,8 @@ def lib():
         L.orc_param_sizes.argtypes = [C.c_void_p, _i64p]
         L.orc_get_params.argtypes = [C.c_void_p, _f64p]
         L.orc_get_mailbox.argtypes = [C.c_void_p, _f64p, _f64p, _i32p]
+        L.orc_set_mailbox.argtypes = [C.c_void_p, _f64p, _f64p, _i32p]
+        L.orc_set_mailbox.restype = C.c_int
         L.orc_set_threads.argtypes = [C.c_int]
         L.orc_set_threads.restype = C.c_int
         _lib = L
@@ -417,6 +419,16 @@ class Oracle:
         mb, ts, cnt = np.empty(N * K * D_m + 1), np.empty(N * K), np.empty(N, np.int32)
         lib().orc_get_mailbox(self._h, _p(mb, _f64p), _p(ts, _f64p), _p(cnt, _i32p))
         return mb[:N * K * D_m].reshape(N, K, D_m), ts.reshape(N, K), cnt
+
+    def set_mailbox(self, mb, mb_ts, mb_cnt):
+        """APAN: replace the committed mailboxes (the layouts of mailbox();
+        after set_state, which empties the queue of write sets)."""
+        mb, mb_ts = _f64(mb), _f64(mb_ts)
+        cnt = np.ascontiguousarray(mb_cnt, dtype=np.int32)
+        N, K, D_m = self.N, self.K_mb, self.D_m
+        assert mb.size == N * K * D_m and mb_ts.size == N * K and cnt.size == N
+        if lib().orc_set_mailbox(self._h, _p(mb, _f64p), _p(mb_ts, _f64p), _p(cnt, _i32p)) != 0:
+            raise ValueError("orc_set_mailbox: not an APAN model, or a count outside [0, K_mb]")
 
     def param_sizes(self) -> list:
         sz = np.zeros(len(PARAM_NAMES), np.int64)

@@ -863,6 +863,31 @@ void orc_get_mailbox(void *p, double *mb, double *mb_ts, int32_t *mb_cnt)
     if (mb_cnt) memcpy(mb_cnt, c->mb_cnt, sizeof(int32_t) * N);
 }
 
+/* APAN: replace the committed mailboxes (the layouts of orc_get_mailbox,
+ * oldest mail first; mails past a count are not read).  Returns 0, or -1
+ * for a model without mailboxes or a count outside [0, K_mb] (nothing is
+ * changed then). */
+int orc_set_mailbox(void *p, const double *mb, const double *mb_ts, const int32_t *mb_cnt)
+{
+    orc_ctx *c = (orc_ctx *)p;
+    if (c->kind != ORC_APAN)
+        return -1;
+    const size_t N = (size_t)c->N, K = (size_t)c->K_mb, D_m = (size_t)c->D_m;
+    for (size_t v = 0; v < N; ++v)
+        if (mb_cnt[v] < 0 || mb_cnt[v] > (int32_t)K)
+            return -1;
+    for (size_t v = 0; v < N; ++v) {
+        c->mb_cnt[v] = mb_cnt[v];
+        for (size_t j = 0; j < K; ++j) {
+            const int used = (int32_t)j < mb_cnt[v];
+            for (size_t k = 0; k < D_m; ++k)
+                c->mb[(v * K + j) * D_m + k] = used ? mb[(v * K + j) * D_m + k] : 0.0;
+            c->mb_ts[v * K + j] = used ? mb_ts[v * K + j] : 0.0;
+        }
+    }
+    return 0;
+}
+
 /* Enables (on != 0) the staleness mitigation of step 3b with quantile p,
  * blend weight lambda and at most K similar nodes. */
 int orc_set_mitigation(void *p, int on, double pq, double lambda, int K)

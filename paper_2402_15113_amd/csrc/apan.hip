@@ -163,13 +163,14 @@ __global__ __launch_bounds__(256) void k_apan_attn(AttnArgs2 a)
 }
 
 // q . b_k per node (the common part of every score), one wavefront per node
-__global__ __launch_bounds__(256) void k_apan_qb(int cap, int M, const float *__restrict__ Q,
+__global__ __launch_bounds__(256) void k_apan_qb(const int32_t *__restrict__ n_nodes, int cap,
+                                                 int M, const float *__restrict__ Q,
                                                  const float *__restrict__ b_k,
                                                  float *__restrict__ qb)
 {
     const int p = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
     const int lane = threadIdx.x & 63;
-    if (p >= cap)
+    if (p >= min(*n_nodes, cap))
         return;
     float acc = 0.f;
     for (int k = lane; k < M; k += kWave)
@@ -439,6 +440,34 @@ __global__ __launch_bounds__(256) void k_apan_read_mb(int32_t N, int K, int D_m,
     }
 }
 
+// Mailboxes given oldest first with their counts into the rings: mail j at
+// slot j, head = count mod K; counts are clamped to [0, K].
+__global__ __launch_bounds__(256) void k_apan_load_mb(int32_t N, int K, int D_m,
+                                                      const float *__restrict__ in,
+                                                      const double *__restrict__ in_ts,
+                                                      const int32_t *__restrict__ in_cnt,
+                                                      float *__restrict__ mb,
+                                                      double *__restrict__ mb_ts,
+                                                      int32_t *__restrict__ head,
+                                                      int32_t *__restrict__ cnt)
+{
+    const int v = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
+    const int lane = threadIdx.x & 63;
+    if (v >= N)
+        return;
+    const int c = min(max(in_cnt[v], 0), K);
+    for (int j = 0; j < c; ++j) {
+        wave_copy_row(mb + ((int64_t)v * K + j) * D_m, in + ((int64_t)v * K + j) * D_m, D_m,
+                      lane);
+        if (lane == 0)
+            mb_ts[(int64_t)v * K + j] = in_ts[(int64_t)v * K + j];
+    }
+    if (lane == 0) {
+        head[v] = c % K;
+        cnt[v] = c;
+    }
+}
+
 __global__ void k_apan_init(int32_t N, int M, int K, int D_m, float *__restrict__ mem,
                             double *__restrict__ mem_ts, int32_t *__restrict__ ver,
                             float *__restrict__ mb, double *__restrict__ mb_ts,
@@ -703,11 +732,11 @@ extern "C" tgm_status_t tgm_apan_step(tgm_apan_t a, tgm_graph_t g, int64_t iter,
                    dim3(256), 0, s, sb->n_nodes, cap, M, D_t, a->f_mem, a->omega, a->beta,
                    a->Xq);
         TGM_TRY_STATUS(gemm_f32(false, true, cap, M, M + D_t, a->Xq, M + D_t, a->W_q, M + D_t,
-                                a->Q, M, a->b_q, false, s));
+                                a->Q, M, a->b_q, false, s, sb->n_nodes));
         TGM_TRY_STATUS(gemm_f32(false, false, cap, D_x, M, a->Q, M, a->W_k, D_x, a->U, D_x,
-                                nullptr, false, s));
+                                nullptr, false, s, sb->n_nodes));
         TGM_LAUNCH(k_apan_qb, dim3((unsigned)cdiv((int64_t)cap * kWave, 256)), dim3(256), 0, s,
-                   cap, M, a->Q, a->b_k, a->qb);
+                   sb->n_nodes, cap, M, a->Q, a->b_k, a->qb);
         AttnArgs2 aa{sb->n_nodes, cap, M, D_m, D_t, K, 1.f / sqrtf((float)M), a->U, a->qb,
                      a->f_mb, a->f_mb_ts, a->f_mem_ts, a->omega, a->beta, a->f_cnt, a->X,
                      a->t_new};
@@ -715,9 +744,9 @@ extern "C" tgm_status_t tgm_apan_step(tgm_apan_t a, tgm_graph_t g, int64_t iter,
                    aa);
         // the GRU on [aggregate || phi(t_newest - mem_ts)]
         TGM_TRY_STATUS(gemm_f32(false, true, cap, 3 * M, D_x, a->X, D_x, a->W_ih, D_x, a->Gx,
-                                3 * M, a->b_ih, false, s));
+                                3 * M, a->b_ih, false, s, sb->n_nodes));
         TGM_TRY_STATUS(gemm_f32(false, true, cap, 3 * M, M, a->f_mem, M, a->W_hh, M, a->Gh,
-                                3 * M, a->b_hh, false, s));
+                                3 * M, a->b_hh, false, s, sb->n_nodes));
         TGM_LAUNCH(k_apan_gru, dim3((unsigned)cdiv((int64_t)cap * M, 256)), dim3(256), 0, s,
                    sb->n_nodes, cap, M, a->f_cnt, a->Gx, a->Gh, a->f_mem, mem_new);
         if (new_mem_ts)
@@ -759,6 +788,46 @@ extern "C" tgm_status_t tgm_apan_step(tgm_apan_t a, tgm_graph_t g, int64_t iter,
     sl.n_del = n_del;
     sl.staged = true;
     a->staged_through = iter;
+    return TGM_OK;
+}
+
+namespace {
+
+void apan_restart(tgm_apan *a, int64_t iter)
+{
+    for (tgm_apan::Slot &sl : a->ring)
+        sl = tgm_apan::Slot{};
+    a->committed_through = iter - 1;
+    a->staged_through = iter - 1;
+}
+
+}  // namespace
+
+extern "C" tgm_status_t tgm_apan_reset(tgm_apan_t a, void *stream)
+{
+    if (!a)
+        return TGM_EINVAL;
+    hipStream_t s = as_stream(stream);
+    TGM_LAUNCH(k_apan_init, dim3(1024), dim3(256), 0, s, a->N, a->M, a->K, a->D_m, a->mem,
+               a->mem_ts, a->ver, a->mb, a->mb_ts, a->head, a->cnt);
+    apan_restart(a, 0);
+    return TGM_OK;
+}
+
+extern "C" tgm_status_t tgm_apan_load(tgm_apan_t a, int64_t iter, const float *mem,
+                                      const double *mem_ts, const int32_t *ver, const float *mb,
+                                      const double *mb_ts, const int32_t *mb_cnt, void *stream)
+{
+    if (!a || iter < 0 || !mem || !mem_ts || !ver || !mb || !mb_ts || !mb_cnt)
+        return TGM_EINVAL;
+    hipStream_t s = as_stream(stream);
+    const size_t N = a->N, M = a->M;
+    TGM_HIP(hipMemcpyAsync(a->mem, mem, 4 * N * M, hipMemcpyDeviceToDevice, s));
+    TGM_HIP(hipMemcpyAsync(a->mem_ts, mem_ts, 8 * N, hipMemcpyDeviceToDevice, s));
+    TGM_HIP(hipMemcpyAsync(a->ver, ver, 4 * N, hipMemcpyDeviceToDevice, s));
+    TGM_LAUNCH(k_apan_load_mb, dim3((unsigned)cdiv((int64_t)N * kWave, 256)), dim3(256), 0, s,
+               a->N, a->K, a->D_m, mb, mb_ts, mb_cnt, a->mb, a->mb_ts, a->head, a->cnt);
+    apan_restart(a, iter);
     return TGM_OK;
 }
 

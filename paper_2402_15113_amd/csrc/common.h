@@ -676,10 +676,12 @@ struct ModelParams {
 tgm_status_t model_repack(tgm_model_t m, const ModelParams &w, hipStream_t s);
 
 // C[m x n] = op(A) op(B) (+ bias[n]) (+ C when accumulate), fp32 MFMA, no
-// split of the reduction (the GEMM of the training step; op as there).
+// split of the reduction (the GEMM of the training step; op as there).  With
+// m_live (device, may be NULL) only the rows below min(m, *m_live) are
+// computed; the rest of C is left as it was.
 tgm_status_t gemm_f32(bool ta, bool tb, int m, int n, int k, const float *A, int lda,
                       const float *B, int ldb, float *C, int ldc, const float *bias,
-                      bool accumulate, hipStream_t s);
+                      bool accumulate, hipStream_t s, const int32_t *m_live = nullptr);
 
 // The training step of one iteration (tgm_train_step) on stream s, from the
 // iteration's sample and fetch buffers, new memories and embeddings.

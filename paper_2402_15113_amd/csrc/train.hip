@@ -46,6 +46,7 @@ struct GemmArgs {
     int accumulate;
     int splits, kchunk;
     float *part;
+    const int32_t *m_live;   // rows at or past *m_live are skipped (NULL: none)
 };
 
 template <bool TA, bool TB>
@@ -55,6 +56,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
     __shared__ __align__(16) float Bs[kGT][kGK + kGPad];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m0 = blockIdx.y * kGT, n0 = blockIdx.x * kGT, z = blockIdx.z;
+    if (g.m_live && m0 >= *g.m_live)
+        return;   // the whole tile is past the live rows
     const int k_lo = z * g.kchunk, k_hi = min(g.k, k_lo + g.kchunk);
     const int wr = (wave >> 1) * 32, wc = (wave & 1) * 32;
     const int q = lane >> 4, rl = lane & 15;
@@ -746,6 +749,7 @@ tgm_status_t gemm(const tgm_trainer *tr, bool ta, bool tb, int m, int n, int k, 
     g.bias = bias;
     g.accumulate = accumulate ? 1 : 0;
     g.part = tr->part;
+    g.m_live = nullptr;
     const int64_t tiles = cdiv(m, kGT) * cdiv(n, kGT);
     int splits = 1;
     if (tiles < 512 && k > 4 * kGK * 16) {
@@ -783,7 +787,7 @@ tgm_status_t colsum(const tgm_trainer *tr, int rows, int n, const float *X, int 
 
 tgm_status_t tgm::gemm_f32(bool ta, bool tb, int m, int n, int k, const float *A, int lda,
                           const float *B, int ldb, float *C, int ldc, const float *bias,
-                          bool accumulate, hipStream_t s)
+                          bool accumulate, hipStream_t s, const int32_t *m_live)
 {
     if (m <= 0 || n <= 0)
         return TGM_OK;
@@ -800,6 +804,7 @@ tgm_status_t tgm::gemm_f32(bool ta, bool tb, int m, int n, int k, const float *A
     g.bias = bias;
     g.accumulate = accumulate ? 1 : 0;
     g.part = nullptr;
+    g.m_live = m_live;
     g.splits = 1;
     g.kchunk = round_up((int32_t)std::max(k, 1), kGK);
     const dim3 grid((unsigned)cdiv(n, kGT), (unsigned)cdiv(m, kGT), 1);

@@ -254,6 +254,10 @@ class Stage:
         return dict(mem=mem.cpu().numpy(), mem_ts=mem_ts.cpu().numpy(), mail=mail.cpu().numpy(),
                     mail_ts=mail_ts.cpu().numpy(), ver=ver.cpu().numpy())
 
+    def reset(self):
+        """The initial state again; the next iteration is 0."""
+        tgm.tgm_state_reset(self.st, stream=self.stream)
+
     def load_state(self, it, mem, mem_ts, mail, mail_ts, ver):
         dev = self.dev
         T = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
@@ -281,14 +285,19 @@ class ApanStage:
     (fetch with the mailboxes, mailbox attention and GRU, identity
     embedding, staged write set with the propagated mails) per iteration."""
 
-    def __init__(self, wl, w, *, s=None, device="cuda", stream=None):
+    def __init__(self, wl, w, *, s=None, device="cuda", stream=None, efeat=None):
+        """``efeat``: a device edge-feature table to use instead of the
+        workload's host one."""
         dev = torch.device(device)
         self.dev, self.wl = dev, wl
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
         T = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
         self.src, self.dst = T(wl.src, torch.int32), T(wl.dst, torch.int32)
         self.t, self.neg = T(wl.t, torch.float64), T(wl.neg, torch.int32)
-        self.efeat = None if wl.efeat is None else T(wl.efeat, torch.float32)
+        if efeat is not None:
+            self.efeat = efeat
+        else:
+            self.efeat = None if wl.efeat is None else T(wl.efeat, torch.float32)
         self.N, self.M, self.nb, self.B = wl.N, wl.M, wl.nb, wl.B
         self.s = wl.s if s is None else s
         self.K = int(w.K_mb)
@@ -319,6 +328,28 @@ class ApanStage:
                           self.h, stream=self.stream)
         self.last = (i, n)
 
+    def run(self, i0: int, n: int):
+        """Iterations i0 .. i0 + n - 1, one after another on the stream."""
+        for i in range(i0, i0 + n):
+            self.step(i)
+
+    def reset(self):
+        tgm.tgm_apan_reset(self.a, stream=self.stream)
+
+    def load_state(self, it, mem, mem_ts, ver, mb, mb_ts, mb_cnt):
+        """Committed tables at iteration ``it`` (host arrays or device
+        tensors, the layouts of ``state()``); the next step is ``it``."""
+        dev = self.dev
+
+        def T(a, dt):
+            if isinstance(a, torch.Tensor):
+                return a.to(dev, dt).contiguous()
+            return torch.from_numpy(np.ascontiguousarray(a)).to(dev, dt)
+        keep = (T(mem, torch.float32), T(mem_ts, torch.float64), T(ver, torch.int32),
+                T(mb, torch.float32), T(mb_ts, torch.float64), T(mb_cnt, torch.int32))
+        tgm.tgm_apan_load(self.a, it, *keep, stream=self.stream)
+        self.stream.synchronize()
+
     def outputs(self):
         """Host copies of the last iteration's node set, fetched rows and
         mailboxes (oldest first), new memories and embeddings (synchronises)."""
@@ -342,14 +373,33 @@ class ApanStage:
     def flush(self):
         tgm.tgm_apan_flush(self.a, stream=self.stream)
 
-    def state(self):
+    def counts(self):
+        """Sizes of the last iteration (synchronises): events, roots, valid
+        sampled slots, node-set size, nodes with mail, fetched mails."""
+        i, n = self.last
+        torch.cuda.synchronize(self.dev)
+        nU = int(self.sb.n_nodes.item())
+        R = 3 * n
+        cnt = torch.empty(self.cap, dtype=torch.int32, device=self.dev)
+        tgm.tgm_apan_fetched(self.a, mb_cnt=cnt, stream=self.stream)
+        c = cnt[:nU]
+        return dict(b=n, R=R, slots=int(self.sb.cnt[:R].sum().item()), n_U=nU,
+                    n_mail=int((c > 0).sum().item()), n_mails=int(c.sum().item()))
+
+    def device_state(self):
+        """The committed tables as device tensors (mem, mem_ts, ver, mb, mb_ts,
+        mb_cnt: the arguments of ``load_state``); ordered on the stream."""
         dev, N, M, K, D_m = self.dev, self.N, self.M, self.K, self.D_m
         e = lambda shape, dt: torch.empty(shape, dtype=dt, device=dev)
         mem, mem_ts, ver = e((N, M), torch.float32), e(N, torch.float64), e(N, torch.int32)
         mb, mb_ts, cnt = e((N, K, D_m), torch.float32), e((N, K), torch.float64), \
             e(N, torch.int32)
         tgm.tgm_apan_read(self.a, mem, mem_ts, ver, mb, mb_ts, cnt, stream=self.stream)
-        torch.cuda.synchronize(dev)
+        return mem, mem_ts, ver, mb, mb_ts, cnt
+
+    def state(self):
+        mem, mem_ts, ver, mb, mb_ts, cnt = self.device_state()
+        torch.cuda.synchronize(self.dev)
         c = lambda x: x.cpu().numpy()
         return dict(mem=c(mem), mem_ts=c(mem_ts), ver=c(ver), mb=c(mb), mb_ts=c(mb_ts),
                     mb_cnt=c(cnt))

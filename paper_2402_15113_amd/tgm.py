@@ -32,6 +32,7 @@ SYMBOLS = ["tgm_status_str", "tgm_last_device_error", "tgm_version", "tgm_alloc_
            "tgm_mitigate_noalloc", "tgm_trainer_create", "tgm_trainer_destroy",
            "tgm_trainer_info", "tgm_trainer_read", "tgm_train_step", "tgm_state_set_training",
            "tgm_apan_create", "tgm_apan_destroy", "tgm_apan_step", "tgm_apan_flush",
+           "tgm_apan_reset", "tgm_apan_load",
            "tgm_apan_read", "tgm_apan_fetched",
            "tgm_embed_projection",
            "tgm_profile_enable", "tgm_profile_reset", "tgm_profile_count", "tgm_profile_get"]
@@ -148,6 +149,8 @@ def lib():
             "tgm_apan_destroy": [V],
             "tgm_apan_step": [V, V, I64, C.POINTER(SampleBuffers), I32, P, P, P, V],
             "tgm_apan_flush": [V, V],
+            "tgm_apan_reset": [V, V],
+            "tgm_apan_load": [V, I64, P, P, P, P, P, P, V],
             "tgm_apan_read": [V, P, P, P, P, P, P, V],
             "tgm_apan_fetched": [V, P, P, P, P, P, P, V],
             "tgm_mitigator_create": [I32, I32, I32, C.POINTER(V)],
@@ -468,6 +471,15 @@ def tgm_apan_step(a, g, it, sample_bufs, cap, mem_new, new_mem_ts, h, stream=Non
 
 def tgm_apan_flush(a, stream=None):
     _check("tgm_apan_flush", lib().tgm_apan_flush(a, _s(stream)))
+
+
+def tgm_apan_reset(a, stream=None):
+    _check("tgm_apan_reset", lib().tgm_apan_reset(a, _s(stream)))
+
+
+def tgm_apan_load(a, it, mem, mem_ts, ver, mb, mb_ts, mb_cnt, stream=None):
+    _check("tgm_apan_load", lib().tgm_apan_load(a, it, _p(mem), _p(mem_ts), _p(ver), _p(mb),
+                                                _p(mb_ts), _p(mb_cnt), _s(stream)))
 
 
 def tgm_apan_read(a, mem=None, mem_ts=None, ver=None, mb=None, mb_ts=None, mb_cnt=None,

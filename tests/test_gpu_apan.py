@@ -20,13 +20,28 @@ def _gpu():
     tgm.lib()
 
 
-def apan_pair(orc, wl, w, n=None, s=None):
+def apan_state(wl, j, K, seed):
+    """Seeded committed tables at iteration j: memories, times and versions,
+    and mailboxes whose mails are older than batch j."""
+    from test_gpu_parity import synthetic_state
+    from workloads import synthetic_mailbox
+    st = synthetic_state(wl, j, seed)
+    mb, mb_ts, cnt = synthetic_mailbox(wl.N, K, wl.D_m, wl.t[wl.batch(j)[0] - 1], seed + 1)
+    return st, (mb, mb_ts, cnt)
+
+
+def apan_pair(orc, wl, w, n=None, s=None, first=0, init=None, efeat=None):
     from paper_2402_15113_amd.stage import ApanStage
     from test_gpu_parity import close, exact
-    st = ApanStage(wl, w, s=s)
+    st = ApanStage(wl, w, s=s, efeat=efeat)
     o = orc.Oracle(wl, w, s=s)
-    n = wl.n_iters if n is None else n
-    for i in range(n):
+    if init is not None:
+        tab, (mb, mb_ts, cnt) = init
+        st.load_state(first, tab["mem"], tab["mem_ts"], tab["ver"], mb, mb_ts, cnt)
+        o.set_state(first, **tab)
+        o.set_mailbox(mb, mb_ts, cnt)
+    n = (wl.n_iters - first) if n is None else n
+    for i in range(first, first + n):
         print(f"[apan] {wl.name} K={w.K_mb} propagate={w.propagate} s={st.s} iter {i}",
               flush=True)
         st.step(i)
@@ -88,6 +103,52 @@ def test_apan_lastfm_window(orc):
     wl = make_workload("lastfm", E=12 * 2000)
     w = make_weights(wl.M, wl.D_e, wl.D_t, model="apan", K_mb=10)
     apan_pair(orc, wl, w)
+
+
+def test_apan_wiki_from_loaded_state(orc):
+    """A mid-run WIKI window from seeded tables and mailboxes (s = 2: the
+    loaded tables plus the window's own write sets from i - 3 on)."""
+    wl = make_workload("wiki", E=60_000)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, model="apan", K_mb=10)
+    apan_pair(orc, wl, w, n=6, first=60, init=apan_state(wl, 60, 10, 7))
+
+
+def test_apan_gdelt_window(orc):
+    """GDELT-shaped batches 20,000 .. 20,001 (B 4000, node sets near all 16,682
+    nodes, mailboxes of 10 mails of 386 values) from seeded tables on the
+    graph of their first 80 M events."""
+    import dataclasses
+    from test_gpu_parity import gdelt_prefix, sparse_features, window_rows
+    j, n = 20_000, 2
+    wl = gdelt_prefix((j + n) * 4000)
+    rows = window_rows(orc, wl, j, n)
+    host, dev = sparse_features(wl, rows)
+    wl = dataclasses.replace(wl, efeat=host)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, model="apan", K_mb=10)
+    apan_pair(orc, wl, w, n=n, first=j, init=apan_state(wl, j, 10, 11), efeat=dev)
+    del dev
+    torch.cuda.empty_cache()
+
+
+def test_apan_reset_repeats_the_run():
+    from paper_2402_15113_amd.stage import ApanStage
+    wl = make_workload("wiki", E=24 * 400)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, model="apan", K_mb=6)
+    st = ApanStage(wl, w)
+    outs = []
+    for rep in range(2):
+        if rep:
+            st.reset()
+        for i in range(wl.n_iters):
+            st.step(i)
+        st.flush()
+        outs.append((st.outputs(), st.state()))
+    (o1, s1), (o2, s2) = outs
+    for k in o1:
+        assert np.array_equal(np.asarray(o1[k]), np.asarray(o2[k])), k
+    for k in s1:
+        assert np.array_equal(s1[k], s2[k]), k
+    st.close()
 
 
 def test_apan_protocol_and_limits():

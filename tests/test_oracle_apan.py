@@ -165,3 +165,40 @@ def test_scores_follow_the_age_of_each_mail(orc):
             np.testing.assert_allclose(r.s_new[k], want, rtol=0, atol=1e-12)
             n += 1
     assert n > 50
+
+
+def test_loaded_state_continues_the_run(orc):
+    """set_state + set_mailbox at iteration j from a run's flushed tables:
+    with s = 0 (every write set committed before the next fetch) the loaded
+    oracle must continue exactly as the run itself; a mailbox loaded in the
+    wrong order or with dropped counts changes the next attention."""
+    wl = make_workload("tiny", E=4000, s=0)
+    w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random", model="apan", K_mb=4)
+    j = 6
+    a, _ = _run(orc, wl, w, s=0, n=j)
+    a.flush()
+    st = a.state()
+    mb, mb_ts, cnt = a.mailbox()
+    assert (cnt == 4).sum() > 0 and ((cnt > 0) & (cnt < 4)).sum() > 0
+    b = orc.Oracle(wl, w, s=0)
+    b.set_state(j, **st)
+    b.set_mailbox(mb, mb_ts, cnt)
+    for _ in range(4):
+        ra, rb = a.step(), b.step()
+        for k in ("f_mem", "f_mb", "f_mb_ts", "f_mb_cnt", "s_new", "h"):
+            assert np.array_equal(getattr(ra, k), getattr(rb, k)), k
+    # the same mails in reverse order: different scores, different updates
+    c = orc.Oracle(wl, w, s=0)
+    c.set_state(j, **st)
+    rev = np.array(mb)
+    rts = np.array(mb_ts)
+    for v in np.nonzero(cnt > 1)[0]:
+        rev[v, :cnt[v]] = mb[v, :cnt[v]][::-1]
+        rts[v, :cnt[v]] = mb_ts[v, :cnt[v]][::-1]
+    c.set_mailbox(rev, rts, cnt)
+    a2 = orc.Oracle(wl, w, s=0)
+    a2.set_state(j, **st)
+    a2.set_mailbox(mb, mb_ts, cnt)
+    assert not np.array_equal(c.step().s_new, a2.step().s_new)
+    with pytest.raises(ValueError):
+        c.set_mailbox(mb, mb_ts, np.full_like(cnt, 5))

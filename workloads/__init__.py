@@ -387,3 +387,16 @@ def make_weights(M: int, D_e: int, D_t: int, *, seed: int = 0,
         W_o=_uniform(r("W_o"), (M, d_a + M), d_a + M),
         b_o=_uniform(r("b_o"), (M,), d_a + M),
     )
+
+
+def synthetic_mailbox(N: int, K: int, D_m: int, t_end: float, seed: int = 0):
+    """A seeded APAN mailbox state (rows [N x K x D_m] and times [N x K],
+    oldest mail first, zero past the count; counts [N]): 70 % of the nodes hold
+    K mails, the rest 0 .. K-1; mail rows N(0, 1) rounded to fp32; each
+    mailbox's times are non-decreasing whole seconds before t_end."""
+    r = np.random.default_rng(seed)
+    cnt = np.where(r.random(N) < 0.7, K, r.integers(0, K, N)).astype(np.int32)
+    used = np.arange(K)[None, :] < cnt[:, None]
+    mb = r.standard_normal((N, K, D_m)).astype(np.float32).astype(np.float64) * used[:, :, None]
+    ts = np.sort(np.floor(r.uniform(0, max(t_end, 1.0), (N, K))), axis=1) * used
+    return mb, ts, cnt
