@@ -342,10 +342,13 @@ def work_model(wl, rows, model="tgn"):
     k["k_mit_prep"] = dict(flops=0, bytes=n_U * (4 + 8 + 8 + nb * 16 + nb * 4 + 4))
     k["k_mit_select"] = dict(flops=0, bytes=n_U * 8 * 9)
     k["k_mit_omega"] = dict(flops=0, bytes=n_U * (8 + 4 + nb * 4))
-    # the attention with the query folded into the key weights computes the
-    # same embedding: the same algorithmic work
+    # the attention with the query folded into the key weights, and the one
+    # that aggregates the slot rows before projecting them, compute the same
+    # embedding: the same algorithmic work (they execute less of it)
     k["k_attn_fold"] = dict(k["k_attn"])
     k["k_attn_fold_gather"] = dict(k["k_attn_gather"])
+    k["k_attn_agg"] = dict(k["k_attn"])
+    k["k_attn_agg_gather"] = dict(k["k_attn_gather"])
     return k
 
 

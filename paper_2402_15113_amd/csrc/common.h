@@ -162,6 +162,9 @@ struct tgm_model {
     float *pbias = nullptr;   // [PNB*16] bias of the node projection: c_q | b_k | b_v | 0
     // attention with the query folded into the key weights (when the shapes fit)
     bool fold = false;
+    // attention by aggregation of the slot rows (when the shapes fit; it
+    // reads the folded attention's packed operands)
+    bool agg = false;
     int32_t VNB = 0, DC = 0;             // 16-col blocks of M, 16-wide chunks of M
     tgm::f4 *v_b = nullptr;              // [KFC(+pad)][VNB][64]: V part of the slot weights
     tgm::f4 *uk_a = nullptr;             // [DC][KFC][64]: W_k^t as A fragments

@@ -1789,6 +1789,403 @@ __global__ __launch_bounds__(512) void k_attn_fold_gather(AttnArgs g, int n_attn
         gather_rows(gp, p, nn, threadIdx.x & 63);
 }
 
+// ---------------------------------------------------------------------------
+// Attention by aggregation.  The value projection is linear, so for root r
+// and head eta, with weights alpha_s over the root's slots s,
+//   o_r,eta = sum_s alpha_s (W_v,a a_s + seedV_s)_eta
+//           = (W_v,a abar_r,eta)_eta + (sum_s alpha_s seedV_s)_eta,
+//   abar_r,eta = sum_s alpha_s a_s,
+// and each score is (a_s . U_r,eta + seedK_s . q_r,eta) / sqrt(d_h) with
+// U_r,eta = W_k,a^t q_r,eta (Eq. 1's emb() restated by linearity; a_s =
+// [phi || efeat] the slot row, seedK_s / seedV_s the neighbour's key / value
+// part of P, the node projection plus the bias).  The per-slot work is one dot
+// product and one axpy of a_s per head, on the VALU; the GEMMs run once per
+// (root, head) row: U, the value projection of the aggregates and the output
+// projection, each a single 16-row MFMA block per workgroup (RT roots, RT H
+// <= 16 rows, row n = root * H + head).
+// Wavefront w owns root r0 + w; phases, separated by barriers:
+//   1. every wave: the query fragments of all RT roots, then its U tiles (16
+//      columns of k each) -> LDS Us, and its 16-slot block of the seed part
+//      seedK_s . q (K = M, the neighbours' key rows of P) -> LDS Sk; its own
+//      root's slot metadata and slot rows a_s, in registers (lane l holds
+//      columns l + 64 i);
+//   2. scores (wave reductions), softmax, abar -> LDS As; the aggregate of the
+//      value seeds and s'_r -> LDS AO;
+//   3. value GEMM, wave cb taking column block cb; a column is kept for the
+//      row of its own head and added into AO;
+//   4. output GEMM h = ReLU(W_o [o || s'_r] + b_o).
+// LDS: 2 x 16 rows of the slot-row width and 16 rows of [o || s'_r], about
+// 53 KB at the GDELT-shaped sizes, so that two workgroups share a CU.
+constexpr int kAggCols = 5;     // slot-row columns per lane (KF <= 320)
+constexpr int kAggTCols = 2;    // of them time codes (D_t <= 128)
+constexpr int kAggDC = 7;       // 16-wide chunks of M (M <= 112)
+constexpr int kAggUT = 3;       // U tiles per wave (KFC <= 24)
+constexpr int kAggMaxH = 4;
+constexpr int kAggMaxKC = 24;   // k-chunks of the value GEMM (KFC) and of the output one (OC)
+constexpr int kAggRing = 8;     // weight chunks in flight per wave in those GEMMs
+
+// Sum over the wavefront, the same in every lane: DPP sums inside each 16-lane
+// row, then the four row sums (lanes 0, 16, 32, 48) read as scalars and added
+// in that order.
+__device__ __forceinline__ float wave_sum_rows(float v)
+{
+    v = row16_sum(v);
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
+// One GEMM of a 16-row A block in LDS (k-chunks of 16 columns) against packed
+// B chunks (kc * bstep apart): the first kAggRing chunks are already in `ring`
+// (loaded by the caller before the barrier that publishes A); a slot is
+// refilled with the chunk kAggRing further on right after its MFMAs are
+// issued (indices clamped: the last rounds reload the last chunk).
+__device__ __forceinline__ f4 agg_gemm(const float *arow, const f4 *pw, int64_t bstep, int KC,
+                                       f4 (&ring)[kAggRing])
+{
+    f4 acc = f4{0, 0, 0, 0};
+    int kc0 = 0;
+    for (; kc0 + kAggRing <= KC; kc0 += kAggRing) {
+#pragma unroll
+        for (int i = 0; i < kAggRing; ++i) {
+            const f4 a = *reinterpret_cast<const f4 *>(arow + 16 * (kc0 + i));
+            acc = mfma_k16(a, ring[i], acc);
+            ring[i] = pw[min(kc0 + kAggRing + i, KC - 1) * bstep];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kAggRing; ++i)
+        if (kc0 + i < KC) {
+            const f4 a = *reinterpret_cast<const f4 *>(arow + 16 * (kc0 + i));
+            acc = mfma_k16(a, ring[i], acc);
+        }
+    return acc;
+}
+
+__device__ __forceinline__ void agg_ring_load(const f4 *pw, int64_t bstep, int KC,
+                                              f4 (&ring)[kAggRing])
+{
+#pragma unroll
+    for (int i = 0; i < kAggRing; ++i)
+        ring[i] = pw[min(i, KC - 1) * bstep];
+}
+
+template <int NBM>   // slots per root held in registers (nb <= NBM)
+__device__ __forceinline__ void attn_agg_block(const AttnArgs &g, float *lds, int bid)
+{
+    const int RT = g.RT;
+    const int r0 = bid * RT;
+    const int nroots = min(RT, g.R - r0);
+    if (nroots <= 0)
+        return;
+    const int M = g.M, nb = g.nb, D_e = g.D_e, D_t = g.D_t, H = g.H;
+    const int KFC = g.KFC, DC = g.DC, VNB = g.VNB, OC = g.OC, ONB = g.ONB;
+    const int KF = D_t + D_e;
+    const int KFP = KFC * 16 + 4, SAO = OC * 16 + 4;
+    const int d_h = M / H;
+    const int n = *g.n_nodes;   // positions and event ids are bounds-checked
+    float *Us = lds;              // [16][KFP]: U rows (r, eta)
+    float *As = Us + 16 * KFP;    // [16][KFP]: abar rows (r, eta)
+    float *AO = As + 16 * KFP;    // [16][SAO]: [o || s'_r || 0]
+    float *Sk = AO + 16 * SAO;    // [RT nb][H]: seedK_s . q_r(s),eta
+    const int tid = threadIdx.x, lane = tid & 63, q4 = 4 * (lane >> 4);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int cn = lane & 15, cr = cn / H, ce = cn - cr * H;
+    const bool own = wave < nroots;
+    const int r = r0 + min(wave, nroots - 1);
+    const bool seeds = wave * 16 < nroots * nb;   // this wave has a 16-slot seed block
+
+    // 1a. loads that depend on nothing: the first U tile's W_k,a^t fragments,
+    // then the indices: the query columns' roots, the seed block's slots, the
+    // own root's slots (lane j < nb: slot j)
+    f4 ua[kAggDC];
+#pragma unroll
+    for (int dc = 0; dc < kAggDC; ++dc)
+        ua[dc] = g.uk_a[((int64_t)min(dc, DC - 1) * KFC + min(wave, KFC - 1)) * kWave + lane];
+    const int qpos = g.root_pos[r0 + min(cr, nroots - 1)];
+    const int sr = wave * 16 + cn;
+    const int sw = min(sr / nb, nroots - 1), sj = sr - (sr / nb) * nb;
+    const int spos = g.nbr_pos[(int64_t)(r0 + sw) * nb + sj];
+    const int c = own ? g.cnt[r] : 0;
+    const int pv = g.root_pos[r];
+    const double t_root = g.root_ts[r];
+    int my_e = -1, my_np = -1;
+    double my_dt = 0.0;
+    if (lane < nb) {
+        const int64_t sl = (int64_t)r * nb + lane;
+        const int64_t e = g.eid[sl];
+        const int q = g.nbr_pos[sl];
+        my_e = (lane < c && D_e > 0 && e >= 0 && e < g.E) ? (int)e : -1;
+        my_np = (lane < c && q >= 0 && q < n) ? q : -1;
+        my_dt = t_root - g.nts[sl];
+    }
+    const bool pv_ok = own && pv >= 0 && pv < n;
+    issue_fence();
+
+    // 1b. query fragments (B operand of the U and seed GEMMs): lane l holds q of
+    // column n = l % 16 (root n / H, head n % H) for d = 16 dc + 4 (l / 16) + j,
+    // zero outside the head, past M and for a column without a root
+    f4 bq[kAggDC];
+    {
+        const bool ok = cr < nroots && qpos >= 0 && qpos < n;
+        const float *qrow = ok ? g.P + (int64_t)qpos * g.ldP : g.pbias;
+#pragma unroll
+        for (int dc = 0; dc < kAggDC; ++dc)
+            bq[dc] = *reinterpret_cast<const f4 *>(qrow + min(16 * dc + q4, M - 4));
+    }
+    issue_fence();
+    {
+        const int lo = ce * d_h, hi = cr < nroots ? lo + d_h : lo;
+#pragma unroll
+        for (int dc = 0; dc < kAggDC; ++dc)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int d = 16 * dc + q4 + j;
+                if (!(dc < DC && d >= lo && d < hi))
+                    bq[dc][j] = 0.f;
+            }
+    }
+    // 1c. U tiles kb = wave + 8 t: U^t[16 kb .. +16][n] = W_k,a^t q_n; the next
+    // tile's fragments load while this one multiplies
+#pragma unroll
+    for (int t = 0; t < kAggUT; ++t) {
+        const int kb = wave + kMaxWaves * t;
+        if (kb < KFC) {
+            f4 cur[kAggDC];
+#pragma unroll
+            for (int dc = 0; dc < kAggDC; ++dc)
+                cur[dc] = ua[dc];
+            if (kb + kMaxWaves < KFC) {
+#pragma unroll
+                for (int dc = 0; dc < kAggDC; ++dc)
+                    ua[dc] = g.uk_a[((int64_t)min(dc, DC - 1) * KFC + kb + kMaxWaves) * kWave +
+                                    lane];
+            }
+            issue_fence();
+            f4 acc = f4{0, 0, 0, 0};
+#pragma unroll
+            for (int dc = 0; dc < kAggDC; ++dc)   // bq is zero past M
+                acc = mfma_k16(cur[dc], bq[dc], acc);
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                Us[cn * KFP + 16 * kb + q4 + v] = acc[v];
+        }
+    }
+    // 1d. the seed part of the scores: rows = the workgroup's slots (root
+    // s / nb, slot s % nb), A = the neighbours' key rows of P (b_k for a slot
+    // without one); kept for the slot's own root
+    f4 sa[kAggDC];
+    {
+        const float *krow = ((spos >= 0 && spos < n) ? g.P + (int64_t)spos * g.ldP : g.pbias) + M;
+#pragma unroll
+        for (int dc = 0; dc < kAggDC; ++dc)
+            sa[dc] = *reinterpret_cast<const f4 *>(krow + min(16 * dc + q4, M - 4));
+    }
+    issue_fence();
+    if (seeds) {
+        f4 acc = f4{0, 0, 0, 0};
+#pragma unroll
+        for (int dc = 0; dc < kAggDC; ++dc)
+            acc = mfma_k16(sa[dc], bq[dc], acc);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int srow = wave * 16 + q4 + v;
+            if (srow < nroots * nb && cr == srow / nb)
+                Sk[srow * H + ce] = acc[v];
+        }
+    }
+    // 1e. the own root's slot rows: edge features (HBM), then the time codes
+    // phi(t_root - t_slot) computed while those are in flight
+    float xs[NBM][kAggCols];   // slot j's columns lane + 64 i
+#pragma unroll
+    for (int j = 0; j < NBM; ++j) {
+        // the slot's event id, the same in every lane (a scalar base address)
+        const int ej = __builtin_amdgcn_readfirstlane(__shfl(my_e, j, kWave));
+        const float *erow = g.efeat + (int64_t)max(ej, 0) * D_e - D_t;
+#pragma unroll
+        for (int i = 0; i < kAggCols; ++i) {
+            const int k = lane + kWave * i;
+            float x = 0.f;
+            if (j < c && ej >= 0 && k >= D_t && k < KF)
+                x = erow[k];
+            xs[j][i] = x;
+        }
+    }
+    issue_fence();
+    {
+        double om[kAggTCols], be[kAggTCols];
+#pragma unroll
+        for (int i = 0; i < kAggTCols; ++i) {
+            const int k = min(lane + kWave * i, max(D_t - 1, 0));
+            om[i] = D_t > 0 ? g.omega[k] : 0.0;
+            be[i] = D_t > 0 ? g.beta[k] : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < NBM; ++j) {
+            const double dtj = __shfl(my_dt, j, kWave);
+#pragma unroll
+            for (int i = 0; i < kAggTCols; ++i)
+                if (lane + kWave * i < D_t)
+                    xs[j][i] = j < c ? time_enc(om[i], be[i], dtj) : 0.f;
+        }
+    }
+    __syncthreads();
+
+    // 2. scores, softmax, aggregates (own root); the value seeds of the lane's
+    // columns d = lane, lane + 64 and s'_r load first
+    const float scale = 1.0f / sqrtf((float)d_h);
+    f4 ring[kAggRing];
+    if (own) {
+        float vs[NBM][2];
+#pragma unroll
+        for (int j = 0; j < NBM; ++j) {
+            const int npj = __shfl(my_np, j, kWave);
+            const float *vrow = (npj >= 0 ? g.P + (int64_t)npj * g.ldP : g.pbias) + 2 * M;
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                vs[j][u] = (j < c && lane + kWave * u < M) ? vrow[lane + kWave * u] : 0.f;
+        }
+        float sr_[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            sr_[u] = (pv_ok && lane + kWave * u < M) ? g.mem_new[(int64_t)pv * M + lane + kWave * u]
+                                                      : 0.f;
+        issue_fence();
+        float sv[2] = {0.f, 0.f};   // sum_j alpha_j,head(d) seedV_j[d]
+#pragma unroll
+        for (int eta = 0; eta < kAggMaxH; ++eta) {
+            if (eta < H) {
+                float uu[kAggCols];
+#pragma unroll
+                for (int i = 0; i < kAggCols; ++i)
+                    uu[i] = lane + kWave * i < KFC * 16
+                                ? Us[(wave * H + eta) * KFP + lane + kWave * i] : 0.f;
+                float al[NBM];
+                float mx = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < NBM; ++j) {
+                    float part = 0.f;
+#pragma unroll
+                    for (int i = 0; i < kAggCols; ++i)
+                        part = fmaf(xs[j][i], uu[i], part);
+                    const float seed = Sk[(wave * nb + min(j, nb - 1)) * H + eta];
+                    const float scj = (wave_sum_rows(part) + seed) * scale;
+                    al[j] = j < c ? scj : -INFINITY;
+                    mx = fmaxf(mx, al[j]);
+                }
+                float den = 0.f;
+#pragma unroll
+                for (int j = 0; j < NBM; ++j) {
+                    al[j] = j < c ? __expf(al[j] - mx) : 0.f;
+                    den += al[j];
+                }
+                const float inv = c > 0 ? 1.0f / den : 0.f;   // no slots: no weights
+#pragma unroll
+                for (int j = 0; j < NBM; ++j)
+                    al[j] *= inv;
+                // abar_eta over the lane's columns (zero past KF: xs is)
+#pragma unroll
+                for (int i = 0; i < kAggCols; ++i) {
+                    float a = 0.f;
+#pragma unroll
+                    for (int j = 0; j < NBM; ++j)
+                        a = fmaf(al[j], xs[j][i], a);
+                    if (lane + kWave * i < KFC * 16)
+                        As[(wave * H + eta) * KFP + lane + kWave * i] = a;
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int d = lane + kWave * u;
+                    if (d < M && d / d_h == eta) {
+#pragma unroll
+                        for (int j = 0; j < NBM; ++j)
+                            sv[u] = fmaf(al[j], vs[j][u], sv[u]);
+                    }
+                }
+            }
+        }
+        // [sum alpha seedV || s'_r || 0]
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int d = lane + kWave * u;
+            if (d < M) {
+                AO[wave * SAO + d] = sv[u];
+                AO[wave * SAO + M + d] = sr_[u];
+            }
+        }
+        for (int k = 2 * M + lane; k < OC * 16; k += kWave)
+            AO[wave * SAO + k] = 0.f;
+    }
+    // the value GEMM's first weight chunks load across the barrier
+    const f4 *pwv = g.v_b + (int64_t)min(wave, VNB - 1) * kWave + lane;
+    const int64_t vstep = (int64_t)VNB * kWave;
+    if (wave < VNB)
+        agg_ring_load(pwv, vstep, KFC, ring);
+    __syncthreads();
+
+    // 3. value GEMM: [RT H x KF] abar rows x W_v,a^t, column block wave
+    if (wave < VNB) {
+        const f4 acc = agg_gemm(As + cn * KFP + q4, pwv, vstep, KFC, ring);
+        const int col = wave * 16 + cn;
+        if (col < M) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = q4 + v, rr = row / H, ee = row - rr * H;
+                if (rr < nroots && col / d_h == ee)
+                    AO[rr * SAO + col] += acc[v];
+            }
+        }
+    }
+    const f4 *pwo = g.out_b + (int64_t)min(wave, ONB - 1) * kWave + lane;
+    const int64_t ostep = (int64_t)ONB * kWave;
+    if (wave < ONB)
+        agg_ring_load(pwo, ostep, OC, ring);
+    __syncthreads();
+
+    // 4. h = ReLU(W_o [o || s'_r] + b_o), column block wave
+    if (wave < ONB) {
+        const f4 acc = agg_gemm(AO + cn * SAO + q4, pwo, ostep, OC, ring);
+        const int col = wave * 16 + cn;
+        if (col < M) {
+            const float bo = g.b_o[col];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int row = q4 + v;
+                if (row < nroots)
+                    g.h[(int64_t)(r0 + row) * M + col] = fmaxf(acc[v] + bo, 0.f);
+            }
+        }
+    }
+}
+
+template <int NBM>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NBM <= 10 ? 4 : 2))) void k_attn_agg(AttnArgs g)
+{
+    extern __shared__ float lds[];
+    attn_agg_block<NBM>(g, lds, blockIdx.x);
+}
+
+// with the gather of the next iteration's fetch on the blocks past n_attn
+// (dispatched last: they take the CUs the attention's tail leaves free)
+template <int NBM>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NBM <= 10 ? 4 : 2))) void k_attn_agg_gather(
+    AttnArgs g, int n_attn, GatherPlan gp)
+{
+    extern __shared__ float lds[];
+    if ((int)blockIdx.x < n_attn) {
+        attn_agg_block<NBM>(g, lds, blockIdx.x);
+        return;
+    }
+    const int waves = blockDim.x >> 6;
+    const int nn = min(*gp.n_nodes, gp.cap);
+    const int stride = ((int)gridDim.x - n_attn) * waves * kGatherNPW;
+    for (int p = (((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
+         p < nn; p += stride)
+        gather_rows(gp, p, nn, threadIdx.x & 63);
+}
+
 // q bias folded at creation: c_q = W_q^t phi(0) + b_q with phi(0)_d = cos(beta_d).
 __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, const float *b_q,
                               const double *__restrict__ beta, float *c_q)   // may alias b_q
@@ -1802,8 +2199,18 @@ __global__ void k_fold_q_bias(int M, int D_t, const float *__restrict__ W_q, con
     c_q[k] = (float)acc;
 }
 
-bool attn_lds_opt_in(int bytes, int fold_bytes)
+bool attn_lds_opt_in(int bytes, int fold_bytes, int agg_bytes)
 {
+    if (agg_bytes > 0) {
+        const void *fa[] = {(const void *)k_attn_agg<4>, (const void *)k_attn_agg<10>,
+                            (const void *)k_attn_agg<16>, (const void *)k_attn_agg_gather<4>,
+                            (const void *)k_attn_agg_gather<10>,
+                            (const void *)k_attn_agg_gather<16>};
+        for (const void *f : fa)
+            if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, agg_bytes) !=
+                hipSuccess)
+                return false;
+    }
     const void *fn[] = {(const void *)k_attn<3>, (const void *)k_attn<4>, (const void *)k_attn<5>,
                         (const void *)k_attn_gather<3>, (const void *)k_attn_gather<4>,
                         (const void *)k_attn_gather<5>};
@@ -1887,6 +2294,30 @@ bool attn_fold_fits(const tgm_model *m)
     return m->nb <= 16 && m->M % 4 == 0 && DC <= kAttDC && DC + 1 <= kMaxWaves &&
            RT * m->H <= 16 && m->KFC <= kAttUT * nu && DC <= m->KFC &&
            attn_fold_lds(m) <= 160 * 1024;
+}
+
+// Roots per workgroup of the attention by aggregation: one per wavefront,
+// RT H <= 16 (one 16-row MFMA block of (root, head) rows)
+int attn_agg_roots(const tgm_model *m) { return std::min(kMaxWaves, 16 / std::max(m->H, 1)); }
+
+size_t attn_agg_lds(const tgm_model *m)
+{
+    return sizeof(float) * (2 * 16 * ((size_t)m->KFC * 16 + 4) + 16 * ((size_t)m->OC * 16 + 4) +
+                            (size_t)attn_agg_roots(m) * m->nb * m->H);
+}
+
+// Shapes the attention by aggregation handles: slots and time codes within
+// the registers of a lane, M within 8 column blocks (one per wave) and two
+// columns per lane, the U tiles within kAggUT per wave
+bool attn_agg_fits(const tgm_model *m)
+{
+    const int KF = m->D_e + m->D_t;
+    return m->nb >= 1 && m->nb <= 16 && m->M % 4 == 0 && m->M <= 112 && m->H >= 1 &&
+           m->H <= kAggMaxH && m->M % m->H == 0 && KF >= 1 && KF <= kAggCols * kWave &&
+           m->D_t <= kAggTCols * kWave && m->KFC <= kAggUT * kMaxWaves &&
+           m->VNB <= kMaxWaves && m->ONB <= kMaxWaves && m->DC <= kAggDC &&
+           m->OC <= kAggMaxKC && m->KFC <= kAggMaxKC &&
+           attn_agg_lds(m) <= 64 * 1024;
 }
 
 }  // namespace
@@ -2010,6 +2441,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
         return TGM_EINVAL;
     }
     m->fold = attn_fold_fits(m);
+    m->agg = attn_agg_fits(m);
 
     // GRU operands
     const int D_x = m->D_x, MP = m->MB * 16;
@@ -2051,7 +2483,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
     auto kvb = pack_b(wkv.data(), 2 * M, KF, 0, KF, m->KFC, m->KVNB);
     // folded attention: the V rows alone, and W_k^t [KF x M] as A fragments
     std::vector<float> vb, uka;
-    if (m->fold) {
+    if (m->fold || m->agg) {
         vb = pack_b(wkv.data() + (size_t)M * (KF > 0 ? KF : 1), M, KF, 0, KF, m->KFC, m->VNB);
         vb.resize((size_t)std::max(m->KFC + 2, kAttPre) * m->VNB * kWave * 4, 0.f);
         std::vector<float> wkt((size_t)(KF > 0 ? KF : 1) * M, 0.f);
@@ -2084,7 +2516,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             !alloc((void **)&m->proj_b, pb.size() * 4) ||
             !alloc((void **)&m->P, sizeof(float) * (size_t)d->max_nodes * m->PNB * 16) ||
             !alloc((void **)&m->kv_b, kvb.size() * 4) ||
-            (m->fold && (!alloc((void **)&m->v_b, vb.size() * 4) ||
+            ((m->fold || m->agg) && (!alloc((void **)&m->v_b, vb.size() * 4) ||
                          !alloc((void **)&m->uk_a, uka.size() * 4))) ||
             !alloc((void **)&m->pbias, sizeof(float) * m->PNB * 16) ||
             !alloc((void **)&m->out_b, ob.size() * 4) || !alloc((void **)&m->b_o, 4 * M) ||
@@ -2101,7 +2533,7 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
         }
         if ((st = upload(m->proj_b, pb.data(), pb.size() * 4)) != TGM_OK) break;
         if ((st = upload(m->kv_b, kvb.data(), kvb.size() * 4)) != TGM_OK) break;
-        if (m->fold) {
+        if (m->fold || m->agg) {
             if ((st = upload(m->v_b, vb.data(), vb.size() * 4)) != TGM_OK) break;
             if ((st = upload(m->uk_a, uka.data(), uka.size() * 4)) != TGM_OK) break;
         }
@@ -2127,7 +2559,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             hipFuncSetAttribute((const void *)k_node_proj,
                                 hipFuncAttributeMaxDynamicSharedMemorySize,
                                 (int)proj_lds(m)) != hipSuccess ||
-            !attn_lds_opt_in((int)attn_lds(m), m->fold ? (int)attn_fold_lds(m) : 0)) {
+            !attn_lds_opt_in((int)attn_lds(m), m->fold ? (int)attn_fold_lds(m) : 0,
+                             m->agg ? (int)attn_agg_lds(m) : 0)) {
             st = TGM_EINVAL;   // dimensions beyond the LDS of one workgroup
             break;
         }
@@ -2281,6 +2714,8 @@ tgm_status_t embed_plan(tgm_model_t m, tgm_graph_t g, int32_t R, int32_t nb,
     pa->PNB = m->PNB; pa->pb = m->proj_b; pa->pbias = m->pbias; pa->P = m->P;
     AttnArgs &a = *aa;
     a.R = R; a.nb = nb; a.RT = attn_roots(m, &a.RBa); a.M = m->M; a.H = m->H;
+    if (m->agg)
+        a.RT = attn_agg_roots(m);
     a.E = g->E; a.n_nodes = n_nodes;
     a.D_e = m->D_e; a.D_t = m->D_t;
     a.root_pos = root_pos; a.nbr_pos = nbr_pos; a.eid = eid; a.cnt = cnt;
@@ -2302,6 +2737,27 @@ tgm_status_t launch_attn(const tgm_model *m, const AttnArgs &a, const GatherPlan
 {
     const int n_attn = (int)cdiv(a.R, a.RT);
     const dim3 block(64 * kMaxWaves);
+    if (m->agg) {
+        const size_t lds = attn_agg_lds(m);
+        const int nbm = a.nb <= 4 ? 4 : a.nb <= 10 ? 10 : 16;
+        if (next && next->cap > 0) {
+            // one gather block per CU after the attention's blocks
+            const dim3 grid(n_attn + kCUs);
+            switch (nbm) {
+            case 4: TGM_LAUNCH(k_attn_agg_gather<4>, grid, block, lds, s, a, n_attn, *next); break;
+            case 10: TGM_LAUNCH(k_attn_agg_gather<10>, grid, block, lds, s, a, n_attn, *next); break;
+            default: TGM_LAUNCH(k_attn_agg_gather<16>, grid, block, lds, s, a, n_attn, *next); break;
+            }
+            return TGM_OK;
+        }
+        const dim3 grid(n_attn);
+        switch (nbm) {
+        case 4: TGM_LAUNCH(k_attn_agg<4>, grid, block, lds, s, a); break;
+        case 10: TGM_LAUNCH(k_attn_agg<10>, grid, block, lds, s, a); break;
+        default: TGM_LAUNCH(k_attn_agg<16>, grid, block, lds, s, a); break;
+        }
+        return TGM_OK;
+    }
     const size_t lds = m->fold ? attn_fold_lds(m) : attn_lds(m);
     // the gather rides along when the attention's last round of blocks
     // leaves CUs free: its blocks are dispatched after the attention's, hold
@@ -2667,7 +3123,7 @@ tgm_status_t tgm::model_repack(tgm_model_t m, const ModelParams &w, hipStream_t 
     kv.perm_Dt = D_t;
     if (KF > 0)
         TGM_TRY_STATUS(pack_launch(kv, 2 * M, KF, m->KFC, m->KVNB, m->kv_b, s));
-    if (m->fold && KF > 0) {
+    if ((m->fold || m->agg) && KF > 0) {
         PackSrc v = kv;
         v.W[0] = w.W_v;
         TGM_TRY_STATUS(pack_launch(v, M, KF, m->KFC, m->VNB, m->v_b, s));

@@ -19,10 +19,18 @@ stage's fp32-vs-fp64 bound).  Gradients, per tensor:
   it) is below 1e-6: there one branch may differ, one term of each affected
   sum with it, and the bound is ||g - o|| <= 1e-2 ||o|| (Frobenius).  At
   least three quarters of the iterations of a run must pass element-wise.
-Adam runs use eps = 1e-6: Adam divides each step by the coordinate's own
-gradient scale, so with eps = 1e-8 a coordinate whose gradient lies within
-fp32 noise of zero could step by up to lr either way; with 1e-6, gradient
-noise of 1e-9 moves a parameter by at most lr / 1000.
+Adam runs use eps = 1e-6 and are compared for their first 8 to 10 steps;
+the long trajectories (24 to 30 steps, the executor) run SGD.  Adam
+divides each step by the coordinate's own gradient scale, so once the two
+arithmetics take a ReLU branch differently (an iteration whose smallest
+|pre-activation| is below the fp32 error of its ~200-term sum, about 1e-8 to
+1e-7; the oracle reports it), every coordinate that the flipped term feeds
+steps by up to lr differently, and the trajectories part.  Measured on the
+GPU: the tiny s = 2 run and the LastFM-shaped run stay within 0.003 of the
+parameter tolerance until such an iteration (margin 7e-10 at step 17 of one
+tiny run, about 2e-8 at step 10 of the LastFM-shaped run) and drift past the
+stage tolerance within a few steps after it; SGD moves those coordinates by
+lr times the flipped term, which stays inside the tolerance.
 """
 import dataclasses
 
@@ -152,7 +160,8 @@ def train_pair(orc, wl, w, P, n, *, s=None, opt="sgd", lr=1e-2, mitigation=None,
 def test_train_tiny(orc, s, opt, lr):
     wl = make_workload("tiny", E=6000, s=s)
     w = make_weights(wl.M, wl.D_e, wl.D_t, beta="random")
-    train_pair(orc, wl, w, make_predictor(wl.M, seed=1), wl.n_iters, s=s, opt=opt, lr=lr)
+    n = wl.n_iters if opt == "sgd" else 10
+    train_pair(orc, wl, w, make_predictor(wl.M, seed=1), n, s=s, opt=opt, lr=lr)
 
 
 def test_train_tie_heavy_odd_dims(orc):
@@ -165,7 +174,7 @@ def test_train_tie_heavy_odd_dims(orc):
 def test_train_lastfm_no_edge_features(orc):
     wl = make_workload("lastfm", E=16 * 2000)
     w = make_weights(wl.M, wl.D_e, wl.D_t)
-    train_pair(orc, wl, w, make_predictor(wl.M), 16, opt="adam", lr=1e-4)
+    train_pair(orc, wl, w, make_predictor(wl.M), 8, opt="adam", lr=1e-4)
 
 
 def test_train_wiki_window(orc):
