@@ -175,26 +175,29 @@ struct GruRows {
 // than any key of this one.  Candidates of one wavefront that hit the same
 // node are first reduced with lane shuffles (the wave's candidates are
 // consecutive, so a node's last lane in the wave holds its wave maximum); only
-// that lane issues the atomic.  Thread c of the grid takes candidate c.
+// that lane issues the atomic.  Thread c of the grid takes candidates c,
+// c + (grid threads), ... (a multiple of 64 apart: a wave's candidates stay
+// consecutive).
 __device__ __forceinline__ void latest_reduce(const GruArgs &g, int n)
 {
-    const int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
-    if (c - (threadIdx.x & (kWave - 1)) >= g.n_cand)
-        return;   // the whole wave is past the candidates
     const int lane = threadIdx.x & (kWave - 1);
-    int p = c < g.n_cand ? ((c & 1) ? g.dst_pos[c >> 1] : g.src_pos[c >> 1]) : -1;
-    const bool live = p >= 0 && p < n;   // positions outside the node set are dropped
-    if (!live)
-        p = -1 - lane;
-    // is there a later lane in this wave with the same position?
-    bool later = false;
-    for (int o = 1; o < kWave; ++o) {
-        const int q = __shfl(p, (lane + o) & (kWave - 1), kWave);
-        later |= (lane + o < kWave) && q == p;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t c = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+         c - lane < g.n_cand; c += stride) {   // the whole wave past the candidates: done
+        int p = c < g.n_cand ? ((c & 1) ? g.dst_pos[c >> 1] : g.src_pos[c >> 1]) : -1;
+        const bool live = p >= 0 && p < n;   // positions outside the node set are dropped
+        if (!live)
+            p = -1 - lane;
+        // is there a later lane in this wave with the same position?
+        bool later = false;
+        for (int o = 1; o < kWave; ++o) {
+            const int q = __shfl(p, (lane + o) & (kWave - 1), kWave);
+            later |= (lane + o < kWave) && q == p;
+        }
+        if (live && !later)
+            atomicMax(reinterpret_cast<unsigned long long *>(g.win + p),
+                      (unsigned long long)(g.tag | (uint64_t)c));
     }
-    if (live && !later)
-        atomicMax(reinterpret_cast<unsigned long long *>(g.win + p),
-                  (unsigned long long)(g.tag | (uint64_t)c));
 }
 
 // The latest-message reduce on its own (the executor runs it on the prefetch

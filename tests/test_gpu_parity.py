@@ -53,8 +53,10 @@ def exact(name, g, o):
                              f"gpu {g[tuple(k)]!r} oracle {o[tuple(k)]!r}")
 
 
-def compare_step(go, r):
-    """go: Stage.outputs(); r: oracle StepResult of the same iteration."""
+def compare_step(go, r, close_fn=None):
+    """go: Stage.outputs(); r: oracle StepResult of the same iteration;
+    close_fn replaces close for the floating-point fields."""
+    cf = close_fn or close
     assert go["iter"] == r.iter and go["b"] == r.b
     exact("root", go["root"], r.root)
     exact("root_ts", go["root_ts"], r.root_ts)
@@ -72,10 +74,10 @@ def compare_step(go, r):
     exact("new_mem_ts", go["new_mem_ts"], r.new_mem_ts)
     exact("winner", go["winner"], r.winner)
     e = {}
-    e["f_mem"] = close("f_mem", go["f_mem"], r.f_mem)
-    e["f_mail"] = close("f_mail", go["f_mail"], r.f_mail)
-    e["s_new"] = close("s_new", go["s_new"], r.s_new)
-    e["h"] = close("h", go["h"], r.h)
+    e["f_mem"] = cf("f_mem", go["f_mem"], r.f_mem)
+    e["f_mail"] = cf("f_mail", go["f_mail"], r.f_mail)
+    e["s_new"] = cf("s_new", go["s_new"], r.s_new)
+    e["h"] = cf("h", go["h"], r.h)
     return e
 
 

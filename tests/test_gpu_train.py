@@ -19,6 +19,11 @@ stage's fp32-vs-fp64 bound).  Gradients, per tensor:
   it) is below 1e-6: there one branch may differ, one term of each affected
   sum with it, and the bound is ||g - o|| <= 1e-2 ||o|| (Frobenius).  At
   least three quarters of the iterations of a run must pass element-wise.
+Trajectories.  From the first iteration whose smallest |pre-activation| is
+within 1e-6 of zero on, the two arithmetics may have taken different ReLU
+branches and the weights they train part: later forward values, parameters
+and tables are held to the stage tolerance plus 1e-4 of the tensor's largest
+magnitude (integers stay exact).
 Adam runs use eps = 1e-6 and are compared for their first 8 to 10 steps;
 the long trajectories (24 to 30 steps, the executor) run SGD.  Adam
 divides each step by the coordinate's own gradient scale, so once the two
@@ -100,6 +105,25 @@ def param_close(name, g, o):
     close(name, g, o)
 
 
+def scaled_close(name, g, o):
+    """The stage tolerance plus 1e-4 of the tensor's largest magnitude: the
+    bound after the trajectories may have parted at a ReLU branch."""
+    from test_gpu_parity import ATOL, RTOL
+    g = np.asarray(g, dtype=np.float64)
+    o = np.asarray(o, dtype=np.float64)
+    assert g.shape == o.shape, (name, g.shape, o.shape)
+    if o.size == 0:
+        return 0.0
+    err = np.abs(g - o)
+    tol = ATOL + RTOL * np.abs(o) + 1e-4 * np.abs(o).max()
+    bad = err > tol
+    if bad.any():
+        k = np.unravel_index(np.argmax(err - tol), err.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())}/{bad.size} outside the scaled tolerance; "
+                             f"worst at {k}: gpu {g[k]!r} oracle {o[k]!r}")
+    return float(err.max())
+
+
 def train_pair(orc, wl, w, P, n, *, s=None, opt="sgd", lr=1e-2, mitigation=None,
                pipelined=False):
     from paper_2402_15113_amd.stage import from_workload
@@ -115,25 +139,33 @@ def train_pair(orc, wl, w, P, n, *, s=None, opt="sgd", lr=1e-2, mitigation=None,
     if pipelined:
         h_tr, s_tr = st.run(0, n, trace=True)
         torch.cuda.synchronize()
+    # once an iteration's smallest |ReLU pre-activation| is within RELU_TAU of
+    # zero the two arithmetics may take different branches there, and the
+    # weights they train part from that step on: later forward values and
+    # parameters are held to the scaled tolerance
+    parted = False
     for i in range(n):
         if not pipelined:
             st.step(i)
         r = o.step()
+        cl = scaled_close if parted else close
         if pipelined:
-            close(f"h[{i}]", h_tr[i, :r.R].cpu().numpy(), r.h)
-            close(f"s_new[{i}]", s_tr[i, :r.n_U].cpu().numpy(), r.s_new)
+            cl(f"h[{i}]", h_tr[i, :r.R].cpu().numpy(), r.h)
+            cl(f"s_new[{i}]", s_tr[i, :r.n_U].cpu().numpy(), r.s_new)
+            parted = parted or r.relu_margin < RELU_TAU
             continue
         # with the mitigation on, the fetch buffer holds the blended rows
         compare_step(st.outputs(), r if mitigation is None else
-                     dataclasses.replace(r, f_mem=r.m_mem))
+                     dataclasses.replace(r, f_mem=r.m_mem), close_fn=cl)
         ts = st.train_state()
         assert abs(ts["loss"][i] - r.loss) <= 1e-5 + 1e-4 * abs(r.loss), (i, ts["loss"][i],
                                                                          r.loss)
         gg, og = split(ts["grad"], sizes), o.split(r.grad)
         grad_check(gg, og, r.relu_margin, stats)
+        parted = parted or r.relu_margin < RELU_TAU
         gp, op = split(ts["params"], sizes), o.split(r.params)
         for k in PARAM_NAMES:
-            param_close(f"param {k} [{i}]", gp[k], op[k])
+            (scaled_close if parted else param_close)(f"param {k} [{i}]", gp[k], op[k])
     ts = st.train_state()
     losses = np.array([0.0] * n)
     if pipelined:
@@ -143,11 +175,18 @@ def train_pair(orc, wl, w, P, n, *, s=None, opt="sgd", lr=1e-2, mitigation=None,
         np.testing.assert_allclose(ts["loss"][:n], losses, rtol=1e-4, atol=1e-5)
     gp, op = split(ts["params"], sizes), o.split(o.params())
     for k in PARAM_NAMES:
-        param_close(f"final param {k}", gp[k], op[k])
+        (scaled_close if parted else param_close)(f"final param {k}", gp[k], op[k])
     st.flush()
     o.flush()
     from test_gpu_parity import compare_state
-    compare_state(st.state(), o.state())
+    gs, os_ = st.state(), o.state()
+    if parted:
+        for k in ("ver", "mem_ts", "mail_ts"):
+            assert np.array_equal(gs[k], os_[k]), k
+        scaled_close("mem", gs["mem"], os_["mem"])
+        scaled_close("mail", gs["mail"], os_["mail"])
+    else:
+        compare_state(gs, os_)
     st.close()
     print(f"[train] iterations checked element-wise / near a kink, worst relative Frobenius "
           f"error per tensor: {stats}", flush=True)
