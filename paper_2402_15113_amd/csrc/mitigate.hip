@@ -22,8 +22,11 @@
 //   k_mit_omega   work items (stale node, chunk of the node set) over a
 //                 fixed grid: the stale node's neighbour set in an LDS hash
 //                 set, every active node's set of the chunk probed against it,
-//                 per-thread sorted lists merged into the top-K, chunk lists
-//                 merged by the last workgroup of the node, and the blend.
+//                 per-thread sorted lists merged into the top-K; with one
+//                 chunk per node, Omega and the blend;
+//   k_mit_final   with several chunks per node: each stale node's chunk
+//                 lists merged into Omega, and the blend (the launch boundary
+//                 orders the lists; no device-wide fence is needed).
 // Integer decisions only; each gap is formed where it is used, by the one fp64
 // subtraction the oracle makes.
 #include <hip/hip_runtime.h>
@@ -44,7 +47,6 @@ struct tgm_mitigator {
     int32_t *stale = nullptr;    // [cap] stale positions, ascending
     int32_t *omega = nullptr;    // [cap x K] Omega positions, -1 padded
     int2 *part = nullptr;        // [kMitOmegaGrid x kMitMaxK] chunk top-K lists of k_mit_omega
-    int32_t *done = nullptr;     // [cap] finished chunks per stale node
 };
 
 namespace {
@@ -63,8 +65,8 @@ static_assert(kMitMaxChunks * kMitMaxK <= kMitChunk, "the chunk lists fit the ro
 constexpr int kMitOmegaGrid = 1024;         // k_mit_omega workgroups
 
 constexpr int kMitMaxNodes = 1 << 20;
-static_assert(TGM_MITIGATE_NOALLOC_MAX_NODES * (64 + 1 + 1 + 16 + 1) * 4 +
-                  kMitOmegaGrid * kMitMaxK * 8 + 9 * 256 <= TGM_MITIGATE_NOALLOC_BYTES,
+static_assert(TGM_MITIGATE_NOALLOC_MAX_NODES * (64 + 1 + 1 + 16) * 4 +
+                  kMitOmegaGrid * kMitMaxK * 8 + 8 * 256 <= TGM_MITIGATE_NOALLOC_BYTES,
               "the no-allocation work space fits its largest call");
 
 // ---------------------------------------------------------------- prep
@@ -179,7 +181,7 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint64_t k, bool in, in
 __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
     const double *__restrict__ t, int64_t first, const double *__restrict__ mem_ts,
     const int32_t *__restrict__ n_nodes, int32_t cap, double pq, double *__restrict__ gamma_out,
-    int32_t *__restrict__ stale, int32_t *__restrict__ n_stale, int32_t *__restrict__ done)
+    int32_t *__restrict__ stale, int32_t *__restrict__ n_stale)
 {
     constexpr int R = kMitSelRegs;
     constexpr int T = kMitSelThreads;
@@ -211,12 +213,64 @@ __global__ __launch_bounds__(kMitSelThreads) void k_mit_select(
         for (int j = 0; j < R; ++j)
             kr[j] = order_key(T0 - x[j]);
     }
-    for (int i = tid; i < n; i += T)
-        done[i] = 0;   // k_mit_omega's per-stale-node chunk counts
     if (tid < 256)
         hist[0][tid] = 0;
     long long rank = (long long)ceil(pq * (double)n);
     rank = rank < 1 ? 1 : (rank > n ? n : rank);
+    {
+        // gamma is the largest gap when at least n - rank + 1 gaps equal it;
+        // then no gap exceeds it and nothing is stale (two barriers instead
+        // of the eight passes)
+        uint64_t km = 0;
+        if (in_regs) {
+#pragma unroll
+            for (int j = 0; j < R; ++j)
+                if (j < rounds && tid + j * T < n)
+                    km = kr[j] > km ? kr[j] : km;
+        } else {
+            for (int i = tid; i < n; i += T) {
+                const uint64_t k = order_key(gap(i));
+                km = k > km ? k : km;
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const uint64_t y = (uint64_t)__shfl_xor((long long)km, o, kWave);
+            km = y > km ? y : km;
+        }
+        __shared__ uint64_t s_km[T / kWave];
+        __shared__ int s_kc[T / kWave];
+        if (lane == 0)
+            s_km[wave] = km;
+        __syncthreads();
+        for (int w = 0; w < T / kWave; ++w)
+            km = s_km[w] > km ? s_km[w] : km;
+        int cnt = 0;
+        if (in_regs) {
+#pragma unroll
+            for (int j = 0; j < R; ++j)
+                if (j < rounds)
+                    cnt += __popcll(__ballot(tid + j * T < n && kr[j] == km));
+        } else {
+            for (int b0 = 0; b0 < n; b0 += T) {   // whole waves per round
+                const int i = b0 + tid;
+                cnt += __popcll(__ballot(i < n && order_key(gap(min(i, n - 1))) == km));
+            }
+        }
+        if (lane == 0)
+            s_kc[wave] = cnt;
+        __syncthreads();
+        int total = 0;
+        for (int w = 0; w < T / kWave; ++w)
+            total += s_kc[w];
+        if ((long long)total >= (long long)n - rank + 1) {   // uniform
+            if (tid == 0) {
+                *n_stale = 0;
+                *gamma_out = key_value(km);
+            }
+            return;
+        }
+    }
     uint32_t krem = (uint32_t)(rank - 1);   // keys below the target among those matching
     uint64_t prefix = 0, mask = 0;
     for (int pass = 0; pass < 8; ++pass) {
@@ -386,39 +440,51 @@ struct Lists {
 // holds the j-th in *mine.  Lane i owns lists i, i + 64, i + 128 and i + 192
 // (nl <= 256), so the heads of neighbouring lanes sit side by side when the
 // lists are interleaved (es = the list count); lane 63 also owns the extra
-// list.  Each round the wave takes its best head with the DPP arg-best.
+// list.  Each lane keeps its five heads in registers; each round the wave
+// takes its best head with the DPP arg-best, and only the winning lane reads
+// the next entry of that list.
 __device__ int merge_lists(const Lists &L, int nl, int ls, int es, int len, int xb, int xl, int K,
                            Cand *mine)
 {
     const int lane = threadIdx.x & 63;
     int h[5] = {0, 0, 0, 0, 0};
+    Cand hd[5];
+    // entry h[i] of owned list i, or an empty entry (similarity 0)
+    auto head = [&](int i) {
+        const int l = lane + kWave * i;
+        const bool own = i < 4 ? (l < nl && h[i] < len) : (lane == 63 && h[4] < xl);
+        const int o = i < 4 ? l * ls + h[i] * es : xb + h[4];
+        Cand x{0, 0.0, 0, -1};
+        if (own && L.sim[o] > 0)
+            x = Cand{L.sim[o], L.mts[o], L.id[o], L.pos[o]};
+        return x;
+    };
+#pragma unroll
+    for (int i = 0; i < 5; ++i)
+        hd[i] = head(i);
     int m = 0;
     for (int r = 0; r < K; ++r) {
-        Cand best{0, 0.0, 0, -1};
-        int bi = -1;
+        Cand best = hd[0];
+        int bi = 0;
 #pragma unroll
-        for (int i = 0; i < 5; ++i) {
-            const int l = lane + kWave * i;
-            const bool own = i < 4 ? (l < nl && h[i] < len) : (lane == 63 && h[4] < xl);
-            const int o = i < 4 ? l * ls + h[i] * es : xb + h[4];
-            if (own && L.sim[o] > 0) {
-                const Cand x{L.sim[o], L.mts[o], L.id[o], L.pos[o]};
-                if (better(x, best)) {   // best starts empty
-                    best = x;
-                    bi = i;
-                }
+        for (int i = 1; i < 5; ++i)
+            if (better(hd[i], best)) {   // empties lose
+                best = hd[i];
+                bi = i;
             }
-        }
         // the winner is unique (positions are distinct)
         Cand wb = best;
-        int wl = bi >= 0 ? lane : -1;
+        int wl = best.sim > 0 ? lane : -1;
         wave_best(wb, wl);   // an empty lane's entry has similarity 0
         if (wl < 0)
             break;   // no candidate left anywhere (uniform)
         if (lane == wl) {
 #pragma unroll
             for (int i = 0; i < 5; ++i)
-                h[i] += i == bi ? 1 : 0;
+                if (i == bi) {
+                    ++h[i];
+                    hd[i] = head(i);
+                }
         }
         if (lane == r)
             *mine = wb;
@@ -432,19 +498,16 @@ __device__ int merge_lists(const Lists &L, int nl, int ls, int es, int len, int 
 // chunk against the stale node's (an LDS hash set), 1024 nodes at a time
 // (kMitPerThread per thread, each thread keeping its best few sorted), and
 // merges the thread lists into a running top-K.  With one chunk that is
-// Omega; otherwise the chunk lists go to `part` and the last workgroup to
-// finish a chunk of q (a device counter, zeroed by k_mit_select) merges them.
-// The workgroup that holds Omega writes it and blends the stale row.  No
-// workgroup waits for another.
+// Omega, which the workgroup writes and blends; otherwise the chunk lists go
+// to `part` for k_mit_final.  No workgroup waits for another.
 template <int NBP>   // padded neighbour-set width: 4 (nb <= 4), 12 (<= 12) or 64
 __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
     const int32_t *__restrict__ nodes, const int32_t *__restrict__ n_nodes, int32_t cap,
     const double *__restrict__ t, int64_t first, const double *__restrict__ mem_ts,
     const int32_t *__restrict__ nset, const int32_t *__restrict__ ncnt,
     const double *__restrict__ gamma_p, const int32_t *__restrict__ stale,
-    const int32_t *__restrict__ n_stale, int2 *__restrict__ part,
-    int32_t *__restrict__ done, int32_t K, float lambda, float *__restrict__ mem, int32_t M,
-    int32_t *__restrict__ omega)
+    const int32_t *__restrict__ n_stale, int2 *__restrict__ part, int32_t K, float lambda,
+    float *__restrict__ mem, int32_t M, int32_t *__restrict__ omega)
 {
     typedef int __attribute__((ext_vector_type(4))) i4;
     constexpr int P = kMitPerThread;
@@ -456,7 +519,7 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
     __shared__ int e_sim[kE];
     __shared__ double e_mts[kE];
     __shared__ int32_t e_id[kE], e_pos[kE];
-    __shared__ int s_m, s_last;
+    __shared__ int s_m;
     const Lists L{e_sim, e_mts, e_id, e_pos};
     const int RB = kSub;   // the running list
     const int tid = threadIdx.x;
@@ -563,37 +626,13 @@ __global__ __launch_bounds__(kMitThreads) void k_mit_omega(
             }
             __syncthreads();
         }
-        if (nce > 1) {
+        if (nce > 1) {   // the chunk's list, for k_mit_final
             int2 *mine = part + ((int64_t)q * nce + c) * K;   // q nce < kMitOmegaGrid
             if (tid < K)
                 mine[tid] = tid < s_m ? make_int2(e_sim[RB + tid], e_pos[RB + tid])
                                       : make_int2(0, -1);
-            __threadfence();   // the list is visible device-wide before the count
-            __syncthreads();
-            if (tid == 0)
-                s_last = atomicAdd(&done[q], 1) == nce - 1;
-            __syncthreads();
-            if (!s_last)
-                continue;   // uniform: s_last is shared
-            __threadfence();   // the other chunks' lists are seen after the count
-            for (int i = tid; i < nce * K; i += blockDim.x) {
-                const int2 e = part[(int64_t)q * nce * K + i];
-                const int ps = e.y < 0 ? 0 : e.y;
-                e_sim[i] = e.x;
-                e_mts[i] = mem_ts[ps];
-                e_id[i] = nodes[ps];
-                e_pos[i] = e.y;
-            }
-            __syncthreads();
-            if (tid < kWave) {
-                Cand w;
-                const int m = merge_lists(L, nce, K, 1, K, 0, 0, K, &w);
-                if (tid < m)
-                    e_pos[RB + tid] = w.pos;
-                if (tid == 0)
-                    s_m = m;
-            }
-            __syncthreads();
+            __syncthreads();   // s_m is reused
+            continue;
         }
         const int m = s_m;
         if (omega && tid < K)
@@ -640,7 +679,6 @@ extern "C" tgm_status_t tgm_mitigator_create(int32_t max_nodes, int32_t nb, int3
         dev_malloc((void **)&mt->stale, sizeof(int32_t) * c) != hipSuccess ||
         dev_malloc((void **)&mt->omega, sizeof(int32_t) * c * K) != hipSuccess ||
         dev_malloc((void **)&mt->part, sizeof(int2) * kMitOmegaGrid * kMitMaxK) != hipSuccess ||
-        dev_malloc((void **)&mt->done, sizeof(int32_t) * c) != hipSuccess ||
         tgm::mitigate_reserve(mt, 1) != TGM_OK) {
         tgm_mitigator_destroy(mt);
         return TGM_ENOMEM;
@@ -660,7 +698,6 @@ extern "C" tgm_status_t tgm_mitigator_destroy(tgm_mitigator_t mt)
     (void)hipFree(mt->stale);
     (void)hipFree(mt->omega);
     (void)hipFree(mt->part);
-    (void)hipFree(mt->done);
     delete mt;
     return TGM_OK;
 }
@@ -691,6 +728,69 @@ tgm_status_t tgm::mitigate_reserve(tgm_mitigator_t mt, int32_t nslots)
 
 namespace {
 
+// Stale nodes q, strided over the grid, when k_mit_omega split each one's
+// node set over several chunks (the same nce as there): the nce chunk lists
+// of q merged into Omega (wave 0), written, and the blend.
+__global__ __launch_bounds__(kMitThreads) void k_mit_final(
+    const int32_t *__restrict__ nodes, const int32_t *__restrict__ n_nodes, int32_t cap,
+    const double *__restrict__ mem_ts, const int32_t *__restrict__ stale,
+    const int32_t *__restrict__ n_stale, const int2 *__restrict__ part, int32_t K, float lambda,
+    float *__restrict__ mem, int32_t M, int32_t *__restrict__ omega)
+{
+    constexpr int kE = kMitMaxChunks * kMitMaxK;
+    __shared__ int e_sim[kE];
+    __shared__ double e_mts[kE];
+    __shared__ int32_t e_id[kE], e_pos[kE];
+    __shared__ int32_t s_pos[kMitMaxK];
+    __shared__ int s_m;
+    const Lists L{e_sim, e_mts, e_id, e_pos};
+    const int tid = threadIdx.x;
+    const int n = min(*n_nodes, cap);
+    const int ns = *n_stale;
+    constexpr int kSub = kMitThreads * kMitPerThread;
+    const int nsub = (n + kSub - 1) / kSub;
+    int nce = min(min(nsub, kMitMaxChunks), max(1, kMitOmegaGrid / max(ns, 1)));
+    const int chunk = (nsub + nce - 1) / nce * kSub;
+    nce = (n + chunk - 1) / chunk;
+    if (nce <= 1)
+        return;   // k_mit_omega finished every stale node (uniform)
+    for (int q = blockIdx.x; q < ns; q += gridDim.x) {
+        for (int i = tid; i < nce * K; i += blockDim.x) {
+            const int2 e = part[(int64_t)q * nce * K + i];
+            const int ps = e.y < 0 ? 0 : e.y;
+            e_sim[i] = e.x;
+            e_mts[i] = mem_ts[ps];
+            e_id[i] = nodes[ps];
+            e_pos[i] = e.y;
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            Cand w;
+            const int m = merge_lists(L, nce, K, 1, K, 0, 0, K, &w);
+            if (tid < m)
+                s_pos[tid] = w.pos;
+            if (tid == 0)
+                s_m = m;
+        }
+        __syncthreads();
+        const int m = s_m;
+        if (omega && tid < K)
+            omega[(int64_t)q * K + tid] = tid < m ? s_pos[tid] : -1;
+        if (m > 0) {
+            const int v = stale[q];
+            const float rest = 1.0f - lambda;
+            for (int cc = tid; cc < M; cc += blockDim.x) {
+                float acc = 0.f;
+                for (int j = 0; j < m; ++j)
+                    acc += mem[(int64_t)s_pos[j] * M + cc];
+                mem[(int64_t)v * M + cc] =
+                    lambda * mem[(int64_t)v * M + cc] + rest * (acc / (float)m);
+            }
+        }
+        __syncthreads();   // the entries and s_m are reused
+    }
+}
+
 // The work space one mitigation reads and writes: a mitigator's (one of its
 // neighbour-set slots), or the fixed per-device array of
 // tgm_mitigate_noalloc.
@@ -698,7 +798,7 @@ struct MitWork {
     int32_t nb = 0, nbp = 0, K = 0;
     int32_t *nset = nullptr, *ncnt = nullptr;   // [cap x nbp], [cap]
     double *gamma = nullptr;
-    int32_t *n_stale = nullptr, *stale = nullptr, *omega = nullptr, *done = nullptr;
+    int32_t *n_stale = nullptr, *stale = nullptr, *omega = nullptr;
     int2 *part = nullptr;
 };
 
@@ -715,7 +815,6 @@ MitWork work_of(const tgm_mitigator *mt, int32_t slot)
     w.n_stale = mt->n_stale;
     w.stale = mt->stale;
     w.omega = mt->omega;
-    w.done = mt->done;
     w.part = mt->part;
     return w;
 }
@@ -737,7 +836,7 @@ tgm_status_t blend_launch(const MitWork &w, tgm_graph_t g, int64_t first_event,
     if (cap == 0)
         return TGM_OK;
     TGM_LAUNCH(k_mit_select, dim3(1), dim3(kMitSelThreads), 0, s, g->t, first_event, mem_ts,
-               n_nodes, cap, p, w.gamma, w.stale, w.n_stale, w.done);
+               n_nodes, cap, p, w.gamma, w.stale, w.n_stale);
     // at most n - ceil(p n) + 1 <= cap (1 - p) + 1 nodes are stale, each in
     // at most ceil(cap / kMitChunk) items; a fixed grid strides over the items
     const int64_t slots = std::min<int64_t>(cap, (int64_t)std::floor(cap * (1.0 - p)) + 1);
@@ -745,15 +844,19 @@ tgm_status_t blend_launch(const MitWork &w, tgm_graph_t g, int64_t first_event,
     if (w.nbp == 4)
         TGM_LAUNCH(k_mit_omega<4>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
                    first_event, mem_ts, w.nset, w.ncnt, w.gamma, w.stale, w.n_stale, w.part,
-                   w.done, w.K, lambda, mem, M, w.omega);
+                   w.K, lambda, mem, M, w.omega);
     else if (w.nbp == 12)
         TGM_LAUNCH(k_mit_omega<12>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
                    first_event, mem_ts, w.nset, w.ncnt, w.gamma, w.stale, w.n_stale, w.part,
-                   w.done, w.K, lambda, mem, M, w.omega);
+                   w.K, lambda, mem, M, w.omega);
     else
         TGM_LAUNCH(k_mit_omega<64>, grid, dim3(kMitThreads), 0, s, nodes, n_nodes, cap, g->t,
                    first_event, mem_ts, w.nset, w.ncnt, w.gamma, w.stale, w.n_stale, w.part,
-                   w.done, w.K, lambda, mem, M, w.omega);
+                   w.K, lambda, mem, M, w.omega);
+    // the stale nodes whose node set k_mit_omega split over several chunks
+    TGM_LAUNCH(k_mit_final, dim3((unsigned)std::min<int64_t>(slots, kMitOmegaGrid)),
+               dim3(kMitThreads), 0, s, nodes, n_nodes, cap, mem_ts, w.stale, w.n_stale, w.part,
+               w.K, lambda, mem, M, w.omega);
     return TGM_OK;
 }
 
@@ -837,7 +940,6 @@ size_t noalloc_layout(int32_t cap, int32_t nbp, int32_t K, char *base, MitWork *
     void *stale = take(sizeof(int32_t) * c);
     void *omega = take(sizeof(int32_t) * c * K);
     void *part = take(sizeof(int2) * kMitOmegaGrid * kMitMaxK);
-    void *done = take(sizeof(int32_t) * c);
     if (w) {
         w->nset = (int32_t *)nset;
         w->ncnt = (int32_t *)ncnt;
@@ -846,7 +948,6 @@ size_t noalloc_layout(int32_t cap, int32_t nbp, int32_t K, char *base, MitWork *
         w->stale = (int32_t *)stale;
         w->omega = (int32_t *)omega;
         w->part = (int2 *)part;
-        w->done = (int32_t *)done;
     }
     return o;
 }
