@@ -358,12 +358,58 @@ __device__ __forceinline__ void copy2_rows_regs(float *__restrict__ d1,
             d2[lane + kWave * u] = b[u];
 }
 
+// The same with V1- and V2-wide vector accesses (row lengths multiples of
+// the widths, every row aligned to them; n2 >= V2): lane l holds vectors
+// l + 64 u of each row.
+template <int V1, int V2, int U1, int U2>
+__device__ __forceinline__ void copy2_rows_vec(float *__restrict__ d1,
+                                               const float *__restrict__ s1, int n1,
+                                               float *__restrict__ d2,
+                                               const float *__restrict__ s2, int n2, int lane)
+{
+    typedef float v1_t __attribute__((ext_vector_type(V1)));
+    typedef float v2_t __attribute__((ext_vector_type(V2)));
+    const int m1 = n1 / V1, m2 = n2 / V2;
+    const v1_t *a1 = reinterpret_cast<const v1_t *>(s1);
+    const v2_t *a2 = reinterpret_cast<const v2_t *>(s2);
+    v1_t a[U1];
+    v2_t b[U2];
+#pragma unroll
+    for (int u = 0; u < U1; ++u)
+        a[u] = a1[min(lane + kWave * u, m1 - 1)];
+#pragma unroll
+    for (int u = 0; u < U2; ++u)
+        b[u] = a2[min(lane + kWave * u, m2 - 1)];
+#pragma unroll
+    for (int u = 0; u < U1; ++u)
+        if (lane + kWave * u < m1)
+            reinterpret_cast<v1_t *>(d1)[lane + kWave * u] = a[u];
+#pragma unroll
+    for (int u = 0; u < U2; ++u)
+        if (lane + kWave * u < m2)
+            reinterpret_cast<v2_t *>(d2)[lane + kWave * u] = b[u];
+}
+
+// Whether rows of n floats at p and q allow w-wide vector accesses
+__device__ __forceinline__ bool rows_vec_ok(const void *p, const void *q, int n, int w)
+{
+    return n % w == 0 &&
+           ((reinterpret_cast<uintptr_t>(p) | reinterpret_cast<uintptr_t>(q)) & (4 * w - 1)) == 0;
+}
+
 // Copies rows (s1 -> d1, n1 floats) and (s2 -> d2, n2 floats) with one
-// wavefront: loads first when the rows are short enough, else row by row.
+// wavefront: loads first when the rows are short enough (vector accesses
+// when the rows allow them), else row by row.
 __device__ __forceinline__ void wave_copy_2rows(float *d1, const float *s1, int n1, float *d2,
                                                 const float *s2, int n2, int lane)
 {
-    if (n1 <= 2 * kWave && n2 <= 8 * kWave) {
+    if (n1 >= 4 && n1 <= 4 * kWave && rows_vec_ok(d1, s1, n1, 4) && n2 >= 4 &&
+        n2 <= 8 * kWave && rows_vec_ok(d2, s2, n2, 4)) {
+        copy2_rows_vec<4, 4, 1, 2>(d1, s1, n1, d2, s2, n2, lane);
+    } else if (n1 >= 4 && n1 <= 4 * kWave && rows_vec_ok(d1, s1, n1, 4) && n2 >= 2 &&
+               n2 <= 8 * kWave && rows_vec_ok(d2, s2, n2, 2)) {
+        copy2_rows_vec<4, 2, 1, 4>(d1, s1, n1, d2, s2, n2, lane);
+    } else if (n1 <= 2 * kWave && n2 <= 8 * kWave) {
         copy2_rows_regs<2, 8>(d1, s1, n1, d2, s2, n2, lane);
     } else if (n1 <= 4 * kWave && n2 <= 16 * kWave) {
         copy2_rows_regs<4, 16>(d1, s1, n1, d2, s2, n2, lane);
@@ -485,10 +531,86 @@ __device__ __forceinline__ void gather_rows_regs(const GatherPlan &g, int p0, in
     }
 }
 
-// Rows p0 .. p0 + kGatherNPW - 1 (those below n) of a gather by one wavefront.
+// The same with VM- and VD-wide vector accesses to the memory and mail rows
+// (both row lengths multiples of their width, every row base aligned to it):
+// lane l holds vectors l + 64 u, so one instruction moves 64 VM (or VD)
+// floats of a row.  UM and UD bound the 64-vector chunks of the two rows.
+template <int VM, int VD, int UM, int UD, int NPW>
+__device__ __forceinline__ void gather_rows_vec(const GatherPlan &g, int p0, int n, int lane)
+{
+    typedef float vm_t __attribute__((ext_vector_type(VM)));
+    typedef float vd_t __attribute__((ext_vector_type(VD)));
+    const int NM = g.M / VM, ND = g.D_m / VD;   // vectors per row
+    const int32_t vid = g.nodes[min(p0 + (lane < NPW ? lane : 0), n - 1)];
+    vm_t a[NPW][UM];
+    vd_t b[NPW][UD];
+#pragma unroll
+    for (int j = 0; j < NPW; ++j) {
+        const int32_t v = __builtin_amdgcn_readlane(vid, j);
+        const vm_t *sm = reinterpret_cast<const vm_t *>(g.mem + (int64_t)v * g.M);
+        const vd_t *sd = reinterpret_cast<const vd_t *>(g.mail + (int64_t)v * g.D_m);
+#pragma unroll
+        for (int u = 0; u < UM; ++u)
+            a[j][u] = sm[min(lane + kWave * u, NM - 1)];
+#pragma unroll
+        for (int u = 0; u < UD; ++u)
+            b[j][u] = sd[min(lane + kWave * u, ND - 1)];
+    }
+    double mts = 0.0, lts = 0.0;
+    int32_t ver = 0;
+    if (lane < NPW) {
+        mts = g.mem_ts[vid];
+        lts = g.mail_ts[vid];
+        ver = g.ver[vid];
+    }
+#pragma unroll
+    for (int j = 0; j < NPW; ++j) {
+        const int p = p0 + j;
+        if (p >= n)
+            break;   // uniform
+        vm_t *dm = reinterpret_cast<vm_t *>(g.o_mem + (int64_t)p * g.M);
+        vd_t *dd = reinterpret_cast<vd_t *>(g.o_mail + (int64_t)p * g.D_m);
+#pragma unroll
+        for (int u = 0; u < UM; ++u)
+            if (lane + kWave * u < NM)
+                dm[lane + kWave * u] = a[j][u];
+#pragma unroll
+        for (int u = 0; u < UD; ++u)
+            if (lane + kWave * u < ND)
+                dd[lane + kWave * u] = b[j][u];
+    }
+    if (lane < NPW && p0 + lane < n) {
+        g.o_mem_ts[p0 + lane] = mts;
+        g.o_mail_ts[p0 + lane] = lts;
+        g.o_ver[p0 + lane] = ver;
+    }
+}
+
+// Whether every row of the four row arrays starts at a multiple of w floats
+// (w = 2 or 4): row lengths multiples of w, bases aligned to 4 w bytes.
+__device__ __forceinline__ bool gather_aligned(const GatherPlan &g, int wm, int wd)
+{
+    const uintptr_t am = reinterpret_cast<uintptr_t>(g.mem) | reinterpret_cast<uintptr_t>(g.o_mem);
+    const uintptr_t ad = reinterpret_cast<uintptr_t>(g.mail) |
+                         reinterpret_cast<uintptr_t>(g.o_mail);
+    return g.M % wm == 0 && (am & (4 * wm - 1)) == 0 && g.D_m % wd == 0 &&
+           (ad & (4 * wd - 1)) == 0;
+}
+
+// Rows p0 .. p0 + kGatherNPW - 1 (those below n) of a gather by one wavefront
+// (VEC: vector accesses where the rows allow them; the launches that carry
+// the gather beside another kernel's blocks keep the 4-byte ones, which need
+// fewer registers).
+template <bool VEC = false>
 __device__ __forceinline__ void gather_rows(const GatherPlan &g, int p0, int n, int lane)
 {
-    if (g.M <= 2 * kWave && g.D_m <= 8 * kWave) {
+    if (VEC && g.M > 0 && g.M <= 4 * kWave && g.D_m > 0 && g.D_m <= 16 * kWave &&
+        gather_aligned(g, 4, 4)) {
+        gather_rows_vec<4, 4, 1, 4, kGatherNPW>(g, p0, n, lane);
+    } else if (VEC && g.M > 0 && g.M <= 4 * kWave && g.D_m > 0 && g.D_m <= 8 * kWave &&
+               gather_aligned(g, 4, 2)) {
+        gather_rows_vec<4, 2, 1, 4, kGatherNPW>(g, p0, n, lane);
+    } else if (g.M <= 2 * kWave && g.D_m <= 8 * kWave) {
         gather_rows_regs<2, 8>(g, p0, n, lane);
     } else {
         for (int j = 0; j < kGatherNPW && p0 + j < n; ++j)

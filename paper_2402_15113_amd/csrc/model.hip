@@ -536,10 +536,32 @@ __device__ __forceinline__ void stage_wave(const StageArgs &g, int c, int lane)
     const float *sp = g.mem_new + (int64_t)p * M;
     float *dm = g.direct ? g.mem + (int64_t)w * M : g.r_mem + (int64_t)c * M;
     float *ml = g.direct ? g.mail + (int64_t)w * D_m : g.r_mail + (int64_t)c * D_m;
-    if (M <= 2 * kWave && D_e <= 4 * kWave) {
+    const float *sq = g.mem_new + (int64_t)q * M, *fe = g.efeat + e * D_e;
+    if (M % 4 == 0 && M <= 4 * kWave && D_e % 2 == 0 && D_m <= 8 * kWave &&
+        ((reinterpret_cast<uintptr_t>(sp) | reinterpret_cast<uintptr_t>(sq) |
+          reinterpret_cast<uintptr_t>(dm)) & 15) == 0 &&
+        ((reinterpret_cast<uintptr_t>(ml) | reinterpret_cast<uintptr_t>(fe)) & 7) == 0) {
+        // vector accesses: the memory row in 16-byte, the message
+        // [s'_p || s'_q || efeat] in 8-byte pieces (pair i of the message
+        // comes from s'_p, s'_q or the feature row); every load first
+        const int m4 = M / 4, h2 = M / 2, n2 = D_m / 2;
+        const f4 a = reinterpret_cast<const f4 *>(sp)[min(lane, m4 - 1)];
+        f2 b[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = min(lane + kWave * u, n2 - 1);
+            const float *src = i < h2 ? sp + 2 * i : (i < M ? sq + 2 * (i - h2) : fe + 2 * (i - M));
+            b[u] = *reinterpret_cast<const f2 *>(src);
+        }
+        if (lane < m4)
+            reinterpret_cast<f4 *>(dm)[lane] = a;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (lane + kWave * u < n2)
+                reinterpret_cast<f2 *>(ml)[lane + kWave * u] = b[u];
+    } else if (M <= 2 * kWave && D_e <= 4 * kWave) {
         // every load before the first store: s'_p, s'_q and the feature row
         // (lane l holds elements l + 64 u, clamped indices)
-        const float *sq = g.mem_new + (int64_t)q * M, *fe = g.efeat + e * D_e;
         float a[2], bq[2], f[4];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {

@@ -64,7 +64,7 @@ __global__ __launch_bounds__(256) void k_gather_state(GatherPlan g)
     const int n = min(*g.n_nodes, g.cap);
     if (p0 >= n)
         return;
-    gather_rows(g, p0, n, threadIdx.x & 63);
+    gather_rows<true>(g, p0, n, threadIdx.x & 63);
 }
 
 tgm_status_t commit_through(tgm_state *st, int64_t target, hipStream_t s)
