@@ -426,14 +426,17 @@ def train_work_model(wl, rows):
 CSRC = ("common.h", "api.hip", "graph.hip", "state.hip", "model.hip", "runner.hip")
 
 
-def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
+def pmc_summary(fetch_csv, write_csv, copy_mib, workload, mfma_csv=None):
     """HBM traffic per launch of every stage kernel from two counter runs.
 
     FETCH_SIZE and WRITE_SIZE are read in KiB per dispatch; each is scaled by
     what it reads for the plain copy of copy_mib MiB (a kernel that moves
     exactly that many bytes each way), so the figures are calibrated HBM
-    bytes.  The result is keyed to a hash of the kernel sources: once those
-    change, the bench reports traffic as unmeasured again."""
+    bytes.  With a third run's SQ_INSTS_VALU_MFMA_MOPS_F32 (512 flop per
+    count) the record also holds the MFMA work each launch executes, which
+    can be less than the algorithmic work where a kernel restates the
+    contraction.  The result is keyed to a hash of the kernel sources: once
+    those change, the bench reports traffic as unmeasured again."""
     import csv
     import re
     assert copy_mib > 0, "--copy-probe-mib must give the size of the calibration copy"
@@ -451,6 +454,7 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
 
     fetch = per_kernel(fetch_csv, "FETCH_SIZE")
     write = per_kernel(write_csv, "WRITE_SIZE")
+    mops = per_kernel(mfma_csv, "SQ_INSTS_VALU_MFMA_MOPS_F32") if mfma_csv else {}
     kib = copy_mib * 1024.0
     # the calibration copy is the largest copy dispatch of the run
     f_copy = max(fetch.get("copy", [0.0])) / kib
@@ -471,14 +475,18 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload):
                "fetch_kib_per_launch": fk, "write_kib_per_launch": wk,
                "copy_factor": {"fetch": f_copy, "write": w_copy, "copy_mib": copy_mib},
                "hbm_bytes_per_launch": hbm}
+        if k in mops:
+            rec["mfma_flops_per_launch"] = 512.0 * sum(mops[k]) / len(mops[k])
         with open(os.path.join(out_dir, f"{k}_{workload}_pmc.json"), "w") as f:
             json.dump(rec, f, indent=1)
     print(f"calibration copy of {copy_mib} MiB: FETCH_SIZE x{f_copy:.4f}, "
           f"WRITE_SIZE x{w_copy:.4f}")
-    print("| kernel | dispatches | FETCH KiB | WRITE KiB | HBM MB / launch |")
-    print("|---|---|---|---|---|")
+    print("| kernel | dispatches | FETCH KiB | WRITE KiB | HBM MB / launch "
+          "| executed MFMA GFLOP / launch |")
+    print("|---|---|---|---|---|---|")
     for k, n, fk, wk, hbm in rows:
-        print(f"| {k} | {n} | {fk:.1f} | {wk:.1f} | {hbm / 1e6:.3f} |")
+        ex = f"{512.0 * sum(mops[k]) / len(mops[k]) / 1e9:.3f}" if k in mops else "—"
+        print(f"| {k} | {n} | {fk:.1f} | {wk:.1f} | {hbm / 1e6:.3f} | {ex} |")
 
 
 def cpu_model():
@@ -636,14 +644,17 @@ def main():
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before pass 1 (the "
                          "calibration kernel of the FETCH_SIZE / WRITE_SIZE counters)")
-    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+    ap.add_argument("--pmc-summary", nargs="+", metavar="CSV",
                     help="no GPU: turn two rocprofv3 --pmc counter_collection.csv files (one "
-                         "FETCH_SIZE run, one WRITE_SIZE run, both with --copy-probe-mib) "
+                         "FETCH_SIZE run, one WRITE_SIZE run, both with --copy-probe-mib; "
+                         "optionally a third, SQ_INSTS_VALU_MFMA_MOPS_F32) "
                          "into profiles/<kernel>_<workload>_pmc.json")
     args = ap.parse_args()
     if args.pmc_summary:
-        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_probe_mib,
-                    args.workload)
+        if len(args.pmc_summary) not in (2, 3):
+            ap.error("--pmc-summary takes FETCH_CSV WRITE_CSV [MFMA_CSV]")
+        pmc_summary(*args.pmc_summary[:2], args.copy_probe_mib, args.workload,
+                    args.pmc_summary[2] if len(args.pmc_summary) == 3 else None)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the stage has no multi-GPU path; "
@@ -804,17 +815,25 @@ def main():
         mfma = work.get(dom, {}).get("flops", 0) > 0
         achieved = dk["TFLOP/s"] if mfma else dk["GB/s"]
         peak = FP32_MFMA_PEAK_TFS if mfma else HBM_PEAK_GBS
-        traffic = None
+        traffic = executed = None
         pmc_path = os.path.join(ROOT, "profiles", f"{dom}_{wl.name}_pmc.json")
         if os.path.exists(pmc_path):
             pmc = json.load(open(pmc_path))
             if pmc.get("source_hash") == source_hash(*pmc.get("sources", [])):
                 traffic = pmc.get("hbm_bytes_per_launch")
+                ex = pmc.get("mfma_flops_per_launch")
+                if mfma and ex:
+                    # what the matrix cores execute per launch (counter run of
+                    # the same sources), beside the algorithmic work
+                    ach = ex / (dk["avg_us"] * 1e-6) / 1e12
+                    executed = {"flops_per_launch": ex, "achieved": ach,
+                                "frac": ach / FP32_MFMA_PEAK_TFS}
         out["roofline"] = {"kernel": dom, "bound": "mfma" if mfma else "hbm",
                            "achieved": achieved, "peak": peak,
                            "unit": "TFLOP/s" if mfma else "GB/s", "frac": achieved / peak,
                            "traffic": traffic,
                            "algorithmic_per_launch": work.get(dom),
+                           "executed_mfma": executed,
                            "avg_launch_us": dk["avg_us"]}
         out["kernels"] = kernels
         # the minimal staleness (Sec. 3.2) for the stage times measured on the
