@@ -2,14 +2,15 @@
 path) against the fp64 oracle.
 
 tgm_stage_run fuses each attention launch with the next iteration's gather
-(k_attn_fold_gather; for JODIE k_tproj_gather) and the staging with the node
+(k_attn_agg_gather; for JODIE k_tproj_gather) and the staging with the node
 projections.  Its optional per-iteration copies of h and of the new memories
 s' let the embeddings and memories of every iteration be compared element by
 element (|gpu - oracle| <= 1e-5 + 1e-4 |oracle|), not only the last one and
 the flushed tables.  Windows (Eq. 2 and Alg. 1 define what each must
 reproduce): the whole WIKI-shaped stream; the first 64 LastFM-shaped
 batches; the first 32 REDDIT-shaped batches at s = 1, 2, 4 and batches
-560..591 of a run from the start; a GDELT-shaped window from a seeded state.
+560..591 of a run from the start; GDELT-shaped batches 48..63 of a run from
+the start, and a GDELT-shaped window at batch 20,000 from a seeded state.
 Also: the executor allocates nothing (tgm_alloc_count does not move).
 """
 import dataclasses
@@ -150,6 +151,20 @@ def test_gdelt_window_every_iteration(orc, model):
     traced_pair(orc, wl, w, j, n, init=synthetic_state(wl, j, 11), gpu_efeat=dev)
     del dev
     torch.cuda.empty_cache()
+
+
+def test_gdelt_from_the_start(orc):
+    """GDELT-shaped (D_e 186, B 4000, s 4): both sides run from the initial
+    state through batch 63 (the GPU with the executor); batches 48..63 are
+    compared every iteration.  The state the window starts from is each side's
+    own: the GPU's after its 48 pipelined batches."""
+    from test_gpu_parity import gdelt_prefix
+    from workloads import CONFIGS, edge_feature_rows
+    wl = gdelt_prefix(64 * 4000)
+    wl = dataclasses.replace(wl, efeat=edge_feature_rows(wl.seed, CONFIGS["gdelt"]["E"],
+                                                          wl.D_e, 0, wl.E))
+    w = make_weights(wl.M, wl.D_e, wl.D_t)
+    traced_pair(orc, wl, w, 0, 64, skip_to=48)
 
 
 @pytest.mark.parametrize("model,mit", [("tgn", None), ("jodie", None),
