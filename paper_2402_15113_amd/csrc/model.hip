@@ -30,8 +30,9 @@ __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + expf
 //   two halves and stream the weights of their half for each of their tasks,
 //   two chunks ahead of the multiply (longer ranges take fewer rounds);
 //   each accumulates r and z over [x | h] and n in its x part and its h part
-//   (which the reset gate scales); the upper half's partial sums go through
-//   LDS to the lower half, which applies the gates.
+//   (which the reset gate scales); the two halves swap partial sums through
+//   LDS, and the lower half applies the gates to the wave's first task, the
+//   upper half to its second.
 // The hb = 0 tasks also write the new memory timestamps.  The same launch
 // runs the batch's latest-message reduce (latest_reduce) first.
 constexpr int kGruWaves = 8;
@@ -335,16 +336,15 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
                             gru_mma<NG>(arow0 + lrow0[q] * SA, cc + 2, KXC, w2[q], ar[q], az[q],
                                         anx[q], anh[q]);
             }
-            if (half) {
-#pragma unroll
-                for (int q = 0; q < S; ++q)
-                    if (live[q]) {
-                        f4 *rw = red + ((j + 4 * q) * 4) * kWave + lane;
-                        rw[0] = ar[q];
-                        rw[kWave] = az[q];
-                        rw[2 * kWave] = anx[q];
-                        rw[3 * kWave] = anh[q];
-                    }
+            // swap partial sums: slot 0 is finished by the lower half and slot
+            // 1 by the upper half, each handing the other its sums
+            const int give = half ? 0 : 1;
+            if (live[give]) {
+                f4 *rw = red + ((j + 4 * give) * 4) * kWave + lane;
+                rw[0] = give ? ar[1] : ar[0];
+                rw[kWave] = give ? az[1] : az[0];
+                rw[2 * kWave] = give ? anx[1] : anx[0];
+                rw[3 * kWave] = give ? anh[1] : anh[0];
             }
         }
         const int64_t tn = te;
@@ -352,24 +352,24 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
         if (tn < t1)   // the next round's rows, in flight during the epilogue
             rows.load(g, (int)(tn / MB) * 16, round_rows(tn, ten), wave, lane);
         __syncthreads();
-        if (!half) {
-#pragma unroll
-            for (int q = 0; q < S; ++q) {
-                if (!live[q])
-                    continue;
+        {
+            const int q = half;   // the slot this wave finishes
+            if (live[q]) {
                 // lane holds values v = 0..3 of rows 4 (lane / 16) + v, column
                 // hb 16 + lane % 16
                 const f4 *rq = red + ((j + 4 * q) * 4) * kWave + lane;
-                const f4 sr = ar[q] + rq[0], sz = az[q] + rq[kWave];
-                const f4 snx = anx[q] + rq[2 * kWave], snh = anh[q] + rq[3 * kWave];
-                const int col = hb[q] * 16 + (lane & 15);
+                const f4 sr = (q ? ar[1] : ar[0]) + rq[0], sz = (q ? az[1] : az[0]) + rq[kWave];
+                const f4 snx = (q ? anx[1] : anx[0]) + rq[2 * kWave];
+                const f4 snh = (q ? anh[1] : anh[0]) + rq[3 * kWave];
+                const int hbq = q ? hb[1] : hb[0], lrq = q ? lrow0[1] : lrow0[0];
+                const int col = hbq * 16 + (lane & 15);
                 const int colc = col < M ? col : 0;
                 const float b_r = g.bias[colc], b_z = g.bias[MP + colc];
                 const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
                 if (col < M) {
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        const int lr = lrow0[q] + 4 * (lane >> 4) + v;
+                        const int lr = lrq + 4 * (lane >> 4) + v;
                         const int p = row0 + lr;
                         if (p < n) {
                             const float h = A[lr * SA + KX + col];
@@ -388,8 +388,8 @@ __device__ __forceinline__ void gru_body(const GruArgs &g, float *lds, int *s_ha
                         }
                     }
                 }
-                if (hb[q] == 0 && g.new_mem_ts && lane < 16 && row0 + lrow0[q] + lane < n)
-                    g.new_mem_ts[row0 + lrow0[q] + lane] = s_nts[lrow0[q] + lane];
+                if (hbq == 0 && g.new_mem_ts && lane < 16 && row0 + lrq + lane < n)
+                    g.new_mem_ts[row0 + lrq + lane] = s_nts[lrq + lane];
             }
         }
         if (tn >= t1)
