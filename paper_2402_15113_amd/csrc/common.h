@@ -149,6 +149,10 @@ struct tgm_model {
     // GRU: packed B operands and biases
     int32_t KXC = 0, KHC = 0, MB = 0;   // 16-wide chunks of D_x, M and hidden blocks
     tgm::f4 *gru_bx = nullptr;           // [3][KXC][MB][64]
+    // the GRU with one hidden block's weights resident in LDS (when the shapes
+    // fit) and its time-encoding input [max_nodes x D_t], formed per call
+    bool gru_w = false;
+    float *phi = nullptr;
     tgm::f4 *gru_bh = nullptr;           // [3][KHC][MB][64]
     float *gru_bias = nullptr;           // [4][MB*16]: b_ir+b_hr, b_iz+b_hz, b_in, b_hn
     double *omega = nullptr, *beta = nullptr;
@@ -243,6 +247,17 @@ __device__ __forceinline__ void keep_loaded(const f4 &a) { asm volatile("" ::"v"
 // Keeps the scheduler from moving instructions across this point (used right
 // after the prefetch loads so they are issued before the iteration's MFMAs).
 __device__ __forceinline__ void issue_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// A workgroup barrier that orders LDS accesses only: each wave waits for its
+// own LDS operations (lgkmcnt), not for its global loads still in flight,
+// which __syncthreads (a release fence over every address space) also waits
+// for.  For exchanges through LDS while the next operands stream in.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 // Reductions over one 16-lane DPP row (lanes 16i .. 16i + 15) with row-local
 // DPP moves: swaps inside quads (quad_perm [1,0,3,2], then [2,3,0,1]), then the
@@ -430,6 +445,11 @@ struct GatherPlan {
     float *o_mem = nullptr, *o_mail = nullptr;
     double *o_mem_ts = nullptr, *o_mail_ts = nullptr;
     int32_t *o_ver = nullptr;
+    // optional: the GRU's time input phi(mail_ts - mem_ts) of each fetched
+    // node ([cap x D_t], zero for a node without mail), formed by the gather
+    const double *omega = nullptr, *beta = nullptr;
+    int32_t D_t = 0;
+    float *o_phi = nullptr;
 };
 
 // Row p of a gather, copied by one wavefront.  Every load of the node's two
@@ -601,9 +621,28 @@ __device__ __forceinline__ bool gather_aligned(const GatherPlan &g, int wm, int 
 // (VEC: vector accesses where the rows allow them; the launches that carry
 // the gather beside another kernel's blocks keep the 4-byte ones, which need
 // fewer registers).
+// phi of the fetched nodes p0 .. p0 + kGatherNPW - 1 (those below n), when the
+// plan asks for it: cos(omega_d (mail_ts - mem_ts) + beta_d) for a node with
+// mail, zero otherwise (the node's times and version as the gather copies
+// them)
+__device__ __forceinline__ void gather_phi(const GatherPlan &g, int p0, int n, int lane)
+{
+    if (!g.o_phi)
+        return;
+    for (int j = 0; j < kGatherNPW && p0 + j < n; ++j) {
+        const int32_t v = g.nodes[p0 + j];
+        const double dt = g.mail_ts[v] - g.mem_ts[v];
+        const bool has = g.ver[v] >= 0;
+        float *o = g.o_phi + (int64_t)(p0 + j) * g.D_t;
+        for (int d = lane; d < g.D_t; d += kWave)
+            o[d] = has ? time_enc(g.omega[d], g.beta[d], dt) : 0.f;
+    }
+}
+
 template <bool VEC = false>
 __device__ __forceinline__ void gather_rows(const GatherPlan &g, int p0, int n, int lane)
 {
+    gather_phi(g, p0, n, lane);
     if (VEC && g.M > 0 && g.M <= 4 * kWave && g.D_m > 0 && g.D_m <= 16 * kWave &&
         gather_aligned(g, 4, 4)) {
         gather_rows_vec<4, 4, 1, 4, kGatherNPW>(g, p0, n, lane);
@@ -767,6 +806,10 @@ tgm_status_t launch_gather(const GatherPlan &plan, hipStream_t s);
 // projections; the attention fused with the next fetch's gather, which needs
 // only the staging's commits.  Same results as tgm_update_memory and
 // tgm_embed of iter followed by tgm_fetch_memory of iter + 1.
+// Makes a fetch plan form the GRU's phi input of the model m as well (when
+// the model's GRU reads it precomputed).
+void phi_plan(const tgm_model *m, GatherPlan *plan);
+
 tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
                                const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
                                int32_t cap, int64_t first_event, int32_t b, int32_t nb,

@@ -415,6 +415,264 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru(GruArgs g)
         gru_body<1, 8, 2, NG>(g, lds, s_has, s_nts);
 }
 
+// ------------------------------------------------------------------ GRU, weights resident
+// The same cell as k_gru with the operands the other way round: workgroup b
+// owns hidden block hb = b % MB, keeps that block's weight fragments (all k
+// chunks, every gate) in LDS for the whole launch, and streams the rows of
+// its range of 16-row blocks through them.  Wavefronts j and j + 4 (one SIMD)
+// split the k range of a row block in two halves, as in k_gru; the four
+// pairs take the range's row blocks four at a time.  The A operand comes
+// straight from the fetched rows in global memory (mail || phi | mem), kGwDepth
+// chunks ahead of the multiply, where phi(mail_ts - mem_ts) was formed once
+// per node by k_phi.  After a row block the two halves swap the partial sums
+// of two of the four rows each lane holds and apply the gates to the other
+// two.
+#ifndef GW_DEPTH
+#define GW_DEPTH 4
+#endif
+constexpr int kGwDepth = GW_DEPTH;   // A chunks in flight per wavefront
+
+// phi[p][d] = cos(omega_d (mail_ts - mem_ts) + beta_d) for the nodes of the
+// set that hold mail (zero otherwise): the time part of the GRU input.
+__global__ __launch_bounds__(256) void k_phi(const int32_t *__restrict__ n_nodes, int32_t cap,
+                                             int D_t, const double *__restrict__ mem_ts,
+                                             const double *__restrict__ mail_ts,
+                                             const int32_t *__restrict__ ver,
+                                             const double *__restrict__ omega,
+                                             const double *__restrict__ beta,
+                                             float *__restrict__ phi)
+{
+    const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const int n = min(*n_nodes, cap);
+    if (i >= (int64_t)n * D_t)
+        return;
+    const int p = (int)(i / D_t), d = (int)(i - (int64_t)p * D_t);
+    phi[i] = ver[p] >= 0 ? time_enc(omega[d], beta[d], mail_ts[p] - mem_ts[p]) : 0.f;
+}
+
+// A fragment of k-chunk c for row p (lane holds k = 16 c + 4 (lane / 16) + 0..3),
+// as two 8-byte pairs: x chunks from the mail row and phi (D_m and D_t even,
+// so a pair never straddles a boundary), h chunks from the memory row.  Past
+// each part the pair is read from the row's start instead: the packed weights
+// are zero there, and every value read is finite, so those products add zero.
+// Only addresses are selected: a select on a loaded value would make the
+// compiler wait for the load where the select is.
+struct GwA {
+    f2 lo, hi;
+};
+
+__device__ __forceinline__ GwA gw_a(const GruArgs &g, const float *mrow, const float *frow,
+                                    const float *hrow, int c, int lane)
+{
+    // global address space spelled out: a pointer picked by a select would
+    // otherwise be loaded as a flat address, which the LDS counter also counts
+    typedef const f2 __attribute__((address_space(1))) *gf2;
+    const int KXC = g.KXC, D_m = g.D_m, D_x = g.D_m + g.D_t;
+    const float *s0, *s1;
+    if (c < KXC) {
+        const int k = 16 * c + 4 * (lane >> 4), k1 = k + 2;
+        s0 = k < D_m ? mrow + k : (k < D_x ? frow + (k - D_m) : mrow);
+        s1 = k1 < D_m ? mrow + k1 : (k1 < D_x ? frow + (k1 - D_m) : mrow);
+    } else {
+        const int k = 16 * (c - KXC) + 4 * (lane >> 4);
+        s0 = k < g.M ? hrow + k : hrow;
+        s1 = k < g.M ? hrow + k + 2 : hrow;
+    }
+    return GwA{*(gf2)(s0), *(gf2)(s1)};
+}
+
+template <int NG>
+__global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float *phi)
+{
+    extern __shared__ float lds[];
+    const int n = *g.n_nodes;
+    latest_reduce(g, n);
+    const int M = g.M, MB = g.MB, KXC = g.KXC, KC = g.KXC + g.KHC, D_t = g.D_t;
+    const int R = (int)gridDim.x / MB;   // row-block ranges
+    const int hb = (int)blockIdx.x % MB, r = (int)blockIdx.x / MB;
+    const int nrb = (n + 15) >> 4;
+    const int rb0 = (int)((int64_t)nrb * r / R), rb1 = (int)((int64_t)nrb * (r + 1) / R);
+    if (r >= R || rb0 >= rb1)
+        return;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int j = wave & 3, half = wave >> 2;
+    const int kc0 = half ? KC / 2 : 0, kc1 = half ? KC : KC / 2;
+    f4 *W = reinterpret_cast<f4 *>(lds);        // [KC][NG][64] fragments of block hb
+    f2 *red = reinterpret_cast<f2 *>(W + (int64_t)KC * NG * kWave);   // [2][4][2][4][64]
+
+    // the rows of this pair's first block, then the weights of block hb
+    const int steps = (rb1 - rb0 + 3) >> 2;
+    int rb = rb0 + j;
+    auto rows_of = [&](int b, const float *&mrow, const float *&frow, const float *&hrow) {
+        const int p = min(b * 16 + (lane & 15), n - 1);   // rows past n repeat the last
+        mrow = g.mail + (int64_t)p * g.D_m;
+        frow = phi + (int64_t)p * D_t;
+        hrow = g.mem + (int64_t)p * M;
+    };
+    const float *mrow, *frow, *hrow;
+    rows_of(min(rb, rb1 - 1), mrow, frow, hrow);
+    GwA ring[kGwDepth];
+#pragma unroll
+    for (int q = 0; q < kGwDepth; ++q)
+        ring[q] = gw_a(g, mrow, frow, hrow, min(kc0 + q, kc1 - 1), lane);
+    {
+        // sixteen fragments per thread in flight before their LDS stores
+        const int64_t kstep = (int64_t)MB * kWave;
+        const int64_t gx = (int64_t)KXC * kstep, gh = (int64_t)g.KHC * kstep;
+        const int total = KC * NG * kWave;
+        for (int i0 = 0; i0 < total; i0 += 16 * (int)blockDim.x) {
+            f4 v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int i = min(i0 + u * (int)blockDim.x + tid, total - 1);
+                const int l = i & (kWave - 1), cq = i >> 6, c = cq / NG, q = cq - c * NG;
+                const bool x = c < KXC;
+                const f4 *src = (x ? g.bx + (int64_t)c * kstep
+                                   : g.bh + (int64_t)(c - KXC) * kstep) +
+                                (int64_t)hb * kWave + l;
+                v[u] = src[q * (x ? gx : gh)];
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int i = i0 + u * (int)blockDim.x + tid;
+                if (i < total)
+                    W[i] = v[u];
+            }
+        }
+    }
+    const int MP = MB * 16;
+    const int col = hb * 16 + (lane & 15);
+    const int colc = col < M ? col : 0;
+    const float b_r = g.bias[colc], b_z = g.bias[MP + colc];
+    const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
+    lds_barrier();   // the weights are in LDS; the A chunks stay in flight
+
+    const int vm = half ? 2 : 0;   // the two of a lane's four rows this wave finishes
+    for (int st = 0; st < steps; ++st, rb += 4) {
+        const bool live = rb < rb1;
+        // the epilogue's inputs of this wave's two rows, in flight during the
+        // multiply
+        float h2[2];
+        int has2[2];
+        double nts2[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int p = min(min(rb, rb1 - 1) * 16 + 4 * (lane >> 4) + vm + u, n - 1);
+            h2[u] = g.mem[(int64_t)p * M + colc];
+            has2[u] = g.ver[p] >= 0;
+            nts2[u] = has2[u] ? g.mail_ts[p] : g.mem_ts[p];
+        }
+        f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
+        if (live) {
+            // chunk c multiplies from ring slot (c - kc0) % kGwDepth, which
+            // then loads chunk c + kGwDepth (clamped: the last rounds reload
+            // the range's last chunk); the B fragments of chunk c + 1 are read
+            // from LDS before chunk c multiplies
+            f4 bw[3], bn[3];
+            auto b_read = [&](int c, f4(&b)[3]) {
+                const f4 *wb = W + (int64_t)min(c, kc1 - 1) * NG * kWave + lane;
+#pragma unroll
+                for (int q = 0; q < NG; ++q)
+                    b[q] = wb[q * kWave];
+            };
+            b_read(kc0, bw);
+            for (int c0 = kc0; c0 < kc1; c0 += kGwDepth) {
+#pragma unroll
+                for (int q = 0; q < kGwDepth; ++q) {
+                    const int c = c0 + q;
+                    if (c < kc1) {
+                        const f4 a = {ring[q].lo[0], ring[q].lo[1], ring[q].hi[0],
+                                      ring[q].hi[1]};
+                        b_read(c + 1, bn);
+                        if (NG == 3) {
+                            ar = mfma_k16(a, bw[0], ar);
+                            az = mfma_k16(a, bw[1], az);
+                            if (c < KXC)
+                                anx = mfma_k16(a, bw[2], anx);
+                            else
+                                anh = mfma_k16(a, bw[2], anh);
+                        } else {
+                            if (c < KXC)
+                                anx = mfma_k16(a, bw[0], anx);
+                            else
+                                anh = mfma_k16(a, bw[0], anh);
+                        }
+                        ring[q] = gw_a(g, mrow, frow, hrow, min(c + kGwDepth, kc1 - 1), lane);
+#pragma unroll
+                        for (int u = 0; u < NG; ++u)
+                            bw[u] = bn[u];
+                    }
+                    issue_fence();
+                }
+            }
+        }
+        // the next row block's first chunks load during the exchange and the
+        // gates (its rows, or the last block's again when this was the last)
+        const int rbn = rb + 4;
+        rows_of(min(rbn, rb1 - 1), mrow, frow, hrow);
+        // values v = 0..3 of rows 4 (lane / 16) + v: the lower half keeps v =
+        // 0, 1 and hands over v = 2, 3; the upper half the reverse
+        // (the swap area alternates between steps, so a step's sums never
+        // land where the previous step's are still being read)
+        f2 *rs = red + (st & 1) * (4 * 2 * 4 * kWave);
+        f2 *rw = rs + ((j * 2 + half) * 4) * kWave + lane;
+        const int vo = half ? 0 : 2;
+        if (live) {
+            rw[0] = f2{ar[vo], ar[vo + 1]};
+            rw[kWave] = f2{az[vo], az[vo + 1]};
+            rw[2 * kWave] = f2{anx[vo], anx[vo + 1]};
+            rw[3 * kWave] = f2{anh[vo], anh[vo + 1]};
+        }
+#pragma unroll
+        for (int q = 0; q < kGwDepth; ++q)
+            if (rbn < rb1)
+                ring[q] = gw_a(g, mrow, frow, hrow, min(kc0 + q, kc1 - 1), lane);
+        lds_barrier();   // the next block's A chunks stay in flight
+        if (live) {
+            const f2 *ro = rs + ((j * 2 + (half ^ 1)) * 4) * kWave + lane;
+            const f2 pr = ro[0], pz = ro[kWave], pnx = ro[2 * kWave], pnh = ro[3 * kWave];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int v = vm + u;
+                const int p = rb * 16 + 4 * (lane >> 4) + v;
+                if (p < n && col < M) {
+                    const float h = h2[u];
+                    float o = h;
+                    if (has2[u]) {
+                        if (NG == 3) {
+                            const float rr = sigmoidf_(ar[v] + pr[u] + b_r);
+                            const float z = sigmoidf_(az[v] + pz[u] + b_z);
+                            const float nn =
+                                tanhf(anx[v] + pnx[u] + b_nx + rr * (anh[v] + pnh[u] + b_nh));
+                            o = (1.0f - z) * nn + z * h;
+                        } else {   // the RNN cell
+                            o = tanhf((anx[v] + pnx[u] + b_nx) + (anh[v] + pnh[u] + b_nh));
+                        }
+                    }
+                    g.mem_new[(int64_t)p * M + col] = o;
+                    if (hb == 0 && g.new_mem_ts && (lane & 15) == 0)
+                        g.new_mem_ts[p] = nts2[u];
+                }
+            }
+        }
+    }
+}
+
+// LDS of k_gru_w: the weight fragments of one hidden block and the swap area
+size_t gru_w_lds(const tgm_model *m, int NG)
+{
+    return (size_t)(m->KXC + m->KHC) * NG * kWave * 16 + 2 * 4 * 2 * 4 * kWave * 8;
+}
+
+// Shapes k_gru_w handles: 8-byte pairs of the mail row, phi and the memory
+// row; the weights of a hidden block within the LDS
+bool gru_w_fits(const tgm_model *m, int NG)
+{
+    return m->D_m % 2 == 0 && m->D_t % 2 == 0 && m->M % 4 == 0 && m->MB <= kGruGrid &&
+           gru_w_lds(m, NG) <= 160 * 1024;
+}
+
 // JODIE's embedding: the time projection h[r] = s'[p] * (1 + w_t (t_r - ts'[p]))
 // of root r's updated memory (p = root_pos[r]), in fp64, one thread per
 // element of h.  A position outside the node set yields a zero row.
@@ -2355,6 +2613,23 @@ namespace {
 // kernel's layout (one gate block, in the slot of the GRU's n gate, and its
 // biases b_ih, b_hh in the n slots), the time encoding, the time projection
 // and the executor's buffer of new memory times.
+// The resident-weight GRU when the shapes fit: its phi buffer and LDS opt-in.
+tgm_status_t gru_w_setup(tgm_model *m, int NG)
+{
+    m->gru_w = gru_w_fits(m, NG);
+    if (!m->gru_w)
+        return TGM_OK;
+    if (dev_malloc((void **)&m->phi,
+                   sizeof(float) * std::max<size_t>(1, (size_t)m->max_nodes * m->D_t)) !=
+        hipSuccess)
+        return TGM_ENOMEM;
+    const void *f = NG == 1 ? (const void *)k_gru_w<1> : (const void *)k_gru_w<3>;
+    if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)gru_w_lds(m, NG)) != hipSuccess)
+        return TGM_EINVAL;
+    return TGM_OK;
+}
+
 tgm_status_t create_jodie(tgm_model *m, const tgm_model_desc *d, const tgm_weights *w)
 {
     const int M = m->M, D_x = m->D_x, D_t = m->D_t, MP = m->MB * 16;
@@ -2387,7 +2662,7 @@ tgm_status_t create_jodie(tgm_model *m, const tgm_model_desc *d, const tgm_weigh
     if (hipFuncSetAttribute((const void *)k_gru<1>, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)gru_lds(m)) != hipSuccess)
         return TGM_EINVAL;
-    return TGM_OK;
+    return gru_w_setup(m, 1);
 }
 
 }  // namespace
@@ -2411,6 +2686,7 @@ extern "C" tgm_status_t tgm_model_destroy(tgm_model_t m)
     hipFree(m->b_o);
     hipFree(m->w_t);
     hipFree(m->nts);
+    hipFree(m->phi);
     delete m;
     return TGM_OK;
 }
@@ -2589,6 +2865,8 @@ extern "C" tgm_status_t tgm_model_create(const tgm_model_desc *d, const tgm_weig
             st = TGM_EINVAL;   // dimensions beyond the LDS of one workgroup
             break;
         }
+        if ((st = gru_w_setup(m, 3)) != TGM_OK)
+            break;
     } while (0);
     hipFree(wq_dev);
     if (st != TGM_OK) {
@@ -2610,7 +2888,8 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
                           const int32_t *ver, int64_t first_event, int32_t b,
                           const int32_t *src_pos, const int32_t *dst_pos, float *mem_new,
                           double *new_mem_ts, hipStream_t s, StageArgs *sa, int *n_items,
-                          uint64_t *tag_out, uint64_t *ext_win = nullptr, uint64_t ext_tag = 0)
+                          uint64_t *tag_out, uint64_t *ext_win = nullptr, uint64_t ext_tag = 0,
+                          bool phi_ready = false)
 {
     if (!st || !m || !g || !n_nodes || cap < 0 || b < 0 || first_event < 0 ||
         first_event + b > g->E)
@@ -2651,11 +2930,30 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
         ga.mem_new = mem_new; ga.new_mem_ts = new_mem_ts;
         ga.n_cand = ext_win ? 0 : n_cand; ga.src_pos = src_pos; ga.dst_pos = dst_pos;
         ga.win = win; ga.tag = tag;
-        // persistent: the node set's tasks are split over kGruGrid workgroups
-        if (m->kind == TGM_MODEL_JODIE)
+        const bool jodie = m->kind == TGM_MODEL_JODIE;
+        const bool w_ok = m->gru_w &&
+                          ((reinterpret_cast<uintptr_t>(mem) | reinterpret_cast<uintptr_t>(mail)) &
+                           7) == 0;
+        if (w_ok) {
+            // phi once per node (unless the fetch formed it), then MB hidden
+            // blocks x (kGruGrid / MB) row ranges
+            if (m->D_t > 0 && !phi_ready)
+                TGM_LAUNCH(k_phi, dim3((unsigned)cdiv((int64_t)cap * m->D_t, 256)), dim3(256), 0,
+                           s, n_nodes, cap, m->D_t, mem_ts, mail_ts, ver, m->omega, m->beta,
+                           m->phi);
+            const dim3 grid((unsigned)(m->MB * (kGruGrid / m->MB)));
+            if (jodie)
+                TGM_LAUNCH(k_gru_w<1>, grid, dim3(64 * kGruWaves), gru_w_lds(m, 1), s, ga,
+                           m->phi);
+            else
+                TGM_LAUNCH(k_gru_w<3>, grid, dim3(64 * kGruWaves), gru_w_lds(m, 3), s, ga,
+                           m->phi);
+        } else if (jodie) {
+            // persistent: the node set's tasks are split over kGruGrid workgroups
             TGM_LAUNCH(k_gru<1>, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
-        else
+        } else {
             TGM_LAUNCH(k_gru<3>, dim3(kGruGrid), dim3(64 * kGruWaves), gru_lds(m), s, ga);
+        }
     }
     const size_t base = (size_t)(iter % slots) * st->ring_rows();
     // the write set of iteration iter - s is committed by the staging launch
@@ -2905,6 +3203,16 @@ extern "C" tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int
     return TGM_OK;
 }
 
+void tgm::phi_plan(const tgm_model *m, GatherPlan *plan)
+{
+    if (!m || !plan || !m->gru_w || m->D_t == 0)
+        return;
+    plan->omega = m->omega;
+    plan->beta = m->beta;
+    plan->D_t = m->D_t;
+    plan->o_phi = m->phi;
+}
+
 tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t iter,
                                     const tgm_sample_buffers &sb, const tgm_fetch_buffers &fb,
                                     int32_t cap, int64_t first_event, int32_t b, int32_t nb,
@@ -2927,7 +3235,7 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     tgm_status_t rc = update_begin(st, m, g, iter, sb.n_nodes, cap, fb.mem, fb.mem_ts, fb.mail,
                                    fb.mail_ts, fb.ver, first_event, b, sb.root_pos,
                                    sb.root_pos + b, mem_new, nts, s, &sa, &n_items, &tag,
-                                   xwin, xtag);
+                                   xwin, xtag, true);   // every executor fetch forms phi
     if (rc != TGM_OK)
         return rc;
     if (jodie) {
@@ -2942,6 +3250,7 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
             TGM_TRY_STATUS(fetch_plan(st, iter + 1, next_sb->nodes, next_sb->n_nodes, cap,
                                       fb.mem, fb.mem_ts, fb.mail, fb.mail_ts, fb.ver, s,
                                       &next_plan));
+            phi_plan(m, &next_plan);
             has_next = next_plan.cap > 0;
         }
         if (n_items > 0)
@@ -2972,6 +3281,7 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
                         fb.mail, fb.mail_ts, fb.ver, s, &next_plan);
         if (rc != TGM_OK)
             return rc;
+        phi_plan(m, &next_plan);
         next = &next_plan;
     }
     // staging items ride in blocks after the projection's

@@ -93,6 +93,7 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
         GatherPlan plan;
         TGM_TRY_STATUS(fetch_plan(st, i0, sb[0].nodes, sb[0].n_nodes, cap, fb->mem, fb->mem_ts,
                                   fb->mail, fb->mail_ts, fb->ver, main, &plan));
+        phi_plan(m, &plan);
         TGM_TRY_STATUS(launch_gather(plan, main));
     }
     for (int64_t c = 0; c < nch; ++c) {
@@ -124,6 +125,7 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
                     TGM_TRY_STATUS(fetch_plan(st, i0 + k + 1, next->nodes, next->n_nodes, cap,
                                               fb->mem, fb->mem_ts, fb->mail, fb->mail_ts,
                                               fb->ver, main, &plan));
+                    phi_plan(m, &plan);
                     TGM_TRY_STATUS(launch_gather(plan, main));
                 }
             }

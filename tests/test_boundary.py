@@ -22,8 +22,9 @@ SETUP = {"tgm_graph_create", "tgm_state_create", "tgm_model_create", "create_jod
          "tgm_mitigator_create", "mitigate_reserve", "tgm_state_set_mitigation",
          "tgm_state_save", "tgm_state_restore", "tgm_state_load", "tgm_state_read",
          "upload", "tgm_profile_get", "tgm_profile_count", "fold_profile", "take_event",
-         "tgm_noalloc_init", "static_scratch_ptr"}
-SETUP_CALLERS = {"mitigate_reserve": {"tgm_mitigator_create", "tgm_state_set_mitigation"}}
+         "tgm_noalloc_init", "static_scratch_ptr", "gru_w_setup"}
+SETUP_CALLERS = {"mitigate_reserve": {"tgm_mitigator_create", "tgm_state_set_mitigation"},
+                 "gru_w_setup": {"tgm_model_create", "create_jodie"}}
 FORBIDDEN = re.compile(r"\b(dev_malloc|hipMalloc\w*|hipDeviceSynchronize|hipEventCreate\w*|"
                        r"hipMemset|hipStreamSynchronize|hipHostMalloc|hipFree)\s*\(")
 
