@@ -325,7 +325,12 @@ def work_model(wl, rows, model="tgn"):
         "k_batch_roots": dict(flops=0, bytes=b * (3 * 4 + d) + 3 * b * (4 + d)),
         # the executor's latest-message reduce: 2b positions in, 2b 64-bit atomics
         "k_latest": dict(flops=0, bytes=2 * b * (4 + 8)),
+        # phi of every fetched node: its two times and version in, D_t values out
+        "k_phi": dict(flops=0, bytes=n_U * (d + d + 4 + D_t * f)),
     }
+    # the GRU with resident weights: the same cell, its time input read as phi
+    k["k_gru_w"] = dict(flops=k["k_gru"]["flops"],
+                        bytes=k["k_gru"]["bytes"] + n_U * D_t * f)
     # the executor's fused launches: staging + node projection; attention +
     # the next iteration's gather
     k["k_stage_proj"] = dict(flops=k["k_node_proj"]["flops"],

@@ -432,8 +432,10 @@ def from_workload(wl, w, *, s=None, device="cuda", stream=None, mitigation=None,
 # attention kernel, so the feature fetch has no kernel of its own; the
 # mitigation belongs to the memory fetch (Sec. 3.3).
 STAGE_KERNELS = {1: ("k_sample_batch", "k_ns_mark", "k_ns_pos"), 2: (),
-                 3: ("k_gather_state", "k_mit_prep", "k_mit_select", "k_mit_omega"),
-                 4: ("k_gru", "k_node_proj", "k_attn_fold", "k_attn", "k_tproj"),
+                 3: ("k_gather_state", "k_mit_prep", "k_mit_select", "k_mit_omega",
+                     "k_mit_final"),
+                 4: ("k_phi", "k_gru", "k_gru_w", "k_node_proj", "k_attn_agg", "k_attn_fold",
+                     "k_attn", "k_tproj"),
                  5: ("k_stage", "k_commit")}
 
 
