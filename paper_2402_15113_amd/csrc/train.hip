@@ -31,7 +31,11 @@ namespace {
 // wavefronts takes a 64 x 64 tile (32 x 32 per wavefront, v_mfma 16x16x4)
 // over the k range of its split (blockIdx.z); with several splits each
 // writes its partial tile to `part` and k_gemm_reduce adds them in order.
-constexpr int kGT = 64, kGK = 16, kGPad = 4;
+// The k range goes in steps of kGK2 = 32 through two LDS buffers: the next
+// step's elements load into registers while the current step multiplies,
+// and one barrier per step hands the buffers over.  Within a split every
+// accumulator takes its k in increasing order, 16 at a time.
+constexpr int kGT = 64, kGK = 16, kGK2 = 32, kGPad = 4;
 constexpr int kMaxSplits = 64;
 
 struct GemmArgs {
@@ -49,11 +53,26 @@ struct GemmArgs {
     const int32_t *m_live;   // rows at or past *m_live are skipped (NULL: none)
 };
 
+// Element u of this thread's share of a 64 x kGK2 operand tile: (row, kk) of
+// the tile, laid out so that consecutive threads read consecutive addresses.
+template <bool T>
+__device__ __forceinline__ void gemm_elem(int tid, int u, int &r, int &kk)
+{
+    const int e = tid + u * 256;
+    if (T) {   // element (r, kk) at X[kk ld + r]: rows contiguous
+        r = e & (kGT - 1);
+        kk = e >> 6;
+    } else {   // element (r, kk) at X[r ld + kk]: k contiguous
+        r = e >> 5;
+        kk = e & (kGK2 - 1);
+    }
+}
+
 template <bool TA, bool TB>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
 {
-    __shared__ __align__(16) float As[kGT][kGK + kGPad];
-    __shared__ __align__(16) float Bs[kGT][kGK + kGPad];
+    __shared__ __align__(16) float As[2][kGT][kGK2 + kGPad];
+    __shared__ __align__(16) float Bs[2][kGT][kGK2 + kGPad];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m0 = blockIdx.y * kGT, n0 = blockIdx.x * kGT, z = blockIdx.z;
     if (g.m_live && m0 >= *g.m_live)
@@ -61,44 +80,67 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g)
     const int k_lo = z * g.kchunk, k_hi = min(g.k, k_lo + g.kchunk);
     const int wr = (wave >> 1) * 32, wc = (wave & 1) * 32;
     const int q = lane >> 4, rl = lane & 15;
+    // the tile's elements of one k step, loaded branch-free (clamped
+    // addresses; the zero mask is applied where they are stored)
+    constexpr int NE = kGT * kGK2 / 256;
+    float ra[NE], rb[NE];
+    auto load = [&](int k0) {
+#pragma unroll
+        for (int u = 0; u < NE; ++u) {
+            int i, kk;
+            gemm_elem<TA>(tid, u, i, kk);
+            const int gi = min(m0 + i, g.m - 1), gk = min(k0 + kk, g.k - 1);
+            ra[u] = TA ? g.A[(int64_t)gk * g.lda + gi] : g.A[(int64_t)gi * g.lda + gk];
+            int j, kb;
+            gemm_elem<!TB>(tid, u, j, kb);
+            const int gj = min(n0 + j, g.n - 1), gkb = min(k0 + kb, g.k - 1);
+            rb[u] = TB ? g.B[(int64_t)gj * g.ldb + gkb] : g.B[(int64_t)gkb * g.ldb + gj];
+        }
+    };
+    auto store = [&](int k0, int buf) {
+#pragma unroll
+        for (int u = 0; u < NE; ++u) {
+            int i, kk;
+            gemm_elem<TA>(tid, u, i, kk);
+            As[buf][i][kk] = (m0 + i < g.m && k0 + kk < k_hi) ? ra[u] : 0.f;
+            int j, kb;
+            gemm_elem<!TB>(tid, u, j, kb);
+            Bs[buf][j][kb] = (n0 + j < g.n && k0 + kb < k_hi) ? rb[u] : 0.f;
+        }
+    };
     f4 acc[2][2];
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj)
             acc[bi][bj] = f4{0.f, 0.f, 0.f, 0.f};
-    for (int k0 = k_lo; k0 < k_hi; k0 += kGK) {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int e = tid + u * 256;
-            const int i = TA ? (e & 63) : (e >> 4), kk = TA ? (e >> 6) : (e & 15);
-            const int gi = m0 + i, gk = k0 + kk;
-            float v = 0.f;
-            if (gi < g.m && gk < k_hi)
-                v = TA ? g.A[(int64_t)gk * g.lda + gi] : g.A[(int64_t)gi * g.lda + gk];
-            As[i][kk] = v;
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int e = tid + u * 256;
-            const int j = TB ? (e >> 4) : (e & 63), kk = TB ? (e & 15) : (e >> 6);
-            const int gj = n0 + j, gk = k0 + kk;
-            float v = 0.f;
-            if (gj < g.n && gk < k_hi)
-                v = TB ? g.B[(int64_t)gj * g.ldb + gk] : g.B[(int64_t)gk * g.ldb + gj];
-            Bs[j][kk] = v;
-        }
+    if (k_lo < k_hi) {
+        load(k_lo);
+        store(k_lo, 0);
         __syncthreads();
+    }
+    int buf = 0;
+    for (int k0 = k_lo; k0 < k_hi; k0 += kGK2, buf ^= 1) {
+        const bool more = k0 + kGK2 < k_hi;
+        if (more)
+            load(k0 + kGK2);
 #pragma unroll
-        for (int bi = 0; bi < 2; ++bi) {
-            const f4 a = *reinterpret_cast<const f4 *>(&As[wr + bi * 16 + rl][4 * q]);
+        for (int h = 0; h < kGK2 / kGK; ++h) {
 #pragma unroll
-            for (int bj = 0; bj < 2; ++bj) {
-                const f4 b = *reinterpret_cast<const f4 *>(&Bs[wc + bj * 16 + rl][4 * q]);
-                acc[bi][bj] = mfma_k16(a, b, acc[bi][bj]);
+            for (int bi = 0; bi < 2; ++bi) {
+                const f4 a = *reinterpret_cast<const f4 *>(&As[buf][wr + bi * 16 + rl][16 * h + 4 * q]);
+#pragma unroll
+                for (int bj = 0; bj < 2; ++bj) {
+                    const f4 bv =
+                        *reinterpret_cast<const f4 *>(&Bs[buf][wc + bj * 16 + rl][16 * h + 4 * q]);
+                    acc[bi][bj] = mfma_k16(a, bv, acc[bi][bj]);
+                }
             }
         }
-        __syncthreads();
+        if (more) {
+            store(k0 + kGK2, buf ^ 1);
+            __syncthreads();
+        }
     }
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
