@@ -127,17 +127,37 @@ __global__ __launch_bounds__(256) void k_apan_attn(AttnArgs2 a)
     const float *rows = a.f_mb + (int64_t)p * K * D_m;
     const double *ts = a.f_mb_ts + (int64_t)p * K;
     const double tref = ts[cnt - 1];
-    float mine = -INFINITY;   // lane j < cnt: the score of mail j
-    for (int j = 0; j < cnt; ++j) {
-        float acc = 0.f;
-        for (int k = lane; k < D_m; k += kWave)
-            acc += u[k] * rows[(int64_t)j * D_m + k];
-        for (int d = lane; d < D_t; d += kWave)
-            acc += u[D_m + d] * time_enc(a.omega[d], a.beta[d], tref - ts[j]);
-        const float sc = (wave_sum(acc) + a.qb[p]) * a.scale;
-        if (lane == j)
-            mine = sc;
+    // every mail's partial score at once: per element of u, the loads of all
+    // the node's mails are in flight together (each lane sums its elements
+    // in the same order as a mail-by-mail loop would)
+    float part[kApanMaxK];
+#pragma unroll
+    for (int j = 0; j < kApanMaxK; ++j)
+        part[j] = 0.f;
+    for (int k = lane; k < D_m; k += kWave) {
+        const float uk = u[k];
+#pragma unroll
+        for (int j = 0; j < kApanMaxK; ++j)
+            if (j < cnt)
+                part[j] += uk * rows[(int64_t)j * D_m + k];
     }
+    for (int d = lane; d < D_t; d += kWave) {
+        const float ud = u[D_m + d];
+        const double om = a.omega[d], be = a.beta[d];
+#pragma unroll
+        for (int j = 0; j < kApanMaxK; ++j)
+            if (j < cnt)
+                part[j] += ud * time_enc(om, be, tref - ts[j]);
+    }
+    const float qb = a.qb[p];
+    float mine = -INFINITY;   // lane j < cnt: the score of mail j
+#pragma unroll
+    for (int j = 0; j < kApanMaxK; ++j)
+        if (j < cnt) {
+            const float sc = (wave_sum(part[j]) + qb) * a.scale;
+            if (lane == j)
+                mine = sc;
+        }
     float mx = mine;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1)
