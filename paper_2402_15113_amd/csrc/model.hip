@@ -488,8 +488,13 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
     const int n = *g.n_nodes;
     latest_reduce(g, n);
     const int M = g.M, MB = g.MB, KXC = g.KXC, KC = g.KXC + g.KHC, D_t = g.D_t;
-    const int R = (int)gridDim.x / MB;   // row-block ranges
-    const int hb = (int)blockIdx.x % MB, r = (int)blockIdx.x / MB;
+    // workgroup b runs on XCD b % 8; its slot counts XCD-major (the 32 slots
+    // of XCD 0 first), and slots [r MB, (r + 1) MB) take the MB blocks of
+    // row range r, so a range's rows are read by at most two XCDs' L2s
+    const int G = (int)gridDim.x;
+    const int slot = ((int)blockIdx.x & 7) * (G >> 3) + ((int)blockIdx.x >> 3);
+    const int R = G / MB;   // row-block ranges
+    const int hb = slot % MB, r = slot / MB;
     const int nrb = (n + 15) >> 4;
     const int rb0 = (int)((int64_t)nrb * r / R), rb1 = (int)((int64_t)nrb * (r + 1) / R);
     if (r >= R || rb0 >= rb1)
@@ -2936,12 +2941,12 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
                            7) == 0;
         if (w_ok) {
             // phi once per node (unless the fetch formed it), then MB hidden
-            // blocks x (kGruGrid / MB) row ranges
+            // blocks x (kGruGrid / MB) row ranges (kGruGrid % MB workgroups idle)
             if (m->D_t > 0 && !phi_ready)
                 TGM_LAUNCH(k_phi, dim3((unsigned)cdiv((int64_t)cap * m->D_t, 256)), dim3(256), 0,
                            s, n_nodes, cap, m->D_t, mem_ts, mail_ts, ver, m->omega, m->beta,
                            m->phi);
-            const dim3 grid((unsigned)(m->MB * (kGruGrid / m->MB)));
+            const dim3 grid((unsigned)kGruGrid);
             if (jodie)
                 TGM_LAUNCH(k_gru_w<1>, grid, dim3(64 * kGruWaves), gru_w_lds(m, 1), s, ga,
                            m->phi);
