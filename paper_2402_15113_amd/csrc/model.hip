@@ -1012,8 +1012,10 @@ __global__ __launch_bounds__(512) void k_node_proj(ProjArgs a)
 }
 
 // The staging of a write set and the node projections in one launch: blocks
-// [0, n_proj) project, the rest stage (one wavefront per staging item).
-__global__ __launch_bounds__(512) void k_stage_proj(StageArgs sa, ProjArgs pa, int n_proj)
+// [0, n_proj) project, the rest stage (one wavefront per staging item).  At
+// most 80 VGPRs (six waves per SIMD), so a CU that holds two projection
+// workgroups has room for a staging workgroup beside them.
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(6))) void k_stage_proj(StageArgs sa, ProjArgs pa, int n_proj)
 {
     extern __shared__ float lds[];
     if ((int)blockIdx.x < n_proj) {
