@@ -92,6 +92,7 @@ struct tgm_graph {
     const float *efeat = nullptr;
     int64_t *off = nullptr;           // [N + 1]
     tgm::AdjRec *adj = nullptr;       // [n_adj]
+    double *tix = nullptr;            // [cdiv(n_adj, 64)] time of record 64 j
     int64_t n_adj = 0;
     int32_t *ns_stamp = nullptr;      // [N] node-set epoch stamps (scratch of tgm_node_set)
     int32_t ns_epoch = 0;             // epoch of the last tgm_node_set call
@@ -289,30 +290,52 @@ __device__ __forceinline__ float row16_sum(float v)
 
 // One wavefront: the adjacency list of v is sorted by (t, e); returns p, the
 // first entry with ts >= tq, so that [*base, p) are v's strictly earlier
-// events.  A 64-ary search: each round lane l probes the last entry of the
-// l-th of 64 equal segments and the ballot's popcount names the segment that
-// holds p.  An id outside [0, N) has an empty list.
+// events.  An id outside [0, N) has an empty list.
+//
+// tix[j] is the time of adjacency record 64 j (the graph's sparse time index,
+// 8 bytes per 64 records).  The records 64 j inside v's list are searched
+// first in tix, whose entries for one list are contiguous: a 64-ary search
+// where each round lane l probes the last entry of the l-th of 64 equal
+// segments, and the ballot's popcount names the segment that holds the
+// boundary.  With c of those records earlier than tq, every record before
+// the c-th is earlier and the (c+1)-th is not, so the boundary lies in one
+// window of at most 64 records (from the c-th such record, or from the list's
+// start when c = 0, up to the next one or the list's end), counted with one
+// more ballot.
 __device__ __forceinline__ int64_t recent_end(const int64_t *__restrict__ off,
-                                              const AdjRec *__restrict__ adj, int32_t v,
+                                              const AdjRec *__restrict__ adj,
+                                              const double *__restrict__ tix, int32_t v,
                                               double tq, int32_t N, int64_t *base)
 {
     const int lane = threadIdx.x & 63;
     const bool ok = v >= 0 && v < N;
-    *base = ok ? off[v] : 0;
-    int64_t lo = *base, hi = ok ? off[v + 1] : 0;
+    const int64_t b0 = ok ? off[v] : 0, e0 = ok ? off[v + 1] : 0;
+    *base = b0;
+    // indexed records 64 j with b0 <= 64 j < e0: j in [j0, j1)
+    const int64_t j0 = (b0 + kWave - 1) >> 6;
+    const int64_t j1 = e0 > b0 ? max(j0, ((e0 - 1) >> 6) + 1) : j0;
+    int64_t lo = j0, hi = j1;
     while (hi - lo > kWave) {
         const int64_t step = (hi - lo + kWave - 1) / kWave;
         const int64_t probe = lo + (int64_t)(lane + 1) * step - 1;
-        const bool below = probe < hi && adj[probe].ts < tq;
+        const bool below = probe < hi && tix[probe] < tq;
         const int c = __popcll(__ballot(below));
         const int64_t nlo = lo + (int64_t)c * step;
         const int64_t nhi = nlo + step < hi ? nlo + step : hi;
         lo = nlo;
         hi = nhi;
     }
-    const int64_t idx = lo + lane;
-    const bool below = idx < hi && adj[idx].ts < tq;
-    return lo + __popcll(__ballot(below));
+    {
+        const int64_t idx = lo + lane;
+        const bool below = idx < hi && tix[idx] < tq;
+        lo += __popcll(__ballot(below));
+    }
+    // lo - j0 indexed records are earlier than tq
+    const int64_t ws = lo > j0 ? (lo - 1) << 6 : b0;
+    const int64_t we = min(lo > j0 ? ws + kWave : (j0 << 6), e0);
+    const int64_t idx = ws + lane;
+    const bool below = idx < we && adj[idx].ts < tq;
+    return ws + __popcll(__ballot(below));
 }
 
 __device__ __forceinline__ float wave_sum(float v)

@@ -71,6 +71,15 @@ __global__ void k_adj_records(int64_t n, const int32_t *__restrict__ key,
     }
 }
 
+// The sparse time index: tix[j] = time of adjacency record 64 j.
+__global__ void k_time_index(int64_t n_tix, const AdjRec *__restrict__ adj,
+                             double *__restrict__ tix)
+{
+    for (int64_t j = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; j < n_tix;
+         j += (int64_t)gridDim.x * blockDim.x)
+        tix[j] = adj[j * kWave].ts;
+}
+
 int grid_for(int64_t n, int block)
 {
     int64_t g = cdiv(n, block);
@@ -103,7 +112,8 @@ __global__ void k_batch_roots(int64_t first, int32_t b, const int32_t *__restric
 // earlier events, then lanes j < nb read entries p-1-j: the nb most recent
 // strictly earlier events, newest first.
 __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
-                                           const AdjRec *__restrict__ adj, int r, int32_t v,
+                                           const AdjRec *__restrict__ adj,
+                                           const double *__restrict__ tix, int r, int32_t v,
                                            double tq, int32_t N, int32_t nb,
                                            int32_t *__restrict__ nbr, int32_t *__restrict__ eid,
                                            double *__restrict__ nts, int32_t *__restrict__ cnt,
@@ -114,7 +124,7 @@ __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
     if (stamp && v >= 0 && v < N && lane == 0)   // node-set mark of the root (see k_ns_mark)
         stamp[v] = epoch;
     int64_t base;
-    const int64_t p = recent_end(off, adj, v, tq, N, &base);
+    const int64_t p = recent_end(off, adj, tix, v, tq, N, &base);
     const int64_t avail = p - base;
     const int c = avail < nb ? (int)avail : nb;
     if (lane < nb) {
@@ -138,6 +148,7 @@ __device__ __forceinline__ void sample_one(const int64_t *__restrict__ off,
 
 __global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
                                                 const AdjRec *__restrict__ adj,
+                                                const double *__restrict__ tix,
                                                 const int32_t *__restrict__ root,
                                                 const double *__restrict__ root_ts, int32_t R,
                                                 int32_t N, int32_t nb, int32_t *__restrict__ nbr,
@@ -148,13 +159,14 @@ __global__ __launch_bounds__(256) void k_sample(const int64_t *__restrict__ off,
     const int r = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6);
     if (r >= R)
         return;
-    sample_one(off, adj, r, root[r], root_ts[r], N, nb, nbr, eid, nts, cnt);
+    sample_one(off, adj, tix, r, root[r], root_ts[r], N, nb, nbr, eid, nts, cnt);
 }
 
 // Roots of a batch and their sampling in one pass: wavefront r takes root r
 // of src[batch] ++ dst[batch] ++ neg[batch] straight from the event arrays.
 __global__ __launch_bounds__(256) void k_sample_batch(
-    const int64_t *__restrict__ off, const AdjRec *__restrict__ adj, int64_t first, int32_t b,
+    const int64_t *__restrict__ off, const AdjRec *__restrict__ adj,
+    const double *__restrict__ tix, int64_t first, int32_t b,
     const int32_t *__restrict__ src, const int32_t *__restrict__ dst,
     const int32_t *__restrict__ neg, const double *__restrict__ t, int32_t N, int32_t nb,
     int32_t *__restrict__ root, double *__restrict__ root_ts, int32_t *__restrict__ nbr,
@@ -172,7 +184,7 @@ __global__ __launch_bounds__(256) void k_sample_batch(
         root[r] = v;
         root_ts[r] = tq;
     }
-    sample_one(off, adj, r, v, tq, N, nb, nbr, eid, nts, cnt, stamp, epoch);
+    sample_one(off, adj, tix, r, v, tq, N, nb, nbr, eid, nts, cnt, stamp, epoch);
 }
 
 // ------------------------------------------------------------ node set
@@ -390,9 +402,14 @@ extern "C" tgm_status_t tgm_graph_create(int32_t N, int64_t E, const int32_t *sr
             hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
         g->n_adj = n_adj;
         if (dev_malloc(&g->adj, sizeof(AdjRec) * (n_adj > 0 ? n_adj : 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
-        if (n_adj > 0)
+        const int64_t n_tix = cdiv(n_adj, kWave);
+        if (dev_malloc(&g->tix, sizeof(double) * (n_tix > 0 ? n_tix : 1)) != hipSuccess) { fail(TGM_ENOMEM); break; }
+        if (n_adj > 0) {
             hipLaunchKernelGGL(k_adj_records, dim3(grid_for(n_adj, 256)), dim3(256), 0, s, n_adj,
                                key2, val2, src, dst, t, g->adj);
+            hipLaunchKernelGGL(k_time_index, dim3(grid_for(n_tix, 256)), dim3(256), 0, s, n_tix,
+                               g->adj, g->tix);
+        }
         if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) { fail(TGM_EDEVICE); break; }
     } while (0);
     hipFree(bad);
@@ -415,6 +432,7 @@ extern "C" tgm_status_t tgm_graph_destroy(tgm_graph_t g)
         return TGM_EINVAL;
     hipFree(g->off);
     hipFree(g->adj);
+    hipFree(g->tix);
     hipFree(g->ns_stamp);
     delete g;
     return TGM_OK;
@@ -458,7 +476,7 @@ extern "C" tgm_status_t tgm_sample(tgm_graph_t g, const int32_t *root, const dou
         return TGM_EINVAL;
     const int per_block = 256 / kWave;
     TGM_LAUNCH(k_sample, dim3(cdiv(R, per_block)), dim3(256), 0, as_stream(stream),
-                       g->off, g->adj, root, root_ts, R, g->N, nb, nbr, eid, nts, cnt);
+                       g->off, g->adj, g->tix, root, root_ts, R, g->N, nb, nbr, eid, nts, cnt);
     return TGM_OK;
 }
 
@@ -475,7 +493,7 @@ extern "C" tgm_status_t tgm_sample_batch(tgm_graph_t g, int64_t first_event, int
         return TGM_EINVAL;
     const int per_block = 256 / kWave;
     TGM_LAUNCH(k_sample_batch, dim3(cdiv(3 * (int64_t)b, per_block)), dim3(256), 0,
-               as_stream(stream), g->off, g->adj, first_event, b, g->src, g->dst, g->neg, g->t,
+               as_stream(stream), g->off, g->adj, g->tix, first_event, b, g->src, g->dst, g->neg, g->t,
                g->N, nb, root, root_ts, nbr, eid, nts, cnt, nullptr, 0);
     return TGM_OK;
 }
@@ -572,7 +590,7 @@ extern "C" tgm_status_t tgm_sample_nodes(tgm_graph_t g, int64_t first_event, int
     if (b > 0) {   // the sampler stamps every root and neighbour it writes
         const int per_block = 256 / kWave;
         TGM_LAUNCH(k_sample_batch, dim3(cdiv(3 * (int64_t)b, per_block)), dim3(256), 0, s, g->off,
-                   g->adj, first_event, b, g->src, g->dst, g->neg, g->t, g->N, nb, root,
+                   g->adj, g->tix, first_event, b, g->src, g->dst, g->neg, g->t, g->N, nb, root,
                    root_ts, nbr, eid, nts, cnt, g->ns_stamp, epoch);
     }
     return ns_rank(g, root, R, nbr, nb, nodes, n_nodes, root_pos, nbr_pos, epoch, s);

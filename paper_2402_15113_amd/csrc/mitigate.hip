@@ -75,7 +75,8 @@ static_assert(TGM_MITIGATE_NOALLOC_MAX_NODES * (64 + 1 + 1 + 16) * 4 +
 // neighbour; duplicates and ranks come from a loop over the c lanes with
 // readlane (c <= nb <= 64).
 __global__ __launch_bounds__(256) void k_mit_prep(const int64_t *__restrict__ off,
-                                                  const AdjRec *__restrict__ adj, int32_t N,
+                                                  const AdjRec *__restrict__ adj,
+                                                  const double *__restrict__ tix, int32_t N,
                                                   const double *__restrict__ t, int64_t first,
                                                   const int32_t *__restrict__ nodes,
                                                   const int32_t *__restrict__ n_nodes,
@@ -91,7 +92,7 @@ __global__ __launch_bounds__(256) void k_mit_prep(const int64_t *__restrict__ of
     const double T = t[first];
     const int32_t v = nodes[p];
     int64_t base;
-    const int64_t end = recent_end(off, adj, v, T, N, &base);
+    const int64_t end = recent_end(off, adj, tix, v, T, N, &base);
     const int c = end - base < nb ? (int)(end - base) : nb;
     const int32_t w = lane < c ? adj[end - 1 - lane].nbr : INT32_MAX;
     bool dup = false;   // an earlier lane holds the same id
@@ -824,7 +825,7 @@ tgm_status_t prep_launch(const MitWork &w, tgm_graph_t g, int64_t first_event,
 {
     if (cap == 0)
         return TGM_OK;
-    TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->N,
+    TGM_LAUNCH(k_mit_prep, dim3((unsigned)cdiv(cap, 4)), dim3(256), 0, s, g->off, g->adj, g->tix, g->N,
                g->t, first_event, nodes, n_nodes, cap, w.nb, w.nbp, w.nset, w.ncnt);
     return TGM_OK;
 }

@@ -904,7 +904,8 @@ constexpr int kProjMaxPC = 8;   // k-chunks of the node projection (K = M <= 128
 // owns block w of its group and keeps that block's weights in registers,
 // loaded once while the first tile's rows are in flight; the next tile's rows
 // load while a tile multiplies.  Two accumulators alternate over the k steps.
-template <int W, int C>
+// PCM: the k-chunks held in registers (PC <= PCM).
+template <int W, int C, int PCM>
 __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ mem_new, int M,
                                                int PC, const f4 *__restrict__ pb, int PNB,
                                                int CS, const float *__restrict__ pbias,
@@ -937,10 +938,10 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
     WaveRows<W, 4, C> x;
     rows_of(row0);
     x.load(mem_new, off, M, lane);
-    f4 w[kProjMaxPC];
+    f4 w[PCM];
     const int64_t kstep = (int64_t)PNB * kWave;
 #pragma unroll
-    for (int kc = 0; kc < kProjMaxPC; ++kc)   // chunks past PC reload chunk 0, unused
+    for (int kc = 0; kc < PCM; ++kc)   // chunks past PC reload chunk 0, unused
         w[kc] = pb[(int64_t)(kc < PC ? kc : 0) * kstep + (int64_t)cb * kWave + lane];
     const float e0 = pbias[cb * 16 + (lane & 15)];
     for (;;) {
@@ -960,7 +961,7 @@ __device__ __forceinline__ void node_proj_body(int n, const float *__restrict__ 
         if (has_cb) {
             f4 c0 = {0, 0, 0, 0}, c1 = c0;
 #pragma unroll
-            for (int kc = 0; kc < kProjMaxPC; ++kc) {
+            for (int kc = 0; kc < PCM; ++kc) {
                 if (kc < PC) {
                     const f4 a = *reinterpret_cast<const f4 *>(arow + kc * 16);
                     c0 = mfma_16x16x4(a[0], w[kc][0], c0);
@@ -991,35 +992,48 @@ struct ProjArgs {
     float *P;
 };
 
-// Block bid of nblk node-projection blocks.
+// Block bid of nblk node-projection blocks.  LEAN: the caller has checked
+// lean_proj() (M % 4 == 0, 16-byte aligned rows, at most 7 k-chunks), so only
+// the variant with seven weight chunks in registers is compiled in.
+template <bool LEAN>
 __device__ __forceinline__ void node_proj_block(const ProjArgs &a, float *lds, int bid, int nblk)
 {
     const int n = *a.n_nodes;
     if ((bid / a.CS) * 16 >= n || bid >= (nblk / a.CS) * a.CS)
         return;
-    if ((a.M & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mem_new) & 15) == 0)
-        node_proj_body<4, 1>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias, a.P, lds, bid,
-                             nblk);
+    if (LEAN)
+        node_proj_body<4, 1, kProjMaxPC - 1>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias,
+                                             a.P, lds, bid, nblk);
+    else if ((a.M & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mem_new) & 15) == 0)
+        node_proj_body<4, 1, kProjMaxPC>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias, a.P,
+                                         lds, bid, nblk);
     else
-        node_proj_body<1, 2>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias, a.P, lds, bid,
-                             nblk);
+        node_proj_body<1, 2, kProjMaxPC>(n, a.mem_new, a.M, a.PC, a.pb, a.PNB, a.CS, a.pbias, a.P,
+                                         lds, bid, nblk);
+}
+
+bool lean_proj(const ProjArgs &a)
+{
+    return (a.M & 3) == 0 && (reinterpret_cast<uintptr_t>(a.mem_new) & 15) == 0 &&
+           a.PC <= kProjMaxPC - 1;
 }
 
 __global__ __launch_bounds__(512) void k_node_proj(ProjArgs a)
 {
     extern __shared__ float lds[];
-    node_proj_block(a, lds, blockIdx.x, gridDim.x);
+    node_proj_block<false>(a, lds, blockIdx.x, gridDim.x);
 }
 
 // The staging of a write set and the node projections in one launch: blocks
-// [0, n_proj) project, the rest stage (one wavefront per staging item).  At
-// most 80 VGPRs (six waves per SIMD), so a CU that holds two projection
-// workgroups has room for a staging workgroup beside them.
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(6))) void k_stage_proj(StageArgs sa, ProjArgs pa, int n_proj)
+// [0, n_proj) project, the rest stage (one wavefront per staging item).  The
+// lean variant is held to 80 VGPRs (six waves per SIMD), so a CU that holds
+// two projection workgroups has room for a staging workgroup beside them.
+template <bool LEAN>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(LEAN ? 6 : 1))) void k_stage_proj(StageArgs sa, ProjArgs pa, int n_proj)
 {
     extern __shared__ float lds[];
     if ((int)blockIdx.x < n_proj) {
-        node_proj_block(pa, lds, blockIdx.x, n_proj);
+        node_proj_block<LEAN>(pa, lds, blockIdx.x, n_proj);
         return;
     }
     const int waves = blockDim.x >> 6;
@@ -3293,8 +3307,11 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     }
     // staging items ride in blocks after the projection's
     const int n_stage_blocks = (int)cdiv(n_items, proj_waves);
-    if (R > 0 || n_items > 0)
-        TGM_LAUNCH(k_stage_proj, dim3((R > 0 ? proj_grid : 0) + n_stage_blocks),
+    if ((R > 0 || n_items > 0) && lean_proj(pa))
+        TGM_LAUNCH(k_stage_proj<true>, dim3((R > 0 ? proj_grid : 0) + n_stage_blocks),
+                   dim3(64 * proj_waves), proj_lds(m), s, sa, pa, R > 0 ? proj_grid : 0);
+    else if (R > 0 || n_items > 0)
+        TGM_LAUNCH(k_stage_proj<false>, dim3((R > 0 ? proj_grid : 0) + n_stage_blocks),
                    dim3(64 * proj_waves), proj_lds(m), s, sa, pa, R > 0 ? proj_grid : 0);
     TGM_TRY_STATUS(update_winner(sa.win, sb.n_nodes, cap, first_event, tag, winner, s));
     if (R > 0)
