@@ -473,6 +473,9 @@ struct GatherPlan {
     const double *omega = nullptr, *beta = nullptr;
     int32_t D_t = 0;
     float *o_phi = nullptr;
+    // o_mem == nullptr: phi alone, no rows copied (the executor's GRU then
+    // reads the committed tables in place; see tgm_stage_run)
+    void phi_only() { o_mem = nullptr; o_mail = nullptr; o_mem_ts = o_mail_ts = nullptr; o_ver = nullptr; }
 };
 
 // Row p of a gather, copied by one wavefront.  Every load of the node's two
@@ -652,13 +655,24 @@ __device__ __forceinline__ void gather_phi(const GatherPlan &g, int p0, int n, i
 {
     if (!g.o_phi)
         return;
-    for (int j = 0; j < kGatherNPW && p0 + j < n; ++j) {
-        const int32_t v = g.nodes[p0 + j];
-        const double dt = g.mail_ts[v] - g.mem_ts[v];
-        const bool has = g.ver[v] >= 0;
-        float *o = g.o_phi + (int64_t)(p0 + j) * g.D_t;
-        for (int d = lane; d < g.D_t; d += kWave)
-            o[d] = has ? time_enc(g.omega[d], g.beta[d], dt) : 0.f;
+    // every load first (the nodes' times and versions; the stores below could
+    // alias them, so loads after a store would wait for it), then the codes
+    double dt[kGatherNPW];
+    bool has[kGatherNPW];
+#pragma unroll
+    for (int j = 0; j < kGatherNPW; ++j) {
+        const int32_t v = g.nodes[min(p0 + j, n - 1)];
+        dt[j] = g.mail_ts[v] - g.mem_ts[v];
+        has[j] = g.ver[v] >= 0;
+    }
+    for (int d0 = 0; d0 < g.D_t; d0 += kWave) {
+        const int d = d0 + lane;
+        const int dc = min(d, g.D_t - 1);
+        const double om = g.omega[dc], be = g.beta[dc];
+#pragma unroll
+        for (int j = 0; j < kGatherNPW; ++j)
+            if (p0 + j < n && d < g.D_t)
+                g.o_phi[(int64_t)(p0 + j) * g.D_t + d] = has[j] ? time_enc(om, be, dt[j]) : 0.f;
     }
 }
 
@@ -666,6 +680,8 @@ template <bool VEC = false>
 __device__ __forceinline__ void gather_rows(const GatherPlan &g, int p0, int n, int lane)
 {
     gather_phi(g, p0, n, lane);
+    if (!g.o_mem)   // phi only: the GRU reads the committed rows in place
+        return;
     if (VEC && g.M > 0 && g.M <= 4 * kWave && g.D_m > 0 && g.D_m <= 16 * kWave &&
         gather_aligned(g, 4, 4)) {
         gather_rows_vec<4, 4, 1, 4, kGatherNPW>(g, p0, n, lane);
@@ -829,6 +845,11 @@ tgm_status_t launch_gather(const GatherPlan &plan, hipStream_t s);
 // projections; the attention fused with the next fetch's gather, which needs
 // only the staging's commits.  Same results as tgm_update_memory and
 // tgm_embed of iter followed by tgm_fetch_memory of iter + 1.
+// inplace: this iteration's fetch formed phi only (GatherPlan::phi_only),
+// and its GRU reads the committed tables in place at the node set's rows
+// (they still hold exactly the write sets through iter - 1 - s: the next
+// commit comes with this iteration's staging); next_inplace: the same for the
+// fetch of iter + 1 made here.
 // Makes a fetch plan form the GRU's phi input of the model m as well (when
 // the model's GRU reads it precomputed).
 void phi_plan(const tgm_model *m, GatherPlan *plan);
@@ -838,7 +859,8 @@ tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int
                                int32_t cap, int64_t first_event, int32_t b, int32_t nb,
                                float *mem_new, double *new_mem_ts, int64_t *winner, float *h,
                                const tgm_sample_buffers *next_sb, int32_t mit_slot,
-                               uint64_t *xwin, uint64_t xtag, hipStream_t s);
+                               uint64_t *xwin, uint64_t xtag, hipStream_t s,
+                               bool inplace = false, bool next_inplace = false);
 
 // The executor's latest-message reduce of an iteration, on the prefetch
 // stream beside its sample: exec_latest_launch reduces the 2b candidates of

@@ -42,6 +42,9 @@ constexpr int kGruSlots = 2;   // tasks per wave pair and round (rounds of 4 kGr
 
 struct GruArgs {
     const int32_t *n_nodes;
+    // set (k_gru_w only): mem, mail, mem_ts, mail_ts and ver are the committed
+    // tables, read at row nodes[p] for position p of the node set
+    const int32_t *nodes;
     const float *mem, *mail;
     const double *mem_ts, *mail_ts;
     const int32_t *ver;
@@ -509,14 +512,26 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
     // the rows of this pair's first block, then the weights of block hb
     const int steps = (rb1 - rb0 + 3) >> 2;
     int rb = rb0 + j;
-    auto rows_of = [&](int b, const float *&mrow, const float *&frow, const float *&hrow) {
-        const int p = min(b * 16 + (lane & 15), n - 1);   // rows past n repeat the last
-        mrow = g.mail + (int64_t)p * g.D_m;
+    const int vm = half ? 2 : 0;   // the two of a lane's four rows this wave finishes
+    // Position p of the node set reads row p of the fetched rows, or (g.nodes
+    // set) the committed tables' row of node nodes[p]: the ids of a step's
+    // rows load a step ahead.  phi stays by position.
+    auto node_of = [&](int p) -> int { return g.nodes ? g.nodes[p] : p; };
+    auto a_pos = [&](int b) { return min(min(b, rb1 - 1) * 16 + (lane & 15), n - 1); };
+    auto e_pos = [&](int b, int u) {
+        return min(min(b, rb1 - 1) * 16 + 4 * (lane >> 4) + vm + u, n - 1);
+    };
+    auto rows_of = [&](int p, int v, const float *&mrow, const float *&frow, const float *&hrow) {
+        mrow = g.mail + (int64_t)v * g.D_m;   // rows past n repeat the last
         frow = phi + (int64_t)p * D_t;
-        hrow = g.mem + (int64_t)p * M;
+        hrow = g.mem + (int64_t)v * M;
     };
     const float *mrow, *frow, *hrow;
-    rows_of(min(rb, rb1 - 1), mrow, frow, hrow);
+    {
+        const int p = a_pos(rb);
+        rows_of(p, node_of(p), mrow, frow, hrow);
+    }
+    int ve[2] = {node_of(e_pos(rb, 0)), node_of(e_pos(rb, 1))};
     GwA ring[kGwDepth];
 #pragma unroll
     for (int q = 0; q < kGwDepth; ++q)
@@ -553,21 +568,25 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
     const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
     lds_barrier();   // the weights are in LDS; the A chunks stay in flight
 
-    const int vm = half ? 2 : 0;   // the two of a lane's four rows this wave finishes
     for (int st = 0; st < steps; ++st, rb += 4) {
         const bool live = rb < rb1;
         // the epilogue's inputs of this wave's two rows, in flight during the
-        // multiply
+        // multiply, and the next step's row ids
         float h2[2];
         int has2[2];
         double nts2[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-            const int p = min(min(rb, rb1 - 1) * 16 + 4 * (lane >> 4) + vm + u, n - 1);
-            h2[u] = g.mem[(int64_t)p * M + colc];
-            has2[u] = g.ver[p] >= 0;
-            nts2[u] = has2[u] ? g.mail_ts[p] : g.mem_ts[p];
+            const int v = ve[u];
+            h2[u] = g.mem[(int64_t)v * M + colc];
+            has2[u] = g.ver[v] >= 0;
+            nts2[u] = has2[u] ? g.mail_ts[v] : g.mem_ts[v];
         }
+        const int pa_next = a_pos(rb + 4);
+        const int va_next = node_of(pa_next);
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+            ve[u] = node_of(e_pos(rb + 4, u));
         f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
         if (live) {
             // chunk c multiplies from ring slot (c - kc0) % kGwDepth, which
@@ -615,7 +634,7 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
         // the next row block's first chunks load during the exchange and the
         // gates (its rows, or the last block's again when this was the last)
         const int rbn = rb + 4;
-        rows_of(min(rbn, rb1 - 1), mrow, frow, hrow);
+        rows_of(pa_next, va_next, mrow, frow, hrow);
         // values v = 0..3 of rows 4 (lane / 16) + v: the lower half keeps v =
         // 0, 1 and hands over v = 2, 3; the upper half the reverse
         // (the swap area alternates between steps, so a step's sums never
@@ -747,6 +766,10 @@ struct StageArgs {
     const uint64_t *win;
     uint64_t tag;   // (update tag) << 32
     const double *t, *mem_ts, *mail_ts;
+    // the new memory times of the node set (written by the GRU launch), read
+    // instead of ver / mem_ts / mail_ts when set (the GRU read the tables in
+    // place, and no fetched rows exist)
+    const double *nts_new;
     const float *efeat, *mem_new;
     // destination ring slot of iteration i
     int32_t *r_flag, *r_node;
@@ -853,7 +876,8 @@ __device__ __forceinline__ void stage_wave(const StageArgs &g, int c, int lane)
             wave_copy_row(ml + 2 * M, g.efeat + e * D_e, D_e, lane);
     }
     if (lane == 0) {
-        const double mts = g.ver[p] >= 0 ? g.mail_ts[p] : g.mem_ts[p];
+        const double mts =
+            g.nts_new ? g.nts_new[p] : (g.ver[p] >= 0 ? g.mail_ts[p] : g.mem_ts[p]);
         if (g.direct) {
             g.t_mem_ts[w] = mts;
             g.t_mail_ts[w] = g.t[e];
@@ -2910,11 +2934,13 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
                           const int32_t *src_pos, const int32_t *dst_pos, float *mem_new,
                           double *new_mem_ts, hipStream_t s, StageArgs *sa, int *n_items,
                           uint64_t *tag_out, uint64_t *ext_win = nullptr, uint64_t ext_tag = 0,
-                          bool phi_ready = false)
+                          bool phi_ready = false, const int32_t *inplace_nodes = nullptr)
 {
     if (!st || !m || !g || !n_nodes || cap < 0 || b < 0 || first_event < 0 ||
         first_event + b > g->E)
         return TGM_EINVAL;
+    if (inplace_nodes && (!m->gru_w || !phi_ready || !new_mem_ts))
+        return TGM_EINVAL;   // only the resident-weights GRU reads the tables in place
     if (m->M != st->M || m->D_m != st->D_m || g->D_e != m->D_e || g->N != st->N)
         return TGM_EINVAL;
     if (b > st->max_batch)
@@ -2944,8 +2970,13 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
     const int n_cand = 2 * b;
     if (cap > 0) {
         GruArgs ga;
-        ga.n_nodes = n_nodes; ga.mem = mem; ga.mail = mail; ga.mem_ts = mem_ts;
-        ga.mail_ts = mail_ts; ga.ver = ver; ga.bx = m->gru_bx; ga.bh = m->gru_bh;
+        ga.n_nodes = n_nodes; ga.nodes = nullptr; ga.mem = mem; ga.mail = mail;
+        ga.mem_ts = mem_ts; ga.mail_ts = mail_ts; ga.ver = ver;
+        if (inplace_nodes) {   // the committed tables, read in place
+            ga.nodes = inplace_nodes; ga.mem = st->mem; ga.mail = st->mail;
+            ga.mem_ts = st->mem_ts; ga.mail_ts = st->mail_ts; ga.ver = st->ver;
+        }
+        ga.bx = m->gru_bx; ga.bh = m->gru_bh;
         ga.bias = m->gru_bias; ga.omega = m->omega; ga.beta = m->beta; ga.M = m->M;
         ga.D_m = m->D_m; ga.D_t = m->D_t; ga.KXC = m->KXC; ga.KHC = m->KHC; ga.MB = m->MB;
         ga.mem_new = mem_new; ga.new_mem_ts = new_mem_ts;
@@ -2953,8 +2984,10 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
         ga.win = win; ga.tag = tag;
         const bool jodie = m->kind == TGM_MODEL_JODIE;
         const bool w_ok = m->gru_w &&
-                          ((reinterpret_cast<uintptr_t>(mem) | reinterpret_cast<uintptr_t>(mail)) &
-                           7) == 0;
+                          ((reinterpret_cast<uintptr_t>(ga.mem) |
+                            reinterpret_cast<uintptr_t>(ga.mail)) & 7) == 0;
+        if (inplace_nodes && (!w_ok || !phi_ready || !new_mem_ts))
+            return TGM_EINVAL;   // only the resident-weights GRU reads in place
         if (w_ok) {
             // phi once per node (unless the fetch formed it), then MB hidden
             // blocks x (kGruGrid / MB) row ranges (kGruGrid % MB workgroups idle)
@@ -2994,6 +3027,7 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
     a.n_nodes = n_nodes; a.src = g->src; a.dst = g->dst; a.src_pos = src_pos;
     a.dst_pos = dst_pos; a.win = win; a.tag = tag; a.ver = ver;
     a.t = g->t; a.mem_ts = mem_ts; a.mail_ts = mail_ts; a.efeat = g->efeat;
+    a.nts_new = inplace_nodes ? new_mem_ts : nullptr;
     a.mem_new = mem_new;
     a.r_flag = st->r_flag + base; a.r_node = st->r_node + base;
     a.r_mem = st->r_mem + base * st->M; a.r_mail = st->r_mail + base * st->D_m;
@@ -3240,7 +3274,7 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
                                     float *mem_new, double *new_mem_ts, int64_t *winner,
                                     float *h, const tgm_sample_buffers *next_sb,
                                     int32_t mit_slot, uint64_t *xwin, uint64_t xtag,
-                                    hipStream_t s)
+                                    hipStream_t s, bool inplace, bool next_inplace)
 {
     if (st && st->mit)   // the mitigation of this iteration's fetched memories
         TGM_TRY_STATUS(mitigate_launch(st->mit, g, first_event, sb.nodes, sb.n_nodes, cap,
@@ -3253,10 +3287,13 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
     // JODIE's projection reads the new memory times: the model's buffer
     // stands in when the caller keeps none
     double *nts = jodie && !new_mem_ts ? m->nts : new_mem_ts;
+    if (inplace && st && st->mit)
+        return TGM_EINVAL;   // the mitigation blends fetched rows
     tgm_status_t rc = update_begin(st, m, g, iter, sb.n_nodes, cap, fb.mem, fb.mem_ts, fb.mail,
                                    fb.mail_ts, fb.ver, first_event, b, sb.root_pos,
                                    sb.root_pos + b, mem_new, nts, s, &sa, &n_items, &tag,
-                                   xwin, xtag, true);   // every executor fetch forms phi
+                                   xwin, xtag, true,   // every executor fetch forms phi
+                                   inplace ? sb.nodes : nullptr);
     if (rc != TGM_OK)
         return rc;
     if (jodie) {
@@ -3272,6 +3309,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
                                       fb.mem, fb.mem_ts, fb.mail, fb.mail_ts, fb.ver, s,
                                       &next_plan));
             phi_plan(m, &next_plan);
+            if (next_inplace)
+                next_plan.phi_only();
             has_next = next_plan.cap > 0;
         }
         if (n_items > 0)
@@ -3303,6 +3342,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
         if (rc != TGM_OK)
             return rc;
         phi_plan(m, &next_plan);
+        if (next_inplace)
+            next_plan.phi_only();
         next = &next_plan;
     }
     // staging items ride in blocks after the projection's
@@ -3338,7 +3379,7 @@ tgm_status_t tgm::exec_latest_launch(tgm_state_t st, int32_t slot, int32_t b,
         return TGM_OK;
     if (!src_pos || !dst_pos)
         return TGM_EINVAL;
-    GruArgs ga;
+    GruArgs ga{};
     ga.n_nodes = n_nodes;
     ga.n_cand = n_cand;
     ga.src_pos = src_pos;

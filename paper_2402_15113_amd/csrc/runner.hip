@@ -64,6 +64,14 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
     // the sample, into mitigator slot 1 + (k % nsb); the latest-message reduce
     // of each batch also runs beside its sample, into key array k % nsb (so
     // the update's GRU launch skips it)
+    // Fetches in place: with neither mitigation (which blends fetched rows)
+    // nor training (whose backward reads them), an iteration's fetch forms
+    // only phi, and its GRU reads the node set's rows from the committed
+    // tables, which hold the same snapshot until that iteration's staging
+    // commits the next write set.  The last iteration's fetch still fills the
+    // fetch buffers, which the caller reads after the run.
+    const bool inplace_ok = !st->mit && !train && m->gru_w && new_mem_ts;
+    auto inplace = [&](int64_t k) { return inplace_ok && k + 1 < n; };
     uint64_t *xwin[TGM_MAX_SAMPLE_SETS] = {};
     uint64_t xtag[TGM_MAX_SAMPLE_SETS] = {};
     auto sample_chunk = [&](int64_t c) -> tgm_status_t {
@@ -94,6 +102,8 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
         TGM_TRY_STATUS(fetch_plan(st, i0, sb[0].nodes, sb[0].n_nodes, cap, fb->mem, fb->mem_ts,
                                   fb->mail, fb->mail_ts, fb->ver, main, &plan));
         phi_plan(m, &plan);
+        if (inplace(0))
+            plan.phi_only();
         TGM_TRY_STATUS(launch_gather(plan, main));
     }
     for (int64_t c = 0; c < nch; ++c) {
@@ -115,7 +125,8 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             TGM_TRY_STATUS(compute_iteration(st, m, g, i0 + k, sb[k % nsb], *fb, cap, lo, b, nb,
                                              mem_new, new_mem_ts, winner, h,
                                              train ? nullptr : next, (int32_t)(1 + k % nsb),
-                                             xwin[k % nsb], xtag[k % nsb], main));
+                                             xwin[k % nsb], xtag[k % nsb], main, inplace(k),
+                                             inplace(k + 1)));
             if (train) {
                 float *lo_ = st->loss_log ? st->loss_log + (i0 + k) % st->loss_log_len : nullptr;
                 TGM_TRY_STATUS(train_step_launch(st->trainer, m, g, b, sb[k % nsb], *fb, mem_new,
