@@ -323,8 +323,16 @@ tgm_status_t tgm_embed_projection(tgm_model_t m, int32_t R, const int32_t *root_
  * three launches per iteration (the staging of a write set shares a launch
  * with the node projections, and the attention with the next fetch's
  * gather; for JODIE models: the update, the staging, and the projection with
- * the next fetch's gather).  The streams synchronise once per chunk.  The
- * prefetch stream starts after everything issued before on `stream`, and
+ * the next fetch's gather).  Without mitigation (tgm_state_set_mitigation)
+ * and without training (tgm_state_set_training), and when the model's GRU
+ * keeps its weights resident (the shapes of the bench workloads) and
+ * new_mem_ts is given, every fetch but the last forms only the GRU's time
+ * input and the GRU reads the node set's rows from the committed tables in
+ * place: until that iteration's staging commits the next write set they hold
+ * the very rows a fetch would copy.  After the call the fetch buffers hold
+ * the last iteration's fetched rows, in every mode.  The streams synchronise
+ * once per chunk.  The prefetch stream starts after everything issued
+ * before on `stream`, and
  * `stream` ends after the last embedding.  Results equal those of issuing
  * tgm_sample_nodes, tgm_fetch_memory, tgm_update_memory and tgm_embed (or
  * tgm_embed_projection) per iteration in order on one stream.
