@@ -651,16 +651,17 @@ __device__ __forceinline__ bool gather_aligned(const GatherPlan &g, int wm, int 
 // plan asks for it: cos(omega_d (mail_ts - mem_ts) + beta_d) for a node with
 // mail, zero otherwise (the node's times and version as the gather copies
 // them)
-__device__ __forceinline__ void gather_phi(const GatherPlan &g, int p0, int n, int lane)
+// The time inputs phi of positions p0 .. p0 + NPW - 1 (those below n), one
+// wavefront: every load first (the nodes' times and versions; the stores
+// below could alias them, so loads after a store would wait for it), then the
+// codes.
+template <int NPW>
+__device__ __forceinline__ void phi_rows(const GatherPlan &g, int p0, int n, int lane)
 {
-    if (!g.o_phi)
-        return;
-    // every load first (the nodes' times and versions; the stores below could
-    // alias them, so loads after a store would wait for it), then the codes
-    double dt[kGatherNPW];
-    bool has[kGatherNPW];
+    double dt[NPW];
+    bool has[NPW];
 #pragma unroll
-    for (int j = 0; j < kGatherNPW; ++j) {
+    for (int j = 0; j < NPW; ++j) {
         const int32_t v = g.nodes[min(p0 + j, n - 1)];
         dt[j] = g.mail_ts[v] - g.mem_ts[v];
         has[j] = g.ver[v] >= 0;
@@ -670,10 +671,16 @@ __device__ __forceinline__ void gather_phi(const GatherPlan &g, int p0, int n, i
         const int dc = min(d, g.D_t - 1);
         const double om = g.omega[dc], be = g.beta[dc];
 #pragma unroll
-        for (int j = 0; j < kGatherNPW; ++j)
+        for (int j = 0; j < NPW; ++j)
             if (p0 + j < n && d < g.D_t)
                 g.o_phi[(int64_t)(p0 + j) * g.D_t + d] = has[j] ? time_enc(om, be, dt[j]) : 0.f;
     }
+}
+
+__device__ __forceinline__ void gather_phi(const GatherPlan &g, int p0, int n, int lane)
+{
+    if (g.o_phi)
+        phi_rows<kGatherNPW>(g, p0, n, lane);
 }
 
 template <bool VEC = false>
@@ -711,6 +718,23 @@ __device__ __forceinline__ void gather_row(const GatherPlan &g, int p, int lane)
             g.o_mail_ts[p] = g.mail_ts[v];
             g.o_ver[p] = g.ver[v];
         }
+    }
+}
+
+// A fetch spread over the nblk workgroups (of `waves` wavefronts) that follow
+// other work in a launch; b is this workgroup's index among them.  Rows:
+// kGatherNPW nodes per wavefront at a time; phi only: kPhiNPW.
+constexpr int kPhiNPW = 16;
+__device__ __forceinline__ void gather_blocks(const GatherPlan &g, int b, int nblk, int waves,
+                                              int wave, int lane)
+{
+    const int n = min(*g.n_nodes, g.cap);
+    if (g.o_mem) {
+        for (int p = (b * waves + wave) * kGatherNPW; p < n; p += nblk * waves * kGatherNPW)
+            gather_rows(g, p, n, lane);
+    } else if (g.o_phi) {
+        for (int p = (b * waves + wave) * kPhiNPW; p < n; p += nblk * waves * kPhiNPW)
+            phi_rows<kPhiNPW>(g, p, n, lane);
     }
 }
 

@@ -740,12 +740,8 @@ __global__ __launch_bounds__(256) void k_tproj_gather(TprojArgs a, int n_tp, Gat
             tproj_elem(a, i, *a.n_nodes);
         return;
     }
-    const int waves = blockDim.x >> 6;
-    const int n = min(*gp.n_nodes, gp.cap);
-    const int stride = n_gather * waves * kGatherNPW;
-    for (int p = ((int)blockIdx.x * waves + (int)(threadIdx.x >> 6)) * kGatherNPW; p < n;
-         p += stride)
-        gather_rows(gp, p, n, threadIdx.x & 63);
+    gather_blocks(gp, (int)blockIdx.x, n_gather, blockDim.x >> 6, threadIdx.x >> 6,
+                  threadIdx.x & 63);
 }
 
 // Stage the write set of iteration i, and commit an older one, in one launch.
@@ -1598,12 +1594,8 @@ __global__ __launch_bounds__(512) void k_attn_gather(AttnArgs g, int n_attn, Gat
         attn_block<RB>(g, lds, blockIdx.x);
         return;
     }
-    const int waves = blockDim.x >> 6;
-    const int n = min(*gp.n_nodes, gp.cap);
-    const int stride = ((int)gridDim.x - n_attn) * waves * kGatherNPW;
-    for (int p = (((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
-         p < n; p += stride)
-        gather_rows(gp, p, n, threadIdx.x & 63);
+    gather_blocks(gp, (int)blockIdx.x - n_attn, (int)gridDim.x - n_attn, blockDim.x >> 6,
+                  threadIdx.x >> 6, threadIdx.x & 63);
 }
 
 // ---------------------------------------------------------------------------
@@ -2109,12 +2101,8 @@ __global__ __launch_bounds__(512) void k_attn_fold_gather(AttnArgs g, int n_attn
         attn_fold_block<RB>(g, lds, blockIdx.x);
         return;
     }
-    const int waves = blockDim.x >> 6;
-    const int nn = min(*gp.n_nodes, gp.cap);
-    const int stride = ((int)gridDim.x - n_attn) * waves * kGatherNPW;
-    for (int p = (((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
-         p < nn; p += stride)
-        gather_rows(gp, p, nn, threadIdx.x & 63);
+    gather_blocks(gp, (int)blockIdx.x - n_attn, (int)gridDim.x - n_attn, blockDim.x >> 6,
+                  threadIdx.x >> 6, threadIdx.x & 63);
 }
 
 // ---------------------------------------------------------------------------
@@ -2506,12 +2494,8 @@ __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NBM <= 10 ?
         attn_agg_block<NBM>(g, lds, blockIdx.x);
         return;
     }
-    const int waves = blockDim.x >> 6;
-    const int nn = min(*gp.n_nodes, gp.cap);
-    const int stride = ((int)gridDim.x - n_attn) * waves * kGatherNPW;
-    for (int p = (((int)blockIdx.x - n_attn) * waves + (int)(threadIdx.x >> 6)) * kGatherNPW;
-         p < nn; p += stride)
-        gather_rows(gp, p, nn, threadIdx.x & 63);
+    gather_blocks(gp, (int)blockIdx.x - n_attn, (int)gridDim.x - n_attn, blockDim.x >> 6,
+                  threadIdx.x >> 6, threadIdx.x & 63);
 }
 
 // q bias folded at creation: c_q = W_q^t phi(0) + b_q with phi(0)_d = cos(beta_d).
