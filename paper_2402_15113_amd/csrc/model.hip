@@ -434,6 +434,17 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru(GruArgs g)
 #define GW_DEPTH 4
 #endif
 constexpr int kGwDepth = GW_DEPTH;   // A chunks in flight per wavefront
+#ifndef GW_J
+#define GW_J 4
+#endif
+constexpr int kGwJ = GW_J;              // row blocks per step (wavefront pairs)
+constexpr int kGwWaves = 2 * kGwJ;
+constexpr int kGwBufs = kGwJ <= 4 ? 2 : 1;   // swap areas (alternating between steps)
+// k-chunks of k_gru_w's weights: KC rounded up to a multiple of 2 kGwDepth
+__host__ __device__ constexpr int gw_chunks(int KC)
+{
+    return (KC + 2 * kGwDepth - 1) / (2 * kGwDepth) * (2 * kGwDepth);
+}
 
 // phi[p][d] = cos(omega_d (mail_ts - mem_ts) + beta_d) for the nodes of the
 // set that hold mail (zero otherwise): the time part of the GRU input.
@@ -485,12 +496,13 @@ __device__ __forceinline__ GwA gw_a(const GruArgs &g, const float *mrow, const f
 }
 
 template <int NG>
-__global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float *phi)
+__global__ __launch_bounds__(64 * kGwWaves) void k_gru_w(GruArgs g, const float *phi)
 {
     extern __shared__ float lds[];
     const int n = *g.n_nodes;
     latest_reduce(g, n);
     const int M = g.M, MB = g.MB, KXC = g.KXC, KC = g.KXC + g.KHC, D_t = g.D_t;
+    const int KCP = gw_chunks(KC);   // with zero chunks: each half a whole number of ring rounds
     // workgroup b runs on XCD b % 8; its slot counts XCD-major (the 32 slots
     // of XCD 0 first), and slots [r MB, (r + 1) MB) take the MB blocks of
     // row range r, so a range's rows are read by at most two XCDs' L2s
@@ -504,18 +516,20 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
         return;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int j = wave & 3, half = wave >> 2;
-    const int kc0 = half ? KC / 2 : 0, kc1 = half ? KC : KC / 2;
-    f4 *W = reinterpret_cast<f4 *>(lds);        // [KC][NG][64] fragments of block hb
-    f2 *red = reinterpret_cast<f2 *>(W + (int64_t)KC * NG * kWave);   // [2][4][2][4][64]
+    const int j = wave % kGwJ, half = wave / kGwJ;
+    const int kc0 = half ? KCP / 2 : 0, kc1 = half ? KCP : KCP / 2;
+    f4 *W = reinterpret_cast<f4 *>(lds);   // [KCP][NG][64] fragments of block hb
+    f2 *red = reinterpret_cast<f2 *>(W + (int64_t)KCP * NG * kWave);   // [bufs][J][2][4][64]
 
     // the rows of this pair's first block, then the weights of block hb
-    const int steps = (rb1 - rb0 + 3) >> 2;
+    const int steps = (rb1 - rb0 + kGwJ - 1) / kGwJ;
     int rb = rb0 + j;
     const int vm = half ? 2 : 0;   // the two of a lane's four rows this wave finishes
     // Position p of the node set reads row p of the fetched rows, or (g.nodes
     // set) the committed tables' row of node nodes[p]: the ids of a step's
-    // rows load a step ahead.  phi stays by position.
+    // epilogue rows load a step ahead, those of its A rows two steps ahead
+    // (the step before reads the A rows' first chunks).  phi stays by
+    // position.
     auto node_of = [&](int p) -> int { return g.nodes ? g.nodes[p] : p; };
     auto a_pos = [&](int b) { return min(min(b, rb1 - 1) * 16 + (lane & 15), n - 1); };
     auto e_pos = [&](int b, int u) {
@@ -532,6 +546,7 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
         rows_of(p, node_of(p), mrow, frow, hrow);
     }
     int ve[2] = {node_of(e_pos(rb, 0)), node_of(e_pos(rb, 1))};
+    int va1 = node_of(a_pos(rb + kGwJ));   // the A rows' ids of the next step
     GwA ring[kGwDepth];
 #pragma unroll
     for (int q = 0; q < kGwDepth; ++q)
@@ -540,12 +555,12 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
         // sixteen fragments per thread in flight before their LDS stores
         const int64_t kstep = (int64_t)MB * kWave;
         const int64_t gx = (int64_t)KXC * kstep, gh = (int64_t)g.KHC * kstep;
-        const int total = KC * NG * kWave;
+        const int total = KCP * NG * kWave;
         for (int i0 = 0; i0 < total; i0 += 16 * (int)blockDim.x) {
             f4 v[16];
 #pragma unroll
             for (int u = 0; u < 16; ++u) {
-                const int i = min(i0 + u * (int)blockDim.x + tid, total - 1);
+                const int i = min(i0 + u * (int)blockDim.x + tid, KC * NG * kWave - 1);
                 const int l = i & (kWave - 1), cq = i >> 6, c = cq / NG, q = cq - c * NG;
                 const bool x = c < KXC;
                 const f4 *src = (x ? g.bx + (int64_t)c * kstep
@@ -557,7 +572,7 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
             for (int u = 0; u < 16; ++u) {
                 const int i = i0 + u * (int)blockDim.x + tid;
                 if (i < total)
-                    W[i] = v[u];
+                    W[i] = i < KC * NG * kWave ? v[u] : f4{0, 0, 0, 0};   // padding chunks
             }
         }
     }
@@ -568,7 +583,7 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
     const float b_nx = g.bias[2 * MP + colc], b_nh = g.bias[3 * MP + colc];
     lds_barrier();   // the weights are in LDS; the A chunks stay in flight
 
-    for (int st = 0; st < steps; ++st, rb += 4) {
+    for (int st = 0; st < steps; ++st, rb += kGwJ) {
         const bool live = rb < rb1;
         // the epilogue's inputs of this wave's two rows, in flight during the
         // multiply, and the next step's row ids
@@ -582,17 +597,22 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
             has2[u] = g.ver[v] >= 0;
             nts2[u] = has2[u] ? g.mail_ts[v] : g.mem_ts[v];
         }
-        const int pa_next = a_pos(rb + 4);
-        const int va_next = node_of(pa_next);
+        // the next step's A rows (their ids loaded a step ago), and the ids
+        // of the step after
+        const float *mrow_n, *frow_n, *hrow_n;
+        rows_of(a_pos(rb + kGwJ), va1, mrow_n, frow_n, hrow_n);
+        va1 = node_of(a_pos(rb + 2 * kGwJ));
 #pragma unroll
         for (int u = 0; u < 2; ++u)
-            ve[u] = node_of(e_pos(rb + 4, u));
+            ve[u] = node_of(e_pos(rb + kGwJ, u));
         f4 ar = {0, 0, 0, 0}, az = ar, anx = ar, anh = ar;
         if (live) {
             // chunk c multiplies from ring slot (c - kc0) % kGwDepth, which
-            // then loads chunk c + kGwDepth (clamped: the last rounds reload
-            // the range's last chunk); the B fragments of chunk c + 1 are read
-            // from LDS before chunk c multiplies
+            // then loads chunk c + kGwDepth, or past kc1 the next row block's
+            // chunk kc0 + (c + kGwDepth - kc1) (kc1 - kc0 is a multiple of
+            // kGwDepth, so that chunk lands in its slot; after the last block
+            // the rows repeat the range's last); the B fragments of chunk c + 1
+            // are read from LDS before chunk c multiplies
             f4 bw[3], bn[3];
             auto b_read = [&](int c, f4(&b)[3]) {
                 const f4 *wb = W + (int64_t)min(c, kc1 - 1) * NG * kWave + lane;
@@ -605,7 +625,7 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
 #pragma unroll
                 for (int q = 0; q < kGwDepth; ++q) {
                     const int c = c0 + q;
-                    if (c < kc1) {
+                    {
                         const f4 a = {ring[q].lo[0], ring[q].lo[1], ring[q].hi[0],
                                       ring[q].hi[1]};
                         b_read(c + 1, bn);
@@ -622,7 +642,10 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
                             else
                                 anh = mfma_k16(a, bw[0], anh);
                         }
-                        ring[q] = gw_a(g, mrow, frow, hrow, min(c + kGwDepth, kc1 - 1), lane);
+                        const int cn = c + kGwDepth;
+                        const bool nx = cn >= kc1;
+                        ring[q] = gw_a(g, nx ? mrow_n : mrow, nx ? frow_n : frow,
+                                       nx ? hrow_n : hrow, nx ? kc0 + (cn - kc1) : cn, lane);
 #pragma unroll
                         for (int u = 0; u < NG; ++u)
                             bw[u] = bn[u];
@@ -631,15 +654,15 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
                 }
             }
         }
-        // the next row block's first chunks load during the exchange and the
-        // gates (its rows, or the last block's again when this was the last)
-        const int rbn = rb + 4;
-        rows_of(pa_next, va_next, mrow, frow, hrow);
+        mrow = mrow_n;
+        frow = frow_n;
+        hrow = hrow_n;
         // values v = 0..3 of rows 4 (lane / 16) + v: the lower half keeps v =
         // 0, 1 and hands over v = 2, 3; the upper half the reverse
-        // (the swap area alternates between steps, so a step's sums never
-        // land where the previous step's are still being read)
-        f2 *rs = red + (st & 1) * (4 * 2 * 4 * kWave);
+        // (with two swap areas they alternate between steps, so a step's sums
+        // never land where the previous step's are still being read; with one,
+        // a second barrier follows the reads)
+        f2 *rs = red + (kGwBufs == 2 ? (st & 1) : 0) * (kGwJ * 2 * 4 * kWave);
         f2 *rw = rs + ((j * 2 + half) * 4) * kWave + lane;
         const int vo = half ? 0 : 2;
         if (live) {
@@ -648,14 +671,18 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
             rw[2 * kWave] = f2{anx[vo], anx[vo + 1]};
             rw[3 * kWave] = f2{anh[vo], anh[vo + 1]};
         }
-#pragma unroll
-        for (int q = 0; q < kGwDepth; ++q)
-            if (rbn < rb1)
-                ring[q] = gw_a(g, mrow, frow, hrow, min(kc0 + q, kc1 - 1), lane);
         lds_barrier();   // the next block's A chunks stay in flight
+        f2 pr = {0, 0}, pz = pr, pnx = pr, pnh = pr;
         if (live) {
             const f2 *ro = rs + ((j * 2 + (half ^ 1)) * 4) * kWave + lane;
-            const f2 pr = ro[0], pz = ro[kWave], pnx = ro[2 * kWave], pnh = ro[3 * kWave];
+            pr = ro[0];
+            pz = ro[kWave];
+            pnx = ro[2 * kWave];
+            pnh = ro[3 * kWave];
+        }
+        if (kGwBufs == 1)
+            lds_barrier();   // every read of the swap area done before the next writes
+        if (live) {
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 const int v = vm + u;
@@ -686,7 +713,8 @@ __global__ __launch_bounds__(64 * kGruWaves) void k_gru_w(GruArgs g, const float
 // LDS of k_gru_w: the weight fragments of one hidden block and the swap area
 size_t gru_w_lds(const tgm_model *m, int NG)
 {
-    return (size_t)(m->KXC + m->KHC) * NG * kWave * 16 + 2 * 4 * 2 * 4 * kWave * 8;
+    return (size_t)gw_chunks(m->KXC + m->KHC) * NG * kWave * 16 +
+           kGwBufs * kGwJ * 2 * 4 * kWave * 8;
 }
 
 // Shapes k_gru_w handles: 8-byte pairs of the mail row, phi and the memory
@@ -2981,10 +3009,10 @@ tgm_status_t update_begin(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int64_t 
                            m->phi);
             const dim3 grid((unsigned)kGruGrid);
             if (jodie)
-                TGM_LAUNCH(k_gru_w<1>, grid, dim3(64 * kGruWaves), gru_w_lds(m, 1), s, ga,
+                TGM_LAUNCH(k_gru_w<1>, grid, dim3(64 * kGwWaves), gru_w_lds(m, 1), s, ga,
                            m->phi);
             else
-                TGM_LAUNCH(k_gru_w<3>, grid, dim3(64 * kGruWaves), gru_w_lds(m, 3), s, ga,
+                TGM_LAUNCH(k_gru_w<3>, grid, dim3(64 * kGwWaves), gru_w_lds(m, 3), s, ga,
                            m->phi);
         } else if (jodie) {
             // persistent: the node set's tasks are split over kGruGrid workgroups
