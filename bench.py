@@ -288,11 +288,12 @@ def window_setup(name, first, L, w, mitigation=None, s=None, state="gpu", traini
     return wl, stage, init, meta
 
 
-def work_model(wl, rows, model="tgn"):
+def work_model(wl, rows, model="tgn", inplace=False):
     """Algorithmic flops / bytes per launch of each kernel (averaged over the
     timed steps).  Counts only useful work: valid slots, nodes with mail,
     winning messages; no tile padding.  model: "tgn" (GRU, three gates) or
-    "jodie" (RNN cell, one gate)."""
+    "jodie" (RNN cell, one gate).  inplace: the executor's fetches form phi
+    only (no mitigation, no training), and its GRU reads the tables' rows."""
     M, D_e, D_t, D_m, nb = wl.M, wl.D_e, wl.D_t, wl.D_m, wl.nb
     gates = 1 if model == "jodie" else 3
     D_x = D_m + D_t
@@ -328,6 +329,10 @@ def work_model(wl, rows, model="tgn"):
         # phi of every fetched node: its two times and version in, D_t values out
         "k_phi": dict(flops=0, bytes=n_U * (d + d + 4 + D_t * f)),
     }
+    # a fetch that forms phi only: the node ids too
+    phi_fetch = dict(flops=0, bytes=k["k_phi"]["bytes"] + n_U * 4)
+    if inplace:   # the executor's fetches (the first of a pass, and the fused ones)
+        k["k_gather_state"] = phi_fetch
     # the GRU with resident weights: the same cell, its time input read as phi
     k["k_gru_w"] = dict(flops=k["k_gru"]["flops"],
                         bytes=k["k_gru"]["bytes"] + n_U * D_t * f)
@@ -337,6 +342,7 @@ def work_model(wl, rows, model="tgn"):
                              bytes=k["k_node_proj"]["bytes"] + k["k_stage"]["bytes"])
     k["k_attn_gather"] = dict(flops=k["k_attn"]["flops"],
                               bytes=k["k_attn"]["bytes"] + k["k_gather_state"]["bytes"])
+    # (with inplace, the fused launches carry the phi-only fetch)
     # JODIE's time projection: per root its memory row, time and position in,
     # the embedding out; with the next fetch's gather in the executor
     k["k_tproj"] = dict(flops=R * 3 * M, bytes=R * (2 * M * f + 4 + d + d) + M * f)
@@ -452,7 +458,7 @@ def pmc_summary(fetch_csv, write_csv, copy_mib, workload, mfma_csv=None):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            m = re.search(r"(k_[a-z0-9_]+)(<\d+>)?\(", name)
+            m = re.search(r"(k_[a-z0-9_]+)(<[^>]*>)?\(", name)
             key = m.group(1) if m else ("copy" if "copy" in name.lower() else name[:40])
             vals.setdefault(key, []).append(float(r["Counter_Value"]))
         return vals
@@ -804,7 +810,9 @@ def main():
             work = apan_work_model(wl, w.K_mb, rows)
         else:
             rows, seq = account(sched, W, K)
-            work = work_model(wl, rows, args.model)
+            # the executor fetches in place unless mitigation or training reads
+            # the fetched rows (every bench workload keeps the GRU weights resident)
+            work = work_model(wl, rows, args.model, inplace=not (args.mitigate or args.train))
         if args.train:
             work.update(train_work_model(wl, rows))
         kernels = {}
