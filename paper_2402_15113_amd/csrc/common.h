@@ -724,7 +724,7 @@ __device__ __forceinline__ void gather_row(const GatherPlan &g, int p, int lane)
 // A fetch spread over the nblk workgroups (of `waves` wavefronts) that follow
 // other work in a launch; b is this workgroup's index among them.  Rows:
 // kGatherNPW nodes per wavefront at a time; phi only: kPhiNPW.
-constexpr int kPhiNPW = 16;
+constexpr int kPhiNPW = 8;   // enough wavefronts for a small node set, and loads enough in flight
 __device__ __forceinline__ void gather_blocks(const GatherPlan &g, int b, int nblk, int waves,
                                               int wave, int lane)
 {
