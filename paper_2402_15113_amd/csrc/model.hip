@@ -483,14 +483,30 @@ __device__ __forceinline__ GwA gw_a(const GruArgs &g, const float *mrow, const f
     typedef const f2 __attribute__((address_space(1))) *gf2;
     const int KXC = g.KXC, D_m = g.D_m, D_x = g.D_m + g.D_t;
     const float *s0, *s1;
+    // a chunk wholly inside one part of the row (the test is the same in
+    // every lane) takes one address; only the chunks that straddle a part's
+    // end choose per lane
     if (c < KXC) {
-        const int k = 16 * c + 4 * (lane >> 4), k1 = k + 2;
-        s0 = k < D_m ? mrow + k : (k < D_x ? frow + (k - D_m) : mrow);
-        s1 = k1 < D_m ? mrow + k1 : (k1 < D_x ? frow + (k1 - D_m) : mrow);
+        const int k0 = 16 * c, k = k0 + 4 * (lane >> 4), k1 = k + 2;
+        if (k0 + 16 <= D_m) {
+            s0 = mrow + k;
+            s1 = s0 + 2;
+        } else if (k0 >= D_m && k0 + 16 <= D_x) {
+            s0 = frow + (k - D_m);
+            s1 = s0 + 2;
+        } else {
+            s0 = k < D_m ? mrow + k : (k < D_x ? frow + (k - D_m) : mrow);
+            s1 = k1 < D_m ? mrow + k1 : (k1 < D_x ? frow + (k1 - D_m) : mrow);
+        }
     } else {
-        const int k = 16 * (c - KXC) + 4 * (lane >> 4);
-        s0 = k < g.M ? hrow + k : hrow;
-        s1 = k < g.M ? hrow + k + 2 : hrow;
+        const int k0 = 16 * (c - KXC), k = k0 + 4 * (lane >> 4);
+        if (k0 + 16 <= g.M) {
+            s0 = hrow + k;
+            s1 = s0 + 2;
+        } else {
+            s0 = k < g.M ? hrow + k : hrow;
+            s1 = k < g.M ? hrow + k + 2 : hrow;
+        }
     }
     return GwA{*(gf2)(s0), *(gf2)(s1)};
 }
