@@ -177,11 +177,12 @@ def oldest_sampled_row(stage, wl, first, L):
     import torch
     from paper_2402_15113_amd import tgm
     lo_row = first * wl.B
+    sb = stage.sb if hasattr(stage, "sb") else stage   # APAN keeps its sample in .sb
     for i in range(first, first + L):
         a, b = wl.batch(i)
-        tgm.tgm_sample_batch(stage.g, a, b - a, wl.nb, stage.root, stage.root_ts, stage.nbr,
-                             stage.eid, stage.nts, stage.cnt, stream=stage.stream)
-        e = stage.eid[:3 * (b - a)]
+        tgm.tgm_sample_batch(stage.g, a, b - a, wl.nb, sb.root, sb.root_ts, sb.nbr, sb.eid,
+                             sb.nts, sb.cnt, stream=stage.stream)
+        e = sb.eid[:3 * (b - a)]
         lo_row = min(lo_row, int(torch.where(e >= 0, e, wl.E).min().item()))
     return lo_row
 
