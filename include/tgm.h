@@ -90,7 +90,7 @@ tgm_status_t tgm_alloc_count(int64_t *count);
  * destination; a self-loop once), sorted by (t, e), as 16-byte records
  * (time, event id, other endpoint), with a sparse index of every 64th
  * record's time (8 bytes per 64 records) that the sampler searches first.
- * The handle holds about 32 E + 8 N bytes.  src, dst, t and neg are
+ * The handle holds about 32.25 E + 12 N bytes.  src, dst, t and neg are
  * [E] device arrays; efeat is [E x D_e] fp32 on the device, NULL iff D_e == 0.
  * All are borrowed.  The call checks ids in [0, N), t non-decreasing, and
  * synchronises `stream` once (creation is not a per-batch call).
