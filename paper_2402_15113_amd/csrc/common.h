@@ -873,7 +873,9 @@ tgm_status_t launch_gather(const GatherPlan &plan, hipStream_t s);
 // and its GRU reads the committed tables in place at the node set's rows
 // (they still hold exactly the write sets through iter - 1 - s: the next
 // commit comes with this iteration's staging); next_inplace: the same for the
-// fetch of iter + 1 made here.
+// fetch of iter + 1 made here.  next_ready (may be NULL): s waits for it
+// right before the launch that carries the next fetch (the event of the
+// next iteration's sample on another stream).
 // Makes a fetch plan form the GRU's phi input of the model m as well (when
 // the model's GRU reads it precomputed).
 void phi_plan(const tgm_model *m, GatherPlan *plan);
@@ -884,7 +886,8 @@ tgm_status_t compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g, int
                                float *mem_new, double *new_mem_ts, int64_t *winner, float *h,
                                const tgm_sample_buffers *next_sb, int32_t mit_slot,
                                uint64_t *xwin, uint64_t xtag, hipStream_t s,
-                               bool inplace = false, bool next_inplace = false);
+                               bool inplace = false, bool next_inplace = false,
+                               hipEvent_t next_ready = nullptr);
 
 // The executor's latest-message reduce of an iteration, on the prefetch
 // stream beside its sample: exec_latest_launch reduces the 2b candidates of

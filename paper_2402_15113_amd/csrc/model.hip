@@ -3302,7 +3302,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
                                     float *mem_new, double *new_mem_ts, int64_t *winner,
                                     float *h, const tgm_sample_buffers *next_sb,
                                     int32_t mit_slot, uint64_t *xwin, uint64_t xtag,
-                                    hipStream_t s, bool inplace, bool next_inplace)
+                                    hipStream_t s, bool inplace, bool next_inplace,
+                                    hipEvent_t next_ready)
 {
     if (st && st->mit)   // the mitigation of this iteration's fetched memories
         TGM_TRY_STATUS(mitigate_launch(st->mit, g, first_event, sb.nodes, sb.n_nodes, cap,
@@ -3345,6 +3346,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
             TGM_LAUNCH(k_stage, dim3((unsigned)cdiv(n_items, 4)), dim3(256), 0, s, sa);
         TGM_TRY_STATUS(update_winner(sa.win, sb.n_nodes, cap, first_event, tag, winner, s));
         const int n_tp = (int)cdiv((int64_t)R * m->M, 256);
+        if (next_ready)
+            TGM_HIP(hipStreamWaitEvent(s, next_ready, 0));
         if (has_next)
             TGM_LAUNCH(k_tproj_gather, dim3((unsigned)(n_tp + kCUs)), dim3(256), 0, s, ta, n_tp,
                        next_plan);
@@ -3383,6 +3386,8 @@ tgm_status_t tgm::compute_iteration(tgm_state_t st, tgm_model_t m, tgm_graph_t g
         TGM_LAUNCH(k_stage_proj<false>, dim3((R > 0 ? proj_grid : 0) + n_stage_blocks),
                    dim3(64 * proj_waves), proj_lds(m), s, sa, pa, R > 0 ? proj_grid : 0);
     TGM_TRY_STATUS(update_winner(sa.win, sb.n_nodes, cap, first_event, tag, winner, s));
+    if (next_ready)
+        TGM_HIP(hipStreamWaitEvent(s, next_ready, 0));
     if (R > 0)
         return launch_attn(m, aa, next, s);
     return next ? launch_gather(*next, s) : TGM_OK;

@@ -117,8 +117,16 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
             int64_t lo = 0;
             const int32_t b = batch(k, &lo);
             const bool more = k + 1 < n;
-            if (more && k + 1 == kend)   // the next iteration's samples are the next chunk's
-                TGM_HIP(hipStreamWaitEvent(main, ev[(c + 1) & 1], 0));
+            // the next iteration's samples are the next chunk's: the wait goes
+            // right before the launch that fetches for it (in training mode,
+            // which fetches after the step, before the whole iteration)
+            hipEvent_t next_ready = nullptr;
+            if (more && k + 1 == kend) {
+                if (train)
+                    TGM_HIP(hipStreamWaitEvent(main, ev[(c + 1) & 1], 0));
+                else
+                    next_ready = ev[(c + 1) & 1];
+            }
             // in training mode the next fetch waits for the training step,
             // which reads this iteration's fetch buffers
             const tgm_sample_buffers *next = more ? &sb[(k + 1) % nsb] : nullptr;
@@ -126,7 +134,7 @@ extern "C" tgm_status_t tgm_stage_run(tgm_graph_t g, tgm_state_t st, tgm_model_t
                                              mem_new, new_mem_ts, winner, h,
                                              train ? nullptr : next, (int32_t)(1 + k % nsb),
                                              xwin[k % nsb], xtag[k % nsb], main, inplace(k),
-                                             inplace(k + 1)));
+                                             inplace(k + 1), next_ready));
             if (train) {
                 float *lo_ = st->loss_log ? st->loss_log + (i0 + k) % st->loss_log_len : nullptr;
                 TGM_TRY_STATUS(train_step_launch(st->trainer, m, g, b, sb[k % nsb], *fb, mem_new,
