@@ -653,7 +653,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip passes 2-3")
-    ap.add_argument("--settle-ms", type=float, default=50.0,
+    ap.add_argument("--settle-ms", type=float, default=300.0,
                     help="untimed dense GPU load right before each pass's warm-up steps, "
                          "so that they start at the clock sustained load reaches (0: none)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -752,8 +752,9 @@ def main():
     def settle():
         """The GPU clock rises only under sustained load: steps of this window
         run at 218 us after 1 ms of load, 198-207 us after 40 ms, 233 us after
-        2 s idle.  Untimed matrix products for settle_ms bridge the idle gap of
-        the state restore, before the W warm-up steps."""
+        2 s idle; 20 timed steps run at 212 us after 50 ms of matrix products,
+        204-207 us after 200-500 ms.  Untimed matrix products for settle_ms
+        bridge the idle gap of the state restore, before the W warm-up steps."""
         if args.settle_ms <= 0:
             return
         a = torch.full((4096, 4096), 1.0 / 4096, dtype=torch.float32, device="cuda")
